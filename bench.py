@@ -1,0 +1,237 @@
+#!/usr/bin/env python3
+"""EG-MLA decode throughput on one MI355X.
+
+One step = one eg_mla_decode call over one batch of synthetic, seeded input:
+absorption, the token-streaming split kernel (gate gather, gating, scores,
+online softmax, latent value sum) and the split merge with W_UV.  Default
+workload: ~1B-model layer, batch 32, 16 heads, d_c 128, d_r 64, context 4096,
+bf16 storage.
+
+Timing: inputs are resident in HBM; R distinct copies of every input (>= 1 GB
+in total) are rotated so the 256 MB last-level cache cannot serve a call from
+the previous one.  The host enqueues the K timed calls behind a GPU spin
+kernel, so launch overhead is hidden and the events measure back-to-back GPU
+execution.  HIP events around every split-kernel launch (on the call's
+stream) give that kernel's average duration for the roofline figure.
+
+Prints ONE JSON line on stdout; progress goes to stderr.
+"""
+import argparse
+import ctypes
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decode tokens/s + achieved HBM GB/s (% of peak) for eg_mla_decode, 1 GPU"
+HBM_PEAK_GBPS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+class Hip:
+    """hipEvent calls through the HIP runtime torch already loaded."""
+
+    def __init__(self):
+        self.L = ctypes.CDLL("libamdhip64.so.7")
+        self.L.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.L.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        self.L.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self.L.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.L.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+
+    def event(self):
+        e = ctypes.c_void_p()
+        assert self.L.hipEventCreate(ctypes.byref(e)) == 0
+        return e
+
+    def record(self, e, stream):
+        assert self.L.hipEventRecord(e, ctypes.c_void_p(stream)) == 0
+
+    def elapsed_ms(self, a, b):
+        ms = ctypes.c_float()
+        assert self.L.hipEventElapsedTime(ctypes.byref(ms), a, b) == 0
+        return ms.value
+
+    def destroy(self, e):
+        self.L.hipEventDestroy(e)
+
+
+def cpu_baseline(inp, seconds):
+    """The fp64 oracle as it stands, timed on the host over whole batches."""
+    from oracle import eg_mla_oracle as orc
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i["num_threads"] for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:
+        threads = 1
+    wl = inp.wl
+    reps = 0
+    t0 = time.perf_counter()
+    while True:
+        orc.decode(inp.q, inp.latent_cache, inp.token_ids, inp.gate_table, inp.w_uk, inp.w_uv, inp.seq_lens,
+                   latent_dim=wl.latent_dim, head_dim=wl.head_dim, rope_dim=wl.rope_dim, storage=wl.dtype,
+                   page_table=inp.page_table, page_size=wl.page_size, max_pages=inp.max_pages)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds or reps >= 100:
+            break
+    return {"value": wl.batch * reps / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{reps} full decode steps of the same workload ({wl.batch} sequences each), "
+                      f"{el:.1f} s, numpy fp64 with {threads} BLAS threads"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", type=int, default=1, help="index into workloads.WORKLOADS")
+    ap.add_argument("--path", choices=["auto", "valu", "mfma"], default="auto")
+    ap.add_argument("--split", type=int, default=0, help="tokens per split (0 = automatic)")
+    ap.add_argument("--rotate-bytes", type=float, default=1.0e9)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py: this build measures one GPU; --gpus {args.gpus} (WORLD_SIZE {world}) is not supported. "
+              "The decode path shards by sequence with no communication; see the design notes.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2509_16686_amd import accounting as A
+    from paper_2509_16686_amd import binding as B
+    from paper_2509_16686_amd import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    L = B.lib()
+    hip = Hip()
+    wl = W.WORKLOADS[args.workload]
+    log(f"bench: generating {wl.name}")
+    inp = W.generate(wl)
+    traffic = A.decode_bytes(batch=wl.batch, heads=wl.heads, head_dim=wl.head_dim, v_head_dim=wl.v_head_dim,
+                             latent_dim=wl.latent_dim, rope_dim=wl.rope_dim, elem_bytes=wl.elem_bytes,
+                             total_tokens=inp.total_tokens(), distinct_ids=inp.unique_ids())
+    copies_bytes = (inp.latent_cache.nbytes + inp.token_ids.nbytes + inp.gate_table.nbytes + inp.q.nbytes +
+                    inp.w_uk.nbytes + inp.w_uv.nbytes)
+    R = max(1, math.ceil(args.rotate_bytes / copies_bytes))
+    dd0 = B.stage_decode(inp)
+    copies = [dd0]
+    for _ in range(R - 1):
+        copies.append(B.DeviceDecode(dims=dd0.dims, q=dd0.q.clone(), cache=dd0.cache.clone(), ids=dd0.ids.clone(),
+                                     gate=dd0.gate.clone(), w_uk=dd0.w_uk.clone(), w_uv=dd0.w_uv.clone(),
+                                     seq_lens=dd0.seq_lens.clone(),
+                                     page_table=None if dd0.page_table is None else dd0.page_table.clone(),
+                                     max_pages=dd0.max_pages, out=torch.empty_like(dd0.out)))
+    path = {"auto": B.PATH_AUTO, "valu": B.PATH_VALU, "mfma": B.PATH_MFMA}[args.path]
+    plan0 = B.make_plan(path, args.split)
+    ws_bytes = B.decode_workspace_size(dd0.dims, wl.batch, dd0.max_pages, plan0)
+    assert ws_bytes > 0, "no plan for this workload"
+    ws = B.alloc_workspace(ws_bytes)
+    stream = torch.cuda.current_stream().cuda_stream
+    K, Wm = args.steps, args.warmup
+    log(f"bench: {R} rotating input copies of {copies_bytes / 1e6:.1f} MB, workspace {ws_bytes / 1e6:.1f} MB")
+
+    ev0 = [hip.event() for _ in range(K)]
+    ev1 = [hip.event() for _ in range(K)]
+    plans = [B.make_plan(path, args.split, ev0[k], ev1[k]) for k in range(K)]
+
+    def argset(dd, plan):
+        return (ctypes.byref(dd.dims), wl.batch, dd.q.data_ptr(), dd.cache.data_ptr(), dd.ids.data_ptr(),
+                dd.gate.data_ptr(), dd.w_uk.data_ptr(), dd.w_uv.data_ptr(), dd.seq_lens.data_ptr(),
+                None if dd.page_table is None else dd.page_table.data_ptr(), dd.max_pages,
+                int(dd.cache.shape[0]), ws.data_ptr(), ws_bytes, dd.out.data_ptr(), stream, ctypes.byref(plan))
+
+    warm_args = [argset(copies[k % R], plan0) for k in range(max(Wm, 1))]
+    timed_args = [argset(copies[k % R], plans[k]) for k in range(K)]
+    call = L.eg_mla_decode_planned
+
+    for a in warm_args:
+        st = call(*a)
+        assert st == 0, B.status_string(st)
+    torch.cuda.synchronize()
+    # host enqueue rate, to size the spin that hides launch overhead
+    h0 = time.perf_counter()
+    for a in warm_args:
+        call(*a)
+    host_per_call = (time.perf_counter() - h0) / len(warm_args)
+    torch.cuda.synchronize()
+
+    # calibrate the spin kernel
+    s0, s1 = hip.event(), hip.event()
+    hip.record(s0, stream)
+    torch.cuda._sleep(1_000_000)
+    hip.record(s1, stream)
+    torch.cuda.synchronize()
+    cycles_per_ms = 1_000_000 / max(hip.elapsed_ms(s0, s1), 1e-3)
+    spin_ms = 2.0 * host_per_call * K * 1e3 + 5.0
+
+    t_start, t_stop = hip.event(), hip.event()
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    torch.cuda._sleep(int(spin_ms * cycles_per_ms))
+    hip.record(t_start, stream)
+    for a in timed_args:
+        call(*a)
+    hip.record(t_stop, stream)
+    enq = time.perf_counter() - wall0
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = hip.elapsed_ms(t_start, t_stop)
+    kernel_ms = [hip.elapsed_ms(ev0[k], ev1[k]) for k in range(K)]
+    if enq * 1e3 > spin_ms:
+        log(f"bench: warning: enqueue took {enq * 1e3:.1f} ms > spin {spin_ms:.1f} ms; GPU may have idled")
+
+    ms_per_step = total_ms / K
+    k_avg_ms = float(np.mean(kernel_ms))
+    k_bytes = traffic.main_kernel
+    achieved = k_bytes / (k_avg_ms * 1e-3) / 1e9
+    tokens_per_s = wl.batch / (ms_per_step * 1e-3)
+    log(f"bench: {ms_per_step * 1e3:.2f} us/step, split kernel {k_avg_ms * 1e3:.2f} us "
+        f"({achieved:.0f} GB/s, {100 * achieved / HBM_PEAK_GBPS:.1f}% of peak), host {host_per_call * 1e6:.1f} us/call, "
+        f"wall {wall:.3f} s")
+
+    out = {
+        "metric": METRIC,
+        "value": tokens_per_s,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": Wm,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.dtype == "bf16" else "fp32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "batch": wl.batch, "heads": wl.heads, "head_dim": wl.head_dim,
+                   "latent_dim": wl.latent_dim, "rope_dim": wl.rope_dim, "vocab": wl.vocab,
+                   "context": wl.seq_len if wl.seq_len else list(wl.seq_len_range), "paged": wl.paged,
+                   "storage": wl.dtype, "path": args.path, "split_tokens": args.split,
+                   "rotating_copies": R},
+        "hbm_gbps_call": traffic.total / (ms_per_step * 1e-3) / 1e9,
+        "hbm_frac_call": traffic.total / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+        "roofline": {"bound": "hbm", "kernel": "split_mfma_kernel" if wl.dtype == "bf16" else "split_valu_kernel",
+                     "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                     "algorithmic_bytes_per_launch": k_bytes, "kernel_us": k_avg_ms * 1e3},
+    }
+    if not args.no_cpu_baseline:
+        log(f"bench: timing the fp64 oracle on the host for ~{args.cpu_seconds:.0f} s")
+        out["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,182 @@
+/*
+ * eg_mla.h -- C ABI of the EG-MLA decode library for AMD Instinct MI355X (gfx950).
+ *
+ * EG-MLA (Embedding-Gated Multi-head Latent Attention, arXiv 2509.16686)
+ * caches one compressed latent c_t (d_c values, Sec. 3.1 Eq. (1)) and one
+ * decoupled RoPE key k^R_t (d_r values shared by all heads, App. C
+ * Eq. (C.10)) per token, plus the token's id i_t.  Each cached latent is
+ * modulated by a token-specific gate g_t looked up from the token id
+ * (Sec. 3.1 Eq. (3)-(5)).  This library applies the gate in the latent
+ * space, c~_t = c_t * G[i_t], where G = Emb W^UE^T is the gate table folded
+ * offline (the table-lookup variant of Sec. 5.2), so the per-head key and
+ * value up-projections can be absorbed:
+ *
+ *   q_lat[h]  = W_UK[h]^T q^C[h]
+ *   s[h,j]    = tau * (q_lat[h] . c~_j + q^R[h] . k^R_j),  tau = 1/sqrt(d_h + d_r)
+ *   out[h]    = W_UV[h] * sum_j softmax_j(s[h,:]) c~_j
+ *
+ * which equals App. C Eq. (C.11)-(C.13) with k_{j,h} = [W_UK[h] c~_j ; k^R_j]
+ * and v_{j,h} = W_UV[h] c~_j.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Every tensor argument is a DEVICE pointer owned by the caller,
+ *    row-major and contiguous.  The library never allocates or frees device
+ *    memory and keeps no state between calls except cached device
+ *    properties.
+ *  - Floating-point tensors have the storage type dims->dtype: IEEE fp32, or
+ *    bf16 (16-bit brain float).  Arithmetic is fp32 (bf16 MFMA products with
+ *    fp32 accumulation on the bf16 fast path).  Integer tensors are int32.
+ *  - Weights follow the [out, in] convention of a linear layer: W_UK[h] is
+ *    [d_h, d_c] (k^C = W_UK[h] c~), W_UV[h] is [d_v, d_c].
+ *  - `stream` is a hipStream_t (NULL = the null stream).  Calls only enqueue
+ *    work on it and return; they are safe to issue concurrently on
+ *    different streams with disjoint workspaces.
+ *  - Host-detectable errors (bad dims, null pointers, workspace too small)
+ *    are returned before anything is enqueued.  A failed launch returns
+ *    EG_MLA_ERR_HIP.  Device-side data are made safe rather than checked:
+ *    sequence lengths are clamped to [0, capacity], token ids to [0, V),
+ *    page numbers and slots to the cache; append skips out-of-range slots.
+ */
+#ifndef EG_MLA_H
+#define EG_MLA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum eg_mla_status {
+  EG_MLA_OK = 0,
+  EG_MLA_ERR_INVALID_ARG = 1,  /* null pointer, non-positive size, inconsistent dims */
+  EG_MLA_ERR_UNSUPPORTED = 2,  /* valid but not implemented (e.g. gate_dim != latent_dim, forced path unavailable) */
+  EG_MLA_ERR_WORKSPACE = 3,    /* workspace pointer null or smaller than the *_workspace_size query */
+  EG_MLA_ERR_HIP = 4           /* a HIP launch or runtime call failed */
+} eg_mla_status;
+
+typedef enum eg_mla_dtype { EG_MLA_FP32 = 0, EG_MLA_BF16 = 1 } eg_mla_dtype;
+
+/* Layer shapes.  gate_dim must equal latent_dim (the gate multiplies the
+ * latent element-wise, Eq. (5) in the latent reading).  softmax_scale <= 0
+ * selects 1/sqrt(head_dim + rope_dim) (App. C Eq. (C.13)). */
+typedef struct eg_mla_dims {
+  int32_t num_heads;    /* H   */
+  int32_t head_dim;     /* d_h: non-RoPE part of each query/key head */
+  int32_t v_head_dim;   /* d_v */
+  int32_t latent_dim;   /* d_c */
+  int32_t rope_dim;     /* d_r (may be 0) */
+  int32_t gate_dim;     /* must equal d_c */
+  int32_t vocab_size;   /* V: rows of the gate table */
+  int32_t page_size;    /* P: tokens per cache page */
+  float softmax_scale;  /* <= 0: default */
+  int32_t dtype;        /* eg_mla_dtype of every floating-point tensor */
+} eg_mla_dims;
+
+/* Optional execution plan for eg_mla_decode_planned (tuning and tests). */
+typedef enum eg_mla_path {
+  EG_MLA_PATH_AUTO = 0,  /* MFMA when dtype is bf16 and the shape has a fast kernel, else VALU */
+  EG_MLA_PATH_VALU = 1,  /* fp32 vector-ALU kernel, any shape and dtype */
+  EG_MLA_PATH_MFMA = 2   /* bf16 matrix-core kernel; EG_MLA_ERR_UNSUPPORTED if the shape has none */
+} eg_mla_path;
+
+typedef struct eg_mla_plan {
+  int32_t path;          /* eg_mla_path */
+  int32_t split_tokens;  /* tokens per split-K work item, multiple of 32; 0 = automatic */
+  /* Optional hipEvent_t handles (NULL = none), recorded on the call's stream
+   * immediately before and after the token-streaming split kernel, so a
+   * caller can time that kernel alone with hipEventElapsedTime. */
+  void* split_start_event;
+  void* split_stop_event;
+} eg_mla_plan;
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char* eg_mla_status_string(eg_mla_status status);
+
+/* Validates `dims` on the host.  EG_MLA_OK, EG_MLA_ERR_INVALID_ARG or
+ * EG_MLA_ERR_UNSUPPORTED.  Touches no device. */
+eg_mla_status eg_mla_check_dims(const eg_mla_dims* dims);
+
+/* ---------------------------------------------------------------------------
+ * Append: write new tokens into the latent cache (Sec. 3.1 Eq. (1); App. C
+ * Eq. (C.10)).  For token i:
+ *   [c | r]  = W_DKV x_i                      (W_DKV = [W^DKV ; W^KR], [d_c+d_r, hidden])
+ *   c        = c / sqrt(mean(c^2) + 1e-6) * kv_norm_w      (only if kv_norm_w != NULL)
+ *   k^R      = RoPE(r, positions[i])         (adjacent pairs (2m, 2m+1), angle pos*theta^(-2m/d_r))
+ *   latent_cache[slots[i]] = [c | k^R]  (rounded to the storage type)
+ *   token_id_cache[slots[i]] = token_ids[i]
+ *
+ *   x          [n_tokens, hidden]
+ *   token_ids  [n_tokens] int32;  positions [n_tokens] int32 (0-based)
+ *   slots      [n_tokens] int32 destination rows (page*P + offset); rows
+ *              outside [0, num_slots) are skipped.  Duplicate slots race.
+ *   w_dkv      [d_c + d_r, hidden];  kv_norm_w [d_c] or NULL
+ *   latent_cache [num_slots, d_c + d_r];  token_id_cache [num_slots] int32
+ * rope_theta <= 0 selects 10000.  n_tokens == 0 is a no-op.
+ * ------------------------------------------------------------------------- */
+eg_mla_status eg_mla_append(const eg_mla_dims* dims, int32_t n_tokens, int32_t hidden, const void* x,
+                            const int32_t* token_ids, const int32_t* positions, const int32_t* slots,
+                            const void* w_dkv, const void* kv_norm_w, float rope_theta, void* latent_cache,
+                            int32_t* token_id_cache, int64_t num_slots, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Decode: one query row per sequence against its whole cached context
+ * (App. C Eq. (C.13) with t = the current token; the gate of Eq. (3)-(5)
+ * applied to each cached latent through its token id).
+ *
+ *   q             [B, H, d_h + d_r]   (q^C | q^R); q^R already rotated
+ *   latent_cache  [num_slots, d_c + d_r]   (latent | RoPE key) per cached token
+ *   token_id_cache[num_slots] int32   token id of every cached row
+ *   gate_table    [V, d_c]            folded gate G = Emb W^UE^T
+ *   w_uk          [H, d_h, d_c];  w_uv [H, d_v, d_c]
+ *   seq_lens      [B] int32  cached tokens per sequence, current token
+ *                 included; clamped to [0, max_pages_per_seq * P]; 0 gives zeros
+ *   page_table    [B, max_pages_per_seq] int32, or NULL for contiguous
+ *                 storage where token j of sequence b is row
+ *                 b * max_pages_per_seq * P + j
+ *   workspace     device scratch of at least
+ *                 eg_mla_decode_workspace_size(dims, B, max_pages_per_seq, plan)
+ *                 bytes, 256-byte aligned; contents need no initialisation
+ *   out           [B, H, d_v]  in the storage type
+ * ------------------------------------------------------------------------- */
+size_t eg_mla_decode_workspace_size(const eg_mla_dims* dims, int32_t batch, int32_t max_pages_per_seq,
+                                    const eg_mla_plan* plan /* NULL = automatic */);
+
+eg_mla_status eg_mla_decode(const eg_mla_dims* dims, int32_t batch, const void* q, const void* latent_cache,
+                            const int32_t* token_id_cache, const void* gate_table, const void* w_uk,
+                            const void* w_uv, const int32_t* seq_lens, const int32_t* page_table,
+                            int32_t max_pages_per_seq, int64_t num_slots, void* workspace,
+                            size_t workspace_bytes, void* out, void* stream);
+
+/* Same as eg_mla_decode with an explicit plan (NULL = automatic).  The
+ * workspace must be sized with the same plan. */
+eg_mla_status eg_mla_decode_planned(const eg_mla_dims* dims, int32_t batch, const void* q,
+                                    const void* latent_cache, const int32_t* token_id_cache,
+                                    const void* gate_table, const void* w_uk, const void* w_uv,
+                                    const int32_t* seq_lens, const int32_t* page_table,
+                                    int32_t max_pages_per_seq, int64_t num_slots, void* workspace,
+                                    size_t workspace_bytes, void* out, void* stream, const eg_mla_plan* plan);
+
+/* ---------------------------------------------------------------------------
+ * Prefill reference: plain causal attention over one sequence of T tokens in
+ * the explicit (non-absorbed) form of App. C Eq. (C.2), (C.6), (C.11)-(C.13):
+ * it materialises k_{j,h} = [W_UK[h] c~_j ; k^R_j] and v_{j,h} = W_UV[h] c~_j
+ * in fp32 in the workspace and runs one softmax per (t, h) over j <= t.
+ * A plain second implementation for cross-checks, not a fast prefill.
+ *
+ *   q [T, H, d_h + d_r];  latent [T, d_c + d_r];  token_ids [T] int32
+ *   gate_table, w_uk, w_uv as for decode;  out [T, H, d_v]
+ * ------------------------------------------------------------------------- */
+size_t eg_mla_prefill_workspace_size(const eg_mla_dims* dims, int32_t seq_len);
+
+eg_mla_status eg_mla_prefill_ref(const eg_mla_dims* dims, int32_t seq_len, const void* q, const void* latent,
+                                 const int32_t* token_ids, const void* gate_table, const void* w_uk,
+                                 const void* w_uv, void* workspace, size_t workspace_bytes, void* out,
+                                 void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EG_MLA_H */

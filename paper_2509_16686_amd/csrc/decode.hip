@@ -1,0 +1,620 @@
+// EG-MLA decode on gfx950: absorbed-MLA attention over a latent KV cache with
+// the token-specific embedding gate applied to each cached latent.
+//
+// Per call (all on the caller's stream):
+//   1. absorb        q_lat[b,h] = W_UK[h]^T q^C[b,h]  (fp32), copied next to q^R
+//   2. split kernel  one work-group per (sequence, context split, head group):
+//                    stream cached rows, gate them by G[token id], scores,
+//                    online softmax (log2 domain), latent-space value sum
+//                    -> partial (max, sum, o_lat) per head
+//   3. combine       log-sum-exp merge of the splits, o_lat / l, then W_UV[h]
+//
+// The math is App. C Eq. (C.11)-(C.13) in absorbed form with the gate of
+// Sec. 3.1 Eq. (3)-(5) applied in the latent space (c~ = c * G[id]).
+#include <hip/hip_runtime.h>
+
+#include <cfloat>
+#include <cmath>
+
+#include "device_common.h"
+#include "eg_mla.h"
+#include "host_plan.h"
+
+namespace egmla {
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+// ---------------------------------------------------------------------------
+// 1. absorption: qfull[b,h,:] = [W_UK[h]^T q^C[b,h] | q^R[b,h]]   (fp32)
+// grid (H, ceil(B / 8)), 256 threads; W_UK[h] is read once per 8 sequences.
+// ---------------------------------------------------------------------------
+constexpr int kAbsorbRows = 8;
+
+template <bool BF16>
+__global__ __launch_bounds__(256) void absorb_kernel(const void* __restrict__ q, const void* __restrict__ w_uk,
+                                                     float* __restrict__ qfull, int B, int H, int DH, int DC,
+                                                     int DR) {
+  extern __shared__ float smem[];  // [kAbsorbRows][DH]
+  const int h = blockIdx.x;
+  const int b0 = blockIdx.y * kAbsorbRows;
+  const int nb = min(kAbsorbRows, B - b0);
+  const int DQin = DH + DR;
+  const int DQ = DC + DR;
+  for (int i = threadIdx.x; i < nb * DH; i += blockDim.x) {
+    const int bb = i / DH, k = i % DH;
+    smem[bb * DH + k] = ld<BF16>(q, (static_cast<int64_t>(b0 + bb) * H + h) * DQin + k);
+  }
+  __syncthreads();
+  const int64_t wbase = static_cast<int64_t>(h) * DH * DC;
+  for (int c = threadIdx.x; c < DC; c += blockDim.x) {
+    float acc[kAbsorbRows];
+#pragma unroll
+    for (int bb = 0; bb < kAbsorbRows; ++bb) acc[bb] = 0.f;
+    for (int k = 0; k < DH; ++k) {
+      const float w = ld<BF16>(w_uk, wbase + static_cast<int64_t>(k) * DC + c);
+#pragma unroll
+      for (int bb = 0; bb < kAbsorbRows; ++bb) acc[bb] = fmaf(w, smem[bb * DH + k], acc[bb]);
+    }
+    for (int bb = 0; bb < nb; ++bb) qfull[(static_cast<int64_t>(b0 + bb) * H + h) * DQ + c] = acc[bb];
+  }
+  for (int i = threadIdx.x; i < nb * DR; i += blockDim.x) {
+    const int bb = i / DR, r = i % DR;
+    qfull[(static_cast<int64_t>(b0 + bb) * H + h) * DQ + DC + r] =
+        ld<BF16>(q, (static_cast<int64_t>(b0 + bb) * H + h) * DQin + DH + r);
+  }
+}
+
+// Split-K bookkeeping shared by the split kernels.
+struct SplitArgs {
+  const float* qfull;         // [B, H, DQ]
+  const void* cache;          // [num_slots, DQ]
+  const int32_t* ids;         // [num_slots]
+  const void* gate;           // [V, DC]
+  const int32_t* seq_lens;    // [B]
+  const int32_t* page_table;  // [B, max_pages] or null
+  float* part_ml;             // [B, s_max, H, 2]
+  float* part_o;              // [B, s_max, H, DC]
+  int64_t num_slots;
+  int B, H, DC, DR, P, max_pages, V, cap, split, s_max, groups, hpg;
+  float scale_log2;           // softmax scale * log2(e)
+};
+
+// ---------------------------------------------------------------------------
+// 2a. VALU split kernel: fp32 arithmetic, any shape, fp32 or bf16 storage.
+// One work-group (256 threads) per (sequence, split, head block of hpg heads).
+// LDS: q [hpg][DQ], gated tile [32][DQ+1], probabilities [hpg][32].
+// ---------------------------------------------------------------------------
+constexpr int kValuThreads = 256;
+constexpr int kValuAcc = 32;  // latent accumulators per thread: hpg * DC <= 8192
+
+template <bool BF16>
+__global__ __launch_bounds__(kValuThreads) void split_valu_kernel(SplitArgs a) {
+  extern __shared__ float smem[];
+  const int DQ = a.DC + a.DR;
+  const int TS = DQ + 1;  // padded tile row
+  const int nblocks = gridDim.x;
+  const int item = xcd_logical_block(blockIdx.x, nblocks);
+  const int hb = item % a.groups;
+  const int s = (item / a.groups) % a.s_max;
+  const int b = item / (a.groups * a.s_max);
+  const int L = clamp_len(a.seq_lens[b], a.cap);
+  const int t0 = s * a.split;
+  if (t0 >= L) return;
+  const int t1 = min(t0 + a.split, L);
+  const int h0 = hb * a.hpg;
+  const int nh = min(a.hpg, a.H - h0);
+
+  float* q_s = smem;                      // [hpg][DQ]
+  float* tile = q_s + a.hpg * DQ;         // [32][TS]
+  float* prob = tile + kTile * TS;        // [hpg][32]
+  float* alpha_s = prob + a.hpg * kTile;  // [hpg]
+  int64_t* slot_s = reinterpret_cast<int64_t*>(alpha_s + a.hpg + (a.hpg & 1));  // [32]
+  int* id_s = reinterpret_cast<int*>(slot_s + kTile);                           // [32]
+
+  const int tid = threadIdx.x;
+  for (int i = tid; i < nh * DQ; i += kValuThreads) q_s[i] = a.qfull[(static_cast<int64_t>(b) * a.H + h0) * DQ + i];
+
+  float acc[kValuAcc];
+#pragma unroll
+  for (int k = 0; k < kValuAcc; ++k) acc[k] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;  // owned by thread tid < nh
+  const int npairs = nh * a.DC;
+
+  for (int tt = t0; tt < t1; tt += kTile) {
+    const int nt = min(kTile, t1 - tt);
+    __syncthreads();  // previous tile fully consumed
+    if (tid < nt) {
+      const int64_t sl = cache_slot(a.page_table, b, tt + tid, a.P, a.max_pages, a.num_slots);
+      slot_s[tid] = sl;
+      id_s[tid] = clamp_id(a.ids[sl], a.V);
+    }
+    __syncthreads();
+    // gated tile: c~ = c * G[id] on the latent part, RoPE key as is
+    for (int e = tid; e < nt * DQ; e += kValuThreads) {
+      const int t = e / DQ, d = e % DQ;
+      float x = ld<BF16>(a.cache, slot_s[t] * DQ + d);
+      if (d < a.DC) x *= ld<BF16>(a.gate, static_cast<int64_t>(id_s[t]) * a.DC + d);
+      tile[t * TS + d] = x;
+    }
+    __syncthreads();
+    // scores (log2 domain)
+    for (int p = tid; p < nh * kTile; p += kValuThreads) {
+      const int h = p / kTile, t = p % kTile;
+      float sc = -INFINITY;
+      if (t < nt) {
+        float dot = 0.f;
+        const float* qr = q_s + h * DQ;
+        const float* tr = tile + t * TS;
+        for (int d = 0; d < DQ; ++d) dot = fmaf(qr[d], tr[d], dot);
+        sc = dot * a.scale_log2;
+      }
+      prob[h * kTile + t] = sc;
+    }
+    __syncthreads();
+    // online softmax update, one thread per head
+    if (tid < nh) {
+      float mt = -INFINITY;
+      for (int t = 0; t < nt; ++t) mt = fmaxf(mt, prob[tid * kTile + t]);
+      const float m_new = fmaxf(m_run, mt);
+      const float alpha = exp2f(m_run - m_new);
+      float sum = 0.f;
+      for (int t = 0; t < kTile; ++t) {
+        const float pv = t < nt ? exp2f(prob[tid * kTile + t] - m_new) : 0.f;
+        prob[tid * kTile + t] = pv;
+        sum += pv;
+      }
+      l_run = l_run * alpha + sum;
+      m_run = m_new;
+      alpha_s[tid] = alpha;
+    }
+    __syncthreads();
+    // latent-space value accumulation
+#pragma unroll
+    for (int k = 0; k < kValuAcc; ++k) {
+      const int idx = tid + k * kValuThreads;
+      if (idx < npairs) {
+        const int h = idx / a.DC, d = idx % a.DC;
+        float o = acc[k] * alpha_s[h];
+        const float* pr = prob + h * kTile;
+        for (int t = 0; t < nt; ++t) o = fmaf(pr[t], tile[t * TS + d], o);
+        acc[k] = o;
+      }
+    }
+  }
+  const int64_t pbase = (static_cast<int64_t>(b) * a.s_max + s) * a.H + h0;
+  if (tid < nh) {
+    a.part_ml[(pbase + tid) * 2 + 0] = m_run;
+    a.part_ml[(pbase + tid) * 2 + 1] = l_run;
+  }
+#pragma unroll
+  for (int k = 0; k < kValuAcc; ++k) {
+    const int idx = tid + k * kValuThreads;
+    if (idx < npairs) a.part_o[pbase * a.DC + idx] = acc[k];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// 2b. MFMA split kernel (bf16 storage, 16 heads per work-group).
+//
+// NW waves per work-group share one (sequence, split, head group); 32-token
+// tiles are dealt round-robin to the waves.  For its tile a wave
+//   * loads each token's row with 16-byte loads straight into the layout of
+//     the MFMA A operand (lane: token lane%16, 8 consecutive dims), loads the
+//     matching 16 bytes of the token's gate row and gates in fp32,
+//   * scores S^T[token][head] = C~K x Q^T with v_mfma_f32_16x16x32_bf16,
+//     reduction over the d_c gated latent dims and the d_r RoPE dims,
+//   * runs the online softmax on the accumulator layout (lane: one head,
+//     4 tokens per 16-token half), whose probabilities are exactly the
+//     B operand of the value product, so P never leaves registers,
+//   * writes the gated latent transposed into its own LDS region (dims x
+//     tokens) so the value product O^T[dim][head] += C~^T x P^T reads its
+//     A operand with 16-byte LDS loads.
+// At the end the waves merge their (max, sum, O) through LDS in a fixed
+// order and write one partial per head.
+// ---------------------------------------------------------------------------
+template <int DC>
+struct MfmaCfg {
+  static constexpr int NW = DC <= 128 ? 4 : 2;
+  static constexpr int CT_STRIDE = 40;  // 32 token slots + 8 pad (bf16 elements)
+  static constexpr int LDS_BYTES_CT = NW * DC * CT_STRIDE * 2;
+  static constexpr int LDS_BYTES_MERGE = NW * 16 * DC * 4 + NW * 16 * 2 * 4;
+  static constexpr int LDS_BYTES = LDS_BYTES_CT > LDS_BYTES_MERGE ? LDS_BYTES_CT : LDS_BYTES_MERGE;
+};
+
+// Position of token t (0..31) of a tile in a transposed LDS row: the 8
+// k-slots of lane group g hold tokens 4g..4g+3 of each 16-token half.
+__device__ __forceinline__ int ct_pos(int half, int t16) { return (t16 >> 2) * 8 + half * 4 + (t16 & 3); }
+
+template <int DC, int DR>
+__global__ __launch_bounds__(MfmaCfg<DC>::NW * 64) void split_mfma_kernel(SplitArgs a) {
+  using Cfg = MfmaCfg<DC>;
+  constexpr int NW = Cfg::NW;
+  constexpr int DQ = DC + DR;
+  constexpr int NKC = DQ / 32;  // 32-dim chunks of a row
+  constexpr int NLC = DC / 32;  // gated (latent) chunks
+  constexpr int NDB = DC / 16;  // 16-dim blocks of the value product
+  constexpr int CTS = Cfg::CT_STRIDE;
+  static_assert(DQ % 32 == 0 && DC % 32 == 0, "row must split into 32-dim chunks");
+  __shared__ __attribute__((aligned(16))) unsigned char lds[Cfg::LDS_BYTES];
+
+  const int item = xcd_logical_block(blockIdx.x, gridDim.x);
+  const int hg = item % a.groups;
+  const int s = (item / a.groups) % a.s_max;
+  const int b = item / (a.groups * a.s_max);
+  const int L = clamp_len(a.seq_lens[b], a.cap);
+  const int t0 = s * a.split;
+  if (t0 >= L) return;
+  const int t1 = min(t0 + a.split, L);
+
+  const int tid = threadIdx.x;
+  const int w = tid >> 6;
+  const int lane = tid & 63;
+  const int r16 = lane & 15;
+  const int g = lane >> 4;
+  const int head = hg * 16 + r16;
+
+  const uint16_t* __restrict__ cache = static_cast<const uint16_t*>(a.cache);
+  const uint16_t* __restrict__ gate = static_cast<const uint16_t*>(a.gate);
+
+  // Q^T operand: lane holds head r16, dims kc*32 + g*8 .. +7 of each chunk.
+  bf16x8_t qb[NKC];
+  {
+    const float* qrow = a.qfull + (static_cast<int64_t>(b) * a.H + head) * DQ + g * 8;
+#pragma unroll
+    for (int kc = 0; kc < NKC; ++kc) {
+      const float4 x0 = *reinterpret_cast<const float4*>(qrow + kc * 32);
+      const float4 x1 = *reinterpret_cast<const float4*>(qrow + kc * 32 + 4);
+      bf16x8_t v;
+      v[0] = static_cast<__bf16>(x0.x); v[1] = static_cast<__bf16>(x0.y);
+      v[2] = static_cast<__bf16>(x0.z); v[3] = static_cast<__bf16>(x0.w);
+      v[4] = static_cast<__bf16>(x1.x); v[5] = static_cast<__bf16>(x1.y);
+      v[6] = static_cast<__bf16>(x1.z); v[7] = static_cast<__bf16>(x1.w);
+      qb[kc] = v;
+    }
+  }
+
+  f32x4_t o[NDB];
+#pragma unroll
+  for (int i = 0; i < NDB; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY;  // running max of head r16 (log2 domain), uniform over g
+  float l_run = 0.f;        // this lane's share of the running sum
+
+  uint16_t* ct = reinterpret_cast<uint16_t*>(lds) + w * DC * CTS;  // this wave's [DC][CTS]
+
+  for (int tile = w;; tile += NW) {
+    const int tt = t0 + tile * kTile;
+    if (tt >= t1) break;
+    const int nt = min(kTile, t1 - tt);
+
+    f32x4_t sacc[2];
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      const int tk = hf * 16 + r16;
+      const int j = tt + (tk < nt ? tk : nt - 1);  // clamp into the valid range; masked below
+      const int64_t slot = cache_slot(a.page_table, b, j, a.P, a.max_pages, a.num_slots);
+      const int id = clamp_id(a.ids[slot], a.V);
+      const uint16_t* row = cache + slot * DQ + g * 8;
+      const uint16_t* grow = gate + static_cast<int64_t>(id) * DC + g * 8;
+      u32x4_t raw[NKC];
+      u32x4_t graw[NLC];
+#pragma unroll
+      for (int kc = 0; kc < NKC; ++kc) raw[kc] = *reinterpret_cast<const u32x4_t*>(row + kc * 32);
+#pragma unroll
+      for (int kc = 0; kc < NLC; ++kc) graw[kc] = *reinterpret_cast<const u32x4_t*>(grow + kc * 32);
+
+      f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+      const int pos = ct_pos(hf, r16);
+#pragma unroll
+      for (int kc = 0; kc < NKC; ++kc) {
+        bf16x8_t av;
+        if (kc < NLC) {
+          // gate in fp32, round the gated latent to bf16 once
+          uint32_t pk[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float lo = bf16_lo(raw[kc][e]) * bf16_lo(graw[kc][e]);
+            const float hi = bf16_hi(raw[kc][e]) * bf16_hi(graw[kc][e]);
+            pk[e] = pack_bf16x2(lo, hi);
+          }
+          u32x4_t pv = {pk[0], pk[1], pk[2], pk[3]};
+          av = __builtin_bit_cast(bf16x8_t, pv);
+          // transposed copy for the value product: ct[dim][pos]
+          uint16_t* col = ct + (kc * 32 + g * 8) * CTS + pos;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            col[(2 * e) * CTS] = static_cast<uint16_t>(pk[e] & 0xffffu);
+            col[(2 * e + 1) * CTS] = static_cast<uint16_t>(pk[e] >> 16);
+          }
+        } else {
+          av = __builtin_bit_cast(bf16x8_t, raw[kc]);
+        }
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, qb[kc], acc, 0, 0, 0);
+      }
+      sacc[hf] = acc;
+    }
+
+    // online softmax: lane holds head r16, tokens hf*16 + 4g + r
+    float sv[8];
+    float mt = -INFINITY;
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int tk = hf * 16 + 4 * g + r;
+        const float x = tk < nt ? sacc[hf][r] * a.scale_log2 : -INFINITY;
+        sv[hf * 4 + r] = x;
+        mt = fmaxf(mt, x);
+      }
+    }
+    mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
+    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+    const float m_new = fmaxf(m_run, mt);
+    const float alpha = exp2f(m_run - m_new);
+    m_run = m_new;
+    float psum = 0.f;
+    bf16x8_t pb;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float p = exp2f(sv[i] - m_new);
+      psum += p;
+      pb[i] = static_cast<__bf16>(p);
+    }
+    l_run = l_run * alpha + psum;
+#pragma unroll
+    for (int i = 0; i < NDB; ++i) o[i] *= alpha;
+
+    wave_lds_sync();
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+      const bf16x8_t av = *reinterpret_cast<const bf16x8_t*>(ct + (db * 16 + r16) * CTS + g * 8);
+      o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, pb, o[db], 0, 0, 0);
+    }
+    wave_lds_sync();
+  }
+
+  // ---- merge the NW waves of this work-group (fixed order) ----
+  l_run += __shfl_xor(l_run, 16, 64);
+  l_run += __shfl_xor(l_run, 32, 64);
+  __syncthreads();  // all waves done with their ct regions
+  float* mo = reinterpret_cast<float*>(lds);  // [NW][16][DC]
+  float* ml = mo + NW * 16 * DC;              // [NW][16][2]
+  if (g == 0) {
+    ml[(w * 16 + r16) * 2 + 0] = m_run;
+    ml[(w * 16 + r16) * 2 + 1] = l_run;
+  }
+  __syncthreads();
+  float M = -INFINITY;
+#pragma unroll
+  for (int v = 0; v < NW; ++v) M = fmaxf(M, ml[(v * 16 + r16) * 2]);
+  const float f = exp2f(m_run - M);  // 0 for a wave that saw no tile
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) mo[(w * 16 + r16) * DC + db * 16 + 4 * g + r] = o[db][r] * f;
+  }
+  __syncthreads();
+  const int64_t pbase = (static_cast<int64_t>(b) * a.s_max + s) * a.H + hg * 16;
+  for (int i = tid; i < 16 * DC; i += NW * 64) {
+    float sum = 0.f;
+#pragma unroll
+    for (int v = 0; v < NW; ++v) sum += mo[v * 16 * DC + i];
+    a.part_o[pbase * DC + i] = sum;
+  }
+  if (tid < 16) {
+    float Mh = -INFINITY;
+#pragma unroll
+    for (int v = 0; v < NW; ++v) Mh = fmaxf(Mh, ml[(v * 16 + tid) * 2]);
+    float Lh = 0.f;
+#pragma unroll
+    for (int v = 0; v < NW; ++v) {
+      const float mv = ml[(v * 16 + tid) * 2];
+      Lh += ml[(v * 16 + tid) * 2 + 1] * (mv == -INFINITY ? 0.f : exp2f(mv - Mh));
+    }
+    a.part_ml[(pbase + tid) * 2 + 0] = Mh;
+    a.part_ml[(pbase + tid) * 2 + 1] = Lh;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// 3. combine: merge the splits of (b, h) and apply W_UV[h].
+// grid (H, B), 256 threads.
+// ---------------------------------------------------------------------------
+template <bool BF16>
+__global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ part_ml,
+                                                      const float* __restrict__ part_o,
+                                                      const void* __restrict__ w_uv,
+                                                      const int32_t* __restrict__ seq_lens, void* __restrict__ out,
+                                                      int H, int DC, int DV, int cap, int split, int s_max) {
+  extern __shared__ float smem[];  // o[DC], wgt[s_max]
+  float* o_s = smem;
+  float* wgt = smem + DC;
+  const int h = blockIdx.x, b = blockIdx.y;
+  const int L = clamp_len(seq_lens[b], cap);
+  const int64_t obase = (static_cast<int64_t>(b) * H + h) * DV;
+  if (L == 0) {
+    for (int v = threadIdx.x; v < DV; v += blockDim.x) st<BF16>(out, obase + v, 0.f);
+    return;
+  }
+  const int ns = min((L + split - 1) / split, s_max);
+  // split weights exp2(m_s - M) / sum_s l_s exp2(m_s - M), computed by wave 0
+  if (threadIdx.x < 64) {
+    float M = -INFINITY;
+    for (int sidx = threadIdx.x; sidx < ns; sidx += 64)
+      M = fmaxf(M, part_ml[((static_cast<int64_t>(b) * s_max + sidx) * H + h) * 2]);
+    M = wave_max(M);
+    float Ls = 0.f;
+    for (int sidx = threadIdx.x; sidx < ns; sidx += 64) {
+      const int64_t k = ((static_cast<int64_t>(b) * s_max + sidx) * H + h) * 2;
+      const float e = exp2f(part_ml[k] - M);
+      wgt[sidx] = e;
+      Ls += part_ml[k + 1] * e;
+    }
+    Ls = wave_sum(Ls);
+    const float inv = 1.f / Ls;
+    for (int sidx = threadIdx.x; sidx < ns; sidx += 64) wgt[sidx] *= inv;
+  }
+  __syncthreads();
+  for (int c = threadIdx.x; c < DC; c += blockDim.x) {
+    float acc = 0.f;
+    for (int sidx = 0; sidx < ns; ++sidx)
+      acc = fmaf(wgt[sidx], part_o[((static_cast<int64_t>(b) * s_max + sidx) * H + h) * DC + c], acc);
+    o_s[c] = acc;
+  }
+  __syncthreads();
+  const int64_t wbase = static_cast<int64_t>(h) * DV * DC;
+  for (int v = threadIdx.x; v < DV; v += blockDim.x) {
+    float acc = 0.f;
+    const int64_t rb = wbase + static_cast<int64_t>(v) * DC;
+    for (int c = 0; c < DC; c += 4) {
+      const float4 wv = ld4<BF16>(w_uv, rb + c);
+      acc = fmaf(wv.x, o_s[c], acc);
+      acc = fmaf(wv.y, o_s[c + 1], acc);
+      acc = fmaf(wv.z, o_s[c + 2], acc);
+      acc = fmaf(wv.w, o_s[c + 3], acc);
+    }
+    st<BF16>(out, obase + v, acc);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// host launch helpers
+// ---------------------------------------------------------------------------
+namespace {
+
+template <typename K>
+hipError_t set_lds(K kernel, size_t bytes) {
+  if (bytes <= 65536) return hipSuccess;
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                             static_cast<int>(bytes));
+}
+
+template <int DC, int DR>
+hipError_t launch_mfma(const SplitArgs& a, int nblocks, hipStream_t stream) {
+  hipLaunchKernelGGL((split_mfma_kernel<DC, DR>), dim3(nblocks), dim3(MfmaCfg<DC>::NW * 64), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_split(const eg_mla_dims& d, const DecodePlan& p, const SplitArgs& a, hipStream_t stream) {
+  const int64_t nblocks64 = static_cast<int64_t>(a.B) * a.s_max * a.groups;
+  if (nblocks64 > 0x7fffffff) return hipErrorInvalidValue;
+  const int nblocks = static_cast<int>(nblocks64);
+  if (p.path == EG_MLA_PATH_MFMA) {
+    if (d.latent_dim == 128) return launch_mfma<128, 64>(a, nblocks, stream);
+    if (d.latent_dim == 320) return launch_mfma<320, 64>(a, nblocks, stream);
+    if (d.latent_dim == 512) return launch_mfma<512, 64>(a, nblocks, stream);
+    return hipErrorInvalidValue;
+  }
+  const int DQ = d.latent_dim + d.rope_dim;
+  size_t lds = sizeof(float) * (static_cast<size_t>(a.hpg) * DQ + kTile * (DQ + 1) + a.hpg * kTile + a.hpg + 1) +
+               kTile * (sizeof(int64_t) + sizeof(int)) + 16;
+  if (d.dtype == EG_MLA_BF16) {
+    hipError_t e = set_lds(split_valu_kernel<true>, lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(split_valu_kernel<true>, dim3(nblocks), dim3(kValuThreads), lds, stream, a);
+  } else {
+    hipError_t e = set_lds(split_valu_kernel<false>, lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(split_valu_kernel<false>, dim3(nblocks), dim3(kValuThreads), lds, stream, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+}  // namespace egmla
+
+using namespace egmla;
+
+extern "C" eg_mla_status eg_mla_decode_planned(const eg_mla_dims* dims, int32_t batch, const void* q,
+                                               const void* latent_cache, const int32_t* token_id_cache,
+                                               const void* gate_table, const void* w_uk, const void* w_uv,
+                                               const int32_t* seq_lens, const int32_t* page_table,
+                                               int32_t max_pages_per_seq, int64_t num_slots, void* workspace,
+                                               size_t workspace_bytes, void* out, void* stream_,
+                                               const eg_mla_plan* plan) {
+  DecodePlan p;
+  eg_mla_status st = validate_decode(dims, batch, q, latent_cache, token_id_cache, gate_table, w_uk, w_uv,
+                                     seq_lens, max_pages_per_seq, num_slots, page_table, workspace,
+                                     workspace_bytes, out, plan, &p);
+  if (st != EG_MLA_OK || batch == 0) return st;
+  const eg_mla_dims& d = *dims;
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  const bool bf = d.dtype == EG_MLA_BF16;
+  (void)hipGetLastError();  // clear a stale error so the checks below are ours
+
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  float* qfull = reinterpret_cast<float*>(ws + p.off_q);
+  float* part_ml = reinterpret_cast<float*>(ws + p.off_ml);
+  float* part_o = reinterpret_cast<float*>(ws + p.off_o);
+
+  // 1. absorption
+  {
+    dim3 grid(d.num_heads, (batch + kAbsorbRows - 1) / kAbsorbRows);
+    const size_t lds = sizeof(float) * kAbsorbRows * d.head_dim;
+    if (bf)
+      hipLaunchKernelGGL(absorb_kernel<true>, grid, dim3(256), lds, stream, q, w_uk, qfull, batch, d.num_heads,
+                         d.head_dim, d.latent_dim, d.rope_dim);
+    else
+      hipLaunchKernelGGL(absorb_kernel<false>, grid, dim3(256), lds, stream, q, w_uk, qfull, batch, d.num_heads,
+                         d.head_dim, d.latent_dim, d.rope_dim);
+    if (hipGetLastError() != hipSuccess) return EG_MLA_ERR_HIP;
+  }
+  // 2. split kernel (skipped when the cache has no capacity: every length clamps to 0)
+  if (p.capacity > 0) {
+    SplitArgs a;
+    a.qfull = qfull;
+    a.cache = latent_cache;
+    a.ids = token_id_cache;
+    a.gate = gate_table;
+    a.seq_lens = seq_lens;
+    a.page_table = page_table;
+    a.part_ml = part_ml;
+    a.part_o = part_o;
+    a.num_slots = num_slots;
+    a.B = batch;
+    a.H = d.num_heads;
+    a.DC = d.latent_dim;
+    a.DR = d.rope_dim;
+    a.P = d.page_size;
+    a.max_pages = max_pages_per_seq;
+    a.V = d.vocab_size;
+    a.cap = p.capacity;
+    a.split = p.split_tokens;
+    a.s_max = p.s_max;
+    a.groups = p.head_groups;
+    a.hpg = p.heads_per_group;
+    a.scale_log2 = softmax_scale(d) * kLog2e;
+    hipEvent_t ev0 = plan ? static_cast<hipEvent_t>(plan->split_start_event) : nullptr;
+    hipEvent_t ev1 = plan ? static_cast<hipEvent_t>(plan->split_stop_event) : nullptr;
+    if (ev0 && hipEventRecord(ev0, stream) != hipSuccess) return EG_MLA_ERR_HIP;
+    if (launch_split(d, p, a, stream) != hipSuccess) return EG_MLA_ERR_HIP;
+    if (ev1 && hipEventRecord(ev1, stream) != hipSuccess) return EG_MLA_ERR_HIP;
+  }
+  // 3. combine + W_UV
+  {
+    dim3 grid(d.num_heads, batch);
+    const size_t lds = sizeof(float) * (d.latent_dim + p.s_max);
+    if (lds > 160 * 1024) return EG_MLA_ERR_UNSUPPORTED;
+    if (bf) {
+      if (set_lds(combine_kernel<true>, lds) != hipSuccess) return EG_MLA_ERR_HIP;
+      hipLaunchKernelGGL(combine_kernel<true>, grid, dim3(256), lds, stream, part_ml, part_o, w_uv, seq_lens, out,
+                         d.num_heads, d.latent_dim, d.v_head_dim, p.capacity, p.split_tokens, p.s_max);
+    } else {
+      if (set_lds(combine_kernel<false>, lds) != hipSuccess) return EG_MLA_ERR_HIP;
+      hipLaunchKernelGGL(combine_kernel<false>, grid, dim3(256), lds, stream, part_ml, part_o, w_uv, seq_lens, out,
+                         d.num_heads, d.latent_dim, d.v_head_dim, p.capacity, p.split_tokens, p.s_max);
+    }
+    if (hipGetLastError() != hipSuccess) return EG_MLA_ERR_HIP;
+  }
+  return EG_MLA_OK;
+}
+
+extern "C" eg_mla_status eg_mla_decode(const eg_mla_dims* dims, int32_t batch, const void* q,
+                                       const void* latent_cache, const int32_t* token_id_cache,
+                                       const void* gate_table, const void* w_uk, const void* w_uv,
+                                       const int32_t* seq_lens, const int32_t* page_table,
+                                       int32_t max_pages_per_seq, int64_t num_slots, void* workspace,
+                                       size_t workspace_bytes, void* out, void* stream) {
+  return eg_mla_decode_planned(dims, batch, q, latent_cache, token_id_cache, gate_table, w_uk, w_uv, seq_lens,
+                               page_table, max_pages_per_seq, num_slots, workspace, workspace_bytes, out, stream,
+                               nullptr);
+}

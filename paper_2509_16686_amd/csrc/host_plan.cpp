@@ -1,0 +1,191 @@
+// Host-side validation, plan selection and workspace layout (no HIP calls).
+#include "host_plan.h"
+
+#include <algorithm>
+
+namespace egmla {
+
+namespace {
+constexpr int kMaxRowDim = 640;     // d_c + d_r handled by the VALU kernel's LDS tile
+constexpr int kMaxHeadDim = 1024;   // d_h and d_v
+constexpr int kTargetWorkItems = 1024;
+constexpr int kMaxSplitTokens = 2048;
+
+int ceil_div(int64_t a, int64_t b) { return static_cast<int>((a + b - 1) / b); }
+bool aligned16(const void* p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; }
+}  // namespace
+
+bool mfma_shape_supported(const eg_mla_dims& d) {
+  if (d.dtype != EG_MLA_BF16) return false;
+  if (d.num_heads % 16 != 0) return false;
+  if (d.rope_dim != 64) return false;
+  return d.latent_dim == 128 || d.latent_dim == 320 || d.latent_dim == 512;
+}
+
+eg_mla_status check_dims(const eg_mla_dims* d) {
+  if (!d) return EG_MLA_ERR_INVALID_ARG;
+  if (d->dtype != EG_MLA_FP32 && d->dtype != EG_MLA_BF16) return EG_MLA_ERR_INVALID_ARG;
+  if (d->num_heads < 1 || d->head_dim < 1 || d->v_head_dim < 1 || d->latent_dim < 1 || d->rope_dim < 0 ||
+      d->vocab_size < 1 || d->page_size < 1 || d->gate_dim < 1)
+    return EG_MLA_ERR_INVALID_ARG;
+  if (d->softmax_scale != d->softmax_scale) return EG_MLA_ERR_INVALID_ARG;  // NaN
+  if (d->gate_dim != d->latent_dim) return EG_MLA_ERR_UNSUPPORTED;
+  // 16-byte vector access to latent rows, gate rows and query rows.
+  const int vec = d->dtype == EG_MLA_BF16 ? 8 : 4;
+  if (d->latent_dim % vec != 0 || d->rope_dim % vec != 0 || d->head_dim % vec != 0)
+    return EG_MLA_ERR_UNSUPPORTED;
+  if (d->latent_dim + d->rope_dim > kMaxRowDim) return EG_MLA_ERR_UNSUPPORTED;
+  if (d->head_dim > kMaxHeadDim || d->v_head_dim > kMaxHeadDim) return EG_MLA_ERR_UNSUPPORTED;
+  return EG_MLA_OK;
+}
+
+eg_mla_status make_decode_plan(const eg_mla_dims& d, int32_t batch, int32_t max_pages_per_seq,
+                               const eg_mla_plan* plan, DecodePlan* out) {
+  DecodePlan p;
+  const int forced = plan ? plan->path : EG_MLA_PATH_AUTO;
+  if (forced != EG_MLA_PATH_AUTO && forced != EG_MLA_PATH_VALU && forced != EG_MLA_PATH_MFMA)
+    return EG_MLA_ERR_INVALID_ARG;
+  const bool mfma_ok = mfma_shape_supported(d);
+  if (forced == EG_MLA_PATH_MFMA && !mfma_ok) return EG_MLA_ERR_UNSUPPORTED;
+  p.path = (forced == EG_MLA_PATH_VALU || !mfma_ok) ? EG_MLA_PATH_VALU : EG_MLA_PATH_MFMA;
+
+  const int64_t cap64 = static_cast<int64_t>(max_pages_per_seq) * d.page_size;
+  if (cap64 > (1 << 30)) return EG_MLA_ERR_INVALID_ARG;
+  p.capacity = static_cast<int>(cap64);
+
+  if (p.path == EG_MLA_PATH_MFMA) {
+    p.heads_per_group = 16;
+  } else {
+    // Heads per VALU work item: at most 8192 latent accumulators per workgroup.
+    p.heads_per_group = std::max(1, std::min({d.num_heads, 8192 / d.latent_dim, 256}));
+  }
+  p.head_groups = ceil_div(d.num_heads, p.heads_per_group);
+
+  int split = plan ? plan->split_tokens : 0;
+  if (split < 0 || split % kTile != 0) return EG_MLA_ERR_INVALID_ARG;
+  if (split == 0) {
+    const int64_t work = static_cast<int64_t>(std::max(batch, 1)) * std::max(p.capacity, 1) * p.head_groups;
+    int64_t s = (work + kTargetWorkItems - 1) / kTargetWorkItems;
+    s = (s + kTile - 1) / kTile * kTile;
+    const int min_split = p.path == EG_MLA_PATH_MFMA ? 256 : 128;
+    s = std::max<int64_t>(s, min_split);
+    s = std::min<int64_t>(s, kMaxSplitTokens);
+    split = static_cast<int>(s);
+  }
+  p.split_tokens = split;
+  p.s_max = std::max(1, ceil_div(std::max(p.capacity, 1), split));
+
+  const size_t B = static_cast<size_t>(std::max(batch, 0));
+  const size_t H = static_cast<size_t>(d.num_heads);
+  const size_t DQ = static_cast<size_t>(d.latent_dim + d.rope_dim);
+  const size_t S = static_cast<size_t>(p.s_max);
+  size_t off = 0;
+  p.off_q = off;
+  off = align_up(off + B * H * DQ * 4);
+  p.off_ml = off;
+  off = align_up(off + B * S * H * 2 * 4);
+  p.off_o = off;
+  off = align_up(off + B * S * H * static_cast<size_t>(d.latent_dim) * 4);
+  p.bytes = std::max<size_t>(off, kAlign);
+  *out = p;
+  return EG_MLA_OK;
+}
+
+eg_mla_status validate_decode(const eg_mla_dims* d, int32_t batch, const void* q, const void* latent_cache,
+                              const int32_t* token_id_cache, const void* gate_table, const void* w_uk,
+                              const void* w_uv, const int32_t* seq_lens, int32_t max_pages_per_seq,
+                              int64_t num_slots, const int32_t* page_table, const void* workspace,
+                              size_t workspace_bytes, const void* out, const eg_mla_plan* plan, DecodePlan* p) {
+  eg_mla_status st = check_dims(d);
+  if (st != EG_MLA_OK) return st;
+  if (batch < 0 || max_pages_per_seq < 0 || num_slots < 0) return EG_MLA_ERR_INVALID_ARG;
+  st = make_decode_plan(*d, batch, max_pages_per_seq, plan, p);
+  if (st != EG_MLA_OK) return st;
+  if (batch == 0) return EG_MLA_OK;
+  if (!q || !gate_table || !w_uk || !w_uv || !seq_lens || !out) return EG_MLA_ERR_INVALID_ARG;
+  if (max_pages_per_seq > 0 && (!latent_cache || !token_id_cache)) return EG_MLA_ERR_INVALID_ARG;
+  if (!page_table) {
+    // contiguous rows: every sequence's capacity must fit in the cache
+    const int64_t need = static_cast<int64_t>(batch) * max_pages_per_seq * d->page_size;
+    if (need > num_slots) return EG_MLA_ERR_INVALID_ARG;
+  } else if (num_slots < d->page_size && max_pages_per_seq > 0) {
+    return EG_MLA_ERR_INVALID_ARG;
+  }
+  // 16-byte vector loads of rows and weights
+  if (!aligned16(q) || !aligned16(latent_cache) || !aligned16(gate_table) || !aligned16(w_uk) || !aligned16(w_uv))
+    return EG_MLA_ERR_INVALID_ARG;
+  if (!workspace || workspace_bytes < p->bytes) return EG_MLA_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return EG_MLA_ERR_WORKSPACE;
+  return EG_MLA_OK;
+}
+
+eg_mla_status validate_append(const eg_mla_dims* d, int32_t n_tokens, int32_t hidden, const void* x,
+                              const int32_t* token_ids, const int32_t* positions, const int32_t* slots,
+                              const void* w_dkv, const void* latent_cache, const int32_t* token_id_cache,
+                              int64_t num_slots) {
+  eg_mla_status st = check_dims(d);
+  if (st != EG_MLA_OK) return st;
+  if (n_tokens < 0 || hidden < 1 || num_slots < 0) return EG_MLA_ERR_INVALID_ARG;
+  if (hidden > 32768) return EG_MLA_ERR_UNSUPPORTED;  // x row staged in LDS
+  if (d->rope_dim % 2 != 0) return EG_MLA_ERR_INVALID_ARG;
+  if (n_tokens == 0) return EG_MLA_OK;
+  if (!x || !token_ids || !positions || !slots || !w_dkv || !latent_cache || !token_id_cache)
+    return EG_MLA_ERR_INVALID_ARG;
+  return EG_MLA_OK;
+}
+
+size_t prefill_workspace_bytes(const eg_mla_dims& d, int32_t seq_len) {
+  const size_t T = static_cast<size_t>(std::max(seq_len, 0));
+  const size_t H = static_cast<size_t>(d.num_heads);
+  // fp32 explicit keys [H, T, d_h + d_r] and values [H, T, d_v]
+  size_t k = align_up(H * T * static_cast<size_t>(d.head_dim + d.rope_dim) * 4);
+  size_t v = align_up(H * T * static_cast<size_t>(d.v_head_dim) * 4);
+  return std::max<size_t>(k + v, kAlign);
+}
+
+eg_mla_status validate_prefill(const eg_mla_dims* d, int32_t seq_len, const void* q, const void* latent,
+                               const int32_t* token_ids, const void* gate_table, const void* w_uk,
+                               const void* w_uv, const void* workspace, size_t workspace_bytes,
+                               const void* out) {
+  eg_mla_status st = check_dims(d);
+  if (st != EG_MLA_OK) return st;
+  if (seq_len < 0) return EG_MLA_ERR_INVALID_ARG;
+  if (seq_len > 32768) return EG_MLA_ERR_UNSUPPORTED;  // one score row staged in LDS
+  if (seq_len == 0) return EG_MLA_OK;
+  if (!q || !latent || !token_ids || !gate_table || !w_uk || !w_uv || !out) return EG_MLA_ERR_INVALID_ARG;
+  if (!workspace || workspace_bytes < prefill_workspace_bytes(*d, seq_len)) return EG_MLA_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return EG_MLA_ERR_WORKSPACE;
+  return EG_MLA_OK;
+}
+
+}  // namespace egmla
+
+extern "C" {
+
+const char* eg_mla_status_string(eg_mla_status s) {
+  switch (s) {
+    case EG_MLA_OK: return "EG_MLA_OK";
+    case EG_MLA_ERR_INVALID_ARG: return "EG_MLA_ERR_INVALID_ARG: invalid argument";
+    case EG_MLA_ERR_UNSUPPORTED: return "EG_MLA_ERR_UNSUPPORTED: shape or option not supported";
+    case EG_MLA_ERR_WORKSPACE: return "EG_MLA_ERR_WORKSPACE: workspace missing, misaligned or too small";
+    case EG_MLA_ERR_HIP: return "EG_MLA_ERR_HIP: HIP runtime or launch failure";
+  }
+  return "EG_MLA_ERR_UNKNOWN";
+}
+
+eg_mla_status eg_mla_check_dims(const eg_mla_dims* dims) { return egmla::check_dims(dims); }
+
+size_t eg_mla_decode_workspace_size(const eg_mla_dims* dims, int32_t batch, int32_t max_pages_per_seq,
+                                    const eg_mla_plan* plan) {
+  if (egmla::check_dims(dims) != EG_MLA_OK || batch < 0 || max_pages_per_seq < 0) return 0;
+  egmla::DecodePlan p;
+  if (egmla::make_decode_plan(*dims, batch, max_pages_per_seq, plan, &p) != EG_MLA_OK) return 0;
+  return p.bytes;
+}
+
+size_t eg_mla_prefill_workspace_size(const eg_mla_dims* dims, int32_t seq_len) {
+  if (egmla::check_dims(dims) != EG_MLA_OK || seq_len < 0) return 0;
+  return egmla::prefill_workspace_bytes(*dims, seq_len);
+}
+
+}  // extern "C"

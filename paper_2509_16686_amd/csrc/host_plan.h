@@ -1,0 +1,69 @@
+// Host-side validation, plan selection and workspace layout for EG-MLA decode.
+// Pure C++: no HIP calls, so it builds and is tested without a GPU.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+
+#include "eg_mla.h"
+
+namespace egmla {
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t x, size_t a = kAlign) { return (x + a - 1) / a * a; }
+
+// Token-tile granularity of every decode kernel.
+constexpr int kTile = 32;
+
+// MFMA kernel instantiations: (latent_dim, rope_dim) pairs with a compiled fast path.
+bool mfma_shape_supported(const eg_mla_dims& d);
+
+struct DecodePlan {
+  int path = EG_MLA_PATH_VALU;  // resolved: VALU or MFMA
+  int split_tokens = 0;         // tokens per split-K work item
+  int s_max = 0;                // splits per sequence (upper bound from the capacity)
+  int capacity = 0;             // max_pages_per_seq * page_size
+  int head_groups = 1;          // work items per (b, split) along heads
+  int heads_per_group = 0;
+  // workspace layout (byte offsets)
+  size_t off_q = 0;     // fp32 [B, H, d_c + d_r]  absorbed query | RoPE query
+  size_t off_ml = 0;    // fp32 [B, s_max, H, 2]   running max (log2 domain), sum
+  size_t off_o = 0;     // fp32 [B, s_max, H, d_c] unnormalised latent outputs
+  size_t bytes = 0;
+};
+
+eg_mla_status check_dims(const eg_mla_dims* d);
+
+// Resolves `plan` (NULL = automatic) for a decode call.  Returns
+// EG_MLA_ERR_UNSUPPORTED when a forced path is unavailable for the shape.
+eg_mla_status make_decode_plan(const eg_mla_dims& d, int32_t batch, int32_t max_pages_per_seq,
+                               const eg_mla_plan* plan, DecodePlan* out);
+
+// Checks every host-visible argument of a decode call (pointers, sizes,
+// workspace) against the resolved plan.
+eg_mla_status validate_decode(const eg_mla_dims* d, int32_t batch, const void* q, const void* latent_cache,
+                              const int32_t* token_id_cache, const void* gate_table, const void* w_uk,
+                              const void* w_uv, const int32_t* seq_lens, int32_t max_pages_per_seq,
+                              int64_t num_slots, const int32_t* page_table, const void* workspace,
+                              size_t workspace_bytes, const void* out, const eg_mla_plan* plan, DecodePlan* p);
+
+eg_mla_status validate_append(const eg_mla_dims* d, int32_t n_tokens, int32_t hidden, const void* x,
+                              const int32_t* token_ids, const int32_t* positions, const int32_t* slots,
+                              const void* w_dkv, const void* latent_cache, const int32_t* token_id_cache,
+                              int64_t num_slots);
+
+size_t prefill_workspace_bytes(const eg_mla_dims& d, int32_t seq_len);
+
+eg_mla_status validate_prefill(const eg_mla_dims* d, int32_t seq_len, const void* q, const void* latent,
+                               const int32_t* token_ids, const void* gate_table, const void* w_uk,
+                               const void* w_uv, const void* workspace, size_t workspace_bytes,
+                               const void* out);
+
+inline float softmax_scale(const eg_mla_dims& d) {
+  if (d.softmax_scale > 0.f) return d.softmax_scale;
+  return 1.0f / __builtin_sqrtf(static_cast<float>(d.head_dim + d.rope_dim));
+}
+
+inline int elem_bytes(const eg_mla_dims& d) { return d.dtype == EG_MLA_BF16 ? 2 : 4; }
+
+}  // namespace egmla

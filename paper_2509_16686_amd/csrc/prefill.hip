@@ -1,0 +1,147 @@
+// Plain causal prefill in the explicit (non-absorbed) form, as a second,
+// independent device-side implementation of App. C Eq. (C.2), (C.6),
+// (C.11)-(C.13) with the latent-space gate of Sec. 3.1 Eq. (3)-(5).
+//
+//   kv kernel:   K[h][t] = [W_UK[h] c~_t ; k^R_t],  V[h][t] = W_UV[h] c~_t   (fp32 workspace)
+//   attn kernel: out[t][h] = sum_{j<=t} softmax_j(tau q_t,h . K[h][j]) V[h][j]
+// Deliberately simple: one work-group per (t, h), no tiling.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+
+#include "device_common.h"
+#include "eg_mla.h"
+#include "host_plan.h"
+
+namespace egmla {
+
+constexpr int kPrefillThreads = 256;
+
+template <bool BF16>
+__global__ __launch_bounds__(kPrefillThreads) void prefill_kv_kernel(const void* __restrict__ latent,
+                                                                     const int32_t* __restrict__ token_ids,
+                                                                     const void* __restrict__ gate,
+                                                                     const void* __restrict__ w_uk,
+                                                                     const void* __restrict__ w_uv,
+                                                                     float* __restrict__ K, float* __restrict__ Vv,
+                                                                     int T, int DH, int DV, int DC, int DR, int Vocab) {
+  extern __shared__ float cg[];  // gated latent [DC]
+  const int t = blockIdx.x, h = blockIdx.y;
+  const int DQ = DC + DR;
+  const int DK = DH + DR;
+  const int id = clamp_id(token_ids[t], Vocab);
+  for (int c = threadIdx.x; c < DC; c += kPrefillThreads)
+    cg[c] = ld<BF16>(latent, static_cast<int64_t>(t) * DQ + c) * ld<BF16>(gate, static_cast<int64_t>(id) * DC + c);
+  __syncthreads();
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t kb = (static_cast<int64_t>(h) * T + t) * DK;
+  const int64_t vb = (static_cast<int64_t>(h) * T + t) * DV;
+  for (int o = w; o < DH + DV; o += kPrefillThreads / 64) {
+    const bool is_k = o < DH;
+    const int64_t rb = is_k ? (static_cast<int64_t>(h) * DH + o) * DC : (static_cast<int64_t>(h) * DV + (o - DH)) * DC;
+    const void* wp = is_k ? w_uk : w_uv;
+    float acc = 0.f;
+    for (int c = lane; c < DC; c += 64) acc = fmaf(ld<BF16>(wp, rb + c), cg[c], acc);
+    acc = wave_sum(acc);
+    if (lane == 0) {
+      if (is_k) K[kb + o] = acc;
+      else Vv[vb + o - DH] = acc;
+    }
+  }
+  for (int r = threadIdx.x; r < DR; r += kPrefillThreads)
+    K[kb + DH + r] = ld<BF16>(latent, static_cast<int64_t>(t) * DQ + DC + r);
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(kPrefillThreads) void prefill_attn_kernel(const void* __restrict__ q,
+                                                                       const float* __restrict__ K,
+                                                                       const float* __restrict__ Vv,
+                                                                       void* __restrict__ out, int T, int H, int DH,
+                                                                       int DV, int DR, float scale) {
+  extern __shared__ float sm[];  // q [DK], scores [T], reduction [kPrefillThreads / 64]
+  const int DK = DH + DR;
+  float* qs = sm;
+  float* sc = qs + DK;
+  float* red = sc + T;
+  const int t = blockIdx.x, h = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  for (int k = tid; k < DK; k += kPrefillThreads) qs[k] = ld<BF16>(q, (static_cast<int64_t>(t) * H + h) * DK + k);
+  __syncthreads();
+  const int n = t + 1;  // causal: keys 0..t
+  float mx = -INFINITY;
+  for (int j = tid; j < n; j += kPrefillThreads) {
+    const float* kr = K + (static_cast<int64_t>(h) * T + j) * DK;
+    float dot = 0.f;
+    for (int k = 0; k < DK; ++k) dot = fmaf(qs[k], kr[k], dot);
+    dot *= scale;
+    sc[j] = dot;
+    mx = fmaxf(mx, dot);
+  }
+  mx = wave_max(mx);
+  if (lane == 0) red[w] = mx;
+  __syncthreads();
+  mx = red[0];
+  for (int i = 1; i < kPrefillThreads / 64; ++i) mx = fmaxf(mx, red[i]);
+  __syncthreads();
+  float sum = 0.f;
+  for (int j = tid; j < n; j += kPrefillThreads) {
+    const float e = expf(sc[j] - mx);
+    sc[j] = e;
+    sum += e;
+  }
+  sum = wave_sum(sum);
+  if (lane == 0) red[w] = sum;
+  __syncthreads();
+  sum = 0.f;
+  for (int i = 0; i < kPrefillThreads / 64; ++i) sum += red[i];
+  const float inv = 1.f / sum;
+  for (int v = tid; v < DV; v += kPrefillThreads) {
+    float acc = 0.f;
+    for (int j = 0; j < n; ++j) acc = fmaf(sc[j], Vv[(static_cast<int64_t>(h) * T + j) * DV + v], acc);
+    st<BF16>(out, (static_cast<int64_t>(t) * H + h) * DV + v, acc * inv);
+  }
+}
+
+}  // namespace egmla
+
+using namespace egmla;
+
+namespace {
+template <bool BF16>
+eg_mla_status launch_prefill(const eg_mla_dims& d, int T, const void* q, const void* latent, const int32_t* ids,
+                             const void* gate, const void* w_uk, const void* w_uv, float* K, float* Vv, void* out,
+                             hipStream_t stream) {
+  dim3 grid(T, d.num_heads);
+  hipLaunchKernelGGL(prefill_kv_kernel<BF16>, grid, dim3(kPrefillThreads), sizeof(float) * d.latent_dim, stream,
+                     latent, ids, gate, w_uk, w_uv, K, Vv, T, d.head_dim, d.v_head_dim, d.latent_dim, d.rope_dim,
+                     d.vocab_size);
+  if (hipGetLastError() != hipSuccess) return EG_MLA_ERR_HIP;
+  const size_t lds = sizeof(float) * (static_cast<size_t>(d.head_dim + d.rope_dim) + T + kPrefillThreads / 64);
+  if (lds > 65536 && hipFuncSetAttribute(reinterpret_cast<const void*>(prefill_attn_kernel<BF16>),
+                                         hipFuncAttributeMaxDynamicSharedMemorySize,
+                                         static_cast<int>(lds)) != hipSuccess)
+    return EG_MLA_ERR_HIP;
+  hipLaunchKernelGGL(prefill_attn_kernel<BF16>, grid, dim3(kPrefillThreads), lds, stream, q, K, Vv, out, T,
+                     d.num_heads, d.head_dim, d.v_head_dim, d.rope_dim, softmax_scale(d));
+  return hipGetLastError() == hipSuccess ? EG_MLA_OK : EG_MLA_ERR_HIP;
+}
+}  // namespace
+
+extern "C" eg_mla_status eg_mla_prefill_ref(const eg_mla_dims* dims, int32_t seq_len, const void* q,
+                                            const void* latent, const int32_t* token_ids, const void* gate_table,
+                                            const void* w_uk, const void* w_uv, void* workspace,
+                                            size_t workspace_bytes, void* out, void* stream_) {
+  eg_mla_status st = validate_prefill(dims, seq_len, q, latent, token_ids, gate_table, w_uk, w_uv, workspace,
+                                      workspace_bytes, out);
+  if (st != EG_MLA_OK || seq_len == 0) return st;
+  const eg_mla_dims& d = *dims;
+  const size_t T = static_cast<size_t>(seq_len);
+  float* K = static_cast<float*>(workspace);
+  float* Vv = reinterpret_cast<float*>(static_cast<unsigned char*>(workspace) +
+                                       align_up(static_cast<size_t>(d.num_heads) * T * (d.head_dim + d.rope_dim) * 4));
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  (void)hipGetLastError();
+  if (d.dtype == EG_MLA_BF16)
+    return launch_prefill<true>(d, seq_len, q, latent, token_ids, gate_table, w_uk, w_uv, K, Vv, out, stream);
+  return launch_prefill<false>(d, seq_len, q, latent, token_ids, gate_table, w_uk, w_uv, K, Vv, out, stream);
+}

@@ -1,0 +1,126 @@
+"""The C-ABI library on the host: it loads, exports every symbol the header
+declares, and rejects malformed calls before touching a device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2509_16686_amd import binding as B
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "eg_mla.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(eg_mla_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    return B.lib()
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = declared_functions()
+    assert len(names) >= 8
+    for n in names:
+        assert hasattr(L, n), n
+    assert sorted(B.EXPORTS) == names
+
+
+def dims(**kw):
+    base = dict(num_heads=16, head_dim=128, v_head_dim=128, latent_dim=128, rope_dim=64, vocab_size=50304,
+                page_size=64, dtype=B.BF16)
+    base.update(kw)
+    return B.make_dims(**base)
+
+
+def test_status_strings(L):
+    for s in range(5):
+        assert B.status_string(s).startswith("EG_MLA_")
+    assert "UNKNOWN" in B.status_string(77)
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(), B.OK),
+    (dict(dtype=B.FP32, latent_dim=32, rope_dim=0, head_dim=32, v_head_dim=32, num_heads=4), B.OK),
+    (dict(num_heads=0), B.ERR_INVALID_ARG),
+    (dict(page_size=0), B.ERR_INVALID_ARG),
+    (dict(dtype=7), B.ERR_INVALID_ARG),
+    (dict(gate_dim=64), B.ERR_UNSUPPORTED),
+    (dict(latent_dim=132), B.ERR_UNSUPPORTED),        # bf16 rows need 8-element multiples
+    (dict(latent_dim=1024), B.ERR_UNSUPPORTED),       # beyond the LDS tile
+    (dict(softmax_scale=float("nan")), B.ERR_INVALID_ARG),
+])
+def test_check_dims(L, kw, expect):
+    assert B.check_dims(dims(**kw)) == expect
+
+
+def test_workspace_size_queries(L):
+    d = dims()
+    auto = B.decode_workspace_size(d, 32, 64)
+    assert auto > 32 * 16 * 192 * 4
+    # explicit split of 512 tokens: 8 splits per 4096-token sequence
+    ws512 = B.decode_workspace_size(d, 32, 64, B.make_plan(B.PATH_MFMA, 512))
+    expect = 32 * 16 * 192 * 4 + 32 * 8 * 16 * 2 * 4 + 32 * 8 * 16 * 128 * 4
+    assert expect <= ws512 <= expect + 3 * 256
+    assert B.decode_workspace_size(d, 32, 64, B.make_plan(B.PATH_MFMA, 100)) == 0   # not a multiple of 32
+    assert B.decode_workspace_size(dims(num_heads=8), 1, 1, B.make_plan(B.PATH_MFMA, 0)) == 0  # no MFMA kernel
+    assert B.decode_workspace_size(dims(gate_dim=1), 1, 1, None) == 0
+    assert B.prefill_workspace_size(d, 100) >= 16 * 100 * (192 + 128) * 4
+
+
+def _decode_call(L, d, ws_bytes=1 << 20, ptr=256, batch=2, max_pages=4, num_slots=512, page_table=None, plan=None):
+    p = ctypes.c_void_p(ptr)
+    args = (ctypes.byref(d), batch, p, p, p, p, p, p, p, page_table, max_pages, num_slots,
+            ctypes.c_void_p(ptr) if ws_bytes else None, ws_bytes, p, None)
+    if plan is None:
+        return L.eg_mla_decode(*args)
+    return L.eg_mla_decode_planned(*args, ctypes.byref(plan))
+
+
+def test_decode_rejects_before_launch(L):
+    d = dims()
+    # null operands
+    z = ctypes.c_void_p(0)
+    st = L.eg_mla_decode(ctypes.byref(d), 2, None, z, z, z, z, z, z, None, 4, 512, None, 0, None, None)
+    assert st == B.ERR_INVALID_ARG
+    # workspace too small / missing
+    assert _decode_call(L, d, ws_bytes=16) == B.ERR_WORKSPACE
+    assert _decode_call(L, d, ws_bytes=0) == B.ERR_WORKSPACE
+    # contiguous cache smaller than batch * capacity
+    assert _decode_call(L, d, num_slots=100) == B.ERR_INVALID_ARG
+    # misaligned operand pointers
+    assert _decode_call(L, d, ptr=258) == B.ERR_INVALID_ARG
+    # forced MFMA on a shape without an MFMA kernel
+    assert _decode_call(L, dims(num_heads=8), plan=B.make_plan(B.PATH_MFMA, 0)) == B.ERR_UNSUPPORTED
+    # bad plan values
+    assert _decode_call(L, d, plan=B.make_plan(9, 0)) == B.ERR_INVALID_ARG
+    assert _decode_call(L, d, plan=B.make_plan(B.PATH_AUTO, 33)) == B.ERR_INVALID_ARG
+    # negative sizes
+    assert _decode_call(L, d, batch=-1) == B.ERR_INVALID_ARG
+    assert _decode_call(L, d, max_pages=-1) == B.ERR_INVALID_ARG
+    # batch 0 is a valid no-op that touches nothing
+    assert _decode_call(L, d, batch=0) == B.OK
+
+
+def test_append_and_prefill_reject_before_launch(L):
+    d = dims()
+    vp = ctypes.c_void_p(256)
+    assert L.eg_mla_append(ctypes.byref(d), 0, 64, None, None, None, None, None, None, 0.0, None, None, 0,
+                           None) == B.OK
+    assert L.eg_mla_append(ctypes.byref(d), 4, 64, None, vp, vp, vp, vp, None, 0.0, vp, vp, 8, None) == \
+        B.ERR_INVALID_ARG
+    assert L.eg_mla_append(ctypes.byref(d), 4, 0, vp, vp, vp, vp, vp, None, 0.0, vp, vp, 8, None) == \
+        B.ERR_INVALID_ARG
+    assert L.eg_mla_append(ctypes.byref(d), 4, 40000, vp, vp, vp, vp, vp, None, 0.0, vp, vp, 8, None) == \
+        B.ERR_UNSUPPORTED
+    assert L.eg_mla_prefill_ref(ctypes.byref(d), 0, None, None, None, None, None, None, None, 0, None,
+                                None) == B.OK
+    assert L.eg_mla_prefill_ref(ctypes.byref(d), 10, vp, vp, vp, vp, vp, vp, vp, 16, vp, None) == B.ERR_WORKSPACE
+    assert L.eg_mla_prefill_ref(ctypes.byref(d), 40000, vp, vp, vp, vp, vp, vp, vp, 1 << 40, vp, None) == \
+        B.ERR_UNSUPPORTED
+    assert L.eg_mla_prefill_ref(ctypes.byref(d), -1, vp, vp, vp, vp, vp, vp, vp, 1 << 20, vp, None) == \
+        B.ERR_INVALID_ARG
