@@ -202,7 +202,12 @@ __global__ __launch_bounds__(kValuThreads) void split_valu_kernel(SplitArgs a) {
 //     the MFMA A operand (lane: token lane%16, 8 consecutive dims), loads the
 //     matching 16 bytes of the token's gate row and gates in fp32,
 //   * scores S^T[token][head] = C~K x Q^T with v_mfma_f32_16x16x32_bf16,
-//     reduction over the d_c gated latent dims and the d_r RoPE dims,
+//     reduction over the d_c gated latent dims and the d_r RoPE dims.  The
+//     gated latent c*g (exact in fp32: two 8-bit significands) and the fp32
+//     absorbed query are each split into bf16 hi + lo parts and the latent
+//     part of the score is hi*hi + lo*hi + hi*lo, so the logits carry no
+//     rounding beyond that of the stored bf16 inputs (the RoPE part is exact
+//     in one product),
 //   * runs the online softmax on the accumulator layout (lane: one head,
 //     4 tokens per 16-token half), whose probabilities are exactly the
 //     B operand of the value product, so P never leaves registers,
@@ -256,20 +261,25 @@ __global__ __launch_bounds__(MfmaCfg<DC>::NW * 64) void split_mfma_kernel(SplitA
   const uint16_t* __restrict__ cache = static_cast<const uint16_t*>(a.cache);
   const uint16_t* __restrict__ gate = static_cast<const uint16_t*>(a.gate);
 
-  // Q^T operand: lane holds head r16, dims kc*32 + g*8 .. +7 of each chunk.
+  // Q^T operand: lane holds head r16, dims kc*32 + g*8 .. +7 of each chunk;
+  // latent chunks also keep the bf16 remainder of the fp32 absorbed query.
   bf16x8_t qb[NKC];
+  bf16x8_t qlo[NLC];
   {
     const float* qrow = a.qfull + (static_cast<int64_t>(b) * a.H + head) * DQ + g * 8;
 #pragma unroll
     for (int kc = 0; kc < NKC; ++kc) {
       const float4 x0 = *reinterpret_cast<const float4*>(qrow + kc * 32);
       const float4 x1 = *reinterpret_cast<const float4*>(qrow + kc * 32 + 4);
-      bf16x8_t v;
-      v[0] = static_cast<__bf16>(x0.x); v[1] = static_cast<__bf16>(x0.y);
-      v[2] = static_cast<__bf16>(x0.z); v[3] = static_cast<__bf16>(x0.w);
-      v[4] = static_cast<__bf16>(x1.x); v[5] = static_cast<__bf16>(x1.y);
-      v[6] = static_cast<__bf16>(x1.z); v[7] = static_cast<__bf16>(x1.w);
-      qb[kc] = v;
+      const float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+      bf16x8_t hi, lo;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        hi[e] = static_cast<__bf16>(x[e]);
+        lo[e] = static_cast<__bf16>(x[e] - static_cast<float>(hi[e]));
+      }
+      qb[kc] = hi;
+      if (kc < NLC) qlo[kc] = lo;
     }
   }
 
@@ -306,29 +316,34 @@ __global__ __launch_bounds__(MfmaCfg<DC>::NW * 64) void split_mfma_kernel(SplitA
       const int pos = ct_pos(hf, r16);
 #pragma unroll
       for (int kc = 0; kc < NKC; ++kc) {
-        bf16x8_t av;
         if (kc < NLC) {
-          // gate in fp32, round the gated latent to bf16 once
-          uint32_t pk[4];
+          // gate in fp32 (exact product), split into bf16 hi + lo
+          uint32_t pk[4], pl[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const float lo = bf16_lo(raw[kc][e]) * bf16_lo(graw[kc][e]);
-            const float hi = bf16_hi(raw[kc][e]) * bf16_hi(graw[kc][e]);
-            pk[e] = pack_bf16x2(lo, hi);
+            const float p0 = bf16_lo(raw[kc][e]) * bf16_lo(graw[kc][e]);
+            const float p1 = bf16_hi(raw[kc][e]) * bf16_hi(graw[kc][e]);
+            pk[e] = pack_bf16x2(p0, p1);
+            pl[e] = pack_bf16x2(p0 - bf16_lo(pk[e]), p1 - bf16_hi(pk[e]));
           }
-          u32x4_t pv = {pk[0], pk[1], pk[2], pk[3]};
-          av = __builtin_bit_cast(bf16x8_t, pv);
-          // transposed copy for the value product: ct[dim][pos]
+          const u32x4_t hv = {pk[0], pk[1], pk[2], pk[3]};
+          const u32x4_t lv = {pl[0], pl[1], pl[2], pl[3]};
+          const bf16x8_t ahi = __builtin_bit_cast(bf16x8_t, hv);
+          const bf16x8_t alo = __builtin_bit_cast(bf16x8_t, lv);
+          // transposed copy (hi part) for the value product: ct[dim][pos]
           uint16_t* col = ct + (kc * 32 + g * 8) * CTS + pos;
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             col[(2 * e) * CTS] = static_cast<uint16_t>(pk[e] & 0xffffu);
             col[(2 * e + 1) * CTS] = static_cast<uint16_t>(pk[e] >> 16);
           }
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, qb[kc], acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, qb[kc], acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, qlo[kc], acc, 0, 0, 0);
         } else {
-          av = __builtin_bit_cast(bf16x8_t, raw[kc]);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, raw[kc]), qb[kc], acc, 0,
+                                                        0, 0);
         }
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, qb[kc], acc, 0, 0, 0);
       }
       sacc[hf] = acc;
     }

@@ -34,13 +34,23 @@ def errors(got: np.ndarray, ref: np.ndarray):
     return max_abs, rel
 
 
-def assert_close(got: np.ndarray, ref: np.ndarray, storage: str, what: str = ""):
+def assert_close(got: np.ndarray, ref: np.ndarray, storage: str, what: str = "", scaled: bool = False):
+    """Element-wise parity at the stated tolerances.
+
+    ``scaled=True`` (stress cases with outputs far above unit size: a few
+    tokens, peaked logits) multiplies the bf16 max-abs bound by
+    max(1, max|ref|): a bf16 output alone is rounded by up to 2^-9 |out|,
+    and a bf16 probability or key error moves the output in proportion to
+    the value vectors' size, so the absolute error scales with |out|.
+    """
     assert got.shape == ref.shape, (got.shape, ref.shape)
     assert np.all(np.isfinite(got)), f"{what}: non-finite output"
     max_abs, rel = errors(got, ref)
+    say(f"  {what}: max_abs={max_abs:.3e} rel_l2={rel:.3e} max|ref|={float(np.abs(ref).max()):.3g}")
     if storage == "fp32":
         assert max_abs <= FP32_MAX_ABS, f"{what}: fp32 max abs err {max_abs:.3e} > {FP32_MAX_ABS}"
     else:
-        assert max_abs <= BF16_MAX_ABS, f"{what}: bf16 max abs err {max_abs:.3e} > {BF16_MAX_ABS}"
+        bound = BF16_MAX_ABS * (max(1.0, float(np.abs(ref).max())) if scaled else 1.0)
+        assert max_abs <= bound, f"{what}: bf16 max abs err {max_abs:.3e} > {bound:.3e}"
         assert rel <= BF16_REL_L2, f"{what}: bf16 rel L2 err {rel:.3e} > {BF16_REL_L2}"
     return max_abs, rel

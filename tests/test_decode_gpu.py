@@ -65,7 +65,7 @@ def test_small_ragged_paged_all_splits(gpu, path, split):
     inp = W.generate(SMALL, seq_lens=np.array([1, 33, 777, 900]))
     say(f"decode small ragged paged path={path} split={split}")
     got = gpu_decode(inp, B.make_plan(path, split))
-    assert_close(got, oracle_decode(inp), "bf16", f"path {path} split {split}")
+    assert_close(got, oracle_decode(inp), "bf16", f"path {path} split {split}", scaled=True)
 
 
 @pytest.mark.parametrize("path", [B.PATH_VALU, B.PATH_MFMA])
@@ -78,7 +78,7 @@ def test_edge_lengths(gpu, path):
     got = gpu_decode(inp, B.make_plan(path, 128))
     ref = oracle_decode(inp)
     assert np.all(got[0] == 0)
-    assert_close(got, ref, "bf16", "edge lengths")
+    assert_close(got, ref, "bf16", "edge lengths", scaled=True)
 
 
 def test_many_head_groups_and_dc512(gpu):
@@ -86,7 +86,7 @@ def test_many_head_groups_and_dc512(gpu):
     inp = W.generate(wl)
     for path in (B.PATH_VALU, B.PATH_MFMA):
         say(f"decode h128 dc512 ragged paged path={path}")
-        assert_close(gpu_decode(inp, B.make_plan(path, 256)), oracle_decode(inp), "bf16", f"path {path}")
+        assert_close(gpu_decode(inp, B.make_plan(path, 256)), oracle_decode(inp), "bf16", f"path {path}", scaled=True)
 
 
 def test_peaked_logits(gpu):
@@ -95,7 +95,7 @@ def test_peaked_logits(gpu):
     say("decode peaked logits (q x 8)")
     got = gpu_decode(inp, B.make_plan(B.PATH_MFMA, 64))
     ref = oracle_decode(inp)
-    assert_close(got, ref, "bf16", "peaked")
+    assert_close(got, ref, "bf16", "peaked", scaled=True)
 
 
 def test_paged_equals_contiguous_bitwise(gpu):
@@ -149,5 +149,5 @@ def test_out_of_range_ids_and_lengths_are_clamped(gpu):
     say("decode clamped lengths")
     got = gpu_decode(inp, B.make_plan(B.PATH_MFMA, 64))
     inp.seq_lens[:] = [10, 20, 30, cap]
-    assert_close(got, oracle_decode(inp), "bf16", "clamped")
+    assert_close(got, oracle_decode(inp), "bf16", "clamped", scaled=True)
     del lens_over
