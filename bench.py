@@ -97,6 +97,8 @@ def main():
     ap.add_argument("--split", type=int, default=0, help="tokens per split (0 = automatic)")
     ap.add_argument("--rotate-bytes", type=float, default=1.0e9)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibration-copy-mib", type=int, default=0,
+                    help="also run one device copy of this many MiB (a known byte count for profiler counters)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     args = ap.parse_args()
 
@@ -154,6 +156,7 @@ def main():
                 int(dd.cache.shape[0]), ws.data_ptr(), ws_bytes, dd.out.data_ptr(), stream, ctypes.byref(plan))
 
     warm_args = [argset(copies[k % R], plan0) for k in range(max(Wm, 1))]
+    step_args = [argset(copies[k % R], plan0) for k in range(K)]
     timed_args = [argset(copies[k % R], plans[k]) for k in range(K)]
     call = L.eg_mla_decode_planned
 
@@ -177,21 +180,36 @@ def main():
     cycles_per_ms = 1_000_000 / max(hip.elapsed_ms(s0, s1), 1e-3)
     spin_ms = 2.0 * host_per_call * K * 1e3 + 5.0
 
-    t_start, t_stop = hip.event(), hip.event()
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    torch.cuda._sleep(int(spin_ms * cycles_per_ms))
-    hip.record(t_start, stream)
-    for a in timed_args:
-        call(*a)
-    hip.record(t_stop, stream)
-    enq = time.perf_counter() - wall0
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-    total_ms = hip.elapsed_ms(t_start, t_stop)
+    def timed_loop(arglist):
+        """K calls queued behind a spin kernel; returns (GPU ms between the outer events, wall s)."""
+        t_start, t_stop = hip.event(), hip.event()
+        torch.cuda.synchronize()
+        wall0 = time.perf_counter()
+        torch.cuda._sleep(int(spin_ms * cycles_per_ms))
+        hip.record(t_start, stream)
+        for a in arglist:
+            call(*a)
+        hip.record(t_stop, stream)
+        enq = time.perf_counter() - wall0
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - wall0
+        if enq * 1e3 > spin_ms:
+            log(f"bench: warning: enqueue took {enq * 1e3:.1f} ms > spin {spin_ms:.1f} ms; GPU may have idled")
+        return hip.elapsed_ms(t_start, t_stop), wall
+
+    if args.calibration_copy_mib > 0:
+        src = torch.empty(args.calibration_copy_mib << 20, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    # (1) whole-call throughput: plain back-to-back calls, nothing between them
+    total_ms, wall = timed_loop(step_args)
+    # (2) the split kernel alone: the same calls with HIP events around every split-kernel launch
+    timed_loop(timed_args)
     kernel_ms = [hip.elapsed_ms(ev0[k], ev1[k]) for k in range(K)]
-    if enq * 1e3 > spin_ms:
-        log(f"bench: warning: enqueue took {enq * 1e3:.1f} ms > spin {spin_ms:.1f} ms; GPU may have idled")
 
     ms_per_step = total_ms / K
     k_avg_ms = float(np.mean(kernel_ms))

@@ -1,0 +1,210 @@
+// MFMA absorption and combine kernels of EG-MLA decode (bf16 storage).
+// Included by decode.hip.  Both are short, latency-bound kernels, so each
+// issues all of its global loads in one batch before using any of them.
+#pragma once
+
+namespace egmla {
+
+// ---------------------------------------------------------------------------
+// Absorption on MFMA: qfull[b, h, c] = sum_k q^C[b, h, k] W_UK[h, k, c] for
+// 16 sequences x 128 latent columns per work-group (grid H x ceil(B/16) x
+// ceil(DC/128), 256 threads), plus the q^R copy.  W_UK[h][:, c-block] is
+// loaded with 16-byte row loads and stored transposed in LDS, so the B
+// operand (8 consecutive k of one column) is one 16-byte LDS read; the A
+// operand (8 consecutive k of one query row) comes straight from global.
+// bf16 x bf16 products are exact in fp32 and accumulate in fp32.
+// ---------------------------------------------------------------------------
+constexpr int kAbsRows = 16;
+constexpr int kAbsCols = 128;
+
+template <int DH>
+__global__ __launch_bounds__(256) void absorb_mfma_kernel(const uint16_t* __restrict__ q,
+                                                          const uint16_t* __restrict__ w_uk,
+                                                          float* __restrict__ qfull, int B, int H, int DC, int DR) {
+  constexpr int KS = DH + 8;  // padded row of the transposed tile (bf16 elements)
+  constexpr int NK = DH / 32;
+  __shared__ __attribute__((aligned(16))) uint16_t wt[kAbsCols * KS];  // [c][k]
+  const int h = blockIdx.x;
+  const int b0 = blockIdx.y * kAbsRows;
+  const int c0 = blockIdx.z * kAbsCols;
+  const int nc = min(kAbsCols, DC - c0);
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
+  const int DQin = DH + DR, DQ = DC + DR;
+
+  // (1) issue every load: this thread's W rows (16 B = 8 columns each) and its A operand chunks
+  constexpr int kRowsPerPass = 256 / (kAbsCols / 8);  // 16 rows of 128 columns per pass
+  constexpr int kPasses = (DH + kRowsPerPass - 1) / kRowsPerPass;
+  const int cc = (tid % (kAbsCols / 8)) * 8;  // first of this thread's 8 columns
+  u32x4_t wv[kPasses];
+#pragma unroll
+  for (int p = 0; p < kPasses; ++p) {
+    const int k = p * kRowsPerPass + tid / (kAbsCols / 8);
+    const int kk = min(k, DH - 1);
+    const int c = min(c0 + cc, DC - 8);
+    wv[p] = *reinterpret_cast<const u32x4_t*>(w_uk + (static_cast<int64_t>(h) * DH + kk) * DC + c);
+  }
+  const int bq = min(b0 + r16, B - 1);
+  u32x4_t qa[NK];
+#pragma unroll
+  for (int ks = 0; ks < NK; ++ks)
+    qa[ks] = *reinterpret_cast<const u32x4_t*>(q + (static_cast<int64_t>(bq) * H + h) * DQin + ks * 32 + g * 8);
+  // (2) transpose W into LDS
+#pragma unroll
+  for (int p = 0; p < kPasses; ++p) {
+    const int k = p * kRowsPerPass + tid / (kAbsCols / 8);
+    if (k < DH) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        wt[(cc + 2 * e) * KS + k] = static_cast<uint16_t>(wv[p][e] & 0xffffu);
+        wt[(cc + 2 * e + 1) * KS + k] = static_cast<uint16_t>(wv[p][e] >> 16);
+      }
+    }
+  }
+  __syncthreads();
+  // (3) wave w computes column tiles w, w+4 (16 columns each)
+  for (int nt = w; nt * 16 < nc; nt += 4) {
+    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < NK; ++ks) {
+      const bf16x8_t bv = *reinterpret_cast<const bf16x8_t*>(wt + (nt * 16 + r16) * KS + ks * 32 + g * 8);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, qa[ks]), bv, acc, 0, 0, 0);
+    }
+    // lane holds D[b = 4g + r][c = nt*16 + r16]
+    const int c = c0 + nt * 16 + r16;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int b = b0 + 4 * g + r;
+      if (b < B && c < DC) qfull[(static_cast<int64_t>(b) * H + h) * DQ + c] = acc[r];
+    }
+  }
+  if (blockIdx.z == 0) {
+    for (int i = tid; i < kAbsRows * DR; i += 256) {
+      const int bb = i / DR, r = i % DR;
+      if (b0 + bb < B)
+        qfull[(static_cast<int64_t>(b0 + bb) * H + h) * DQ + DC + r] =
+            bf16_to_f32(q[(static_cast<int64_t>(b0 + bb) * H + h) * DQin + DH + r]);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Combine on MFMA: grid (H, ceil(B / 4)), 256 threads.  Wave w merges the
+// splits of sequence b0 + w for head h into LDS (fp32, divided by the softmax
+// sum): the split weights come from one load per split, then every partial
+// value of the wave is loaded in one batch.  Then out^T[v][b] =
+// W_UV[h][v][:] . o[b][:] runs on v_mfma_f32_16x16x32_bf16 with W_UV rows as
+// the A operand (16-byte loads, all issued before the first product) and o
+// split into bf16 hi + lo as the B operand (4 of its 16 columns used).
+// ---------------------------------------------------------------------------
+constexpr int kCombSeq = 4;
+
+template <int DC, int DV>
+__global__ __launch_bounds__(256) void combine_mfma_kernel(const float* __restrict__ part_ml,
+                                                           const float* __restrict__ part_o,
+                                                           const uint16_t* __restrict__ w_uv,
+                                                           const int32_t* __restrict__ seq_lens,
+                                                           uint16_t* __restrict__ out, int B, int H, int cap,
+                                                           int split, int s_max) {
+  constexpr int OS = DC + 4;
+  constexpr int PER = DC / 64;  // latent columns per lane
+  constexpr int SB = 8;         // splits per load batch
+  constexpr int NKC = DC / 32;
+  __shared__ __attribute__((aligned(16))) float o_s[16 * OS];  // rows 4..15 stay zero
+  const int h = blockIdx.x;
+  const int b0 = blockIdx.y * kCombSeq;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
+
+  // W_UV rows of this wave's output tiles: issued first, used last
+  constexpr int nvt = (DV + 15) / 16;
+  constexpr int kMaxVt = (nvt + 3) / 4;  // v-tiles per wave
+  u32x4_t wa[kMaxVt][NKC];
+#pragma unroll
+  for (int i = 0; i < kMaxVt; ++i) {
+    const int vt = w + 4 * i;
+    if (vt < nvt) {
+      const int v = min(vt * 16 + r16, DV - 1);
+#pragma unroll
+      for (int kc = 0; kc < NKC; ++kc)
+        wa[i][kc] = *reinterpret_cast<const u32x4_t*>(w_uv + (static_cast<int64_t>(h) * DV + v) * DC + kc * 32 + g * 8);
+    }
+  }
+
+  for (int i = tid; i < 12 * OS; i += 256) o_s[4 * OS + i] = 0.f;
+  {
+    const int b = b0 + w;
+    const int L = b < B ? clamp_len(seq_lens[b], cap) : 0;
+    float* orow = o_s + w * OS;
+    if (L == 0) {
+#pragma unroll
+      for (int j = 0; j < PER; ++j) orow[lane + 64 * j] = 0.f;
+    } else {
+      const int ns = min((L + split - 1) / split, s_max);
+      const int64_t base = static_cast<int64_t>(b) * s_max * H + h;  // + s * H
+      float M = -INFINITY;
+      for (int sidx = lane; sidx < ns; sidx += 64) M = fmaxf(M, part_ml[(base + static_cast<int64_t>(sidx) * H) * 2]);
+      M = wave_max(M);
+      float acc[PER];
+#pragma unroll
+      for (int j = 0; j < PER; ++j) acc[j] = 0.f;
+      float Ls = 0.f;
+      for (int s0 = 0; s0 < ns; s0 += SB) {
+        float pv[SB][PER];
+        float mv[SB], lv[SB];
+#pragma unroll
+        for (int u = 0; u < SB; ++u) {
+          const int sidx = min(s0 + u, ns - 1);
+          const int64_t row = base + static_cast<int64_t>(sidx) * H;
+          mv[u] = part_ml[row * 2];
+          lv[u] = part_ml[row * 2 + 1];
+#pragma unroll
+          for (int j = 0; j < PER; ++j) pv[u][j] = part_o[row * DC + lane + 64 * j];
+        }
+#pragma unroll
+        for (int u = 0; u < SB; ++u) {
+          const float e = s0 + u < ns ? exp2f(mv[u] - M) : 0.f;
+          Ls += lv[u] * e;
+#pragma unroll
+          for (int j = 0; j < PER; ++j) acc[j] = fmaf(e, pv[u][j], acc[j]);
+        }
+      }
+      const float inv = 1.f / Ls;
+#pragma unroll
+      for (int j = 0; j < PER; ++j) orow[lane + 64 * j] = acc[j] * inv;
+    }
+  }
+  __syncthreads();
+
+  const int b = b0 + r16;
+#pragma unroll
+  for (int i = 0; i < kMaxVt; ++i) {
+    const int vt = w + 4 * i;
+    if (vt >= nvt) break;
+    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kc = 0; kc < NKC; ++kc) {
+      const float* orow = o_s + r16 * OS + kc * 32 + g * 8;
+      const float4 x0 = *reinterpret_cast<const float4*>(orow);
+      const float4 x1 = *reinterpret_cast<const float4*>(orow + 4);
+      const float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+      bf16x8_t hi, lo;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        hi[e] = static_cast<__bf16>(x[e]);
+        lo[e] = static_cast<__bf16>(x[e] - static_cast<float>(hi[e]));
+      }
+      const bf16x8_t av = __builtin_bit_cast(bf16x8_t, wa[i][kc]);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, hi, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, lo, acc, 0, 0, 0);
+    }
+    // lane holds out^T[vt*16 + 4g + r][b0 + r16]
+    if (r16 < kCombSeq && b < B) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int vv = vt * 16 + 4 * g + r;
+        if (vv < DV) out[(static_cast<int64_t>(b) * H + h) * DV + vv] = f32_to_bf16(acc[r]);
+      }
+    }
+  }
+}
+
+}  // namespace egmla

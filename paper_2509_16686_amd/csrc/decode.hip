@@ -26,41 +26,67 @@ constexpr float kLog2e = 1.4426950408889634f;
 
 // ---------------------------------------------------------------------------
 // 1. absorption: qfull[b,h,:] = [W_UK[h]^T q^C[b,h] | q^R[b,h]]   (fp32)
-// grid (H, ceil(B / 8)), 256 threads; W_UK[h] is read once per 8 sequences.
+// grid (H, ceil(DC / 64), ceil(B / 16)), 256 threads = 64 latent columns x
+// 4 slices of the head dim.  Each W_UK row segment is read once per 16
+// sequences with 128-byte coalesced loads; the 4 slices are summed in LDS.
 // ---------------------------------------------------------------------------
-constexpr int kAbsorbRows = 8;
+constexpr int kAbsorbRows = 16;
+constexpr int kAbsorbCols = 64;
 
 template <bool BF16>
 __global__ __launch_bounds__(256) void absorb_kernel(const void* __restrict__ q, const void* __restrict__ w_uk,
                                                      float* __restrict__ qfull, int B, int H, int DH, int DC,
                                                      int DR) {
-  extern __shared__ float smem[];  // [kAbsorbRows][DH]
+  extern __shared__ float smem[];  // q rows [kAbsorbRows][DH], partial sums [4][kAbsorbRows][kAbsorbCols]
+  float* q_s = smem;
+  float* red = smem + kAbsorbRows * DH;
   const int h = blockIdx.x;
-  const int b0 = blockIdx.y * kAbsorbRows;
+  const int c0 = blockIdx.y * kAbsorbCols;
+  const int b0 = blockIdx.z * kAbsorbRows;
   const int nb = min(kAbsorbRows, B - b0);
   const int DQin = DH + DR;
   const int DQ = DC + DR;
-  for (int i = threadIdx.x; i < nb * DH; i += blockDim.x) {
+  const int tid = threadIdx.x;
+  for (int i = tid; i < kAbsorbRows * DH; i += 256) {
     const int bb = i / DH, k = i % DH;
-    smem[bb * DH + k] = ld<BF16>(q, (static_cast<int64_t>(b0 + bb) * H + h) * DQin + k);
+    q_s[i] = bb < nb ? ld<BF16>(q, (static_cast<int64_t>(b0 + bb) * H + h) * DQin + k) : 0.f;
   }
   __syncthreads();
-  const int64_t wbase = static_cast<int64_t>(h) * DH * DC;
-  for (int c = threadIdx.x; c < DC; c += blockDim.x) {
-    float acc[kAbsorbRows];
+  const int cl = tid & (kAbsorbCols - 1);
+  const int kq = tid / kAbsorbCols;  // 0..3
+  const int c = c0 + cl;
+  const int kper = (DH + 3) / 4;
+  const int k_lo = kq * kper, k_hi = min(DH, k_lo + kper);
+  float acc[kAbsorbRows];
 #pragma unroll
-    for (int bb = 0; bb < kAbsorbRows; ++bb) acc[bb] = 0.f;
-    for (int k = 0; k < DH; ++k) {
-      const float w = ld<BF16>(w_uk, wbase + static_cast<int64_t>(k) * DC + c);
+  for (int bb = 0; bb < kAbsorbRows; ++bb) acc[bb] = 0.f;
+  if (c < DC) {
+    const int64_t wbase = static_cast<int64_t>(h) * DH * DC + c;
+#pragma unroll 4
+    for (int k = k_lo; k < k_hi; ++k) {
+      const float wv = ld<BF16>(w_uk, wbase + static_cast<int64_t>(k) * DC);
 #pragma unroll
-      for (int bb = 0; bb < kAbsorbRows; ++bb) acc[bb] = fmaf(w, smem[bb * DH + k], acc[bb]);
+      for (int bb = 0; bb < kAbsorbRows; ++bb) acc[bb] = fmaf(wv, q_s[bb * DH + k], acc[bb]);
     }
-    for (int bb = 0; bb < nb; ++bb) qfull[(static_cast<int64_t>(b0 + bb) * H + h) * DQ + c] = acc[bb];
   }
-  for (int i = threadIdx.x; i < nb * DR; i += blockDim.x) {
-    const int bb = i / DR, r = i % DR;
-    qfull[(static_cast<int64_t>(b0 + bb) * H + h) * DQ + DC + r] =
-        ld<BF16>(q, (static_cast<int64_t>(b0 + bb) * H + h) * DQin + DH + r);
+#pragma unroll
+  for (int bb = 0; bb < kAbsorbRows; ++bb) red[(kq * kAbsorbRows + bb) * kAbsorbCols + cl] = acc[bb];
+  __syncthreads();
+  for (int i = tid; i < kAbsorbRows * kAbsorbCols; i += 256) {
+    const int bb = i / kAbsorbCols, cc = i % kAbsorbCols;
+    if (bb < nb && c0 + cc < DC) {
+      float v = 0.f;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) v += red[(j * kAbsorbRows + bb) * kAbsorbCols + cc];
+      qfull[(static_cast<int64_t>(b0 + bb) * H + h) * DQ + c0 + cc] = v;
+    }
+  }
+  if (blockIdx.y == 0) {
+    for (int i = tid; i < nb * DR; i += 256) {
+      const int bb = i / DR, r = i % DR;
+      qfull[(static_cast<int64_t>(b0 + bb) * H + h) * DQ + DC + r] =
+          ld<BF16>(q, (static_cast<int64_t>(b0 + bb) * H + h) * DQin + DH + r);
+    }
   }
 }
 
@@ -194,241 +220,11 @@ __global__ __launch_bounds__(kValuThreads) void split_valu_kernel(SplitArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// 2b. MFMA split kernel (bf16 storage, 16 heads per work-group).
-//
-// NW waves per work-group share one (sequence, split, head group); 32-token
-// tiles are dealt round-robin to the waves.  For its tile a wave
-//   * loads each token's row with 16-byte loads straight into the layout of
-//     the MFMA A operand (lane: token lane%16, 8 consecutive dims), loads the
-//     matching 16 bytes of the token's gate row and gates in fp32,
-//   * scores S^T[token][head] = C~K x Q^T with v_mfma_f32_16x16x32_bf16,
-//     reduction over the d_c gated latent dims and the d_r RoPE dims.  The
-//     gated latent c*g (exact in fp32: two 8-bit significands) and the fp32
-//     absorbed query are each split into bf16 hi + lo parts and the latent
-//     part of the score is hi*hi + lo*hi + hi*lo, so the logits carry no
-//     rounding beyond that of the stored bf16 inputs (the RoPE part is exact
-//     in one product),
-//   * runs the online softmax on the accumulator layout (lane: one head,
-//     4 tokens per 16-token half), whose probabilities are exactly the
-//     B operand of the value product, so P never leaves registers,
-//   * writes the gated latent transposed into its own LDS region (dims x
-//     tokens) so the value product O^T[dim][head] += C~^T x P^T reads its
-//     A operand with 16-byte LDS loads.
-// At the end the waves merge their (max, sum, O) through LDS in a fixed
-// order and write one partial per head.
+// 2b. MFMA split kernel (bf16 storage, 16 heads per work-group): split_mfma.h
 // ---------------------------------------------------------------------------
-template <int DC>
-struct MfmaCfg {
-  static constexpr int NW = DC <= 128 ? 4 : 2;
-  static constexpr int CT_STRIDE = 40;  // 32 token slots + 8 pad (bf16 elements)
-  static constexpr int LDS_BYTES_CT = NW * DC * CT_STRIDE * 2;
-  static constexpr int LDS_BYTES_MERGE = NW * 16 * DC * 4 + NW * 16 * 2 * 4;
-  static constexpr int LDS_BYTES = LDS_BYTES_CT > LDS_BYTES_MERGE ? LDS_BYTES_CT : LDS_BYTES_MERGE;
-};
-
-// Position of token t (0..31) of a tile in a transposed LDS row: the 8
-// k-slots of lane group g hold tokens 4g..4g+3 of each 16-token half.
-__device__ __forceinline__ int ct_pos(int half, int t16) { return (t16 >> 2) * 8 + half * 4 + (t16 & 3); }
-
-template <int DC, int DR>
-__global__ __launch_bounds__(MfmaCfg<DC>::NW * 64) void split_mfma_kernel(SplitArgs a) {
-  using Cfg = MfmaCfg<DC>;
-  constexpr int NW = Cfg::NW;
-  constexpr int DQ = DC + DR;
-  constexpr int NKC = DQ / 32;  // 32-dim chunks of a row
-  constexpr int NLC = DC / 32;  // gated (latent) chunks
-  constexpr int NDB = DC / 16;  // 16-dim blocks of the value product
-  constexpr int CTS = Cfg::CT_STRIDE;
-  static_assert(DQ % 32 == 0 && DC % 32 == 0, "row must split into 32-dim chunks");
-  __shared__ __attribute__((aligned(16))) unsigned char lds[Cfg::LDS_BYTES];
-
-  const int item = xcd_logical_block(blockIdx.x, gridDim.x);
-  const int hg = item % a.groups;
-  const int s = (item / a.groups) % a.s_max;
-  const int b = item / (a.groups * a.s_max);
-  const int L = clamp_len(a.seq_lens[b], a.cap);
-  const int t0 = s * a.split;
-  if (t0 >= L) return;
-  const int t1 = min(t0 + a.split, L);
-
-  const int tid = threadIdx.x;
-  const int w = tid >> 6;
-  const int lane = tid & 63;
-  const int r16 = lane & 15;
-  const int g = lane >> 4;
-  const int head = hg * 16 + r16;
-
-  const uint16_t* __restrict__ cache = static_cast<const uint16_t*>(a.cache);
-  const uint16_t* __restrict__ gate = static_cast<const uint16_t*>(a.gate);
-
-  // Q^T operand: lane holds head r16, dims kc*32 + g*8 .. +7 of each chunk;
-  // latent chunks also keep the bf16 remainder of the fp32 absorbed query.
-  bf16x8_t qb[NKC];
-  bf16x8_t qlo[NLC];
-  {
-    const float* qrow = a.qfull + (static_cast<int64_t>(b) * a.H + head) * DQ + g * 8;
-#pragma unroll
-    for (int kc = 0; kc < NKC; ++kc) {
-      const float4 x0 = *reinterpret_cast<const float4*>(qrow + kc * 32);
-      const float4 x1 = *reinterpret_cast<const float4*>(qrow + kc * 32 + 4);
-      const float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
-      bf16x8_t hi, lo;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        hi[e] = static_cast<__bf16>(x[e]);
-        lo[e] = static_cast<__bf16>(x[e] - static_cast<float>(hi[e]));
-      }
-      qb[kc] = hi;
-      if (kc < NLC) qlo[kc] = lo;
-    }
-  }
-
-  f32x4_t o[NDB];
-#pragma unroll
-  for (int i = 0; i < NDB; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  float m_run = -INFINITY;  // running max of head r16 (log2 domain), uniform over g
-  float l_run = 0.f;        // this lane's share of the running sum
-
-  uint16_t* ct = reinterpret_cast<uint16_t*>(lds) + w * DC * CTS;  // this wave's [DC][CTS]
-
-  for (int tile = w;; tile += NW) {
-    const int tt = t0 + tile * kTile;
-    if (tt >= t1) break;
-    const int nt = min(kTile, t1 - tt);
-
-    f32x4_t sacc[2];
-#pragma unroll
-    for (int hf = 0; hf < 2; ++hf) {
-      const int tk = hf * 16 + r16;
-      const int j = tt + (tk < nt ? tk : nt - 1);  // clamp into the valid range; masked below
-      const int64_t slot = cache_slot(a.page_table, b, j, a.P, a.max_pages, a.num_slots);
-      const int id = clamp_id(a.ids[slot], a.V);
-      const uint16_t* row = cache + slot * DQ + g * 8;
-      const uint16_t* grow = gate + static_cast<int64_t>(id) * DC + g * 8;
-      u32x4_t raw[NKC];
-      u32x4_t graw[NLC];
-#pragma unroll
-      for (int kc = 0; kc < NKC; ++kc) raw[kc] = *reinterpret_cast<const u32x4_t*>(row + kc * 32);
-#pragma unroll
-      for (int kc = 0; kc < NLC; ++kc) graw[kc] = *reinterpret_cast<const u32x4_t*>(grow + kc * 32);
-
-      f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-      const int pos = ct_pos(hf, r16);
-#pragma unroll
-      for (int kc = 0; kc < NKC; ++kc) {
-        if (kc < NLC) {
-          // gate in fp32 (exact product), split into bf16 hi + lo
-          uint32_t pk[4], pl[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float p0 = bf16_lo(raw[kc][e]) * bf16_lo(graw[kc][e]);
-            const float p1 = bf16_hi(raw[kc][e]) * bf16_hi(graw[kc][e]);
-            pk[e] = pack_bf16x2(p0, p1);
-            pl[e] = pack_bf16x2(p0 - bf16_lo(pk[e]), p1 - bf16_hi(pk[e]));
-          }
-          const u32x4_t hv = {pk[0], pk[1], pk[2], pk[3]};
-          const u32x4_t lv = {pl[0], pl[1], pl[2], pl[3]};
-          const bf16x8_t ahi = __builtin_bit_cast(bf16x8_t, hv);
-          const bf16x8_t alo = __builtin_bit_cast(bf16x8_t, lv);
-          // transposed copy (hi part) for the value product: ct[dim][pos]
-          uint16_t* col = ct + (kc * 32 + g * 8) * CTS + pos;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            col[(2 * e) * CTS] = static_cast<uint16_t>(pk[e] & 0xffffu);
-            col[(2 * e + 1) * CTS] = static_cast<uint16_t>(pk[e] >> 16);
-          }
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, qb[kc], acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, qb[kc], acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, qlo[kc], acc, 0, 0, 0);
-        } else {
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, raw[kc]), qb[kc], acc, 0,
-                                                        0, 0);
-        }
-      }
-      sacc[hf] = acc;
-    }
-
-    // online softmax: lane holds head r16, tokens hf*16 + 4g + r
-    float sv[8];
-    float mt = -INFINITY;
-#pragma unroll
-    for (int hf = 0; hf < 2; ++hf) {
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int tk = hf * 16 + 4 * g + r;
-        const float x = tk < nt ? sacc[hf][r] * a.scale_log2 : -INFINITY;
-        sv[hf * 4 + r] = x;
-        mt = fmaxf(mt, x);
-      }
-    }
-    mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
-    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-    const float m_new = fmaxf(m_run, mt);
-    const float alpha = exp2f(m_run - m_new);
-    m_run = m_new;
-    float psum = 0.f;
-    bf16x8_t pb;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const float p = exp2f(sv[i] - m_new);
-      psum += p;
-      pb[i] = static_cast<__bf16>(p);
-    }
-    l_run = l_run * alpha + psum;
-#pragma unroll
-    for (int i = 0; i < NDB; ++i) o[i] *= alpha;
-
-    wave_lds_sync();
-#pragma unroll
-    for (int db = 0; db < NDB; ++db) {
-      const bf16x8_t av = *reinterpret_cast<const bf16x8_t*>(ct + (db * 16 + r16) * CTS + g * 8);
-      o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, pb, o[db], 0, 0, 0);
-    }
-    wave_lds_sync();
-  }
-
-  // ---- merge the NW waves of this work-group (fixed order) ----
-  l_run += __shfl_xor(l_run, 16, 64);
-  l_run += __shfl_xor(l_run, 32, 64);
-  __syncthreads();  // all waves done with their ct regions
-  float* mo = reinterpret_cast<float*>(lds);  // [NW][16][DC]
-  float* ml = mo + NW * 16 * DC;              // [NW][16][2]
-  if (g == 0) {
-    ml[(w * 16 + r16) * 2 + 0] = m_run;
-    ml[(w * 16 + r16) * 2 + 1] = l_run;
-  }
-  __syncthreads();
-  float M = -INFINITY;
-#pragma unroll
-  for (int v = 0; v < NW; ++v) M = fmaxf(M, ml[(v * 16 + r16) * 2]);
-  const float f = exp2f(m_run - M);  // 0 for a wave that saw no tile
-#pragma unroll
-  for (int db = 0; db < NDB; ++db) {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) mo[(w * 16 + r16) * DC + db * 16 + 4 * g + r] = o[db][r] * f;
-  }
-  __syncthreads();
-  const int64_t pbase = (static_cast<int64_t>(b) * a.s_max + s) * a.H + hg * 16;
-  for (int i = tid; i < 16 * DC; i += NW * 64) {
-    float sum = 0.f;
-#pragma unroll
-    for (int v = 0; v < NW; ++v) sum += mo[v * 16 * DC + i];
-    a.part_o[pbase * DC + i] = sum;
-  }
-  if (tid < 16) {
-    float Mh = -INFINITY;
-#pragma unroll
-    for (int v = 0; v < NW; ++v) Mh = fmaxf(Mh, ml[(v * 16 + tid) * 2]);
-    float Lh = 0.f;
-#pragma unroll
-    for (int v = 0; v < NW; ++v) {
-      const float mv = ml[(v * 16 + tid) * 2];
-      Lh += ml[(v * 16 + tid) * 2 + 1] * (mv == -INFINITY ? 0.f : exp2f(mv - Mh));
-    }
-    a.part_ml[(pbase + tid) * 2 + 0] = Mh;
-    a.part_ml[(pbase + tid) * 2 + 1] = Lh;
-  }
-}
+}  // namespace egmla
+#include "split_mfma.h"
+namespace egmla {
 
 // ---------------------------------------------------------------------------
 // 3. combine: merge the splits of (b, h) and apply W_UV[h].
@@ -491,6 +287,10 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
   }
 }
 
+}  // namespace egmla
+#include "aux_mfma.h"
+namespace egmla {
+
 // ---------------------------------------------------------------------------
 // host launch helpers
 // ---------------------------------------------------------------------------
@@ -505,7 +305,7 @@ hipError_t set_lds(K kernel, size_t bytes) {
 
 template <int DC, int DR>
 hipError_t launch_mfma(const SplitArgs& a, int nblocks, hipStream_t stream) {
-  hipLaunchKernelGGL((split_mfma_kernel<DC, DR>), dim3(nblocks), dim3(MfmaCfg<DC>::NW * 64), 0, stream, a);
+  hipLaunchKernelGGL((split_mfma_kernel<DC, DR>), dim3(nblocks), dim3(DsplitCfg<DC, DR>::NW * 64), 0, stream, a);
   return hipGetLastError();
 }
 
@@ -563,14 +363,21 @@ extern "C" eg_mla_status eg_mla_decode_planned(const eg_mla_dims* dims, int32_t 
 
   // 1. absorption
   {
-    dim3 grid(d.num_heads, (batch + kAbsorbRows - 1) / kAbsorbRows);
-    const size_t lds = sizeof(float) * kAbsorbRows * d.head_dim;
-    if (bf)
+    dim3 grid(d.num_heads, (d.latent_dim + kAbsorbCols - 1) / kAbsorbCols, (batch + kAbsorbRows - 1) / kAbsorbRows);
+    const size_t lds = sizeof(float) * (kAbsorbRows * d.head_dim + 4 * kAbsorbRows * kAbsorbCols);
+    if (bf && d.head_dim == 128) {
+      dim3 ga(d.num_heads, (batch + kAbsRows - 1) / kAbsRows, (d.latent_dim + kAbsCols - 1) / kAbsCols);
+      hipLaunchKernelGGL(absorb_mfma_kernel<128>, ga, dim3(256), 0, stream, static_cast<const uint16_t*>(q),
+                         static_cast<const uint16_t*>(w_uk), qfull, batch, d.num_heads, d.latent_dim, d.rope_dim);
+    } else if (bf) {
+      if (set_lds(absorb_kernel<true>, lds) != hipSuccess) return EG_MLA_ERR_HIP;
       hipLaunchKernelGGL(absorb_kernel<true>, grid, dim3(256), lds, stream, q, w_uk, qfull, batch, d.num_heads,
                          d.head_dim, d.latent_dim, d.rope_dim);
-    else
+    } else {
+      if (set_lds(absorb_kernel<false>, lds) != hipSuccess) return EG_MLA_ERR_HIP;
       hipLaunchKernelGGL(absorb_kernel<false>, grid, dim3(256), lds, stream, q, w_uk, qfull, batch, d.num_heads,
                          d.head_dim, d.latent_dim, d.rope_dim);
+    }
     if (hipGetLastError() != hipSuccess) return EG_MLA_ERR_HIP;
   }
   // 2. split kernel (skipped when the cache has no capacity: every length clamps to 0)
@@ -609,7 +416,24 @@ extern "C" eg_mla_status eg_mla_decode_planned(const eg_mla_dims* dims, int32_t 
     dim3 grid(d.num_heads, batch);
     const size_t lds = sizeof(float) * (d.latent_dim + p.s_max);
     if (lds > 160 * 1024) return EG_MLA_ERR_UNSUPPORTED;
-    if (bf) {
+    const bool mfma_comb = bf && d.v_head_dim == 128 &&
+                           (d.latent_dim == 128 || d.latent_dim == 320 || d.latent_dim == 512);
+    if (mfma_comb) {
+      dim3 g2(d.num_heads, (batch + kCombSeq - 1) / kCombSeq);
+      const float* pm = part_ml;
+      const float* po = part_o;
+      const uint16_t* wv = static_cast<const uint16_t*>(w_uv);
+      uint16_t* ov = static_cast<uint16_t*>(out);
+      if (d.latent_dim == 128)
+        hipLaunchKernelGGL((combine_mfma_kernel<128, 128>), g2, dim3(256), 0, stream, pm, po, wv, seq_lens, ov, batch,
+                           d.num_heads, p.capacity, p.split_tokens, p.s_max);
+      else if (d.latent_dim == 320)
+        hipLaunchKernelGGL((combine_mfma_kernel<320, 128>), g2, dim3(256), 0, stream, pm, po, wv, seq_lens, ov, batch,
+                           d.num_heads, p.capacity, p.split_tokens, p.s_max);
+      else
+        hipLaunchKernelGGL((combine_mfma_kernel<512, 128>), g2, dim3(256), 0, stream, pm, po, wv, seq_lens, ov, batch,
+                           d.num_heads, p.capacity, p.split_tokens, p.s_max);
+    } else if (bf) {
       if (set_lds(combine_kernel<true>, lds) != hipSuccess) return EG_MLA_ERR_HIP;
       hipLaunchKernelGGL(combine_kernel<true>, grid, dim3(256), lds, stream, part_ml, part_o, w_uv, seq_lens, out,
                          d.num_heads, d.latent_dim, d.v_head_dim, p.capacity, p.split_tokens, p.s_max);

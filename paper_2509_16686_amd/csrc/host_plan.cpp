@@ -9,7 +9,6 @@ namespace {
 constexpr int kMaxRowDim = 640;     // d_c + d_r handled by the VALU kernel's LDS tile
 constexpr int kMaxHeadDim = 1024;   // d_h and d_v
 constexpr int kTargetWorkItems = 1024;
-constexpr int kMaxSplitTokens = 2048;
 
 int ceil_div(int64_t a, int64_t b) { return static_cast<int>((a + b - 1) / b); }
 bool aligned16(const void* p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; }
@@ -63,6 +62,7 @@ eg_mla_status make_decode_plan(const eg_mla_dims& d, int32_t batch, int32_t max_
 
   int split = plan ? plan->split_tokens : 0;
   if (split < 0 || split % kTile != 0) return EG_MLA_ERR_INVALID_ARG;
+  if (p.path == EG_MLA_PATH_MFMA && split > kMaxSplitTokens) return EG_MLA_ERR_UNSUPPORTED;
   if (split == 0) {
     const int64_t work = static_cast<int64_t>(std::max(batch, 1)) * std::max(p.capacity, 1) * p.head_groups;
     int64_t s = (work + kTargetWorkItems - 1) / kTargetWorkItems;
@@ -99,6 +99,7 @@ eg_mla_status validate_decode(const eg_mla_dims* d, int32_t batch, const void* q
   eg_mla_status st = check_dims(d);
   if (st != EG_MLA_OK) return st;
   if (batch < 0 || max_pages_per_seq < 0 || num_slots < 0) return EG_MLA_ERR_INVALID_ARG;
+  if (num_slots >= (int64_t{1} << 31)) return EG_MLA_ERR_UNSUPPORTED;  // 32-bit row indices in the kernels
   st = make_decode_plan(*d, batch, max_pages_per_seq, plan, p);
   if (st != EG_MLA_OK) return st;
   if (batch == 0) return EG_MLA_OK;

@@ -15,6 +15,11 @@ inline size_t align_up(size_t x, size_t a = kAlign) { return (x + a - 1) / a * a
 // Token-tile granularity of every decode kernel.
 constexpr int kTile = 32;
 
+// Largest split-K work item (tokens); the MFMA kernel stages the slot and id
+// of every token of its split in LDS.
+constexpr int kMaxSplitTokens = 2048;
+constexpr int kMaxSplitTokensDevice = kMaxSplitTokens;
+
 // MFMA kernel instantiations: (latent_dim, rope_dim) pairs with a compiled fast path.
 bool mfma_shape_supported(const eg_mla_dims& d);
 
