@@ -224,6 +224,7 @@ __global__ __launch_bounds__(kValuThreads) void split_valu_kernel(SplitArgs a) {
 // ---------------------------------------------------------------------------
 }  // namespace egmla
 #include "split_mfma.h"
+#include "split_tok.h"
 namespace egmla {
 
 // ---------------------------------------------------------------------------
@@ -303,6 +304,17 @@ hipError_t set_lds(K kernel, size_t bytes) {
                              static_cast<int>(bytes));
 }
 
+// Token-split kernel: waves per work-group and units in flight per wave.
+constexpr int kTokWaves = 4;
+constexpr int kTokDepth = 3;
+
+template <int DC, int DR>
+hipError_t launch_tok(const SplitArgs& a, int nblocks, hipStream_t stream) {
+  hipLaunchKernelGGL((split_tok_kernel<DC, DR, kTokWaves, kTokDepth>), dim3(nblocks), dim3(kTokWaves * 64), 0, stream,
+                     a);
+  return hipGetLastError();
+}
+
 template <int DC, int DR>
 hipError_t launch_mfma(const SplitArgs& a, int nblocks, hipStream_t stream) {
   hipLaunchKernelGGL((split_mfma_kernel<DC, DR>), dim3(nblocks), dim3(DsplitCfg<DC, DR>::NW * 64), 0, stream, a);
@@ -314,7 +326,7 @@ hipError_t launch_split(const eg_mla_dims& d, const DecodePlan& p, const SplitAr
   if (nblocks64 > 0x7fffffff) return hipErrorInvalidValue;
   const int nblocks = static_cast<int>(nblocks64);
   if (p.path == EG_MLA_PATH_MFMA) {
-    if (d.latent_dim == 128) return launch_mfma<128, 64>(a, nblocks, stream);
+    if (tok_kernel_shape(d)) return launch_tok<128, 64>(a, nblocks, stream);
     if (d.latent_dim == 320) return launch_mfma<320, 64>(a, nblocks, stream);
     if (d.latent_dim == 512) return launch_mfma<512, 64>(a, nblocks, stream);
     return hipErrorInvalidValue;

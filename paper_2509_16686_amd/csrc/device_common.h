@@ -10,6 +10,7 @@ typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
 typedef __attribute__((ext_vector_type(4))) float f32x4_t;
 typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
 typedef __attribute__((ext_vector_type(2))) uint32_t u32x2_t;
+typedef __attribute__((ext_vector_type(4))) short s16x4_t;  // operand of the 16x16x16 bf16 MFMA
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -20,8 +21,59 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
   __bf16 h = static_cast<__bf16>(f);
   return __builtin_bit_cast(uint16_t, h);
 }
+// Gated latent of one 16-byte chunk: word e of the result packs
+// bf16(lat.lo * gate.lo) and bf16(lat.hi * gate.hi) of word e.  Each product is
+// v_dot2_f32_bf16 of the latent word with the gate word's other half zeroed: a
+// product of two bf16 values fits fp32 exactly, and adding the zero product
+// and the zero accumulator is exact; v_cvt_pk_bf16_f32 then rounds once.  The
+// sequence is one asm block because the compiler's hazard checks cannot see
+// into it: a value written by a DOT instruction must not be read by another
+// VALU instruction for 3 wait states, so all eight products come first and the
+// last conversion, 3 instructions after the last product, gets 2 more; and a
+// VALU result must not feed an MFMA operand for 2 wait states, so the block
+// ends with 2 (each s_nop 1).
+__device__ __forceinline__ u32x4_t gate_chunk(u32x4_t lat, u32x4_t gate) {
+  u32x4_t out;
+  float t0, t1, t2, t3, t4, t5, t6, t7;
+  asm("v_dot2_f32_bf16 %[t0], %[a0], %[l0], 0\n\t"
+      "v_dot2_f32_bf16 %[t1], %[a0], %[h0], 0\n\t"
+      "v_dot2_f32_bf16 %[t2], %[a1], %[l1], 0\n\t"
+      "v_dot2_f32_bf16 %[t3], %[a1], %[h1], 0\n\t"
+      "v_dot2_f32_bf16 %[t4], %[a2], %[l2], 0\n\t"
+      "v_dot2_f32_bf16 %[t5], %[a2], %[h2], 0\n\t"
+      "v_dot2_f32_bf16 %[t6], %[a3], %[l3], 0\n\t"
+      "v_dot2_f32_bf16 %[t7], %[a3], %[h3], 0\n\t"
+      "v_cvt_pk_bf16_f32 %[o0], %[t0], %[t1]\n\t"
+      "v_cvt_pk_bf16_f32 %[o1], %[t2], %[t3]\n\t"
+      "v_cvt_pk_bf16_f32 %[o2], %[t4], %[t5]\n\t"
+      "s_nop 1\n\t"
+      "v_cvt_pk_bf16_f32 %[o3], %[t6], %[t7]\n\t"
+      "s_nop 1"
+      : [o0] "=&v"(out[0]), [o1] "=&v"(out[1]), [o2] "=&v"(out[2]), [o3] "=&v"(out[3]), [t0] "=&v"(t0),
+        [t1] "=&v"(t1), [t2] "=&v"(t2), [t3] "=&v"(t3), [t4] "=&v"(t4), [t5] "=&v"(t5), [t6] "=&v"(t6),
+        [t7] "=&v"(t7)
+      : [a0] "v"(lat[0]), [a1] "v"(lat[1]), [a2] "v"(lat[2]), [a3] "v"(lat[3]), [l0] "v"(gate[0] & 0xffffu),
+        [l1] "v"(gate[1] & 0xffffu), [l2] "v"(gate[2] & 0xffffu), [l3] "v"(gate[3] & 0xffffu),
+        [h0] "v"(gate[0] & 0xffff0000u), [h1] "v"(gate[1] & 0xffff0000u), [h2] "v"(gate[2] & 0xffff0000u),
+        [h3] "v"(gate[3] & 0xffff0000u));
+  return out;
+}
+
+// Maximum over the four lanes i, i ^ 16, i ^ 32, i ^ 48 (VALU lane swaps).
+__device__ __forceinline__ float max_over_row_groups(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const auto s32 = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  x = fmaxf(__uint_as_float(s32[0]), __uint_as_float(s32[1]));
+  const uint32_t v = __float_as_uint(x);
+  const auto s16 = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  return fmaxf(__uint_as_float(s16[0]), __uint_as_float(s16[1]));
+}
+
+// Two fp32 -> packed bf16 pair (lo in bits 0..15), one v_cvt_pk_bf16_f32.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
+  typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+  typedef __attribute__((ext_vector_type(2))) float f32x2_t;
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
 }
 
 // Storage-typed scalar access.

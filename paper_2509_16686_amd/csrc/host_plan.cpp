@@ -9,6 +9,9 @@ namespace {
 constexpr int kMaxRowDim = 640;     // d_c + d_r handled by the VALU kernel's LDS tile
 constexpr int kMaxHeadDim = 1024;   // d_h and d_v
 constexpr int kTargetWorkItems = 1024;
+// Token-split MFMA kernel: one 4-wave work-group per compute unit streams
+// longest without gaps between its loads (256 compute units).
+constexpr int kTargetWorkItemsTok = 256;
 
 int ceil_div(int64_t a, int64_t b) { return static_cast<int>((a + b - 1) / b); }
 bool aligned16(const void* p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; }
@@ -20,6 +23,8 @@ bool mfma_shape_supported(const eg_mla_dims& d) {
   if (d.rope_dim != 64) return false;
   return d.latent_dim == 128 || d.latent_dim == 320 || d.latent_dim == 512;
 }
+
+bool tok_kernel_shape(const eg_mla_dims& d) { return d.latent_dim == 128 && d.rope_dim == 64; }
 
 eg_mla_status check_dims(const eg_mla_dims* d) {
   if (!d) return EG_MLA_ERR_INVALID_ARG;
@@ -65,7 +70,8 @@ eg_mla_status make_decode_plan(const eg_mla_dims& d, int32_t batch, int32_t max_
   if (p.path == EG_MLA_PATH_MFMA && split > kMaxSplitTokens) return EG_MLA_ERR_UNSUPPORTED;
   if (split == 0) {
     const int64_t work = static_cast<int64_t>(std::max(batch, 1)) * std::max(p.capacity, 1) * p.head_groups;
-    int64_t s = (work + kTargetWorkItems - 1) / kTargetWorkItems;
+    const int64_t target = p.path == EG_MLA_PATH_MFMA && tok_kernel_shape(d) ? kTargetWorkItemsTok : kTargetWorkItems;
+    int64_t s = (work + target - 1) / target;
     s = (s + kTile - 1) / kTile * kTile;
     const int min_split = p.path == EG_MLA_PATH_MFMA ? 256 : 128;
     s = std::max<int64_t>(s, min_split);

@@ -22,6 +22,8 @@ constexpr int kMaxSplitTokensDevice = kMaxSplitTokens;
 
 // MFMA kernel instantiations: (latent_dim, rope_dim) pairs with a compiled fast path.
 bool mfma_shape_supported(const eg_mla_dims& d);
+// MFMA shapes served by the token-split kernel (the others by the dimension-split one).
+bool tok_kernel_shape(const eg_mla_dims& d);
 
 struct DecodePlan {
   int path = EG_MLA_PATH_VALU;  // resolved: VALU or MFMA

@@ -40,7 +40,7 @@ struct DsplitCfg {
   static constexpr int NRC = DR / 32;                  // RoPE chunks
   static constexpr int CPW = DC == 128 ? 1 : 2;        // latent chunks per wave
   static constexpr int NW = NLC / CPW;                 // waves per work-group
-  static constexpr int RPW = NRC > 0 ? 1 : 0;          // RoPE chunk slots per wave (waves < NRC use them)
+  static constexpr int RPW = NRC > 0 ? 1 : 0;          // RoPE chunk slots per wave (waves < NRC own theirs)
   static constexpr int NDB = CPW * 2;                  // 16-dim blocks of the value product per wave
   static constexpr int kDepth = DC == 128 ? 4 : 3;     // tiles in flight per wave
   static constexpr int CT_STRIDE = 40;                 // 32 token slots + 8 pad (bf16 elements)
@@ -86,8 +86,12 @@ __global__ __launch_bounds__((DsplitCfg<DC, DR>::NW * 64)) void split_mfma_kerne
   const int n = t1 - t0;
   const int ntiles = (n + kTile - 1) / kTile;
 
-  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
+  const int tid = threadIdx.x, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const bool has_rope = RPW > 0 && w < Cfg::NRC;
+  // RoPE chunk this wave loads: its own, else a duplicate of another wave's
+  // (against a zero query), so the loads never depend on a branch.
+  const int rope_chunk = Cfg::NRC > 0 ? w % (Cfg::NRC > 0 ? Cfg::NRC : 1) : 0;
 
   // ---- (1) resolve slots and ids of the split; (2) query chunks of this wave ----
   for (int j = tid; j < n; j += NW * 64) {
@@ -95,8 +99,8 @@ __global__ __launch_bounds__((DsplitCfg<DC, DR>::NW * 64)) void split_mfma_kerne
     tok_slot[j] = sl;
     tok_id[j] = clamp_id(a.ids[sl], a.V);
   }
-  // Waves without a RoPE chunk keep zero RoPE operands and still issue the
-  // (then zero) RoPE product, so no MFMA depends on a branch.
+  // Waves without a RoPE chunk of their own use a zero RoPE query, so their
+  // (duplicate) RoPE product adds exactly zero and nothing depends on a branch.
   bf16x8_t qh[CPW], ql[CPW];
   bf16x8_t qr = {};
   {
@@ -113,13 +117,13 @@ __global__ __launch_bounds__((DsplitCfg<DC, DR>::NW * 64)) void split_mfma_kerne
         ql[c][e] = static_cast<__bf16>(x[e] - static_cast<float>(qh[c][e]));
       }
     }
-    if (has_rope) {
-      const float* p = qrow + DC + w * 32;
+    if constexpr (RPW > 0) {
+      const float* p = qrow + DC + rope_chunk * 32;
       const float4 x0 = *reinterpret_cast<const float4*>(p);
       const float4 x1 = *reinterpret_cast<const float4*>(p + 4);
       const float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
 #pragma unroll
-      for (int e = 0; e < 8; ++e) qr[e] = static_cast<__bf16>(x[e]);  // q^R is a stored bf16 value: exact
+      for (int e = 0; e < 8; ++e) qr[e] = static_cast<__bf16>(has_rope ? x[e] : 0.f);  // q^R is bf16: exact
     }
   }
   __syncthreads();
@@ -141,19 +145,20 @@ __global__ __launch_bounds__((DsplitCfg<DC, DR>::NW * 64)) void split_mfma_kerne
         r.gat[hf][c] = *reinterpret_cast<const u32x4_t*>(grow + (w * CPW + c) * 32);
         r.lat[hf][c] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(row + (w * CPW + c) * 32));
       }
-      if constexpr (RPW > 0) {
-        if (has_rope)
-          r.rop[hf][0] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(row + DC + w * 32));
-      }
+      if constexpr (RPW > 0)
+        r.rop[hf][0] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(row + DC + rope_chunk * 32));
     }
   };
 
+  // Every load is unconditional (indexes past the split repeat its last
+  // token), so the compiler's wait counters track each tile exactly and D
+  // tiles stay in flight; a branch around a load would make it wait for all.
+  // Loads return in issue order, so tile k must also be issued before tile k + 1.
   TileRegs<CPW, RPW> ring[D];
 #pragma unroll
   for (int k = 0; k < D; ++k) {
-#pragma unroll
-    for (int hf = 0; hf < 2; ++hf) ring[k].rop[hf][0] = u32x4_t{0u, 0u, 0u, 0u};
-    if (k < ntiles) issue(ring[k], k);
+    issue(ring[k], k);
+    __builtin_amdgcn_sched_barrier(0);
   }
 
   f32x4_t o[NDB];
@@ -163,13 +168,18 @@ __global__ __launch_bounds__((DsplitCfg<DC, DR>::NW * 64)) void split_mfma_kerne
   float l_run = 0.f;        // this lane's share of the running sum
   uint16_t* ct = ct_all + w * CPW * 32 * CTS;  // this wave's [CPW*32 dims][CTS]
 
-  for (int k0 = 0; k0 < ntiles; k0 += D) {
+  // Tiles run in groups of D; those past the split are fully masked (their
+  // probabilities are exactly 0 and the running max is unchanged).
+  const int ngroups = (ntiles + D - 1) / D;
+  for (int k0 = 0; k0 < ngroups * D; k0 += D) {
 #pragma unroll
     for (int u = 0; u < D; ++u) {
+      // Keep tiles in source order: hoisting a later tile's products above
+      // this point would make the wave wait for that tile's loads too.
+      __builtin_amdgcn_sched_barrier(0);
       const int k = k0 + u;
-      if (k >= ntiles) break;
       TileRegs<CPW, RPW>& r = ring[u];
-      const int nt = min(kTile, n - k * kTile);
+      const int nt = n - k * kTile;  // valid tokens of the tile (may be <= 0)
 
       // partial scores over this wave's dims
       f32x4_t sp[2];
@@ -202,7 +212,7 @@ __global__ __launch_bounds__((DsplitCfg<DC, DR>::NW * 64)) void split_mfma_kerne
         sp[hf] = acc;
       }
       // this tile's registers are free: issue tile k + D into them
-      if (k + D < ntiles) issue(r, k + D);
+      issue(r, k + D);
 
       // sum the partial scores of all waves
       float* sb = sbuf + ((k & 1) * NW) * 64 * 8;
