@@ -207,7 +207,8 @@ def main():
 
     # (1) whole-call throughput: plain back-to-back calls, nothing between them
     total_ms, wall = timed_loop(step_args)
-    # (2) the split kernel alone: the same calls with HIP events around every split-kernel launch
+    # (2) the split kernel alone: the same calls with a start/stop event pair per split-kernel
+    #     launch, stamped by the dispatch itself (hipExtLaunchKernelGGL), on the kernel's stream
     timed_loop(timed_args)
     kernel_ms = [hip.elapsed_ms(ev0[k], ev1[k]) for k in range(K)]
 

@@ -84,9 +84,11 @@ typedef enum eg_mla_path {
 typedef struct eg_mla_plan {
   int32_t path;          /* eg_mla_path */
   int32_t split_tokens;  /* tokens per split-K work item, multiple of 32; 0 = automatic */
-  /* Optional hipEvent_t handles (NULL = none), recorded on the call's stream
-   * immediately before and after the token-streaming split kernel, so a
-   * caller can time that kernel alone with hipEventElapsedTime. */
+  /* Optional hipEvent_t handles (NULL = none) that time the token-streaming
+   * split kernel alone with hipEventElapsedTime.  On the MFMA path they are
+   * passed to hipExtLaunchKernelGGL and stamped by the dispatch itself (kernel
+   * start and end); on the VALU path they are recorded on the call's stream
+   * immediately before and after the kernel. */
   void* split_start_event;
   void* split_stop_event;
 } eg_mla_plan;

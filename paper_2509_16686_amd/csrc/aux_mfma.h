@@ -9,10 +9,11 @@ namespace egmla {
 // Absorption on MFMA: qfull[b, h, c] = sum_k q^C[b, h, k] W_UK[h, k, c] for
 // 16 sequences x 128 latent columns per work-group (grid H x ceil(B/16) x
 // ceil(DC/128), 256 threads), plus the q^R copy.  W_UK[h][:, c-block] is
-// loaded with 16-byte row loads and stored transposed in LDS, so the B
-// operand (8 consecutive k of one column) is one 16-byte LDS read; the A
-// operand (8 consecutive k of one query row) comes straight from global.
-// bf16 x bf16 products are exact in fp32 and accumulate in fp32.
+// loaded with 16-byte row loads and stored row-major in LDS; the B operand
+// (8 consecutive k of one column) is two ds_read_b64_tr_b16, whose 16-lane
+// transpose hands lane n the column n of 4 consecutive rows.  The A operand
+// (8 consecutive k of one query row) comes straight from global.  bf16 x bf16
+// products are exact in fp32 and accumulate in fp32.
 // ---------------------------------------------------------------------------
 constexpr int kAbsRows = 16;
 constexpr int kAbsCols = 128;
@@ -21,9 +22,9 @@ template <int DH>
 __global__ __launch_bounds__(256) void absorb_mfma_kernel(const uint16_t* __restrict__ q,
                                                           const uint16_t* __restrict__ w_uk,
                                                           float* __restrict__ qfull, int B, int H, int DC, int DR) {
-  constexpr int KS = DH + 8;  // padded row of the transposed tile (bf16 elements)
+  constexpr int RS = kAbsCols + 8;  // padded LDS row (bf16 elements)
   constexpr int NK = DH / 32;
-  __shared__ __attribute__((aligned(16))) uint16_t wt[kAbsCols * KS];  // [c][k]
+  __shared__ __attribute__((aligned(16))) uint16_t wrm[DH * RS];  // [k][c], row-major
   const int h = blockIdx.x;
   const int b0 = blockIdx.y * kAbsRows;
   const int c0 = blockIdx.z * kAbsCols;
@@ -48,25 +49,38 @@ __global__ __launch_bounds__(256) void absorb_mfma_kernel(const uint16_t* __rest
 #pragma unroll
   for (int ks = 0; ks < NK; ++ks)
     qa[ks] = *reinterpret_cast<const u32x4_t*>(q + (static_cast<int64_t>(bq) * H + h) * DQin + ks * 32 + g * 8);
-  // (2) transpose W into LDS
+  // RoPE part of the query rows (copied as fp32): when d_r is a multiple of 4
+  // and at most 64, thread t loads 4 consecutive values of row t / (d_r / 4)
+  // (one 8-byte load, index clamped so the load is unconditional); other
+  // shapes copy element by element after the product.
+  const bool rope_vec = blockIdx.z == 0 && DR > 0 && DR % 4 == 0 && DR <= 64;
+  const int rq_row = rope_vec ? tid / (DR / 4) : 0;
+  const int rq_col = rope_vec ? 4 * (tid % (DR / 4)) : 0;
+  const bool rq_ok = rope_vec && rq_row < kAbsRows && b0 + rq_row < B;
+  const int rq_b = min(b0 + min(rq_row, kAbsRows - 1), B - 1);
+  const uint2 rq = rope_vec ? *reinterpret_cast<const uint2*>(q + (static_cast<int64_t>(rq_b) * H + h) * DQin + DH + rq_col)
+                            : make_uint2(0u, 0u);
+  // (2) W rows into LDS as loaded (columns past DC hold unused values)
 #pragma unroll
   for (int p = 0; p < kPasses; ++p) {
     const int k = p * kRowsPerPass + tid / (kAbsCols / 8);
-    if (k < DH) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        wt[(cc + 2 * e) * KS + k] = static_cast<uint16_t>(wv[p][e] & 0xffffu);
-        wt[(cc + 2 * e + 1) * KS + k] = static_cast<uint16_t>(wv[p][e] >> 16);
-      }
-    }
+    if (k < DH) *reinterpret_cast<u32x4_t*>(wrm + k * RS + cc) = wv[p];
   }
   __syncthreads();
-  // (3) wave w computes column tiles w, w+4 (16 columns each)
+  // (3) wave w computes column tiles w, w+4 (16 columns each).  For rows
+  // k0 .. k0 + 3 of the tile, lane r16 of group g reads columns
+  // 4 (r16 % 4) .. + 3 of row k0 + r16 / 4; the transposed read hands lane r16
+  // column r16 of the 4 rows.
   for (int nt = w; nt * 16 < nc; nt += 4) {
     f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < NK; ++ks) {
-      const bf16x8_t bv = *reinterpret_cast<const bf16x8_t*>(wt + (nt * 16 + r16) * KS + ks * 32 + g * 8);
+      uint16_t* t0 = wrm + (ks * 32 + 8 * g + (r16 >> 2)) * RS + nt * 16 + 4 * (r16 & 3);
+      const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t*)t0);
+      const s16x4_t hi =
+          __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t*)(t0 + 4 * RS));
+      const u32x2_t l2 = __builtin_bit_cast(u32x2_t, lo), h2 = __builtin_bit_cast(u32x2_t, hi);
+      const bf16x8_t bv = __builtin_bit_cast(bf16x8_t, u32x4_t{l2[0], l2[1], h2[0], h2[1]});
       acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, qa[ks]), bv, acc, 0, 0, 0);
     }
     // lane holds D[b = 4g + r][c = nt*16 + r16]
@@ -77,7 +91,10 @@ __global__ __launch_bounds__(256) void absorb_mfma_kernel(const uint16_t* __rest
       if (b < B && c < DC) qfull[(static_cast<int64_t>(b) * H + h) * DQ + c] = acc[r];
     }
   }
-  if (blockIdx.z == 0) {
+  if (rq_ok) {
+    *reinterpret_cast<float4*>(qfull + (static_cast<int64_t>(b0 + rq_row) * H + h) * DQ + DC + rq_col) =
+        make_float4(bf16_lo(rq.x), bf16_hi(rq.x), bf16_lo(rq.y), bf16_hi(rq.y));
+  } else if (blockIdx.z == 0 && !rope_vec) {
     for (int i = tid; i < kAbsRows * DR; i += 256) {
       const int bb = i / DR, r = i % DR;
       if (b0 + bb < B)
@@ -90,8 +107,8 @@ __global__ __launch_bounds__(256) void absorb_mfma_kernel(const uint16_t* __rest
 // ---------------------------------------------------------------------------
 // Combine on MFMA: grid (H, ceil(B / 4)), 256 threads.  Wave w merges the
 // splits of sequence b0 + w for head h into LDS (fp32, divided by the softmax
-// sum): the split weights come from one load per split, then every partial
-// value of the wave is loaded in one batch.  Then out^T[v][b] =
+// sum), online over batches of 16 splits whose maxima, sums and partial
+// outputs are loaded together.  Then out^T[v][b] =
 // W_UV[h][v][:] . o[b][:] runs on v_mfma_f32_16x16x32_bf16 with W_UV rows as
 // the A operand (16-byte loads, all issued before the first product) and o
 // split into bf16 hi + lo as the B operand (4 of its 16 columns used).
@@ -107,7 +124,7 @@ __global__ __launch_bounds__(256) void combine_mfma_kernel(const float* __restri
                                                            int split, int s_max) {
   constexpr int OS = DC + 4;
   constexpr int PER = DC / 64;  // latent columns per lane
-  constexpr int SB = 8;         // splits per load batch
+  constexpr int SB = 16;        // splits per load batch
   constexpr int NKC = DC / 32;
   __shared__ __attribute__((aligned(16))) float o_s[16 * OS];  // rows 4..15 stay zero
   const int h = blockIdx.x;
@@ -138,15 +155,16 @@ __global__ __launch_bounds__(256) void combine_mfma_kernel(const float* __restri
 #pragma unroll
       for (int j = 0; j < PER; ++j) orow[lane + 64 * j] = 0.f;
     } else {
+      // Online merge of the splits in batches of SB: each batch loads its
+      // maxima, sums and partial outputs together, so a sequence with up to SB
+      // splits costs one round trip.  Every split below ns holds a token, so
+      // its maximum is finite.
       const int ns = min((L + split - 1) / split, s_max);
       const int64_t base = static_cast<int64_t>(b) * s_max * H + h;  // + s * H
-      float M = -INFINITY;
-      for (int sidx = lane; sidx < ns; sidx += 64) M = fmaxf(M, part_ml[(base + static_cast<int64_t>(sidx) * H) * 2]);
-      M = wave_max(M);
+      float M = -INFINITY, Ls = 0.f;
       float acc[PER];
 #pragma unroll
       for (int j = 0; j < PER; ++j) acc[j] = 0.f;
-      float Ls = 0.f;
       for (int s0 = 0; s0 < ns; s0 += SB) {
         float pv[SB][PER];
         float mv[SB], lv[SB];
@@ -159,13 +177,22 @@ __global__ __launch_bounds__(256) void combine_mfma_kernel(const float* __restri
 #pragma unroll
           for (int j = 0; j < PER; ++j) pv[u][j] = part_o[row * DC + lane + 64 * j];
         }
+        float mb = -INFINITY;
+#pragma unroll
+        for (int u = 0; u < SB; ++u) mb = fmaxf(mb, mv[u]);  // repeated last split: no effect on the max
+        const float Mn = fmaxf(M, mb);
+        const float sc = exp2f(M - Mn);  // 0 for the first batch
+        Ls *= sc;
+#pragma unroll
+        for (int j = 0; j < PER; ++j) acc[j] *= sc;
 #pragma unroll
         for (int u = 0; u < SB; ++u) {
-          const float e = s0 + u < ns ? exp2f(mv[u] - M) : 0.f;
+          const float e = s0 + u < ns ? exp2f(mv[u] - Mn) : 0.f;
           Ls += lv[u] * e;
 #pragma unroll
           for (int j = 0; j < PER; ++j) acc[j] = fmaf(e, pv[u][j], acc[j]);
         }
+        M = Mn;
       }
       const float inv = 1.f / Ls;
 #pragma unroll

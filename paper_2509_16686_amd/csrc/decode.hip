@@ -11,6 +11,7 @@
 //
 // The math is App. C Eq. (C.11)-(C.13) in absorbed form with the gate of
 // Sec. 3.1 Eq. (3)-(5) applied in the latent space (c~ = c * G[id]).
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cfloat>
@@ -308,29 +309,34 @@ hipError_t set_lds(K kernel, size_t bytes) {
 constexpr int kTokWaves = 4;
 constexpr int kTokDepth = 3;
 
+// The MFMA split kernels launch with hipExtLaunchKernelGGL so that optional
+// timing events are stamped by the dispatch itself (kernel start and end).
 template <int DC, int DR>
-hipError_t launch_tok(const SplitArgs& a, int nblocks, hipStream_t stream) {
-  hipLaunchKernelGGL((split_tok_kernel<DC, DR, kTokWaves, kTokDepth>), dim3(nblocks), dim3(kTokWaves * 64), 0, stream,
-                     a);
+hipError_t launch_tok(const SplitArgs& a, int nblocks, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
+  hipExtLaunchKernelGGL((split_tok_kernel<DC, DR, kTokWaves, kTokDepth>), dim3(nblocks), dim3(kTokWaves * 64), 0,
+                        stream, ev0, ev1, 0, a);
   return hipGetLastError();
 }
 
 template <int DC, int DR>
-hipError_t launch_mfma(const SplitArgs& a, int nblocks, hipStream_t stream) {
-  hipLaunchKernelGGL((split_mfma_kernel<DC, DR>), dim3(nblocks), dim3(DsplitCfg<DC, DR>::NW * 64), 0, stream, a);
+hipError_t launch_mfma(const SplitArgs& a, int nblocks, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
+  hipExtLaunchKernelGGL((split_mfma_kernel<DC, DR>), dim3(nblocks), dim3(DsplitCfg<DC, DR>::NW * 64), 0, stream, ev0,
+                        ev1, 0, a);
   return hipGetLastError();
 }
 
-hipError_t launch_split(const eg_mla_dims& d, const DecodePlan& p, const SplitArgs& a, hipStream_t stream) {
+hipError_t launch_split(const eg_mla_dims& d, const DecodePlan& p, const SplitArgs& a, hipStream_t stream,
+                        hipEvent_t ev0, hipEvent_t ev1) {
   const int64_t nblocks64 = static_cast<int64_t>(a.B) * a.s_max * a.groups;
   if (nblocks64 > 0x7fffffff) return hipErrorInvalidValue;
   const int nblocks = static_cast<int>(nblocks64);
   if (p.path == EG_MLA_PATH_MFMA) {
-    if (tok_kernel_shape(d)) return launch_tok<128, 64>(a, nblocks, stream);
-    if (d.latent_dim == 320) return launch_mfma<320, 64>(a, nblocks, stream);
-    if (d.latent_dim == 512) return launch_mfma<512, 64>(a, nblocks, stream);
+    if (tok_kernel_shape(d)) return launch_tok<128, 64>(a, nblocks, stream, ev0, ev1);
+    if (d.latent_dim == 320) return launch_mfma<320, 64>(a, nblocks, stream, ev0, ev1);
+    if (d.latent_dim == 512) return launch_mfma<512, 64>(a, nblocks, stream, ev0, ev1);
     return hipErrorInvalidValue;
   }
+  if (ev0 && hipEventRecord(ev0, stream) != hipSuccess) return hipErrorInvalidValue;
   const int DQ = d.latent_dim + d.rope_dim;
   size_t lds = sizeof(float) * (static_cast<size_t>(a.hpg) * DQ + kTile * (DQ + 1) + a.hpg * kTile + a.hpg + 1) +
                kTile * (sizeof(int64_t) + sizeof(int)) + 16;
@@ -343,7 +349,9 @@ hipError_t launch_split(const eg_mla_dims& d, const DecodePlan& p, const SplitAr
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(split_valu_kernel<false>, dim3(nblocks), dim3(kValuThreads), lds, stream, a);
   }
-  return hipGetLastError();
+  hipError_t e = hipGetLastError();
+  if (e == hipSuccess && ev1) e = hipEventRecord(ev1, stream);
+  return e;
 }
 
 }  // namespace
@@ -419,9 +427,7 @@ extern "C" eg_mla_status eg_mla_decode_planned(const eg_mla_dims* dims, int32_t 
     a.scale_log2 = softmax_scale(d) * kLog2e;
     hipEvent_t ev0 = plan ? static_cast<hipEvent_t>(plan->split_start_event) : nullptr;
     hipEvent_t ev1 = plan ? static_cast<hipEvent_t>(plan->split_stop_event) : nullptr;
-    if (ev0 && hipEventRecord(ev0, stream) != hipSuccess) return EG_MLA_ERR_HIP;
-    if (launch_split(d, p, a, stream) != hipSuccess) return EG_MLA_ERR_HIP;
-    if (ev1 && hipEventRecord(ev1, stream) != hipSuccess) return EG_MLA_ERR_HIP;
+    if (launch_split(d, p, a, stream, ev0, ev1) != hipSuccess) return EG_MLA_ERR_HIP;
   }
   // 3. combine + W_UV
   {
