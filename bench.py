@@ -29,7 +29,33 @@ sys.path.insert(0, ROOT)
 
 METRIC = "decode tokens/s + achieved HBM GB/s (% of peak) for eg_mla_decode, 1 GPU"
 HBM_PEAK_GBPS = 8000.0
+REPO = os.path.dirname(os.path.abspath(__file__))
+# Calibrated FETCH_SIZE + WRITE_SIZE counters of the split kernel on the default workload,
+# valid only while the kernel's sources hash to the recorded value.
+TRAFFIC_PROFILE = os.path.join(REPO, "profiles", "split_tok_b32_h16_dc128_dr64_l4096_traffic.md")
 
+
+
+def recorded_traffic():
+    """Bytes per split-kernel launch from the committed counter summary, or None when the
+    summary is missing or the kernel sources changed since the counters were taken."""
+    import hashlib
+    try:
+        fields = {}
+        for line in open(TRAFFIC_PROFILE):
+            if ":" in line and line.split(":", 1)[0] in ("traffic_bytes_per_launch", "kernel_sources",
+                                                        "kernel_sources_sha256"):
+                k, v = line.split(":", 1)
+                fields[k] = v.strip()
+        h = hashlib.sha256()
+        for rel in fields["kernel_sources"].split():
+            with open(os.path.join(REPO, rel), "rb") as f:
+                h.update(f.read())
+        if h.hexdigest() != fields["kernel_sources_sha256"]:
+            return None
+        return int(fields["traffic_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
@@ -216,6 +242,9 @@ def main():
     k_avg_ms = float(np.mean(kernel_ms))
     k_bytes = traffic.main_kernel
     achieved = k_bytes / (k_avg_ms * 1e-3) / 1e9
+    # counters were taken on the default workload with the automatic plan only
+    t_bytes = recorded_traffic() if (args.workload == 1 and args.path == "auto" and args.split == 0) else None
+    traffic_gbps = None if t_bytes is None else t_bytes / (k_avg_ms * 1e-3) / 1e9
     tokens_per_s = wl.batch / (ms_per_step * 1e-3)
     log(f"bench: {ms_per_step * 1e3:.2f} us/step, split kernel {k_avg_ms * 1e3:.2f} us "
         f"({achieved:.0f} GB/s, {100 * achieved / HBM_PEAK_GBPS:.1f}% of peak), host {host_per_call * 1e6:.1f} us/call, "
@@ -243,8 +272,8 @@ def main():
         "hbm_frac_call": traffic.total / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
         "roofline": {"bound": "hbm", "kernel": "split_mfma_kernel" if wl.dtype == "bf16" else "split_valu_kernel",
                      "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
-                     "algorithmic_bytes_per_launch": k_bytes, "kernel_us": k_avg_ms * 1e3},
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic_gbps,
+                     "algorithmic_bytes_per_launch": k_bytes, "traffic_bytes_per_launch": t_bytes, "kernel_us": k_avg_ms * 1e3},
     }
     if not args.no_cpu_baseline:
         log(f"bench: timing the fp64 oracle on the host for ~{args.cpu_seconds:.0f} s")
