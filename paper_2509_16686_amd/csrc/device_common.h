@@ -130,20 +130,27 @@ __device__ __forceinline__ int xcd_logical_block(int bid, int nblocks) {
   return xcd * per + min(xcd, rem) + local;
 }
 
+// Cache row of token j given its page-table entry, clamped into the cache.
+__device__ __forceinline__ int64_t paged_slot(int page, int j, int P, int64_t num_slots) {
+  const int64_t npages = num_slots / P;
+  page = page < 0 ? 0 : page;
+  int64_t s = (static_cast<int64_t>(page) < npages ? static_cast<int64_t>(page) : npages - 1) * P + j % P;
+  s = s < 0 ? 0 : s;
+  return s < num_slots ? s : num_slots - 1;
+}
+
+// Cache row of token j of sequence b in a contiguous cache, clamped into the cache.
+__device__ __forceinline__ int64_t contiguous_slot(int b, int j, int P, int max_pages, int64_t num_slots) {
+  int64_t s = static_cast<int64_t>(b) * max_pages * P + j;
+  s = s < 0 ? 0 : s;
+  return s < num_slots ? s : num_slots - 1;
+}
+
 // Cache row of token j of sequence b (paged or contiguous), clamped into the cache.
 __device__ __forceinline__ int64_t cache_slot(const int32_t* __restrict__ page_table, int b, int j, int P,
                                               int max_pages, int64_t num_slots) {
-  int64_t s;
-  if (page_table) {
-    int page = page_table[static_cast<int64_t>(b) * max_pages + j / P];
-    const int64_t npages = num_slots / P;
-    page = page < 0 ? 0 : page;
-    s = (static_cast<int64_t>(page) < npages ? static_cast<int64_t>(page) : npages - 1) * P + j % P;
-  } else {
-    s = static_cast<int64_t>(b) * max_pages * P + j;
-  }
-  s = s < 0 ? 0 : s;
-  return s < num_slots ? s : num_slots - 1;
+  if (page_table) return paged_slot(page_table[static_cast<int64_t>(b) * max_pages + j / P], j, P, num_slots);
+  return contiguous_slot(b, j, P, max_pages, num_slots);
 }
 
 __device__ __forceinline__ int clamp_id(int id, int V) { return id < 0 ? 0 : (id >= V ? V - 1 : id); }
