@@ -107,13 +107,67 @@ __global__ __launch_bounds__(256) void absorb_mfma_kernel(const uint16_t* __rest
 // ---------------------------------------------------------------------------
 // Combine on MFMA: grid (H, ceil(B / 4)), 256 threads.  Wave w merges the
 // splits of sequence b0 + w for head h into LDS (fp32, divided by the softmax
-// sum), online over batches of 16 splits whose maxima, sums and partial
+// sum), online over batches of 4 or 16 splits whose maxima, sums and partial
 // outputs are loaded together.  Then out^T[v][b] =
 // W_UV[h][v][:] . o[b][:] runs on v_mfma_f32_16x16x32_bf16 with W_UV rows as
 // the A operand (16-byte loads, all issued before the first product) and o
 // split into bf16 hi + lo as the B operand (4 of its 16 columns used).
 // ---------------------------------------------------------------------------
 constexpr int kCombSeq = 4;
+
+// Latent dim held in accumulator j of a combine lane: with an even number of
+// dims per lane, lane l holds the adjacent pairs 128 i + 2 l + {0, 1} (8-byte
+// loads); otherwise dims l + 64 j.
+template <int DC>
+__device__ __forceinline__ int comb_dim(int lane, int j) {
+  constexpr int PER = DC / 64;
+  if constexpr (PER % 2 == 0) return 128 * (j >> 1) + 2 * lane + (j & 1);
+  else return lane + 64 * j;
+}
+
+// One batch of SB splits of the online merge (s0 .. s0 + SB - 1, clamped to
+// ns - 1): maxima, sums and partial outputs load together.
+template <int DC, int SB>
+__device__ __forceinline__ void merge_batch(const float* __restrict__ part_ml, const float* __restrict__ part_o,
+                                            int64_t base, int H, int s0, int ns, int lane, float& M, float& Ls,
+                                            float (&acc)[DC / 64]) {
+  constexpr int PER = DC / 64;
+  float pv[SB][PER];
+  float2 ml[SB];
+#pragma unroll
+  for (int u = 0; u < SB; ++u) {
+    const int64_t row = base + static_cast<int64_t>(min(s0 + u, ns - 1)) * H;
+    ml[u] = *reinterpret_cast<const float2*>(part_ml + row * 2);
+    if constexpr (PER % 2 == 0) {
+#pragma unroll
+      for (int i = 0; i < PER / 2; ++i) {
+        const float2 v = *reinterpret_cast<const float2*>(part_o + row * DC + 128 * i + 2 * lane);
+        pv[u][2 * i] = v.x;
+        pv[u][2 * i + 1] = v.y;
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < PER; ++j) pv[u][j] = part_o[row * DC + lane + 64 * j];
+    }
+  }
+  float mb = -INFINITY;
+#pragma unroll
+  for (int u = 0; u < SB; ++u) mb = fmaxf(mb, ml[u].x);  // repeated last split: no effect on the max
+  const float Mn = fmaxf(M, mb);
+  const float sc = __builtin_amdgcn_exp2f(M - Mn);  // 0 for the first batch (exp2(-inf))
+  Ls *= sc;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) acc[j] *= sc;
+#pragma unroll
+  for (int u = 0; u < SB; ++u) {
+    const float e = s0 + u < ns ? __builtin_amdgcn_exp2f(ml[u].x - Mn) : 0.f;
+    Ls += ml[u].y * e;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) acc[j] = fmaf(e, pv[u][j], acc[j]);
+  }
+  M = Mn;
+}
+
 
 template <int DC, int DV>
 __global__ __launch_bounds__(256) void combine_mfma_kernel(const float* __restrict__ part_ml,
@@ -124,7 +178,6 @@ __global__ __launch_bounds__(256) void combine_mfma_kernel(const float* __restri
                                                            int split, int s_max) {
   constexpr int OS = DC + 4;
   constexpr int PER = DC / 64;  // latent columns per lane
-  constexpr int SB = 16;        // splits per load batch
   constexpr int NKC = DC / 32;
   __shared__ __attribute__((aligned(16))) float o_s[16 * OS];  // rows 4..15 stay zero
   const int h = blockIdx.x;
@@ -153,50 +206,26 @@ __global__ __launch_bounds__(256) void combine_mfma_kernel(const float* __restri
     float* orow = o_s + w * OS;
     if (L == 0) {
 #pragma unroll
-      for (int j = 0; j < PER; ++j) orow[lane + 64 * j] = 0.f;
+      for (int j = 0; j < PER; ++j) orow[comb_dim<DC>(lane, j)] = 0.f;
     } else {
-      // Online merge of the splits in batches of SB: each batch loads its
-      // maxima, sums and partial outputs together, so a sequence with up to SB
-      // splits costs one round trip.  Every split below ns holds a token, so
-      // its maximum is finite.
+      // Online merge of the splits in batches (4 when the sequence has at
+      // most 4 splits, else 16): each batch loads its maxima, sums and partial
+      // outputs together.  Every split below ns holds a token, so its maximum
+      // is finite.
       const int ns = min((L + split - 1) / split, s_max);
       const int64_t base = static_cast<int64_t>(b) * s_max * H + h;  // + s * H
       float M = -INFINITY, Ls = 0.f;
       float acc[PER];
 #pragma unroll
       for (int j = 0; j < PER; ++j) acc[j] = 0.f;
-      for (int s0 = 0; s0 < ns; s0 += SB) {
-        float pv[SB][PER];
-        float mv[SB], lv[SB];
-#pragma unroll
-        for (int u = 0; u < SB; ++u) {
-          const int sidx = min(s0 + u, ns - 1);
-          const int64_t row = base + static_cast<int64_t>(sidx) * H;
-          mv[u] = part_ml[row * 2];
-          lv[u] = part_ml[row * 2 + 1];
-#pragma unroll
-          for (int j = 0; j < PER; ++j) pv[u][j] = part_o[row * DC + lane + 64 * j];
-        }
-        float mb = -INFINITY;
-#pragma unroll
-        for (int u = 0; u < SB; ++u) mb = fmaxf(mb, mv[u]);  // repeated last split: no effect on the max
-        const float Mn = fmaxf(M, mb);
-        const float sc = exp2f(M - Mn);  // 0 for the first batch
-        Ls *= sc;
-#pragma unroll
-        for (int j = 0; j < PER; ++j) acc[j] *= sc;
-#pragma unroll
-        for (int u = 0; u < SB; ++u) {
-          const float e = s0 + u < ns ? exp2f(mv[u] - Mn) : 0.f;
-          Ls += lv[u] * e;
-#pragma unroll
-          for (int j = 0; j < PER; ++j) acc[j] = fmaf(e, pv[u][j], acc[j]);
-        }
-        M = Mn;
+      if (ns <= 4) {
+        merge_batch<DC, 4>(part_ml, part_o, base, H, 0, ns, lane, M, Ls, acc);
+      } else {
+        for (int s0 = 0; s0 < ns; s0 += 16) merge_batch<DC, 16>(part_ml, part_o, base, H, s0, ns, lane, M, Ls, acc);
       }
       const float inv = 1.f / Ls;
 #pragma unroll
-      for (int j = 0; j < PER; ++j) orow[lane + 64 * j] = acc[j] * inv;
+      for (int j = 0; j < PER; ++j) orow[comb_dim<DC>(lane, j)] = acc[j] * inv;
     }
   }
   __syncthreads();
