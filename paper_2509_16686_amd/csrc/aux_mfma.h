@@ -105,15 +105,22 @@ __global__ __launch_bounds__(256) void absorb_mfma_kernel(const uint16_t* __rest
 }
 
 // ---------------------------------------------------------------------------
-// Combine on MFMA: grid (H, ceil(B / 4)), 256 threads.  Wave w merges the
-// splits of sequence b0 + w for head h into LDS (fp32, divided by the softmax
-// sum), online over batches of 4 or 16 splits whose maxima, sums and partial
-// outputs are loaded together.  Then out^T[v][b] =
-// W_UV[h][v][:] . o[b][:] runs on v_mfma_f32_16x16x32_bf16 with W_UV rows as
-// the A operand (16-byte loads, all issued before the first product) and o
-// split into bf16 hi + lo as the B operand (4 of its 16 columns used).
+// Combine on MFMA: grid (H, ceil(B / 16)), 1024 threads (16 waves), one head
+// and up to 16 sequences per work-group.
+//  1. Waves 0 .. nvt-1 issue the W_UV rows of their 16-row output tile first.
+//  2. The splits of each sequence are merged online in fp32: with n
+//     sequences in the group, each gets wps = 16 / pow2ceil(n) waves, and wave
+//     p of a sequence merges its splits p, p + wps, ... in batches of 4, 8 or 16
+//     (maxima, sums and partial outputs loaded together) into LDS.
+//  3. All threads merge each sequence's wps parts into its latent row o / l.
+//  4. out^T[v][b] = W_UV[h][v][:] . o[b][:] on v_mfma_f32_16x16x32_bf16, the
+//     16 sequences being the 16 columns of the B operand, o split into bf16
+//     hi + lo (two products) so the up-projection adds only W_UV's own
+//     rounding.
 // ---------------------------------------------------------------------------
-constexpr int kCombSeq = 4;
+constexpr int kCombSeq = 16;
+constexpr int kCombWaves = 16;
+constexpr size_t combine_lds_bytes(int DC) { return sizeof(float) * (kCombSeq * (DC + 4) + kCombWaves * DC + 2 * kCombWaves); }
 
 // Latent dim held in accumulator j of a combine lane: with an even number of
 // dims per lane, lane l holds the adjacent pairs 128 i + 2 l + {0, 1} (8-byte
@@ -125,18 +132,19 @@ __device__ __forceinline__ int comb_dim(int lane, int j) {
   else return lane + 64 * j;
 }
 
-// One batch of SB splits of the online merge (s0 .. s0 + SB - 1, clamped to
-// ns - 1): maxima, sums and partial outputs load together.
+// One batch of SB splits of the online merge: the splits first + stride * t
+// for t = s0 .. s0 + SB - 1 (t clamped to ns - 1, counted while t < ns).
+// Their maxima, sums and partial outputs load together.
 template <int DC, int SB>
 __device__ __forceinline__ void merge_batch(const float* __restrict__ part_ml, const float* __restrict__ part_o,
-                                            int64_t base, int H, int s0, int ns, int lane, float& M, float& Ls,
-                                            float (&acc)[DC / 64]) {
+                                            int64_t base, int H, int first, int stride, int s0, int ns, int lane,
+                                            float& M, float& Ls, float (&acc)[DC / 64]) {
   constexpr int PER = DC / 64;
   float pv[SB][PER];
   float2 ml[SB];
 #pragma unroll
   for (int u = 0; u < SB; ++u) {
-    const int64_t row = base + static_cast<int64_t>(min(s0 + u, ns - 1)) * H;
+    const int64_t row = base + static_cast<int64_t>(first + stride * min(s0 + u, ns - 1)) * H;
     ml[u] = *reinterpret_cast<const float2*>(part_ml + row * 2);
     if constexpr (PER % 2 == 0) {
 #pragma unroll
@@ -168,74 +176,95 @@ __device__ __forceinline__ void merge_batch(const float* __restrict__ part_ml, c
   M = Mn;
 }
 
-
 template <int DC, int DV>
-__global__ __launch_bounds__(256) void combine_mfma_kernel(const float* __restrict__ part_ml,
-                                                           const float* __restrict__ part_o,
-                                                           const uint16_t* __restrict__ w_uv,
-                                                           const int32_t* __restrict__ seq_lens,
-                                                           uint16_t* __restrict__ out, int B, int H, int cap,
-                                                           int split, int s_max) {
+__global__ __launch_bounds__(kCombWaves * 64) void combine_mfma_kernel(const float* __restrict__ part_ml,
+                                                                       const float* __restrict__ part_o,
+                                                                       const uint16_t* __restrict__ w_uv,
+                                                                       const int32_t* __restrict__ seq_lens,
+                                                                       uint16_t* __restrict__ out, int B, int H,
+                                                                       int cap, int split, int s_max) {
   constexpr int OS = DC + 4;
   constexpr int PER = DC / 64;  // latent columns per lane
   constexpr int NKC = DC / 32;
-  __shared__ __attribute__((aligned(16))) float o_s[16 * OS];  // rows 4..15 stay zero
+  constexpr int nvt = (DV + 15) / 16;
+  static_assert(nvt <= kCombWaves, "one output tile per wave");
+  extern __shared__ __attribute__((aligned(16))) float comb_lds[];  // combine_lds_bytes(DC) bytes
+  float* o_s = comb_lds;                                            // [kCombSeq][OS]: merged rows (B operand)
+  float* o_part = o_s + kCombSeq * OS;                              // [kCombWaves][DC]: each wave's partial merge
+  float* m_part = o_part + kCombWaves * DC;                         // [kCombWaves]
+  float* l_part = m_part + kCombWaves;                              // [kCombWaves]
   const int h = blockIdx.x;
   const int b0 = blockIdx.y * kCombSeq;
-  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
+  const int tid = threadIdx.x, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int nseq = min(kCombSeq, B - b0);
+  int np2 = 1;
+  while (np2 < nseq) np2 <<= 1;
+  const int wps = kCombWaves / np2;  // waves per sequence (power of two)
 
-  // W_UV rows of this wave's output tiles: issued first, used last
-  constexpr int nvt = (DV + 15) / 16;
-  constexpr int kMaxVt = (nvt + 3) / 4;  // v-tiles per wave
-  u32x4_t wa[kMaxVt][NKC];
+  // (1) W_UV rows of this wave's output tile: issued first, used last
+  u32x4_t wa[NKC];
+  const int vt = w;
+  if (vt < nvt) {
+    const int v = min(vt * 16 + r16, DV - 1);
 #pragma unroll
-  for (int i = 0; i < kMaxVt; ++i) {
-    const int vt = w + 4 * i;
-    if (vt < nvt) {
-      const int v = min(vt * 16 + r16, DV - 1);
-#pragma unroll
-      for (int kc = 0; kc < NKC; ++kc)
-        wa[i][kc] = *reinterpret_cast<const u32x4_t*>(w_uv + (static_cast<int64_t>(h) * DV + v) * DC + kc * 32 + g * 8);
-    }
+    for (int kc = 0; kc < NKC; ++kc)
+      wa[kc] = *reinterpret_cast<const u32x4_t*>(w_uv + (static_cast<int64_t>(h) * DV + v) * DC + kc * 32 + g * 8);
   }
 
-  for (int i = tid; i < 12 * OS; i += 256) o_s[4 * OS + i] = 0.f;
-  {
-    const int b = b0 + w;
-    const int L = b < B ? clamp_len(seq_lens[b], cap) : 0;
-    float* orow = o_s + w * OS;
-    if (L == 0) {
+  // (2) this wave's part of its sequence's splits
+  const int k = w / wps, part = w % wps;
+  const int b = b0 + k;
+  const int L = (k < nseq) ? clamp_len(seq_lens[b], cap) : 0;
+  const int ns_all = L > 0 ? min((L + split - 1) / split, s_max) : 0;
+  const int ns = ns_all > part ? (ns_all - part + wps - 1) / wps : 0;  // this part's splits
+  float M = -INFINITY, Ls = 0.f;
+  float acc[PER];
 #pragma unroll
-      for (int j = 0; j < PER; ++j) orow[comb_dim<DC>(lane, j)] = 0.f;
+  for (int j = 0; j < PER; ++j) acc[j] = 0.f;
+  if (ns > 0) {  // every split below ns_all holds a token, so its maximum is finite
+    const int64_t base = static_cast<int64_t>(b) * s_max * H + h;  // + s * H
+    if (ns <= 4) {
+      merge_batch<DC, 4>(part_ml, part_o, base, H, part, wps, 0, ns, lane, M, Ls, acc);
+    } else if (ns <= 8) {
+      merge_batch<DC, 8>(part_ml, part_o, base, H, part, wps, 0, ns, lane, M, Ls, acc);
     } else {
-      // Online merge of the splits in batches (4 when the sequence has at
-      // most 4 splits, else 16): each batch loads its maxima, sums and partial
-      // outputs together.  Every split below ns holds a token, so its maximum
-      // is finite.
-      const int ns = min((L + split - 1) / split, s_max);
-      const int64_t base = static_cast<int64_t>(b) * s_max * H + h;  // + s * H
-      float M = -INFINITY, Ls = 0.f;
-      float acc[PER];
-#pragma unroll
-      for (int j = 0; j < PER; ++j) acc[j] = 0.f;
-      if (ns <= 4) {
-        merge_batch<DC, 4>(part_ml, part_o, base, H, 0, ns, lane, M, Ls, acc);
-      } else {
-        for (int s0 = 0; s0 < ns; s0 += 16) merge_batch<DC, 16>(part_ml, part_o, base, H, s0, ns, lane, M, Ls, acc);
-      }
-      const float inv = 1.f / Ls;
-#pragma unroll
-      for (int j = 0; j < PER; ++j) orow[comb_dim<DC>(lane, j)] = acc[j] * inv;
+      for (int s0 = 0; s0 < ns; s0 += 16) merge_batch<DC, 16>(part_ml, part_o, base, H, part, wps, s0, ns, lane, M, Ls, acc);
     }
+  }
+#pragma unroll
+  for (int j = 0; j < PER; ++j) o_part[w * DC + comb_dim<DC>(lane, j)] = acc[j];
+  if (lane == 0) {
+    m_part[w] = M;
+    l_part[w] = Ls;
   }
   __syncthreads();
 
-  const int b = b0 + r16;
-#pragma unroll
-  for (int i = 0; i < kMaxVt; ++i) {
-    const int vt = w + 4 * i;
-    if (vt >= nvt) break;
-    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+  // (3) merge the parts of each sequence into its row o / l (rows past the
+  // group's sequences, and empty sequences, are zero)
+  for (int i = tid; i < kCombSeq * DC; i += kCombWaves * 64) {
+    const int kk = i / DC, c = i - kk * DC;
+    float v = 0.f;
+    if (kk < nseq) {
+      float Mx = -INFINITY;
+      for (int p = 0; p < wps; ++p) Mx = fmaxf(Mx, m_part[kk * wps + p]);
+      if (Mx > -INFINITY) {
+        float num = 0.f, den = 0.f;
+        for (int p = 0; p < wps; ++p) {
+          const float e = __builtin_amdgcn_exp2f(m_part[kk * wps + p] - Mx);  // empty part: exp2(-inf) = 0
+          num = fmaf(e, o_part[(kk * wps + p) * DC + c], num);
+          den = fmaf(e, l_part[kk * wps + p], den);
+        }
+        v = num / den;
+      }
+    }
+    o_s[kk * OS + c] = v;
+  }
+  __syncthreads();
+
+  // (4) out^T[vt*16 + 4g + r][b0 + r16] for this wave's tile
+  if (vt < nvt) {
+    f32x4_t o = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kc = 0; kc < NKC; ++kc) {
       const float* orow = o_s + r16 * OS + kc * 32 + g * 8;
@@ -248,16 +277,16 @@ __global__ __launch_bounds__(256) void combine_mfma_kernel(const float* __restri
         hi[e] = static_cast<__bf16>(x[e]);
         lo[e] = static_cast<__bf16>(x[e] - static_cast<float>(hi[e]));
       }
-      const bf16x8_t av = __builtin_bit_cast(bf16x8_t, wa[i][kc]);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, hi, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, lo, acc, 0, 0, 0);
+      const bf16x8_t av = __builtin_bit_cast(bf16x8_t, wa[kc]);
+      o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, hi, o, 0, 0, 0);
+      o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, lo, o, 0, 0, 0);
     }
-    // lane holds out^T[vt*16 + 4g + r][b0 + r16]
-    if (r16 < kCombSeq && b < B) {
+    const int bb = b0 + r16;
+    if (r16 < nseq) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int vv = vt * 16 + 4 * g + r;
-        if (vv < DV) out[(static_cast<int64_t>(b) * H + h) * DV + vv] = f32_to_bf16(acc[r]);
+        if (vv < DV) out[(static_cast<int64_t>(bb) * H + h) * DV + vv] = f32_to_bf16(o[r]);
       }
     }
   }

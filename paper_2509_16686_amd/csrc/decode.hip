@@ -309,6 +309,25 @@ hipError_t set_lds(K kernel, size_t bytes) {
 constexpr int kTokWaves = 4;
 constexpr int kTokDepth = 3;
 
+template <int DC>
+hipError_t launch_combine_dc(dim3 grid, hipStream_t stream, const float* pm, const float* po, const uint16_t* wv,
+                             const int32_t* seq_lens, uint16_t* ov, int B, int H, int cap, int split, int s_max) {
+  const size_t lds = combine_lds_bytes(DC);
+  hipError_t e = set_lds(combine_mfma_kernel<DC, 128>, lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((combine_mfma_kernel<DC, 128>), grid, dim3(kCombWaves * 64), lds, stream, pm, po, wv, seq_lens,
+                     ov, B, H, cap, split, s_max);
+  return hipGetLastError();
+}
+
+hipError_t launch_combine_mfma(int dc, dim3 grid, hipStream_t stream, const float* pm, const float* po,
+                               const uint16_t* wv, const int32_t* seq_lens, uint16_t* ov, int B, int H, int cap,
+                               int split, int s_max) {
+  if (dc == 128) return launch_combine_dc<128>(grid, stream, pm, po, wv, seq_lens, ov, B, H, cap, split, s_max);
+  if (dc == 320) return launch_combine_dc<320>(grid, stream, pm, po, wv, seq_lens, ov, B, H, cap, split, s_max);
+  return launch_combine_dc<512>(grid, stream, pm, po, wv, seq_lens, ov, B, H, cap, split, s_max);
+}
+
 // The MFMA split kernels launch with hipExtLaunchKernelGGL so that optional
 // timing events are stamped by the dispatch itself (kernel start and end).
 template <int DC, int DR>
@@ -442,15 +461,9 @@ extern "C" eg_mla_status eg_mla_decode_planned(const eg_mla_dims* dims, int32_t 
       const float* po = part_o;
       const uint16_t* wv = static_cast<const uint16_t*>(w_uv);
       uint16_t* ov = static_cast<uint16_t*>(out);
-      if (d.latent_dim == 128)
-        hipLaunchKernelGGL((combine_mfma_kernel<128, 128>), g2, dim3(256), 0, stream, pm, po, wv, seq_lens, ov, batch,
-                           d.num_heads, p.capacity, p.split_tokens, p.s_max);
-      else if (d.latent_dim == 320)
-        hipLaunchKernelGGL((combine_mfma_kernel<320, 128>), g2, dim3(256), 0, stream, pm, po, wv, seq_lens, ov, batch,
-                           d.num_heads, p.capacity, p.split_tokens, p.s_max);
-      else
-        hipLaunchKernelGGL((combine_mfma_kernel<512, 128>), g2, dim3(256), 0, stream, pm, po, wv, seq_lens, ov, batch,
-                           d.num_heads, p.capacity, p.split_tokens, p.s_max);
+      if (launch_combine_mfma(d.latent_dim, g2, stream, pm, po, wv, seq_lens, ov, batch, d.num_heads, p.capacity,
+                              p.split_tokens, p.s_max) != hipSuccess)
+        return EG_MLA_ERR_HIP;
     } else if (bf) {
       if (set_lds(combine_kernel<true>, lds) != hipSuccess) return EG_MLA_ERR_HIP;
       hipLaunchKernelGGL(combine_kernel<true>, grid, dim3(256), lds, stream, part_ml, part_o, w_uv, seq_lens, out,
