@@ -226,6 +226,7 @@ __global__ __launch_bounds__(kValuThreads) void split_valu_kernel(SplitArgs a) {
 }  // namespace egmla
 #include "split_mfma.h"
 #include "split_tok.h"
+#include "split_heads.h"
 namespace egmla {
 
 // ---------------------------------------------------------------------------
@@ -338,6 +339,13 @@ hipError_t launch_tok(const SplitArgs& a, int nblocks, hipStream_t stream, hipEv
 }
 
 template <int DC, int DR>
+hipError_t launch_heads(const SplitArgs& a, int nblocks, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
+  hipExtLaunchKernelGGL((split_heads_kernel<DC, DR>), dim3(nblocks), dim3(HsplitCfg<DC, DR>::NT), 0, stream, ev0,
+                        ev1, 0, a);
+  return hipGetLastError();
+}
+
+template <int DC, int DR>
 hipError_t launch_mfma(const SplitArgs& a, int nblocks, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
   hipExtLaunchKernelGGL((split_mfma_kernel<DC, DR>), dim3(nblocks), dim3(DsplitCfg<DC, DR>::NW * 64), 0, stream, ev0,
                         ev1, 0, a);
@@ -351,6 +359,7 @@ hipError_t launch_split(const eg_mla_dims& d, const DecodePlan& p, const SplitAr
   const int nblocks = static_cast<int>(nblocks64);
   if (p.path == EG_MLA_PATH_MFMA) {
     if (tok_kernel_shape(d)) return launch_tok<128, 64>(a, nblocks, stream, ev0, ev1);
+    if (heads_kernel_shape(d)) return launch_heads<512, 64>(a, nblocks, stream, ev0, ev1);
     if (d.latent_dim == 320) return launch_mfma<320, 64>(a, nblocks, stream, ev0, ev1);
     if (d.latent_dim == 512) return launch_mfma<512, 64>(a, nblocks, stream, ev0, ev1);
     return hipErrorInvalidValue;

@@ -25,6 +25,9 @@ bool mfma_shape_supported(const eg_mla_dims& d) {
 }
 
 bool tok_kernel_shape(const eg_mla_dims& d) { return d.latent_dim == 128 && d.rope_dim == 64; }
+bool heads_kernel_shape(const eg_mla_dims& d) {
+  return d.latent_dim == 512 && d.rope_dim == 64 && d.num_heads % kHeadsPerItemWide == 0;
+}
 
 eg_mla_status check_dims(const eg_mla_dims* d) {
   if (!d) return EG_MLA_ERR_INVALID_ARG;
@@ -58,7 +61,7 @@ eg_mla_status make_decode_plan(const eg_mla_dims& d, int32_t batch, int32_t max_
   p.capacity = static_cast<int>(cap64);
 
   if (p.path == EG_MLA_PATH_MFMA) {
-    p.heads_per_group = 16;
+    p.heads_per_group = heads_kernel_shape(d) ? kHeadsPerItemWide : 16;
   } else {
     // Heads per VALU work item: at most 8192 latent accumulators per workgroup.
     p.heads_per_group = std::max(1, std::min({d.num_heads, 8192 / d.latent_dim, 256}));
@@ -70,7 +73,8 @@ eg_mla_status make_decode_plan(const eg_mla_dims& d, int32_t batch, int32_t max_
   if (p.path == EG_MLA_PATH_MFMA && split > kMaxSplitTokens) return EG_MLA_ERR_UNSUPPORTED;
   if (split == 0) {
     const int64_t work = static_cast<int64_t>(std::max(batch, 1)) * std::max(p.capacity, 1) * p.head_groups;
-    const int64_t target = p.path == EG_MLA_PATH_MFMA && tok_kernel_shape(d) ? kTargetWorkItemsTok : kTargetWorkItems;
+    const int64_t target =
+        p.path == EG_MLA_PATH_MFMA && (tok_kernel_shape(d) || heads_kernel_shape(d)) ? kTargetWorkItemsTok : kTargetWorkItems;
     int64_t s = (work + target - 1) / target;
     s = (s + kTile - 1) / kTile * kTile;
     const int min_split = p.path == EG_MLA_PATH_MFMA ? 256 : 128;

@@ -22,8 +22,12 @@ constexpr int kMaxSplitTokensDevice = kMaxSplitTokens;
 
 // MFMA kernel instantiations: (latent_dim, rope_dim) pairs with a compiled fast path.
 bool mfma_shape_supported(const eg_mla_dims& d);
-// MFMA shapes served by the token-split kernel (the others by the dimension-split one).
+// MFMA shapes served by the token-split kernel (16 heads per work item)...
 bool tok_kernel_shape(const eg_mla_dims& d);
+// ... and by the head-split kernel (128 heads per work item); the others by the
+// dimension-split kernel (16 heads per work item).
+bool heads_kernel_shape(const eg_mla_dims& d);
+constexpr int kHeadsPerItemWide = 128;
 
 struct DecodePlan {
   int path = EG_MLA_PATH_VALU;  // resolved: VALU or MFMA
