@@ -89,6 +89,27 @@ def test_many_head_groups_and_dc512(gpu):
         assert_close(gpu_decode(inp, B.make_plan(path, 256)), oracle_decode(inp), "bf16", f"path {path}", scaled=True)
 
 
+@pytest.mark.parametrize("split", [32, 2048])
+def test_two_head_blocks_dc512(gpu, split):
+    # 256 heads: the head-split kernel runs two blocks of 128 heads per split
+    wl = W.WORKLOADS[4].replace(name="h256_dc512", heads=256, batch=2, seq_len_range=(40, 300), seed=43)
+    inp = W.generate(wl)
+    say(f"decode h256 dc512 ragged paged split={split}")
+    assert_close(gpu_decode(inp, B.make_plan(B.PATH_MFMA, split)), oracle_decode(inp), "bf16", f"h256 split {split}",
+                 scaled=True)
+
+
+def test_edge_lengths_dc512(gpu):
+    wl = W.WORKLOADS[4].replace(name="edge_dc512", batch=7, paged=False, seq_len_range=(1, 64), seed=44)
+    # empty, one token, a partial tile, one tile, one past a tile, two tiles plus one, full capacity
+    lens = np.array([0, 1, 15, 16, 17, 33, 64])
+    inp = W.generate(wl, seq_lens=lens)
+    say(f"decode dc512 edge lengths {lens.tolist()}")
+    got = gpu_decode(inp, B.make_plan(B.PATH_MFMA, 32))
+    assert np.all(got[0] == 0)
+    assert_close(got, oracle_decode(inp), "bf16", "dc512 edge lengths", scaled=True)
+
+
 def test_peaked_logits(gpu):
     inp = W.generate(SMALL.replace(seed=22), seq_lens=np.array([64, 500, 129, 7]))
     inp.q[:] = W.f32_to_bf16_bits(W.bf16_bits_to_f32(inp.q) * np.float32(8.0))
