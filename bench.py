@@ -36,6 +36,19 @@ TRAFFIC_PROFILE = os.path.join(REPO, "profiles", "split_tok_b32_h16_dc128_dr64_l
 
 
 
+
+def split_kernel_name(wl, path):
+    """The split kernel the library launches for this workload and path (see host_plan.cpp)."""
+    if wl.dtype != "bf16" or path == "valu":
+        return "split_valu_kernel"
+    if wl.latent_dim == 128 and wl.rope_dim == 64:
+        return "split_tok_kernel"
+    if wl.latent_dim == 512 and wl.rope_dim == 64 and wl.heads % 128 == 0:
+        return "split_heads_kernel"
+    if wl.heads % 16 == 0 and wl.rope_dim == 64 and wl.latent_dim in (320, 512):
+        return "split_mfma_kernel"
+    return "split_valu_kernel"
+
 def recorded_traffic():
     """Bytes per split-kernel launch from the committed counter summary, or None when the
     summary is missing or the kernel sources changed since the counters were taken."""
@@ -270,7 +283,7 @@ def main():
                    "rotating_copies": R},
         "hbm_gbps_call": traffic.total / (ms_per_step * 1e-3) / 1e9,
         "hbm_frac_call": traffic.total / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
-        "roofline": {"bound": "hbm", "kernel": "split_mfma_kernel" if wl.dtype == "bf16" else "split_valu_kernel",
+        "roofline": {"bound": "hbm", "kernel": split_kernel_name(wl, args.path),
                      "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic_gbps,
                      "algorithmic_bytes_per_launch": k_bytes, "traffic_bytes_per_launch": t_bytes, "kernel_us": k_avg_ms * 1e3},

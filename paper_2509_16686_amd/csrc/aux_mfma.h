@@ -7,32 +7,40 @@ namespace egmla {
 
 // ---------------------------------------------------------------------------
 // Absorption on MFMA: qfull[b, h, c] = sum_k q^C[b, h, k] W_UK[h, k, c] for
-// 16 sequences x 128 latent columns per work-group (grid H x ceil(B/16) x
-// ceil(DC/128), 256 threads), plus the q^R copy.  W_UK[h][:, c-block] is
-// loaded with 16-byte row loads and stored row-major in LDS; the B operand
-// (8 consecutive k of one column) is two ds_read_b64_tr_b16, whose 16-lane
-// transpose hands lane n the column n of 4 consecutive rows.  The A operand
-// (8 consecutive k of one query row) comes straight from global.  bf16 x bf16
-// products are exact in fp32 and accumulate in fp32.
+// BLOCKS (1..4) blocks of 16 sequences x 128 latent columns per work-group
+// (grid H x ceil(B / (16 blocks)) x ceil(DC/128), 256 threads), plus the q^R
+// copy.  More blocks per work-group read W_UK fewer times; fewer spread a
+// small batch over more compute units.
+// W_UK[h][:, c-block] is read once per work-group with 16-byte row loads and
+// stored row-major in LDS; the B operand (8 consecutive k of one column) is
+// two ds_read_b64_tr_b16, whose 16-lane transpose hands lane n the column n
+// of 4 consecutive rows, and serves every sequence block.  The A operands (8
+// consecutive k of one query row) come straight from global.  Every load is
+// issued before the first use.  bf16 x bf16 products are exact in fp32 and
+// accumulate in fp32.
 // ---------------------------------------------------------------------------
-constexpr int kAbsRows = 16;
+constexpr int kAbsRows = 16;    // sequences per MFMA row block
+constexpr int kAbsBlocks = 4;   // row blocks per work-group, at most
 constexpr int kAbsCols = 128;
 
-template <int DH>
+template <int DH, int BLOCKS>
 __global__ __launch_bounds__(256) void absorb_mfma_kernel(const uint16_t* __restrict__ q,
                                                           const uint16_t* __restrict__ w_uk,
                                                           float* __restrict__ qfull, int B, int H, int DC, int DR) {
+  static_assert(BLOCKS >= 1 && BLOCKS <= kAbsBlocks, "row blocks per work-group");
   constexpr int RS = kAbsCols + 8;  // padded LDS row (bf16 elements)
   constexpr int NK = DH / 32;
   __shared__ __attribute__((aligned(16))) uint16_t wrm[DH * RS];  // [k][c], row-major
+  constexpr int ROWS = kAbsRows * BLOCKS;  // sequences of this work-group
   const int h = blockIdx.x;
-  const int b0 = blockIdx.y * kAbsRows;
+  const int b0 = blockIdx.y * ROWS;
   const int c0 = blockIdx.z * kAbsCols;
   const int nc = min(kAbsCols, DC - c0);
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
   const int DQin = DH + DR, DQ = DC + DR;
 
-  // (1) issue every load: this thread's W rows (16 B = 8 columns each) and its A operand chunks
+  // (1) issue every load: this thread's W rows (16 B = 8 columns each), its A
+  // operand chunks for every row block, and its RoPE query values
   constexpr int kRowsPerPass = 256 / (kAbsCols / 8);  // 16 rows of 128 columns per pass
   constexpr int kPasses = (DH + kRowsPerPass - 1) / kRowsPerPass;
   const int cc = (tid % (kAbsCols / 8)) * 8;  // first of this thread's 8 columns
@@ -44,22 +52,28 @@ __global__ __launch_bounds__(256) void absorb_mfma_kernel(const uint16_t* __rest
     const int c = min(c0 + cc, DC - 8);
     wv[p] = *reinterpret_cast<const u32x4_t*>(w_uk + (static_cast<int64_t>(h) * DH + kk) * DC + c);
   }
-  const int bq = min(b0 + r16, B - 1);
-  u32x4_t qa[NK];
+  u32x4_t qa[BLOCKS][NK];
 #pragma unroll
-  for (int ks = 0; ks < NK; ++ks)
-    qa[ks] = *reinterpret_cast<const u32x4_t*>(q + (static_cast<int64_t>(bq) * H + h) * DQin + ks * 32 + g * 8);
+  for (int rb = 0; rb < BLOCKS; ++rb) {
+    const int bq = min(b0 + rb * kAbsRows + r16, B - 1);
+#pragma unroll
+    for (int ks = 0; ks < NK; ++ks)
+      qa[rb][ks] = *reinterpret_cast<const u32x4_t*>(q + (static_cast<int64_t>(bq) * H + h) * DQin + ks * 32 + g * 8);
+  }
   // RoPE part of the query rows (copied as fp32): when d_r is a multiple of 4
   // and at most 64, thread t loads 4 consecutive values of row t / (d_r / 4)
-  // (one 8-byte load, index clamped so the load is unconditional); other
-  // shapes copy element by element after the product.
+  // of each row block (8-byte loads, rows clamped so the loads are
+  // unconditional); other shapes copy element by element after the product.
   const bool rope_vec = blockIdx.z == 0 && DR > 0 && DR % 4 == 0 && DR <= 64;
-  const int rq_row = rope_vec ? tid / (DR / 4) : 0;
+  const int rq_row = rope_vec ? tid / (DR / 4) : 0;  // row within a block
   const int rq_col = rope_vec ? 4 * (tid % (DR / 4)) : 0;
-  const bool rq_ok = rope_vec && rq_row < kAbsRows && b0 + rq_row < B;
-  const int rq_b = min(b0 + min(rq_row, kAbsRows - 1), B - 1);
-  const uint2 rq = rope_vec ? *reinterpret_cast<const uint2*>(q + (static_cast<int64_t>(rq_b) * H + h) * DQin + DH + rq_col)
-                            : make_uint2(0u, 0u);
+  uint2 rq[BLOCKS];
+#pragma unroll
+  for (int rb = 0; rb < BLOCKS; ++rb) {
+    const int rb_b = min(b0 + rb * kAbsRows + min(rq_row, kAbsRows - 1), B - 1);
+    rq[rb] = rope_vec ? *reinterpret_cast<const uint2*>(q + (static_cast<int64_t>(rb_b) * H + h) * DQin + DH + rq_col)
+                      : make_uint2(0u, 0u);
+  }
   // (2) W rows into LDS as loaded (columns past DC hold unused values)
 #pragma unroll
   for (int p = 0; p < kPasses; ++p) {
@@ -67,12 +81,14 @@ __global__ __launch_bounds__(256) void absorb_mfma_kernel(const uint16_t* __rest
     if (k < DH) *reinterpret_cast<u32x4_t*>(wrm + k * RS + cc) = wv[p];
   }
   __syncthreads();
-  // (3) wave w computes column tiles w, w+4 (16 columns each).  For rows
-  // k0 .. k0 + 3 of the tile, lane r16 of group g reads columns
-  // 4 (r16 % 4) .. + 3 of row k0 + r16 / 4; the transposed read hands lane r16
-  // column r16 of the 4 rows.
+  // (3) wave w computes column tiles w, w+4 (16 columns each) of every row
+  // block.  For rows k0 .. k0 + 3 of the tile, lane r16 of group g reads
+  // columns 4 (r16 % 4) .. + 3 of row k0 + r16 / 4; the transposed read hands
+  // lane r16 column r16 of the 4 rows.
   for (int nt = w; nt * 16 < nc; nt += 4) {
-    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+    f32x4_t acc[BLOCKS];
+#pragma unroll
+    for (int rb = 0; rb < BLOCKS; ++rb) acc[rb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < NK; ++ks) {
       uint16_t* t0 = wrm + (ks * 32 + 8 * g + (r16 >> 2)) * RS + nt * 16 + 4 * (r16 & 3);
@@ -81,21 +97,31 @@ __global__ __launch_bounds__(256) void absorb_mfma_kernel(const uint16_t* __rest
           __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t*)(t0 + 4 * RS));
       const u32x2_t l2 = __builtin_bit_cast(u32x2_t, lo), h2 = __builtin_bit_cast(u32x2_t, hi);
       const bf16x8_t bv = __builtin_bit_cast(bf16x8_t, u32x4_t{l2[0], l2[1], h2[0], h2[1]});
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, qa[ks]), bv, acc, 0, 0, 0);
+#pragma unroll
+      for (int rb = 0; rb < BLOCKS; ++rb)
+        acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, qa[rb][ks]), bv, acc[rb], 0, 0, 0);
     }
-    // lane holds D[b = 4g + r][c = nt*16 + r16]
+    // lane holds D[b = 4g + r][c = nt*16 + r16] of each row block
     const int c = c0 + nt * 16 + r16;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int b = b0 + 4 * g + r;
-      if (b < B && c < DC) qfull[(static_cast<int64_t>(b) * H + h) * DQ + c] = acc[r];
+    for (int rb = 0; rb < BLOCKS; ++rb) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int b = b0 + rb * kAbsRows + 4 * g + r;
+        if (b < B && c < DC) qfull[(static_cast<int64_t>(b) * H + h) * DQ + c] = acc[rb][r];
+      }
     }
   }
-  if (rq_ok) {
-    *reinterpret_cast<float4*>(qfull + (static_cast<int64_t>(b0 + rq_row) * H + h) * DQ + DC + rq_col) =
-        make_float4(bf16_lo(rq.x), bf16_hi(rq.x), bf16_lo(rq.y), bf16_hi(rq.y));
-  } else if (blockIdx.z == 0 && !rope_vec) {
-    for (int i = tid; i < kAbsRows * DR; i += 256) {
+  if (rope_vec) {
+#pragma unroll
+    for (int rb = 0; rb < BLOCKS; ++rb) {
+      const int b = b0 + rb * kAbsRows + rq_row;
+      if (rq_row < kAbsRows && b < B)
+        *reinterpret_cast<float4*>(qfull + (static_cast<int64_t>(b) * H + h) * DQ + DC + rq_col) =
+            make_float4(bf16_lo(rq[rb].x), bf16_hi(rq[rb].x), bf16_lo(rq[rb].y), bf16_hi(rq[rb].y));
+    }
+  } else if (blockIdx.z == 0) {
+    for (int i = tid; i < ROWS * DR; i += 256) {
       const int bb = i / DR, r = i % DR;
       if (b0 + bb < B)
         qfull[(static_cast<int64_t>(b0 + bb) * H + h) * DQ + DC + r] =
@@ -107,10 +133,12 @@ __global__ __launch_bounds__(256) void absorb_mfma_kernel(const uint16_t* __rest
 // ---------------------------------------------------------------------------
 // Combine on MFMA: grid (H, ceil(B / 16)), 1024 threads (16 waves), one head
 // and up to 16 sequences per work-group.
-//  1. Waves 0 .. nvt-1 issue the W_UV rows of their 16-row output tile first.
+//  1. Waves 0 .. nvt-1 issue the W_UV rows of their 16-row output tile (first
+//     for d_c <= 128; after step 3 for wider latents, to stay in registers).
 //  2. The splits of each sequence are merged online in fp32: with n
 //     sequences in the group, each gets wps = 16 / pow2ceil(n) waves, and wave
 //     p of a sequence merges its splits p, p + wps, ... in batches of 4, 8 or 16
+//     (at most 8 for d_c > 128)
 //     (maxima, sums and partial outputs loaded together) into LDS.
 //  3. All threads merge each sequence's wps parts into its latent row o / l.
 //  4. out^T[v][b] = W_UV[h][v][:] . o[b][:] on v_mfma_f32_16x16x32_bf16, the
@@ -202,15 +230,22 @@ __global__ __launch_bounds__(kCombWaves * 64) void combine_mfma_kernel(const flo
   while (np2 < nseq) np2 <<= 1;
   const int wps = kCombWaves / np2;  // waves per sequence (power of two)
 
-  // (1) W_UV rows of this wave's output tile: issued first, used last
+  // (1) W_UV rows of this wave's output tile, issued first for narrow
+  // latents; for wide ones (NKC x 16 bytes per lane) after the merge, which
+  // then has the registers to itself.
+  constexpr bool kEarlyW = DC <= 128;
+  constexpr int kSBMax = DC <= 128 ? 16 : 8;  // splits per merge batch, at most
   u32x4_t wa[NKC];
   const int vt = w;
-  if (vt < nvt) {
-    const int v = min(vt * 16 + r16, DV - 1);
+  auto load_w = [&]() {
+    if (vt < nvt) {
+      const int v = min(vt * 16 + r16, DV - 1);
 #pragma unroll
-    for (int kc = 0; kc < NKC; ++kc)
-      wa[kc] = *reinterpret_cast<const u32x4_t*>(w_uv + (static_cast<int64_t>(h) * DV + v) * DC + kc * 32 + g * 8);
-  }
+      for (int kc = 0; kc < NKC; ++kc)
+        wa[kc] = *reinterpret_cast<const u32x4_t*>(w_uv + (static_cast<int64_t>(h) * DV + v) * DC + kc * 32 + g * 8);
+    }
+  };
+  if constexpr (kEarlyW) load_w();
 
   // (2) this wave's part of its sequence's splits
   const int k = w / wps, part = w % wps;
@@ -229,7 +264,8 @@ __global__ __launch_bounds__(kCombWaves * 64) void combine_mfma_kernel(const flo
     } else if (ns <= 8) {
       merge_batch<DC, 8>(part_ml, part_o, base, H, part, wps, 0, ns, lane, M, Ls, acc);
     } else {
-      for (int s0 = 0; s0 < ns; s0 += 16) merge_batch<DC, 16>(part_ml, part_o, base, H, part, wps, s0, ns, lane, M, Ls, acc);
+      for (int s0 = 0; s0 < ns; s0 += kSBMax)
+        merge_batch<DC, kSBMax>(part_ml, part_o, base, H, part, wps, s0, ns, lane, M, Ls, acc);
     }
   }
 #pragma unroll
@@ -263,6 +299,7 @@ __global__ __launch_bounds__(kCombWaves * 64) void combine_mfma_kernel(const flo
   __syncthreads();
 
   // (4) out^T[vt*16 + 4g + r][b0 + r16] for this wave's tile
+  if constexpr (!kEarlyW) load_w();
   if (vt < nvt) {
     f32x4_t o = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll

@@ -414,9 +414,20 @@ extern "C" eg_mla_status eg_mla_decode_planned(const eg_mla_dims* dims, int32_t 
     dim3 grid(d.num_heads, (d.latent_dim + kAbsorbCols - 1) / kAbsorbCols, (batch + kAbsorbRows - 1) / kAbsorbRows);
     const size_t lds = sizeof(float) * (kAbsorbRows * d.head_dim + 4 * kAbsorbRows * kAbsorbCols);
     if (bf && d.head_dim == 128) {
-      dim3 ga(d.num_heads, (batch + kAbsRows - 1) / kAbsRows, (d.latent_dim + kAbsCols - 1) / kAbsCols);
-      hipLaunchKernelGGL(absorb_mfma_kernel<128>, ga, dim3(256), 0, stream, static_cast<const uint16_t*>(q),
-                         static_cast<const uint16_t*>(w_uk), qfull, batch, d.num_heads, d.latent_dim, d.rope_dim);
+      // A W_UK of a few MB is read once per block of sequences: group blocks so
+      // it is read about once; a small one is cheap to re-read, and one block
+      // per work-group spreads the work over more compute units.
+      const size_t wuk_bytes = static_cast<size_t>(d.num_heads) * d.head_dim * d.latent_dim * 2;
+      const bool grouped = wuk_bytes >= (size_t{4} << 20);
+      const int rows = kAbsRows * (grouped ? kAbsBlocks : 1);
+      dim3 ga(d.num_heads, (batch + rows - 1) / rows, (d.latent_dim + kAbsCols - 1) / kAbsCols);
+      if (grouped)
+        hipLaunchKernelGGL((absorb_mfma_kernel<128, kAbsBlocks>), ga, dim3(256), 0, stream,
+                           static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(w_uk), qfull, batch,
+                           d.num_heads, d.latent_dim, d.rope_dim);
+      else
+        hipLaunchKernelGGL((absorb_mfma_kernel<128, 1>), ga, dim3(256), 0, stream, static_cast<const uint16_t*>(q),
+                           static_cast<const uint16_t*>(w_uk), qfull, batch, d.num_heads, d.latent_dim, d.rope_dim);
     } else if (bf) {
       if (set_lds(absorb_kernel<true>, lds) != hipSuccess) return EG_MLA_ERR_HIP;
       hipLaunchKernelGGL(absorb_kernel<true>, grid, dim3(256), lds, stream, q, w_uk, qfull, batch, d.num_heads,
