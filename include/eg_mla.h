@@ -141,6 +141,15 @@ eg_mla_status eg_mla_append(const eg_mla_dims* dims, int32_t n_tokens, int32_t h
  *                 eg_mla_decode_workspace_size(dims, B, max_pages_per_seq, plan)
  *                 bytes, 256-byte aligned; contents need no initialisation
  *   out           [B, H, d_v]  in the storage type
+ *
+ * Arithmetic (bf16 storage, MFMA path): each gated latent is the exact fp32
+ * product of two bf16 values rounded once to bf16; scores and the value sum
+ * are bf16 x bf16 products accumulated in fp32, with the absorbed query
+ * split into bf16 hi + lo (rounded to bf16 for d_c = 512 with 128-head work
+ * items) and the probabilities rounded to bf16; the split merge is fp32 and
+ * the up-projection takes the merged latent as bf16 hi + lo.  The VALU path
+ * computes in fp32.  The call is asynchronous on `stream`; calls that share a
+ * workspace must be ordered (same stream or synchronised).
  * ------------------------------------------------------------------------- */
 size_t eg_mla_decode_workspace_size(const eg_mla_dims* dims, int32_t batch, int32_t max_pages_per_seq,
                                     const eg_mla_plan* plan /* NULL = automatic */);
