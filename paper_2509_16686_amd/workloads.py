@@ -116,7 +116,7 @@ WORKLOADS = [
 ]
 
 # Plain-MLA comparison for the large-batch case: latent 320, all-ones gate.
-MLA_BASELINE_BIGBATCH = WORKLOADS[3].replace(
+MLA_DC320_BIGBATCH = WORKLOADS[3].replace(
     name="mla_bigbatch_b256_h16_dc320_dr64_l2048", latent_dim=320, gate_dim=320,
     gate_all_ones=True, description="plain MLA baseline (d_c=320, all-ones gate), batch 256, context 2048")
 

@@ -45,8 +45,8 @@ def test_workload_full_size_auto_plan(gpu, idx):
     say(f"  max_abs={max_abs:.3e} rel_l2={rel:.3e}")
 
 
-def test_mla_baseline_dc320_all_ones_gate(gpu):
-    wl = W.MLA_BASELINE_BIGBATCH.replace(batch=32)
+def test_plain_mla_dc320_all_ones_gate(gpu):
+    wl = W.MLA_DC320_BIGBATCH.replace(batch=32)
     inp = W.generate(wl)
     say(f"decode {wl.name} (batch 32) auto plan")
     got = gpu_decode(inp)
