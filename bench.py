@@ -42,7 +42,7 @@ def split_kernel_name(wl, path):
     if wl.dtype != "bf16" or path == "valu":
         return "split_valu_kernel"
     if wl.latent_dim == 128 and wl.rope_dim == 64:
-        return "split_tok_kernel"
+        return "split_slice_kernel"
     if wl.latent_dim == 512 and wl.rope_dim == 64 and wl.heads % 128 == 0:
         return "split_heads_kernel"
     if wl.heads % 16 == 0 and wl.rope_dim == 64 and wl.latent_dim in (320, 512):
@@ -134,6 +134,8 @@ def main():
     ap.add_argument("--workload", type=int, default=1, help="index into workloads.WORKLOADS")
     ap.add_argument("--path", choices=["auto", "valu", "mfma"], default="auto")
     ap.add_argument("--split", type=int, default=0, help="tokens per split (0 = automatic)")
+    ap.add_argument("--id-slices", type=int, default=0, choices=[0, 1, 8],
+                    help="token-id slices per split of the d_c=128 kernel (0 = automatic)")
     ap.add_argument("--rotate-bytes", type=float, default=1.0e9)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibration-copy-mib", type=int, default=0,
@@ -176,7 +178,7 @@ def main():
                                      page_table=None if dd0.page_table is None else dd0.page_table.clone(),
                                      max_pages=dd0.max_pages, out=torch.empty_like(dd0.out)))
     path = {"auto": B.PATH_AUTO, "valu": B.PATH_VALU, "mfma": B.PATH_MFMA}[args.path]
-    plan0 = B.make_plan(path, args.split)
+    plan0 = B.make_plan(path, args.split, id_slices=args.id_slices)
     ws_bytes = B.decode_workspace_size(dd0.dims, wl.batch, dd0.max_pages, plan0)
     assert ws_bytes > 0, "no plan for this workload"
     ws = B.alloc_workspace(ws_bytes)
@@ -186,7 +188,7 @@ def main():
 
     ev0 = [hip.event() for _ in range(K)]
     ev1 = [hip.event() for _ in range(K)]
-    plans = [B.make_plan(path, args.split, ev0[k], ev1[k]) for k in range(K)]
+    plans = [B.make_plan(path, args.split, ev0[k], ev1[k], id_slices=args.id_slices) for k in range(K)]
 
     def argset(dd, plan):
         return (ctypes.byref(dd.dims), wl.batch, dd.q.data_ptr(), dd.cache.data_ptr(), dd.ids.data_ptr(),
@@ -256,7 +258,8 @@ def main():
     k_bytes = traffic.main_kernel
     achieved = k_bytes / (k_avg_ms * 1e-3) / 1e9
     # counters were taken on the default workload with the automatic plan only
-    t_bytes = recorded_traffic() if (args.workload == 1 and args.path == "auto" and args.split == 0) else None
+    t_bytes = recorded_traffic() if (args.workload == 1 and args.path == "auto" and args.split == 0
+                                     and args.id_slices == 0) else None
     traffic_gbps = None if t_bytes is None else t_bytes / (k_avg_ms * 1e-3) / 1e9
     tokens_per_s = wl.batch / (ms_per_step * 1e-3)
     log(f"bench: {ms_per_step * 1e3:.2f} us/step, split kernel {k_avg_ms * 1e3:.2f} us "
@@ -279,7 +282,7 @@ def main():
         "config": {"workload": wl.name, "batch": wl.batch, "heads": wl.heads, "head_dim": wl.head_dim,
                    "latent_dim": wl.latent_dim, "rope_dim": wl.rope_dim, "vocab": wl.vocab,
                    "context": wl.seq_len if wl.seq_len else list(wl.seq_len_range), "paged": wl.paged,
-                   "storage": wl.dtype, "path": args.path, "split_tokens": args.split,
+                   "storage": wl.dtype, "path": args.path, "split_tokens": args.split, "id_slices": args.id_slices,
                    "rotating_copies": R},
         "hbm_gbps_call": traffic.total / (ms_per_step * 1e-3) / 1e9,
         "hbm_frac_call": traffic.total / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,

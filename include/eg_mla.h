@@ -91,6 +91,13 @@ typedef struct eg_mla_plan {
    * immediately before and after the kernel. */
   void* split_start_event;
   void* split_stop_event;
+  /* Token-id slices per context split on the MFMA path with d_c = 128 and
+   * d_r = 64: 0 = automatic (currently none), 1 = none, 8 = eight work items
+   * per split, the one run by work-group x taking the tokens whose id is
+   * x mod 8, so that each of the 8 XCDs gathers one eighth of the gate
+   * table.  Other values: EG_MLA_ERR_INVALID_ARG; ignored by the other
+   * kernels. */
+  int32_t id_slices;
 } eg_mla_plan;
 
 /* Human-readable name of a status code (static string, never NULL). */

@@ -34,7 +34,8 @@ class Dims(ctypes.Structure):
 
 class Plan(ctypes.Structure):
     _fields_ = [("path", ctypes.c_int32), ("split_tokens", ctypes.c_int32),
-                ("split_start_event", ctypes.c_void_p), ("split_stop_event", ctypes.c_void_p)]
+                ("split_start_event", ctypes.c_void_p), ("split_stop_event", ctypes.c_void_p),
+                ("id_slices", ctypes.c_int32)]
 
 
 class EgMlaError(RuntimeError):
@@ -88,8 +89,9 @@ def make_dims(*, num_heads, head_dim, v_head_dim, latent_dim, rope_dim, vocab_si
                 latent_dim if gate_dim is None else gate_dim, vocab_size, page_size, softmax_scale, dtype)
 
 
-def make_plan(path: int = PATH_AUTO, split_tokens: int = 0, start_event=None, stop_event=None) -> Plan:
-    return Plan(path, split_tokens, start_event, stop_event)
+def make_plan(path: int = PATH_AUTO, split_tokens: int = 0, start_event=None, stop_event=None,
+              id_slices: int = 0) -> Plan:
+    return Plan(path, split_tokens, start_event, stop_event, id_slices)
 
 
 def _ptr(t) -> Optional[int]:

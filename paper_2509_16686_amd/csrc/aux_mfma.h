@@ -135,11 +135,12 @@ __global__ __launch_bounds__(256) void absorb_mfma_kernel(const uint16_t* __rest
 // and up to 16 sequences per work-group.
 //  1. Waves 0 .. nvt-1 issue the W_UV rows of their 16-row output tile (first
 //     for d_c <= 128; after step 3 for wider latents, to stay in registers).
-//  2. The splits of each sequence are merged online in fp32: with n
-//     sequences in the group, each gets wps = 16 / pow2ceil(n) waves, and wave
-//     p of a sequence merges its splits p, p + wps, ... in batches of 4, 8 or 16
-//     (at most 8 for d_c > 128)
-//     (maxima, sums and partial outputs loaded together) into LDS.
+//  2. The partials of each sequence (`slices` per context split; a partial
+//     of an id slice without tokens has maximum -inf and is skipped) are
+//     merged online in fp32: with n sequences in the group, each gets
+//     wps = 16 / pow2ceil(n) waves, and wave p of a sequence merges its
+//     partials p, p + wps, ... in batches of 4, 8 or 16 (at most 8 for
+//     d_c > 128) (maxima, sums and partial outputs loaded together) into LDS.
 //  3. All threads merge each sequence's wps parts into its latent row o / l.
 //  4. out^T[v][b] = W_UV[h][v][:] . o[b][:] on v_mfma_f32_16x16x32_bf16, the
 //     16 sequences being the 16 columns of the B operand, o split into bf16
@@ -190,13 +191,16 @@ __device__ __forceinline__ void merge_batch(const float* __restrict__ part_ml, c
 #pragma unroll
   for (int u = 0; u < SB; ++u) mb = fmaxf(mb, ml[u].x);  // repeated last split: no effect on the max
   const float Mn = fmaxf(M, mb);
-  const float sc = __builtin_amdgcn_exp2f(M - Mn);  // 0 for the first batch (exp2(-inf))
+  // a partial without tokens has maximum -inf; while every partial so far is
+  // one, nothing is accumulated (and exp2(-inf - -inf) is never formed)
+  const bool live = Mn > -INFINITY;
+  const float sc = live ? __builtin_amdgcn_exp2f(M - Mn) : 1.f;  // 0 for the first live batch (exp2(-inf))
   Ls *= sc;
 #pragma unroll
   for (int j = 0; j < PER; ++j) acc[j] *= sc;
 #pragma unroll
   for (int u = 0; u < SB; ++u) {
-    const float e = s0 + u < ns ? __builtin_amdgcn_exp2f(ml[u].x - Mn) : 0.f;
+    const float e = s0 + u < ns && live ? __builtin_amdgcn_exp2f(ml[u].x - Mn) : 0.f;
     Ls += ml[u].y * e;
 #pragma unroll
     for (int j = 0; j < PER; ++j) acc[j] = fmaf(e, pv[u][j], acc[j]);
@@ -210,7 +214,7 @@ __global__ __launch_bounds__(kCombWaves * 64) void combine_mfma_kernel(const flo
                                                                        const uint16_t* __restrict__ w_uv,
                                                                        const int32_t* __restrict__ seq_lens,
                                                                        uint16_t* __restrict__ out, int B, int H,
-                                                                       int cap, int split, int s_max) {
+                                                                       int cap, int split, int s_max, int slices) {
   constexpr int OS = DC + 4;
   constexpr int PER = DC / 64;  // latent columns per lane
   constexpr int NKC = DC / 32;
@@ -251,14 +255,16 @@ __global__ __launch_bounds__(kCombWaves * 64) void combine_mfma_kernel(const flo
   const int k = w / wps, part = w % wps;
   const int b = b0 + k;
   const int L = (k < nseq) ? clamp_len(seq_lens[b], cap) : 0;
-  const int ns_all = L > 0 ? min((L + split - 1) / split, s_max) : 0;
-  const int ns = ns_all > part ? (ns_all - part + wps - 1) / wps : 0;  // this part's splits
+  // partials of sequence b: `slices` per split; a split below the sequence's
+  // length holds a token, though one of its id slices may hold none
+  const int ns_all = L > 0 ? min((L + split - 1) / split, s_max) * slices : 0;
+  const int ns = ns_all > part ? (ns_all - part + wps - 1) / wps : 0;  // this part's partials
   float M = -INFINITY, Ls = 0.f;
   float acc[PER];
 #pragma unroll
   for (int j = 0; j < PER; ++j) acc[j] = 0.f;
-  if (ns > 0) {  // every split below ns_all holds a token, so its maximum is finite
-    const int64_t base = static_cast<int64_t>(b) * s_max * H + h;  // + s * H
+  if (ns > 0) {
+    const int64_t base = static_cast<int64_t>(b) * s_max * slices * H + h;  // + partial * H
     if (ns <= 4) {
       merge_batch<DC, 4>(part_ml, part_o, base, H, part, wps, 0, ns, lane, M, Ls, acc);
     } else if (ns <= 8) {

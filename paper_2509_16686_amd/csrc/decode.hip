@@ -225,7 +225,7 @@ __global__ __launch_bounds__(kValuThreads) void split_valu_kernel(SplitArgs a) {
 // ---------------------------------------------------------------------------
 }  // namespace egmla
 #include "split_mfma.h"
-#include "split_tok.h"
+#include "split_slice.h"
 #include "split_heads.h"
 namespace egmla {
 
@@ -238,8 +238,11 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
                                                       const float* __restrict__ part_o,
                                                       const void* __restrict__ w_uv,
                                                       const int32_t* __restrict__ seq_lens, void* __restrict__ out,
-                                                      int H, int DC, int DV, int cap, int split, int s_max) {
-  extern __shared__ float smem[];  // o[DC], wgt[s_max]
+                                                      int H, int DC, int DV, int cap, int split, int s_max,
+                                                      int slices) {
+  // s_max splits of `slices` partials each per sequence; a partial without
+  // tokens has maximum -inf and contributes nothing
+  extern __shared__ float smem[];  // o[DC], wgt[s_max * slices]
   float* o_s = smem;
   float* wgt = smem + DC;
   const int h = blockIdx.x, b = blockIdx.y;
@@ -249,7 +252,8 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
     for (int v = threadIdx.x; v < DV; v += blockDim.x) st<BF16>(out, obase + v, 0.f);
     return;
   }
-  const int ns = min((L + split - 1) / split, s_max);
+  const int ns = min((L + split - 1) / split, s_max) * slices;
+  s_max *= slices;
   // split weights exp2(m_s - M) / sum_s l_s exp2(m_s - M), computed by wave 0
   if (threadIdx.x < 64) {
     float M = -INFINITY;
@@ -306,35 +310,43 @@ hipError_t set_lds(K kernel, size_t bytes) {
                              static_cast<int>(bytes));
 }
 
-// Token-split kernel: waves per work-group and units in flight per wave.
-constexpr int kTokWaves = 4;
-constexpr int kTokDepth = 3;
+// Id-sliced kernel: waves per work-group and units in flight per wave.
+constexpr int kSliceWaves = 4;
+constexpr int kSliceDepth = 3;
 
 template <int DC>
 hipError_t launch_combine_dc(dim3 grid, hipStream_t stream, const float* pm, const float* po, const uint16_t* wv,
-                             const int32_t* seq_lens, uint16_t* ov, int B, int H, int cap, int split, int s_max) {
+                             const int32_t* seq_lens, uint16_t* ov, int B, int H, int cap, int split, int s_max,
+                             int slices) {
   const size_t lds = combine_lds_bytes(DC);
   hipError_t e = set_lds(combine_mfma_kernel<DC, 128>, lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((combine_mfma_kernel<DC, 128>), grid, dim3(kCombWaves * 64), lds, stream, pm, po, wv, seq_lens,
-                     ov, B, H, cap, split, s_max);
+                     ov, B, H, cap, split, s_max, slices);
   return hipGetLastError();
 }
 
 hipError_t launch_combine_mfma(int dc, dim3 grid, hipStream_t stream, const float* pm, const float* po,
                                const uint16_t* wv, const int32_t* seq_lens, uint16_t* ov, int B, int H, int cap,
-                               int split, int s_max) {
-  if (dc == 128) return launch_combine_dc<128>(grid, stream, pm, po, wv, seq_lens, ov, B, H, cap, split, s_max);
-  if (dc == 320) return launch_combine_dc<320>(grid, stream, pm, po, wv, seq_lens, ov, B, H, cap, split, s_max);
-  return launch_combine_dc<512>(grid, stream, pm, po, wv, seq_lens, ov, B, H, cap, split, s_max);
+                               int split, int s_max, int slices) {
+  if (dc == 128)
+    return launch_combine_dc<128>(grid, stream, pm, po, wv, seq_lens, ov, B, H, cap, split, s_max, slices);
+  if (dc == 320)
+    return launch_combine_dc<320>(grid, stream, pm, po, wv, seq_lens, ov, B, H, cap, split, s_max, slices);
+  return launch_combine_dc<512>(grid, stream, pm, po, wv, seq_lens, ov, B, H, cap, split, s_max, slices);
 }
 
 // The MFMA split kernels launch with hipExtLaunchKernelGGL so that optional
 // timing events are stamped by the dispatch itself (kernel start and end).
 template <int DC, int DR>
-hipError_t launch_tok(const SplitArgs& a, int nblocks, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
-  hipExtLaunchKernelGGL((split_tok_kernel<DC, DR, kTokWaves, kTokDepth>), dim3(nblocks), dim3(kTokWaves * 64), 0,
-                        stream, ev0, ev1, 0, a);
+hipError_t launch_slice(const SplitArgs& a, int slices, int nblocks, hipStream_t stream, hipEvent_t ev0,
+                        hipEvent_t ev1) {
+  if (slices == kIdSlices)
+    hipExtLaunchKernelGGL((split_slice_kernel<DC, DR, kSliceWaves, kSliceDepth, kIdSlices>), dim3(nblocks * slices),
+                          dim3(kSliceWaves * 64), 0, stream, ev0, ev1, 0, a);
+  else
+    hipExtLaunchKernelGGL((split_slice_kernel<DC, DR, kSliceWaves, kSliceDepth, 1>), dim3(nblocks),
+                          dim3(kSliceWaves * 64), 0, stream, ev0, ev1, 0, a);
   return hipGetLastError();
 }
 
@@ -358,7 +370,10 @@ hipError_t launch_split(const eg_mla_dims& d, const DecodePlan& p, const SplitAr
   if (nblocks64 > 0x7fffffff) return hipErrorInvalidValue;
   const int nblocks = static_cast<int>(nblocks64);
   if (p.path == EG_MLA_PATH_MFMA) {
-    if (tok_kernel_shape(d)) return launch_tok<128, 64>(a, nblocks, stream, ev0, ev1);
+    if (tok_kernel_shape(d)) {
+      if (static_cast<int64_t>(nblocks) * p.slices > 0x7fffffff) return hipErrorInvalidValue;
+      return launch_slice<128, 64>(a, p.slices, nblocks, stream, ev0, ev1);
+    }
     if (heads_kernel_shape(d)) return launch_heads<512, 64>(a, nblocks, stream, ev0, ev1);
     if (d.latent_dim == 320) return launch_mfma<320, 64>(a, nblocks, stream, ev0, ev1);
     if (d.latent_dim == 512) return launch_mfma<512, 64>(a, nblocks, stream, ev0, ev1);
@@ -471,7 +486,7 @@ extern "C" eg_mla_status eg_mla_decode_planned(const eg_mla_dims* dims, int32_t 
   // 3. combine + W_UV
   {
     dim3 grid(d.num_heads, batch);
-    const size_t lds = sizeof(float) * (d.latent_dim + p.s_max);
+    const size_t lds = sizeof(float) * (d.latent_dim + static_cast<size_t>(p.s_max) * p.slices);
     if (lds > 160 * 1024) return EG_MLA_ERR_UNSUPPORTED;
     const bool mfma_comb = bf && d.v_head_dim == 128 &&
                            (d.latent_dim == 128 || d.latent_dim == 320 || d.latent_dim == 512);
@@ -482,16 +497,16 @@ extern "C" eg_mla_status eg_mla_decode_planned(const eg_mla_dims* dims, int32_t 
       const uint16_t* wv = static_cast<const uint16_t*>(w_uv);
       uint16_t* ov = static_cast<uint16_t*>(out);
       if (launch_combine_mfma(d.latent_dim, g2, stream, pm, po, wv, seq_lens, ov, batch, d.num_heads, p.capacity,
-                              p.split_tokens, p.s_max) != hipSuccess)
+                              p.split_tokens, p.s_max, p.slices) != hipSuccess)
         return EG_MLA_ERR_HIP;
     } else if (bf) {
       if (set_lds(combine_kernel<true>, lds) != hipSuccess) return EG_MLA_ERR_HIP;
       hipLaunchKernelGGL(combine_kernel<true>, grid, dim3(256), lds, stream, part_ml, part_o, w_uv, seq_lens, out,
-                         d.num_heads, d.latent_dim, d.v_head_dim, p.capacity, p.split_tokens, p.s_max);
+                         d.num_heads, d.latent_dim, d.v_head_dim, p.capacity, p.split_tokens, p.s_max, p.slices);
     } else {
       if (set_lds(combine_kernel<false>, lds) != hipSuccess) return EG_MLA_ERR_HIP;
       hipLaunchKernelGGL(combine_kernel<false>, grid, dim3(256), lds, stream, part_ml, part_o, w_uv, seq_lens, out,
-                         d.num_heads, d.latent_dim, d.v_head_dim, p.capacity, p.split_tokens, p.s_max);
+                         d.num_heads, d.latent_dim, d.v_head_dim, p.capacity, p.split_tokens, p.s_max, p.slices);
     }
     if (hipGetLastError() != hipSuccess) return EG_MLA_ERR_HIP;
   }

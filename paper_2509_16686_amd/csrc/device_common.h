@@ -59,6 +59,11 @@ __device__ __forceinline__ u32x4_t gate_chunk(u32x4_t lat, u32x4_t gate) {
   return out;
 }
 
+// Largest growth (log2 units) of a head's running maximum that an online
+// softmax absorbs without rescaling its accumulators: probabilities relative
+// to the stale maximum stay below 2^8, far from fp32 overflow.
+constexpr float kLazyRescale = 8.0f;
+
 // Maximum over the four lanes i, i ^ 16, i ^ 32, i ^ 48 (VALU lane swaps).
 __device__ __forceinline__ float max_over_row_groups(float x) {
   const uint32_t u = __float_as_uint(x);

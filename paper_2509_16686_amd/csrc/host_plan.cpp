@@ -68,18 +68,30 @@ eg_mla_status make_decode_plan(const eg_mla_dims& d, int32_t batch, int32_t max_
   }
   p.head_groups = ceil_div(d.num_heads, p.heads_per_group);
 
+  const int req_slices = plan ? plan->id_slices : 0;
+  if (req_slices != 0 && req_slices != 1 && req_slices != kIdSlices) return EG_MLA_ERR_INVALID_ARG;
+  const bool sliced_kernel = p.path == EG_MLA_PATH_MFMA && tok_kernel_shape(d);
+  // automatic: no slices (measured faster on MI355X: a sliced work item must
+  // resolve its token ids before its first cache-row load)
+  p.slices = sliced_kernel && req_slices == kIdSlices ? kIdSlices : 1;
+  const int max_split = sliced_kernel ? kMaxSliceSplitTokens : kMaxSplitTokens;
+
   int split = plan ? plan->split_tokens : 0;
   if (split < 0 || split % kTile != 0) return EG_MLA_ERR_INVALID_ARG;
-  if (p.path == EG_MLA_PATH_MFMA && split > kMaxSplitTokens) return EG_MLA_ERR_UNSUPPORTED;
+  if (p.path == EG_MLA_PATH_MFMA && split > max_split) return EG_MLA_ERR_UNSUPPORTED;
   if (split == 0) {
-    const int64_t work = static_cast<int64_t>(std::max(batch, 1)) * std::max(p.capacity, 1) * p.head_groups;
+    // Work items (splits x slices) to fill the chip: each work item of the
+    // sliced kernel handles 1/slices of its split's tokens.
+    const int64_t work =
+        static_cast<int64_t>(std::max(batch, 1)) * std::max(p.capacity, 1) * p.head_groups * p.slices;
     const int64_t target =
         p.path == EG_MLA_PATH_MFMA && (tok_kernel_shape(d) || heads_kernel_shape(d)) ? kTargetWorkItemsTok : kTargetWorkItems;
     int64_t s = (work + target - 1) / target;
-    s = (s + kTile - 1) / kTile * kTile;
+    const int gran = p.slices > 1 ? 256 : kTile;  // sliced kernel: whole 256-position scan rows
+    s = (s + gran - 1) / gran * gran;
     const int min_split = p.path == EG_MLA_PATH_MFMA ? 256 : 128;
     s = std::max<int64_t>(s, min_split);
-    s = std::min<int64_t>(s, kMaxSplitTokens);
+    s = std::min<int64_t>(s, max_split);
     split = static_cast<int>(s);
   }
   p.split_tokens = split;
@@ -88,7 +100,7 @@ eg_mla_status make_decode_plan(const eg_mla_dims& d, int32_t batch, int32_t max_
   const size_t B = static_cast<size_t>(std::max(batch, 0));
   const size_t H = static_cast<size_t>(d.num_heads);
   const size_t DQ = static_cast<size_t>(d.latent_dim + d.rope_dim);
-  const size_t S = static_cast<size_t>(p.s_max);
+  const size_t S = static_cast<size_t>(p.s_max) * static_cast<size_t>(p.slices);
   size_t off = 0;
   p.off_q = off;
   off = align_up(off + B * H * DQ * 4);

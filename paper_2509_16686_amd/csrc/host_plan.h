@@ -19,6 +19,10 @@ constexpr int kTile = 32;
 // of every token of its split in LDS.
 constexpr int kMaxSplitTokens = 2048;
 constexpr int kMaxSplitTokensDevice = kMaxSplitTokens;
+// Largest split of the id-sliced kernel (it lists the kept tokens of its split in LDS).
+constexpr int kMaxSliceSplitTokens = 4096;
+// Id slices of the sliced kernel: one per XCD.
+constexpr int kIdSlices = 8;
 
 // MFMA kernel instantiations: (latent_dim, rope_dim) pairs with a compiled fast path.
 bool mfma_shape_supported(const eg_mla_dims& d);
@@ -36,10 +40,11 @@ struct DecodePlan {
   int capacity = 0;             // max_pages_per_seq * page_size
   int head_groups = 1;          // work items per (b, split) along heads
   int heads_per_group = 0;
+  int slices = 1;               // partials per (b, split, head group): token-id slices of the sliced kernel
   // workspace layout (byte offsets)
   size_t off_q = 0;     // fp32 [B, H, d_c + d_r]  absorbed query | RoPE query
-  size_t off_ml = 0;    // fp32 [B, s_max, H, 2]   running max (log2 domain), sum
-  size_t off_o = 0;     // fp32 [B, s_max, H, d_c] unnormalised latent outputs
+  size_t off_ml = 0;    // fp32 [B, s_max, slices, H, 2]   running max (log2 domain), sum
+  size_t off_o = 0;     // fp32 [B, s_max, slices, H, d_c] unnormalised latent outputs
   size_t bytes = 0;
 };
 

@@ -59,23 +59,55 @@ SMALL = W.WORKLOADS[1].replace(name="small_h16", batch=4, seq_len=None, seq_len_
                                page_size=64, seed=21)
 
 
-@pytest.mark.parametrize("path", [B.PATH_VALU, B.PATH_MFMA])
-@pytest.mark.parametrize("split", [32, 64, 256, 2048])
-def test_small_ragged_paged_all_splits(gpu, path, split):
+# (path, token-id slices of the d_c = 128 MFMA kernel)
+PATHS = [(B.PATH_VALU, 0), (B.PATH_MFMA, 1), (B.PATH_MFMA, 8)]
+
+
+@pytest.mark.parametrize("path,slices", PATHS)
+@pytest.mark.parametrize("split", [32, 64, 256, 2048, 4096])
+def test_small_ragged_paged_all_splits(gpu, path, slices, split):
     inp = W.generate(SMALL, seq_lens=np.array([1, 33, 777, 900]))
-    say(f"decode small ragged paged path={path} split={split}")
-    got = gpu_decode(inp, B.make_plan(path, split))
-    assert_close(got, oracle_decode(inp), "bf16", f"path {path} split {split}", scaled=True)
+    say(f"decode small ragged paged path={path} slices={slices} split={split}")
+    got = gpu_decode(inp, B.make_plan(path, split, id_slices=slices))
+    assert_close(got, oracle_decode(inp), "bf16", f"path {path} slices {slices} split {split}", scaled=True)
 
 
-@pytest.mark.parametrize("path", [B.PATH_VALU, B.PATH_MFMA])
-def test_edge_lengths(gpu, path):
+@pytest.mark.parametrize("slices", [1, 8])
+def test_id_slices_skewed_and_empty(gpu, slices):
+    # every id in one slice (7 of 8 slices without tokens), and sequences of 1..7 tokens whose
+    # slices are mostly empty: the merge must skip partials without tokens
+    inp = W.generate(SMALL.replace(seed=25, batch=6), seq_lens=np.array([1, 2, 7, 300, 0, 901]))
+    ids_one = inp.token_ids.copy()
+    ids_one[:] = (ids_one // 8) * 8 + 5
+    ids_one[ids_one >= inp.wl.vocab] -= 8
+    for what, ids in (("random ids", inp.token_ids.copy()), ("one slice", ids_one)):
+        inp.token_ids[:] = ids
+        say(f"decode id slices={slices} {what}")
+        got = gpu_decode(inp, B.make_plan(B.PATH_MFMA, 256, id_slices=slices))
+        assert np.all(got[4] == 0)
+        assert_close(got, oracle_decode(inp), "bf16", f"slices {slices} {what}", scaled=True)
+
+
+@pytest.mark.parametrize("paged", [False, True])
+def test_pages_not_multiple_of_four(gpu, paged):
+    # 6-token pages: slots of 4 consecutive positions are not 16-byte aligned, so the
+    # sliced kernel loads ids one by one; contiguous capacity 18 is not a multiple of 4 either
+    wl = SMALL.replace(seed=26, batch=4, page_size=6, paged=paged)
+    inp = W.generate(wl, seq_lens=np.array([13, 5, 1, 12]))
+    for slices in (1, 8):
+        say(f"decode 6-token pages paged={paged} slices={slices}")
+        got = gpu_decode(inp, B.make_plan(B.PATH_MFMA, 32, id_slices=slices))
+        assert_close(got, oracle_decode(inp), "bf16", f"P=6 paged={paged} slices {slices}", scaled=True)
+
+
+@pytest.mark.parametrize("path,slices", PATHS)
+def test_edge_lengths(gpu, path, slices):
     wl = SMALL.replace(batch=6, paged=False, seq_len_range=(1, 320))
     # empty, single token, full capacity, exactly one tile, one past a tile, shorter than the split
     lens = np.array([0, 1, 320, 32, 33, 100])
     inp = W.generate(wl, seq_lens=lens)
-    say(f"decode edge lengths {lens.tolist()} path={path}")
-    got = gpu_decode(inp, B.make_plan(path, 128))
+    say(f"decode edge lengths {lens.tolist()} path={path} slices={slices}")
+    got = gpu_decode(inp, B.make_plan(path, 128, id_slices=slices))
     ref = oracle_decode(inp)
     assert np.all(got[0] == 0)
     assert_close(got, ref, "bf16", "edge lengths", scaled=True)
@@ -134,10 +166,10 @@ def test_paged_equals_contiguous_bitwise(gpu):
             paged.latent_cache[dst] = inp.latent_cache[src]
             paged.token_ids[dst] = inp.token_ids[src]
     paged.page_table = pt
-    for path in (B.PATH_VALU, B.PATH_MFMA):
-        say(f"decode paged vs contiguous path={path}")
-        a = gpu_decode(inp, B.make_plan(path, 96))
-        b = gpu_decode(paged, B.make_plan(path, 96))
+    for path, slices in PATHS:
+        say(f"decode paged vs contiguous path={path} slices={slices}")
+        a = gpu_decode(inp, B.make_plan(path, 96, id_slices=slices))
+        b = gpu_decode(paged, B.make_plan(path, 96, id_slices=slices))
         assert np.array_equal(a, b)
 
 
@@ -155,9 +187,10 @@ def test_repeatable_bitwise(gpu):
 def test_split_choice_changes_result_within_tolerance(gpu):
     inp = full_inputs(2)
     ref = full_ref(2)
-    for split in (256, 1024, 2048):
-        say(f"decode longctx split={split}")
-        assert_close(gpu_decode(inp, B.make_plan(B.PATH_MFMA, split)), ref, "bf16", f"split {split}")
+    for split, slices in ((256, 1), (1024, 1), (2048, 1), (256, 8), (1024, 8), (4096, 8)):
+        say(f"decode longctx split={split} slices={slices}")
+        assert_close(gpu_decode(inp, B.make_plan(B.PATH_MFMA, split, id_slices=slices)), ref, "bf16",
+                     f"split {split} slices {slices}")
     say("decode longctx VALU path")
     assert_close(gpu_decode(inp, B.make_plan(B.PATH_VALU, 0)), ref, "bf16", "valu")
 
