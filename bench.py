@@ -32,7 +32,7 @@ HBM_PEAK_GBPS = 8000.0
 REPO = os.path.dirname(os.path.abspath(__file__))
 # Calibrated FETCH_SIZE + WRITE_SIZE counters of the split kernel on the default workload,
 # valid only while the kernel's sources hash to the recorded value.
-TRAFFIC_PROFILE = os.path.join(REPO, "profiles", "split_tok_b32_h16_dc128_dr64_l4096_traffic.md")
+TRAFFIC_PROFILE = os.path.join(REPO, "profiles", "split_slice_b32_h16_dc128_dr64_l4096_traffic.md")
 
 
 
