@@ -33,6 +33,27 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
+PROBE = os.path.join(PKG, "stream_probe")
+
+
+def build_probe(verbose: bool = False) -> str:
+    """Compiles the streaming-read reference (csrc/stream_probe.hip, not part of the library)."""
+    fd, tmp = tempfile.mkstemp(dir=PKG, prefix=".stream_probe.")
+    os.close(fd)
+    flags = [f for f in HIPCC_FLAGS if f not in ("-fPIC", "-shared")]
+    cmd = [hipcc(), *flags, os.path.join(CSRC, "stream_probe.hip"), "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        os.unlink(tmp)
+        sys.stderr.write(r.stdout + r.stderr)
+        raise RuntimeError(f"hipcc failed with exit code {r.returncode}")
+    os.chmod(tmp, 0o755)
+    os.replace(tmp, PROBE)
+    return PROBE
+
+
 def build(verbose: bool = False) -> str:
     """Compiles every source into libegmla.so next to this file; returns its path."""
     srcs = [os.path.join(CSRC, s) for s in SOURCES]
@@ -57,3 +78,4 @@ def build(verbose: bool = False) -> str:
 
 if __name__ == "__main__":
     print(build(verbose=True))
+    print(build_probe(verbose=True))
