@@ -335,4 +335,115 @@ __global__ __launch_bounds__(kCombWaves * 64) void combine_mfma_kernel(const flo
   }
 }
 
+// ---------------------------------------------------------------------------
+// Merge on MFMA with small work-groups: grid (H, ceil(B / 4)), 256 threads,
+// one head and up to 4 sequences per work-group.  For batches whose partials
+// fit one merge batch per sequence, many small work-groups finish sooner than
+// 16-wave ones.  Wave w merges sequence b0 + w (every partial of it: `slices`
+// per context split) online in fp32 and writes its row o / l to LDS; then
+// out^T[v][b] = W_UV[h][v][:] . o[b][:] on v_mfma_f32_16x16x32_bf16, wave w
+// taking output tiles w, w + 4, ... of 16 rows, the merged rows as the B
+// operand's first 4 columns (bf16 hi + lo).  The W_UV rows are loaded first;
+// `wait(b)` is called by each wave before it loads the partials of its
+// sequence (nothing to wait for in a kernel of its own).
+// ---------------------------------------------------------------------------
+constexpr int kComb4Seq = 4;
+template <int DC>
+constexpr int combine4_lds_bytes() { return kComb4Seq * (DC + 4) * 4; }
+
+template <int DC, int DV, typename Wait>
+__device__ __forceinline__ void combine4_block(const float* __restrict__ part_ml, const float* __restrict__ part_o,
+                                               const uint16_t* __restrict__ w_uv,
+                                               const int32_t* __restrict__ seq_lens, uint16_t* __restrict__ out,
+                                               int B, int H, int cap, int split, int s_max, int slices, int h,
+                                               int b0, float* o_s, Wait wait) {
+  constexpr int OS = DC + 4;
+  constexpr int PER = DC / 64;
+  constexpr int NKC = DC / 32;
+  constexpr int nvt = (DV + 15) / 16;
+  constexpr int TPW = (nvt + 3) / 4;  // output tiles per wave
+  const int tid = threadIdx.x, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int nseq = min(kComb4Seq, B - b0);
+
+  // (1) this wave's W_UV rows
+  u32x4_t wa[TPW][NKC];
+#pragma unroll
+  for (int t = 0; t < TPW; ++t) {
+    const int vt = w + 4 * t;
+    const int v = min(vt * 16 + r16, DV - 1);
+#pragma unroll
+    for (int kc = 0; kc < NKC; ++kc)
+      wa[t][kc] = *reinterpret_cast<const u32x4_t*>(w_uv + (static_cast<int64_t>(h) * DV + v) * DC + kc * 32 + g * 8);
+  }
+  // (2) wave w merges sequence b0 + w
+  {
+    const int b = b0 + w;
+    const int L = w < nseq ? clamp_len(seq_lens[b], cap) : 0;
+    const int ns = L > 0 ? min((L + split - 1) / split, s_max) * slices : 0;
+    float M = -INFINITY, Ls = 0.f;
+    float acc[PER];
+#pragma unroll
+    for (int j = 0; j < PER; ++j) acc[j] = 0.f;
+    if (w < nseq) wait(b);
+    if (ns > 0) {
+      const int64_t base = static_cast<int64_t>(b) * s_max * slices * H + h;
+      if (ns <= 8) {
+        merge_batch<DC, 8>(part_ml, part_o, base, H, 0, 1, 0, ns, lane, M, Ls, acc);
+      } else {
+        for (int s0 = 0; s0 < ns; s0 += 16)
+          merge_batch<DC, 16>(part_ml, part_o, base, H, 0, 1, s0, ns, lane, M, Ls, acc);
+      }
+    }
+    const float inv = Ls > 0.f ? 1.f / Ls : 0.f;  // a sequence with tokens has Ls >= 1
+#pragma unroll
+    for (int j = 0; j < PER; ++j) o_s[w * OS + comb_dim<DC>(lane, j)] = acc[j] * inv;
+  }
+  __syncthreads();
+  // (3) out^T[vt*16 + 4g + r][b0 + r16] for this wave's tiles
+#pragma unroll
+  for (int t = 0; t < TPW; ++t) {
+    const int vt = w + 4 * t;
+    if (vt >= nvt) continue;
+    f32x4_t o = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kc = 0; kc < NKC; ++kc) {
+      float x[8];
+      if (r16 < kComb4Seq) {
+        const float4 x0 = *reinterpret_cast<const float4*>(o_s + r16 * OS + kc * 32 + g * 8);
+        const float4 x1 = *reinterpret_cast<const float4*>(o_s + r16 * OS + kc * 32 + g * 8 + 4);
+        x[0] = x0.x; x[1] = x0.y; x[2] = x0.z; x[3] = x0.w; x[4] = x1.x; x[5] = x1.y; x[6] = x1.z; x[7] = x1.w;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[e] = 0.f;
+      }
+      bf16x8_t hi, lo;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        hi[e] = static_cast<__bf16>(x[e]);
+        lo[e] = static_cast<__bf16>(x[e] - static_cast<float>(hi[e]));
+      }
+      const bf16x8_t av = __builtin_bit_cast(bf16x8_t, wa[t][kc]);
+      o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, hi, o, 0, 0, 0);
+      o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, lo, o, 0, 0, 0);
+    }
+    if (r16 < nseq) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int vv = vt * 16 + 4 * g + r;
+        if (vv < DV) out[(static_cast<int64_t>(b0 + r16) * H + h) * DV + vv] = f32_to_bf16(o[r]);
+      }
+    }
+  }
+}
+template <int DC, int DV>
+__global__ __launch_bounds__(256) void combine4_kernel(const float* __restrict__ part_ml, const float* __restrict__ part_o,
+                                                       const uint16_t* __restrict__ w_uv, const int32_t* __restrict__ seq_lens,
+                                                       uint16_t* __restrict__ out, int B, int H, int cap, int split,
+                                                       int s_max, int slices) {
+  __shared__ __attribute__((aligned(16))) float o_s[kComb4Seq * (DC + 4)];
+  combine4_block<DC, DV>(part_ml, part_o, w_uv, seq_lens, out, B, H, cap, split, s_max, slices, blockIdx.x,
+                         blockIdx.y * kComb4Seq, o_s, [](int) {});
+}
+
 }  // namespace egmla

@@ -318,6 +318,16 @@ template <int DC>
 hipError_t launch_combine_dc(dim3 grid, hipStream_t stream, const float* pm, const float* po, const uint16_t* wv,
                              const int32_t* seq_lens, uint16_t* ov, int B, int H, int cap, int split, int s_max,
                              int slices) {
+  // Small work-groups when every sequence's partials fit one merge batch and
+  // the grid stays within two work-groups per compute unit (measured faster
+  // there; many partials per sequence, or many work-groups, favour the
+  // 16-wave kernel).
+  const int64_t small_wg = static_cast<int64_t>(H) * ((B + kComb4Seq - 1) / kComb4Seq);
+  if (static_cast<int64_t>(s_max) * slices <= 8 && small_wg <= 512) {
+    hipLaunchKernelGGL((combine4_kernel<DC, 128>), dim3(H, (B + kComb4Seq - 1) / kComb4Seq), dim3(256), 0, stream,
+                       pm, po, wv, seq_lens, ov, B, H, cap, split, s_max, slices);
+    return hipGetLastError();
+  }
   const size_t lds = combine_lds_bytes(DC);
   hipError_t e = set_lds(combine_mfma_kernel<DC, 128>, lds);
   if (e != hipSuccess) return e;
