@@ -7,10 +7,11 @@ namespace egmla {
 
 // ---------------------------------------------------------------------------
 // Absorption on MFMA: qfull[b, h, c] = sum_k q^C[b, h, k] W_UK[h, k, c] for
-// BLOCKS (1..4) blocks of 16 sequences x 128 latent columns per work-group
-// (grid H x ceil(B / (16 blocks)) x ceil(DC/128), 256 threads), plus the q^R
-// copy.  More blocks per work-group read W_UK fewer times; fewer spread a
-// small batch over more compute units.
+// BLOCKS (1..4) blocks of 16 sequences x COLS (32 or 128) latent columns per
+// work-group (grid H x ceil(B / (16 blocks)) x ceil(DC/COLS), 256 threads),
+// plus the q^R copy.  More blocks per work-group read W_UK fewer times; fewer
+// blocks and narrower column slices spread a small batch over more compute
+// units.
 // W_UK[h][:, c-block] is read once per work-group with 16-byte row loads and
 // stored row-major in LDS; the B operand (8 consecutive k of one column) is
 // two ds_read_b64_tr_b16, whose 16-lane transpose hands lane n the column n
@@ -21,33 +22,37 @@ namespace egmla {
 // ---------------------------------------------------------------------------
 constexpr int kAbsRows = 16;    // sequences per MFMA row block
 constexpr int kAbsBlocks = 4;   // row blocks per work-group, at most
-constexpr int kAbsCols = 128;
+constexpr int kAbsCols = 128;     // latent columns per work-group, at most
+constexpr int kAbsColsNarrow = 32;
+// Below this many work-groups the absorption takes the narrow column slices.
+constexpr int kAbsMinWorkGroups = 128;
 
-template <int DH, int BLOCKS>
+template <int DH, int BLOCKS, int COLS>
 __global__ __launch_bounds__(256) void absorb_mfma_kernel(const uint16_t* __restrict__ q,
                                                           const uint16_t* __restrict__ w_uk,
                                                           float* __restrict__ qfull, int B, int H, int DC, int DR) {
   static_assert(BLOCKS >= 1 && BLOCKS <= kAbsBlocks, "row blocks per work-group");
-  constexpr int RS = kAbsCols + 8;  // padded LDS row (bf16 elements)
+  static_assert(COLS % 16 == 0 && COLS <= 128, "latent columns per work-group");
+  constexpr int RS = COLS + 8;  // padded LDS row (bf16 elements)
   constexpr int NK = DH / 32;
   __shared__ __attribute__((aligned(16))) uint16_t wrm[DH * RS];  // [k][c], row-major
   constexpr int ROWS = kAbsRows * BLOCKS;  // sequences of this work-group
   const int h = blockIdx.x;
   const int b0 = blockIdx.y * ROWS;
-  const int c0 = blockIdx.z * kAbsCols;
-  const int nc = min(kAbsCols, DC - c0);
+  const int c0 = blockIdx.z * COLS;
+  const int nc = min(COLS, DC - c0);
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
   const int DQin = DH + DR, DQ = DC + DR;
 
   // (1) issue every load: this thread's W rows (16 B = 8 columns each), its A
   // operand chunks for every row block, and its RoPE query values
-  constexpr int kRowsPerPass = 256 / (kAbsCols / 8);  // 16 rows of 128 columns per pass
+  constexpr int kRowsPerPass = 256 / (COLS / 8);  // e.g. 16 rows of 128 columns per pass
   constexpr int kPasses = (DH + kRowsPerPass - 1) / kRowsPerPass;
-  const int cc = (tid % (kAbsCols / 8)) * 8;  // first of this thread's 8 columns
+  const int cc = (tid % (COLS / 8)) * 8;  // first of this thread's 8 columns
   u32x4_t wv[kPasses];
 #pragma unroll
   for (int p = 0; p < kPasses; ++p) {
-    const int k = p * kRowsPerPass + tid / (kAbsCols / 8);
+    const int k = p * kRowsPerPass + tid / (COLS / 8);
     const int kk = min(k, DH - 1);
     const int c = min(c0 + cc, DC - 8);
     wv[p] = *reinterpret_cast<const u32x4_t*>(w_uk + (static_cast<int64_t>(h) * DH + kk) * DC + c);
@@ -77,7 +82,7 @@ __global__ __launch_bounds__(256) void absorb_mfma_kernel(const uint16_t* __rest
   // (2) W rows into LDS as loaded (columns past DC hold unused values)
 #pragma unroll
   for (int p = 0; p < kPasses; ++p) {
-    const int k = p * kRowsPerPass + tid / (kAbsCols / 8);
+    const int k = p * kRowsPerPass + tid / (COLS / 8);
     if (k < DH) *reinterpret_cast<u32x4_t*>(wrm + k * RS + cc) = wv[p];
   }
   __syncthreads();

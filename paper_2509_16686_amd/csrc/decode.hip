@@ -445,14 +445,23 @@ extern "C" eg_mla_status eg_mla_decode_planned(const eg_mla_dims* dims, int32_t 
       const size_t wuk_bytes = static_cast<size_t>(d.num_heads) * d.head_dim * d.latent_dim * 2;
       const bool grouped = wuk_bytes >= (size_t{4} << 20);
       const int rows = kAbsRows * (grouped ? kAbsBlocks : 1);
-      dim3 ga(d.num_heads, (batch + rows - 1) / rows, (d.latent_dim + kAbsCols - 1) / kAbsCols);
+      const int row_blocks = (batch + rows - 1) / rows;
+      // a small grid takes narrower column slices: more work-groups, each
+      // with less of W_UK to load (measured faster for B32 H16, slower for B256)
+      const bool narrow = !grouped && d.num_heads * row_blocks < kAbsMinWorkGroups;
+      const int cols = narrow ? kAbsColsNarrow : kAbsCols;
+      dim3 ga(d.num_heads, row_blocks, (d.latent_dim + cols - 1) / cols);
+      const uint16_t* q16 = static_cast<const uint16_t*>(q);
+      const uint16_t* wuk16 = static_cast<const uint16_t*>(w_uk);
       if (grouped)
-        hipLaunchKernelGGL((absorb_mfma_kernel<128, kAbsBlocks>), ga, dim3(256), 0, stream,
-                           static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(w_uk), qfull, batch,
-                           d.num_heads, d.latent_dim, d.rope_dim);
+        hipLaunchKernelGGL((absorb_mfma_kernel<128, kAbsBlocks, kAbsCols>), ga, dim3(256), 0, stream, q16, wuk16,
+                           qfull, batch, d.num_heads, d.latent_dim, d.rope_dim);
+      else if (narrow)
+        hipLaunchKernelGGL((absorb_mfma_kernel<128, 1, kAbsColsNarrow>), ga, dim3(256), 0, stream, q16, wuk16, qfull,
+                           batch, d.num_heads, d.latent_dim, d.rope_dim);
       else
-        hipLaunchKernelGGL((absorb_mfma_kernel<128, 1>), ga, dim3(256), 0, stream, static_cast<const uint16_t*>(q),
-                           static_cast<const uint16_t*>(w_uk), qfull, batch, d.num_heads, d.latent_dim, d.rope_dim);
+        hipLaunchKernelGGL((absorb_mfma_kernel<128, 1, kAbsCols>), ga, dim3(256), 0, stream, q16, wuk16, qfull, batch,
+                           d.num_heads, d.latent_dim, d.rope_dim);
     } else if (bf) {
       if (set_lds(absorb_kernel<true>, lds) != hipSuccess) return EG_MLA_ERR_HIP;
       hipLaunchKernelGGL(absorb_kernel<true>, grid, dim3(256), lds, stream, q, w_uk, qfull, batch, d.num_heads,
