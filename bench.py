@@ -33,6 +33,10 @@ REPO = os.path.dirname(os.path.abspath(__file__))
 # Calibrated FETCH_SIZE + WRITE_SIZE counters of the split kernel on the default workload,
 # valid only while the kernel's sources hash to the recorded value.
 TRAFFIC_PROFILE = os.path.join(REPO, "profiles", "split_slice_b32_h16_dc128_dr64_l4096_traffic.md")
+# Streaming-read reference (csrc/stream_probe.hip): context for the roofline, not a target.
+STREAM_PROFILE = os.path.join(REPO, "profiles", "stream_read_ceiling.md")
+# Layers of the paper's largest model (App. A), for an indicative whole-model rate.
+MODEL_LAYERS = 24
 
 
 
@@ -102,6 +106,30 @@ class Hip:
         self.L.hipEventDestroy(e)
 
 
+def cpu_model():
+    """The host CPU's model name, as the kernel reports it."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def recorded_stream_ceiling(mib=60):
+    """GB/s of the streaming-read reference program for a launch of `mib` MiB (best work-group
+    count), from its committed summary; None when missing."""
+    try:
+        for line in open(STREAM_PROFILE):
+            cells = [c.strip() for c in line.strip().strip("|").split("|")]
+            if len(cells) >= 4 and cells[0] == str(mib):
+                return float(cells[3])
+    except (OSError, ValueError):
+        pass
+    return None
+
+
 def cpu_baseline(inp, seconds):
     """The fp64 oracle as it stands, timed on the host over whole batches."""
     from oracle import eg_mla_oracle as orc
@@ -123,7 +151,8 @@ def cpu_baseline(inp, seconds):
             break
     return {"value": wl.batch * reps / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
             "sample": f"{reps} full decode steps of the same workload ({wl.batch} sequences each), "
-                      f"{el:.1f} s, numpy fp64 with {threads} BLAS threads"}
+                      f"{el:.1f} s, numpy fp64 with {threads} BLAS threads",
+            "cpu_model": cpu_model(), "host_cpus": len(os.sched_getaffinity(0))}
 
 
 def main():
@@ -286,6 +315,10 @@ def main():
                    "rotating_copies": R},
         "hbm_gbps_call": traffic.total / (ms_per_step * 1e-3) / 1e9,
         "hbm_frac_call": traffic.total / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+        # estimate, not a measurement: every layer of a 24-layer model taking one such call
+        "model_tokens_per_s_estimate": tokens_per_s / MODEL_LAYERS,
+        # context: a plain streaming read of ~60 MiB in one launch (committed reference profile)
+        "stream_read_ceiling_gbps": recorded_stream_ceiling(),
         "roofline": {"bound": "hbm", "kernel": split_kernel_name(wl, args.path),
                      "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic_gbps,
