@@ -48,7 +48,7 @@ def split_kernel_name(wl, path):
     if wl.latent_dim == 128 and wl.rope_dim == 64:
         return "split_slice_kernel"
     if wl.latent_dim == 512 and wl.rope_dim == 64 and wl.heads % 128 == 0:
-        return "split_heads_kernel"
+        return "split_wide_kernel"
     if wl.heads % 16 == 0 and wl.rope_dim == 64 and wl.latent_dim in (320, 512):
         return "split_mfma_kernel"
     return "split_valu_kernel"

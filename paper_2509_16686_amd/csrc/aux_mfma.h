@@ -219,7 +219,8 @@ __global__ __launch_bounds__(kCombWaves * 64) void combine_mfma_kernel(const flo
                                                                        const uint16_t* __restrict__ w_uv,
                                                                        const int32_t* __restrict__ seq_lens,
                                                                        uint16_t* __restrict__ out, int B, int H,
-                                                                       int cap, int split, int s_max, int slices) {
+                                                                       int cap, int split, int s_max, int slices,
+                                                                       const int2* __restrict__ seq_rows) {
   constexpr int OS = DC + 4;
   constexpr int PER = DC / 64;  // latent columns per lane
   constexpr int NKC = DC / 32;
@@ -260,16 +261,18 @@ __global__ __launch_bounds__(kCombWaves * 64) void combine_mfma_kernel(const flo
   const int k = w / wps, part = w % wps;
   const int b = b0 + k;
   const int L = (k < nseq) ? clamp_len(seq_lens[b], cap) : 0;
-  // partials of sequence b: `slices` per split; a split below the sequence's
-  // length holds a token, though one of its id slices may hold none
-  const int ns_all = L > 0 ? min((L + split - 1) / split, s_max) * slices : 0;
+  // partials of sequence b: `slices` per split (a split below the sequence's
+  // length holds a token, though one of its id slices may hold none), or the
+  // rows seq_rows[b] lists (balanced schedule)
+  const int ns_all = L <= 0 ? 0 : seq_rows ? seq_rows[b].y : min((L + split - 1) / split, s_max) * slices;
   const int ns = ns_all > part ? (ns_all - part + wps - 1) / wps : 0;  // this part's partials
   float M = -INFINITY, Ls = 0.f;
   float acc[PER];
 #pragma unroll
   for (int j = 0; j < PER; ++j) acc[j] = 0.f;
   if (ns > 0) {
-    const int64_t base = static_cast<int64_t>(b) * s_max * slices * H + h;  // + partial * H
+    const int64_t row0 = seq_rows ? seq_rows[b].x : static_cast<int64_t>(b) * s_max * slices;
+    const int64_t base = row0 * H + h;  // + partial * H
     if (ns <= 4) {
       merge_batch<DC, 4>(part_ml, part_o, base, H, part, wps, 0, ns, lane, M, Ls, acc);
     } else if (ns <= 8) {

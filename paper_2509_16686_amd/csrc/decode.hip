@@ -14,6 +14,7 @@
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cfloat>
 #include <cmath>
 
@@ -99,8 +100,10 @@ struct SplitArgs {
   const void* gate;           // [V, DC]
   const int32_t* seq_lens;    // [B]
   const int32_t* page_table;  // [B, max_pages] or null
-  float* part_ml;             // [B, s_max, H, 2]
-  float* part_o;              // [B, s_max, H, DC]
+  float* part_ml;             // [rows, H, 2]   rows: B * s_max, or the balanced schedule's rows
+  float* part_o;              // [rows, H, DC]
+  const int64_t* sched_hdr;   // balanced schedule (wide kernel): total tokens, work-groups
+  const int2* wg_start;       // balanced schedule: (sequence, offset) where each work-group starts
   int64_t num_slots;
   int B, H, DC, DR, P, max_pages, V, cap, split, s_max, groups, hpg;
   float scale_log2;           // softmax scale * log2(e)
@@ -226,7 +229,7 @@ __global__ __launch_bounds__(kValuThreads) void split_valu_kernel(SplitArgs a) {
 }  // namespace egmla
 #include "split_mfma.h"
 #include "split_slice.h"
-#include "split_heads.h"
+#include "split_wide.h"
 namespace egmla {
 
 // ---------------------------------------------------------------------------
@@ -239,30 +242,31 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
                                                       const void* __restrict__ w_uv,
                                                       const int32_t* __restrict__ seq_lens, void* __restrict__ out,
                                                       int H, int DC, int DV, int cap, int split, int s_max,
-                                                      int slices) {
-  // s_max splits of `slices` partials each per sequence; a partial without
-  // tokens has maximum -inf and contributes nothing
-  extern __shared__ float smem[];  // o[DC], wgt[s_max * slices]
+                                                      int slices, const int2* __restrict__ seq_rows) {
+  // s_max splits of `slices` partials each per sequence, or (balanced
+  // schedule) the rows seq_rows[b] lists; a partial without tokens has
+  // maximum -inf and contributes nothing
+  extern __shared__ float smem[];  // o[DC], wgt[partials of one sequence]
   float* o_s = smem;
   float* wgt = smem + DC;
   const int h = blockIdx.x, b = blockIdx.y;
   const int L = clamp_len(seq_lens[b], cap);
   const int64_t obase = (static_cast<int64_t>(b) * H + h) * DV;
-  if (L == 0) {
+  const int ns = L == 0 ? 0 : seq_rows ? seq_rows[b].y : min((L + split - 1) / split, s_max) * slices;
+  if (ns == 0) {
     for (int v = threadIdx.x; v < DV; v += blockDim.x) st<BF16>(out, obase + v, 0.f);
     return;
   }
-  const int ns = min((L + split - 1) / split, s_max) * slices;
-  s_max *= slices;
+  const int64_t row0 = seq_rows ? seq_rows[b].x : static_cast<int64_t>(b) * s_max * slices;
   // split weights exp2(m_s - M) / sum_s l_s exp2(m_s - M), computed by wave 0
   if (threadIdx.x < 64) {
     float M = -INFINITY;
     for (int sidx = threadIdx.x; sidx < ns; sidx += 64)
-      M = fmaxf(M, part_ml[((static_cast<int64_t>(b) * s_max + sidx) * H + h) * 2]);
+      M = fmaxf(M, part_ml[((row0 + sidx) * H + h) * 2]);
     M = wave_max(M);
     float Ls = 0.f;
     for (int sidx = threadIdx.x; sidx < ns; sidx += 64) {
-      const int64_t k = ((static_cast<int64_t>(b) * s_max + sidx) * H + h) * 2;
+      const int64_t k = ((row0 + sidx) * H + h) * 2;
       const float e = exp2f(part_ml[k] - M);
       wgt[sidx] = e;
       Ls += part_ml[k + 1] * e;
@@ -275,7 +279,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
   for (int c = threadIdx.x; c < DC; c += blockDim.x) {
     float acc = 0.f;
     for (int sidx = 0; sidx < ns; ++sidx)
-      acc = fmaf(wgt[sidx], part_o[((static_cast<int64_t>(b) * s_max + sidx) * H + h) * DC + c], acc);
+      acc = fmaf(wgt[sidx], part_o[((row0 + sidx) * H + h) * DC + c], acc);
     o_s[c] = acc;
   }
   __syncthreads();
@@ -317,13 +321,13 @@ constexpr int kSliceDepth = 2;
 template <int DC>
 hipError_t launch_combine_dc(dim3 grid, hipStream_t stream, const float* pm, const float* po, const uint16_t* wv,
                              const int32_t* seq_lens, uint16_t* ov, int B, int H, int cap, int split, int s_max,
-                             int slices) {
+                             int slices, const int2* seq_rows) {
   // Small work-groups when every sequence's partials fit one merge batch and
   // the grid stays within two work-groups per compute unit (measured faster
   // there; many partials per sequence, or many work-groups, favour the
   // 16-wave kernel).
   const int64_t small_wg = static_cast<int64_t>(H) * ((B + kComb4Seq - 1) / kComb4Seq);
-  if (static_cast<int64_t>(s_max) * slices <= 8 && small_wg <= 512) {
+  if (!seq_rows && static_cast<int64_t>(s_max) * slices <= 8 && small_wg <= 512) {
     hipLaunchKernelGGL((combine4_kernel<DC, 128>), dim3(H, (B + kComb4Seq - 1) / kComb4Seq), dim3(256), 0, stream,
                        pm, po, wv, seq_lens, ov, B, H, cap, split, s_max, slices);
     return hipGetLastError();
@@ -332,18 +336,31 @@ hipError_t launch_combine_dc(dim3 grid, hipStream_t stream, const float* pm, con
   hipError_t e = set_lds(combine_mfma_kernel<DC, 128>, lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((combine_mfma_kernel<DC, 128>), grid, dim3(kCombWaves * 64), lds, stream, pm, po, wv, seq_lens,
-                     ov, B, H, cap, split, s_max, slices);
+                     ov, B, H, cap, split, s_max, slices, seq_rows);
   return hipGetLastError();
 }
 
 hipError_t launch_combine_mfma(int dc, dim3 grid, hipStream_t stream, const float* pm, const float* po,
                                const uint16_t* wv, const int32_t* seq_lens, uint16_t* ov, int B, int H, int cap,
-                               int split, int s_max, int slices) {
+                               int split, int s_max, int slices, const int2* seq_rows) {
   if (dc == 128)
-    return launch_combine_dc<128>(grid, stream, pm, po, wv, seq_lens, ov, B, H, cap, split, s_max, slices);
+    return launch_combine_dc<128>(grid, stream, pm, po, wv, seq_lens, ov, B, H, cap, split, s_max, slices, seq_rows);
   if (dc == 320)
-    return launch_combine_dc<320>(grid, stream, pm, po, wv, seq_lens, ov, B, H, cap, split, s_max, slices);
-  return launch_combine_dc<512>(grid, stream, pm, po, wv, seq_lens, ov, B, H, cap, split, s_max, slices);
+    return launch_combine_dc<320>(grid, stream, pm, po, wv, seq_lens, ov, B, H, cap, split, s_max, slices, seq_rows);
+  return launch_combine_dc<512>(grid, stream, pm, po, wv, seq_lens, ov, B, H, cap, split, s_max, slices, seq_rows);
+}
+
+// Compute units of the current device (cached per device).
+int device_cus() {
+  static int cus[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cus[dev] = n;
+  }
+  return cus[dev];
 }
 
 // The MFMA split kernels launch with hipExtLaunchKernelGGL so that optional
@@ -360,12 +377,15 @@ hipError_t launch_slice(const SplitArgs& a, int slices, int nblocks, hipStream_t
   return hipGetLastError();
 }
 
-template <int DC, int DR>
-hipError_t launch_heads(const SplitArgs& a, int nblocks, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
-  hipExtLaunchKernelGGL((split_heads_kernel<DC, DR>), dim3(nblocks), dim3(HsplitCfg<DC, DR>::NT), 0, stream, ev0,
-                        ev1, 0, a);
+// Balanced head-split kernel: `wgs` work-groups per block of 128 heads.
+hipError_t launch_wide(const SplitArgs& a, int wgs, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
+  hipExtLaunchKernelGGL(split_wide_kernel, dim3(wgs * a.groups), dim3(WideCfg::NT), 0, stream, ev0, ev1, 0, a);
   return hipGetLastError();
 }
+
+// Work-groups per block of 128 heads of the balanced schedule: one work-group
+// per compute unit over all head blocks.
+int wide_groups(int head_groups) { return std::max(1, std::min(kWideMaxGroups, device_cus() / std::max(1, head_groups))); }
 
 template <int DC, int DR>
 hipError_t launch_mfma(const SplitArgs& a, int nblocks, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
@@ -384,7 +404,7 @@ hipError_t launch_split(const eg_mla_dims& d, const DecodePlan& p, const SplitAr
       if (static_cast<int64_t>(nblocks) * p.slices > 0x7fffffff) return hipErrorInvalidValue;
       return launch_slice<128, 64>(a, p.slices, nblocks, stream, ev0, ev1);
     }
-    if (heads_kernel_shape(d)) return launch_heads<512, 64>(a, nblocks, stream, ev0, ev1);
+    if (heads_kernel_shape(d)) return launch_wide(a, wide_groups(a.groups), stream, ev0, ev1);
     if (d.latent_dim == 320) return launch_mfma<320, 64>(a, nblocks, stream, ev0, ev1);
     if (d.latent_dim == 512) return launch_mfma<512, 64>(a, nblocks, stream, ev0, ev1);
     return hipErrorInvalidValue;
@@ -434,6 +454,18 @@ extern "C" eg_mla_status eg_mla_decode_planned(const eg_mla_dims* dims, int32_t 
   float* part_ml = reinterpret_cast<float*>(ws + p.off_ml);
   float* part_o = reinterpret_cast<float*>(ws + p.off_o);
 
+  int64_t* sched_hdr = nullptr;
+  int2* wg_start = nullptr;
+  int2* seq_rows = nullptr;
+  if (p.balanced) {
+    // 0. balanced schedule of the head-split kernel (token ranges per work-group)
+    sched_hdr = reinterpret_cast<int64_t*>(ws + p.off_sched);
+    wg_start = reinterpret_cast<int2*>(ws + p.off_sched + 16);
+    seq_rows = reinterpret_cast<int2*>(ws + p.off_sched + 16 + kWideMaxGroups * 8);
+    hipLaunchKernelGGL(wide_schedule_kernel, dim3(1), dim3(kSchedThreads), 0, stream, seq_lens, batch, p.capacity,
+                       wide_groups(p.head_groups), sched_hdr, wg_start, seq_rows);
+    if (hipGetLastError() != hipSuccess) return EG_MLA_ERR_HIP;
+  }
   // 1. absorption
   {
     dim3 grid(d.num_heads, (d.latent_dim + kAbsorbCols - 1) / kAbsorbCols, (batch + kAbsorbRows - 1) / kAbsorbRows);
@@ -484,6 +516,8 @@ extern "C" eg_mla_status eg_mla_decode_planned(const eg_mla_dims* dims, int32_t 
     a.page_table = page_table;
     a.part_ml = part_ml;
     a.part_o = part_o;
+    a.sched_hdr = sched_hdr;
+    a.wg_start = wg_start;
     a.num_slots = num_slots;
     a.B = batch;
     a.H = d.num_heads;
@@ -505,7 +539,8 @@ extern "C" eg_mla_status eg_mla_decode_planned(const eg_mla_dims* dims, int32_t 
   // 3. combine + W_UV
   {
     dim3 grid(d.num_heads, batch);
-    const size_t lds = sizeof(float) * (d.latent_dim + static_cast<size_t>(p.s_max) * p.slices);
+    const size_t lds = sizeof(float) * (d.latent_dim + (p.balanced ? static_cast<size_t>(kWideMaxGroups)
+                                                                    : static_cast<size_t>(p.s_max) * p.slices));
     if (lds > 160 * 1024) return EG_MLA_ERR_UNSUPPORTED;
     const bool mfma_comb = bf && d.v_head_dim == 128 &&
                            (d.latent_dim == 128 || d.latent_dim == 320 || d.latent_dim == 512);
@@ -516,16 +551,18 @@ extern "C" eg_mla_status eg_mla_decode_planned(const eg_mla_dims* dims, int32_t 
       const uint16_t* wv = static_cast<const uint16_t*>(w_uv);
       uint16_t* ov = static_cast<uint16_t*>(out);
       if (launch_combine_mfma(d.latent_dim, g2, stream, pm, po, wv, seq_lens, ov, batch, d.num_heads, p.capacity,
-                              p.split_tokens, p.s_max, p.slices) != hipSuccess)
+                              p.split_tokens, p.s_max, p.slices, seq_rows) != hipSuccess)
         return EG_MLA_ERR_HIP;
     } else if (bf) {
       if (set_lds(combine_kernel<true>, lds) != hipSuccess) return EG_MLA_ERR_HIP;
       hipLaunchKernelGGL(combine_kernel<true>, grid, dim3(256), lds, stream, part_ml, part_o, w_uv, seq_lens, out,
-                         d.num_heads, d.latent_dim, d.v_head_dim, p.capacity, p.split_tokens, p.s_max, p.slices);
+                         d.num_heads, d.latent_dim, d.v_head_dim, p.capacity, p.split_tokens, p.s_max, p.slices,
+                         seq_rows);
     } else {
       if (set_lds(combine_kernel<false>, lds) != hipSuccess) return EG_MLA_ERR_HIP;
       hipLaunchKernelGGL(combine_kernel<false>, grid, dim3(256), lds, stream, part_ml, part_o, w_uv, seq_lens, out,
-                         d.num_heads, d.latent_dim, d.v_head_dim, p.capacity, p.split_tokens, p.s_max, p.slices);
+                         d.num_heads, d.latent_dim, d.v_head_dim, p.capacity, p.split_tokens, p.s_max, p.slices,
+                         seq_rows);
     }
     if (hipGetLastError() != hipSuccess) return EG_MLA_ERR_HIP;
   }

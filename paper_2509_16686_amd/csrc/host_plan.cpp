@@ -96,18 +96,27 @@ eg_mla_status make_decode_plan(const eg_mla_dims& d, int32_t batch, int32_t max_
   }
   p.split_tokens = split;
   p.s_max = std::max(1, ceil_div(std::max(p.capacity, 1), split));
+  // The head-split kernel balances tokens over its work-groups whatever the
+  // length mix; its split size only caps the token list it stages at a time.
+  p.balanced = p.path == EG_MLA_PATH_MFMA && heads_kernel_shape(d);
+  if (p.balanced && (plan == nullptr || plan->split_tokens == 0)) p.split_tokens = kMaxSplitTokens;
 
   const size_t B = static_cast<size_t>(std::max(batch, 0));
   const size_t H = static_cast<size_t>(d.num_heads);
   const size_t DQ = static_cast<size_t>(d.latent_dim + d.rope_dim);
-  const size_t S = static_cast<size_t>(p.s_max) * static_cast<size_t>(p.slices);
+  const size_t rows = p.balanced ? kWideMaxGroups + B
+                                 : B * static_cast<size_t>(p.s_max) * static_cast<size_t>(p.slices);
   size_t off = 0;
   p.off_q = off;
   off = align_up(off + B * H * DQ * 4);
   p.off_ml = off;
-  off = align_up(off + B * S * H * 2 * 4);
+  off = align_up(off + rows * H * 2 * 4);
   p.off_o = off;
-  off = align_up(off + B * S * H * static_cast<size_t>(d.latent_dim) * 4);
+  off = align_up(off + rows * H * static_cast<size_t>(d.latent_dim) * 4);
+  if (p.balanced) {
+    p.off_sched = off;
+    off = align_up(off + 16 + kWideMaxGroups * 8 + B * 8);
+  }
   p.bytes = std::max<size_t>(off, kAlign);
   *out = p;
   return EG_MLA_OK;

@@ -32,6 +32,9 @@ bool tok_kernel_shape(const eg_mla_dims& d);
 // dimension-split kernel (16 heads per work item).
 bool heads_kernel_shape(const eg_mla_dims& d);
 constexpr int kHeadsPerItemWide = 128;
+// Balanced schedule of the head-split kernel: at most this many work-groups
+// per block of 128 heads (one per compute unit of the device).
+constexpr int kWideMaxGroups = 512;
 
 struct DecodePlan {
   int path = EG_MLA_PATH_VALU;  // resolved: VALU or MFMA
@@ -41,11 +44,13 @@ struct DecodePlan {
   int head_groups = 1;          // work items per (b, split) along heads
   int heads_per_group = 0;
   int slices = 1;               // partials per (b, split, head group): token-id slices of the sliced kernel
+  bool balanced = false;        // head-split kernel: balanced schedule (split_tokens = list chunk)
   // workspace layout (byte offsets)
   size_t off_q = 0;     // fp32 [B, H, d_c + d_r]  absorbed query | RoPE query
-  size_t off_ml = 0;    // fp32 [B, s_max, slices, H, 2]   running max (log2 domain), sum
-  size_t off_o = 0;     // fp32 [B, s_max, slices, H, d_c] unnormalised latent outputs
-  size_t bytes = 0;
+  size_t off_ml = 0;    // fp32 [rows, H, 2]   running max (log2 domain), sum
+  size_t off_o = 0;     // fp32 [rows, H, d_c] unnormalised latent outputs
+  size_t off_sched = 0; // balanced schedule: int64 [2] header, int2 [kWideMaxGroups] starts, int2 [B] rows
+  size_t bytes = 0;     // rows: B * s_max * slices, or kWideMaxGroups + B when balanced
 };
 
 eg_mla_status check_dims(const eg_mla_dims* d);
