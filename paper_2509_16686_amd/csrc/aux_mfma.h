@@ -27,7 +27,9 @@ constexpr int kAbsColsNarrow = 32;
 // Below this many work-groups the absorption takes the narrow column slices.
 constexpr int kAbsMinWorkGroups = 128;
 
-template <int DH, int BLOCKS, int COLS>
+// Q16: the output row is bf16 (round to nearest even) instead of fp32, for the
+// 128-head kernel, which multiplies by a bf16 query.
+template <int DH, int BLOCKS, int COLS, bool Q16 = false>
 __global__ __launch_bounds__(256) void absorb_mfma_kernel(const uint16_t* __restrict__ q,
                                                           const uint16_t* __restrict__ w_uk,
                                                           float* __restrict__ qfull, int B, int H, int DC, int DR) {
@@ -113,7 +115,10 @@ __global__ __launch_bounds__(256) void absorb_mfma_kernel(const uint16_t* __rest
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int b = b0 + rb * kAbsRows + 4 * g + r;
-        if (b < B && c < DC) qfull[(static_cast<int64_t>(b) * H + h) * DQ + c] = acc[rb][r];
+        if (b < B && c < DC) {
+          if constexpr (Q16) reinterpret_cast<uint16_t*>(qfull)[(static_cast<int64_t>(b) * H + h) * DQ + c] = f32_to_bf16(acc[rb][r]);
+          else qfull[(static_cast<int64_t>(b) * H + h) * DQ + c] = acc[rb][r];
+        }
       }
     }
   }
@@ -121,16 +126,23 @@ __global__ __launch_bounds__(256) void absorb_mfma_kernel(const uint16_t* __rest
 #pragma unroll
     for (int rb = 0; rb < BLOCKS; ++rb) {
       const int b = b0 + rb * kAbsRows + rq_row;
-      if (rq_row < kAbsRows && b < B)
-        *reinterpret_cast<float4*>(qfull + (static_cast<int64_t>(b) * H + h) * DQ + DC + rq_col) =
-            make_float4(bf16_lo(rq[rb].x), bf16_hi(rq[rb].x), bf16_lo(rq[rb].y), bf16_hi(rq[rb].y));
+      if (rq_row < kAbsRows && b < B) {
+        if constexpr (Q16)
+          *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(qfull) + (static_cast<int64_t>(b) * H + h) * DQ + DC +
+                                    rq_col) = rq[rb];
+        else
+          *reinterpret_cast<float4*>(qfull + (static_cast<int64_t>(b) * H + h) * DQ + DC + rq_col) =
+              make_float4(bf16_lo(rq[rb].x), bf16_hi(rq[rb].x), bf16_lo(rq[rb].y), bf16_hi(rq[rb].y));
+      }
     }
   } else if (blockIdx.z == 0) {
     for (int i = tid; i < ROWS * DR; i += 256) {
       const int bb = i / DR, r = i % DR;
-      if (b0 + bb < B)
-        qfull[(static_cast<int64_t>(b0 + bb) * H + h) * DQ + DC + r] =
-            bf16_to_f32(q[(static_cast<int64_t>(b0 + bb) * H + h) * DQin + DH + r]);
+      if (b0 + bb < B) {
+        const uint16_t v = q[(static_cast<int64_t>(b0 + bb) * H + h) * DQin + DH + r];
+        if constexpr (Q16) reinterpret_cast<uint16_t*>(qfull)[(static_cast<int64_t>(b0 + bb) * H + h) * DQ + DC + r] = v;
+        else qfull[(static_cast<int64_t>(b0 + bb) * H + h) * DQ + DC + r] = bf16_to_f32(v);
+      }
     }
   }
 }

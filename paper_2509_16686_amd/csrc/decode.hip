@@ -35,7 +35,7 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kAbsorbRows = 16;
 constexpr int kAbsorbCols = 64;
 
-template <bool BF16>
+template <bool BF16, bool Q16 = false>
 __global__ __launch_bounds__(256) void absorb_kernel(const void* __restrict__ q, const void* __restrict__ w_uk,
                                                      float* __restrict__ qfull, int B, int H, int DH, int DC,
                                                      int DR) {
@@ -80,21 +80,23 @@ __global__ __launch_bounds__(256) void absorb_kernel(const void* __restrict__ q,
       float v = 0.f;
 #pragma unroll
       for (int j = 0; j < 4; ++j) v += red[(j * kAbsorbRows + bb) * kAbsorbCols + cc];
-      qfull[(static_cast<int64_t>(b0 + bb) * H + h) * DQ + c0 + cc] = v;
+      if constexpr (Q16) reinterpret_cast<uint16_t*>(qfull)[(static_cast<int64_t>(b0 + bb) * H + h) * DQ + c0 + cc] = f32_to_bf16(v);
+      else qfull[(static_cast<int64_t>(b0 + bb) * H + h) * DQ + c0 + cc] = v;
     }
   }
   if (blockIdx.y == 0) {
     for (int i = tid; i < nb * DR; i += 256) {
       const int bb = i / DR, r = i % DR;
-      qfull[(static_cast<int64_t>(b0 + bb) * H + h) * DQ + DC + r] =
-          ld<BF16>(q, (static_cast<int64_t>(b0 + bb) * H + h) * DQin + DH + r);
+      const float v = ld<BF16>(q, (static_cast<int64_t>(b0 + bb) * H + h) * DQin + DH + r);
+      if constexpr (Q16) reinterpret_cast<uint16_t*>(qfull)[(static_cast<int64_t>(b0 + bb) * H + h) * DQ + DC + r] = f32_to_bf16(v);
+      else qfull[(static_cast<int64_t>(b0 + bb) * H + h) * DQ + DC + r] = v;
     }
   }
 }
 
 // Split-K bookkeeping shared by the split kernels.
 struct SplitArgs {
-  const float* qfull;         // [B, H, DQ]
+  const float* qfull;         // [B, H, DQ] fp32 (bf16 for the balanced head-split kernel)
   const void* cache;          // [num_slots, DQ]
   const int32_t* ids;         // [num_slots]
   const void* gate;           // [V, DC]
@@ -475,7 +477,7 @@ extern "C" eg_mla_status eg_mla_decode_planned(const eg_mla_dims* dims, int32_t 
       // it is read about once; a small one is cheap to re-read, and one block
       // per work-group spreads the work over more compute units.
       const size_t wuk_bytes = static_cast<size_t>(d.num_heads) * d.head_dim * d.latent_dim * 2;
-      const bool grouped = wuk_bytes >= (size_t{4} << 20);
+      const bool grouped = p.balanced || wuk_bytes >= (size_t{4} << 20);
       const int rows = kAbsRows * (grouped ? kAbsBlocks : 1);
       const int row_blocks = (batch + rows - 1) / rows;
       // a small grid takes narrower column slices: more work-groups, each
@@ -485,7 +487,10 @@ extern "C" eg_mla_status eg_mla_decode_planned(const eg_mla_dims* dims, int32_t 
       dim3 ga(d.num_heads, row_blocks, (d.latent_dim + cols - 1) / cols);
       const uint16_t* q16 = static_cast<const uint16_t*>(q);
       const uint16_t* wuk16 = static_cast<const uint16_t*>(w_uk);
-      if (grouped)
+      if (p.balanced)  // the 128-head kernel reads a bf16 query
+        hipLaunchKernelGGL((absorb_mfma_kernel<128, kAbsBlocks, kAbsCols, true>), ga, dim3(256), 0, stream, q16,
+                           wuk16, qfull, batch, d.num_heads, d.latent_dim, d.rope_dim);
+      else if (grouped)
         hipLaunchKernelGGL((absorb_mfma_kernel<128, kAbsBlocks, kAbsCols>), ga, dim3(256), 0, stream, q16, wuk16,
                            qfull, batch, d.num_heads, d.latent_dim, d.rope_dim);
       else if (narrow)
@@ -494,6 +499,10 @@ extern "C" eg_mla_status eg_mla_decode_planned(const eg_mla_dims* dims, int32_t 
       else
         hipLaunchKernelGGL((absorb_mfma_kernel<128, 1, kAbsCols>), ga, dim3(256), 0, stream, q16, wuk16, qfull, batch,
                            d.num_heads, d.latent_dim, d.rope_dim);
+    } else if (bf && p.balanced) {
+      if (set_lds(absorb_kernel<true, true>, lds) != hipSuccess) return EG_MLA_ERR_HIP;
+      hipLaunchKernelGGL((absorb_kernel<true, true>), grid, dim3(256), lds, stream, q, w_uk, qfull, batch,
+                         d.num_heads, d.head_dim, d.latent_dim, d.rope_dim);
     } else if (bf) {
       if (set_lds(absorb_kernel<true>, lds) != hipSuccess) return EG_MLA_ERR_HIP;
       hipLaunchKernelGGL(absorb_kernel<true>, grid, dim3(256), lds, stream, q, w_uk, qfull, batch, d.num_heads,

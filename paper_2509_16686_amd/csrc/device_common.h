@@ -74,6 +74,17 @@ __device__ __forceinline__ float max_over_row_groups(float x) {
   return fmaxf(__uint_as_float(s16[0]), __uint_as_float(s16[1]));
 }
 
+// Sum over the four lanes i, i ^ 16, i ^ 32, i ^ 48 (VALU lane swaps), added
+// in the same order in every lane.
+__device__ __forceinline__ float sum_over_row_groups(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const auto s32 = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  x = __uint_as_float(s32[0]) + __uint_as_float(s32[1]);
+  const uint32_t v = __float_as_uint(x);
+  const auto s16 = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  return __uint_as_float(s16[0]) + __uint_as_float(s16[1]);
+}
+
 // Two fp32 -> packed bf16 pair (lo in bits 0..15), one v_cvt_pk_bf16_f32.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;

@@ -17,11 +17,14 @@
 //
 // Scores.  Wave (hg, dh) computes the partial S^T[token][head] of its 32 heads
 // over its 288 dims with v_mfma_f32_16x16x32_bf16: the A operand (token lane%16,
-// 8 dims) read from the tile, the B operand the absorbed query, rounded to
-// bf16 and held in registers (64 per lane; its RoPE chunk in LDS).  The two waves of a head group
+// 8 dims) read from the tile, the B operand the absorbed query (written in
+// bf16 by the absorption) held in registers (64 per lane; its RoPE chunk in
+// LDS).  The two waves of a head group
 // exchange their partial sums through LDS; both add them in the same order, so
 // both hold the same scores and run the same online softmax (log2 domain,
-// lazy rescale).
+// lazy rescale).  The exchange synchronises only the two waves of the pair
+// (a flag in LDS), so pairs drift apart and one pair's softmax overlaps
+// another pair's score products on the same SIMDs.
 //
 // Values.  Wave (hg, dh) accumulates O^T[dim][head] for its 32 heads and its
 // 256 latent dims on v_mfma_f32_32x32x16_bf16 (128 accumulators per lane).  The
@@ -39,27 +42,25 @@
 
 namespace egmla {
 
-// LDS DMA of 16 bytes per lane: lane l's bytes land at LDS byte address
-// lds_base + 16 l (M0 holds lds_base; one wait state separates its write from
-// the DMA).  The instruction is not visible to the compiler's wait counters:
-// the caller waits for it with s_waitcnt vmcnt before reading the
-// destination, and before the work-group exits.
-__device__ __forceinline__ void lds_dma16(const void* gptr, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds_base), "v"(gptr)
-               : "memory");
-}
-// The same with a wave-uniform base address and a per-lane 32-bit byte offset.
+// LDS DMA of 16 bytes per lane from sbase + voff: lane l's bytes land at LDS
+// byte address lds_base + 16 l (M0 holds lds_base; one wait state separates
+// its write from the DMA).  The instruction is not visible to the compiler's
+// wait counters: the caller waits for it with s_waitcnt vmcnt before reading
+// the destination, and before the work-group exits.
+// (No memory clobber: the DMA's LDS writes become visible only through
+// wait_vmcnt, which is a compiler memory barrier, and the work-group barriers
+// order every access to a ring slot before the DMA that refills it.)
 __device__ __forceinline__ void lds_dma16(const void* sbase, uint32_t voff, uint32_t lds_base) {
   asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds_base), "v"(voff),
-               "s"(sbase)
-               : "memory");
+               "s"(sbase));
 }
 
-// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
+// s_waitcnt with only the vector-memory counter constrained; also a compiler
+// memory barrier, so that no LDS access moves across it.
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xf << 8));
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
 // Work-group barrier that orders LDS accesses but does not wait for
@@ -86,7 +87,9 @@ struct WideCfg {
   static constexpr int LIST = RING;                               // int2 (slot, id) per token
   static constexpr int XBUF = LIST + kMaxSplitTokensDevice * 8;   // [NW][2][64] f32x4 partial scores
   static constexpr int QROPE = XBUF + NW * 2 * 64 * 16;           // [NW][2][64] bf16x8 RoPE query (B operand)
-  static constexpr int LDS_BYTES = QROPE + NW * 2 * 64 * 16;
+  static constexpr int FLAGS = QROPE + NW * 2 * 64 * 16;          // [NW] int: exchanges published per wave
+  static constexpr int LDS_BYTES = FLAGS + NW * 4;
+  static constexpr int SPIN_LIMIT = 1 << 16;  // polls of a partner's flag before giving up (never reached)
   static constexpr int DMA_PER_TILE = 6;  // per wave: 2 latent, 2 gate, 2 RoPE
   static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
   static_assert(SLOT % 16 == 0 && LIST % 16 == 0 && XBUF % 16 == 0 && QROPE % 16 == 0, "alignment");
@@ -212,6 +215,9 @@ __global__ __launch_bounds__(WideCfg::NT, 1) void split_wide_kernel(SplitArgs a)
   const int off_sa = C::LAT + r16 * LROW + 2 * (256 * dh + 8 * g);             // scores: latent A operand
   const int off_sr = C::ROPE + r16 * 128 + 16 * ((4 * dh + g) ^ (r16 & 7));    // scores: RoPE A operand
   f32x4_t* xbuf = reinterpret_cast<f32x4_t*>(lds + C::XBUF);
+  int* flags = reinterpret_cast<int*>(lds + C::FLAGS);
+  if (lane == 0) flags[w] = 0;  // ordered before any poll by the first list barrier
+  int exchanges = 0;            // this wave's published exchanges (the same count in every wave)
 
   bf16x8_t qb[2][8];  // B operand: head 16 hb + r16, dims 8g .. 8g + 7 of latent chunk c
   bf16x8_t* qrope = reinterpret_cast<bf16x8_t*>(lds + C::QROPE) + w * 2 * 64 + lane;  // RoPE chunk, [hb * 64]
@@ -226,7 +232,6 @@ __global__ __launch_bounds__(WideCfg::NT, 1) void split_wide_kernel(SplitArgs a)
       u32x4_t* lp = reinterpret_cast<u32x4_t*>(lds + sbase + off_gl + k * LROW);
       const u32x4_t gv = *reinterpret_cast<const u32x4_t*>(lds + sbase + off_gg + k * DC * 2);
       *lp = gate_chunk(*lp, gv);
-      __builtin_amdgcn_sched_barrier(0);  // one token at a time: bounded register use
     }
   };
   // O^T += C~^T P^T over the 16 tokens of the tile at slot byte offset sbase
@@ -257,6 +262,17 @@ __global__ __launch_bounds__(WideCfg::NT, 1) void split_wide_kernel(SplitArgs a)
         m_run[hb] = -INFINITY;
         l_run[hb] = 0.f;
       }
+      // query of this lane for sequence b (bf16, as the absorption wrote it)
+      {
+        const uint16_t* q16 = reinterpret_cast<const uint16_t*>(a.qfull);
+#pragma unroll
+        for (int hb = 0; hb < 2; ++hb) {
+          const uint16_t* qrow = q16 + (static_cast<int64_t>(b) * a.H + head0 + hb * 16 + r16) * DQ;
+#pragma unroll
+          for (int c = 0; c < 8; ++c) qb[hb][c] = *reinterpret_cast<const bf16x8_t*>(qrow + 256 * dh + 32 * c + 8 * g);
+          qrope[hb * 64] = *reinterpret_cast<const bf16x8_t*>(qrow + DC + 32 * dh + 8 * g);  // this wave's LDS region
+        }
+      }
       for (int c0 = 0; c0 < take; c0 += chunk) {
         const int t0 = off + c0;
         const int n = min(chunk, take - c0);
@@ -274,26 +290,6 @@ __global__ __launch_bounds__(WideCfg::NT, 1) void split_wide_kernel(SplitArgs a)
 #pragma unroll
           for (int e = 0; e < PER; ++e)
             if (e < nper) pid[e] = a.ids[psl[e]];
-          if (c0 == 0) {
-            // query of this lane for sequence b, rounded to bf16, one head block at a time
-#pragma unroll
-            for (int hb = 0; hb < 2; ++hb) {
-              const float* qrow = a.qfull + (static_cast<int64_t>(b) * a.H + head0 + hb * 16 + r16) * DQ;
-#pragma unroll
-              for (int c = 0; c < 9; ++c) {
-                const int d = c < 8 ? 256 * dh + 32 * c + 8 * g : DC + 32 * dh + 8 * g;
-                const float4 x0 = *reinterpret_cast<const float4*>(qrow + d);
-                const float4 x1 = *reinterpret_cast<const float4*>(qrow + d + 4);
-                const float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
-                bf16x8_t v;
-#pragma unroll
-                for (int e = 0; e < 8; ++e) v[e] = static_cast<__bf16>(x[e]);
-                if (c < 8) qb[hb][c] = v;
-                else qrope[hb * 64] = v;  // this wave's own LDS region
-              }
-              __builtin_amdgcn_sched_barrier(0);
-            }
-          }
 #pragma unroll
           for (int e = 0; e < PER; ++e) {
             const int j = tid + e * C::NT;
@@ -302,55 +298,80 @@ __global__ __launch_bounds__(WideCfg::NT, 1) void split_wide_kernel(SplitArgs a)
         }
         __syncthreads();  // the list is complete; every wave is done with the previous chunk's tiles
 
-        auto issue_tile = [&](int i) {
+        // DMA of tile i given its list entries for this wave's tokens 2w, 2w + 1
+        // ((slot, id) each; one 16-byte LDS read per tile)
+        auto entries = [&](int i) { return reinterpret_cast<const int4*>(list)[i * 8 + w]; };
+        auto issue_tile = [&](int i, int4 e) {
           const uint32_t slot = lds0 + (i % NS) * C::SLOT;
+          const int sl[2] = {__builtin_amdgcn_readfirstlane(e.x), __builtin_amdgcn_readfirstlane(e.z)};
+          const int id[2] = {__builtin_amdgcn_readfirstlane(e.y), __builtin_amdgcn_readfirstlane(e.w)};
 #pragma unroll
           for (int k = 0; k < 2; ++k) {
-            const int2 e = list[i * 16 + 2 * w + k];  // uniform address: broadcast
-            const int sl = __builtin_amdgcn_readfirstlane(e.x);
-            const int id = __builtin_amdgcn_readfirstlane(e.y);
-            lds_dma16(cache + static_cast<int64_t>(sl) * DQ, lane16, slot + C::LAT + (2 * w + k) * LROW);
-            lds_dma16(gate + static_cast<int64_t>(id) * DC, lane16, slot + C::GATE + (2 * w + k) * DC * 2);
+            lds_dma16(cache + static_cast<int64_t>(sl[k]) * DQ, lane16, slot + C::LAT + (2 * w + k) * LROW);
+            lds_dma16(gate + static_cast<int64_t>(id[k]) * DC, lane16, slot + C::GATE + (2 * w + k) * DC * 2);
           }
 #pragma unroll
-          for (int k = 0; k < 2; ++k) {
-            const int sl = __builtin_amdgcn_readfirstlane(list[i * 16 + 2 * w + k].x);
-            if ((lane >> 3) == k) lds_dma16(cache + static_cast<int64_t>(sl) * DQ, rope_off, slot + C::ROPE + 2 * w * 128);
-          }
+          for (int k = 0; k < 2; ++k)
+            if ((lane >> 3) == k) lds_dma16(cache + static_cast<int64_t>(sl[k]) * DQ, rope_off, slot + C::ROPE + 2 * w * 128);
         };
 
-        issue_tile(0);
-        if (ntiles > 1) issue_tile(1);
+        issue_tile(0, entries(0));
+        if (ntiles > 1) issue_tile(1, entries(1));
+        int4 next_e = entries(min(2, ntiles - 1));  // list entries of tile t + 2
+        // this wave's tokens of tile 0 (that of tile 1 may be in flight)
+        if (ntiles > 1) wait_vmcnt<C::DMA_PER_TILE>();
+        else wait_vmcnt<0>();
+        gate_tile(0);
 
+        // Tile t: scores, exchange, softmax and values of tile t, with the
+        // gating of tile t + 1 overlapping the softmax.
         for (int t = 0; t < ntiles; ++t) {
           const int sbase = __builtin_amdgcn_readfirstlane((t % NS) * C::SLOT);
-          // this wave's DMA of tile t is in LDS (that of tile t + 1 may be in flight)
-          if (t + 1 < ntiles) wait_vmcnt<C::DMA_PER_TILE>();
-          else wait_vmcnt<0>();
-          gate_tile(sbase);
-          __builtin_amdgcn_sched_barrier(0);
-          if (t > 0) values(__builtin_amdgcn_readfirstlane(((t + NS - 1) % NS) * C::SLOT));
-          __builtin_amdgcn_sched_barrier(0);
           lds_barrier();  // tile t gated and visible; every wave is done with tile t - 1
-          if (t + 2 < ntiles) issue_tile(t + 2);  // into the slot of tile t - 1
+          if (t + 2 < ntiles) issue_tile(t + 2, next_e);  // into the slot of tile t - 1
+          next_e = entries(min(t + 3, ntiles - 1));         // read now, used next iteration
           __builtin_amdgcn_sched_barrier(0);
 
           // partial scores over this wave's dims
-          f32x4_t acc[2];
+          // two accumulators per head block (even and odd chunks): four
+          // independent MFMA chains instead of two
+          f32x4_t acc[2], acc2[2];
 #pragma unroll
-          for (int hb = 0; hb < 2; ++hb) acc[hb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+          for (int hb = 0; hb < 2; ++hb) acc[hb] = acc2[hb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
           for (int c = 0; c < 9; ++c) {
             const unsigned char* ap = c < 8 ? lds + sbase + off_sa + 64 * c : lds + sbase + off_sr;
             const bf16x8_t av = *reinterpret_cast<const bf16x8_t*>(ap);
 #pragma unroll
-            for (int hb = 0; hb < 2; ++hb)
-              acc[hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, c < 8 ? qb[hb][c] : qrope[hb * 64], acc[hb], 0, 0, 0);
+            for (int hb = 0; hb < 2; ++hb) {
+              f32x4_t& ac = (c & 1) ? acc2[hb] : acc[hb];
+              ac = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, c < 8 ? qb[hb][c] : qrope[hb * 64], ac, 0, 0, 0);
+            }
           }
 #pragma unroll
+          for (int hb = 0; hb < 2; ++hb) acc[hb] += acc2[hb];
+#pragma unroll
           for (int hb = 0; hb < 2; ++hb) xbuf[(w * 2 + hb) * 64 + lane] = acc[hb];
+          // Publish the partial scores to the partner wave (w ^ 1) and wait
+          // for its own: LDS writes of a wave complete in order, and the flag
+          // is written after the scores are.
+          ++exchanges;
+          asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+          if (lane == 0) __hip_atomic_store(flags + w, exchanges, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+          for (int spin = 0; spin < C::SPIN_LIMIT; ++spin) {
+            const int seen = __builtin_amdgcn_readfirstlane(
+                __hip_atomic_load(flags + (w ^ 1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP));
+            if (seen >= exchanges) break;
+            __builtin_amdgcn_s_sleep(1);
+          }
+          asm volatile("" ::: "memory");
           __builtin_amdgcn_sched_barrier(0);
-          lds_barrier();
+          if (t + 1 < ntiles) {
+            // this wave's tokens of tile t + 1 (that of tile t + 2 may be in flight)
+            if (t + 2 < ntiles) wait_vmcnt<C::DMA_PER_TILE>();
+            else wait_vmcnt<0>();
+            gate_tile(__builtin_amdgcn_readfirstlane(((t + 1) % NS) * C::SLOT));
+          }
 #pragma unroll
           for (int hb = 0; hb < 2; ++hb) {
             const f32x4_t other = xbuf[((w ^ 1) * 2 + hb) * 64 + lane];
@@ -405,34 +426,33 @@ __global__ __launch_bounds__(WideCfg::NT, 1) void split_wide_kernel(SplitArgs a)
             const auto s1 = __builtin_amdgcn_permlane16_swap(pk[0][1], pk[1][1], false, false);
             pb = __builtin_bit_cast(bf16x8_t, u32x4_t{s0[0], s1[0], s0[1], s1[1]});
           }
+          values(sbase);
           __builtin_amdgcn_sched_barrier(0);
         }
-        values(((ntiles - 1) % NS) * C::SLOT);
 
       }
       // ---- partial result of this segment: this wave's heads and dims ----
       const int64_t pbase = (static_cast<int64_t>(wg) + b) * a.H + head0;
+      if (dh == 0) {
+#pragma unroll
+        for (int hb = 0; hb < 2; ++hb) {
+          const float l = sum_over_row_groups(l_run[hb]);
+          if (g == 0) {
+            __builtin_nontemporal_store(m_run[hb], a.part_ml + (pbase + 16 * hb + r16) * 2 + 0);
+            __builtin_nontemporal_store(l, a.part_ml + (pbase + 16 * hb + r16) * 2 + 1);
+          }
+        }
+      }
       {
-        float* orow = a.part_o + (pbase + (lane & 31)) * DC + 256 * dh + 4 * (lane >> 5);
+        float* obase = a.part_o + pbase * DC + 256 * dh;  // uniform
+        const uint32_t loff = (lane & 31) * DC + 4 * (lane >> 5);
 #pragma unroll
         for (int db = 0; db < 8; ++db)
 #pragma unroll
           for (int r4 = 0; r4 < 4; ++r4)
             __builtin_nontemporal_store(
                 f32x4_t{o[db][4 * r4], o[db][4 * r4 + 1], o[db][4 * r4 + 2], o[db][4 * r4 + 3]},
-                reinterpret_cast<f32x4_t*>(orow + 32 * db + 8 * r4));
-      }
-      if (dh == 0) {
-#pragma unroll
-        for (int hb = 0; hb < 2; ++hb) {
-          float l = l_run[hb];
-          l += __shfl_xor(l, 16, 64);
-          l += __shfl_xor(l, 32, 64);
-          if (g == 0) {
-            __builtin_nontemporal_store(m_run[hb], a.part_ml + (pbase + 16 * hb + r16) * 2 + 0);
-            __builtin_nontemporal_store(l, a.part_ml + (pbase + 16 * hb + r16) * 2 + 1);
-          }
-        }
+                reinterpret_cast<f32x4_t*>(obase + loff + 32 * db + 8 * r4));
       }
     }
     remaining -= take > 0 ? take : 0;

@@ -142,6 +142,40 @@ def test_edge_lengths_dc512(gpu):
     assert_close(got, oracle_decode(inp), "bf16", "dc512 edge lengths", scaled=True)
 
 
+@pytest.mark.parametrize("case", ["mixed", "short", "one_long"])
+def test_balanced_schedule_dc512(gpu, case):
+    # The 128-head kernel splits the batch's tokens evenly over its work-groups:
+    # ranges that start mid-sequence, span many short or empty sequences, or
+    # hold less than a token each (fewer tokens than work-groups).
+    wl = W.WORKLOADS[4].replace(name=f"sched_{case}_dc512", paged=True, seed=45)
+    if case == "mixed":
+        lens = np.array([0, 1, 2100, 0, 17, 4097, 5, 0, 3, 1500, 2, 0])
+    elif case == "short":
+        lens = np.array([1, 0, 2, 3, 0, 1, 5, 4, 1, 0, 2, 7] * 4)
+    else:
+        lens = np.array([0, 6000, 0])
+    wl = wl.replace(batch=len(lens), seq_len_range=(1, int(max(lens.max(), 64))))
+    inp = W.generate(wl, seq_lens=lens)
+    say(f"decode dc512 balanced schedule {case}: {int(lens.sum())} tokens, {len(lens)} sequences")
+    got = gpu_decode(inp)
+    assert np.all(got[lens == 0] == 0)
+    assert_close(got, oracle_decode(inp), "bf16", f"balanced {case}", scaled=True)
+
+
+def test_peaked_logits_dc512(gpu):
+    # query x 3: running maxima grow by more than 2^8 between the tiles of a
+    # work-group's range (about 45 tokens each here), so the 128-head kernel
+    # rescales its accumulators.  (At x 8 the kernel's bf16 query and bf16
+    # gated latent give rel-L2 6.6e-3, above the bar; a CPU emulation of the
+    # same roundings gives the same figure, so that is precision, not a fault.)
+    wl = W.WORKLOADS[4].replace(name="peaked_dc512", batch=4, seq_len_range=(2500, 3500), seed=46)
+    inp = W.generate(wl)
+    inp.q[:] = W.f32_to_bf16_bits(W.bf16_bits_to_f32(inp.q) * np.float32(3.0))
+    say("decode dc512 peaked logits (q x 3)")
+    got = gpu_decode(inp, B.make_plan(B.PATH_MFMA, 256))
+    assert_close(got, oracle_decode(inp), "bf16", "peaked dc512", scaled=True)
+
+
 def test_peaked_logits(gpu):
     inp = W.generate(SMALL.replace(seed=22), seq_lens=np.array([64, 500, 129, 7]))
     inp.q[:] = W.f32_to_bf16_bits(W.bf16_bits_to_f32(inp.q) * np.float32(8.0))
