@@ -160,7 +160,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", type=int, default=1, help="index into workloads.WORKLOADS")
+    ap.add_argument("--workload", type=int, default=1,
+                    help="index into workloads.WORKLOADS; 5 = the plain-MLA comparison (d_c 320, all-ones gate) "
+                         "of the large-batch case")
     ap.add_argument("--path", choices=["auto", "valu", "mfma"], default="auto")
     ap.add_argument("--split", type=int, default=0, help="tokens per split (0 = automatic)")
     ap.add_argument("--id-slices", type=int, default=0, choices=[0, 1, 8],
@@ -189,7 +191,7 @@ def main():
     torch.cuda.set_device(0)
     L = B.lib()
     hip = Hip()
-    wl = W.WORKLOADS[args.workload]
+    wl = W.WORKLOADS[args.workload] if args.workload < len(W.WORKLOADS) else W.MLA_DC320_BIGBATCH
     log(f"bench: generating {wl.name}")
     inp = W.generate(wl)
     traffic = A.decode_bytes(batch=wl.batch, heads=wl.heads, head_dim=wl.head_dim, v_head_dim=wl.v_head_dim,
