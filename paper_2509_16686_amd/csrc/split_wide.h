@@ -73,12 +73,19 @@ __device__ __forceinline__ void lds_barrier() {
 
 typedef __attribute__((ext_vector_type(16))) float f32x16_t;
 
+// Latent rows in LDS are stored with their 16-byte pieces permuted: logical
+// piece p of tile row r sits at piece p ^ lat_swz(r).  The permutation keeps
+// both MFMA operand reads free of bank conflicts (32 or 64 banks): the score
+// read (16 rows, one piece each) hits 16 distinct 4-bank groups, and the
+// transposed value read (4 rows x 32 bytes per 16 lanes) 4 distinct pairs.
+__device__ __forceinline__ int lat_swz(int r) { return ((0xCA60 >> (4 * (r & 3))) & 15) ^ (r >> 2); }
+
 struct WideCfg {
   static constexpr int DC = 512, DR = 64, DQ = DC + DR;
   static constexpr int NW = 8, NT = NW * 64;
   static constexpr int HEADS = 128;       // heads per work-group
   static constexpr int NS = 3;            // ring slots
-  static constexpr int LROW = DC * 2 + 16;  // bytes per latent row in LDS (16 bytes of padding)
+  static constexpr int LROW = DC * 2;       // bytes per latent row in LDS (pieces swizzled, see lat_swz)
   static constexpr int LAT = 0;                       // [16][LROW]   latent, gated in place
   static constexpr int ROPE = LAT + 16 * LROW;        // [16][128 B]  RoPE keys, 16-byte pieces swizzled
   static constexpr int GATE = ROPE + 16 * DR * 2;     // [16][1024 B] gate rows
@@ -204,15 +211,22 @@ __global__ __launch_bounds__(WideCfg::NT, 1) void split_wide_kernel(SplitArgs a)
   // l % 8 of token 2w + l / 8 with piece (l % 8) ^ (token % 8), one DMA per
   // token (lanes 0-7, then lanes 8-15)
   const uint32_t rope_off = 2 * DC + 16 * ((lane & 7) ^ ((2 * w + ((lane >> 3) & 1)) & 7));
-  const uint32_t lane16 = 16 * lane;
+  // latent / gate DMA of token 2w + k: lane l fetches logical piece l ^ lat_swz(2w + k)
+  const uint32_t lane16s[2] = {static_cast<uint32_t>(16 * (lane ^ lat_swz(2 * w))),
+                               static_cast<uint32_t>(16 * (lane ^ lat_swz(2 * w + 1)))};
   // Loop-invariant per-lane byte offsets inside a slot.
   const int off_gl = C::LAT + 2 * w * LROW + 16 * lane;       // gating: latent piece of token 2w
   const int off_gg = C::GATE + 2 * w * DC * 2 + 16 * lane;    // gating: gate piece of token 2w
-  // values: lane r16 of 16-lane group R reads 4 dims of token 8 (R / 2) + 4 j + r16 / 4
-  // and receives dim 16 (R % 2) + r16 of tokens 8 (R / 2) + 4 j .. + 3
-  const int off_tr = C::LAT + (8 * (lane >> 5) + (r16 >> 2)) * LROW +
-                     2 * (256 * dh + 16 * ((lane >> 4) & 1) + 4 * (r16 & 3));
-  const int off_sa = C::LAT + r16 * LROW + 2 * (256 * dh + 8 * g);             // scores: latent A operand
+  // values: lane r16 of 16-lane group R reads 4 dims (8 bytes) of token
+  // 8 (R / 2) + 4 j + r16 / 4 and receives dim 16 (R % 2) + r16 of tokens
+  // 8 (R / 2) + 4 j .. + 3; logical piece 32 dh + 4 db + tr_s of that row
+  const int tr_row0 = 8 * (lane >> 5) + (r16 >> 2);
+  const int tr_s = 2 * ((lane >> 4) & 1) + ((r16 & 3) >> 1);
+  const int tr_f[2] = {lat_swz(tr_row0), lat_swz(tr_row0 + 4)};
+  const int off_tr = C::LAT + tr_row0 * LROW + 512 * dh + 8 * (r16 & 1);
+  // scores: lane (token r16, g) reads logical piece 32 dh + 4 c + g
+  const int sa_x = g ^ lat_swz(r16);
+  const int off_sa = C::LAT + r16 * LROW + 512 * dh + 16 * (sa_x & 3);
   const int off_sr = C::ROPE + r16 * 128 + 16 * ((4 * dh + g) ^ (r16 & 7));    // scores: RoPE A operand
   f32x4_t* xbuf = reinterpret_cast<f32x4_t*>(lds + C::XBUF);
   int* flags = reinterpret_cast<int*>(lds + C::FLAGS);
@@ -239,10 +253,13 @@ __global__ __launch_bounds__(WideCfg::NT, 1) void split_wide_kernel(SplitArgs a)
     const unsigned char* tp = lds + sbase + off_tr;
 #pragma unroll
     for (int db = 0; db < 8; ++db) {
+      // physical piece (4 db + tr_s) ^ f = 4 (db ^ (f >> 2)) + (tr_s ^ (f & 3))
+      const int p0 = 4 * (db ^ (tr_f[0] >> 2)) + (tr_s ^ (tr_f[0] & 3));
+      const int p1 = 4 * (db ^ (tr_f[1] >> 2)) + (tr_s ^ (tr_f[1] & 3));
       const s16x4_t a0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-          (__attribute__((address_space(3))) s16x4_t*)(tp + 64 * db));
+          (__attribute__((address_space(3))) s16x4_t*)(tp + 16 * p0));
       const s16x4_t a1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-          (__attribute__((address_space(3))) s16x4_t*)(tp + 4 * LROW + 64 * db));
+          (__attribute__((address_space(3))) s16x4_t*)(tp + 4 * LROW + 16 * p1));
       const bf16x8_t av = __builtin_bit_cast(
           bf16x8_t, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
       o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb, o[db], 0, 0, 0);
@@ -307,8 +324,8 @@ __global__ __launch_bounds__(WideCfg::NT, 1) void split_wide_kernel(SplitArgs a)
           const int id[2] = {__builtin_amdgcn_readfirstlane(e.y), __builtin_amdgcn_readfirstlane(e.w)};
 #pragma unroll
           for (int k = 0; k < 2; ++k) {
-            lds_dma16(cache + static_cast<int64_t>(sl[k]) * DQ, lane16, slot + C::LAT + (2 * w + k) * LROW);
-            lds_dma16(gate + static_cast<int64_t>(id[k]) * DC, lane16, slot + C::GATE + (2 * w + k) * DC * 2);
+            lds_dma16(cache + static_cast<int64_t>(sl[k]) * DQ, lane16s[k], slot + C::LAT + (2 * w + k) * LROW);
+            lds_dma16(gate + static_cast<int64_t>(id[k]) * DC, lane16s[k], slot + C::GATE + (2 * w + k) * DC * 2);
           }
 #pragma unroll
           for (int k = 0; k < 2; ++k)
@@ -340,7 +357,8 @@ __global__ __launch_bounds__(WideCfg::NT, 1) void split_wide_kernel(SplitArgs a)
           for (int hb = 0; hb < 2; ++hb) acc[hb] = acc2[hb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
           for (int c = 0; c < 9; ++c) {
-            const unsigned char* ap = c < 8 ? lds + sbase + off_sa + 64 * c : lds + sbase + off_sr;
+            // physical piece (4 c + g) ^ f = 4 (c ^ (sa_x >> 2)) + (sa_x & 3)
+            const unsigned char* ap = c < 8 ? lds + sbase + off_sa + 64 * (c ^ (sa_x >> 2)) : lds + sbase + off_sr;
             const bf16x8_t av = *reinterpret_cast<const bf16x8_t*>(ap);
 #pragma unroll
             for (int hb = 0; hb < 2; ++hb) {
