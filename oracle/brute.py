@@ -46,3 +46,15 @@ def decode(q, cache, token_ids, gate, w_uk, w_uv, seq_lens, rows_of, *, latent_d
                              for v in range(d_v)])
         out.append(per_head)
     return out
+
+
+def gate_rows(emb, w_ue, ids):
+    """Eq. (4) element by element: g[i][c] = sum_k W^UE[c][k] Emb[ids[i]][k].
+
+    ``emb`` and ``w_ue`` are nested lists of floats; ids are clamped into the
+    table like the library does."""
+    out = []
+    for i in ids:
+        e = emb[min(max(int(i), 0), len(emb) - 1)]
+        out.append([sum(w_ue[c][k] * e[k] for k in range(len(e))) for c in range(len(w_ue))])
+    return out

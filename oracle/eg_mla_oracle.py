@@ -12,7 +12,8 @@ What it computes (EG-MLA, arXiv 2509.16686):
   RoPE key k^R_t = RoPE(W^KR x_t) of App. C Eq. (C.10), one d_r vector shared
   by all heads.
 * Embedding gate, Sec. 3.1 Eq. (3)-(5): e_t = Emb(i_t), g_t = W^UE e_t, applied
-  by a Hadamard product.  Reading taken here (the paper places the gate in
+  by a Hadamard product (``gate_rows`` computes g for given ids; over the
+  whole vocabulary it is the folded table G).  Reading taken here (the paper places the gate in
   the latent space in its abstract, related-work and Sec. 5 text, but after
   the up-projection in Eq. (5) and its listing): the gate multiplies the
   cached latent, c~_t = c_t * G[i_t], where G = Emb W^UE^T is the gate table
@@ -87,6 +88,22 @@ def _softmax(s: np.ndarray) -> np.ndarray:
     m = s.max(axis=-1, keepdims=True)
     e = np.exp(s - m)
     return e / e.sum(axis=-1, keepdims=True)
+
+
+# ---------------------------------------------------------------------------
+# gate rows from the token embedding (Sec. 3.1 Eq. (3)-(4))
+# ---------------------------------------------------------------------------
+def gate_rows(emb, w_ue, ids, *, storage: str) -> np.ndarray:
+    """g_i = W^UE e_i with e_i = Emb[ids[i]]; returns [n, d_c] in float64.
+
+    emb [V_e, e], w_ue [d_c, e] ([out, in] like every weight here), ids [n]
+    (clamped into [0, V_e) as the library does).  Over ids 0..V-1 this is the
+    folded gate table G = Emb W^UE^T of the table-lookup variant (Sec. 5.2).
+    """
+    ef = widen(emb, storage)
+    wf = widen(w_ue, storage)
+    idx = np.clip(np.asarray(ids, dtype=np.int64), 0, ef.shape[0] - 1)
+    return ef[idx] @ wf.T                                    # row i: W^UE e_{ids[i]}
 
 
 # ---------------------------------------------------------------------------

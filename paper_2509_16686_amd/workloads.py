@@ -232,6 +232,29 @@ def generate(wl: Workload, seq_lens: Optional[np.ndarray] = None) -> DecodeInput
 
 
 @dataclass
+class GateEmbedding:
+    """Unfolded gate of Sec. 3.1 Eq. (3)-(4): an embedding table and W^UE.
+
+    Component 0 of every embedding row is 1 and column 0 of W^UE is 1, so
+    g = W^UE e = 1 + (a zero-mean term of std 0.1): the same statistics as the
+    folded tables the decode workloads draw."""
+
+    emb: np.ndarray    # [V, e]
+    w_ue: np.ndarray   # [d_c, e]
+
+
+def generate_gate_embedding(wl: Workload, emb_dim: int, seed: Optional[int] = None) -> GateEmbedding:
+    """Seeded embedding table [V, emb_dim] ~ N(0, 1) and W^UE [d_c, emb_dim] ~ N(0, 0.1 / sqrt(emb_dim - 1))."""
+    rng = np.random.default_rng(wl.seed + 2000 if seed is None else seed)
+    emb = rng.standard_normal((wl.vocab, emb_dim), dtype=np.float32)
+    emb[:, 0] = 1.0
+    w_ue = rng.standard_normal((wl.latent_dim, emb_dim), dtype=np.float32) * np.float32(
+        0.1 / math.sqrt(max(emb_dim - 1, 1)))
+    w_ue[:, 0] = 1.0
+    return GateEmbedding(emb=_store(emb, wl.dtype), w_ue=_store(w_ue, wl.dtype))
+
+
+@dataclass
 class AppendInputs:
     """Host arrays for one append call (new tokens written into a cache)."""
 

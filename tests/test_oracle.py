@@ -68,6 +68,58 @@ def test_brute_force_tiny_fp32_workload():
     assert rel_err(run(orc.decode, inp), np.array(got)) < 1e-12
 
 
+# ---- gate rows from the token embedding (Eq. (3)-(4)) --------------------
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_gate_rows_brute_force(dtype):
+    wl = tiny(dtype=dtype, vocab=9, latent_dim=5, gate_dim=5)
+    ge = W.generate_gate_embedding(wl, emb_dim=6)
+    ids = np.array([0, 8, 3, 3, -2, 11, 4], dtype=np.int32)  # out of range: clamped
+    f = lambda a: orc.widen(a, dtype).tolist()
+    got = np.array(brute.gate_rows(f(ge.emb), f(ge.w_ue), ids.tolist()))
+    ref = orc.gate_rows(ge.emb, ge.w_ue, ids, storage=dtype)
+    assert ref.shape == (7, 5)
+    assert rel_err(ref, got) < 1e-12
+
+
+def test_gate_rows_identity_projection_returns_embeddings():
+    # W^UE = I (e = d_c): the gate is the embedding row itself, exactly
+    wl = tiny(vocab=9)
+    ge = W.generate_gate_embedding(wl, emb_dim=wl.latent_dim)
+    eye = np.eye(wl.latent_dim, dtype=np.float32)
+    ids = np.arange(9, dtype=np.int32)
+    g = orc.gate_rows(ge.emb, eye, ids, storage="fp32")
+    np.testing.assert_array_equal(g, orc.widen(ge.emb, "fp32"))
+
+
+def test_unfolded_gate_decode_matches_brute_force():
+    # EG-MLA with the gate computed from the embedding (Eq. (3)-(5)) through
+    # the folded table G = Emb W^UE^T (the table-lookup variant): brute force
+    # computes G and the decode with scalar loops, the oracle with NumPy
+    wl = tiny(vocab=9, seq_len=7)
+    inp = W.generate(wl)
+    ge = W.generate_gate_embedding(wl, emb_dim=6)
+    f = lambda a: orc.widen(a, wl.dtype).tolist()
+    G_brute = brute.gate_rows(f(ge.emb), f(ge.w_ue), list(range(wl.vocab)))
+    L = to_lists(inp)
+    got = brute.decode(L["q"], L["cache"], L["token_ids"], G_brute, L["w_uk"], L["w_uv"], L["seq_lens"],
+                       lambda b: [inp.slot(b, j) for j in range(int(inp.seq_lens[b]))],
+                       latent_dim=wl.latent_dim, head_dim=wl.head_dim, rope_dim=wl.rope_dim)
+    G = orc.gate_rows(ge.emb, ge.w_ue, np.arange(wl.vocab), storage=wl.dtype)
+    ref = orc.decode(
+        orc.widen(inp.q, wl.dtype), orc.widen(inp.latent_cache, wl.dtype), inp.token_ids, G,
+        orc.widen(inp.w_uk, wl.dtype), orc.widen(inp.w_uv, wl.dtype), inp.seq_lens, latent_dim=wl.latent_dim,
+        head_dim=wl.head_dim, rope_dim=wl.rope_dim, storage="f64", page_table=inp.page_table,
+        page_size=wl.page_size, max_pages=inp.max_pages)
+    assert rel_err(ref, np.array(got)) < 1e-12
+
+
+def test_gate_embedding_recipe_centres_gates_at_one():
+    wl = W.WORKLOADS[1].replace(vocab=4000)
+    ge = W.generate_gate_embedding(wl, emb_dim=512)
+    G = orc.gate_rows(ge.emb, ge.w_ue, np.arange(4000), storage=wl.dtype)
+    assert abs(G.mean() - 1.0) < 0.01 and 0.08 < G.std() < 0.12
+
+
 # ---- P2: absorbed == explicit --------------------------------------------
 @pytest.mark.parametrize("wl", [tiny(), tiny(paged=True, batch=3, seq_len=9), W.WORKLOADS[0],
                                 W.WORKLOADS[1].replace(batch=2, seq_len=300),
