@@ -172,6 +172,10 @@ def main():
     ap.add_argument("--calibration-copy-mib", type=int, default=0,
                     help="also run one device copy of this many MiB (a known byte count for profiler counters)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--unfolded-gate", type=int, default=0, metavar="E",
+                    help="unfolded gate with embedding width E (the paper recommends 512): every step first "
+                         "computes one gate row per cache row from its token embedding (eg_mla_gate_rows), then "
+                         "decodes with the row indices as ids; 0 = the folded gate table")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -208,6 +212,22 @@ def main():
                                      seq_lens=dd0.seq_lens.clone(),
                                      page_table=None if dd0.page_table is None else dd0.page_table.clone(),
                                      max_pages=dd0.max_pages, out=torch.empty_like(dd0.out)))
+    E = args.unfolded_gate
+    if E > 0:
+        # per-step gate rows: one per cache row, written to one buffer the decode then reads
+        ge = W.generate_gate_embedding(wl, E)
+        emb_d, wue_d = B.to_device_tensor(ge.emb, wl.dtype), B.to_device_tensor(ge.w_ue, wl.dtype)
+        n_rows = inp.num_rows
+        row_gate = torch.empty((n_rows, wl.latent_dim), dtype=dd0.gate.dtype, device="cuda")
+        row_ids = torch.arange(n_rows, dtype=torch.int32, device="cuda")
+        dims_u = B.dims_for(wl.replace(vocab=n_rows))
+        for c in copies:
+            c.gate_src_ids, c.dims, c.gate, c.ids = c.ids, dims_u, row_gate, row_ids
+        gate_call = L.eg_mla_gate_rows
+        # the decode now gathers one distinct gate row per cache row
+        traffic = A.decode_bytes(batch=wl.batch, heads=wl.heads, head_dim=wl.head_dim, v_head_dim=wl.v_head_dim,
+                                 latent_dim=wl.latent_dim, rope_dim=wl.rope_dim, elem_bytes=wl.elem_bytes,
+                                 total_tokens=inp.total_tokens(), distinct_ids=inp.total_tokens())
     path = {"auto": B.PATH_AUTO, "valu": B.PATH_VALU, "mfma": B.PATH_MFMA}[args.path]
     plan0 = B.make_plan(path, args.split, id_slices=args.id_slices)
     ws_bytes = B.decode_workspace_size(dd0.dims, wl.batch, dd0.max_pages, plan0)
@@ -227,19 +247,33 @@ def main():
                 None if dd.page_table is None else dd.page_table.data_ptr(), dd.max_pages,
                 int(dd.cache.shape[0]), ws.data_ptr(), ws_bytes, dd.out.data_ptr(), stream, ctypes.byref(plan))
 
-    warm_args = [argset(copies[k % R], plan0) for k in range(max(Wm, 1))]
-    step_args = [argset(copies[k % R], plan0) for k in range(K)]
-    timed_args = [argset(copies[k % R], plans[k]) for k in range(K)]
     call = L.eg_mla_decode_planned
 
-    for a in warm_args:
-        st = call(*a)
-        assert st == 0, B.status_string(st)
+    def gate_args(dd):
+        return (ctypes.byref(dd.dims), E, int(emb_d.shape[0]), n_rows, dd.gate_src_ids.data_ptr(),
+                emb_d.data_ptr(), wue_d.data_ptr(), row_gate.data_ptr(), stream)
+
+    def step(dd, plan):
+        """One step: a list of (function, arguments) calls."""
+        calls = [(call, argset(dd, plan))]
+        if E > 0:
+            calls.insert(0, (gate_call, gate_args(dd)))
+        return calls
+
+    warm_args = [step(copies[k % R], plan0) for k in range(max(Wm, 1))]
+    step_args = [step(copies[k % R], plan0) for k in range(K)]
+    timed_args = [step(copies[k % R], plans[k]) for k in range(K)]
+
+    for s in warm_args:
+        for f, a in s:
+            st = f(*a)
+            assert st == 0, B.status_string(st)
     torch.cuda.synchronize()
     # host enqueue rate, to size the spin that hides launch overhead
     h0 = time.perf_counter()
-    for a in warm_args:
-        call(*a)
+    for s in warm_args:
+        for f, a in s:
+            f(*a)
     host_per_call = (time.perf_counter() - h0) / len(warm_args)
     torch.cuda.synchronize()
 
@@ -259,8 +293,9 @@ def main():
         wall0 = time.perf_counter()
         torch.cuda._sleep(int(spin_ms * cycles_per_ms))
         hip.record(t_start, stream)
-        for a in arglist:
-            call(*a)
+        for s in arglist:
+            for f, a in s:
+                f(*a)
         hip.record(t_stop, stream)
         enq = time.perf_counter() - wall0
         torch.cuda.synchronize()
@@ -283,6 +318,18 @@ def main():
     #     launch, stamped by the dispatch itself (hipExtLaunchKernelGGL), on the kernel's stream
     timed_loop(timed_args)
     kernel_ms = [hip.elapsed_ms(ev0[k], ev1[k]) for k in range(K)]
+    if E > 0:
+        # (3) the gate-row kernel alone: an event pair around each launch (one kernel per call)
+        g0 = [hip.event() for _ in range(K)]
+        g1 = [hip.event() for _ in range(K)]
+        torch.cuda.synchronize()
+        torch.cuda._sleep(int(spin_ms * cycles_per_ms))
+        for k in range(K):
+            hip.record(g0[k], stream)
+            gate_call(*gate_args(copies[k % R]))
+            hip.record(g1[k], stream)
+        torch.cuda.synchronize()
+        gate_ms = float(np.mean([hip.elapsed_ms(g0[k], g1[k]) for k in range(K)]))
 
     ms_per_step = total_ms / K
     k_avg_ms = float(np.mean(kernel_ms))
@@ -290,7 +337,7 @@ def main():
     achieved = k_bytes / (k_avg_ms * 1e-3) / 1e9
     # counters were taken on the default workload with the automatic plan only
     t_bytes = recorded_traffic() if (args.workload == 1 and args.path == "auto" and args.split == 0
-                                     and args.id_slices == 0) else None
+                                     and args.id_slices == 0 and E == 0) else None
     traffic_gbps = None if t_bytes is None else t_bytes / (k_avg_ms * 1e-3) / 1e9
     tokens_per_s = wl.batch / (ms_per_step * 1e-3)
     log(f"bench: {ms_per_step * 1e3:.2f} us/step, split kernel {k_avg_ms * 1e3:.2f} us "
@@ -314,7 +361,7 @@ def main():
                    "latent_dim": wl.latent_dim, "rope_dim": wl.rope_dim, "vocab": wl.vocab,
                    "context": wl.seq_len if wl.seq_len else list(wl.seq_len_range), "paged": wl.paged,
                    "storage": wl.dtype, "path": args.path, "split_tokens": args.split, "id_slices": args.id_slices,
-                   "rotating_copies": R},
+                   "rotating_copies": R, "gate": f"unfolded, embedding width {E}" if E > 0 else "folded table"},
         "hbm_gbps_call": traffic.total / (ms_per_step * 1e-3) / 1e9,
         "hbm_frac_call": traffic.total / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
         # estimate, not a measurement: every layer of a 24-layer model taking one such call
@@ -326,6 +373,14 @@ def main():
                      "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic_gbps,
                      "algorithmic_bytes_per_launch": k_bytes, "traffic_bytes_per_launch": t_bytes, "kernel_us": k_avg_ms * 1e3},
     }
+    if E > 0:
+        # algorithmic: the gathered embedding rows, the gate rows written, the ids, W^UE once
+        g_bytes = n_rows * (E * wl.elem_bytes + wl.latent_dim * wl.elem_bytes + 4) + wl.latent_dim * E * wl.elem_bytes
+        out["unfolded_gate"] = {"emb_dim": E, "rows": n_rows, "gate_rows_us": gate_ms * 1e3,
+                                "gate_rows_gbps": g_bytes / (gate_ms * 1e-3) / 1e9,
+                                "gate_rows_tflops": 2.0 * n_rows * E * wl.latent_dim / (gate_ms * 1e-3) / 1e12,
+                                "algorithmic_bytes": g_bytes}
+        log(f"bench: gate rows {gate_ms * 1e3:.2f} us ({out['unfolded_gate']['gate_rows_gbps']:.0f} GB/s)")
     if not args.no_cpu_baseline:
         log(f"bench: timing the fp64 oracle on the host for ~{args.cpu_seconds:.0f} s")
         out["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds)

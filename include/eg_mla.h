@@ -177,6 +177,28 @@ eg_mla_status eg_mla_decode_planned(const eg_mla_dims* dims, int32_t batch, cons
                                     size_t workspace_bytes, void* out, void* stream, const eg_mla_plan* plan);
 
 /* ---------------------------------------------------------------------------
+ * Gate rows from the token embedding (Sec. 3.1 Eq. (3)-(4)): for i < n,
+ *   out[i, :] = W^UE Emb[ids[i], :]
+ * with e = emb_dim embedding components in and d_c = dims->latent_dim gate
+ * values out, products accumulated in fp32 and rounded once to the storage
+ * type (bf16 x bf16 MFMA products when dtype is bf16, emb_dim % 32 == 0,
+ * d_c % 16 == 0 and emb/w_ue are 16-byte aligned; fp32 VALU otherwise).
+ *   - ids = 0 .. V-1 gives the folded gate table G = Emb W^UE^T that
+ *     eg_mla_decode takes (the table-lookup variant of Sec. 5.2, folded
+ *     once when the model is loaded);
+ *   - the ids of a step's cached tokens give the unfolded model's gates for
+ *     that step; eg_mla_decode then takes `out` as its gate table with a
+ *     token_id_cache that holds, for each cached row, its row index in `out`
+ *     (dims->vocab_size = n).
+ *
+ *   emb   [emb_vocab, emb_dim];  w_ue [d_c, emb_dim] ([out, in]);
+ *   ids   [n] int32, clamped to [0, emb_vocab);  out [n, d_c]
+ * n == 0 is a no-op.  emb_dim above 16384 is EG_MLA_ERR_UNSUPPORTED.
+ * ------------------------------------------------------------------------- */
+eg_mla_status eg_mla_gate_rows(const eg_mla_dims* dims, int32_t emb_dim, int32_t emb_vocab, int64_t n,
+                               const int32_t* ids, const void* emb, const void* w_ue, void* out, void* stream);
+
+/* ---------------------------------------------------------------------------
  * Prefill reference: plain causal attention over one sequence of T tokens in
  * the explicit (non-absorbed) form of App. C Eq. (C.2), (C.6), (C.11)-(C.13):
  * it materialises k_{j,h} = [W_UK[h] c~_j ; k^R_j] and v_{j,h} = W_UV[h] c~_j

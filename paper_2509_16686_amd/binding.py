@@ -22,7 +22,8 @@ PATH_AUTO, PATH_VALU, PATH_MFMA = 0, 1, 2
 
 # Every symbol include/eg_mla.h declares.
 EXPORTS = ["eg_mla_status_string", "eg_mla_check_dims", "eg_mla_append", "eg_mla_decode_workspace_size",
-           "eg_mla_decode", "eg_mla_decode_planned", "eg_mla_prefill_workspace_size", "eg_mla_prefill_ref"]
+           "eg_mla_decode", "eg_mla_decode_planned", "eg_mla_gate_rows", "eg_mla_prefill_workspace_size",
+           "eg_mla_prefill_ref"]
 
 
 class Dims(ctypes.Structure):
@@ -71,6 +72,8 @@ def lib() -> ctypes.CDLL:
     L.eg_mla_decode.argtypes = [pd, i32, vp, vp, vp, vp, vp, vp, vp, vp, i32, i64, vp, sz, vp, vp]
     L.eg_mla_decode_planned.restype = ctypes.c_int
     L.eg_mla_decode_planned.argtypes = [pd, i32, vp, vp, vp, vp, vp, vp, vp, vp, i32, i64, vp, sz, vp, vp, pp]
+    L.eg_mla_gate_rows.restype = ctypes.c_int
+    L.eg_mla_gate_rows.argtypes = [pd, i32, i32, i64, vp, vp, vp, vp, vp]
     L.eg_mla_prefill_workspace_size.restype = sz
     L.eg_mla_prefill_workspace_size.argtypes = [pd, i32]
     L.eg_mla_prefill_ref.restype = ctypes.c_int
@@ -146,6 +149,14 @@ def append(dims: Dims, x, token_ids, positions, slots, w_dkv, kv_norm_w, latent_
     _check(lib().eg_mla_append(ctypes.byref(dims), n, hidden, _ptr(x), _ptr(token_ids), _ptr(positions),
                                _ptr(slots), _ptr(w_dkv), _ptr(kv_norm_w), rope_theta, _ptr(latent_cache),
                                _ptr(token_id_cache), int(latent_cache.shape[0]), _stream(stream)), "eg_mla_append")
+
+
+def gate_rows(dims: Dims, ids, emb, w_ue, out, stream=None) -> None:
+    """eg_mla_gate_rows over device tensors: out[i] = W_UE Emb[ids[i]]."""
+    n = int(ids.shape[0])
+    emb_vocab, emb_dim = int(emb.shape[0]), int(emb.shape[1])
+    _check(lib().eg_mla_gate_rows(ctypes.byref(dims), emb_dim, emb_vocab, n, _ptr(ids), _ptr(emb), _ptr(w_ue),
+                                  _ptr(out), _stream(stream)), "eg_mla_gate_rows")
 
 
 def prefill_ref(dims: Dims, q, latent, token_ids, gate_table, w_uk, w_uv, workspace, out, stream=None) -> None:

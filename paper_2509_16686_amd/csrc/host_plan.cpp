@@ -166,6 +166,17 @@ eg_mla_status validate_append(const eg_mla_dims* d, int32_t n_tokens, int32_t hi
   return EG_MLA_OK;
 }
 
+eg_mla_status validate_gate_rows(const eg_mla_dims* d, int32_t emb_dim, int32_t emb_vocab, int64_t n,
+                                 const int32_t* ids, const void* emb, const void* w_ue, const void* out) {
+  eg_mla_status st = check_dims(d);
+  if (st != EG_MLA_OK) return st;
+  if (emb_dim < 1 || emb_vocab < 1 || n < 0) return EG_MLA_ERR_INVALID_ARG;
+  if (emb_dim > 16384) return EG_MLA_ERR_UNSUPPORTED;  // one embedding row staged in LDS (VALU kernel)
+  if (n == 0) return EG_MLA_OK;
+  if (!ids || !emb || !w_ue || !out) return EG_MLA_ERR_INVALID_ARG;
+  return EG_MLA_OK;
+}
+
 size_t prefill_workspace_bytes(const eg_mla_dims& d, int32_t seq_len) {
   const size_t T = static_cast<size_t>(std::max(seq_len, 0));
   const size_t H = static_cast<size_t>(d.num_heads);

@@ -73,6 +73,9 @@ eg_mla_status validate_append(const eg_mla_dims* d, int32_t n_tokens, int32_t hi
                               const void* w_dkv, const void* latent_cache, const int32_t* token_id_cache,
                               int64_t num_slots);
 
+eg_mla_status validate_gate_rows(const eg_mla_dims* d, int32_t emb_dim, int32_t emb_vocab, int64_t n,
+                                 const int32_t* ids, const void* emb, const void* w_ue, const void* out);
+
 size_t prefill_workspace_bytes(const eg_mla_dims& d, int32_t seq_len);
 
 eg_mla_status validate_prefill(const eg_mla_dims* d, int32_t seq_len, const void* q, const void* latent,

@@ -135,3 +135,18 @@ def test_append_and_prefill_reject_before_launch(L):
         B.ERR_UNSUPPORTED
     assert L.eg_mla_prefill_ref(ctypes.byref(d), -1, vp, vp, vp, vp, vp, vp, vp, 1 << 20, vp, None) == \
         B.ERR_INVALID_ARG
+
+
+def test_gate_rows_rejects_before_launch(L):
+    d = dims()
+    vp = ctypes.c_void_p(256)
+    # n == 0 is a no-op whatever the pointers
+    assert L.eg_mla_gate_rows(ctypes.byref(d), 512, 1000, 0, None, None, None, None, None) == B.OK
+    assert L.eg_mla_gate_rows(ctypes.byref(d), 512, 1000, 5, None, vp, vp, vp, None) == B.ERR_INVALID_ARG
+    assert L.eg_mla_gate_rows(ctypes.byref(d), 512, 1000, 5, vp, vp, vp, None, None) == B.ERR_INVALID_ARG
+    assert L.eg_mla_gate_rows(ctypes.byref(d), 0, 1000, 5, vp, vp, vp, vp, None) == B.ERR_INVALID_ARG
+    assert L.eg_mla_gate_rows(ctypes.byref(d), 512, 0, 5, vp, vp, vp, vp, None) == B.ERR_INVALID_ARG
+    assert L.eg_mla_gate_rows(ctypes.byref(d), 512, 1000, -1, vp, vp, vp, vp, None) == B.ERR_INVALID_ARG
+    assert L.eg_mla_gate_rows(ctypes.byref(d), 20000, 1000, 5, vp, vp, vp, vp, None) == B.ERR_UNSUPPORTED
+    bad = dims(gate_dim=64)
+    assert L.eg_mla_gate_rows(ctypes.byref(bad), 512, 1000, 5, vp, vp, vp, vp, None) == B.ERR_UNSUPPORTED
