@@ -221,8 +221,11 @@ def main():
         row_gate = torch.empty((n_rows, wl.latent_dim), dtype=dd0.gate.dtype, device="cuda")
         row_ids = torch.arange(n_rows, dtype=torch.int32, device="cuda")
         dims_u = B.dims_for(wl.replace(vocab=n_rows))
-        for c in copies:
+        # one embedding table per rotating copy, so that the table (tens of MB)
+        # is not served from the 256 MB MALL from one step to the next
+        for k, c in enumerate(copies):
             c.gate_src_ids, c.dims, c.gate, c.ids = c.ids, dims_u, row_gate, row_ids
+            c.emb = emb_d if k == 0 else emb_d.clone()
         gate_call = L.eg_mla_gate_rows
         # the decode now gathers one distinct gate row per cache row
         traffic = A.decode_bytes(batch=wl.batch, heads=wl.heads, head_dim=wl.head_dim, v_head_dim=wl.v_head_dim,
@@ -250,8 +253,8 @@ def main():
     call = L.eg_mla_decode_planned
 
     def gate_args(dd):
-        return (ctypes.byref(dd.dims), E, int(emb_d.shape[0]), n_rows, dd.gate_src_ids.data_ptr(),
-                emb_d.data_ptr(), wue_d.data_ptr(), row_gate.data_ptr(), stream)
+        return (ctypes.byref(dd.dims), E, int(dd.emb.shape[0]), n_rows, dd.gate_src_ids.data_ptr(),
+                dd.emb.data_ptr(), wue_d.data_ptr(), row_gate.data_ptr(), stream)
 
     def step(dd, plan):
         """One step: a list of (function, arguments) calls."""

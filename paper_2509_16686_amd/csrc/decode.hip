@@ -352,6 +352,8 @@ hipError_t launch_combine_mfma(int dc, dim3 grid, hipStream_t stream, const floa
   return launch_combine_dc<512>(grid, stream, pm, po, wv, seq_lens, ov, B, H, cap, split, s_max, slices, seq_rows);
 }
 
+}  // namespace
+
 // Compute units of the current device (cached per device).
 int device_cus() {
   static int cus[64] = {0};
@@ -364,6 +366,8 @@ int device_cus() {
   }
   return cus[dev];
 }
+
+namespace {
 
 // The MFMA split kernels launch with hipExtLaunchKernelGGL so that optional
 // timing events are stamped by the dispatch itself (kernel start and end).

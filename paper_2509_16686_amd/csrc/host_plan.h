@@ -90,4 +90,7 @@ inline float softmax_scale(const eg_mla_dims& d) {
 
 inline int elem_bytes(const eg_mla_dims& d) { return d.dtype == EG_MLA_BF16 ? 2 : 4; }
 
+// Compute units of the current device (queried once per device).
+int device_cus();
+
 }  // namespace egmla

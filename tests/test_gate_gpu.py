@@ -48,13 +48,20 @@ def check_rows(got, ge, ids, storage):
 
 
 @pytest.mark.parametrize("latent_dim,emb_dim,dtype,n", [
-    (128, 512, "bf16", 1000),   # MFMA, one column slice, ragged last row block
-    (512, 512, "bf16", 777),    # MFMA, four column slices
-    (128, 96, "bf16", 65),      # MFMA, three 32-component chunks
-    (128, 1024, "bf16", 40),    # MFMA, two passes of 512 components
-    (144, 40, "bf16", 33),      # VALU: embedding width not a multiple of 32
-    (32, 32, "fp32", 300),      # VALU, fp32 storage
-    (128, 512, "bf16", 1),      # a single row
+    (128, 512, "bf16", 1000),     # MFMA, one pass, one 128-column slice, ragged last block
+    (128, 512, "bf16", 200003),   # several blocks per wave through the two-half pipeline
+    (512, 512, "bf16", 777),      # four column slices
+    (128, 384, "bf16", 65),       # one pass of 24 chunks
+    (96, 256, "bf16", 70),        # slice padded past d_c (96 of 128 columns)
+    (64, 128, "bf16", 33),        # two 32-column blocks
+    (32, 128, "bf16", 50),        # d_c 32: a padded 64-column slice
+    (32, 768, "bf16", 90),        # one 32-column block, passes of 256 components
+    (128, 1024, "bf16", 40),      # passes of 256 components
+    (64, 640, "bf16", 100),       # passes of 128 components
+    (128, 96, "bf16", 65),        # VALU: embedding width not a multiple of 128
+    (144, 40, "bf16", 33),        # VALU: d_c not a multiple of 32
+    (32, 32, "fp32", 300),        # VALU, fp32 storage
+    (128, 512, "bf16", 1),        # a single row
 ])
 def test_gate_rows_match_oracle(gpu, latent_dim, emb_dim, dtype, n):
     wl = W.WORKLOADS[1].replace(latent_dim=latent_dim, gate_dim=latent_dim, dtype=dtype, vocab=3000, seed=51)
