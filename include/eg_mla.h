@@ -215,6 +215,38 @@ eg_mla_status eg_mla_prefill_ref(const eg_mla_dims* dims, int32_t seq_len, const
                                  const void* w_uv, void* workspace, size_t workspace_bytes, void* out,
                                  void* stream);
 
+/* ---------------------------------------------------------------------------
+ * Causal prefill of a batch of sequences packed back to back (App. C
+ * Eq. (C.2), (C.11)-(C.13) in the absorbed form, with the latent-space gate of
+ * Sec. 3.1 Eq. (3)-(5)): row (t, h) attends to the tokens j <= t of t's own
+ * sequence,
+ *   out[t,h] = W_UV[h] sum_j softmax_j(tau (q_lat[t,h].c~_j + q^R[t,h].k^R_j)) c~_j,
+ *   q_lat[t,h] = W_UK[h]^T q^C[t,h],  c~_j = c_j (.) G[token_ids[j]].
+ * MFMA kernels for bf16 storage with 16 heads, d_h = d_v = d_c = 128 and
+ * d_r = 64 (the d_c 128 layer); every other shape is EG_MLA_ERR_UNSUPPORTED
+ * (eg_mla_prefill_ref covers any shape, one sequence at a time).
+ *
+ *   cu_seqlens [batch + 1] int32 (device): sequence b is tokens
+ *       cu_seqlens[b] .. cu_seqlens[b+1]-1; cu_seqlens[0] = 0,
+ *       non-decreasing, cu_seqlens[batch] = total_tokens (empty sequences
+ *       allowed).  Values outside that are not checked; the kernels clamp
+ *       every index into range.
+ *   q [total, H, d_h + d_r] (q^R already rotated); latent [total, d_c + d_r]
+ *       (rows as eg_mla_append writes them); token_ids [total];
+ *   gate_table, w_uk, w_uv as for decode;  out [total, H, d_v].
+ *   workspace: eg_mla_prefill_varlen_workspace_size bytes, 256-byte aligned
+ *       (per-token sequence starts, the absorbed queries in bf16 and the
+ *       normalised latent outputs in fp32).
+ * Pointers 16-byte aligned.  total_tokens == 0 is a no-op.
+ * ------------------------------------------------------------------------- */
+size_t eg_mla_prefill_varlen_workspace_size(const eg_mla_dims* dims, int32_t total_tokens);
+
+eg_mla_status eg_mla_prefill_varlen(const eg_mla_dims* dims, int32_t batch, int32_t total_tokens,
+                                    const int32_t* cu_seqlens, const void* q, const void* latent,
+                                    const int32_t* token_ids, const void* gate_table, const void* w_uk,
+                                    const void* w_uv, void* workspace, size_t workspace_bytes, void* out,
+                                    void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -23,7 +23,7 @@ PATH_AUTO, PATH_VALU, PATH_MFMA = 0, 1, 2
 # Every symbol include/eg_mla.h declares.
 EXPORTS = ["eg_mla_status_string", "eg_mla_check_dims", "eg_mla_append", "eg_mla_decode_workspace_size",
            "eg_mla_decode", "eg_mla_decode_planned", "eg_mla_gate_rows", "eg_mla_prefill_workspace_size",
-           "eg_mla_prefill_ref"]
+           "eg_mla_prefill_ref", "eg_mla_prefill_varlen_workspace_size", "eg_mla_prefill_varlen"]
 
 
 class Dims(ctypes.Structure):
@@ -78,6 +78,10 @@ def lib() -> ctypes.CDLL:
     L.eg_mla_prefill_workspace_size.argtypes = [pd, i32]
     L.eg_mla_prefill_ref.restype = ctypes.c_int
     L.eg_mla_prefill_ref.argtypes = [pd, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp, vp]
+    L.eg_mla_prefill_varlen_workspace_size.restype = sz
+    L.eg_mla_prefill_varlen_workspace_size.argtypes = [pd, i32]
+    L.eg_mla_prefill_varlen.restype = ctypes.c_int
+    L.eg_mla_prefill_varlen.argtypes = [pd, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp, vp]
     _lib = L
     return L
 
@@ -157,6 +161,21 @@ def gate_rows(dims: Dims, ids, emb, w_ue, out, stream=None) -> None:
     emb_vocab, emb_dim = int(emb.shape[0]), int(emb.shape[1])
     _check(lib().eg_mla_gate_rows(ctypes.byref(dims), emb_dim, emb_vocab, n, _ptr(ids), _ptr(emb), _ptr(w_ue),
                                   _ptr(out), _stream(stream)), "eg_mla_gate_rows")
+
+
+def prefill_varlen_workspace_size(dims: Dims, total_tokens: int) -> int:
+    return lib().eg_mla_prefill_varlen_workspace_size(ctypes.byref(dims), total_tokens)
+
+
+def prefill_varlen(dims: Dims, cu_seqlens, q, latent, token_ids, gate_table, w_uk, w_uv, workspace, out,
+                   stream=None) -> None:
+    """eg_mla_prefill_varlen over device tensors (sequences packed back to back)."""
+    batch = int(cu_seqlens.shape[0]) - 1
+    T = int(q.shape[0])
+    _check(lib().eg_mla_prefill_varlen(ctypes.byref(dims), batch, T, _ptr(cu_seqlens), _ptr(q), _ptr(latent),
+                                       _ptr(token_ids), _ptr(gate_table), _ptr(w_uk), _ptr(w_uv), _ptr(workspace),
+                                       workspace.numel() * workspace.element_size(), _ptr(out), _stream(stream)),
+           "eg_mla_prefill_varlen")
 
 
 def prefill_ref(dims: Dims, q, latent, token_ids, gate_table, w_uk, w_uv, workspace, out, stream=None) -> None:

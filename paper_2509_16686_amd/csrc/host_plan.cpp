@@ -201,6 +201,42 @@ eg_mla_status validate_prefill(const eg_mla_dims* d, int32_t seq_len, const void
   return EG_MLA_OK;
 }
 
+PrefillVarlenLayout prefill_varlen_layout(const eg_mla_dims& d, int32_t total_tokens) {
+  const size_t T = static_cast<size_t>(std::max(total_tokens, 0));
+  const size_t H = static_cast<size_t>(d.num_heads);
+  PrefillVarlenLayout L;
+  L.off_seq_start = 0;                                                             // int32 [T]
+  L.off_qf = align_up(T * 4);                                                      // bf16 [T][H][d_c + d_r]
+  L.off_olat = L.off_qf + align_up(T * H * static_cast<size_t>(d.latent_dim + d.rope_dim) * 2);  // fp32 [T][H][d_c]
+  L.bytes = std::max<size_t>(L.off_olat + align_up(T * H * static_cast<size_t>(d.latent_dim) * 4), kAlign);
+  return L;
+}
+
+bool prefill_varlen_shape_ok(const eg_mla_dims& d) {
+  return d.dtype == EG_MLA_BF16 && d.num_heads == 16 && d.head_dim == 128 && d.v_head_dim == 128 &&
+         d.latent_dim == 128 && d.rope_dim == 64 && d.gate_dim == d.latent_dim;
+}
+
+eg_mla_status validate_prefill_varlen(const eg_mla_dims* d, int32_t batch, int32_t total_tokens,
+                                      const int32_t* cu_seqlens, const void* q, const void* latent,
+                                      const int32_t* token_ids, const void* gate_table, const void* w_uk,
+                                      const void* w_uv, const void* workspace, size_t workspace_bytes,
+                                      const void* out) {
+  eg_mla_status st = check_dims(d);
+  if (st != EG_MLA_OK) return st;
+  if (batch < 1 || total_tokens < 0) return EG_MLA_ERR_INVALID_ARG;
+  if (!prefill_varlen_shape_ok(*d)) return EG_MLA_ERR_UNSUPPORTED;
+  if (total_tokens == 0) return EG_MLA_OK;
+  if (!cu_seqlens || !q || !latent || !token_ids || !gate_table || !w_uk || !w_uv || !out)
+    return EG_MLA_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(latent) || !aligned16(gate_table) || !aligned16(w_uk) || !aligned16(w_uv) ||
+      !aligned16(out))
+    return EG_MLA_ERR_INVALID_ARG;
+  if (!workspace || workspace_bytes < prefill_varlen_layout(*d, total_tokens).bytes) return EG_MLA_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return EG_MLA_ERR_WORKSPACE;
+  return EG_MLA_OK;
+}
+
 }  // namespace egmla
 
 extern "C" {
@@ -229,6 +265,11 @@ size_t eg_mla_decode_workspace_size(const eg_mla_dims* dims, int32_t batch, int3
 size_t eg_mla_prefill_workspace_size(const eg_mla_dims* dims, int32_t seq_len) {
   if (egmla::check_dims(dims) != EG_MLA_OK || seq_len < 0) return 0;
   return egmla::prefill_workspace_bytes(*dims, seq_len);
+}
+
+size_t eg_mla_prefill_varlen_workspace_size(const eg_mla_dims* dims, int32_t total_tokens) {
+  if (egmla::check_dims(dims) != EG_MLA_OK || total_tokens < 0 || !egmla::prefill_varlen_shape_ok(*dims)) return 0;
+  return egmla::prefill_varlen_layout(*dims, total_tokens).bytes;
 }
 
 }  // extern "C"

@@ -83,6 +83,18 @@ eg_mla_status validate_prefill(const eg_mla_dims* d, int32_t seq_len, const void
                                const void* w_uv, const void* workspace, size_t workspace_bytes,
                                const void* out);
 
+// Batched (packed, variable-length) causal prefill on MFMA.
+struct PrefillVarlenLayout {
+  size_t off_seq_start, off_qf, off_olat, bytes;
+};
+PrefillVarlenLayout prefill_varlen_layout(const eg_mla_dims& d, int32_t total_tokens);
+bool prefill_varlen_shape_ok(const eg_mla_dims& d);
+eg_mla_status validate_prefill_varlen(const eg_mla_dims* d, int32_t batch, int32_t total_tokens,
+                                      const int32_t* cu_seqlens, const void* q, const void* latent,
+                                      const int32_t* token_ids, const void* gate_table, const void* w_uk,
+                                      const void* w_uv, const void* workspace, size_t workspace_bytes,
+                                      const void* out);
+
 inline float softmax_scale(const eg_mla_dims& d) {
   if (d.softmax_scale > 0.f) return d.softmax_scale;
   return 1.0f / __builtin_sqrtf(static_cast<float>(d.head_dim + d.rope_dim));

@@ -12,6 +12,8 @@
 #include "device_common.h"
 #include "eg_mla.h"
 #include "host_plan.h"
+#include "aux_mfma.h"
+#include "prefill_mfma.h"
 
 namespace egmla {
 
@@ -144,4 +146,47 @@ extern "C" eg_mla_status eg_mla_prefill_ref(const eg_mla_dims* dims, int32_t seq
   if (d.dtype == EG_MLA_BF16)
     return launch_prefill<true>(d, seq_len, q, latent, token_ids, gate_table, w_uk, w_uv, K, Vv, out, stream);
   return launch_prefill<false>(d, seq_len, q, latent, token_ids, gate_table, w_uk, w_uv, K, Vv, out, stream);
+}
+
+extern "C" eg_mla_status eg_mla_prefill_varlen(const eg_mla_dims* dims, int32_t batch, int32_t total_tokens,
+                                               const int32_t* cu_seqlens, const void* q, const void* latent,
+                                               const int32_t* token_ids, const void* gate_table, const void* w_uk,
+                                               const void* w_uv, void* workspace, size_t workspace_bytes, void* out,
+                                               void* stream_) {
+  eg_mla_status st = validate_prefill_varlen(dims, batch, total_tokens, cu_seqlens, q, latent, token_ids,
+                                             gate_table, w_uk, w_uv, workspace, workspace_bytes, out);
+  if (st != EG_MLA_OK || total_tokens == 0) return st;
+  const eg_mla_dims& d = *dims;
+  const int T = total_tokens;
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  (void)hipGetLastError();
+  const PrefillVarlenLayout L = prefill_varlen_layout(d, T);
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  int32_t* seq_start = reinterpret_cast<int32_t*>(ws + L.off_seq_start);
+  uint16_t* qf = reinterpret_cast<uint16_t*>(ws + L.off_qf);
+  float* olat = reinterpret_cast<float*>(ws + L.off_olat);
+
+  hipLaunchKernelGGL(prefill_seqmap_kernel, dim3((T + 255) / 256), dim3(256), 0, stream, cu_seqlens, batch, T,
+                     seq_start);
+  // q_lat (bf16) and q^R for every token: the absorption with tokens as its batch
+  const int rows = kAbsRows * kAbsBlocks;
+  hipLaunchKernelGGL((absorb_mfma_kernel<128, kAbsBlocks, kAbsCols, true>), dim3(d.num_heads, (T + rows - 1) / rows, 1),
+                     dim3(256), 0, stream, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(w_uk),
+                     reinterpret_cast<float*>(qf), T, d.num_heads, d.latent_dim, d.rope_dim);
+  PrefillArgs a;
+  a.qf = qf;
+  a.latent = static_cast<const uint16_t*>(latent);
+  a.ids = token_ids;
+  a.gate = static_cast<const uint16_t*>(gate_table);
+  a.seq_start = seq_start;
+  a.olat = olat;
+  a.T = T;
+  a.V = d.vocab_size;
+  a.scale_log2 = softmax_scale(d) * 1.4426950408889634f;
+  const size_t lds = 2 * kPfBufBytes;
+  hipLaunchKernelGGL(prefill_attn_mfma_kernel, dim3((T + kPfTokens - 1) / kPfTokens), dim3(kPfThreads), lds, stream,
+                     a);
+  hipLaunchKernelGGL(prefill_uv_kernel, dim3((T + kPfUvTokens - 1) / kPfUvTokens, d.num_heads), dim3(256), 0, stream,
+                     olat, static_cast<const uint16_t*>(w_uv), static_cast<uint16_t*>(out), T);
+  return hipGetLastError() == hipSuccess ? EG_MLA_OK : EG_MLA_ERR_HIP;
 }

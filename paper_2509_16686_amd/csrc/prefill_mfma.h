@@ -1,0 +1,360 @@
+// Causal prefill of EG-MLA on gfx950 MFMA, in the absorbed form of App. C
+// Eq. (C.13) with the latent-space gate of Sec. 3.1 Eq. (5), for d_c = 128,
+// d_r = 64, d_h = d_v = 128 and 16 heads (bf16 storage).  Included by
+// prefill.hip.
+//
+// Every query row (token t, head h) attends to the gated latents c~_j and RoPE
+// keys k^R_j of its own sequence's tokens j <= t:
+//   s = tau (q_lat[t,h] . c~_j + q^R[t,h] . k^R_j),   q_lat = W_UK[h]^T q^C,
+//   o_lat[t,h] = sum_j softmax_j(s) c~_j,   out[t,h] = W_UV[h] o_lat[t,h].
+// All 16 heads share one key and value per token (the latent), so a tile of
+// keys serves 256 query rows at once: the kernel is a multi-query flash
+// attention with 192-dim keys and 128-dim values.
+//
+// Four launches: a map from each token to its sequence's first token; the
+// absorption (q_lat in bf16, with q^R, for every token: the decode's kernel
+// with tokens as its batch); the attention kernel below, which writes o_lat / l
+// in fp32; and the up-projection by W_UV per head (o_lat as bf16 hi + lo).
+//
+// Attention kernel.  A work-group (8 waves) takes 16 consecutive tokens of the
+// packed token stream (a block may straddle sequences: each row masks keys
+// outside its own sequence) and walks tiles of 64 keys from the first token's
+// sequence start to the block's last token.  Blocks are launched heaviest
+// first (last in the stream first).
+//  * Tile: 256 threads each load two 16-byte latent pieces with the matching
+//    gate pieces and one RoPE piece of the next tile while the current one is
+//    computed; the gated latent (exact fp32 products, one bf16 rounding) is
+//    written to the other of two LDS buffers.  Rows of 256 bytes hold the
+//    16-byte pieces XOR-swizzled by f(key) = 4 (key % 4) + (key / 4) % 4, RoPE
+//    rows of 128 bytes by (key / 2) % 8: the 16 lanes of a 16-byte read cycle
+//    and the 32 lanes of a transposed 8-byte read cycle each hit distinct banks.
+//  * Scores: wave w holds rows (tokens 2w, 2w + 1) x 16 heads = 32 rows, its
+//    query in registers as the B operand of v_mfma_f32_32x32x16_bf16 (lane:
+//    row lane % 32, dims 8 (lane / 32) + 16 c).  S^T[key][row] comes from 12
+//    products per 32 keys with the tile rows as the A operand.
+//  * Online softmax per row in the log2 domain, lazy rescale (as the decode).
+//    A lane holds 16 of each 32 keys' scores of its row; the other 16 are in
+//    lane ^ 32 (one permlane32 swap for the maximum; the sums are combined
+//    once at the end).
+//  * Values: O^T[dim][row] += C~^T P^T.  In the score accumulator lane L holds
+//    keys 8q + 4 (L / 32) + 0..3 (q = 0..3) of each 32; the value product sums
+//    over keys in any order that its two operands share, so the B operand of
+//    16-key chunk m is the lane's own probabilities of q = 2m, 2m + 1 (no lane
+//    exchange), and the A operand is two ds_read_b64_tr_b16 of the tile (one
+//    dim per lane, keys 16 m + 4 (L / 32) + 0..3 and 16 m + 8 + 4 (L / 32) + 0..3).
+#pragma once
+
+namespace egmla {
+
+constexpr int kPfTokens = 16;     // query tokens per work-group (x 16 heads = 256 rows)
+constexpr int kPfHeads = 16;
+constexpr int kPfKeys = 64;       // keys per tile
+constexpr int kPfThreads = 512;   // 8 waves, 32 query rows each
+constexpr int kPfDC = 128, kPfDR = 64, kPfDQ = kPfDC + kPfDR;
+constexpr int kPfLatRow = 2 * kPfDC;    // bytes per key row of the gated latent
+constexpr int kPfRopeRow = 2 * kPfDR;   // bytes per key row of the RoPE key
+constexpr int kPfLatBytes = kPfKeys * kPfLatRow;
+constexpr int kPfBufBytes = kPfLatBytes + kPfKeys * kPfRopeRow;  // one tile buffer (24 KB)
+constexpr int kPfUvTokens = 128;  // up-projection: tokens per work-group (4 waves x 32)
+
+typedef __attribute__((ext_vector_type(16))) float pf_f32x16_t;
+
+__device__ __forceinline__ int pf_lat_swz(int key) { return ((key & 3) << 2) | ((key >> 2) & 3); }
+__device__ __forceinline__ int pf_rope_swz(int key) { return (key >> 1) & 7; }
+
+// Maximum and sum of lanes i and i ^ 32, the same value (same order) in both.
+__device__ __forceinline__ float pf_pair_max(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const auto s = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return fmaxf(__uint_as_float(s[0]), __uint_as_float(s[1]));
+}
+__device__ __forceinline__ float pf_pair_sum(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const auto s = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return __uint_as_float(s[0]) + __uint_as_float(s[1]);
+}
+
+// seq_start[t] = the first token of t's sequence (cu_seqlens[b] for the last b
+// with cu_seqlens[b] <= t), clamped into [0, t].
+__global__ __launch_bounds__(256) void prefill_seqmap_kernel(const int32_t* __restrict__ cu, int B, int T,
+                                                             int32_t* __restrict__ seq_start) {
+  const int t = blockIdx.x * 256 + threadIdx.x;
+  if (t >= T) return;
+  int lo = 0, hi = B - 1;  // largest b in [0, B) with cu[b] <= t (b = 0 if none)
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (cu[mid] <= t) lo = mid;
+    else hi = mid - 1;
+  }
+  seq_start[t] = min(max(cu[lo], 0), t);
+}
+
+struct PrefillArgs {
+  const uint16_t* qf;          // [T][16][192] bf16: q_lat | q^R
+  const uint16_t* latent;      // [T][192] bf16: c | k^R
+  const int32_t* ids;          // [T]
+  const uint16_t* gate;        // [V][128] bf16
+  const int32_t* seq_start;    // [T]
+  float* olat;                 // [T][16][128] fp32: o_lat / l
+  int T, V;
+  float scale_log2;            // tau log2(e)
+};
+
+__global__ __launch_bounds__(kPfThreads, 1) void prefill_attn_mfma_kernel(PrefillArgs a) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds[];  // two tile buffers
+  const int nblk = (a.T + kPfTokens - 1) / kPfTokens;
+  const int q0 = (nblk - 1 - static_cast<int>(blockIdx.x)) * kPfTokens;  // heaviest blocks first
+  const int q_last = min(q0 + kPfTokens, a.T) - 1;
+  const int kbeg = min(max(a.seq_start[q0], 0), q0);                 // keys from here ...
+  const int kend = q_last + 1;                                       // ... to here (exclusive)
+  const int s_max = min(max(a.seq_start[q_last], kbeg), q_last);     // latest sequence start in the block
+  const int ntiles = (kend - kbeg + kPfKeys - 1) / kPfKeys;
+
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r32 = lane & 31, h = lane >> 5;
+  const int r16 = lane & 15, R1 = (lane >> 4) & 1;
+  // this lane's query row; rows past the stream repeat its last token and are not stored
+  const int t_row = q0 + 2 * w + (r32 >> 4);
+  const bool row_ok = t_row < a.T;
+  const int t_c = min(t_row, a.T - 1);
+  const int head = r32 & 15;
+  const int s_row = min(max(a.seq_start[t_c], kbeg), t_c);
+
+  bf16x8_t qv[kPfDQ / 16];
+  {
+    const uint16_t* qrow = a.qf + (static_cast<int64_t>(t_c) * kPfHeads + head) * kPfDQ + 8 * h;
+#pragma unroll
+    for (int c = 0; c < kPfDQ / 16; ++c) qv[c] = *reinterpret_cast<const bf16x8_t*>(qrow + 16 * c);
+  }
+
+  // tile loads: latent/gate pieces pl of keys kl and kl + 32, RoPE piece pr of key kr
+  const int kl = tid >> 4, pl = tid & 15, kr = tid >> 3, pr = tid & 7;
+  auto key_at = [&](int tile, int k) { return min(kbeg + tile * kPfKeys + k, kend - 1); };
+  u32x4_t nl[2], ng[2], nr;
+  int idn[2];
+  auto load_ids = [&](int tile) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) idn[j] = clamp_id(a.ids[key_at(tile, kl + 32 * j)], a.V);
+  };
+  auto load_tile = [&](int tile) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      nl[j] = *reinterpret_cast<const u32x4_t*>(a.latent + static_cast<int64_t>(key_at(tile, kl + 32 * j)) * kPfDQ +
+                                                 8 * pl);
+      ng[j] = *reinterpret_cast<const u32x4_t*>(a.gate + static_cast<int64_t>(idn[j]) * kPfDC + 8 * pl);
+    }
+    nr = *reinterpret_cast<const u32x4_t*>(a.latent + static_cast<int64_t>(key_at(tile, kr)) * kPfDQ + kPfDC + 8 * pr);
+  };
+  auto store_tile = [&](int buf) {
+    unsigned char* base = lds + buf * kPfBufBytes;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int key = kl + 32 * j;
+      *reinterpret_cast<u32x4_t*>(base + key * kPfLatRow + 16 * (pl ^ pf_lat_swz(key))) = gate_chunk(nl[j], ng[j]);
+    }
+    *reinterpret_cast<u32x4_t*>(base + kPfLatBytes + kr * kPfRopeRow + 16 * (pr ^ pf_rope_swz(kr))) = nr;
+  };
+
+  // per-lane LDS offsets (bytes within a tile buffer)
+  const int off_sl = r32 * kPfLatRow;               // score A: key row 32 kb + r32 (+ 32 kb rows)
+  const int swz_sl = pf_lat_swz(r32);
+  const int off_sr = kPfLatBytes + r32 * kPfRopeRow;
+  const int swz_sr = pf_rope_swz(r32);
+  // value A (transposed reads): rows 16 m + 4 h + r16 / 4 (+ 8), byte 8 (r16 % 2) of the piece
+  const int off_v = (4 * h + (r16 >> 2)) * kPfLatRow + 8 * (r16 & 1);
+  const int vlo = 2 * R1 + ((r16 & 3) >> 1);  // low 2 bits of the logical piece
+
+  pf_f32x16_t o[kPfDC / 32];
+#pragma unroll
+  for (int db = 0; db < kPfDC / 32; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
+  float m_run = -1e30f, l_run = 0.f;  // finite start: a fully masked tile leaves both unchanged
+
+  load_ids(0);
+  load_tile(0);
+  if (ntiles > 1) load_ids(1);
+  store_tile(0);
+  __syncthreads();
+
+  for (int i = 0; i < ntiles; ++i) {
+    if (i + 1 < ntiles) {
+      load_tile(i + 1);
+      if (i + 2 < ntiles) load_ids(i + 2);
+    }
+    const unsigned char* tb = lds + (i & 1) * kPfBufBytes;
+    const int k_lo = kbeg + i * kPfKeys;
+
+    // ---- scores S^T[key][row] for keys k_lo + 32 kb + (0..31) ----
+    pf_f32x16_t s[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
+#pragma unroll
+    for (int c = 0; c < kPfDC / 16; ++c)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const bf16x8_t av = *reinterpret_cast<const bf16x8_t*>(tb + off_sl + 32 * kb * kPfLatRow +
+                                                                16 * ((2 * c + h) ^ swz_sl));
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qv[c], s[kb], 0, 0, 0);
+      }
+#pragma unroll
+    for (int c = 0; c < kPfDR / 16; ++c)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const bf16x8_t av = *reinterpret_cast<const bf16x8_t*>(tb + off_sr + 32 * kb * kPfRopeRow +
+                                                                16 * ((2 * c + h) ^ swz_sr));
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qv[kPfDC / 16 + c], s[kb], 0, 0, 0);
+      }
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[kb][r] *= a.scale_log2;
+    // keys outside [s_row, t_row] (or past the block) only in tiles that reach
+    // past the block's first token or start before its latest sequence start
+    if (k_lo + kPfKeys - 1 > q0 || k_lo < s_max) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = k_lo + 32 * kb + 8 * (r >> 2) + 4 * h + (r & 3);
+          if (key < s_row || key > t_c) s[kb][r] = -INFINITY;
+        }
+    }
+
+    // ---- online softmax (row = lane % 32; keys split between lanes L and L ^ 32) ----
+    float mt = s[0][0];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[kb][r]);
+    mt = pf_pair_max(mt);
+    const float m_new = fmaxf(m_run, mt);
+    const bool grow = m_new > m_run + kLazyRescale;
+    const float alpha = grow ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.0f;
+    m_run = grow ? m_new : m_run;
+    l_run *= alpha;
+    if (__builtin_amdgcn_ballot_w64(grow)) {
+#pragma unroll
+      for (int db = 0; db < kPfDC / 32; ++db) o[db] *= alpha;
+    }
+    bf16x8_t pb[2][2];  // [kb][16-key chunk m]: keys 16 m + 8 (e / 4) + 4 h + e % 4 of element e
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int m = 0; m < 2; ++m) {
+        float p[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          p[e] = __builtin_amdgcn_exp2f(s[kb][8 * m + e] - m_run);
+          l_run += p[e];
+        }
+        pb[kb][m] = __builtin_bit_cast(bf16x8_t, u32x4_t{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
+                                                         pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7])});
+      }
+
+    // ---- values O^T[dim][row] += C~^T P^T ----
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int m = 0; m < 2; ++m) {
+        const unsigned char* vp = tb + off_v + (32 * kb + 16 * m) * kPfLatRow;
+#pragma unroll
+        for (int db = 0; db < kPfDC / 32; ++db) {
+          // logical piece 4 db + vlo; rows +0 and +8 swizzle with 4 (r16 / 4) + h and + 2
+          const int p0 = 4 * (db ^ (r16 >> 2)) + (vlo ^ h);
+          const int p1 = 4 * (db ^ (r16 >> 2)) + (vlo ^ (h + 2));
+          const s16x4_t a0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) s16x4_t*)(vp + 16 * p0));
+          const s16x4_t a1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) s16x4_t*)(vp + 8 * kPfLatRow + 16 * p1));
+          const bf16x8_t av =
+              __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
+          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[kb][m], o[db], 0, 0, 0);
+        }
+      }
+
+    if (i + 1 < ntiles) store_tile((i + 1) & 1);
+    __syncthreads();
+  }
+
+  // ---- o_lat / l: lane holds dims 32 db + 8 q + 4 h + 0..3 of its row ----
+  const float inv = 1.0f / pf_pair_sum(l_run);
+  if (row_ok) {
+    float* orow = a.olat + (static_cast<int64_t>(t_row) * kPfHeads + head) * kPfDC + 4 * h;
+#pragma unroll
+    for (int db = 0; db < kPfDC / 32; ++db)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        *reinterpret_cast<f32x4_t*>(orow + 32 * db + 8 * q) =
+            f32x4_t{o[db][4 * q] * inv, o[db][4 * q + 1] * inv, o[db][4 * q + 2] * inv, o[db][4 * q + 3] * inv};
+  }
+}
+
+// out[t, h, :] = W_UV[h] o_lat[t, h, :] for 128 tokens of one head per
+// work-group (4 waves of 32 tokens): W_UV[h] ([d_v][d_c], rows padded by 16
+// bytes) in LDS as the A operand, o_lat rows straight from global as the B
+// operand, split into bf16 hi + lo (two products, so o_lat keeps ~16 bits);
+// the accumulator holds out^T, stored 4 consecutive v at a time.
+__global__ __launch_bounds__(256) void prefill_uv_kernel(const float* __restrict__ olat,
+                                                         const uint16_t* __restrict__ w_uv,
+                                                         uint16_t* __restrict__ out, int T) {
+  constexpr int DV = 128, RS = kPfDC + 8;
+  __shared__ __attribute__((aligned(16))) uint16_t wl[DV * RS];
+  const int hh = blockIdx.y;
+  const int t0 = blockIdx.x * kPfUvTokens;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r32 = lane & 31, h = lane >> 5;
+  const int t = t0 + 32 * w + r32;
+  const int tc = min(t, T - 1);
+  bf16x8_t ob_hi[kPfDC / 16], ob_lo[kPfDC / 16];
+  {
+    const float* orow = olat + (static_cast<int64_t>(tc) * kPfHeads + hh) * kPfDC + 8 * h;
+    f32x4_t ov[kPfDC / 16][2];
+#pragma unroll
+    for (int c = 0; c < kPfDC / 16; ++c)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) ov[c][j] = *reinterpret_cast<const f32x4_t*>(orow + 16 * c + 4 * j);
+#pragma unroll
+    for (int c = 0; c < kPfDC / 16; ++c) {
+      uint32_t hi[4], lo[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float x0 = ov[c][e >> 1][2 * (e & 1)], x1 = ov[c][e >> 1][2 * (e & 1) + 1];
+        hi[e] = pack_bf16x2(x0, x1);
+        lo[e] = pack_bf16x2(x0 - bf16_lo(hi[e]), x1 - bf16_hi(hi[e]));
+      }
+      ob_hi[c] = __builtin_bit_cast(bf16x8_t, u32x4_t{hi[0], hi[1], hi[2], hi[3]});
+      ob_lo[c] = __builtin_bit_cast(bf16x8_t, u32x4_t{lo[0], lo[1], lo[2], lo[3]});
+    }
+  }
+  for (int p = tid; p < DV * kPfDC / 8; p += 256) {
+    const int v = p / (kPfDC / 8), k8 = (p % (kPfDC / 8)) * 8;
+    *reinterpret_cast<u32x4_t*>(wl + v * RS + k8) =
+        *reinterpret_cast<const u32x4_t*>(w_uv + (static_cast<int64_t>(hh) * DV + v) * kPfDC + k8);
+  }
+  __syncthreads();
+  pf_f32x16_t acc[DV / 32];
+#pragma unroll
+  for (int vb = 0; vb < DV / 32; ++vb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[vb][r] = 0.f;
+#pragma unroll
+  for (int c = 0; c < kPfDC / 16; ++c)
+#pragma unroll
+    for (int vb = 0; vb < DV / 32; ++vb) {
+      const bf16x8_t av = *reinterpret_cast<const bf16x8_t*>(wl + (32 * vb + r32) * RS + 16 * c + 8 * h);
+      acc[vb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, ob_hi[c], acc[vb], 0, 0, 0);
+      acc[vb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, ob_lo[c], acc[vb], 0, 0, 0);
+    }
+  if (t < T) {
+    uint16_t* dst = out + (static_cast<int64_t>(t) * kPfHeads + hh) * DV + 4 * h;
+#pragma unroll
+    for (int vb = 0; vb < DV / 32; ++vb)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        *reinterpret_cast<u32x2_t*>(dst + 32 * vb + 8 * q) =
+            u32x2_t{pack_bf16x2(acc[vb][4 * q], acc[vb][4 * q + 1]), pack_bf16x2(acc[vb][4 * q + 2], acc[vb][4 * q + 3])};
+  }
+}
+
+}  // namespace egmla

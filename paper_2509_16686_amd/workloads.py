@@ -322,6 +322,36 @@ def generate_prefill(wl: Workload, seq_len: int, seed: Optional[int] = None) -> 
                          w_uv=_store(w_uv, wl.dtype))
 
 
+@dataclass
+class PrefillBatch:
+    """Host arrays for a causal prefill of several sequences packed back to back."""
+
+    wl: Workload
+    cu_seqlens: np.ndarray  # [B + 1] int32 offsets
+    q: np.ndarray           # [T, H, d_h + d_r]
+    latent: np.ndarray      # [T, d_c + d_r]
+    token_ids: np.ndarray   # [T] int32
+    gate_table: np.ndarray
+    w_uk: np.ndarray
+    w_uv: np.ndarray
+
+    def sequence(self, b: int) -> PrefillInputs:
+        """Sequence b alone, as a single-sequence prefill (views of the packed arrays)."""
+        lo, hi = int(self.cu_seqlens[b]), int(self.cu_seqlens[b + 1])
+        return PrefillInputs(wl=self.wl, q=self.q[lo:hi], latent=self.latent[lo:hi], token_ids=self.token_ids[lo:hi],
+                             gate_table=self.gate_table, w_uk=self.w_uk, w_uv=self.w_uv)
+
+
+def generate_prefill_batch(wl: Workload, seq_lens, seed: Optional[int] = None) -> PrefillBatch:
+    """Sequences of the given lengths (zeros allowed) drawn as one prefill of their total, then split."""
+    lens = np.asarray(seq_lens, dtype=np.int64)
+    cu = np.zeros(len(lens) + 1, dtype=np.int32)
+    cu[1:] = np.cumsum(lens)
+    one = generate_prefill(wl, int(cu[-1]), seed=seed)
+    return PrefillBatch(wl=wl, cu_seqlens=cu, q=one.q, latent=one.latent, token_ids=one.token_ids,
+                        gate_table=one.gate_table, w_uk=one.w_uk, w_uv=one.w_uv)
+
+
 def small_workload(base: Workload, **kw) -> Workload:
     """A reduced copy of ``base`` for parity tests that the oracle finishes in seconds."""
     return base.replace(**kw)

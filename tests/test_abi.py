@@ -150,3 +150,30 @@ def test_gate_rows_rejects_before_launch(L):
     assert L.eg_mla_gate_rows(ctypes.byref(d), 20000, 1000, 5, vp, vp, vp, vp, None) == B.ERR_UNSUPPORTED
     bad = dims(gate_dim=64)
     assert L.eg_mla_gate_rows(ctypes.byref(bad), 512, 1000, 5, vp, vp, vp, vp, None) == B.ERR_UNSUPPORTED
+
+
+def test_prefill_varlen_rejects_before_launch(L):
+    d = dims()
+    vp = ctypes.c_void_p(256)
+    ws = ctypes.c_void_p(4096)
+    n = 100
+    need = L.eg_mla_prefill_varlen_workspace_size(ctypes.byref(d), n)
+    assert need >= n * 16 * (192 + 128) * 2
+    args = lambda **kw: [kw.get(k, v) for k, v in [("cu", vp), ("q", vp), ("lat", vp), ("ids", vp), ("gate", vp),
+                                                     ("wk", vp), ("wv", vp), ("ws", ws), ("wsb", need),
+                                                     ("out", vp)]]
+    call = lambda dd, batch, T, **kw: L.eg_mla_prefill_varlen(ctypes.byref(dd), batch, T, *args(**kw), None)
+    # zero tokens is a no-op whatever the pointers
+    assert L.eg_mla_prefill_varlen(ctypes.byref(d), 1, 0, *[None] * 7, None, 0, None, None) == B.OK
+    assert call(d, 0, n) == B.ERR_INVALID_ARG
+    assert call(d, 2, -1) == B.ERR_INVALID_ARG
+    assert call(d, 2, n, cu=None) == B.ERR_INVALID_ARG
+    assert call(d, 2, n, out=None) == B.ERR_INVALID_ARG
+    assert call(d, 2, n, q=ctypes.c_void_p(258)) == B.ERR_INVALID_ARG  # misaligned
+    assert call(d, 2, n, wsb=need - 1) == B.ERR_WORKSPACE
+    assert call(d, 2, n, ws=ctypes.c_void_p(4100)) == B.ERR_WORKSPACE
+    # the MFMA prefill covers the d_c 128 / d_r 64 / 16-head bf16 layer only
+    for bad in (dims(num_heads=32), dims(latent_dim=512), dims(rope_dim=32), dims(dtype=B.FP32),
+                dims(v_head_dim=64)):
+        assert call(bad, 2, n) == B.ERR_UNSUPPORTED
+        assert L.eg_mla_prefill_varlen_workspace_size(ctypes.byref(bad), n) == 0

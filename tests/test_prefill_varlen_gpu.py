@@ -1,0 +1,93 @@
+"""GPU parity of eg_mla_prefill_varlen (App. C Eq. (C.13), absorbed, with the
+latent-space gate of Sec. 3.1 Eq. (5)) against the fp64 oracle's single-sequence
+prefill, run sequence by sequence over the same packed inputs."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import eg_mla_oracle as orc
+from paper_2509_16686_amd import binding as B
+from paper_2509_16686_amd import workloads as W
+from parity import assert_close, say
+
+pytestmark = pytest.mark.gpu
+
+LAYER = W.WORKLOADS[1]  # 16 heads, d_c 128, d_r 64, bf16
+
+
+def run_varlen(pb):
+    wl = pb.wl
+    T = int(pb.cu_seqlens[-1])
+    dims = B.dims_for(wl)
+    ws = B.alloc_workspace(B.prefill_varlen_workspace_size(dims, T))
+    out = torch.empty((T, wl.heads, wl.v_head_dim), dtype=torch.bfloat16, device="cuda")
+    st = wl.dtype
+    B.prefill_varlen(dims, B.to_device_tensor(pb.cu_seqlens, "int"), B.to_device_tensor(pb.q, st),
+                     B.to_device_tensor(pb.latent, st), B.to_device_tensor(pb.token_ids, "int"),
+                     B.to_device_tensor(pb.gate_table, st), B.to_device_tensor(pb.w_uk, st),
+                     B.to_device_tensor(pb.w_uv, st), ws, out)
+    torch.cuda.synchronize()
+    return B.out_to_f64(out)
+
+
+def oracle_varlen(pb):
+    wl = pb.wl
+    parts = []
+    for b in range(len(pb.cu_seqlens) - 1):
+        s = pb.sequence(b)
+        if s.q.shape[0] == 0:
+            continue
+        parts.append(orc.prefill(s.q, s.latent, s.token_ids, s.gate_table, s.w_uk, s.w_uv, latent_dim=wl.latent_dim,
+                                 head_dim=wl.head_dim, rope_dim=wl.rope_dim, storage=wl.dtype))
+    return np.concatenate(parts, 0)
+
+
+@pytest.mark.parametrize("lens", [
+    [1],                          # one token: the tile holds a single key
+    [16],                         # one full block
+    [17, 15],                     # a block straddling two sequences
+    [300],                        # several tiles, ragged last tile
+    [5, 0, 64, 1, 130, 0, 33],    # empty sequences, exact tiles, short ones
+    [1000, 3, 700],               # long sequences around a short one
+])
+def test_prefill_varlen_matches_oracle(gpu, lens):
+    pb = W.generate_prefill_batch(LAYER, lens, seed=61)
+    say(f"prefill_varlen lens={lens}")
+    got = run_varlen(pb)
+    ref = oracle_varlen(pb)
+    # short sequences give outputs of a few units: the bf16 bound scales with max|ref|
+    assert_close(got, ref, "bf16", f"prefill varlen {lens}", scaled=True)
+
+
+def test_prefill_varlen_equals_prefill_ref(gpu):
+    # the same sequence through the MFMA path and the plain explicit-form kernels
+    wl = LAYER
+    pb = W.generate_prefill_batch(wl, [257], seed=62)
+    say("prefill_varlen vs prefill_ref T=257")
+    got = run_varlen(pb)
+    T = 257
+    dims = B.dims_for(wl)
+    ws = B.alloc_workspace(B.prefill_workspace_size(dims, T))
+    out = torch.empty((T, wl.heads, wl.v_head_dim), dtype=torch.bfloat16, device="cuda")
+    B.prefill_ref(dims, B.to_device_tensor(pb.q, "bf16"), B.to_device_tensor(pb.latent, "bf16"),
+                  B.to_device_tensor(pb.token_ids, "int"), B.to_device_tensor(pb.gate_table, "bf16"),
+                  B.to_device_tensor(pb.w_uk, "bf16"), B.to_device_tensor(pb.w_uv, "bf16"), ws, out)
+    torch.cuda.synchronize()
+    assert_close(got, B.out_to_f64(out), "bf16", "varlen vs ref", scaled=True)
+
+
+def test_prefill_varlen_long_sequence_sampled(gpu):
+    # 4096 tokens (the decode workload's context): every 97th row against the oracle's causal row
+    wl = LAYER
+    T = 4096
+    pb = W.generate_prefill_batch(wl, [T], seed=63)
+    say("prefill_varlen T=4096 sampled rows")
+    got = run_varlen(pb)
+    rows = np.arange(0, T, 97)
+    rows = np.append(rows, T - 1)
+    # row t of a causal prefill is the decode of the prefix 0..t with query q_t
+    ref = orc.decode(pb.q[rows], pb.latent, pb.token_ids, pb.gate_table, pb.w_uk, pb.w_uv,
+                     (rows + 1).astype(np.int32), latent_dim=wl.latent_dim, head_dim=wl.head_dim,
+                     rope_dim=wl.rope_dim, storage="bf16", page_table=np.zeros((len(rows), T // 64), np.int32)
+                     + np.arange(T // 64, dtype=np.int32)[None, :], page_size=64, max_pages=T // 64)
+    assert_close(got[rows], ref, "bf16", "prefill varlen T=4096 sampled", scaled=True)
