@@ -8,21 +8,24 @@
 //   s = tau (q_lat[t,h] . c~_j + q^R[t,h] . k^R_j),   q_lat = W_UK[h]^T q^C,
 //   o_lat[t,h] = sum_j softmax_j(s) c~_j,   out[t,h] = W_UV[h] o_lat[t,h].
 // All 16 heads share one key and value per token (the latent), so a tile of
-// keys serves 256 query rows at once: the kernel is a multi-query flash
-// attention with 192-dim keys and 128-dim values.
+// keys serves every head of a work-group's tokens at once (128 query rows):
+// the kernel is a multi-query flash attention with 192-dim keys and 128-dim
+// values.
 //
 // Four launches: a map from each token to its sequence's first token; the
 // absorption (q_lat in bf16, with q^R, for every token: the decode's kernel
 // with tokens as its batch); the attention kernel below, which writes o_lat / l
 // in fp32; and the up-projection by W_UV per head (o_lat as bf16 hi + lo).
 //
-// Attention kernel.  A work-group (8 waves) takes 16 consecutive tokens of the
+// Attention kernel.  A work-group (4 waves; two per CU, whose barriers are
+// independent, so that one's softmax overlaps the other's products on the
+// same SIMDs) takes 8 consecutive tokens of the
 // packed token stream (a block may straddle sequences: each row masks keys
 // outside its own sequence) and walks tiles of 64 keys from the first token's
 // sequence start to the block's last token.  Blocks are launched heaviest
 // first (last in the stream first).
-//  * Tile: 256 threads each load two 16-byte latent pieces with the matching
-//    gate pieces and one RoPE piece of the next tile while the current one is
+//  * Tile: 256 threads each load four 16-byte latent pieces with the matching
+//    gate pieces and two RoPE pieces of the next tile while the current one is
 //    computed; the gated latent (exact fp32 products, one bf16 rounding) is
 //    written to the other of two LDS buffers.  Rows of 256 bytes hold the
 //    16-byte pieces XOR-swizzled by f(key) = 4 (key % 4) + (key / 4) % 4, RoPE
@@ -46,10 +49,10 @@
 
 namespace egmla {
 
-constexpr int kPfTokens = 16;     // query tokens per work-group (x 16 heads = 256 rows)
+constexpr int kPfTokens = 8;      // query tokens per work-group (x 16 heads = 128 rows)
 constexpr int kPfHeads = 16;
 constexpr int kPfKeys = 64;       // keys per tile
-constexpr int kPfThreads = 512;   // 8 waves, 32 query rows each
+constexpr int kPfThreads = 256;   // 4 waves, 32 query rows each; two work-groups per CU
 constexpr int kPfDC = 128, kPfDR = 64, kPfDQ = kPfDC + kPfDR;
 constexpr int kPfLatRow = 2 * kPfDC;    // bytes per key row of the gated latent
 constexpr int kPfRopeRow = 2 * kPfDR;   // bytes per key row of the RoPE key
@@ -100,7 +103,7 @@ struct PrefillArgs {
   float scale_log2;            // tau log2(e)
 };
 
-__global__ __launch_bounds__(kPfThreads, 1) void prefill_attn_mfma_kernel(PrefillArgs a) {
+__global__ __launch_bounds__(kPfThreads, 2) void prefill_attn_mfma_kernel(PrefillArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];  // two tile buffers
   const int nblk = (a.T + kPfTokens - 1) / kPfTokens;
   const int q0 = (nblk - 1 - static_cast<int>(blockIdx.x)) * kPfTokens;  // heaviest blocks first
@@ -126,32 +129,40 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_attn_mfma_kernel(Prefil
     for (int c = 0; c < kPfDQ / 16; ++c) qv[c] = *reinterpret_cast<const bf16x8_t*>(qrow + 16 * c);
   }
 
-  // tile loads: latent/gate pieces pl of keys kl and kl + 32, RoPE piece pr of key kr
+  // tile loads: latent/gate pieces pl of keys kl + 16 j, RoPE piece pr of keys kr + 32 j
+  constexpr int NLJ = kPfKeys * (kPfDC / 8) / kPfThreads, NRJ = kPfKeys * (kPfDR / 8) / kPfThreads;
   const int kl = tid >> 4, pl = tid & 15, kr = tid >> 3, pr = tid & 7;
   auto key_at = [&](int tile, int k) { return min(kbeg + tile * kPfKeys + k, kend - 1); };
-  u32x4_t nl[2], ng[2], nr;
-  int idn[2];
+  u32x4_t nl[NLJ], ng[NLJ], nr[NRJ];
+  int idn[NLJ];
   auto load_ids = [&](int tile) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) idn[j] = clamp_id(a.ids[key_at(tile, kl + 32 * j)], a.V);
+    for (int j = 0; j < NLJ; ++j) idn[j] = clamp_id(a.ids[key_at(tile, kl + 16 * j)], a.V);
   };
   auto load_tile = [&](int tile) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      nl[j] = *reinterpret_cast<const u32x4_t*>(a.latent + static_cast<int64_t>(key_at(tile, kl + 32 * j)) * kPfDQ +
+    for (int j = 0; j < NLJ; ++j) {
+      nl[j] = *reinterpret_cast<const u32x4_t*>(a.latent + static_cast<int64_t>(key_at(tile, kl + 16 * j)) * kPfDQ +
                                                  8 * pl);
       ng[j] = *reinterpret_cast<const u32x4_t*>(a.gate + static_cast<int64_t>(idn[j]) * kPfDC + 8 * pl);
     }
-    nr = *reinterpret_cast<const u32x4_t*>(a.latent + static_cast<int64_t>(key_at(tile, kr)) * kPfDQ + kPfDC + 8 * pr);
+#pragma unroll
+    for (int j = 0; j < NRJ; ++j)
+      nr[j] = *reinterpret_cast<const u32x4_t*>(a.latent + static_cast<int64_t>(key_at(tile, kr + 32 * j)) * kPfDQ +
+                                                 kPfDC + 8 * pr);
   };
   auto store_tile = [&](int buf) {
     unsigned char* base = lds + buf * kPfBufBytes;
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int key = kl + 32 * j;
+    for (int j = 0; j < NLJ; ++j) {
+      const int key = kl + 16 * j;
       *reinterpret_cast<u32x4_t*>(base + key * kPfLatRow + 16 * (pl ^ pf_lat_swz(key))) = gate_chunk(nl[j], ng[j]);
     }
-    *reinterpret_cast<u32x4_t*>(base + kPfLatBytes + kr * kPfRopeRow + 16 * (pr ^ pf_rope_swz(kr))) = nr;
+#pragma unroll
+    for (int j = 0; j < NRJ; ++j) {
+      const int key = kr + 32 * j;
+      *reinterpret_cast<u32x4_t*>(base + kPfLatBytes + key * kPfRopeRow + 16 * (pr ^ pf_rope_swz(key))) = nr[j];
+    }
   };
 
   // per-lane LDS offsets (bytes within a tile buffer)
@@ -206,10 +217,6 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_attn_mfma_kernel(Prefil
                                                                 16 * ((2 * c + h) ^ swz_sr));
         s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qv[kPfDC / 16 + c], s[kb], 0, 0, 0);
       }
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) s[kb][r] *= a.scale_log2;
     // keys outside [s_row, t_row] (or past the block) only in tiles that reach
     // past the block's first token or start before its latest sequence start
     if (k_lo + kPfKeys - 1 > q0 || k_lo < s_max) {
@@ -223,12 +230,13 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_attn_mfma_kernel(Prefil
     }
 
     // ---- online softmax (row = lane % 32; keys split between lanes L and L ^ 32) ----
+    // the scale (tau log2 e > 0) commutes with the maximum; it is applied inside the exponent
     float mt = s[0][0];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[kb][r]);
-    mt = pf_pair_max(mt);
+    mt = pf_pair_max(mt) * a.scale_log2;
     const float m_new = fmaxf(m_run, mt);
     const bool grow = m_new > m_run + kLazyRescale;
     const float alpha = grow ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.0f;
@@ -246,7 +254,7 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_attn_mfma_kernel(Prefil
         float p[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          p[e] = __builtin_amdgcn_exp2f(s[kb][8 * m + e] - m_run);
+          p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][8 * m + e], a.scale_log2, -m_run));
           l_run += p[e];
         }
         pb[kb][m] = __builtin_bit_cast(bf16x8_t, u32x4_t{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
