@@ -155,6 +155,119 @@ def cpu_baseline(inp, seconds):
             "cpu_model": cpu_model(), "host_cpus": len(os.sched_getaffinity(0))}
 
 
+PREFILL_METRIC = "prefill tokens/s + achieved bf16 TFLOP/s (% of MFMA peak) for eg_mla_prefill_varlen, 1 GPU"
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def prefill_flops(lens, heads=16, dc=128, dr=64, dh=128, dv=128):
+    """Algorithmic flops of one causal prefill call: scores and values over every (row, key <= row)
+    pair of each sequence, plus the absorption and the up-projection of every row."""
+    pairs = sum(t * (t + 1) // 2 for t in lens)
+    rows = sum(lens) * heads
+    return pairs * heads * 2 * (dc + dr + dc) + rows * 2 * dh * dc + rows * 2 * dc * dv
+
+
+def prefill_cpu_baseline(wl, seconds):
+    """The fp64 oracle's prefill of one 512-token sequence, repeated for about `seconds`."""
+    from oracle import eg_mla_oracle as orc
+    from paper_2509_16686_amd import workloads as W
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i["num_threads"] for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:
+        threads = 1
+    pin = W.generate_prefill(wl, 512, seed=wl.seed + 3001)
+    reps = 0
+    t0 = time.perf_counter()
+    while True:
+        orc.prefill(pin.q, pin.latent, pin.token_ids, pin.gate_table, pin.w_uk, pin.w_uv, latent_dim=wl.latent_dim,
+                    head_dim=wl.head_dim, rope_dim=wl.rope_dim, storage=wl.dtype)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds or reps >= 100:
+            break
+    return {"value": 512 * reps / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{reps} causal prefills of one 512-token sequence of the same layer, {el:.1f} s, "
+                      f"numpy fp64 with {threads} BLAS threads",
+            "cpu_model": cpu_model(), "host_cpus": len(os.sched_getaffinity(0))}
+
+
+def prefill_main(args):
+    """Times eg_mla_prefill_varlen on `--prefill BxT` (B sequences of T tokens, packed)."""
+    import numpy as np
+    import torch
+
+    from paper_2509_16686_amd import binding as B
+    from paper_2509_16686_amd import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    L = B.lib()
+    hip = Hip()
+    nb, T = (int(x) for x in args.prefill.lower().split("x"))
+    lens = [T] * nb
+    wl = W.WORKLOADS[1]
+    log(f"bench: generating a prefill of {nb} x {T} tokens ({wl.name} layer)")
+    pb = W.generate_prefill_batch(wl, lens, seed=wl.seed + 3000)
+    total = int(pb.cu_seqlens[-1])
+    dims = B.dims_for(wl)
+    copy_bytes = pb.q.nbytes + pb.latent.nbytes + pb.token_ids.nbytes + total * wl.heads * wl.v_head_dim * 2
+    R = max(1, math.ceil(args.rotate_bytes / copy_bytes))
+    st = wl.dtype
+    shared = [B.to_device_tensor(pb.cu_seqlens, "int"), B.to_device_tensor(pb.gate_table, st),
+              B.to_device_tensor(pb.w_uk, st), B.to_device_tensor(pb.w_uv, st)]
+    copies = []
+    for _ in range(R):
+        copies.append([B.to_device_tensor(pb.q, st), B.to_device_tensor(pb.latent, st),
+                       B.to_device_tensor(pb.token_ids, "int"),
+                       torch.empty((total, wl.heads, wl.v_head_dim), dtype=torch.bfloat16, device="cuda")])
+    ws_bytes = B.prefill_varlen_workspace_size(dims, total)
+    ws = B.alloc_workspace(ws_bytes)
+    stream = torch.cuda.current_stream().cuda_stream
+    call = L.eg_mla_prefill_varlen
+
+    def argset(c):
+        cu, gate, wk, wv = shared
+        q, lat, ids, out = c
+        return (ctypes.byref(dims), nb, total, cu.data_ptr(), q.data_ptr(), lat.data_ptr(), ids.data_ptr(),
+                gate.data_ptr(), wk.data_ptr(), wv.data_ptr(), ws.data_ptr(), ws_bytes, out.data_ptr(), stream)
+
+    K, Wm = args.steps, args.warmup
+    arglist = [argset(copies[k % R]) for k in range(K)]
+    for k in range(max(Wm, 1)):
+        assert call(*argset(copies[k % R])) == 0
+    torch.cuda.synchronize()
+    e0, e1 = hip.event(), hip.event()
+    torch.cuda._sleep(20_000_000)  # the host enqueues the K calls behind a spin
+    hip.record(e0, stream)
+    for a in arglist:
+        call(*a)
+    hip.record(e1, stream)
+    torch.cuda.synchronize()
+    ms = hip.elapsed_ms(e0, e1) / K
+    fl = prefill_flops(lens)
+    tflops = fl / (ms * 1e-3) / 1e12
+    log(f"bench: prefill {nb} x {T}: {ms * 1e3:.1f} us/call, {total / ms * 1e3 / 1e6:.2f} M tokens/s, "
+        f"{tflops:.0f} TFLOP/s ({100 * tflops / MFMA_BF16_PEAK_TFLOPS:.1f} % of the bf16 MFMA peak)")
+    out = {
+        "metric": PREFILL_METRIC, "value": total / (ms * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": K,
+        "warmup": Wm, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"prefill_{nb}x{T}_{wl.name}", "sequences": nb, "tokens_per_sequence": T,
+                   "heads": wl.heads, "latent_dim": wl.latent_dim, "rope_dim": wl.rope_dim, "storage": wl.dtype,
+                   "rotating_copies": R},
+        "roofline": {"bound": "mfma", "kernel": "eg_mla_prefill_varlen (whole call: absorption, attention, "
+                                                "up-projection)",
+                     "achieved": tflops, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": tflops / MFMA_BF16_PEAK_TFLOPS, "traffic": None, "algorithmic_flops_per_call": fl,
+                     "call_us": ms * 1e3},
+    }
+    if not args.no_cpu_baseline:
+        log(f"bench: timing the fp64 oracle's prefill on the host for ~{args.cpu_seconds:.0f} s")
+        out["cpu_baseline"] = prefill_cpu_baseline(wl, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -172,6 +285,9 @@ def main():
     ap.add_argument("--calibration-copy-mib", type=int, default=0,
                     help="also run one device copy of this many MiB (a known byte count for profiler counters)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--prefill", default="", metavar="BxT",
+                    help="time the causal prefill (eg_mla_prefill_varlen) of B packed sequences of T tokens "
+                         "instead of the decode, e.g. 8x4096")
     ap.add_argument("--unfolded-gate", type=int, default=0, metavar="E",
                     help="unfolded gate with embedding width E (the paper recommends 512): every step first "
                          "computes one gate row per cache row from its token embedding (eg_mla_gate_rows), then "
@@ -183,6 +299,9 @@ def main():
         print(f"bench.py: this build measures one GPU; --gpus {args.gpus} (WORLD_SIZE {world}) is not supported. "
               "The decode path shards by sequence with no communication; see the design notes.", file=sys.stderr)
         sys.exit(2)
+
+    if args.prefill:
+        return prefill_main(args)
 
     import numpy as np
     import torch

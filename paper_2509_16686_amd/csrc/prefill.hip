@@ -12,7 +12,6 @@
 #include "device_common.h"
 #include "eg_mla.h"
 #include "host_plan.h"
-#include "aux_mfma.h"
 #include "prefill_mfma.h"
 
 namespace egmla {
@@ -168,11 +167,9 @@ extern "C" eg_mla_status eg_mla_prefill_varlen(const eg_mla_dims* dims, int32_t 
 
   hipLaunchKernelGGL(prefill_seqmap_kernel, dim3((T + 255) / 256), dim3(256), 0, stream, cu_seqlens, batch, T,
                      seq_start);
-  // q_lat (bf16) and q^R for every token: the absorption with tokens as its batch
-  const int rows = kAbsRows * kAbsBlocks;
-  hipLaunchKernelGGL((absorb_mfma_kernel<128, kAbsBlocks, kAbsCols, true>), dim3(d.num_heads, (T + rows - 1) / rows, 1),
-                     dim3(256), 0, stream, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(w_uk),
-                     reinterpret_cast<float*>(qf), T, d.num_heads, d.latent_dim, d.rope_dim);
+  // q_lat (bf16) and q^R for every token
+  hipLaunchKernelGGL(prefill_absorb_kernel, dim3((T + kPfUvTokens - 1) / kPfUvTokens, d.num_heads), dim3(256), 0, stream,
+                     static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(w_uk), qf, T);
   PrefillArgs a;
   a.qf = qf;
   a.latent = static_cast<const uint16_t*>(latent);

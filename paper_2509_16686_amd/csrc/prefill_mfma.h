@@ -13,9 +13,9 @@
 // values.
 //
 // Four launches: a map from each token to its sequence's first token; the
-// absorption (q_lat in bf16, with q^R, for every token: the decode's kernel
-// with tokens as its batch); the attention kernel below, which writes o_lat / l
-// in fp32; and the up-projection by W_UV per head (o_lat as bf16 hi + lo).
+// absorption (q_lat in bf16, with q^R, for every token); the attention kernel
+// below, which writes o_lat / l in fp32; and the up-projection by W_UV per
+// head (o_lat as bf16 hi + lo).
 //
 // Attention kernel.  A work-group (4 waves; two per CU, whose barriers are
 // independent, so that one's softmax overlaps the other's products on the
@@ -296,6 +296,80 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_attn_mfma_kernel(Prefil
       for (int q = 0; q < 4; ++q)
         *reinterpret_cast<f32x4_t*>(orow + 32 * db + 8 * q) =
             f32x4_t{o[db][4 * q] * inv, o[db][4 * q + 1] * inv, o[db][4 * q + 2] * inv, o[db][4 * q + 3] * inv};
+  }
+}
+
+// q_lat[t, h, :] = W_UK[h]^T q^C[t, h, :] in bf16, and q^R copied, for 128
+// tokens of one head per work-group (4 waves of 32 tokens).  W_UK[h]
+// ([d_h][d_c] row-major, rows padded to 288 bytes) is staged in LDS once and
+// read back as the A operand of v_mfma_f32_32x32x16_bf16 with
+// ds_read_b64_tr_b16 (one output column per lane, 4 consecutive rows per
+// read); the query rows come straight from global as the B operand, and the
+// accumulator holds q_lat^T, stored 4 consecutive columns at a time.
+__global__ __launch_bounds__(256) void prefill_absorb_kernel(const uint16_t* __restrict__ q,
+                                                             const uint16_t* __restrict__ w_uk,
+                                                             uint16_t* __restrict__ qf, int T) {
+  constexpr int DH = 128, RS = kPfDC + 16, DQin = DH + kPfDR;
+  __shared__ __attribute__((aligned(16))) uint16_t wk[DH * RS];
+  const int hh = blockIdx.y;
+  const int t0 = blockIdx.x * kPfUvTokens;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r32 = lane & 31, h = lane >> 5;
+  const int r16 = lane & 15, R1 = (lane >> 4) & 1;
+  const int t = t0 + 32 * w + r32;
+  const int tc = min(t, T - 1);
+  bf16x8_t qb[DH / 16];
+  {
+    const uint16_t* qrow = q + (static_cast<int64_t>(tc) * kPfHeads + hh) * DQin + 8 * h;
+#pragma unroll
+    for (int c = 0; c < DH / 16; ++c) qb[c] = *reinterpret_cast<const bf16x8_t*>(qrow + 16 * c);
+  }
+  // q^R of the 128 tokens: thread copies 32 dims (4 x 16 bytes) of token t0 + tid / 2
+  const int rt = min(t0 + (tid >> 1), T - 1);
+  u32x4_t rq[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    rq[j] = *reinterpret_cast<const u32x4_t*>(q + (static_cast<int64_t>(rt) * kPfHeads + hh) * DQin + DH +
+                                              32 * (tid & 1) + 8 * j);
+  for (int p = tid; p < DH * kPfDC / 8; p += 256) {
+    const int k = p / (kPfDC / 8), c8 = (p % (kPfDC / 8)) * 8;
+    *reinterpret_cast<u32x4_t*>(wk + k * RS + c8) =
+        *reinterpret_cast<const u32x4_t*>(w_uk + (static_cast<int64_t>(hh) * DH + k) * kPfDC + c8);
+  }
+  __syncthreads();
+  pf_f32x16_t acc[kPfDC / 32];
+#pragma unroll
+  for (int cb = 0; cb < kPfDC / 32; ++cb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[cb][r] = 0.f;
+  // A operand of chunk c, column block cb: lane (column 32 cb + 16 R1 + r16) gets
+  // rows 16 c + 8 h + 0..7; lane r16 of a 16-lane group addresses row + r16 / 4,
+  // columns 4 (r16 % 4) .. + 3 of the group's 16
+  const uint16_t* abase = wk + (8 * h + (r16 >> 2)) * RS + 16 * R1 + 4 * (r16 & 3);
+#pragma unroll
+  for (int c = 0; c < DH / 16; ++c)
+#pragma unroll
+    for (int cb = 0; cb < kPfDC / 32; ++cb) {
+      const uint16_t* ap = abase + 16 * c * RS + 32 * cb;
+      const s16x4_t a0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t*)ap);
+      const s16x4_t a1 =
+          __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t*)(ap + 4 * RS));
+      const bf16x8_t av = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
+      acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qb[c], acc[cb], 0, 0, 0);
+    }
+  if (t < T) {
+    uint16_t* dst = qf + (static_cast<int64_t>(t) * kPfHeads + hh) * kPfDQ + 4 * h;
+#pragma unroll
+    for (int cb = 0; cb < kPfDC / 32; ++cb)
+#pragma unroll
+      for (int qq = 0; qq < 4; ++qq)
+        *reinterpret_cast<u32x2_t*>(dst + 32 * cb + 8 * qq) =
+            u32x2_t{pack_bf16x2(acc[cb][4 * qq], acc[cb][4 * qq + 1]), pack_bf16x2(acc[cb][4 * qq + 2], acc[cb][4 * qq + 3])};
+  }
+  if (t0 + (tid >> 1) < T) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      *reinterpret_cast<u32x4_t*>(qf + (static_cast<int64_t>(rt) * kPfHeads + hh) * kPfDQ + kPfDC + 32 * (tid & 1) +
+                                  8 * j) = rq[j];
   }
 }
 
