@@ -5,8 +5,9 @@
 //   c       = RMSNorm(c) * kv_norm_w      (optional latent norm, eps 1e-6)
 //   k^R     = RoPE(r, position)           (adjacent pairs, angle pos * theta^(-2m/d_r))
 // and the row [c | k^R] plus the token id are stored at the token's slot.
-// One work-group (256 threads) per token; each wave computes output features
-// as coalesced dot products over the hidden dimension.
+// General shapes: one work-group (256 threads) per token; each wave computes
+// output features as coalesced dot products over the hidden dimension.  The
+// d_c 128 / d_r 64 bf16 layer takes the MFMA kernel below.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -79,6 +80,197 @@ __global__ __launch_bounds__(kAppendThreads) void append_kernel(const void* __re
   if (tid == 0) ids[slot] = token_ids[i];
 }
 
+// ---------------------------------------------------------------------------
+// MFMA append for bf16 storage with d_c = 128, d_r = 64 and hidden a multiple
+// of 128: Y^T[o][t] = sum_k W_DKV[o][k] x[t][k] on v_mfma_f32_32x32x16_bf16,
+// both operands straight from global (A: output row o = lane % 32, 8
+// consecutive k; B: token t = lane % 32, the same k), so the accumulator holds
+// 32 outputs x 32 tokens with each token's values in lanes t and t + 32.
+// Work-group y = 0 takes the 128 latent outputs (the RMSNorm needs all of a
+// token's latent), y = 1 the 64 RoPE outputs (a rotation pair, outputs 2m and
+// 2m + 1, sits in one lane).  KSPLIT (few tokens): the 4 waves share 32 tokens
+// and split the hidden dimension, partial sums meet in LDS and wave 0 finishes;
+// otherwise each wave takes its own 32 tokens over the whole hidden dimension.
+// Every load is in bounds: token rows past n repeat the last token and are not
+// stored.
+// ---------------------------------------------------------------------------
+constexpr int kAppMfmaDC = 128, kAppMfmaDR = 64;
+typedef __attribute__((ext_vector_type(16))) float app_f32x16_t;
+
+template <int NOB, bool KSPLIT, bool LATENT>
+__device__ __forceinline__ void append_mfma_part(const uint16_t* __restrict__ x, const int32_t* __restrict__ token_ids,
+                                                 const int32_t* __restrict__ positions,
+                                                 const int32_t* __restrict__ slots,
+                                                 const uint16_t* __restrict__ w_dkv,
+                                                 const uint16_t* __restrict__ kv_norm_w, float theta,
+                                                 uint16_t* __restrict__ cache, int32_t* __restrict__ ids,
+                                                 int64_t num_slots, int n, int hidden, float* red,
+                                                 const double* freq) {
+  constexpr int DQ = kAppMfmaDC + kAppMfmaDR;
+  constexpr int O0 = LATENT ? 0 : kAppMfmaDC;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r32 = lane & 31, h = lane >> 5;
+  const int tok = blockIdx.x * (KSPLIT ? 32 : 128) + (KSPLIT ? 0 : 32 * w) + r32;
+  const int tc = min(tok, n - 1);
+  const int kspan = KSPLIT ? hidden / 4 : hidden;
+  const int k_lo = KSPLIT ? w * kspan : 0;
+  const uint16_t* xb = x + static_cast<int64_t>(tc) * hidden + k_lo + 8 * h;
+  const uint16_t* wb = w_dkv + static_cast<int64_t>(O0 + r32) * hidden + k_lo + 8 * h;
+  // the epilogue's inputs travel while the products run: destination slot,
+  // token id or position, and with few tokens (KSPLIT: registers to spare)
+  // the norm weights of this lane's 4 x NOB groups of 4 outputs
+  const int64_t slot_pre = slots[tc];
+  const int32_t aux_pre = LATENT ? token_ids[tc] : positions[tc];
+  constexpr bool kNormEarly = LATENT && KSPLIT;
+  u32x2_t nw_pre[LATENT ? NOB * 4 : 1];
+  auto load_norm = [&]() {
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        nw_pre[4 * ob + q] = kv_norm_w ? *reinterpret_cast<const u32x2_t*>(kv_norm_w + 32 * ob + 8 * q + 4 * h)
+                                       : u32x2_t{0u, 0u};
+  };
+  if constexpr (kNormEarly) load_norm();
+  app_f32x16_t acc[NOB];
+#pragma unroll
+  for (int ob = 0; ob < NOB; ++ob)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[ob][r] = 0.f;
+  // batches of 4 chunks of 16: the next batch's loads are in flight while
+  // this batch's products run (kspan is a multiple of 128: an even count)
+  bf16x8_t bv[2][4], av[2][4][NOB];
+  auto load = [&](int buf, int k0) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      bv[buf][c] = *reinterpret_cast<const bf16x8_t*>(xb + k0 + 16 * c);
+#pragma unroll
+      for (int ob = 0; ob < NOB; ++ob)
+        av[buf][c][ob] = *reinterpret_cast<const bf16x8_t*>(wb + static_cast<int64_t>(32 * ob) * hidden + k0 + 16 * c);
+    }
+  };
+  auto products = [&](int buf) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+#pragma unroll
+      for (int ob = 0; ob < NOB; ++ob)
+        acc[ob] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[buf][c][ob], bv[buf][c], acc[ob], 0, 0, 0);
+  };
+  load(0, 0);
+  for (int k0 = 0; k0 < kspan; k0 += 128) {
+    load(1, k0 + 64);
+    __builtin_amdgcn_sched_barrier(0);
+    products(0);
+    if (k0 + 128 < kspan) load(0, k0 + 128);
+    __builtin_amdgcn_sched_barrier(0);
+    products(1);
+  }
+  if constexpr (KSPLIT) {
+    // partial sums of waves 1..3 to LDS ([wave][ob][r][lane]), wave 0 adds them in order
+    if (w > 0) {
+#pragma unroll
+      for (int ob = 0; ob < NOB; ++ob)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) red[(((w - 1) * NOB + ob) * 16 + r) * 64 + lane] = acc[ob][r];
+    }
+    __syncthreads();
+    if (w > 0) return;
+#pragma unroll
+    for (int v = 0; v < 3; ++v)
+#pragma unroll
+      for (int ob = 0; ob < NOB; ++ob)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[ob][r] += red[((v * NOB + ob) * 16 + r) * 64 + lane];
+  }
+  if (tok >= n) return;
+  const int64_t slot = slot_pre;
+  const bool store = slot >= 0 && slot < num_slots;  // out-of-range destination: skipped
+  uint16_t* row = cache + (store ? slot : 0) * DQ + O0 + 4 * h;
+  // lane holds outputs O0 + 32 ob + 8 q + 4 h + (0..3) of token tok in acc[ob][4 q + (0..3)]
+  if constexpr (LATENT) {
+    if constexpr (!kNormEarly) load_norm();
+    float inv_rms = 1.f;
+    if (kv_norm_w) {
+      float ss = 0.f;
+#pragma unroll
+      for (int ob = 0; ob < NOB; ++ob)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) ss = fmaf(acc[ob][r], acc[ob][r], ss);
+      const uint32_t u = __float_as_uint(ss);
+      const auto sw = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+      ss = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+      inv_rms = 1.f / sqrtf(ss / static_cast<float>(kAppMfmaDC) + kRmsEps);
+    }
+    if (store) {
+#pragma unroll
+      for (int ob = 0; ob < NOB; ++ob)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          float v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            v[e] = acc[ob][4 * q + e];
+            if (kv_norm_w) {
+              const uint32_t wpair = nw_pre[4 * ob + q][e >> 1];
+              v[e] = v[e] * inv_rms * ((e & 1) ? bf16_hi(wpair) : bf16_lo(wpair));
+            }
+          }
+          *reinterpret_cast<u32x2_t*>(row + 32 * ob + 8 * q) = u32x2_t{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+        }
+      if (h == 0) ids[slot] = aux_pre;
+    }
+  } else {
+    if (store) {
+      // the angle pos * theta^(-2m/d_r) and its reduction to [-pi, pi] are
+      // formed in fp64 (frequencies from the work-group's table), so that
+      // large positions keep full accuracy; the sine and cosine of the reduced
+      // angle are fp32 (error ~1e-7, far below the bf16 result)
+      const double pos = static_cast<double>(aux_pre);
+      constexpr double kTwoPi = 6.283185307179586476925286766559;
+#pragma unroll
+      for (int ob = 0; ob < NOB; ++ob)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          float v[4];
+#pragma unroll
+          for (int pr = 0; pr < 2; ++pr) {
+            const int m = (32 * ob + 8 * q + 4 * h + 2 * pr) / 2;  // pair index within the RoPE key
+            const double ang = pos * freq[m];
+            const double turns = rint(ang * (1.0 / kTwoPi));
+            const float red_ang = static_cast<float>(fma(-turns, kTwoPi, ang));
+            float sn, cs;
+            sincosf(red_ang, &sn, &cs);
+            const float x0 = acc[ob][4 * q + 2 * pr], x1 = acc[ob][4 * q + 2 * pr + 1];
+            v[2 * pr] = x0 * cs - x1 * sn;
+            v[2 * pr + 1] = x0 * sn + x1 * cs;
+          }
+          *reinterpret_cast<u32x2_t*>(row + 32 * ob + 8 * q) = u32x2_t{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+        }
+    }
+  }
+}
+
+template <bool KSPLIT>
+__global__ __launch_bounds__(256) void append_mfma_kernel(const uint16_t* __restrict__ x,
+                                                          const int32_t* __restrict__ token_ids,
+                                                          const int32_t* __restrict__ positions,
+                                                          const int32_t* __restrict__ slots,
+                                                          const uint16_t* __restrict__ w_dkv,
+                                                          const uint16_t* __restrict__ kv_norm_w, float theta,
+                                                          uint16_t* __restrict__ cache, int32_t* __restrict__ ids,
+                                                          int64_t num_slots, int n, int hidden) {
+  __shared__ float red[KSPLIT ? 3 * 4 * 16 * 64 : 1];
+  __shared__ double freq[kAppMfmaDR / 2];  // theta^(-2m/d_r), m = 0 .. d_r/2 - 1
+  if (threadIdx.x < kAppMfmaDR / 2)
+    freq[threadIdx.x] = pow(static_cast<double>(theta), -2.0 * threadIdx.x / static_cast<double>(kAppMfmaDR));
+  __syncthreads();
+  if (blockIdx.y == 0)
+    append_mfma_part<4, KSPLIT, true>(x, token_ids, positions, slots, w_dkv, kv_norm_w, theta, cache, ids, num_slots,
+                                      n, hidden, red, freq);
+  else
+    append_mfma_part<2, KSPLIT, false>(x, token_ids, positions, slots, w_dkv, kv_norm_w, theta, cache, ids,
+                                       num_slots, n, hidden, red, freq);
+}
+
 }  // namespace egmla
 
 using namespace egmla;
@@ -96,7 +288,26 @@ extern "C" eg_mla_status eg_mla_append(const eg_mla_dims* dims, int32_t n_tokens
   const float theta = rope_theta > 0.f ? rope_theta : 10000.f;
   const size_t lds = sizeof(float) * (static_cast<size_t>(hidden) + d.latent_dim + d.rope_dim + 4);
   (void)hipGetLastError();
-  if (d.dtype == EG_MLA_BF16) {
+  const bool aligned = reinterpret_cast<uintptr_t>(x) % 16 == 0 && reinterpret_cast<uintptr_t>(w_dkv) % 16 == 0 &&
+                       reinterpret_cast<uintptr_t>(latent_cache) % 8 == 0 &&
+                       reinterpret_cast<uintptr_t>(kv_norm_w) % 8 == 0;  // null passes
+  if (d.dtype == EG_MLA_BF16 && d.latent_dim == kAppMfmaDC && d.rope_dim == kAppMfmaDR && hidden % 512 == 0 &&
+      aligned) {
+    // few tokens: split the hidden dimension over the 4 waves of a 32-token work-group
+    const bool ksplit = n_tokens <= 8192;
+    const int per = ksplit ? 32 : 128;
+    const dim3 grid((n_tokens + per - 1) / per, 2);
+    const uint16_t* xb = static_cast<const uint16_t*>(x);
+    const uint16_t* wb = static_cast<const uint16_t*>(w_dkv);
+    const uint16_t* nw = static_cast<const uint16_t*>(kv_norm_w);
+    uint16_t* cb = static_cast<uint16_t*>(latent_cache);
+    if (ksplit)
+      hipLaunchKernelGGL(append_mfma_kernel<true>, grid, dim3(256), 0, stream, xb, token_ids, positions, slots, wb, nw,
+                         theta, cb, token_id_cache, num_slots, n_tokens, hidden);
+    else
+      hipLaunchKernelGGL(append_mfma_kernel<false>, grid, dim3(256), 0, stream, xb, token_ids, positions, slots, wb,
+                         nw, theta, cb, token_id_cache, num_slots, n_tokens, hidden);
+  } else if (d.dtype == EG_MLA_BF16) {
     if (lds > 65536 && hipFuncSetAttribute(reinterpret_cast<const void*>(append_kernel<true>),
                                            hipFuncAttributeMaxDynamicSharedMemorySize,
                                            static_cast<int>(lds)) != hipSuccess)

@@ -119,3 +119,24 @@ def test_append_then_decode(gpu):
     inp.latent_cache[slots] = W.f32_to_bf16_bits(rows.astype(np.float32))
     inp.token_ids[slots] = ap.token_ids
     assert_close(got, oracle_decode(inp), "bf16", "append then decode")
+
+
+@pytest.mark.parametrize("n", [1, 31, 33, 8192, 8193, 9000])
+def test_append_token_counts(gpu, n):
+    # the d_c 128 / d_r 64 layer's MFMA append: hidden split over the waves up
+    # to 8192 tokens, 128 tokens per work-group above; ragged last tiles
+    wl = W.WORKLOADS[1]
+    rows = n + 300
+    ap = W.generate_append(wl, n, rows, with_norm=True, seed=71 + n)
+    dims = B.dims_for(wl)
+    cache = torch.zeros((rows, wl.row_dim), dtype=torch.bfloat16, device="cuda")
+    idc = torch.full((rows,), -7, dtype=torch.int32, device="cuda")
+    say(f"append {wl.name} n={n}")
+    B.append(dims, stage(ap.x, "bf16"), stage(ap.token_ids, "int"), stage(ap.positions, "int"),
+             stage(ap.slots, "int"), stage(ap.w_dkv, "bf16"), stage(ap.kv_norm_w, "bf16"), cache, idc)
+    torch.cuda.synchronize()
+    ref = orc.append(ap.x, ap.w_dkv, ap.kv_norm_w, ap.positions, latent_dim=wl.latent_dim, rope_dim=wl.rope_dim,
+                     storage="bf16")
+    got = B.out_to_f64(cache)[ap.slots]
+    assert np.all(np.abs(got - ref) <= 2.0 ** -7 * np.abs(ref) + 1e-5), float(np.max(np.abs(got - ref)))
+    np.testing.assert_array_equal(idc.cpu().numpy()[ap.slots], ap.token_ids)
