@@ -27,6 +27,11 @@ What it computes (EG-MLA, arXiv 2509.16686):
   value aggregation in latent space and one W_UV[i] at the end.  This equals
   the explicit form by associativity of the matrix products.
 
+* The paper-literal gate (``literal_kv``, ``decode_literal``): Eq. (2)-(5) as
+  printed and the model listing's order, kv^C = W^UKV c, x = kv^C * g (or
+  kv^C + g, the ablation), LN over all heads' H (d_h + d_v) dims (or none, the
+  other ablation), then attention with the listing's per-head key/value split.
+
 Functions that follow an algorithm step by step rather than a closed
 definition: ``append`` (projection, optional RMSNorm, RoPE).  Its RoPE pairing
 (adjacent pairs, base 10000, 0-based positions) and RMSNorm epsilon (1e-6)
@@ -173,6 +178,73 @@ def decode_explicit(q, cache, token_ids, gate_table, w_uk, w_uv, seq_lens, *, la
             k = np.concatenate([k_c, k_r], axis=1)           # Eq. (C.12)
             s = tau * (k @ qf[b, h, :d_h + d_r])             # Eq. (C.13) logits
             out[b, h] = _softmax(s) @ v_c
+    return out
+
+
+# ---------------------------------------------------------------------------
+# the paper-literal gate (Sec. 3.1 Eq. (2)-(5) as printed, and the model
+# listing of App. E): the gate multiplies the up-projected keys and values of
+# every head, and a LayerNorm spans all heads' dims
+# ---------------------------------------------------------------------------
+LN_EPS = 1e-5  # the listing's nn.LayerNorm default
+
+
+def literal_kv(cache_rows_c, token_ids, gate_full, w_uk, w_uv, ln_w, ln_b, *, mode: str = "mul",
+               use_ln: bool = True) -> np.ndarray:
+    """Gated, normalised up-projected rows [n, H (d_h + d_v)] (float64 inputs).
+
+    Eq. (2): kv^C_t = W^UKV c_t, whose per-head blocks are [W_UK[h] c_t ; W_UV[h] c_t]
+    (the listing views kv as [n_h, d_nope + d_v] and splits each head into key
+    and value parts).  Eq. (3)-(5): x_t = kv^C_t (.) g_t with g_t = G[i_t] (the
+    full-width gate row; mode "add" is the ablation's kv^C_t + g_t), then
+    kv~_t = LN(x_t) over all H (d_h + d_v) dims with weight ln_w and bias ln_b
+    (use_ln False is the other ablation).
+    """
+    H = w_uk.shape[0]
+    kv = np.concatenate([np.concatenate([cache_rows_c @ w_uk[h].T, cache_rows_c @ w_uv[h].T], axis=1)
+                         for h in range(H)], axis=1)
+    g = gate_full[np.asarray(token_ids).astype(np.int64)]
+    x = kv * g if mode == "mul" else kv + g
+    if not use_ln:
+        return x
+    mu = x.mean(axis=1, keepdims=True)
+    var = ((x - mu) ** 2).mean(axis=1, keepdims=True)
+    return (x - mu) / np.sqrt(var + LN_EPS) * ln_w + ln_b
+
+
+def decode_literal(q, cache, token_ids, gate_full, w_uk, w_uv, ln_w, ln_b, seq_lens, *, latent_dim: int,
+                   head_dim: int, rope_dim: int, storage: str, page_table=None, page_size: int = 64,
+                   max_pages: int = 0, mode: str = "mul", use_ln: bool = True) -> np.ndarray:
+    """Decode with the paper-literal gate; returns out [B, H, d_v] in float64.
+
+    Per head h: k_j = [kv~_j[h, :d_h] ; k^R_j], v_j = kv~_j[h, d_h:] (App. C
+    Eq. (C.11)-(C.13) with the listing's split), u = softmax(q . k / sqrt(d_h + d_r)) v.
+    gate_full [V, H (d_h + d_v)] is head-major like kv; ln_w, ln_b [H (d_h + d_v)].
+    """
+    qf = widen(q, storage)
+    cf = widen(cache, storage)
+    gf = widen(gate_full, storage)
+    wk = widen(w_uk, storage)
+    wv = widen(w_uv, storage)
+    lw = widen(ln_w, storage) if ln_w is not None else None
+    lb = widen(ln_b, storage) if ln_b is not None else None
+    B, H, _ = qf.shape
+    d_c, d_h, d_r = latent_dim, head_dim, rope_dim
+    d_v = wv.shape[1]
+    tau = softmax_scale(d_h, d_r)
+    out = np.zeros((B, H, d_v), dtype=np.float64)
+    for b in range(B):
+        L = int(seq_lens[b])
+        if L == 0:
+            continue
+        rows = cache_rows(L, b, page_table, page_size, max_pages)
+        kvt = literal_kv(cf[rows, :d_c], np.asarray(token_ids)[rows], gf, wk, wv, lw, lb, mode=mode, use_ln=use_ln)
+        k_r = cf[rows, d_c:d_c + d_r]
+        for h in range(H):
+            blk = kvt[:, h * (d_h + d_v):(h + 1) * (d_h + d_v)]
+            k = np.concatenate([blk[:, :d_h], k_r], axis=1)
+            s = tau * (k @ qf[b, h, :d_h + d_r])
+            out[b, h] = _softmax(s) @ blk[:, d_h:]
     return out
 
 

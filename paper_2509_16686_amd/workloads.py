@@ -255,6 +255,27 @@ def generate_gate_embedding(wl: Workload, emb_dim: int, seed: Optional[int] = No
 
 
 @dataclass
+class LiteralGate:
+    """Inputs of the paper-literal gate (Sec. 3.1 Eq. (2)-(5)): a full-width gate
+    table and the LayerNorm's affine parameters, all head-major like kv^C =
+    W^UKV c (per head: d_h key dims, then d_v value dims)."""
+
+    gate_full: np.ndarray   # [V, H (d_h + d_v)]
+    ln_w: np.ndarray        # [H (d_h + d_v)]
+    ln_b: np.ndarray        # [H (d_h + d_v)]
+
+
+def generate_literal_gate(wl: Workload, seed: Optional[int] = None) -> LiteralGate:
+    """Seeded gate rows 1 + 0.1 N(0, 1), LayerNorm weight 1 + 0.1 N(0, 1) and bias 0.1 N(0, 1)."""
+    rng = np.random.default_rng(wl.seed + 4000 if seed is None else seed)
+    width = wl.heads * (wl.head_dim + wl.v_head_dim)
+    g = np.float32(1.0) + np.float32(0.1) * rng.standard_normal((wl.vocab, width), dtype=np.float32)
+    lw = np.float32(1.0) + np.float32(0.1) * rng.standard_normal(width, dtype=np.float32)
+    lb = np.float32(0.1) * rng.standard_normal(width, dtype=np.float32)
+    return LiteralGate(gate_full=_store(g, wl.dtype), ln_w=_store(lw, wl.dtype), ln_b=_store(lb, wl.dtype))
+
+
+@dataclass
 class AppendInputs:
     """Host arrays for one append call (new tokens written into a cache)."""
 

@@ -376,3 +376,102 @@ def test_bf16_widening_is_exact():
     back = orc.widen(bits, "bf16")
     ref = torch.from_numpy(vals).to(torch.bfloat16).to(torch.float64).numpy()
     np.testing.assert_array_equal(back, ref)
+
+
+# ---- the paper-literal gate (Sec. 3.1 Eq. (2)-(5) as printed) --------------
+def literal(inp, lg, **over):
+    wl = inp.wl
+    args = kw(inp)
+    args.update(over)
+    return orc.decode_literal(inp.q, inp.latent_cache, inp.token_ids, lg.gate_full, inp.w_uk, inp.w_uv, lg.ln_w,
+                              lg.ln_b, inp.seq_lens, **args)
+
+
+@pytest.mark.parametrize("mode,use_ln", [("mul", True), ("mul", False), ("add", True), ("add", False)])
+@pytest.mark.parametrize("over", [dict(), dict(paged=True, heads=3, v_head_dim=2)])
+def test_literal_gate_brute_force(mode, use_ln, over):
+    wl = tiny(**over)
+    inp = W.generate(wl)
+    lg = W.generate_literal_gate(wl)
+    L = to_lists(inp)
+    f = lambda a: orc.widen(a, wl.dtype).tolist()
+    got = brute.decode_literal(L["q"], L["cache"], L["token_ids"], f(lg.gate_full), L["w_uk"], L["w_uv"],
+                               f(lg.ln_w), f(lg.ln_b), L["seq_lens"],
+                               lambda b: [inp.slot(b, j) for j in range(int(inp.seq_lens[b]))],
+                               latent_dim=wl.latent_dim, head_dim=wl.head_dim, rope_dim=wl.rope_dim, mode=mode,
+                               use_ln=use_ln)
+    ref = literal(inp, lg, mode=mode, use_ln=use_ln)
+    assert rel_err(ref, np.array(got)) < 1e-12
+
+
+def test_literal_without_ln_and_unit_gate_is_plain_mla():
+    # no LayerNorm and an all-ones product gate (or a zero additive gate) leave
+    # plain MLA, which the absorbed decode computes by another route
+    wl = tiny(seq_len=9, batch=3)
+    inp = W.generate(wl)
+    lg = W.generate_literal_gate(wl)
+    plain = run(orc.decode, inp, use_gate=False)
+    ones = dataclass_replace(lg, gate_full=np.ones_like(lg.gate_full))
+    zeros = dataclass_replace(lg, gate_full=np.zeros_like(lg.gate_full))
+    assert rel_err(literal(inp, ones, use_ln=False), plain) < 1e-12
+    assert rel_err(literal(inp, zeros, mode="add", use_ln=False), plain) < 1e-12
+
+
+def dataclass_replace(obj, **kw_):
+    import dataclasses
+    return dataclasses.replace(obj, **kw_)
+
+
+def test_literal_kv_rows_are_layer_normalised():
+    # with unit weight and zero bias every gated row has mean 0 and variance
+    # var / (var + eps) over all heads' dims
+    wl = tiny(heads=4, head_dim=5, v_head_dim=3)
+    inp = W.generate(wl)
+    lg = W.generate_literal_gate(wl)
+    c = orc.widen(inp.latent_cache, wl.dtype)[:, :wl.latent_dim]
+    width = wl.heads * (wl.head_dim + wl.v_head_dim)
+    x = orc.literal_kv(c, inp.token_ids, orc.widen(lg.gate_full, wl.dtype), orc.widen(inp.w_uk, wl.dtype),
+                       orc.widen(inp.w_uv, wl.dtype), np.ones(width), np.zeros(width))
+    raw = orc.literal_kv(c, inp.token_ids, orc.widen(lg.gate_full, wl.dtype), orc.widen(inp.w_uk, wl.dtype),
+                         orc.widen(inp.w_uv, wl.dtype), None, None, use_ln=False)
+    var = raw.var(axis=1)
+    np.testing.assert_allclose(x.mean(axis=1), 0.0, atol=1e-12)
+    np.testing.assert_allclose(x.var(axis=1), var / (var + orc.LN_EPS), rtol=1e-12)
+    # head-major split: head h's key rows are W_UK[h] c, its value rows W_UV[h] c (before the gate)
+    kv = orc.literal_kv(c, inp.token_ids, np.ones_like(orc.widen(lg.gate_full, wl.dtype)),
+                        orc.widen(inp.w_uk, wl.dtype), orc.widen(inp.w_uv, wl.dtype), None, None, use_ln=False)
+    h = 2
+    d = wl.head_dim + wl.v_head_dim
+    np.testing.assert_allclose(kv[:, h * d:h * d + wl.head_dim], c @ orc.widen(inp.w_uk, wl.dtype)[h].T, rtol=1e-13)
+    np.testing.assert_allclose(kv[:, h * d + wl.head_dim:(h + 1) * d], c @ orc.widen(inp.w_uv, wl.dtype)[h].T,
+                               rtol=1e-13)
+
+
+def test_literal_zero_ln_weight_returns_bias_values():
+    # LN weight 0: every key and value is the bias, so each head's output is its
+    # value part of the bias (the softmax weights sum to one)
+    wl = tiny(seq_len=8)
+    inp = W.generate(wl)
+    lg = W.generate_literal_gate(wl)
+    lg0 = dataclass_replace(lg, ln_w=np.zeros_like(lg.ln_w))
+    out = literal(inp, lg0)
+    b = orc.widen(lg.ln_b, wl.dtype)
+    d = wl.head_dim + wl.v_head_dim
+    for h in range(wl.heads):
+        np.testing.assert_allclose(out[:, h], np.broadcast_to(b[h * d + wl.head_dim:(h + 1) * d], out[:, h].shape),
+                                   rtol=1e-12, atol=1e-14)
+
+
+def test_literal_ln_removes_latent_scale():
+    # scaling one token's cached latent by 3 scales its gated row by 3, which the
+    # LayerNorm removes up to its epsilon (LN(3x) normalises with eps / 9: a
+    # change of order eps / var); without the norm the output changes
+    wl = tiny(seq_len=7)
+    inp = W.generate(wl)
+    lg = W.generate_literal_gate(wl)
+    base = literal(inp, lg)
+    inp2 = W.generate(wl)
+    r = inp2.slot(0, 3)
+    inp2.latent_cache[r, :wl.latent_dim] *= 3
+    assert rel_err(literal(inp2, lg), base) < 1e-5
+    assert rel_err(literal(inp2, lg, use_ln=False), literal(inp, lg, use_ln=False)) > 1e-3
