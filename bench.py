@@ -268,6 +268,63 @@ def prefill_main(args):
     print(json.dumps(out), flush=True)
 
 
+def literal_main(args):
+    """Times eg_mla_decode_literal on the decode workload (one step = one call)."""
+    import torch
+
+    from paper_2509_16686_amd import binding as B
+    from paper_2509_16686_amd import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    L = B.lib()
+    hip = Hip()
+    wl = W.WORKLOADS[args.workload] if args.workload < len(W.WORKLOADS) else W.MLA_DC320_BIGBATCH
+    log(f"bench: generating {wl.name} with the literal gate ({args.literal})")
+    inp = W.generate(wl)
+    lg = W.generate_literal_gate(wl)
+    flags = {"mul_ln": 0, "mul": B.LITERAL_NO_LN, "add_ln": B.LITERAL_ADD,
+             "add": B.LITERAL_NO_LN | B.LITERAL_ADD}[args.literal]
+    dd = B.stage_decode(inp)
+    gate = B.to_device_tensor(lg.gate_full, wl.dtype)
+    lw, lb = B.to_device_tensor(lg.ln_w, wl.dtype), B.to_device_tensor(lg.ln_b, wl.dtype)
+    nslots = int(dd.cache.shape[0])
+    ws_bytes = B.decode_literal_workspace_size(dd.dims, nslots)
+    ws = B.alloc_workspace(ws_bytes)
+    stream = torch.cuda.current_stream().cuda_stream
+    a = (ctypes.byref(dd.dims), wl.batch, dd.q.data_ptr(), dd.cache.data_ptr(), dd.ids.data_ptr(), gate.data_ptr(),
+         dd.w_uk.data_ptr(), dd.w_uv.data_ptr(), lw.data_ptr(), lb.data_ptr(), flags, dd.seq_lens.data_ptr(),
+         None if dd.page_table is None else dd.page_table.data_ptr(), dd.max_pages, nslots, ws.data_ptr(), ws_bytes,
+         dd.out.data_ptr(), stream)
+    call = L.eg_mla_decode_literal
+    K, Wm = args.steps, args.warmup
+    for _ in range(max(Wm, 1)):
+        assert call(*a) == 0
+    torch.cuda.synchronize()
+    e0, e1 = hip.event(), hip.event()
+    torch.cuda._sleep(20_000_000)
+    hip.record(e0, stream)
+    for _ in range(K):
+        call(*a)
+    hip.record(e1, stream)
+    torch.cuda.synchronize()
+    ms = hip.elapsed_ms(e0, e1) / K
+    tokens = inp.total_tokens()
+    width = wl.heads * (wl.head_dim + wl.v_head_dim)
+    flops = tokens * 2 * width * wl.latent_dim
+    log(f"bench: literal ({args.literal}) {ms * 1e3:.1f} us/step, {wl.batch / ms * 1e3:.0f} tokens/s; up-projection "
+        f"{flops / 1e9:.1f} GFLOP per step")
+    out = {"metric": METRIC.replace("eg_mla_decode", "eg_mla_decode_literal"), "value": wl.batch / (ms * 1e-3),
+           "unit": "tokens/s", "n_gpus": 1, "steps": K, "warmup": Wm, "ms_per_step": ms, "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+           "config": {"workload": wl.name, "gate": f"literal ({args.literal}): after the up-projection, width {width}",
+                      "batch": wl.batch, "heads": wl.heads, "latent_dim": wl.latent_dim,
+                      "context": wl.seq_len if wl.seq_len else list(wl.seq_len_range)},
+           "up_projection_gflop_per_step": flops / 1e9,
+           "gate_bytes_per_step": tokens * width * 2}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -288,6 +345,9 @@ def main():
     ap.add_argument("--prefill", default="", metavar="BxT",
                     help="time the causal prefill (eg_mla_prefill_varlen) of B packed sequences of T tokens "
                          "instead of the decode, e.g. 8x4096")
+    ap.add_argument("--literal", default="", choices=["", "mul_ln", "mul", "add_ln", "add"],
+                    help="time eg_mla_decode_literal (the paper-literal gate after the up-projection, with or "
+                         "without the LayerNorm, product or sum) on the same workload instead of the decode")
     ap.add_argument("--unfolded-gate", type=int, default=0, metavar="E",
                     help="unfolded gate with embedding width E (the paper recommends 512): every step first "
                          "computes one gate row per cache row from its token embedding (eg_mla_gate_rows), then "
@@ -302,6 +362,8 @@ def main():
 
     if args.prefill:
         return prefill_main(args)
+    if args.literal:
+        return literal_main(args)
 
     import numpy as np
     import torch

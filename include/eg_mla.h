@@ -247,6 +247,47 @@ eg_mla_status eg_mla_prefill_varlen(const eg_mla_dims* dims, int32_t batch, int3
                                     const void* w_uv, void* workspace, size_t workspace_bytes, void* out,
                                     void* stream);
 
+/* ---------------------------------------------------------------------------
+ * Decode with the paper-literal gate (Sec. 3.1 Eq. (2)-(5) as printed and the
+ * model listing's order): for every cached token j of sequence b,
+ *   kv_j = [W_UK[h] c_j ; W_UV[h] c_j]_h      (W^UKV c_j, head-major, H (d_h + d_v) dims)
+ *   x_j  = kv_j (.) G[i_j]     (or kv_j + G[i_j] with EG_MLA_LITERAL_ADD)
+ *   y_j  = LN(x_j)             over all H (d_h + d_v) dims, eps 1e-5, weight and
+ *                              bias (skipped with EG_MLA_LITERAL_NO_LN)
+ * and per head out[b,h] = sum_j softmax_j(tau q_h . [y_j[h,:d_h] ; k^R_j]) y_j[h,d_h:].
+ * The gate follows the up-projection and the LayerNorm spans all heads, so
+ * nothing is absorbed: each call up-projects every cached token.  (The main
+ * decode applies the gate to the latent; this call is the literal variant
+ * and its two ablations.)
+ *
+ * bf16 storage with d_c = d_h = d_v = 128, d_r = 64, any head count, and a
+ * capacity (max_pages_per_seq x page_size) of at most 32768 tokens; other
+ * shapes EG_MLA_ERR_UNSUPPORTED.  dims->gate_dim is not used here (it must
+ * still pass eg_mla_check_dims).
+ *
+ *   q, latent_cache, token_id_cache, w_uk, w_uv, seq_lens, page_table,
+ *       max_pages_per_seq, num_slots: as for eg_mla_decode;
+ *   gate_full [vocab_size, H (d_h + d_v)]: per-token gate rows, head-major
+ *       like kv (per head d_h key dims, then d_v value dims);
+ *   ln_weight, ln_bias [H (d_h + d_v)] (may be null with EG_MLA_LITERAL_NO_LN);
+ *   flags: 0, EG_MLA_LITERAL_NO_LN, EG_MLA_LITERAL_ADD or both;
+ *   workspace: eg_mla_decode_literal_workspace_size(dims, num_slots) bytes,
+ *       256-byte aligned (a gated bf16 row and its LayerNorm moments per
+ *       cache row);  out [batch, H, d_v].
+ * Host-detectable errors as for eg_mla_decode.
+ * ------------------------------------------------------------------------- */
+#define EG_MLA_LITERAL_NO_LN 1u
+#define EG_MLA_LITERAL_ADD 2u
+
+size_t eg_mla_decode_literal_workspace_size(const eg_mla_dims* dims, int64_t num_slots);
+
+eg_mla_status eg_mla_decode_literal(const eg_mla_dims* dims, int32_t batch, const void* q, const void* latent_cache,
+                                    const int32_t* token_id_cache, const void* gate_full, const void* w_uk,
+                                    const void* w_uv, const void* ln_weight, const void* ln_bias, uint32_t flags,
+                                    const int32_t* seq_lens, const int32_t* page_table, int32_t max_pages_per_seq,
+                                    int64_t num_slots, void* workspace, size_t workspace_bytes, void* out,
+                                    void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -23,7 +23,9 @@ PATH_AUTO, PATH_VALU, PATH_MFMA = 0, 1, 2
 # Every symbol include/eg_mla.h declares.
 EXPORTS = ["eg_mla_status_string", "eg_mla_check_dims", "eg_mla_append", "eg_mla_decode_workspace_size",
            "eg_mla_decode", "eg_mla_decode_planned", "eg_mla_gate_rows", "eg_mla_prefill_workspace_size",
-           "eg_mla_prefill_ref", "eg_mla_prefill_varlen_workspace_size", "eg_mla_prefill_varlen"]
+           "eg_mla_prefill_ref", "eg_mla_prefill_varlen_workspace_size", "eg_mla_prefill_varlen",
+           "eg_mla_decode_literal_workspace_size", "eg_mla_decode_literal"]
+LITERAL_NO_LN, LITERAL_ADD = 1, 2
 
 
 class Dims(ctypes.Structure):
@@ -82,6 +84,11 @@ def lib() -> ctypes.CDLL:
     L.eg_mla_prefill_varlen_workspace_size.argtypes = [pd, i32]
     L.eg_mla_prefill_varlen.restype = ctypes.c_int
     L.eg_mla_prefill_varlen.argtypes = [pd, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp, vp]
+    L.eg_mla_decode_literal_workspace_size.restype = sz
+    L.eg_mla_decode_literal_workspace_size.argtypes = [pd, i64]
+    L.eg_mla_decode_literal.restype = ctypes.c_int
+    L.eg_mla_decode_literal.argtypes = [pd, i32, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_uint32, vp, vp, i32, i64,
+                                        vp, sz, vp, vp]
     _lib = L
     return L
 
@@ -161,6 +168,20 @@ def gate_rows(dims: Dims, ids, emb, w_ue, out, stream=None) -> None:
     emb_vocab, emb_dim = int(emb.shape[0]), int(emb.shape[1])
     _check(lib().eg_mla_gate_rows(ctypes.byref(dims), emb_dim, emb_vocab, n, _ptr(ids), _ptr(emb), _ptr(w_ue),
                                   _ptr(out), _stream(stream)), "eg_mla_gate_rows")
+
+
+def decode_literal_workspace_size(dims: Dims, num_slots: int) -> int:
+    return lib().eg_mla_decode_literal_workspace_size(ctypes.byref(dims), num_slots)
+
+
+def decode_literal(dd, gate_full, ln_w, ln_b, flags: int, workspace, stream=None) -> None:
+    """eg_mla_decode_literal over a staged DeviceDecode (its gate table is not used)."""
+    _check(lib().eg_mla_decode_literal(ctypes.byref(dd.dims), int(dd.q.shape[0]), _ptr(dd.q), _ptr(dd.cache),
+                                       _ptr(dd.ids), _ptr(gate_full), _ptr(dd.w_uk), _ptr(dd.w_uv), _ptr(ln_w),
+                                       _ptr(ln_b), flags, _ptr(dd.seq_lens), _ptr(dd.page_table), dd.max_pages,
+                                       int(dd.cache.shape[0]), _ptr(workspace),
+                                       workspace.numel() * workspace.element_size(), _ptr(dd.out), _stream(stream)),
+           "eg_mla_decode_literal")
 
 
 def prefill_varlen_workspace_size(dims: Dims, total_tokens: int) -> int:

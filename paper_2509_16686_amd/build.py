@@ -16,7 +16,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libegmla.so")
 
-SOURCES = ["host_plan.cpp", "decode.hip", "append.hip", "prefill.hip", "gate.hip"]
+SOURCES = ["host_plan.cpp", "decode.hip", "append.hip", "prefill.hip", "gate.hip", "literal.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

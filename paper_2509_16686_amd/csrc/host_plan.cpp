@@ -237,6 +237,45 @@ eg_mla_status validate_prefill_varlen(const eg_mla_dims* d, int32_t batch, int32
   return EG_MLA_OK;
 }
 
+size_t literal_stats_offset(const eg_mla_dims& d, int64_t num_slots) {
+  return align_up(static_cast<size_t>(std::max<int64_t>(num_slots, 0)) * d.num_heads *
+                  static_cast<size_t>(d.head_dim + d.v_head_dim) * 2);
+}
+
+size_t literal_workspace_bytes(const eg_mla_dims& d, int64_t num_slots) {
+  return std::max<size_t>(literal_stats_offset(d, num_slots) +
+                              align_up(static_cast<size_t>(std::max<int64_t>(num_slots, 0)) * 8),
+                          kAlign);
+}
+
+eg_mla_status validate_literal(const eg_mla_dims* d, int32_t batch, const void* q, const void* latent_cache,
+                               const int32_t* token_id_cache, const void* gate_full, const void* w_uk,
+                               const void* w_uv, const void* ln_w, const void* ln_b, uint32_t flags,
+                               const int32_t* seq_lens, const int32_t* page_table, int32_t max_pages_per_seq,
+                               int64_t num_slots, const void* workspace, size_t workspace_bytes, const void* out) {
+  eg_mla_status st = check_dims(d);
+  if (st != EG_MLA_OK) return st;
+  if (batch < 0 || max_pages_per_seq < 0 || num_slots < 0) return EG_MLA_ERR_INVALID_ARG;
+  if ((flags & ~(EG_MLA_LITERAL_NO_LN | EG_MLA_LITERAL_ADD)) != 0) return EG_MLA_ERR_INVALID_ARG;
+  if (d->dtype != EG_MLA_BF16 || d->latent_dim != 128 || d->head_dim != 128 || d->v_head_dim != 128 ||
+      d->rope_dim != 64)
+    return EG_MLA_ERR_UNSUPPORTED;
+  if (static_cast<int64_t>(max_pages_per_seq) * d->page_size > 32768) return EG_MLA_ERR_UNSUPPORTED;  // scores in LDS
+  if (num_slots >= (int64_t{1} << 31)) return EG_MLA_ERR_UNSUPPORTED;
+  if (batch == 0) return EG_MLA_OK;
+  if (!q || !gate_full || !w_uk || !w_uv || !seq_lens || !out || !latent_cache || !token_id_cache)
+    return EG_MLA_ERR_INVALID_ARG;
+  if (max_pages_per_seq < 1 || num_slots < 1) return EG_MLA_ERR_INVALID_ARG;
+  if (!page_table && static_cast<int64_t>(batch) * max_pages_per_seq * d->page_size > num_slots)
+    return EG_MLA_ERR_INVALID_ARG;  // contiguous rows: every sequence's capacity must fit in the cache
+  if ((flags & EG_MLA_LITERAL_NO_LN) == 0 && (!ln_w || !ln_b)) return EG_MLA_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(latent_cache) || !aligned16(gate_full) || !aligned16(w_uk) || !aligned16(w_uv))
+    return EG_MLA_ERR_INVALID_ARG;
+  if (!workspace || workspace_bytes < literal_workspace_bytes(*d, num_slots)) return EG_MLA_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return EG_MLA_ERR_WORKSPACE;
+  return EG_MLA_OK;
+}
+
 }  // namespace egmla
 
 extern "C" {

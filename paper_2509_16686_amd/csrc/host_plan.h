@@ -95,6 +95,16 @@ eg_mla_status validate_prefill_varlen(const eg_mla_dims* d, int32_t batch, int32
                                       const void* w_uv, const void* workspace, size_t workspace_bytes,
                                       const void* out);
 
+// Decode with the paper-literal gate: workspace = gated rows (bf16, by cache
+// row) then per-row LayerNorm moments (fp32 pairs).
+size_t literal_workspace_bytes(const eg_mla_dims& d, int64_t num_slots);
+size_t literal_stats_offset(const eg_mla_dims& d, int64_t num_slots);
+eg_mla_status validate_literal(const eg_mla_dims* d, int32_t batch, const void* q, const void* latent_cache,
+                               const int32_t* token_id_cache, const void* gate_full, const void* w_uk,
+                               const void* w_uv, const void* ln_w, const void* ln_b, uint32_t flags,
+                               const int32_t* seq_lens, const int32_t* page_table, int32_t max_pages_per_seq,
+                               int64_t num_slots, const void* workspace, size_t workspace_bytes, const void* out);
+
 inline float softmax_scale(const eg_mla_dims& d) {
   if (d.softmax_scale > 0.f) return d.softmax_scale;
   return 1.0f / __builtin_sqrtf(static_cast<float>(d.head_dim + d.rope_dim));

@@ -177,3 +177,27 @@ def test_prefill_varlen_rejects_before_launch(L):
                 dims(v_head_dim=64)):
         assert call(bad, 2, n) == B.ERR_UNSUPPORTED
         assert L.eg_mla_prefill_varlen_workspace_size(ctypes.byref(bad), n) == 0
+
+
+def test_decode_literal_rejects_before_launch(L):
+    d = dims()
+    vp = ctypes.c_void_p(256)
+    ws = ctypes.c_void_p(4096)
+    slots = 64 * 64
+    need = L.eg_mla_decode_literal_workspace_size(ctypes.byref(d), slots)
+    assert need >= slots * 16 * 256 * 2 + slots * 8
+
+    def call(dd=d, batch=2, flags=0, lnw=vp, lnb=vp, pt=None, maxp=4, nslots=slots, wsp=ws, wsb=need, q=vp):
+        return L.eg_mla_decode_literal(ctypes.byref(dd), batch, q, vp, vp, vp, vp, vp, lnw, lnb, flags, vp, pt, maxp,
+                                       nslots, wsp, wsb, vp, None)
+    assert call(batch=0) == B.OK
+    assert call(flags=4) == B.ERR_INVALID_ARG
+    assert call(lnw=None) == B.ERR_INVALID_ARG            # the LayerNorm needs its weight ...
+    assert call(lnb=None) == B.ERR_INVALID_ARG            # ... and bias
+    assert call(q=ctypes.c_void_p(258)) == B.ERR_INVALID_ARG
+    assert call(nslots=2 * 4 * 64 - 1) == B.ERR_INVALID_ARG  # contiguous rows must hold every sequence
+    assert call(wsb=need - 1) == B.ERR_WORKSPACE
+    assert call(wsp=ctypes.c_void_p(4100)) == B.ERR_WORKSPACE
+    assert call(maxp=513) == B.ERR_UNSUPPORTED            # capacity above 32768 tokens
+    for bad in (dims(latent_dim=512, gate_dim=512), dims(rope_dim=32), dims(dtype=B.FP32), dims(v_head_dim=64)):
+        assert call(dd=bad) == B.ERR_UNSUPPORTED

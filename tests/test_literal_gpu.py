@@ -1,0 +1,55 @@
+"""GPU parity of eg_mla_decode_literal (the paper-literal gate of Sec. 3.1
+Eq. (2)-(5): gate on the up-projected keys and values, LayerNorm over all
+heads' dims, and the two ablations) against the fp64 oracle."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import eg_mla_oracle as orc
+from paper_2509_16686_amd import binding as B
+from paper_2509_16686_amd import workloads as W
+from parity import assert_close, say
+
+pytestmark = pytest.mark.gpu
+
+MODES = [(0, "mul", True), (B.LITERAL_NO_LN, "mul", False), (B.LITERAL_ADD, "add", True),
+         (B.LITERAL_NO_LN | B.LITERAL_ADD, "add", False)]
+
+
+def run_literal(inp, lg, flags):
+    dd = B.stage_decode(inp)
+    ws = B.alloc_workspace(B.decode_literal_workspace_size(dd.dims, int(dd.cache.shape[0])))
+    gate = B.to_device_tensor(lg.gate_full, "bf16")
+    lw, lb = B.to_device_tensor(lg.ln_w, "bf16"), B.to_device_tensor(lg.ln_b, "bf16")
+    B.decode_literal(dd, gate, lw, lb, flags, ws)
+    torch.cuda.synchronize()
+    return B.out_to_f64(dd.out)
+
+
+def oracle_literal(inp, lg, mode, use_ln):
+    wl = inp.wl
+    return orc.decode_literal(inp.q, inp.latent_cache, inp.token_ids, lg.gate_full, inp.w_uk, inp.w_uv, lg.ln_w,
+                              lg.ln_b, inp.seq_lens, latent_dim=wl.latent_dim, head_dim=wl.head_dim,
+                              rope_dim=wl.rope_dim, storage=wl.dtype, page_table=inp.page_table,
+                              page_size=wl.page_size, max_pages=inp.max_pages, mode=mode, use_ln=use_ln)
+
+
+@pytest.mark.parametrize("flags,mode,use_ln", MODES, ids=["mul_ln", "mul", "add_ln", "add"])
+def test_literal_contiguous(gpu, flags, mode, use_ln):
+    wl = W.WORKLOADS[1].replace(batch=3, seq_len=300, vocab=2000, seed=81)
+    inp = W.generate(wl)
+    lg = W.generate_literal_gate(wl)
+    say(f"literal decode contiguous mode={mode} ln={use_ln}")
+    assert_close(run_literal(inp, lg, flags), oracle_literal(inp, lg, mode, use_ln), "bf16",
+                 f"literal {mode} ln={use_ln}", scaled=True)
+
+
+def test_literal_paged_ragged_with_empty(gpu):
+    wl = W.WORKLOADS[1].replace(batch=5, seq_len=None, seq_len_range=(1, 700), paged=True, vocab=3000, seed=82)
+    inp = W.generate(wl, seq_lens=np.array([1, 128, 0, 129, 700]))
+    lg = W.generate_literal_gate(wl)
+    say("literal decode paged ragged lens 1,128,0,129,700")
+    got = run_literal(inp, lg, 0)
+    ref = oracle_literal(inp, lg, "mul", True)
+    assert np.all(got[2] == 0)
+    assert_close(got, ref, "bf16", "literal paged ragged", scaled=True)
