@@ -10,10 +10,12 @@
 //
 // Two kernels (bf16 storage, d_c = d_h = d_v = 128, d_r = 64, any head count):
 //  1. literal_kv_kernel: for the cached rows of every sequence, x = kv (.) g
-//     on v_mfma_f32_32x32x16_bf16 (A: 32 rows of W_UK[h] or W_UV[h]; B: the
-//     row's latent, in registers), written in bf16 to the workspace by cache
-//     row, with the row's mean and 1/sqrt(var + eps) over all dims (moments
-//     summed in fp32 from the unrounded products).
+//     on v_mfma_f32_32x32x16_bf16 (A: 32 rows of W_UK[h] or W_UV[h] from LDS,
+//     where one head's 256 rows are staged with coalesced loads while the
+//     previous head computes; B: the row's latent, in registers), written in
+//     bf16 to the workspace by cache row, with the row's mean and
+//     1/sqrt(var + eps) over all dims (moments summed in fp32 from the
+//     unrounded products).
 //  2. literal_attn_kernel: one work-group per (sequence, head).  The
 //     LayerNorm is applied while reading: a score is
 //     rstd (sum_d q_d w_d x_d - mu sum_d q_d w_d) + sum_d q_d b_d + q^R . k^R,
@@ -34,19 +36,24 @@ constexpr int kLtHeadW = kLtDH + kLtDV;  // gated dims per head
 constexpr float kLtLnEps = 1e-5f;        // the listing's LayerNorm default
 typedef __attribute__((ext_vector_type(16))) float lt_f32x16_t;
 
-__global__ __launch_bounds__(256) void literal_kv_kernel(const uint16_t* __restrict__ cache,
-                                                         const int32_t* __restrict__ ids,
-                                                         const uint16_t* __restrict__ gate,
-                                                         const uint16_t* __restrict__ w_uk,
-                                                         const uint16_t* __restrict__ w_uv,
-                                                         const int32_t* __restrict__ seq_lens,
-                                                         const int32_t* __restrict__ page_table, int P, int max_pages,
-                                                         int64_t num_slots, int H, int V, int add_mode,
-                                                         uint16_t* __restrict__ Y, float2* __restrict__ stats) {
+constexpr int kLtWRow = kLtDC + 8;                  // padded LDS row of W (272 bytes: 16-lane reads hit 16 bank groups)
+constexpr int kLtWLds = kLtHeadW * kLtWRow * 2;      // one head's W_UK and W_UV rows in LDS (69.6 KB)
+
+__global__ __launch_bounds__(256, 2) void literal_kv_kernel(const uint16_t* __restrict__ cache,
+                                                            const int32_t* __restrict__ ids,
+                                                            const uint16_t* __restrict__ gate,
+                                                            const uint16_t* __restrict__ w_uk,
+                                                            const uint16_t* __restrict__ w_uv,
+                                                            const int32_t* __restrict__ seq_lens,
+                                                            const int32_t* __restrict__ page_table, int P,
+                                                            int max_pages, int64_t num_slots, int H, int V,
+                                                            int add_mode, uint16_t* __restrict__ Y,
+                                                            float2* __restrict__ stats) {
+  extern __shared__ __attribute__((aligned(16))) uint16_t wsh[];  // [256 rows: W_UK[h] then W_UV[h]][kLtWRow]
   const int b = blockIdx.y;
   const int L = clamp_len(seq_lens[b], P * max_pages);
   const int j0 = blockIdx.x * 128;
-  if (j0 >= L) return;  // whole work-group; this kernel has no barrier
+  if (j0 >= L) return;  // whole work-group, before any barrier
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r32 = lane & 31, h = lane >> 5;
   const int j = j0 + 32 * w + r32;
   const bool ok = j < L;  // positions past the sequence repeat its last token and are not stored
@@ -59,34 +66,61 @@ __global__ __launch_bounds__(256) void literal_kv_kernel(const uint16_t* __restr
     cb[c] = *reinterpret_cast<const bf16x8_t*>(cache + row * (kLtDC + kLtDR) + 16 * c + 8 * h);
   const uint16_t* grow = gate + static_cast<int64_t>(id) * width + 4 * h;
   uint16_t* yrow = Y + row * width + 4 * h;
+
+  // a head's 256 weight rows (W_UK[h] then W_UV[h]) as 4096 16-byte pieces:
+  // thread tid takes pieces tid + 256 i (row (tid + 256 i) / 16: 16 lanes read one 256-byte row)
+  u32x4_t stage[16];
+  auto fetch = [&](int head) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int p = tid + 256 * i, r = p >> 4, k8 = (p & 15) * 8;
+      const uint16_t* src = (r < kLtDH ? w_uk + (static_cast<int64_t>(head) * kLtDH + r) * kLtDC
+                                       : w_uv + (static_cast<int64_t>(head) * kLtDV + r - kLtDH) * kLtDC) + k8;
+      stage[i] = *reinterpret_cast<const u32x4_t*>(src);
+    }
+  };
+  auto put = [&]() {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int p = tid + 256 * i;
+      *reinterpret_cast<u32x4_t*>(wsh + (p >> 4) * kLtWRow + (p & 15) * 8) = stage[i];
+    }
+  };
   float s1 = 0.f, s2 = 0.f;
-  for (int ob = 0; ob < width / 32; ++ob) {  // 32 outputs: head ob / 8, part (ob / 4) % 2, rows 32 (ob % 4) ..
-    const int head = ob >> 3, r0 = (ob & 3) * 32;
-    const uint16_t* wrow = ((ob >> 2) & 1 ? w_uv : w_uk) + (static_cast<int64_t>(head) * kLtDH + r0 + r32) * kLtDC + 8 * h;
-    bf16x8_t av[kLtDC / 16];
+  fetch(0);
+  for (int head = 0; head < H; ++head) {
+    __syncthreads();  // every wave is done with the previous head's rows
+    put();
+    __syncthreads();
+    if (head + 1 < H) fetch(head + 1);  // travels while this head's 8 blocks compute
+#pragma unroll 2
+    for (int blk = 0; blk < kLtHeadW / 32; ++blk) {  // 32 outputs: LDS rows 32 blk .. + 31
+      const int ob = head * (kLtHeadW / 32) + blk;
+      u32x2_t gv[4];
 #pragma unroll
-    for (int c = 0; c < kLtDC / 16; ++c) av[c] = *reinterpret_cast<const bf16x8_t*>(wrow + 16 * c);
-    u32x2_t gv[4];
+      for (int q = 0; q < 4; ++q) gv[q] = *reinterpret_cast<const u32x2_t*>(grow + 32 * ob + 8 * q);
+      lt_f32x16_t acc;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) gv[q] = *reinterpret_cast<const u32x2_t*>(grow + 32 * ob + 8 * q);
-    lt_f32x16_t acc;
+      for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+      const uint16_t* arow = wsh + (32 * blk + r32) * kLtWRow + 8 * h;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+      for (int c = 0; c < kLtDC / 16; ++c)
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8_t*>(arow + 16 * c), cb[c], acc,
+                                                      0, 0, 0);
+      // lane holds outputs 32 ob + 8 q + 4 h + e of its row in acc[4 q + e]
 #pragma unroll
-    for (int c = 0; c < kLtDC / 16; ++c) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[c], cb[c], acc, 0, 0, 0);
-    // lane holds outputs 32 ob + 8 q + 4 h + e of its row in acc[4 q + e]
+      for (int q = 0; q < 4; ++q) {
+        float x[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      float x[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float g = (e & 1) ? bf16_hi(gv[q][e >> 1]) : bf16_lo(gv[q][e >> 1]);
-        x[e] = add_mode ? acc[4 * q + e] + g : acc[4 * q + e] * g;
-        s1 += x[e];
-        s2 = fmaf(x[e], x[e], s2);
+        for (int e = 0; e < 4; ++e) {
+          const float g = (e & 1) ? bf16_hi(gv[q][e >> 1]) : bf16_lo(gv[q][e >> 1]);
+          x[e] = add_mode ? acc[4 * q + e] + g : acc[4 * q + e] * g;
+          s1 += x[e];
+          s2 = fmaf(x[e], x[e], s2);
+        }
+        if (ok)
+          *reinterpret_cast<u32x2_t*>(yrow + 32 * ob + 8 * q) = u32x2_t{pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3])};
       }
-      if (ok)
-        *reinterpret_cast<u32x2_t*>(yrow + 32 * ob + 8 * q) = u32x2_t{pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3])};
     }
   }
   // lanes r32 and r32 + 32 hold the two halves of the row's outputs
@@ -255,7 +289,10 @@ extern "C" eg_mla_status eg_mla_decode_literal(const eg_mla_dims* dims, int32_t 
   float2* stats = reinterpret_cast<float2*>(static_cast<unsigned char*>(workspace) + literal_stats_offset(d, num_slots));
   const bool use_ln = (flags & EG_MLA_LITERAL_NO_LN) == 0;
   const int add = (flags & EG_MLA_LITERAL_ADD) != 0;
-  hipLaunchKernelGGL(literal_kv_kernel, dim3((cap + 127) / 128, batch), dim3(256), 0, stream,
+  if (hipFuncSetAttribute(reinterpret_cast<const void*>(literal_kv_kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                          kLtWLds) != hipSuccess)
+    return EG_MLA_ERR_HIP;
+  hipLaunchKernelGGL(literal_kv_kernel, dim3((cap + 127) / 128, batch), dim3(256), kLtWLds, stream,
                      static_cast<const uint16_t*>(latent_cache), token_id_cache, static_cast<const uint16_t*>(gate_full),
                      static_cast<const uint16_t*>(w_uk), static_cast<const uint16_t*>(w_uv), seq_lens, page_table, P,
                      max_pages_per_seq, num_slots, d.num_heads, d.vocab_size, add, Y, stats);
