@@ -135,16 +135,19 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_attn_mfma_kernel(Prefil
   auto key_at = [&](int tile, int k) { return min(kbeg + tile * kPfKeys + k, kend - 1); };
   u32x4_t nl[NLJ], ng[NLJ], nr[NRJ];
   int idn[NLJ];
+  // the ids are clamped only where they become gate addresses, one iteration
+  // after their loads: clamping right away would wait for them, and the loads
+  // complete in order, so that wait would also take the tile loads before them
   auto load_ids = [&](int tile) {
 #pragma unroll
-    for (int j = 0; j < NLJ; ++j) idn[j] = clamp_id(a.ids[key_at(tile, kl + 16 * j)], a.V);
+    for (int j = 0; j < NLJ; ++j) idn[j] = a.ids[key_at(tile, kl + 16 * j)];
   };
   auto load_tile = [&](int tile) {
 #pragma unroll
     for (int j = 0; j < NLJ; ++j) {
       nl[j] = *reinterpret_cast<const u32x4_t*>(a.latent + static_cast<int64_t>(key_at(tile, kl + 16 * j)) * kPfDQ +
                                                  8 * pl);
-      ng[j] = *reinterpret_cast<const u32x4_t*>(a.gate + static_cast<int64_t>(idn[j]) * kPfDC + 8 * pl);
+      ng[j] = *reinterpret_cast<const u32x4_t*>(a.gate + static_cast<int64_t>(clamp_id(idn[j], a.V)) * kPfDC + 8 * pl);
     }
 #pragma unroll
     for (int j = 0; j < NRJ; ++j)
