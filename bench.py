@@ -268,6 +268,56 @@ def prefill_main(args):
     print(json.dumps(out), flush=True)
 
 
+def append_main(args):
+    """Times eg_mla_append of `--append N` tokens (one call per step)."""
+    import torch
+
+    from paper_2509_16686_amd import binding as B
+    from paper_2509_16686_amd import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    L = B.lib()
+    hip = Hip()
+    wl = W.WORKLOADS[args.workload] if args.workload < len(W.WORKLOADS) else W.MLA_DC320_BIGBATCH
+    n = args.append
+    rows = max(2 * n, 4096)
+    log(f"bench: generating an append of {n} tokens ({wl.name} layer, hidden {wl.hidden})")
+    ai = W.generate_append(wl, n, rows, with_norm=True)
+    dims = B.dims_for(wl)
+    st = wl.dtype
+    t = lambda a, kind: B.to_device_tensor(a, kind)
+    x, ids, pos, slots = t(ai.x, st), t(ai.token_ids, "int"), t(ai.positions, "int"), t(ai.slots, "int")
+    w, nw = t(ai.w_dkv, st), t(ai.kv_norm_w, st)
+    cache = torch.zeros((rows, wl.row_dim), dtype=torch.bfloat16 if st == "bf16" else torch.float32, device="cuda")
+    idc = torch.zeros((rows,), dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    a = (ctypes.byref(dims), n, wl.hidden, x.data_ptr(), ids.data_ptr(), pos.data_ptr(), slots.data_ptr(), w.data_ptr(),
+         nw.data_ptr(), ai.rope_theta, cache.data_ptr(), idc.data_ptr(), rows, stream)
+    call = L.eg_mla_append
+    K, Wm = args.steps, args.warmup
+    for _ in range(max(Wm, 1)):
+        assert call(*a) == 0
+    torch.cuda.synchronize()
+    e0, e1 = hip.event(), hip.event()
+    torch.cuda._sleep(20_000_000)  # the K calls queue behind a spin: GPU time, not host enqueue time
+    hip.record(e0, stream)
+    for _ in range(K):
+        call(*a)
+    hip.record(e1, stream)
+    torch.cuda.synchronize()
+    ms = hip.elapsed_ms(e0, e1) / K
+    flops = 2.0 * n * wl.hidden * wl.row_dim
+    log(f"bench: append of {n} tokens: {ms * 1e3:.1f} us/call, {n / ms * 1e3 / 1e6:.2f} M tokens/s, "
+        f"{flops / (ms * 1e-3) / 1e12:.1f} TFLOP/s")
+    out = {"metric": "append tokens/s for eg_mla_append, 1 GPU", "value": n / (ms * 1e-3), "unit": "tokens/s",
+           "n_gpus": 1, "steps": K, "warmup": Wm, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "bf16" if st == "bf16" else "fp32", "data": "synthetic",
+           "config": {"workload": f"append_{n}_{wl.name}", "tokens": n, "hidden": wl.hidden,
+                      "row_dim": wl.row_dim, "latent_norm": True}}
+    print(json.dumps(out), flush=True)
+
+
 def literal_main(args):
     """Times eg_mla_decode_literal on the decode workload (one step = one call)."""
     import torch
@@ -345,6 +395,9 @@ def main():
     ap.add_argument("--prefill", default="", metavar="BxT",
                     help="time the causal prefill (eg_mla_prefill_varlen) of B packed sequences of T tokens "
                          "instead of the decode, e.g. 8x4096")
+    ap.add_argument("--append", type=int, default=0, metavar="N",
+                    help="time eg_mla_append of N new tokens (the default workload's layer, with the latent norm) "
+                         "instead of the decode")
     ap.add_argument("--literal", default="", choices=["", "mul_ln", "mul", "add_ln", "add"],
                     help="time eg_mla_decode_literal (the paper-literal gate after the up-projection, with or "
                          "without the LayerNorm, product or sum) on the same workload instead of the decode")
@@ -364,6 +417,8 @@ def main():
         return prefill_main(args)
     if args.literal:
         return literal_main(args)
+    if args.append:
+        return append_main(args)
 
     import numpy as np
     import torch
