@@ -339,7 +339,7 @@ def literal_main(args):
     gate = B.to_device_tensor(lg.gate_full, wl.dtype)
     lw, lb = B.to_device_tensor(lg.ln_w, wl.dtype), B.to_device_tensor(lg.ln_b, wl.dtype)
     nslots = int(dd.cache.shape[0])
-    ws_bytes = B.decode_literal_workspace_size(dd.dims, nslots)
+    ws_bytes = B.decode_literal_workspace_size(dd.dims, wl.batch, dd.max_pages)
     ws = B.alloc_workspace(ws_bytes)
     stream = torch.cuda.current_stream().cuda_stream
     a = (ctypes.byref(dd.dims), wl.batch, dd.q.data_ptr(), dd.cache.data_ptr(), dd.ids.data_ptr(), gate.data_ptr(),

@@ -260,10 +260,12 @@ eg_mla_status eg_mla_prefill_varlen(const eg_mla_dims* dims, int32_t batch, int3
  * decode applies the gate to the latent; this call is the literal variant
  * and its two ablations.)
  *
- * bf16 storage with d_c = d_h = d_v = 128, d_r = 64, any head count, and a
- * capacity (max_pages_per_seq x page_size) of at most 32768 tokens; other
- * shapes EG_MLA_ERR_UNSUPPORTED.  dims->gate_dim is not used here (it must
- * still pass eg_mla_check_dims).
+ * bf16 storage with d_c = d_h = d_v = 128, d_r = 64, at most 160 heads
+ * (per-head state of a 128-token tile lives in LDS) and a gate table below
+ * 4 GB (32-bit row offsets); other shapes
+ * EG_MLA_ERR_UNSUPPORTED.  dims->gate_dim is not used here (it must still
+ * pass eg_mla_check_dims).  Softmax partials are formed per 128-token tile
+ * and merged, so the context length is not limited.
  *
  *   q, latent_cache, token_id_cache, w_uk, w_uv, seq_lens, page_table,
  *       max_pages_per_seq, num_slots: as for eg_mla_decode;
@@ -271,15 +273,15 @@ eg_mla_status eg_mla_prefill_varlen(const eg_mla_dims* dims, int32_t batch, int3
  *       like kv (per head d_h key dims, then d_v value dims);
  *   ln_weight, ln_bias [H (d_h + d_v)] (may be null with EG_MLA_LITERAL_NO_LN);
  *   flags: 0, EG_MLA_LITERAL_NO_LN, EG_MLA_LITERAL_ADD or both;
- *   workspace: eg_mla_decode_literal_workspace_size(dims, num_slots) bytes,
- *       256-byte aligned (a gated bf16 row and its LayerNorm moments per
- *       cache row);  out [batch, H, d_v].
+ *   workspace: eg_mla_decode_literal_workspace_size(dims, batch,
+ *       max_pages_per_seq) bytes, 256-byte aligned (fp32 softmax partials
+ *       per sequence, 128-token tile and head);  out [batch, H, d_v].
  * Host-detectable errors as for eg_mla_decode.
  * ------------------------------------------------------------------------- */
 #define EG_MLA_LITERAL_NO_LN 1u
 #define EG_MLA_LITERAL_ADD 2u
 
-size_t eg_mla_decode_literal_workspace_size(const eg_mla_dims* dims, int64_t num_slots);
+size_t eg_mla_decode_literal_workspace_size(const eg_mla_dims* dims, int32_t batch, int32_t max_pages_per_seq);
 
 eg_mla_status eg_mla_decode_literal(const eg_mla_dims* dims, int32_t batch, const void* q, const void* latent_cache,
                                     const int32_t* token_id_cache, const void* gate_full, const void* w_uk,

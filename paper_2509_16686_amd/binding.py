@@ -85,7 +85,7 @@ def lib() -> ctypes.CDLL:
     L.eg_mla_prefill_varlen.restype = ctypes.c_int
     L.eg_mla_prefill_varlen.argtypes = [pd, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp, vp]
     L.eg_mla_decode_literal_workspace_size.restype = sz
-    L.eg_mla_decode_literal_workspace_size.argtypes = [pd, i64]
+    L.eg_mla_decode_literal_workspace_size.argtypes = [pd, i32, i32]
     L.eg_mla_decode_literal.restype = ctypes.c_int
     L.eg_mla_decode_literal.argtypes = [pd, i32, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_uint32, vp, vp, i32, i64,
                                         vp, sz, vp, vp]
@@ -170,8 +170,8 @@ def gate_rows(dims: Dims, ids, emb, w_ue, out, stream=None) -> None:
                                   _ptr(out), _stream(stream)), "eg_mla_gate_rows")
 
 
-def decode_literal_workspace_size(dims: Dims, num_slots: int) -> int:
-    return lib().eg_mla_decode_literal_workspace_size(ctypes.byref(dims), num_slots)
+def decode_literal_workspace_size(dims: Dims, batch: int, max_pages: int) -> int:
+    return lib().eg_mla_decode_literal_workspace_size(ctypes.byref(dims), batch, max_pages)
 
 
 def decode_literal(dd, gate_full, ln_w, ln_b, flags: int, workspace, stream=None) -> None:

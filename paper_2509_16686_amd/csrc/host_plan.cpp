@@ -237,14 +237,18 @@ eg_mla_status validate_prefill_varlen(const eg_mla_dims* d, int32_t batch, int32
   return EG_MLA_OK;
 }
 
-size_t literal_stats_offset(const eg_mla_dims& d, int64_t num_slots) {
-  return align_up(static_cast<size_t>(std::max<int64_t>(num_slots, 0)) * d.num_heads *
-                  static_cast<size_t>(d.head_dim + d.v_head_dim) * 2);
+size_t literal_lds_bytes(int num_heads) {
+  // weight / gate-tile region, per-wave scores [4][H][32], value sums [4][d_v],
+  // two sums per head and three per-wave figures per head (all fp32)
+  return 272 * 256 + 4 * static_cast<size_t>(num_heads) * 32 * 4 + 4 * 128 * 4 +
+         static_cast<size_t>(num_heads) * (2 + 12) * 4;
 }
 
-size_t literal_workspace_bytes(const eg_mla_dims& d, int64_t num_slots) {
-  return std::max<size_t>(literal_stats_offset(d, num_slots) +
-                              align_up(static_cast<size_t>(std::max<int64_t>(num_slots, 0)) * 8),
+size_t literal_workspace_bytes(const eg_mla_dims& d, int32_t batch, int32_t max_pages_per_seq) {
+  const int64_t cap = static_cast<int64_t>(std::max(max_pages_per_seq, 0)) * d.page_size;
+  const int64_t tiles = (cap + 127) / 128;
+  return std::max<size_t>(align_up(static_cast<size_t>(std::max(batch, 0)) * static_cast<size_t>(tiles) *
+                                   d.num_heads * (d.v_head_dim + 4) * sizeof(float)),
                           kAlign);
 }
 
@@ -260,7 +264,10 @@ eg_mla_status validate_literal(const eg_mla_dims* d, int32_t batch, const void* 
   if (d->dtype != EG_MLA_BF16 || d->latent_dim != 128 || d->head_dim != 128 || d->v_head_dim != 128 ||
       d->rope_dim != 64)
     return EG_MLA_ERR_UNSUPPORTED;
-  if (static_cast<int64_t>(max_pages_per_seq) * d->page_size > 32768) return EG_MLA_ERR_UNSUPPORTED;  // scores in LDS
+  if (literal_lds_bytes(d->num_heads) > 160 * 1024) return EG_MLA_ERR_UNSUPPORTED;  // per-head state in LDS
+  if (static_cast<int64_t>(d->vocab_size) * d->num_heads * (d->head_dim + d->v_head_dim) * 2 >= (int64_t{1} << 32))
+    return EG_MLA_ERR_UNSUPPORTED;  // gate rows are addressed by 32-bit byte offsets
+  if (static_cast<int64_t>(max_pages_per_seq) * d->page_size > (int64_t{1} << 30)) return EG_MLA_ERR_UNSUPPORTED;
   if (num_slots >= (int64_t{1} << 31)) return EG_MLA_ERR_UNSUPPORTED;
   if (batch == 0) return EG_MLA_OK;
   if (!q || !gate_full || !w_uk || !w_uv || !seq_lens || !out || !latent_cache || !token_id_cache)
@@ -271,7 +278,8 @@ eg_mla_status validate_literal(const eg_mla_dims* d, int32_t batch, const void* 
   if ((flags & EG_MLA_LITERAL_NO_LN) == 0 && (!ln_w || !ln_b)) return EG_MLA_ERR_INVALID_ARG;
   if (!aligned16(q) || !aligned16(latent_cache) || !aligned16(gate_full) || !aligned16(w_uk) || !aligned16(w_uv))
     return EG_MLA_ERR_INVALID_ARG;
-  if (!workspace || workspace_bytes < literal_workspace_bytes(*d, num_slots)) return EG_MLA_ERR_WORKSPACE;
+  if (!workspace || workspace_bytes < literal_workspace_bytes(*d, batch, max_pages_per_seq))
+    return EG_MLA_ERR_WORKSPACE;
   if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return EG_MLA_ERR_WORKSPACE;
   return EG_MLA_OK;
 }

@@ -95,10 +95,11 @@ eg_mla_status validate_prefill_varlen(const eg_mla_dims* d, int32_t batch, int32
                                       const void* w_uv, const void* workspace, size_t workspace_bytes,
                                       const void* out);
 
-// Decode with the paper-literal gate: workspace = gated rows (bf16, by cache
-// row) then per-row LayerNorm moments (fp32 pairs).
-size_t literal_workspace_bytes(const eg_mla_dims& d, int64_t num_slots);
-size_t literal_stats_offset(const eg_mla_dims& d, int64_t num_slots);
+// Decode with the paper-literal gate: workspace = one fp32 record per
+// (sequence, 128-token tile, head): d_v value sums, the tile's max, sum of p,
+// sum of a mu, one pad.  LDS of the tile kernel for a head count.
+size_t literal_workspace_bytes(const eg_mla_dims& d, int32_t batch, int32_t max_pages_per_seq);
+size_t literal_lds_bytes(int num_heads);
 eg_mla_status validate_literal(const eg_mla_dims* d, int32_t batch, const void* q, const void* latent_cache,
                                const int32_t* token_id_cache, const void* gate_full, const void* w_uk,
                                const void* w_uv, const void* ln_w, const void* ln_b, uint32_t flags,

@@ -184,8 +184,9 @@ def test_decode_literal_rejects_before_launch(L):
     vp = ctypes.c_void_p(256)
     ws = ctypes.c_void_p(4096)
     slots = 64 * 64
-    need = L.eg_mla_decode_literal_workspace_size(ctypes.byref(d), slots)
-    assert need >= slots * 16 * 256 * 2 + slots * 8
+    need = L.eg_mla_decode_literal_workspace_size(ctypes.byref(d), 2, 4)
+    assert need >= 2 * (4 * 64 // 128) * 16 * (128 + 4) * 4   # fp32 partials per (sequence, 128-token tile, head)
+    assert L.eg_mla_decode_literal_workspace_size(ctypes.byref(d), 2, 5) > need  # a ragged last tile counts
 
     def call(dd=d, batch=2, flags=0, lnw=vp, lnb=vp, pt=None, maxp=4, nslots=slots, wsp=ws, wsb=need, q=vp):
         return L.eg_mla_decode_literal(ctypes.byref(dd), batch, q, vp, vp, vp, vp, vp, lnw, lnb, flags, vp, pt, maxp,
@@ -198,6 +199,10 @@ def test_decode_literal_rejects_before_launch(L):
     assert call(nslots=2 * 4 * 64 - 1) == B.ERR_INVALID_ARG  # contiguous rows must hold every sequence
     assert call(wsb=need - 1) == B.ERR_WORKSPACE
     assert call(wsp=ctypes.c_void_p(4100)) == B.ERR_WORKSPACE
-    assert call(maxp=513) == B.ERR_UNSUPPORTED            # capacity above 32768 tokens
-    for bad in (dims(latent_dim=512, gate_dim=512), dims(rope_dim=32), dims(dtype=B.FP32), dims(v_head_dim=64)):
+    big = L.eg_mla_decode_literal_workspace_size(ctypes.byref(d), 2, 1024)
+    assert big >= 2 * (1024 * 64 // 128) * 16 * (128 + 4) * 4  # 65536-token capacity: no limit on the context
+    assert call(maxp=1024, nslots=2 * 1024 * 64, wsb=big - 1) == B.ERR_WORKSPACE
+    for bad in (dims(latent_dim=512, gate_dim=512), dims(rope_dim=32), dims(dtype=B.FP32), dims(v_head_dim=64),
+                dims(num_heads=200),   # per-head tile state beyond the LDS
+                dims(vocab_size=600000)):  # a gate table of 4 GB or more
         assert call(dd=bad) == B.ERR_UNSUPPORTED

@@ -18,7 +18,7 @@ MODES = [(0, "mul", True), (B.LITERAL_NO_LN, "mul", False), (B.LITERAL_ADD, "add
 
 def run_literal(inp, lg, flags):
     dd = B.stage_decode(inp)
-    ws = B.alloc_workspace(B.decode_literal_workspace_size(dd.dims, int(dd.cache.shape[0])))
+    ws = B.alloc_workspace(B.decode_literal_workspace_size(dd.dims, int(dd.q.shape[0]), dd.max_pages))
     gate = B.to_device_tensor(lg.gate_full, "bf16")
     lw, lb = B.to_device_tensor(lg.ln_w, "bf16"), B.to_device_tensor(lg.ln_b, "bf16")
     B.decode_literal(dd, gate, lw, lb, flags, ws)
@@ -53,3 +53,18 @@ def test_literal_paged_ragged_with_empty(gpu):
     ref = oracle_literal(inp, lg, "mul", True)
     assert np.all(got[2] == 0)
     assert_close(got, ref, "bf16", "literal paged ragged", scaled=True)
+
+
+@pytest.mark.parametrize("heads,lens,flags,mode,use_ln", [
+    (4, [33000, 257], 0, "mul", True),                     # past 32768 tokens: 258 tiles merged
+    (20, [300, 1], B.LITERAL_ADD, "add", True),            # 20 heads: tile state beyond 80 KB of LDS
+    (1, [129, 64], B.LITERAL_NO_LN, "mul", False),          # a single head
+], ids=["h4_l33000", "h20", "h1"])
+def test_literal_head_counts_and_long_context(gpu, heads, lens, flags, mode, use_ln):
+    wl = W.WORKLOADS[1].replace(batch=len(lens), heads=heads, seq_len=None, seq_len_range=(1, max(lens)),
+                                vocab=1500, seed=83)
+    inp = W.generate(wl, seq_lens=np.array(lens))
+    lg = W.generate_literal_gate(wl)
+    say(f"literal decode H={heads} lens {lens} mode={mode} ln={use_ln}")
+    assert_close(run_literal(inp, lg, flags), oracle_literal(inp, lg, mode, use_ln), "bf16",
+                 f"literal H={heads}", scaled=True)
