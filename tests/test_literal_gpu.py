@@ -68,3 +68,29 @@ def test_literal_head_counts_and_long_context(gpu, heads, lens, flags, mode, use
     say(f"literal decode H={heads} lens {lens} mode={mode} ln={use_ln}")
     assert_close(run_literal(inp, lg, flags), oracle_literal(inp, lg, mode, use_ln), "bf16",
                  f"literal H={heads}", scaled=True)
+
+
+def test_literal_full_size_sampled(gpu):
+    # the bench's workload and launch (B32 H16 L4096, 50304 gate rows, LayerNorm);
+    # the oracle recomputes two sampled sequences on their own, from their cache
+    # rows and the gate rows their ids select
+    wl = W.WORKLOADS[1]
+    inp = W.generate(wl)
+    lg = W.generate_literal_gate(wl)
+    say(f"literal decode full size {wl.name}, sampled sequences")
+    got = run_literal(inp, lg, 0)
+    P = wl.page_size
+    for b in (0, wl.batch - 1):
+        L = int(inp.seq_lens[b])
+        j = np.arange(L)
+        if inp.page_table is None:
+            rows = b * inp.max_pages * P + j
+        else:
+            rows = inp.page_table[b, j // P].astype(np.int64) * P + j % P
+        uniq, inv = np.unique(inp.token_ids[rows], return_inverse=True)
+        ref = orc.decode_literal(inp.q[b:b + 1], inp.latent_cache[rows], inv.astype(np.int32), lg.gate_full[uniq],
+                                 inp.w_uk, inp.w_uv, lg.ln_w, lg.ln_b, np.array([L], dtype=np.int32),
+                                 latent_dim=wl.latent_dim, head_dim=wl.head_dim, rope_dim=wl.rope_dim,
+                                 storage=wl.dtype, page_table=None, page_size=P, max_pages=-(-L // P), mode="mul",
+                                 use_ln=True)
+        assert_close(got[b:b + 1], ref, "bf16", f"literal full size, sequence {b}", scaled=True)
