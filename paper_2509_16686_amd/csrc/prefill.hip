@@ -168,7 +168,8 @@ extern "C" eg_mla_status eg_mla_prefill_varlen(const eg_mla_dims* dims, int32_t 
   hipLaunchKernelGGL(prefill_seqmap_kernel, dim3((T + 255) / 256), dim3(256), 0, stream, cu_seqlens, batch, T,
                      seq_start);
   // q_lat (bf16) and q^R for every token
-  hipLaunchKernelGGL(prefill_absorb_kernel, dim3((T + kPfUvTokens - 1) / kPfUvTokens, d.num_heads), dim3(256), 0, stream,
+  const int side_wgs = ((T + kPfUvTokens - 1) / kPfUvTokens + kPfSideChunks - 1) / kPfSideChunks;
+  hipLaunchKernelGGL(prefill_absorb_kernel, dim3(side_wgs, d.num_heads), dim3(256), 0, stream,
                      static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(w_uk), qf, T);
   PrefillArgs a;
   a.qf = qf;
@@ -183,7 +184,7 @@ extern "C" eg_mla_status eg_mla_prefill_varlen(const eg_mla_dims* dims, int32_t 
   const size_t lds = 2 * kPfBufBytes;
   hipLaunchKernelGGL(prefill_attn_mfma_kernel, dim3((T + kPfTokens - 1) / kPfTokens), dim3(kPfThreads), lds, stream,
                      a);
-  hipLaunchKernelGGL(prefill_uv_kernel, dim3((T + kPfUvTokens - 1) / kPfUvTokens, d.num_heads), dim3(256), 0, stream,
+  hipLaunchKernelGGL(prefill_uv_kernel, dim3(side_wgs, d.num_heads), dim3(256), 0, stream,
                      olat, static_cast<const uint16_t*>(w_uv), static_cast<uint16_t*>(out), T);
   return hipGetLastError() == hipSuccess ? EG_MLA_OK : EG_MLA_ERR_HIP;
 }

@@ -58,7 +58,8 @@ constexpr int kPfLatRow = 2 * kPfDC;    // bytes per key row of the gated latent
 constexpr int kPfRopeRow = 2 * kPfDR;   // bytes per key row of the RoPE key
 constexpr int kPfLatBytes = kPfKeys * kPfLatRow;
 constexpr int kPfBufBytes = kPfLatBytes + kPfKeys * kPfRopeRow;  // one tile buffer (24 KB)
-constexpr int kPfUvTokens = 128;  // up-projection: tokens per work-group (4 waves x 32)
+constexpr int kPfUvTokens = 128;  // absorption and up-projection: tokens per chunk (4 waves x 32)
+constexpr int kPfSideChunks = 4;  // chunks per work-group: the head's weights are staged once for them
 
 typedef __attribute__((ext_vector_type(16))) float pf_f32x16_t;
 
@@ -302,8 +303,9 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_attn_mfma_kernel(Prefil
   }
 }
 
-// q_lat[t, h, :] = W_UK[h]^T q^C[t, h, :] in bf16, and q^R copied, for 128
-// tokens of one head per work-group (4 waves of 32 tokens).  W_UK[h]
+// q_lat[t, h, :] = W_UK[h]^T q^C[t, h, :] in bf16, and q^R copied, for up to
+// 4 chunks of 128 tokens of one head per work-group (4 waves of 32 tokens; the
+// next chunk's rows load while a chunk computes and stores).  W_UK[h]
 // ([d_h][d_c] row-major, rows padded to 288 bytes) is staged in LDS once and
 // read back as the A operand of v_mfma_f32_32x32x16_bf16 with
 // ds_read_b64_tr_b16 (one output column per lane, 4 consecutive rows per
@@ -315,69 +317,84 @@ __global__ __launch_bounds__(256) void prefill_absorb_kernel(const uint16_t* __r
   constexpr int DH = 128, RS = kPfDC + 16, DQin = DH + kPfDR;
   __shared__ __attribute__((aligned(16))) uint16_t wk[DH * RS];
   const int hh = blockIdx.y;
-  const int t0 = blockIdx.x * kPfUvTokens;
+  const int c0 = blockIdx.x * kPfSideChunks;
+  const int nch = min(kPfSideChunks, (T + kPfUvTokens - 1) / kPfUvTokens - c0);
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r32 = lane & 31, h = lane >> 5;
   const int r16 = lane & 15, R1 = (lane >> 4) & 1;
-  const int t = t0 + 32 * w + r32;
-  const int tc = min(t, T - 1);
+  // a chunk's operands: the lane's token's q^C (B operand) and, per thread, 32
+  // dims (4 x 16 bytes) of q^R of token t0 + tid / 2 (copied through)
   bf16x8_t qb[DH / 16];
-  {
+  u32x4_t rq[4];
+  auto load = [&](int chunk) {
+    const int t0 = chunk * kPfUvTokens;
+    const int tc = min(t0 + 32 * w + r32, T - 1);
     const uint16_t* qrow = q + (static_cast<int64_t>(tc) * kPfHeads + hh) * DQin + 8 * h;
 #pragma unroll
     for (int c = 0; c < DH / 16; ++c) qb[c] = *reinterpret_cast<const bf16x8_t*>(qrow + 16 * c);
-  }
-  // q^R of the 128 tokens: thread copies 32 dims (4 x 16 bytes) of token t0 + tid / 2
-  const int rt = min(t0 + (tid >> 1), T - 1);
-  u32x4_t rq[4];
+    const int rt = min(t0 + (tid >> 1), T - 1);
 #pragma unroll
-  for (int j = 0; j < 4; ++j)
-    rq[j] = *reinterpret_cast<const u32x4_t*>(q + (static_cast<int64_t>(rt) * kPfHeads + hh) * DQin + DH +
-                                              32 * (tid & 1) + 8 * j);
+    for (int j = 0; j < 4; ++j)
+      rq[j] = *reinterpret_cast<const u32x4_t*>(q + (static_cast<int64_t>(rt) * kPfHeads + hh) * DQin + DH +
+                                                32 * (tid & 1) + 8 * j);
+  };
+  load(c0);
   for (int p = tid; p < DH * kPfDC / 8; p += 256) {
     const int k = p / (kPfDC / 8), c8 = (p % (kPfDC / 8)) * 8;
     *reinterpret_cast<u32x4_t*>(wk + k * RS + c8) =
         *reinterpret_cast<const u32x4_t*>(w_uk + (static_cast<int64_t>(hh) * DH + k) * kPfDC + c8);
   }
   __syncthreads();
-  pf_f32x16_t acc[kPfDC / 32];
-#pragma unroll
-  for (int cb = 0; cb < kPfDC / 32; ++cb)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) acc[cb][r] = 0.f;
   // A operand of chunk c, column block cb: lane (column 32 cb + 16 R1 + r16) gets
   // rows 16 c + 8 h + 0..7; lane r16 of a 16-lane group addresses row + r16 / 4,
   // columns 4 (r16 % 4) .. + 3 of the group's 16
   const uint16_t* abase = wk + (8 * h + (r16 >> 2)) * RS + 16 * R1 + 4 * (r16 & 3);
-#pragma unroll
-  for (int c = 0; c < DH / 16; ++c)
-#pragma unroll
-    for (int cb = 0; cb < kPfDC / 32; ++cb) {
-      const uint16_t* ap = abase + 16 * c * RS + 32 * cb;
-      const s16x4_t a0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t*)ap);
-      const s16x4_t a1 =
-          __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t*)(ap + 4 * RS));
-      const bf16x8_t av = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
-      acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qb[c], acc[cb], 0, 0, 0);
-    }
-  if (t < T) {
-    uint16_t* dst = qf + (static_cast<int64_t>(t) * kPfHeads + hh) * kPfDQ + 4 * h;
+  for (int k = 0; k < nch; ++k) {
+    const int t0 = (c0 + k) * kPfUvTokens;
+    const int t = t0 + 32 * w + r32;
+    pf_f32x16_t acc[kPfDC / 32];
 #pragma unroll
     for (int cb = 0; cb < kPfDC / 32; ++cb)
 #pragma unroll
-      for (int qq = 0; qq < 4; ++qq)
-        *reinterpret_cast<u32x2_t*>(dst + 32 * cb + 8 * qq) =
-            u32x2_t{pack_bf16x2(acc[cb][4 * qq], acc[cb][4 * qq + 1]), pack_bf16x2(acc[cb][4 * qq + 2], acc[cb][4 * qq + 3])};
-  }
-  if (t0 + (tid >> 1) < T) {
+      for (int r = 0; r < 16; ++r) acc[cb][r] = 0.f;
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      *reinterpret_cast<u32x4_t*>(qf + (static_cast<int64_t>(rt) * kPfHeads + hh) * kPfDQ + kPfDC + 32 * (tid & 1) +
-                                  8 * j) = rq[j];
+    for (int c = 0; c < DH / 16; ++c)
+#pragma unroll
+      for (int cb = 0; cb < kPfDC / 32; ++cb) {
+        const uint16_t* ap = abase + 16 * c * RS + 32 * cb;
+        const s16x4_t a0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t*)ap);
+        const s16x4_t a1 =
+            __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t*)(ap + 4 * RS));
+        const bf16x8_t av = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
+        acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qb[c], acc[cb], 0, 0, 0);
+      }
+    const u32x4_t r0 = rq[0], r1 = rq[1], r2 = rq[2], r3 = rq[3];
+    // the next chunk's rows travel while this one is stored (the last chunk loads itself again)
+    __builtin_amdgcn_sched_barrier(0);
+    load(c0 + min(k + 1, nch - 1));
+    __builtin_amdgcn_sched_barrier(0);
+    if (t < T) {
+      uint16_t* dst = qf + (static_cast<int64_t>(t) * kPfHeads + hh) * kPfDQ + 4 * h;
+#pragma unroll
+      for (int cb = 0; cb < kPfDC / 32; ++cb)
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq)
+          *reinterpret_cast<u32x2_t*>(dst + 32 * cb + 8 * qq) =
+              u32x2_t{pack_bf16x2(acc[cb][4 * qq], acc[cb][4 * qq + 1]),
+                      pack_bf16x2(acc[cb][4 * qq + 2], acc[cb][4 * qq + 3])};
+    }
+    if (t0 + (tid >> 1) < T) {
+      uint16_t* dr = qf + (static_cast<int64_t>(t0 + (tid >> 1)) * kPfHeads + hh) * kPfDQ + kPfDC + 32 * (tid & 1);
+      *reinterpret_cast<u32x4_t*>(dr) = r0;
+      *reinterpret_cast<u32x4_t*>(dr + 8) = r1;
+      *reinterpret_cast<u32x4_t*>(dr + 16) = r2;
+      *reinterpret_cast<u32x4_t*>(dr + 24) = r3;
+    }
   }
 }
 
-// out[t, h, :] = W_UV[h] o_lat[t, h, :] for 128 tokens of one head per
-// work-group (4 waves of 32 tokens): W_UV[h] ([d_v][d_c], rows padded by 16
+// out[t, h, :] = W_UV[h] o_lat[t, h, :] for up to 4 chunks of 128 tokens of
+// one head per work-group (4 waves of 32 tokens; the next chunk's rows load
+// while a chunk is stored and converted): W_UV[h] ([d_v][d_c], rows padded by 16
 // bytes) in LDS as the A operand, o_lat rows straight from global as the B
 // operand, split into bf16 hi + lo (two products, so o_lat keeps ~16 bits);
 // the accumulator holds out^T, stored 4 consecutive v at a time.
@@ -387,18 +404,28 @@ __global__ __launch_bounds__(256) void prefill_uv_kernel(const float* __restrict
   constexpr int DV = 128, RS = kPfDC + 8;
   __shared__ __attribute__((aligned(16))) uint16_t wl[DV * RS];
   const int hh = blockIdx.y;
-  const int t0 = blockIdx.x * kPfUvTokens;
+  const int c0 = blockIdx.x * kPfSideChunks;
+  const int nch = min(kPfSideChunks, (T + kPfUvTokens - 1) / kPfUvTokens - c0);
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r32 = lane & 31, h = lane >> 5;
-  const int t = t0 + 32 * w + r32;
-  const int tc = min(t, T - 1);
-  bf16x8_t ob_hi[kPfDC / 16], ob_lo[kPfDC / 16];
-  {
+  f32x4_t ov[kPfDC / 16][2];  // the lane's token's o_lat, dims 16 c + 8 h .. + 7
+  auto load = [&](int chunk) {
+    const int tc = min(chunk * kPfUvTokens + 32 * w + r32, T - 1);
     const float* orow = olat + (static_cast<int64_t>(tc) * kPfHeads + hh) * kPfDC + 8 * h;
-    f32x4_t ov[kPfDC / 16][2];
 #pragma unroll
     for (int c = 0; c < kPfDC / 16; ++c)
 #pragma unroll
       for (int j = 0; j < 2; ++j) ov[c][j] = *reinterpret_cast<const f32x4_t*>(orow + 16 * c + 4 * j);
+  };
+  load(c0);
+  for (int p = tid; p < DV * kPfDC / 8; p += 256) {
+    const int v = p / (kPfDC / 8), k8 = (p % (kPfDC / 8)) * 8;
+    *reinterpret_cast<u32x4_t*>(wl + v * RS + k8) =
+        *reinterpret_cast<const u32x4_t*>(w_uv + (static_cast<int64_t>(hh) * DV + v) * kPfDC + k8);
+  }
+  __syncthreads();
+  for (int k = 0; k < nch; ++k) {
+    const int t = (c0 + k) * kPfUvTokens + 32 * w + r32;
+    bf16x8_t ob_hi[kPfDC / 16], ob_lo[kPfDC / 16];
 #pragma unroll
     for (int c = 0; c < kPfDC / 16; ++c) {
       uint32_t hi[4], lo[4];
@@ -411,34 +438,32 @@ __global__ __launch_bounds__(256) void prefill_uv_kernel(const float* __restrict
       ob_hi[c] = __builtin_bit_cast(bf16x8_t, u32x4_t{hi[0], hi[1], hi[2], hi[3]});
       ob_lo[c] = __builtin_bit_cast(bf16x8_t, u32x4_t{lo[0], lo[1], lo[2], lo[3]});
     }
-  }
-  for (int p = tid; p < DV * kPfDC / 8; p += 256) {
-    const int v = p / (kPfDC / 8), k8 = (p % (kPfDC / 8)) * 8;
-    *reinterpret_cast<u32x4_t*>(wl + v * RS + k8) =
-        *reinterpret_cast<const u32x4_t*>(w_uv + (static_cast<int64_t>(hh) * DV + v) * kPfDC + k8);
-  }
-  __syncthreads();
-  pf_f32x16_t acc[DV / 32];
-#pragma unroll
-  for (int vb = 0; vb < DV / 32; ++vb)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) acc[vb][r] = 0.f;
-#pragma unroll
-  for (int c = 0; c < kPfDC / 16; ++c)
-#pragma unroll
-    for (int vb = 0; vb < DV / 32; ++vb) {
-      const bf16x8_t av = *reinterpret_cast<const bf16x8_t*>(wl + (32 * vb + r32) * RS + 16 * c + 8 * h);
-      acc[vb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, ob_hi[c], acc[vb], 0, 0, 0);
-      acc[vb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, ob_lo[c], acc[vb], 0, 0, 0);
-    }
-  if (t < T) {
-    uint16_t* dst = out + (static_cast<int64_t>(t) * kPfHeads + hh) * DV + 4 * h;
+    pf_f32x16_t acc[DV / 32];
 #pragma unroll
     for (int vb = 0; vb < DV / 32; ++vb)
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        *reinterpret_cast<u32x2_t*>(dst + 32 * vb + 8 * q) =
-            u32x2_t{pack_bf16x2(acc[vb][4 * q], acc[vb][4 * q + 1]), pack_bf16x2(acc[vb][4 * q + 2], acc[vb][4 * q + 3])};
+      for (int r = 0; r < 16; ++r) acc[vb][r] = 0.f;
+#pragma unroll
+    for (int c = 0; c < kPfDC / 16; ++c)
+#pragma unroll
+      for (int vb = 0; vb < DV / 32; ++vb) {
+        const bf16x8_t av = *reinterpret_cast<const bf16x8_t*>(wl + (32 * vb + r32) * RS + 16 * c + 8 * h);
+        acc[vb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, ob_hi[c], acc[vb], 0, 0, 0);
+        acc[vb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, ob_lo[c], acc[vb], 0, 0, 0);
+      }
+    // the next chunk's rows travel while this one is stored (the last chunk loads itself again)
+    __builtin_amdgcn_sched_barrier(0);
+    load(c0 + min(k + 1, nch - 1));
+    __builtin_amdgcn_sched_barrier(0);
+    if (t < T) {
+      uint16_t* dst = out + (static_cast<int64_t>(t) * kPfHeads + hh) * DV + 4 * h;
+#pragma unroll
+      for (int vb = 0; vb < DV / 32; ++vb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          *reinterpret_cast<u32x2_t*>(dst + 32 * vb + 8 * q) = u32x2_t{
+              pack_bf16x2(acc[vb][4 * q], acc[vb][4 * q + 1]), pack_bf16x2(acc[vb][4 * q + 2], acc[vb][4 * q + 3])};
+    }
   }
 }
 
