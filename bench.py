@@ -315,6 +315,15 @@ def append_main(args):
            "vs_baseline": None, "dtype": "bf16" if st == "bf16" else "fp32", "data": "synthetic",
            "config": {"workload": f"append_{n}_{wl.name}", "tokens": n, "hidden": wl.hidden,
                       "row_dim": wl.row_dim, "latent_norm": True}}
+    # whole call against HBM: hidden states and W_DKV read once, rows and ids written,
+    # slots / ids / positions read (4 bytes each), the norm weight
+    esz = 2 if st == "bf16" else 4
+    nbytes = n * wl.hidden * esz + wl.row_dim * wl.hidden * esz + n * (wl.row_dim * esz + 4) + 12 * n + \
+        wl.latent_dim * esz
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    out["roofline"] = {"bound": "hbm", "kernel": "eg_mla_append (whole call)", "achieved": gbs, "peak": HBM_PEAK_GBPS,
+                       "unit": "GB/s", "frac": gbs / HBM_PEAK_GBPS, "traffic": None,
+                       "algorithmic_bytes_per_call": nbytes, "mfma_tflops": flops / (ms * 1e-3) / 1e12}
     print(json.dumps(out), flush=True)
 
 
@@ -372,6 +381,16 @@ def literal_main(args):
                       "context": wl.seq_len if wl.seq_len else list(wl.seq_len_range)},
            "up_projection_gflop_per_step": flops / 1e9,
            "gate_bytes_per_step": tokens * width * 2}
+    # whole step against HBM: each cached token's gate row once, its cache row and id,
+    # the weights, queries and outputs (the value halves re-read by the kernel's
+    # second pass are its own overhead, not counted)
+    nbytes = tokens * (width * 2 + (wl.latent_dim + wl.rope_dim) * 2 + 4) + \
+        wl.heads * (wl.head_dim + wl.v_head_dim) * wl.latent_dim * 2 + \
+        wl.batch * wl.heads * (wl.head_dim + wl.rope_dim + wl.v_head_dim) * 2 + width * 4
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    out["roofline"] = {"bound": "hbm", "kernel": "eg_mla_decode_literal (whole call: tile and merge kernels)",
+                       "achieved": gbs, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBPS,
+                       "traffic": None, "algorithmic_bytes_per_call": nbytes}
     print(json.dumps(out), flush=True)
 
 
