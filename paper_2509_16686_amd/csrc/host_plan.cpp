@@ -264,7 +264,8 @@ eg_mla_status validate_literal(const eg_mla_dims* d, int32_t batch, const void* 
   if (d->dtype != EG_MLA_BF16 || d->latent_dim != 128 || d->head_dim != 128 || d->v_head_dim != 128 ||
       d->rope_dim != 64)
     return EG_MLA_ERR_UNSUPPORTED;
-  if (literal_lds_bytes(d->num_heads) > 160 * 1024) return EG_MLA_ERR_UNSUPPORTED;  // per-head state in LDS
+  // per-head state of a tile lives in LDS: 160 heads fit in 160 KB
+  if (d->num_heads > 160 || literal_lds_bytes(d->num_heads) > 160 * 1024) return EG_MLA_ERR_UNSUPPORTED;
   if (static_cast<int64_t>(d->vocab_size) * d->num_heads * (d->head_dim + d->v_head_dim) * 2 >= (int64_t{1} << 32))
     return EG_MLA_ERR_UNSUPPORTED;  // gate rows are addressed by 32-bit byte offsets
   if (static_cast<int64_t>(max_pages_per_seq) * d->page_size > (int64_t{1} << 30)) return EG_MLA_ERR_UNSUPPORTED;

@@ -203,6 +203,6 @@ def test_decode_literal_rejects_before_launch(L):
     assert big >= 2 * (1024 * 64 // 128) * 16 * (128 + 4) * 4  # 65536-token capacity: no limit on the context
     assert call(maxp=1024, nslots=2 * 1024 * 64, wsb=big - 1) == B.ERR_WORKSPACE
     for bad in (dims(latent_dim=512, gate_dim=512), dims(rope_dim=32), dims(dtype=B.FP32), dims(v_head_dim=64),
-                dims(num_heads=200),   # per-head tile state beyond the LDS
+                dims(num_heads=161),   # per-head tile state beyond the LDS
                 dims(vocab_size=600000)):  # a gate table of 4 GB or more
         assert call(dd=bad) == B.ERR_UNSUPPORTED
