@@ -59,7 +59,8 @@ def test_literal_paged_ragged_with_empty(gpu):
     (4, [33000, 257], 0, "mul", True),                     # past 32768 tokens: 258 tiles merged
     (20, [300, 1], B.LITERAL_ADD, "add", True),            # 20 heads: tile state beyond 80 KB of LDS
     (1, [129, 64], B.LITERAL_NO_LN, "mul", False),          # a single head
-], ids=["h4_l33000", "h20", "h1"])
+    (3, [260, 5], 0, "mul", True),                          # odd head count: a pair of heads, then the last alone
+], ids=["h4_l33000", "h20", "h1", "h3"])
 def test_literal_head_counts_and_long_context(gpu, heads, lens, flags, mode, use_ln):
     wl = W.WORKLOADS[1].replace(batch=len(lens), heads=heads, seq_len=None, seq_len_range=(1, max(lens)),
                                 vocab=1500, seed=83)
