@@ -35,7 +35,7 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kAbsorbRows = 16;
 constexpr int kAbsorbCols = 64;
 
-template <bool BF16, bool Q16 = false>
+template <bool BF16>
 __global__ __launch_bounds__(256) void absorb_kernel(const void* __restrict__ q, const void* __restrict__ w_uk,
                                                      float* __restrict__ qfull, int B, int H, int DH, int DC,
                                                      int DR) {
@@ -80,23 +80,20 @@ __global__ __launch_bounds__(256) void absorb_kernel(const void* __restrict__ q,
       float v = 0.f;
 #pragma unroll
       for (int j = 0; j < 4; ++j) v += red[(j * kAbsorbRows + bb) * kAbsorbCols + cc];
-      if constexpr (Q16) reinterpret_cast<uint16_t*>(qfull)[(static_cast<int64_t>(b0 + bb) * H + h) * DQ + c0 + cc] = f32_to_bf16(v);
-      else qfull[(static_cast<int64_t>(b0 + bb) * H + h) * DQ + c0 + cc] = v;
+      qfull[(static_cast<int64_t>(b0 + bb) * H + h) * DQ + c0 + cc] = v;
     }
   }
   if (blockIdx.y == 0) {
     for (int i = tid; i < nb * DR; i += 256) {
       const int bb = i / DR, r = i % DR;
-      const float v = ld<BF16>(q, (static_cast<int64_t>(b0 + bb) * H + h) * DQin + DH + r);
-      if constexpr (Q16) reinterpret_cast<uint16_t*>(qfull)[(static_cast<int64_t>(b0 + bb) * H + h) * DQ + DC + r] = f32_to_bf16(v);
-      else qfull[(static_cast<int64_t>(b0 + bb) * H + h) * DQ + DC + r] = v;
+      qfull[(static_cast<int64_t>(b0 + bb) * H + h) * DQ + DC + r] = ld<BF16>(q, (static_cast<int64_t>(b0 + bb) * H + h) * DQin + DH + r);
     }
   }
 }
 
 // Split-K bookkeeping shared by the split kernels.
 struct SplitArgs {
-  const float* qfull;         // [B, H, DQ] fp32 (bf16 for the balanced head-split kernel)
+  const float* qfull;         // [B, H, DQ] fp32; wide kernel: bf16 [B, H, DC + DQ] = [q hi | q^R | q lo]
   const void* cache;          // [num_slots, DQ]
   const int32_t* ids;         // [num_slots]
   const void* gate;           // [V, DC]
@@ -383,15 +380,18 @@ hipError_t launch_slice(const SplitArgs& a, int slices, int nblocks, hipStream_t
   return hipGetLastError();
 }
 
-// Balanced head-split kernel: `wgs` work-groups per block of 128 heads.
-hipError_t launch_wide(const SplitArgs& a, int wgs, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
-  hipExtLaunchKernelGGL(split_wide_kernel, dim3(wgs * a.groups), dim3(WideCfg::NT), 0, stream, ev0, ev1, 0, a);
+// Balanced head-split kernel: `ranges` token ranges x a.groups blocks of 64 heads.
+hipError_t launch_wide(const SplitArgs& a, int ranges, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
+  hipExtLaunchKernelGGL(split_wide_kernel, dim3(ranges * a.groups), dim3(WideCfg::NT), 0, stream, ev0, ev1, 0, a);
   return hipGetLastError();
 }
 
-// Work-groups per block of 128 heads of the balanced schedule: one work-group
-// per compute unit over all head blocks.
-int wide_groups(int head_groups) { return std::max(1, std::min(kWideMaxGroups, device_cus() / std::max(1, head_groups))); }
+// Token ranges of the balanced schedule: one work-group per compute unit over
+// all head blocks, a multiple of 8 (the head blocks of a range share an XCD).
+int wide_groups(int head_groups) {
+  const int g = std::min(kWideMaxGroups, device_cus() / std::max(1, head_groups));
+  return std::max(8, g / 8 * 8);
+}
 
 template <int DC, int DR>
 hipError_t launch_mfma(const SplitArgs& a, int nblocks, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
@@ -491,7 +491,7 @@ extern "C" eg_mla_status eg_mla_decode_planned(const eg_mla_dims* dims, int32_t 
       dim3 ga(d.num_heads, row_blocks, (d.latent_dim + cols - 1) / cols);
       const uint16_t* q16 = static_cast<const uint16_t*>(q);
       const uint16_t* wuk16 = static_cast<const uint16_t*>(w_uk);
-      if (p.balanced)  // the 128-head kernel reads a bf16 query
+      if (p.balanced)  // the wide kernel takes the query as bf16 hi + lo rows
         hipLaunchKernelGGL((absorb_mfma_kernel<128, kAbsBlocks, kAbsCols, true>), ga, dim3(256), 0, stream, q16,
                            wuk16, qfull, batch, d.num_heads, d.latent_dim, d.rope_dim);
       else if (grouped)
@@ -503,10 +503,6 @@ extern "C" eg_mla_status eg_mla_decode_planned(const eg_mla_dims* dims, int32_t 
       else
         hipLaunchKernelGGL((absorb_mfma_kernel<128, 1, kAbsCols>), ga, dim3(256), 0, stream, q16, wuk16, qfull, batch,
                            d.num_heads, d.latent_dim, d.rope_dim);
-    } else if (bf && p.balanced) {
-      if (set_lds(absorb_kernel<true, true>, lds) != hipSuccess) return EG_MLA_ERR_HIP;
-      hipLaunchKernelGGL((absorb_kernel<true, true>), grid, dim3(256), lds, stream, q, w_uk, qfull, batch,
-                         d.num_heads, d.head_dim, d.latent_dim, d.rope_dim);
     } else if (bf) {
       if (set_lds(absorb_kernel<true>, lds) != hipSuccess) return EG_MLA_ERR_HIP;
       hipLaunchKernelGGL(absorb_kernel<true>, grid, dim3(256), lds, stream, q, w_uk, qfull, batch, d.num_heads,

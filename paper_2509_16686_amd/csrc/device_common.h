@@ -21,6 +21,13 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
   __bf16 h = static_cast<__bf16>(f);
   return __builtin_bit_cast(uint16_t, h);
 }
+// Two fp32 -> packed bf16 pair (lo in bits 0..15), one v_cvt_pk_bf16_f32.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+  typedef __attribute__((ext_vector_type(2))) float f32x2_t;
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
+}
+
 // Gated latent of one 16-byte chunk: word e of the result packs
 // bf16(lat.lo * gate.lo) and bf16(lat.hi * gate.hi) of word e.  Each product is
 // v_dot2_f32_bf16 of the latent word with the gate word's other half zeroed: a
@@ -59,6 +66,39 @@ __device__ __forceinline__ u32x4_t gate_chunk(u32x4_t lat, u32x4_t gate) {
   return out;
 }
 
+// Gated latent of one 16-byte chunk as bf16 hi + lo: hi is gate_chunk's
+// result and lo packs bf16(t - hi) of each exact fp32 product t.  A product of
+// two bf16 values has at most 16 significant bits and hi keeps the top 8
+// (rounded), so the remainder fits a bf16 exactly: hi + lo == lat * gate.  The
+// products are read here after gate_chunk's block has ended, which leaves
+// them more than the 3 wait states a DOT result needs.
+__device__ __forceinline__ void gate_chunk_hilo(u32x4_t lat, u32x4_t gate, u32x4_t& hi, u32x4_t& lo) {
+  float t[8];
+  asm("v_dot2_f32_bf16 %[t0], %[a0], %[l0], 0\n\t"
+      "v_dot2_f32_bf16 %[t1], %[a0], %[h0], 0\n\t"
+      "v_dot2_f32_bf16 %[t2], %[a1], %[l1], 0\n\t"
+      "v_dot2_f32_bf16 %[t3], %[a1], %[h1], 0\n\t"
+      "v_dot2_f32_bf16 %[t4], %[a2], %[l2], 0\n\t"
+      "v_dot2_f32_bf16 %[t5], %[a2], %[h2], 0\n\t"
+      "v_dot2_f32_bf16 %[t6], %[a3], %[l3], 0\n\t"
+      "v_dot2_f32_bf16 %[t7], %[a3], %[h3], 0\n\t"
+      "v_cvt_pk_bf16_f32 %[o0], %[t0], %[t1]\n\t"
+      "v_cvt_pk_bf16_f32 %[o1], %[t2], %[t3]\n\t"
+      "v_cvt_pk_bf16_f32 %[o2], %[t4], %[t5]\n\t"
+      "s_nop 1\n\t"
+      "v_cvt_pk_bf16_f32 %[o3], %[t6], %[t7]\n\t"
+      "s_nop 1"
+      : [o0] "=&v"(hi[0]), [o1] "=&v"(hi[1]), [o2] "=&v"(hi[2]), [o3] "=&v"(hi[3]), [t0] "=&v"(t[0]),
+        [t1] "=&v"(t[1]), [t2] "=&v"(t[2]), [t3] "=&v"(t[3]), [t4] "=&v"(t[4]), [t5] "=&v"(t[5]), [t6] "=&v"(t[6]),
+        [t7] "=&v"(t[7])
+      : [a0] "v"(lat[0]), [a1] "v"(lat[1]), [a2] "v"(lat[2]), [a3] "v"(lat[3]), [l0] "v"(gate[0] & 0xffffu),
+        [l1] "v"(gate[1] & 0xffffu), [l2] "v"(gate[2] & 0xffffu), [l3] "v"(gate[3] & 0xffffu),
+        [h0] "v"(gate[0] & 0xffff0000u), [h1] "v"(gate[1] & 0xffff0000u), [h2] "v"(gate[2] & 0xffff0000u),
+        [h3] "v"(gate[3] & 0xffff0000u));
+#pragma unroll
+  for (int e = 0; e < 4; ++e) lo[e] = pack_bf16x2(t[2 * e] - bf16_lo(hi[e]), t[2 * e + 1] - bf16_hi(hi[e]));
+}
+
 // Largest growth (log2 units) of a head's running maximum that an online
 // softmax absorbs without rescaling its accumulators: probabilities relative
 // to the stale maximum stay below 2^8, far from fp32 overflow.
@@ -85,12 +125,6 @@ __device__ __forceinline__ float sum_over_row_groups(float x) {
   return __uint_as_float(s16[0]) + __uint_as_float(s16[1]);
 }
 
-// Two fp32 -> packed bf16 pair (lo in bits 0..15), one v_cvt_pk_bf16_f32.
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
-  typedef __attribute__((ext_vector_type(2))) float f32x2_t;
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
-}
 
 // Storage-typed scalar access.
 template <bool BF16>

@@ -26,7 +26,7 @@ bool mfma_shape_supported(const eg_mla_dims& d) {
 
 bool tok_kernel_shape(const eg_mla_dims& d) { return d.latent_dim == 128 && d.rope_dim == 64; }
 bool heads_kernel_shape(const eg_mla_dims& d) {
-  return d.latent_dim == 512 && d.rope_dim == 64 && d.num_heads % kHeadsPerItemWide == 0;
+  return d.latent_dim == 512 && d.rope_dim == 64 && d.head_dim == 128 && d.num_heads % kHeadsPerItemWide == 0;
 }
 
 eg_mla_status check_dims(const eg_mla_dims* d) {
@@ -239,9 +239,9 @@ eg_mla_status validate_prefill_varlen(const eg_mla_dims* d, int32_t batch, int32
 
 size_t literal_lds_bytes(int num_heads) {
   // weight / gate-tile region, per-wave scores [4][H][32], value sums [4][d_v],
-  // two sums per head and three per-wave figures per head (all fp32)
+  // two sums per head, per-wave figures per head, token means [4][32] (all fp32)
   return 272 * 256 + 4 * static_cast<size_t>(num_heads) * 32 * 4 + 4 * 128 * 4 +
-         static_cast<size_t>(num_heads) * (2 + 12) * 4;
+         static_cast<size_t>(num_heads) * (2 + 12) * 4 + 4 * 32 * 4;
 }
 
 size_t literal_workspace_bytes(const eg_mla_dims& d, int32_t batch, int32_t max_pages_per_seq) {

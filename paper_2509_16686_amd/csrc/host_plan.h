@@ -28,12 +28,13 @@ constexpr int kIdSlices = 8;
 bool mfma_shape_supported(const eg_mla_dims& d);
 // MFMA shapes served by the token-split kernel (16 heads per work item)...
 bool tok_kernel_shape(const eg_mla_dims& d);
-// ... and by the head-split kernel (128 heads per work item); the others by the
+// ... and by the head-split kernel (64 heads per work item); the others by the
 // dimension-split kernel (16 heads per work item).
 bool heads_kernel_shape(const eg_mla_dims& d);
-constexpr int kHeadsPerItemWide = 128;
-// Balanced schedule of the head-split kernel: at most this many work-groups
-// per block of 128 heads (one per compute unit of the device).
+constexpr int kHeadsPerItemWide = 64;
+// Balanced schedule of the head-split kernel: at most this many token ranges
+// (one work-group per range and block of 64 heads, one per compute unit of the
+// device over all head blocks).
 constexpr int kWideMaxGroups = 512;
 
 struct DecodePlan {
@@ -96,8 +97,8 @@ eg_mla_status validate_prefill_varlen(const eg_mla_dims* d, int32_t batch, int32
                                       const void* out);
 
 // Decode with the paper-literal gate: workspace = one fp32 record per
-// (sequence, 128-token tile, head): d_v value sums, the tile's max, sum of p,
-// sum of a mu, one pad.  LDS of the tile kernel for a head count.
+// (sequence, 128-token tile, head): d_v centred value sums, the tile's max,
+// sum of p, two pads.  LDS of the tile kernel for a head count.
 size_t literal_workspace_bytes(const eg_mla_dims& d, int32_t batch, int32_t max_pages_per_seq);
 size_t literal_lds_bytes(int num_heads);
 eg_mla_status validate_literal(const eg_mla_dims* d, int32_t batch, const void* q, const void* latent_cache,

@@ -10,8 +10,12 @@
 //
 // The LayerNorm is linear once a token's moments are known, so neither the
 // gated rows nor the normalised ones are ever stored:
-//   score  = tau (rstd (sum_d q_d w_d x_d - mu sum_d q_d w_d) + sum_d q_d b_d + q^R . k^R)
-//   out    = w_v (sum_j a_j x_j - sum_j a_j mu_j) / sum_j p_j + b_v,   a_j = p_j rstd_j.
+//   score  = tau (rstd (sum_d q_d w_d (x_d - K) - (mu - K) sum_d q_d w_d) + sum_d q_d b_d + q^R . k^R)
+//   out    = w_v (sum_j a_j (x_j - mu_j)) / sum_j p_j + b_v,   a_j = p_j rstd_j.
+// K is a per-token pivot (the token's first gated value): the moments and
+// the key dots are sums of x - K, which stay of the size of the spread of x
+// even when |mu| is many times sigma (no cancellation in m2 - m1^2), and the
+// value pass centres each x on its token's mean before weighting it.
 // Two kernels (bf16 storage, d_c = d_h = d_v = 128, d_r = 64):
 //  1. literal_tile_kernel: one work-group per (sequence, 128 cached tokens),
 //     4 waves of 32 tokens, split-K style.  Pass 1 walks the heads: one head's
@@ -24,7 +28,7 @@
 //     for 16 tokens), its gate tile staged in LDS by whole 256-byte rows and
 //     read back with ds_read_b64_tr_b16, so sum_j a_j x_j is 16 FMAs per lane
 //     and one exchange between the lane halves.  Emits per (tile, head)
-//     o = sum_j a_j x_j, the max, sum_j p_j and sum_j a_j mu_j.
+//     o = sum_j a_j (x_j - mu_j), the max and sum_j p_j.
 //  2. literal_merge_kernel: one work-group per (sequence, head) rescales the
 //     tiles' partials to a common max and applies the value part's affine.
 // HBM traffic per cached token: its gate row once, plus the value half again
@@ -78,7 +82,8 @@ __global__ __launch_bounds__(256, 2) void literal_tile_kernel(
   float* ob = kd + 4 * H * 32;                                 // [4][d_v] pass-2 sums; pass 1: q w of the head
   float* sqw = ob + 4 * kLtDV;                                 // [H] sum_d q_d w_d
   float* sqb = sqw + H;                                        // [H] sum_d q_d b_d
-  float* wr = sqb + H;                                         // [3][4][H] per-wave max, sum p, sum a mu
+  float* wr = sqb + H;                                         // [2][4][H] per-wave max, sum p
+  float* mus = wr + 12 * H;                                    // [4 waves][32 tokens] token means
   // at least one head (the host checks): every head loop runs, so no load is
   // left pending on a zero-trip path into the loops after it
   __builtin_assume(H >= 1);
@@ -164,7 +169,8 @@ __global__ __launch_bounds__(256, 2) void literal_tile_kernel(
       sqb[hh] = kd[4 * hh + 1] + kd[4 * hh + 3];
     }
   }
-  float s1 = 0.f, s2 = 0.f;
+  // moments of the token's x - K (K: the pivot) and the key dots sum q w (x - K)
+  float s1 = 0.f, s2 = 0.f, K = 0.f;
   auto block = [&](int head, int blk, float& kdp) {
     lt_f32x16_t acc;
 #pragma unroll
@@ -175,6 +181,15 @@ __global__ __launch_bounds__(256, 2) void literal_tile_kernel(
       acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8_t*>(arow + 16 * c), cb[c], acc, 0,
                                                     0, 0);
     // lane holds outputs 32 blk + 8 qq + 4 hf + e of its token in acc[4 qq + e]
+    if (LN && blk == 0) {
+      // pivot: the token's first gated value (output 0 of head 0, in the lane
+      // half hf = 0), the same in both halves; set on the first head only
+      const uint32_t gw = gv[0][0][0];
+      const float x0 = ADD ? acc[0] + bf16_lo(gw) : acc[0] * bf16_lo(gw);
+      const uint32_t u = __float_as_uint(x0);
+      const auto sw = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+      K = head == 0 ? __uint_as_float(sw[0]) : K;
+    }
 #pragma unroll
     for (int qq = 0; qq < 4; ++qq) {
       float4 qa = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -183,7 +198,7 @@ __global__ __launch_bounds__(256, 2) void literal_tile_kernel(
       for (int e = 0; e < 4; ++e) {
         const uint32_t gw = gv[blk & 3][qq][e >> 1];
         const float g = (e & 1) ? bf16_hi(gw) : bf16_lo(gw);
-        const float x = ADD ? acc[4 * qq + e] + g : acc[4 * qq + e] * g;
+        const float x = (ADD ? acc[4 * qq + e] + g : acc[4 * qq + e] * g) - K;  // K = 0 without a LayerNorm
         if (LN) {
           s1 += x;
           s2 = fmaf(x, x, s2);
@@ -251,12 +266,16 @@ __global__ __launch_bounds__(256, 2) void literal_tile_kernel(
   __syncthreads();  // region R is free
   float* qrs = reinterpret_cast<float*>(lt_lds);  // [H][d_r]
   for (int i = tid; i < H * kLtDR; i += 256) qrs[i] = bf16_to_f32(qb[(i >> 6) * (kLtDH + kLtDR) + kLtDH + (i & 63)]);
-  float mu = 0.f, rstd = 1.f;
+  float mu = 0.f, dmu = 0.f, rstd = 1.f;  // mean, mean - K, 1 / sigma
   if (LN) {
+    // moments about the pivot: m1 = mean(x - K) is of the size of sigma or a
+    // few sigma, so m2 - m1^2 keeps its precision
     const float m1 = lane_half_sum(s1) / static_cast<float>(width);
     const float m2 = lane_half_sum(s2) / static_cast<float>(width);
-    mu = m1;
+    dmu = m1;
+    mu = K + m1;
     rstd = 1.0f / sqrtf(fmaxf(m2 - m1 * m1, 0.f) + kLtLnEps);
+    if (hf == 0) mus[w * 32 + t] = mu;
   }
   __syncthreads();
   for (int head = 0; head < H; ++head) {
@@ -274,7 +293,7 @@ __global__ __launch_bounds__(256, 2) void literal_tile_kernel(
     const float rd = lane_half_sum(rp);
     float* kp = kd + (w * H + head) * 32 + t;
     const float dot = *kp;
-    const float base = LN ? rstd * (dot - mu * sqw[head]) + sqb[head] : dot;
+    const float base = LN ? rstd * (dot - dmu * sqw[head]) + sqb[head] : dot;
     const float s = ok ? scale_log2 * (base + rd) : -INFINITY;
     const float wm = wave_max(s);
     if (hf == 0) *kp = s;
@@ -288,20 +307,15 @@ __global__ __launch_bounds__(256, 2) void literal_tile_kernel(
     const float a = p * rstd;
     // both lane halves hold the same token: half of the wave sum is exact
     const float sp = 0.5f * wave_sum(p);
-    const float sa = LN ? 0.5f * wave_sum(a * mu) : 0.f;
     __builtin_amdgcn_wave_barrier();
     if (hf == 0) *kp = a;
-    if (lane == 0) {
-      wr[(4 + w) * H + head] = sp;
-      wr[(8 + w) * H + head] = sa;
-    }
+    if (lane == 0) wr[(4 + w) * H + head] = sp;
   }
   __syncthreads();
   for (int hh = tid; hh < H; hh += 256) {
     float* rec = pb + hh * (kLtDV + 4) + kLtDV;
     rec[0] = fmaxf(fmaxf(wr[hh], wr[H + hh]), fmaxf(wr[2 * H + hh], wr[3 * H + hh]));
     rec[1] = (wr[4 * H + hh] + wr[5 * H + hh]) + (wr[6 * H + hh] + wr[7 * H + hh]);
-    rec[2] = (wr[8 * H + hh] + wr[9 * H + hh]) + (wr[10 * H + hh] + wr[11 * H + hh]);
   }
 
   // ---- pass 2: sum_j a_j x_j of the value part ---------------------------------
@@ -326,10 +340,13 @@ __global__ __launch_bounds__(256, 2) void literal_tile_kernel(
     }
   };
   auto values = [&](int head) {
-    // a_j of tokens 8 qq + 4 hf + i (the rows of this lane's accumulator registers)
-    float4 av[4];
+    // a_j and mu_j of tokens 8 qq + 4 hf + i (the rows of this lane's accumulator registers)
+    float4 av[4], mv[4];
 #pragma unroll
-    for (int qq = 0; qq < 4; ++qq) av[qq] = *reinterpret_cast<const float4*>(kd + (w * H + head) * 32 + 8 * qq + 4 * hf);
+    for (int qq = 0; qq < 4; ++qq) {
+      av[qq] = *reinterpret_cast<const float4*>(kd + (w * H + head) * 32 + 8 * qq + 4 * hf);
+      mv[qq] = LN ? *reinterpret_cast<const float4*>(mus + w * 32 + 8 * qq + 4 * hf) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
 #pragma unroll
     for (int blk = 0; blk < kLtDV / 32; ++blk) {
       lt_f32x16_t acc;
@@ -350,7 +367,7 @@ __global__ __launch_bounds__(256, 2) void literal_tile_kernel(
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const float g = bf16_to_f32(static_cast<uint16_t>(g4[i]));
-          const float x = ADD ? acc[4 * qq + i] + g : acc[4 * qq + i] * g;
+          const float x = (ADD ? acc[4 * qq + i] + g : acc[4 * qq + i] * g) - (&mv[qq].x)[i];  // x - mu_j
           o = fmaf((&av[qq].x)[i], x, o);
         }
       }
@@ -417,28 +434,26 @@ __global__ __launch_bounds__(128) void literal_merge_kernel(const float* __restr
 #pragma unroll
     for (int k = 0; k < 8; ++k) m = fmaxf(m, mk[k]);
   }
-  float o = 0.f, l = 0.f, amu = 0.f;
+  float o = 0.f, l = 0.f;
   for (int i0 = 0; i0 < nt; i0 += 8) {
-    float ok_[8], mk[8], lk[8], ak[8];
+    float ok_[8], mk[8], lk[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
       const float* rec = pp + min(i0 + k, nt - 1) * stride;
       ok_[k] = rec[v];
       mk[k] = i0 + k < nt ? rec[kLtDV] : -INFINITY;  // a missing tile weighs 0
       lk[k] = rec[kLtDV + 1];
-      ak[k] = rec[kLtDV + 2];
     }
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
       const float e = exp2f(mk[k] - m);
       o = fmaf(e, ok_[k], o);
       l = fmaf(e, lk[k], l);
-      amu = fmaf(e, ak[k], amu);
     }
   }
   const float wv = use_ln ? bf16_to_f32(ln_w[hh * kLtHeadW + kLtDH + v]) : 1.f;
   const float bv = use_ln ? bf16_to_f32(ln_b[hh * kLtHeadW + kLtDH + v]) : 0.f;
-  orow[v] = f32_to_bf16(wv * (o - amu) / l + bv);
+  orow[v] = f32_to_bf16(wv * o / l + bv);  // o: sum of a_j (x_j - mu_j), already centred
 }
 
 }  // namespace egmla

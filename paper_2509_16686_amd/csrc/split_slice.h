@@ -23,14 +23,16 @@
 //   * loads whole 128-byte lines: each latent and gate instruction covers 4
 //     tokens x 256 bytes (16 lanes per token, 16 bytes each), each RoPE-key
 //     instruction 8 tokens x 128 bytes;
-//   * gates in fp32 (exact product of two bf16 values, rounded once to bf16)
-//     and stores the gated unit row-major ([token][latent | RoPE key]) in its
-//     own LDS tile;
+//   * gates in fp32 (exact product of two bf16 values) and stores the gated
+//     unit row-major ([token][latent hi | RoPE key | latent lo]) in its own
+//     LDS tile: the product rounded to bf16 (hi) and the bf16 remainder (lo),
+//     whose sum is the product exactly;
 //   * reads the tile back in the layout of the MFMA A operand (lane: token
 //     lane % 16, 16 bytes = 8 consecutive dims of a 32-dim chunk) and
-//     computes S^T[token][head] with v_mfma_f32_16x16x32_bf16; the fp32
-//     absorbed query enters as bf16 hi + lo (two products), the RoPE query
-//     (a stored bf16 value) once;
+//     computes S^T[token][head] with v_mfma_f32_16x16x32_bf16: the fp32
+//     absorbed query q enters as bf16 hi + lo, and the latent part of a score
+//     is hi.q_hi + hi.q_lo + lo.q_hi (only the lo.lo product, below 2^-16 of
+//     the score, is left out); the RoPE query (a stored bf16 value) once;
 //   * runs the online softmax on the accumulator layout (lane: one head, 4
 //     tokens), rescaling only when a head's maximum grows by more than 2^8;
 //   * reads each 16-dim block of the latent part with ds_read_b64_tr_b16,
@@ -59,7 +61,7 @@ struct SsplitCfg {
   static constexpr int RPT = DR / 8;                 // lanes per token of a RoPE load
   static constexpr int TPR = RPT > 0 ? 64 / RPT : 1; // tokens per RoPE load instruction
   static constexpr int NRI = RPT > 0 ? 16 / TPR : 0; // RoPE load instructions per unit
-  static constexpr int TS = DQ + 8;                  // bf16 elements per tile row (16 bytes of padding)
+  static constexpr int TS = DQ + DC + 8;             // tile row: latent hi | RoPE key | latent lo | 16 bytes of padding
   static constexpr int ROWS = kMaxScanTokens / 256;  // scan rows of a work item, at most
   static constexpr int RPW = ROWS / NW;              // scan rows per wave, at most
   static constexpr int LDS_LIST = kMaxScanTokens * 8;            // slot + id of every kept token
@@ -369,28 +371,35 @@ __global__ __launch_bounds__(NW * 64, 2) void split_slice_kernel(SplitArgs a) {
     uint16_t* tread = tile + (4 * g + (r16 >> 2)) * TS + 4 * (r16 & 3);
     auto process = [&](SliceRegs<NLI, NRI>& rg, int i, bool refill) {
       const int nt = ntok - (w + i * NW) * 16;  // valid tokens of the unit (>= 1)
-      // gate the latent; stage the unit row-major in this wave's tile
+      // gate the latent (hi and lo); stage the unit row-major in this wave's tile
 #pragma unroll
-      for (int c = 0; c < NLI; ++c)
-        *reinterpret_cast<u32x4_t*>(tile + (TPL * c + lt) * TS + lc) = gate_chunk(rg.lat[c], rg.gat[c]);
+      for (int c = 0; c < NLI; ++c) {
+        u32x4_t hi, lo;
+        gate_chunk_hilo(rg.lat[c], rg.gat[c], hi, lo);
+        *reinterpret_cast<u32x4_t*>(tile + (TPL * c + lt) * TS + lc) = hi;
+        *reinterpret_cast<u32x4_t*>(tile + (TPL * c + lt) * TS + DQ + lc) = lo;
+      }
 #pragma unroll
       for (int c = 0; c < NRI; ++c) *reinterpret_cast<u32x4_t*>(tile + (TPR * c + rt) * TS + DC + rcol) = rg.rop[c];
       // this unit's registers are free: issue unit i + D into them
       if (refill) issue(rg, i + D);
       wave_lds_sync();
-      // S^T[token 4g + q][head r16]
-      f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+      // S^T[token 4g + q][head r16], two accumulator chains
+      f32x4_t acc = {0.f, 0.f, 0.f, 0.f}, acc2 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int c = 0; c < NC; ++c) {
         const bf16x8_t av = *reinterpret_cast<const bf16x8_t*>(tile + r16 * TS + c * 32 + g * 8);
+        const bf16x8_t al = *reinterpret_cast<const bf16x8_t*>(tile + r16 * TS + DQ + c * 32 + g * 8);
         acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, qh[c], acc, 0, 0, 0);
+        acc2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, qh[c], acc2, 0, 0, 0);
         acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, ql[c], acc, 0, 0, 0);
       }
 #pragma unroll
       for (int rc = 0; rc < NR; ++rc) {
         const bf16x8_t av = *reinterpret_cast<const bf16x8_t*>(tile + r16 * TS + DC + rc * 32 + g * 8);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, qr[rc], acc, 0, 0, 0);
+        acc2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, qr[rc], acc2, 0, 0, 0);
       }
+      acc += acc2;
 
       // online softmax over the unit's 16 tokens
       float x[4];

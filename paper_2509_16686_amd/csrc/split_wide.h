@@ -1,43 +1,45 @@
-// Wide split kernel of EG-MLA decode: 128 heads per work-group, latent dim
-// 512, RoPE dim 64, bf16 storage.  Included by decode.hip after SplitArgs.
+// Wide split kernel of EG-MLA decode: latent dim 512, RoPE dim 64, bf16
+// storage, heads in blocks of 64.  Included by decode.hip after SplitArgs.
 //
-// One work-group of 8 waves (two per SIMD) per (sequence b, context split s,
-// block of 128 heads).  Wave w = 2 hg + dh pairs a head group hg (32 heads) with
-// a dimension half dh (latent dims 256 dh .. + 255 and RoPE dims 32 dh .. + 31,
-// 288 of the 576 score dims).  The split's tokens are taken 16 at a time (a
-// tile).
+// Work split.  One work-group of 4 waves (one per SIMD) per (token range, block
+// of 64 heads); wave w holds heads 16 w .. 16 w + 15 of the block over all 576
+// score dims and all 512 value dims, so no wave needs another wave's scores.
+// The two head blocks of a 128-head layer run the same token range on the same
+// XCD (blocks 8 apart), so the second fetch of a token's rows hits that XCD's
+// L2 cache.
 //
-// Staging.  Cache rows and gate rows go from HBM straight into LDS with
-// global_load_lds_dwordx4 (no registers): a ring of 3 tile slots, two tiles in
-// flight ahead of the one being computed.  Wave w fetches tokens 2w and 2w + 1
-// of every tile: per token one instruction for the 1024-byte latent row, one
-// for the 1024-byte gate row and one (8 lanes) for the 128-byte RoPE key.
-// It then gates those 2 tokens in place (exact fp32 product, one bf16
-// rounding), so the tile holds [token][gated latent] and [token][RoPE key].
+// Precision.  The absorbed query (fp32) is held as bf16 hi + lo, and each gated
+// latent c * g (an exact fp32 product of two bf16 values, 16 significant bits)
+// as bf16 hi + lo whose sum is the product exactly.  A score's latent part is
+// hi.q_hi + hi.q_lo + lo.q_hi (the lo.lo product, below 2^-16 of the score, is
+// left out), so a score carries fp32-level error even when the logits are
+// large and the softmax is sharp; the RoPE part (bf16 x bf16) is exact.  The
+// value product takes the gated latent's hi part and bf16 probabilities.
 //
-// Scores.  Wave (hg, dh) computes the partial S^T[token][head] of its 32 heads
-// over its 288 dims with v_mfma_f32_16x16x32_bf16: the A operand (token lane%16,
-// 8 dims) read from the tile, the B operand the absorbed query (written in
-// bf16 by the absorption) held in registers (64 per lane; its RoPE chunk in
-// LDS).  The two waves of a head group
-// exchange their partial sums through LDS; both add them in the same order, so
-// both hold the same scores and run the same online softmax (log2 domain,
-// lazy rescale).  The exchange synchronises only the two waves of the pair
-// (a flag in LDS), so pairs drift apart and one pair's softmax overlaps
-// another pair's score products on the same SIMDs.
+// Staging.  Tokens are taken 16 at a time (a slot); a ring of 4 slots holds two
+// pairs of slots, one computed while the other's rows travel.  Cache rows and
+// gate rows go from HBM straight into LDS with global_load_lds_dwordx4 (no
+// registers): per token one 1024-byte latent DMA (into the slot's HI region),
+// one 1024-byte gate DMA (into its LO region) and a 128-byte RoPE key.  Wave w
+// fetches and then gates tokens 4 w .. 4 w + 3 of every slot in place: HI
+// receives bf16(c g), LO the remainder.
 //
-// Values.  Wave (hg, dh) accumulates O^T[dim][head] for its 32 heads and its
-// 256 latent dims on v_mfma_f32_32x32x16_bf16 (128 accumulators per lane).  The
-// A operand is two ds_read_b64_tr_b16 of the gated latent (16-lane transposes:
-// one dim, 4 tokens each); the B operand is the probabilities, moved from the
-// score accumulator layout into the operand layout with v_permlane16_swap.
+// Scores.  S^T[token][head] of a slot on v_mfma_f32_16x16x32_bf16: the A
+// operand (token lane % 16, 8 dims) is read from the slot, the B operand is
+// the query (16 heads) held in registers: 3 latent products per 32-dim chunk
+// on three accumulator chains, then the RoPE chunks.
 //
-// Registers: 128 accumulators + 64 query + the tile's temporaries fit the 256
-// of a wave at two waves per SIMD in one register file.
+// Softmax and values.  Per pair of slots the lane holds 8 scores of its head
+// (4 tokens of each slot); online softmax in the log2 domain with a lazy
+// rescale.  O^T[dim][head] += C~^T P^T on v_mfma_f32_16x16x32_bf16 with K = the
+// pair's 32 tokens: each lane's own 8 probabilities are its B operand, and two
+// ds_read_b64_tr_b16 (one per slot, the same 4 token rows) are its A operand,
+// so the token order inside K is the same for both operands.
 //
-// LDS traffic per tile (bytes): tile data 35 K written by the DMA, gating 32 K
-// read and 16 K written, scores 74 K read, exchange 16 K written and read,
-// values 64 K read.
+// Registers per wave: query hi + lo 128 (its RoPE chunks wait in LDS), value
+// accumulators 128 (32 blocks of 16 dims x 16 heads), the score chain and the
+// operands in flight: one wave per SIMD.  Each phase (gating, scores, values)
+// reads its LDS operands at most two steps ahead of their use.
 #pragma once
 
 namespace egmla {
@@ -53,6 +55,12 @@ namespace egmla {
 __device__ __forceinline__ void lds_dma16(const void* sbase, uint32_t voff, uint32_t lds_base) {
   asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds_base), "v"(voff),
                "s"(sbase));
+}
+
+// The same with a full 64-bit address per lane (lanes of one instruction may
+// read different rows); inactive lanes move nothing.
+__device__ __forceinline__ void lds_dma16_addr(uint64_t addr, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds_base), "v"(addr));
 }
 
 // s_waitcnt with only the vector-memory counter constrained; also a compiler
@@ -71,47 +79,46 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 }
 
-typedef __attribute__((ext_vector_type(16))) float f32x16_t;
-
-// Latent rows in LDS are stored with their 16-byte pieces permuted: logical
-// piece p of tile row r sits at piece p ^ lat_swz(r).  The permutation keeps
-// both MFMA operand reads free of bank conflicts (32 or 64 banks): the score
-// read (16 rows, one piece each) hits 16 distinct 4-bank groups, and the
-// transposed value read (4 rows x 32 bytes per 16 lanes) 4 distinct pairs.
+// Rows in a slot's HI and LO regions are stored with their 16-byte pieces
+// permuted: logical piece p of slot row r sits at piece p ^ lat_swz(r)
+// (lat_swz(r) < 16 takes 16 distinct values over r = 0..15).  The score read
+// (16 rows, one piece each: 4-bank group (p ^ lat_swz(r)) mod 16) and the
+// transposed value read (4 rows x one 32-byte pair each: pair index
+// (p / 2) ^ (lat_swz(r) / 2) differs over each group of 4 rows) are then free
+// of bank conflicts.
 __device__ __forceinline__ int lat_swz(int r) { return ((0xCA60 >> (4 * (r & 3))) & 15) ^ (r >> 2); }
 
 struct WideCfg {
   static constexpr int DC = 512, DR = 64, DQ = DC + DR;
-  static constexpr int NW = 8, NT = NW * 64;
-  static constexpr int HEADS = 128;       // heads per work-group
-  static constexpr int NS = 3;            // ring slots
-  static constexpr int LROW = DC * 2;       // bytes per latent row in LDS (pieces swizzled, see lat_swz)
-  static constexpr int LAT = 0;                       // [16][LROW]   latent, gated in place
-  static constexpr int ROPE = LAT + 16 * LROW;        // [16][128 B]  RoPE keys, 16-byte pieces swizzled
-  static constexpr int GATE = ROPE + 16 * DR * 2;     // [16][1024 B] gate rows
-  static constexpr int SLOT = GATE + 16 * DC * 2;     // bytes per slot
+  static constexpr int NW = 4, NT = NW * 64;
+  static constexpr int HEADS = 64;        // heads per work-group
+  static constexpr int TOK = 16;          // tokens per slot
+  static constexpr int NS = 4;            // ring slots (two pairs)
+  static constexpr int LROW = DC * 2;     // bytes per latent row in LDS (pieces swizzled, see lat_swz)
+  static constexpr int HI = 0;                       // [16][LROW] latent, then bf16(c g)
+  static constexpr int LO = HI + TOK * LROW;         // [16][LROW] gate row, then c g - bf16(c g)
+  static constexpr int ROPE = LO + TOK * LROW;       // [16][128 B] RoPE keys, 16-byte pieces swizzled
+  static constexpr int SLOT = ROPE + TOK * DR * 2;   // bytes per slot
   static constexpr int RING = NS * SLOT;
-  static constexpr int LIST = RING;                               // int2 (slot, id) per token
-  static constexpr int XBUF = LIST + kMaxSplitTokensDevice * 8;   // [NW][2][64] f32x4 partial scores
-  static constexpr int QROPE = XBUF + NW * 2 * 64 * 16;           // [NW][2][64] bf16x8 RoPE query (B operand)
-  static constexpr int FLAGS = QROPE + NW * 2 * 64 * 16;          // [NW] int: exchanges published per wave
-  static constexpr int LDS_BYTES = FLAGS + NW * 4;
-  static constexpr int SPIN_LIMIT = 1 << 16;  // polls of a partner's flag before giving up (never reached)
-  static constexpr int DMA_PER_TILE = 6;  // per wave: 2 latent, 2 gate, 2 RoPE
+  static constexpr int LIST = RING;                  // int2 (slot, id) per token
+  static constexpr int LISTCAP = 1024;               // tokens listed at a time (a multiple of 32)
+  static constexpr int QROPE = LIST + LISTCAP * 8;   // [NW][2 chunks][64 lanes] bf16x8: RoPE query (B operand)
+  static constexpr int LDS_BYTES = QROPE + NW * 2 * 64 * 16;
+  static constexpr int DMA_PER_PAIR = 2 * 9;  // per wave and pair: 4 latent, 4 gate, 1 RoPE DMA per slot
   static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
-  static_assert(SLOT % 16 == 0 && LIST % 16 == 0 && XBUF % 16 == 0 && QROPE % 16 == 0, "alignment");
+  static_assert(SLOT % 16 == 0 && LIST % 16 == 0, "alignment");
 };
 
 // Balanced schedule of the wide kernel.  The batch's tokens, taken sequence
-// after sequence, form one range of N = sum of the clamped lengths; work-group
-// g of G_eff = min(G, N) takes positions [g N / G_eff, (g + 1) N / G_eff), which
-// may span several sequences, so every work-group gets the same number of
-// tokens (+-1) whatever the length mix.  Its part of sequence b is a segment
-// with its own partial result, stored at partial row g + b: along the
-// staircase of (work-group, sequence) pairs that have tokens, g + b grows by one
-// at every step, so the rows are distinct (at most G_eff + B - 1 of them) and
-// those of sequence b are consecutive.  One work-group of 1024 threads computes
-// the prefix sums of the lengths and writes:
+// after sequence, form one range of N = sum of the clamped lengths; range g of
+// G_eff = min(G, N) takes positions [g N / G_eff, (g + 1) N / G_eff), which
+// may span several sequences, so every range gets the same number of tokens
+// (+-1) whatever the length mix.  Its part of sequence b is a segment with its
+// own partial result, stored at partial row g + b: along the staircase of
+// (range, sequence) pairs that have tokens, g + b grows by one at every step,
+// so the rows are distinct (at most G_eff + B - 1 of them) and those of
+// sequence b are consecutive.  One work-group of 1024 threads computes the
+// prefix sums of the lengths and writes:
 //   hdr[0] = N, hdr[1] = G_eff;
 //   wg_start[g] = (sequence, offset) of position g N / G_eff;
 //   seq_rows[b] = (first partial row, number of rows) of sequence b (0 rows
@@ -167,11 +174,11 @@ __global__ __launch_bounds__(kSchedThreads) void wide_schedule_kernel(const int3
     const int64_t P = carry_s + block_scan(L, tot);  // tokens before sequence b
     if (b < B) {
       if (L > 0) {
-        // work-group of position p: the largest g with g N / G_eff <= p
+        // range of position p: the largest g with g N / G_eff <= p
         const int g_first = static_cast<int>(((P + 1) * Ge - 1) / N);
         const int g_last = static_cast<int>(((P + L) * Ge - 1) / N);
         seq_rows[b] = make_int2(g_first + b, g_last - g_first + 1);
-        // work-groups whose first position lies in sequence b
+        // ranges whose first position lies in sequence b
         for (int g = static_cast<int>((P * Ge + N - 1) / N); g <= g_last; ++g)
           wg_start[g] = make_int2(b, static_cast<int>(static_cast<int64_t>(g) * N / Ge - P));
       } else {
@@ -184,15 +191,24 @@ __global__ __launch_bounds__(kSchedThreads) void wide_schedule_kernel(const int3
   }
 }
 
+// Work-group id -> (token range, head block): with `groups` head blocks and
+// G ranges (G a multiple of 8), block ids 8 apart share an XCD, so the head
+// blocks of range g are block ids 8 (groups (g / 8) + hb) + g % 8.
+__device__ __forceinline__ void wide_block(int bid, int groups, int& range, int& hb) {
+  const int xcd = bid & 7, j = bid >> 3;
+  hb = j % groups;
+  range = (j / groups) * 8 + xcd;
+}
+
 __global__ __launch_bounds__(WideCfg::NT, 1) void split_wide_kernel(SplitArgs a) {
   using C = WideCfg;
-  constexpr int DC = C::DC, DQ = C::DQ, NS = C::NS, LROW = C::LROW;
+  constexpr int DC = C::DC, DQ = C::DQ, LROW = C::LROW;
   __shared__ __attribute__((aligned(16))) unsigned char lds[C::LDS_BYTES];
-  int2* list = reinterpret_cast<int2*>(lds + C::LIST);
+  const int2* list = reinterpret_cast<const int2*>(lds + C::LIST);
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds));
 
-  const int hb128 = blockIdx.x % a.groups;
-  const int wg = blockIdx.x / a.groups;
+  int wg, hblk;
+  wide_block(blockIdx.x, a.groups, wg, hblk);
   const int64_t N = a.sched_hdr[0];
   const int Ge = static_cast<int>(a.sched_hdr[1]);
   if (wg >= Ge) return;  // uniform over the work-group
@@ -201,104 +217,68 @@ __global__ __launch_bounds__(WideCfg::NT, 1) void split_wide_kernel(SplitArgs a)
 
   const int tid = threadIdx.x, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int hg = w >> 1, dh = w & 1;
-  const int head0 = hb128 * C::HEADS + hg * 32;  // first head of this wave's head group
-  const int chunk = a.split;                     // list capacity per rebuild (<= kMaxSplitTokensDevice)
+  const int head0 = hblk * C::HEADS + 16 * w;  // first head of this wave
 
   const uint16_t* __restrict__ cache = static_cast<const uint16_t*>(a.cache);
   const uint16_t* __restrict__ gate = static_cast<const uint16_t*>(a.gate);
-  // RoPE keys of tokens 2w and 2w + 1: lane l < 16 fills 16-byte position
-  // l % 8 of token 2w + l / 8 with piece (l % 8) ^ (token % 8), one DMA per
-  // token (lanes 0-7, then lanes 8-15)
-  const uint32_t rope_off = 2 * DC + 16 * ((lane & 7) ^ ((2 * w + ((lane >> 3) & 1)) & 7));
-  // latent / gate DMA of token 2w + k: lane l fetches logical piece l ^ lat_swz(2w + k)
-  const uint32_t lane16s[2] = {static_cast<uint32_t>(16 * (lane ^ lat_swz(2 * w))),
-                               static_cast<uint32_t>(16 * (lane ^ lat_swz(2 * w + 1)))};
-  // Loop-invariant per-lane byte offsets inside a slot.
-  const int off_gl = C::LAT + 2 * w * LROW + 16 * lane;       // gating: latent piece of token 2w
-  const int off_gg = C::GATE + 2 * w * DC * 2 + 16 * lane;    // gating: gate piece of token 2w
-  // values: lane r16 of 16-lane group R reads 4 dims (8 bytes) of token
-  // 8 (R / 2) + 4 j + r16 / 4 and receives dim 16 (R % 2) + r16 of tokens
-  // 8 (R / 2) + 4 j .. + 3; logical piece 32 dh + 4 db + tr_s of that row
-  const int tr_row0 = 8 * (lane >> 5) + (r16 >> 2);
-  const int tr_s = 2 * ((lane >> 4) & 1) + ((r16 & 3) >> 1);
-  const int tr_f[2] = {lat_swz(tr_row0), lat_swz(tr_row0 + 4)};
-  const int off_tr = C::LAT + tr_row0 * LROW + 512 * dh + 8 * (r16 & 1);
-  // scores: lane (token r16, g) reads logical piece 32 dh + 4 c + g
+  // latent / gate DMA of slot row 4w + k: lane l fetches logical piece l ^ lat_swz(4w + k)
+  uint32_t dma_off[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) dma_off[k] = static_cast<uint32_t>(16 * (lane ^ lat_swz(4 * w + k)));
+  // RoPE DMA (lanes 0..31): lane l fills 16-byte position l % 8 of slot row
+  // 4w + l / 8 with logical piece (l % 8) ^ (row % 8)
+  const int rope_row = 4 * w + ((lane >> 3) & 3);
+  const uint32_t rope_src = static_cast<uint32_t>(2 * DC + 16 * ((lane & 7) ^ (rope_row & 7)));
+  // gating: lane l takes physical piece l of this wave's rows
+  const int off_gate = (4 * w) * LROW + 16 * lane;
+  // scores: lane (token r16, group g) reads logical piece 4 c + g of slot row r16
   const int sa_x = g ^ lat_swz(r16);
-  const int off_sa = C::LAT + r16 * LROW + 512 * dh + 16 * (sa_x & 3);
-  const int off_sr = C::ROPE + r16 * 128 + 16 * ((4 * dh + g) ^ (r16 & 7));    // scores: RoPE A operand
-  f32x4_t* xbuf = reinterpret_cast<f32x4_t*>(lds + C::XBUF);
-  int* flags = reinterpret_cast<int*>(lds + C::FLAGS);
-  if (lane == 0) flags[w] = 0;  // ordered before any poll by the first list barrier
-  int exchanges = 0;            // this wave's published exchanges (the same count in every wave)
+  const int off_sa = r16 * LROW + 16 * (sa_x & 3);                               // + 64 (c ^ (sa_x >> 2))
+  const int off_sr = C::ROPE + r16 * 128 + 16 * ((4 * 0 + g) ^ (r16 & 7));        // RoPE chunk 0
+  const int off_sr1 = C::ROPE + r16 * 128 + 16 * ((4 * 1 + g) ^ (r16 & 7));       // RoPE chunk 1
+  // values: lane r16 of group g reads dims 16 db + 4 (r16 % 4) .. + 3 of slot row
+  // 4g + r16 / 4 (logical piece 2 db + (r16 % 4) / 2, half r16 % 2)
+  const int tr_row = 4 * g + (r16 >> 2);
+  const int tr_f = lat_swz(tr_row);
+  const int tr_s = ((r16 & 3) >> 1) ^ (tr_f & 1);
+  const int off_tr = tr_row * LROW + 16 * tr_s + 8 * (r16 & 1);                    // + 32 (db ^ (tr_f >> 1))
+  const int tr_fh = tr_f >> 1;
 
-  bf16x8_t qb[2][8];  // B operand: head 16 hb + r16, dims 8g .. 8g + 7 of latent chunk c
-  bf16x8_t* qrope = reinterpret_cast<bf16x8_t*>(lds + C::QROPE) + w * 2 * 64 + lane;  // RoPE chunk, [hb * 64]
-  f32x16_t o[8];      // O^T[dim 256 dh + 32 db + row][head lane % 32]
-  float m_run[2], l_run[2];  // head 16 hb + r16 (log2 domain); l: this lane's 4 tokens of each tile
-  bf16x8_t pb;  // B operand of the value product: head lane % 32, tokens 8 (lane / 32) .. + 7
+  bf16x8_t qh[16], ql[16];  // B operands: head r16, dims 8g .. 8g + 7 of each 32-dim chunk
+  bf16x8_t* qrope = reinterpret_cast<bf16x8_t*>(lds + C::QROPE) + w * 2 * 64 + lane;  // RoPE chunks c: [64 c]
+  f32x4_t o[32];                   // O^T[dim 16 db + 4g + i][head r16]
+  float m_run, l_run;              // head r16 (log2 domain); l: this lane's tokens
 
-  // gate this wave's 2 tokens of the tile at slot byte offset sbase (in place)
-  auto gate_tile = [&](int sbase) {
-#pragma unroll
-    for (int k = 0; k < 2; ++k) {
-      u32x4_t* lp = reinterpret_cast<u32x4_t*>(lds + sbase + off_gl + k * LROW);
-      const u32x4_t gv = *reinterpret_cast<const u32x4_t*>(lds + sbase + off_gg + k * DC * 2);
-      *lp = gate_chunk(*lp, gv);
-    }
-  };
-  // O^T += C~^T P^T over the 16 tokens of the tile at slot byte offset sbase
-  auto values = [&](int sbase) {
-    const unsigned char* tp = lds + sbase + off_tr;
-#pragma unroll
-    for (int db = 0; db < 8; ++db) {
-      // physical piece (4 db + tr_s) ^ f = 4 (db ^ (f >> 2)) + (tr_s ^ (f & 3))
-      const int p0 = 4 * (db ^ (tr_f[0] >> 2)) + (tr_s ^ (tr_f[0] & 3));
-      const int p1 = 4 * (db ^ (tr_f[1] >> 2)) + (tr_s ^ (tr_f[1] & 3));
-      const s16x4_t a0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-          (__attribute__((address_space(3))) s16x4_t*)(tp + 16 * p0));
-      const s16x4_t a1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-          (__attribute__((address_space(3))) s16x4_t*)(tp + 4 * LROW + 16 * p1));
-      const bf16x8_t av = __builtin_bit_cast(
-          bf16x8_t, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
-      o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb, o[db], 0, 0, 0);
-    }
-  };
-
-  while (remaining > 0 && b < a.B) {  // one segment: this work-group's part of sequence b
+  while (remaining > 0 && b < a.B) {  // one segment: this range's part of sequence b
     const int L = clamp_len(a.seq_lens[b], a.cap);
     const int take = static_cast<int>(min(static_cast<int64_t>(L - off), remaining));
     if (take > 0) {
 #pragma unroll
-      for (int db = 0; db < 8; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
-#pragma unroll
-      for (int hb = 0; hb < 2; ++hb) {
-        m_run[hb] = -INFINITY;
-        l_run[hb] = 0.f;
-      }
-      // query of this lane for sequence b (bf16, as the absorption wrote it)
+      for (int db = 0; db < 32; ++db) o[db] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      m_run = -INFINITY;
+      l_run = 0.f;
+      // query of this lane's head for sequence b, as the absorption wrote it:
+      // [q hi | q^R | q lo] in bf16
       {
-        const uint16_t* q16 = reinterpret_cast<const uint16_t*>(a.qfull);
+        const uint16_t* qrow = reinterpret_cast<const uint16_t*>(a.qfull) +
+                               (static_cast<int64_t>(b) * a.H + head0 + r16) * (DC + DQ) + 8 * g;
 #pragma unroll
-        for (int hb = 0; hb < 2; ++hb) {
-          const uint16_t* qrow = q16 + (static_cast<int64_t>(b) * a.H + head0 + hb * 16 + r16) * DQ;
-#pragma unroll
-          for (int c = 0; c < 8; ++c) qb[hb][c] = *reinterpret_cast<const bf16x8_t*>(qrow + 256 * dh + 32 * c + 8 * g);
-          qrope[hb * 64] = *reinterpret_cast<const bf16x8_t*>(qrow + DC + 32 * dh + 8 * g);  // this wave's LDS region
+        for (int c = 0; c < 16; ++c) {
+          qh[c] = *reinterpret_cast<const bf16x8_t*>(qrow + 32 * c);
+          ql[c] = *reinterpret_cast<const bf16x8_t*>(qrow + DQ + 32 * c);
         }
+#pragma unroll
+        for (int c = 0; c < 2; ++c) qrope[64 * c] = *reinterpret_cast<const bf16x8_t*>(qrow + DC + 32 * c);  // own region
       }
-      for (int c0 = 0; c0 < take; c0 += chunk) {
+      for (int c0 = 0; c0 < take; c0 += C::LISTCAP) {
         const int t0 = off + c0;
-        const int n = min(chunk, take - c0);
-        const int ntiles = (n + 15) / 16;
-        // ---- token list: (slot, id) of positions t0 .. t0 + 16 ntiles - 1 (past
+        const int n = min(C::LISTCAP, take - c0);
+        const int npairs = (n + 31) / 32;
+        // ---- token list: (slot, id) of positions t0 .. t0 + 32 npairs - 1 (past
         // the segment the last token repeats; masked) ----
         {
-          constexpr int PER = kMaxSplitTokensDevice / C::NT;
-          const int npad = ntiles * 16;
+          constexpr int PER = C::LISTCAP / C::NT;
+          const int npad = npairs * 32;
           const int nper = (npad + C::NT - 1) / C::NT;  // uniform
           int pp[PER], psl[PER], pid[PER];
 #pragma unroll
@@ -307,171 +287,176 @@ __global__ __launch_bounds__(WideCfg::NT, 1) void split_wide_kernel(SplitArgs a)
 #pragma unroll
           for (int e = 0; e < PER; ++e)
             if (e < nper) pid[e] = a.ids[psl[e]];
+          int2* lw = reinterpret_cast<int2*>(lds + C::LIST);
 #pragma unroll
           for (int e = 0; e < PER; ++e) {
             const int j = tid + e * C::NT;
-            if (e < nper && j < npad) list[j] = make_int2(psl[e], clamp_id(pid[e], a.V));
+            if (e < nper && j < npad) lw[j] = make_int2(psl[e], clamp_id(pid[e], a.V));
           }
         }
-        __syncthreads();  // the list is complete; every wave is done with the previous chunk's tiles
+        __syncthreads();  // the list is complete; every wave is done with the previous chunk's slots
 
-        // DMA of tile i given its list entries for this wave's tokens 2w, 2w + 1
-        // ((slot, id) each; one 16-byte LDS read per tile)
-        auto entries = [&](int i) { return reinterpret_cast<const int4*>(list)[i * 8 + w]; };
-        auto issue_tile = [&](int i, int4 e) {
-          const uint32_t slot = lds0 + (i % NS) * C::SLOT;
-          const int sl[2] = {__builtin_amdgcn_readfirstlane(e.x), __builtin_amdgcn_readfirstlane(e.z)};
-          const int id[2] = {__builtin_amdgcn_readfirstlane(e.y), __builtin_amdgcn_readfirstlane(e.w)};
+        // DMAs of slot s (list tokens 16 s ..) for this wave's rows 4w .. 4w + 3
+        auto issue_slot = [&](int s) {
+          const uint32_t sb = lds0 + (s % C::NS) * C::SLOT;
+          const int4 e01 = reinterpret_cast<const int4*>(list)[(16 * s + 4 * w) / 2];
+          const int4 e23 = reinterpret_cast<const int4*>(list)[(16 * s + 4 * w) / 2 + 1];
+          const int sl[4] = {__builtin_amdgcn_readfirstlane(e01.x), __builtin_amdgcn_readfirstlane(e01.z),
+                             __builtin_amdgcn_readfirstlane(e23.x), __builtin_amdgcn_readfirstlane(e23.z)};
+          const int id[4] = {__builtin_amdgcn_readfirstlane(e01.y), __builtin_amdgcn_readfirstlane(e01.w),
+                             __builtin_amdgcn_readfirstlane(e23.y), __builtin_amdgcn_readfirstlane(e23.w)};
 #pragma unroll
-          for (int k = 0; k < 2; ++k) {
-            lds_dma16(cache + static_cast<int64_t>(sl[k]) * DQ, lane16s[k], slot + C::LAT + (2 * w + k) * LROW);
-            lds_dma16(gate + static_cast<int64_t>(id[k]) * DC, lane16s[k], slot + C::GATE + (2 * w + k) * DC * 2);
+          for (int k = 0; k < 4; ++k) {
+            lds_dma16(cache + static_cast<int64_t>(sl[k]) * DQ, dma_off[k], sb + C::HI + (4 * w + k) * LROW);
+            lds_dma16(gate + static_cast<int64_t>(id[k]) * DC, dma_off[k], sb + C::LO + (4 * w + k) * LROW);
+          }
+          // RoPE keys of the 4 rows: lane l < 32 reads row 4w + l / 8 (its own list entry)
+          const int slk = list[16 * s + rope_row].x;
+          const uint64_t addr = reinterpret_cast<uint64_t>(cache + static_cast<int64_t>(slk) * DQ) + rope_src;
+          if (lane < 32) lds_dma16_addr(addr, sb + C::ROPE + 4 * w * 128);
+        };
+        auto issue_pair = [&](int p) {
+          issue_slot(2 * p);
+          issue_slot(2 * p + 1);
+        };
+        // gate this wave's rows of slot s in place: HI <- bf16(c g), LO <- c g - HI
+        // (one row's pieces are read while the previous row is gated)
+        auto gate_slot = [&](int s) {
+          unsigned char* sp = lds + (s % C::NS) * C::SLOT + off_gate;
+          u32x4_t lat[2], gat[2];
+          lat[0] = *reinterpret_cast<const u32x4_t*>(sp + C::HI);
+          gat[0] = *reinterpret_cast<const u32x4_t*>(sp + C::LO);
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            if (k + 1 < 4) {
+              lat[(k + 1) & 1] = *reinterpret_cast<const u32x4_t*>(sp + C::HI + (k + 1) * LROW);
+              gat[(k + 1) & 1] = *reinterpret_cast<const u32x4_t*>(sp + C::LO + (k + 1) * LROW);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            u32x4_t hi, lo;
+            gate_chunk_hilo(lat[k & 1], gat[k & 1], hi, lo);
+            *reinterpret_cast<u32x4_t*>(sp + C::HI + k * LROW) = hi;
+            *reinterpret_cast<u32x4_t*>(sp + C::LO + k * LROW) = lo;
+            __builtin_amdgcn_sched_barrier(0);
+          }
+        };
+        // S^T[token 4g + q][head r16] of slot s (unscaled), one accumulator
+        // chain.  The operands of chunk c + 1 are read while chunk c's products
+        // run, and nothing is hoisted further (every chunk's reads would
+        // otherwise be live at once).
+        auto scores = [&](int s) {
+          const unsigned char* sp = lds + (s % C::NS) * C::SLOT;
+          f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+          bf16x8_t ah[2], al[2];
+          auto rd = [&](int c) {
+            const int pc = off_sa + 64 * (c ^ (sa_x >> 2));
+            ah[c & 1] = *reinterpret_cast<const bf16x8_t*>(sp + C::HI + pc);
+            al[c & 1] = *reinterpret_cast<const bf16x8_t*>(sp + C::LO + pc);
+          };
+          rd(0);
+#pragma unroll
+          for (int c = 0; c < 16; ++c) {
+            if (c + 1 < 16) rd(c + 1);
+            __builtin_amdgcn_sched_barrier(0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[c & 1], qh[c], acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[c & 1], ql[c], acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[c & 1], qh[c], acc, 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
           }
 #pragma unroll
-          for (int k = 0; k < 2; ++k)
-            if ((lane >> 3) == k) lds_dma16(cache + static_cast<int64_t>(sl[k]) * DQ, rope_off, slot + C::ROPE + 2 * w * 128);
+          for (int c = 0; c < 2; ++c) {
+            const bf16x8_t ar = *reinterpret_cast<const bf16x8_t*>(sp + (c ? off_sr1 : off_sr));
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ar, qrope[64 * c], acc, 0, 0, 0);
+          }
+          return acc;
         };
 
-        issue_tile(0, entries(0));
-        if (ntiles > 1) issue_tile(1, entries(1));
-        int4 next_e = entries(min(2, ntiles - 1));  // list entries of tile t + 2
-        // this wave's tokens of tile 0 (that of tile 1 may be in flight)
-        if (ntiles > 1) wait_vmcnt<C::DMA_PER_TILE>();
-        else wait_vmcnt<0>();
-        gate_tile(0);
-
-        // Tile t: scores, exchange, softmax and values of tile t, with the
-        // gating of tile t + 1 overlapping the softmax.
-        for (int t = 0; t < ntiles; ++t) {
-          const int sbase = __builtin_amdgcn_readfirstlane((t % NS) * C::SLOT);
-          lds_barrier();  // tile t gated and visible; every wave is done with tile t - 1
-          if (t + 2 < ntiles) issue_tile(t + 2, next_e);  // into the slot of tile t - 1
-          next_e = entries(min(t + 3, ntiles - 1));         // read now, used next iteration
+        issue_pair(0);
+        if (npairs > 1) issue_pair(1);
+        for (int p = 0; p < npairs; ++p) {
+          // this wave's DMAs of pair p have landed (those of pair p + 1 may be in flight)
+          if (p == 0 && npairs > 1) wait_vmcnt<C::DMA_PER_PAIR>();
+          else wait_vmcnt<0>();
+          gate_slot(2 * p);
+          gate_slot(2 * p + 1);
+          lds_barrier();  // pair p gated and visible; every wave is done with pair p - 1
+          if (p >= 1 && p + 1 < npairs) issue_pair(p + 1);  // into the slots of pair p - 1
           __builtin_amdgcn_sched_barrier(0);
 
-          // partial scores over this wave's dims
-          // two accumulators per head block (even and odd chunks): four
-          // independent MFMA chains instead of two
-          f32x4_t acc[2], acc2[2];
+          const f32x4_t sa = scores(2 * p);
+          const f32x4_t sb = scores(2 * p + 1);
+          float x[8];
 #pragma unroll
-          for (int hb = 0; hb < 2; ++hb) acc[hb] = acc2[hb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int c = 0; c < 9; ++c) {
-            // physical piece (4 c + g) ^ f = 4 (c ^ (sa_x >> 2)) + (sa_x & 3)
-            const unsigned char* ap = c < 8 ? lds + sbase + off_sa + 64 * (c ^ (sa_x >> 2)) : lds + sbase + off_sr;
-            const bf16x8_t av = *reinterpret_cast<const bf16x8_t*>(ap);
-#pragma unroll
-            for (int hb = 0; hb < 2; ++hb) {
-              f32x4_t& ac = (c & 1) ? acc2[hb] : acc[hb];
-              ac = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, c < 8 ? qb[hb][c] : qrope[hb * 64], ac, 0, 0, 0);
-            }
+          for (int q = 0; q < 4; ++q) {
+            x[q] = sa[q] * a.scale_log2;
+            x[4 + q] = sb[q] * a.scale_log2;
           }
-#pragma unroll
-          for (int hb = 0; hb < 2; ++hb) acc[hb] += acc2[hb];
-#pragma unroll
-          for (int hb = 0; hb < 2; ++hb) xbuf[(w * 2 + hb) * 64 + lane] = acc[hb];
-          // Publish the partial scores to the partner wave (w ^ 1) and wait
-          // for its own: LDS writes of a wave complete in order, and the flag
-          // is written after the scores are.
-          ++exchanges;
-          asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-          if (lane == 0) __hip_atomic_store(flags + w, exchanges, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-          for (int spin = 0; spin < C::SPIN_LIMIT; ++spin) {
-            const int seen = __builtin_amdgcn_readfirstlane(
-                __hip_atomic_load(flags + (w ^ 1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP));
-            if (seen >= exchanges) break;
-            __builtin_amdgcn_s_sleep(1);
-          }
-          asm volatile("" ::: "memory");
-          __builtin_amdgcn_sched_barrier(0);
-          if (t + 1 < ntiles) {
-            // this wave's tokens of tile t + 1 (that of tile t + 2 may be in flight)
-            if (t + 2 < ntiles) wait_vmcnt<C::DMA_PER_TILE>();
-            else wait_vmcnt<0>();
-            gate_tile(__builtin_amdgcn_readfirstlane(((t + 1) % NS) * C::SLOT));
-          }
-#pragma unroll
-          for (int hb = 0; hb < 2; ++hb) {
-            const f32x4_t other = xbuf[((w ^ 1) * 2 + hb) * 64 + lane];
-            // the same order in both waves of the pair: dim half 0 + dim half 1
-            acc[hb] = dh == 0 ? acc[hb] + other : other + acc[hb];
-#pragma unroll
-            for (int q = 0; q < 4; ++q) acc[hb][q] *= a.scale_log2;
-          }
-          const int nt = n - t * 16;  // valid tokens of the tile (1..16)
-          if (nt < 16) {
-#pragma unroll
-            for (int hb = 0; hb < 2; ++hb)
-#pragma unroll
-              for (int q = 0; q < 4; ++q)
-                if (4 * g + q >= nt) acc[hb][q] = -INFINITY;
-          }
-          // online softmax per head (lane: head 16 hb + r16, tokens 4g .. 4g + 3)
-          float alpha[2];
-          bool any_grow = false;
-#pragma unroll
-          for (int hb = 0; hb < 2; ++hb) {
-            const float mt = max_over_row_groups(fmaxf(fmaxf(acc[hb][0], acc[hb][1]), fmaxf(acc[hb][2], acc[hb][3])));
-            const float m_new = fmaxf(m_run[hb], mt);  // finite: the tile has a valid token
-            const bool grow = m_new > m_run[hb] + kLazyRescale;
-            alpha[hb] = grow ? __builtin_amdgcn_exp2f(m_run[hb] - m_new) : 1.0f;
-            m_run[hb] = grow ? m_new : m_run[hb];
-            l_run[hb] *= alpha[hb];
-            any_grow |= grow;
-          }
-          if (__builtin_amdgcn_ballot_w64(any_grow)) {
-            // accumulator lane holds head lane % 32 = 16 ((lane / 16) % 2) + r16
-            const float al = (lane >> 4) & 1 ? alpha[1] : alpha[0];
-#pragma unroll
-            for (int db = 0; db < 8; ++db) o[db] *= al;
-          }
-          uint32_t pk[2][2];
-#pragma unroll
-          for (int hb = 0; hb < 2; ++hb) {
-            float p[4];
+          const int nt = n - 32 * p;  // valid tokens of the pair (1..32)
+          if (nt < 32) {
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-              p[q] = __builtin_amdgcn_exp2f(acc[hb][q] - m_run[hb]);
-              l_run[hb] += p[q];
+              if (4 * g + q >= nt) x[q] = -INFINITY;
+              if (16 + 4 * g + q >= nt) x[4 + q] = -INFINITY;
             }
-            pk[hb][0] = pack_bf16x2(p[0], p[1]);
-            pk[hb][1] = pack_bf16x2(p[2], p[3]);
           }
-          // rows (16-lane groups) 2k and 2k + 1 of head blocks 0 and 1 ->
-          // lane L: head L % 32, tokens 8 (L / 32) .. + 7
-          {
-            const auto s0 = __builtin_amdgcn_permlane16_swap(pk[0][0], pk[1][0], false, false);
-            const auto s1 = __builtin_amdgcn_permlane16_swap(pk[0][1], pk[1][1], false, false);
-            pb = __builtin_bit_cast(bf16x8_t, u32x4_t{s0[0], s1[0], s0[1], s1[1]});
+          // online softmax of head r16 over the pair's 32 tokens
+          float mt = x[0];
+#pragma unroll
+          for (int q = 1; q < 8; ++q) mt = fmaxf(mt, x[q]);
+          mt = max_over_row_groups(mt);
+          const float m_new = fmaxf(m_run, mt);  // finite: the pair has a valid token
+          const bool grow = m_new > m_run + kLazyRescale;  // false while both are -inf
+          if (__builtin_amdgcn_ballot_w64(grow)) {
+            const float alpha = grow ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.0f;  // exp2(-inf) = 0
+            m_run = grow ? m_new : m_run;
+            l_run *= alpha;
+#pragma unroll
+            for (int db = 0; db < 32; ++db) o[db] *= alpha;
           }
-          values(sbase);
+          float pr[8];
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            pr[q] = __builtin_amdgcn_exp2f(x[q] - m_run);  // masked: exp2(-inf) = 0
+            l_run += pr[q];
+          }
+          // B operand: k = 8g + i <-> slot 2p token 4g + i (i < 4), slot 2p + 1 token 4g + i - 4
+          const bf16x8_t pb = __builtin_bit_cast(
+              bf16x8_t, u32x4_t{pack_bf16x2(pr[0], pr[1]), pack_bf16x2(pr[2], pr[3]), pack_bf16x2(pr[4], pr[5]),
+                                pack_bf16x2(pr[6], pr[7])});
+          // O^T += C~^T P^T, A operand: dim 16 db + r16 of the same 8 tokens
+          const unsigned char* sp0 = lds + ((2 * p) % C::NS) * C::SLOT + C::HI + off_tr;
+          const unsigned char* sp1 = lds + ((2 * p + 1) % C::NS) * C::SLOT + C::HI + off_tr;
+          // (the operands of block db + 1 are read while block db's product runs)
+          s16x4_t v0[2], v1[2];
+          auto rdv = [&](int db) {
+            const int pd = 32 * (db ^ tr_fh);
+            v0[db & 1] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t*)(sp0 + pd));
+            v1[db & 1] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t*)(sp1 + pd));
+          };
+          rdv(0);
+#pragma unroll
+          for (int db = 0; db < 32; ++db) {
+            if (db + 1 < 32) rdv(db + 1);
+            __builtin_amdgcn_sched_barrier(0);
+            const bf16x8_t av =
+                __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(v0[db & 1], v1[db & 1], 0, 1, 2, 3, 4, 5, 6, 7));
+            o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, pb, o[db], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+          }
           __builtin_amdgcn_sched_barrier(0);
         }
-
       }
-      // ---- partial result of this segment: this wave's heads and dims ----
+      // ---- partial result of this segment: this wave's 16 heads ----
       const int64_t pbase = (static_cast<int64_t>(wg) + b) * a.H + head0;
-      if (dh == 0) {
-#pragma unroll
-        for (int hb = 0; hb < 2; ++hb) {
-          const float l = sum_over_row_groups(l_run[hb]);
-          if (g == 0) {
-            __builtin_nontemporal_store(m_run[hb], a.part_ml + (pbase + 16 * hb + r16) * 2 + 0);
-            __builtin_nontemporal_store(l, a.part_ml + (pbase + 16 * hb + r16) * 2 + 1);
-          }
-        }
+      const float l = sum_over_row_groups(l_run);
+      if (g == 0) {
+        __builtin_nontemporal_store(m_run, a.part_ml + (pbase + r16) * 2 + 0);
+        __builtin_nontemporal_store(l, a.part_ml + (pbase + r16) * 2 + 1);
       }
-      {
-        float* obase = a.part_o + pbase * DC + 256 * dh;  // uniform
-        const uint32_t loff = (lane & 31) * DC + 4 * (lane >> 5);
+      float* obase = a.part_o + (pbase + r16) * DC + 4 * g;
 #pragma unroll
-        for (int db = 0; db < 8; ++db)
-#pragma unroll
-          for (int r4 = 0; r4 < 4; ++r4)
-            __builtin_nontemporal_store(
-                f32x4_t{o[db][4 * r4], o[db][4 * r4 + 1], o[db][4 * r4 + 2], o[db][4 * r4 + 3]},
-                reinterpret_cast<f32x4_t*>(obase + loff + 32 * db + 8 * r4));
-      }
+      for (int db = 0; db < 32; ++db)
+        __builtin_nontemporal_store(o[db], reinterpret_cast<f32x4_t*>(obase + 16 * db));
     }
     remaining -= take > 0 ? take : 0;
     ++b;

@@ -265,11 +265,12 @@ class LiteralGate:
     ln_b: np.ndarray        # [H (d_h + d_v)]
 
 
-def generate_literal_gate(wl: Workload, seed: Optional[int] = None) -> LiteralGate:
-    """Seeded gate rows 1 + 0.1 N(0, 1), LayerNorm weight 1 + 0.1 N(0, 1) and bias 0.1 N(0, 1)."""
+def generate_literal_gate(wl: Workload, seed: Optional[int] = None, center: float = 1.0) -> LiteralGate:
+    """Seeded gate rows center + 0.1 N(0, 1) (center 1 by default), LayerNorm weight
+    1 + 0.1 N(0, 1) and bias 0.1 N(0, 1)."""
     rng = np.random.default_rng(wl.seed + 4000 if seed is None else seed)
     width = wl.heads * (wl.head_dim + wl.v_head_dim)
-    g = np.float32(1.0) + np.float32(0.1) * rng.standard_normal((wl.vocab, width), dtype=np.float32)
+    g = np.float32(center) + np.float32(0.1) * rng.standard_normal((wl.vocab, width), dtype=np.float32)
     lw = np.float32(1.0) + np.float32(0.1) * rng.standard_normal(width, dtype=np.float32)
     lb = np.float32(0.1) * rng.standard_normal(width, dtype=np.float32)
     return LiteralGate(gate_full=_store(g, wl.dtype), ln_w=_store(lw, wl.dtype), ln_b=_store(lb, wl.dtype))

@@ -69,7 +69,7 @@ def test_small_ragged_paged_all_splits(gpu, path, slices, split):
     inp = W.generate(SMALL, seq_lens=np.array([1, 33, 777, 900]))
     say(f"decode small ragged paged path={path} slices={slices} split={split}")
     got = gpu_decode(inp, B.make_plan(path, split, id_slices=slices))
-    assert_close(got, oracle_decode(inp), "bf16", f"path {path} slices {slices} split {split}", scaled=True)
+    assert_close(got, oracle_decode(inp), "bf16", f"path {path} slices {slices} split {split}")
 
 
 @pytest.mark.parametrize("slices", [1, 8])
@@ -85,7 +85,7 @@ def test_id_slices_skewed_and_empty(gpu, slices):
         say(f"decode id slices={slices} {what}")
         got = gpu_decode(inp, B.make_plan(B.PATH_MFMA, 256, id_slices=slices))
         assert np.all(got[4] == 0)
-        assert_close(got, oracle_decode(inp), "bf16", f"slices {slices} {what}", scaled=True)
+        assert_close(got, oracle_decode(inp), "bf16", f"slices {slices} {what}")
 
 
 @pytest.mark.parametrize("paged", [False, True])
@@ -97,7 +97,7 @@ def test_pages_not_multiple_of_four(gpu, paged):
     for slices in (1, 8):
         say(f"decode 6-token pages paged={paged} slices={slices}")
         got = gpu_decode(inp, B.make_plan(B.PATH_MFMA, 32, id_slices=slices))
-        assert_close(got, oracle_decode(inp), "bf16", f"P=6 paged={paged} slices {slices}", scaled=True)
+        assert_close(got, oracle_decode(inp), "bf16", f"P=6 paged={paged} slices {slices}")
 
 
 @pytest.mark.parametrize("path,slices", PATHS)
@@ -110,7 +110,7 @@ def test_edge_lengths(gpu, path, slices):
     got = gpu_decode(inp, B.make_plan(path, 128, id_slices=slices))
     ref = oracle_decode(inp)
     assert np.all(got[0] == 0)
-    assert_close(got, ref, "bf16", "edge lengths", scaled=True)
+    assert_close(got, ref, "bf16", "edge lengths")
 
 
 def test_many_head_groups_and_dc512(gpu):
@@ -118,17 +118,17 @@ def test_many_head_groups_and_dc512(gpu):
     inp = W.generate(wl)
     for path in (B.PATH_VALU, B.PATH_MFMA):
         say(f"decode h128 dc512 ragged paged path={path}")
-        assert_close(gpu_decode(inp, B.make_plan(path, 256)), oracle_decode(inp), "bf16", f"path {path}", scaled=True)
+        assert_close(gpu_decode(inp, B.make_plan(path, 256)), oracle_decode(inp), "bf16", f"path {path}")
 
 
-@pytest.mark.parametrize("split", [32, 2048])
-def test_two_head_blocks_dc512(gpu, split):
-    # 256 heads: the head-split kernel runs two blocks of 128 heads per split
-    wl = W.WORKLOADS[4].replace(name="h256_dc512", heads=256, batch=2, seq_len_range=(40, 300), seed=43)
+@pytest.mark.parametrize("heads,split", [(256, 32), (256, 2048), (64, 256)])
+def test_head_blocks_dc512(gpu, heads, split):
+    # the head-split kernel takes heads in blocks of 64: 256 heads run four
+    # blocks per token range, 64 heads a single one
+    wl = W.WORKLOADS[4].replace(name=f"h{heads}_dc512", heads=heads, batch=2, seq_len_range=(40, 300), seed=43)
     inp = W.generate(wl)
-    say(f"decode h256 dc512 ragged paged split={split}")
-    assert_close(gpu_decode(inp, B.make_plan(B.PATH_MFMA, split)), oracle_decode(inp), "bf16", f"h256 split {split}",
-                 scaled=True)
+    say(f"decode h{heads} dc512 ragged paged split={split}")
+    assert_close(gpu_decode(inp, B.make_plan(B.PATH_MFMA, split)), oracle_decode(inp), "bf16", f"h{heads} split {split}")
 
 
 def test_edge_lengths_dc512(gpu):
@@ -139,7 +139,7 @@ def test_edge_lengths_dc512(gpu):
     say(f"decode dc512 edge lengths {lens.tolist()}")
     got = gpu_decode(inp, B.make_plan(B.PATH_MFMA, 32))
     assert np.all(got[0] == 0)
-    assert_close(got, oracle_decode(inp), "bf16", "dc512 edge lengths", scaled=True)
+    assert_close(got, oracle_decode(inp), "bf16", "dc512 edge lengths")
 
 
 @pytest.mark.parametrize("case", ["mixed", "short", "one_long"])
@@ -159,21 +159,21 @@ def test_balanced_schedule_dc512(gpu, case):
     say(f"decode dc512 balanced schedule {case}: {int(lens.sum())} tokens, {len(lens)} sequences")
     got = gpu_decode(inp)
     assert np.all(got[lens == 0] == 0)
-    assert_close(got, oracle_decode(inp), "bf16", f"balanced {case}", scaled=True)
+    assert_close(got, oracle_decode(inp), "bf16", f"balanced {case}")
 
 
 def test_peaked_logits_dc512(gpu):
-    # query x 3: running maxima grow by more than 2^8 between the tiles of a
-    # work-group's range (about 45 tokens each here), so the 128-head kernel
-    # rescales its accumulators.  (At x 8 the kernel's bf16 query and bf16
-    # gated latent give rel-L2 6.6e-3, above the bar; a CPU emulation of the
-    # same roundings gives the same figure, so that is precision, not a fault.)
+    # query x 8: logits of standard deviation about 8, so the softmax is sharp
+    # and a score error of 2^-9 relative moves the output by more than the bar;
+    # the 128-head kernel must take the query and the gated latent as bf16 hi +
+    # lo.  Running maxima also grow by more than 2^8 between the tiles of a
+    # range, so the kernel rescales its accumulators.
     wl = W.WORKLOADS[4].replace(name="peaked_dc512", batch=4, seq_len_range=(2500, 3500), seed=46)
     inp = W.generate(wl)
-    inp.q[:] = W.f32_to_bf16_bits(W.bf16_bits_to_f32(inp.q) * np.float32(3.0))
-    say("decode dc512 peaked logits (q x 3)")
+    inp.q[:] = W.f32_to_bf16_bits(W.bf16_bits_to_f32(inp.q) * np.float32(8.0))
+    say("decode dc512 peaked logits (q x 8)")
     got = gpu_decode(inp, B.make_plan(B.PATH_MFMA, 256))
-    assert_close(got, oracle_decode(inp), "bf16", "peaked dc512", scaled=True)
+    assert_close(got, oracle_decode(inp), "bf16", "peaked dc512")
 
 
 def test_peaked_logits(gpu):
@@ -182,7 +182,7 @@ def test_peaked_logits(gpu):
     say("decode peaked logits (q x 8)")
     got = gpu_decode(inp, B.make_plan(B.PATH_MFMA, 64))
     ref = oracle_decode(inp)
-    assert_close(got, ref, "bf16", "peaked", scaled=True)
+    assert_close(got, ref, "bf16", "peaked")
 
 
 def test_paged_equals_contiguous_bitwise(gpu):
@@ -229,13 +229,36 @@ def test_split_choice_changes_result_within_tolerance(gpu):
     assert_close(gpu_decode(inp, B.make_plan(B.PATH_VALU, 0)), ref, "bf16", "valu")
 
 
-def test_out_of_range_ids_and_lengths_are_clamped(gpu):
+@pytest.mark.parametrize("path,slices", PATHS)
+def test_out_of_range_ids_and_lengths_are_clamped(gpu, path, slices):
+    # lengths beyond the capacity clamp to the capacity; cached ids below 0 or
+    # at or past V clamp into [0, V): the oracle is fed the clamped values
     inp = W.generate(SMALL.replace(seed=24, paged=False), seq_lens=np.array([10, 20, 30, 40]))
-    lens_over = inp.seq_lens.copy()
-    inp.seq_lens[:] = [10, 20, 30, 10 ** 6]          # beyond capacity -> clamped to capacity
+    V = inp.wl.vocab
     cap = inp.max_pages * inp.wl.page_size
-    say("decode clamped lengths")
-    got = gpu_decode(inp, B.make_plan(B.PATH_MFMA, 64))
+    inp.seq_lens[:] = [10, 20, 30, 10 ** 6]
+    used = np.concatenate([b * cap + np.arange(min(int(L), cap)) for b, L in enumerate(inp.seq_lens)])
+    bad = np.random.default_rng(7).choice(used, size=64, replace=False)
+    inp.token_ids[bad[:32]] = -3
+    inp.token_ids[bad[32:]] = V + 7
+    say(f"decode clamped ids and lengths path={path} slices={slices}")
+    got = gpu_decode(inp, B.make_plan(path, 64, id_slices=slices))
     inp.seq_lens[:] = [10, 20, 30, cap]
-    assert_close(got, oracle_decode(inp), "bf16", "clamped", scaled=True)
-    del lens_over
+    inp.token_ids[:] = np.clip(inp.token_ids, 0, V - 1)
+    assert_close(got, oracle_decode(inp), "bf16", "clamped")
+
+
+def test_out_of_range_ids_dc512(gpu):
+    wl = W.WORKLOADS[4].replace(name="clamp_dc512", batch=3, seq_len_range=(40, 300), seed=47)
+    inp = W.generate(wl)
+    V = wl.vocab
+    P = wl.page_size
+    used = np.concatenate([inp.page_table[b, np.arange(L) // P].astype(np.int64) * P + np.arange(L) % P
+                           for b, L in enumerate(inp.seq_lens)])
+    bad = np.random.default_rng(8).choice(used, size=200, replace=False)
+    inp.token_ids[bad[:100]] = -1
+    inp.token_ids[bad[100:]] = V
+    say("decode dc512 clamped ids")
+    got = gpu_decode(inp)
+    inp.token_ids[:] = np.clip(inp.token_ids, 0, V - 1)
+    assert_close(got, oracle_decode(inp), "bf16", "clamped dc512")
