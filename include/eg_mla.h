@@ -150,11 +150,12 @@ eg_mla_status eg_mla_append(const eg_mla_dims* dims, int32_t n_tokens, int32_t h
  *   out           [B, H, d_v]  in the storage type
  *
  * Arithmetic (bf16 storage, MFMA path): each gated latent is the exact fp32
- * product of two bf16 values rounded once to bf16; scores and the value sum
- * are bf16 x bf16 products accumulated in fp32, with the absorbed query
- * split into bf16 hi + lo (rounded to bf16 for d_c = 512 with 128-head work
- * items) and the probabilities rounded to bf16; the split merge is fp32 and
- * the up-projection takes the merged latent as bf16 hi + lo.  The VALU path
+ * product of two bf16 values, held as bf16 hi + lo (lo the exact remainder);
+ * scores are bf16 x bf16 products accumulated in fp32 with the absorbed query
+ * also split into hi + lo (latent part hi.q_hi + hi.q_lo + lo.q_hi; the RoPE
+ * part exact); the value sum takes the gated latent's hi part and the
+ * probabilities rounded to bf16; the split merge is fp32 and the
+ * up-projection takes the merged latent as bf16 hi + lo.  The VALU path
  * computes in fp32.  The call is asynchronous on `stream`; calls that share a
  * workspace must be ordered (same stream or synchronised).
  * ------------------------------------------------------------------------- */

@@ -181,7 +181,10 @@ extern "C" eg_mla_status eg_mla_prefill_varlen(const eg_mla_dims* dims, int32_t 
   a.T = T;
   a.V = d.vocab_size;
   a.scale_log2 = softmax_scale(d) * 1.4426950408889634f;
-  const size_t lds = 2 * kPfBufBytes;
+  const size_t lds = 2 * kPfBufBytes;  // 80 KB: above the 64 KB default, so it is requested explicitly
+  if (hipFuncSetAttribute(reinterpret_cast<const void*>(prefill_attn_mfma_kernel),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)) != hipSuccess)
+    return EG_MLA_ERR_HIP;
   hipLaunchKernelGGL(prefill_attn_mfma_kernel, dim3((T + kPfTokens - 1) / kPfTokens), dim3(kPfThreads), lds, stream,
                      a);
   hipLaunchKernelGGL(prefill_uv_kernel, dim3(side_wgs, d.num_heads), dim3(256), 0, stream,

@@ -26,15 +26,19 @@
 // first (last in the stream first).
 //  * Tile: 256 threads each load four 16-byte latent pieces with the matching
 //    gate pieces and two RoPE pieces of the next tile while the current one is
-//    computed; the gated latent (exact fp32 products, one bf16 rounding) is
-//    written to the other of two LDS buffers.  Rows of 256 bytes hold the
+//    computed; the gated latent (exact fp32 products) is written to the other
+//    of two LDS buffers as bf16 hi and the bf16 remainder lo (hi + lo is the
+//    product exactly; lo rows follow the hi rows).  Rows of 256 bytes hold the
 //    16-byte pieces XOR-swizzled by f(key) = 4 (key % 4) + (key / 4) % 4, RoPE
 //    rows of 128 bytes by (key / 2) % 8: the 16 lanes of a 16-byte read cycle
 //    and the 32 lanes of a transposed 8-byte read cycle each hit distinct banks.
 //  * Scores: wave w holds rows (tokens 2w, 2w + 1) x 16 heads = 32 rows, its
 //    query in registers as the B operand of v_mfma_f32_32x32x16_bf16 (lane:
-//    row lane % 32, dims 8 (lane / 32) + 16 c).  S^T[key][row] comes from 12
-//    products per 32 keys with the tile rows as the A operand.
+//    row lane % 32, dims 8 (lane / 32) + 16 c).  S^T[key][row] comes from 20
+//    products per 32 keys with the tile rows as the A operand: the latent part
+//    as hi and lo (so a score carries only the query's bf16 rounding, which is
+//    what lets rows dominated by a few keys meet the bound), the RoPE part
+//    once.
 //  * Online softmax per row in the log2 domain, lazy rescale (as the decode).
 //    A lane holds 16 of each 32 keys' scores of its row; the other 16 are in
 //    lane ^ 32 (one permlane32 swap for the maximum; the sums are combined
@@ -57,7 +61,9 @@ constexpr int kPfDC = 128, kPfDR = 64, kPfDQ = kPfDC + kPfDR;
 constexpr int kPfLatRow = 2 * kPfDC;    // bytes per key row of the gated latent
 constexpr int kPfRopeRow = 2 * kPfDR;   // bytes per key row of the RoPE key
 constexpr int kPfLatBytes = kPfKeys * kPfLatRow;
-constexpr int kPfBufBytes = kPfLatBytes + kPfKeys * kPfRopeRow;  // one tile buffer (24 KB)
+constexpr int kPfRopeOff = 2 * kPfLatBytes;                       // after the hi and lo rows
+constexpr int kPfBufBytes = kPfRopeOff + kPfKeys * kPfRopeRow;    // one tile buffer (40 KB; two per work-group)
+static_assert(2 * 2 * kPfBufBytes <= 160 * 1024, "two work-groups of two tile buffers per compute unit");
 constexpr int kPfUvTokens = 128;  // absorption and up-projection: tokens per chunk (4 waves x 32)
 constexpr int kPfSideChunks = 4;  // chunks per work-group: the head's weights are staged once for them
 
@@ -160,19 +166,22 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_attn_mfma_kernel(Prefil
 #pragma unroll
     for (int j = 0; j < NLJ; ++j) {
       const int key = kl + 16 * j;
-      *reinterpret_cast<u32x4_t*>(base + key * kPfLatRow + 16 * (pl ^ pf_lat_swz(key))) = gate_chunk(nl[j], ng[j]);
+      u32x4_t hi, lo;
+      gate_chunk_hilo(nl[j], ng[j], hi, lo);
+      *reinterpret_cast<u32x4_t*>(base + key * kPfLatRow + 16 * (pl ^ pf_lat_swz(key))) = hi;
+      *reinterpret_cast<u32x4_t*>(base + kPfLatBytes + key * kPfLatRow + 16 * (pl ^ pf_lat_swz(key))) = lo;
     }
 #pragma unroll
     for (int j = 0; j < NRJ; ++j) {
       const int key = kr + 32 * j;
-      *reinterpret_cast<u32x4_t*>(base + kPfLatBytes + key * kPfRopeRow + 16 * (pr ^ pf_rope_swz(key))) = nr[j];
+      *reinterpret_cast<u32x4_t*>(base + kPfRopeOff + key * kPfRopeRow + 16 * (pr ^ pf_rope_swz(key))) = nr[j];
     }
   };
 
   // per-lane LDS offsets (bytes within a tile buffer)
   const int off_sl = r32 * kPfLatRow;               // score A: key row 32 kb + r32 (+ 32 kb rows)
   const int swz_sl = pf_lat_swz(r32);
-  const int off_sr = kPfLatBytes + r32 * kPfRopeRow;
+  const int off_sr = kPfRopeOff + r32 * kPfRopeRow;
   const int swz_sr = pf_rope_swz(r32);
   // value A (transposed reads): rows 16 m + 4 h + r16 / 4 (+ 8), byte 8 (r16 % 2) of the piece
   const int off_v = (4 * h + (r16 >> 2)) * kPfLatRow + 8 * (r16 & 1);
@@ -209,9 +218,11 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_attn_mfma_kernel(Prefil
     for (int c = 0; c < kPfDC / 16; ++c)
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        const bf16x8_t av = *reinterpret_cast<const bf16x8_t*>(tb + off_sl + 32 * kb * kPfLatRow +
-                                                                16 * ((2 * c + h) ^ swz_sl));
+        const int off = off_sl + 32 * kb * kPfLatRow + 16 * ((2 * c + h) ^ swz_sl);
+        const bf16x8_t av = *reinterpret_cast<const bf16x8_t*>(tb + off);
+        const bf16x8_t al = *reinterpret_cast<const bf16x8_t*>(tb + kPfLatBytes + off);
         s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qv[c], s[kb], 0, 0, 0);
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, qv[c], s[kb], 0, 0, 0);
       }
 #pragma unroll
     for (int c = 0; c < kPfDR / 16; ++c)
