@@ -23,7 +23,8 @@
  *  - Every tensor argument is a DEVICE pointer owned by the caller,
  *    row-major and contiguous.  The library never allocates or frees device
  *    memory and keeps no state between calls except cached device
- *    properties.
+ *    properties and the scratch array of eg_mla_decode_noalloc (a static
+ *    device array of EG_MLA_NOALLOC_SCRATCH_BYTES per GPU).
  *  - Floating-point tensors have the storage type dims->dtype: IEEE fp32, or
  *    bf16 (16-bit brain float).  Arithmetic is fp32 (bf16 MFMA products with
  *    fp32 accumulation on the bf16 fast path).  Integer tensors are int32.
@@ -176,6 +177,35 @@ eg_mla_status eg_mla_decode_planned(const eg_mla_dims* dims, int32_t batch, cons
                                     const int32_t* seq_lens, const int32_t* page_table,
                                     int32_t max_pages_per_seq, int64_t num_slots, void* workspace,
                                     size_t workspace_bytes, void* out, void* stream, const eg_mla_plan* plan);
+
+/* ---------------------------------------------------------------------------
+ * Decode without a caller workspace, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc).  Same arguments, arithmetic and automatic plan as
+ * eg_mla_decode, minus the workspace: the call uses a scratch array of
+ * EG_MLA_NOALLOC_SCRATCH_BYTES bytes that the library holds in device memory
+ * (one per GPU, for as long as the process runs) and allocates nothing.
+ *   - A call whose plan needs more than EG_MLA_NOALLOC_SCRATCH_BYTES of
+ *     workspace (eg_mla_decode_workspace_size with a NULL plan) returns
+ *     EG_MLA_ERR_WORKSPACE before anything is enqueued; so do the checks of
+ *     eg_mla_decode (status codes as there).  32 MiB covers batch 32 at
+ *     context 4096, batch 4 at 32768 and batch 256 at 2048 of the 16-head
+ *     d_c = 128 layer, not the 128-head d_c = 512 one.
+ *   - Every call on one GPU shares that GPU's array, which keeps the last
+ *     call's contents (nothing in it needs to start at zero).  Calls that
+ *     overlap on one GPU (different streams, or host threads without
+ *     ordering) race: order them, or use eg_mla_decode with separate
+ *     workspaces.
+ *   - The first call on a device looks up the array's device address
+ *     (hipGetSymbolAddress) with that device current; a failure of that
+ *     lookup returns EG_MLA_ERR_HIP.
+ * ------------------------------------------------------------------------- */
+#define EG_MLA_NOALLOC_SCRATCH_BYTES (32u << 20)
+
+eg_mla_status eg_mla_decode_noalloc(const eg_mla_dims* dims, int32_t batch, const void* q, const void* latent_cache,
+                                    const int32_t* token_id_cache, const void* gate_table, const void* w_uk,
+                                    const void* w_uv, const int32_t* seq_lens, const int32_t* page_table,
+                                    int32_t max_pages_per_seq, int64_t num_slots, void* out, void* stream);
 
 /* ---------------------------------------------------------------------------
  * Gate rows from the token embedding (Sec. 3.1 Eq. (3)-(4)): for i < n,

@@ -24,7 +24,8 @@ PATH_AUTO, PATH_VALU, PATH_MFMA = 0, 1, 2
 EXPORTS = ["eg_mla_status_string", "eg_mla_check_dims", "eg_mla_append", "eg_mla_decode_workspace_size",
            "eg_mla_decode", "eg_mla_decode_planned", "eg_mla_gate_rows", "eg_mla_prefill_workspace_size",
            "eg_mla_prefill_ref", "eg_mla_prefill_varlen_workspace_size", "eg_mla_prefill_varlen",
-           "eg_mla_decode_literal_workspace_size", "eg_mla_decode_literal"]
+           "eg_mla_decode_literal_workspace_size", "eg_mla_decode_literal", "eg_mla_decode_noalloc"]
+NOALLOC_SCRATCH_BYTES = 32 << 20  # EG_MLA_NOALLOC_SCRATCH_BYTES
 LITERAL_NO_LN, LITERAL_ADD = 1, 2
 
 
@@ -74,6 +75,8 @@ def lib() -> ctypes.CDLL:
     L.eg_mla_decode.argtypes = [pd, i32, vp, vp, vp, vp, vp, vp, vp, vp, i32, i64, vp, sz, vp, vp]
     L.eg_mla_decode_planned.restype = ctypes.c_int
     L.eg_mla_decode_planned.argtypes = [pd, i32, vp, vp, vp, vp, vp, vp, vp, vp, i32, i64, vp, sz, vp, vp, pp]
+    L.eg_mla_decode_noalloc.restype = ctypes.c_int
+    L.eg_mla_decode_noalloc.argtypes = [pd, i32, vp, vp, vp, vp, vp, vp, vp, vp, i32, i64, vp, vp]
     L.eg_mla_gate_rows.restype = ctypes.c_int
     L.eg_mla_gate_rows.argtypes = [pd, i32, i32, i64, vp, vp, vp, vp, vp]
     L.eg_mla_prefill_workspace_size.restype = sz
@@ -151,6 +154,15 @@ def decode(dims: Dims, q, latent_cache, token_id_cache, gate_table, w_uk, w_uv, 
         _check(L.eg_mla_decode(*args), "eg_mla_decode")
     else:
         _check(L.eg_mla_decode_planned(*args, ctypes.byref(plan)), "eg_mla_decode_planned")
+
+
+def decode_noalloc(dims: Dims, q, latent_cache, token_id_cache, gate_table, w_uk, w_uv, seq_lens, page_table,
+                   max_pages_per_seq: int, out, stream=None) -> None:
+    """eg_mla_decode_noalloc over device tensors (no workspace: the library's scratch array)."""
+    _check(lib().eg_mla_decode_noalloc(ctypes.byref(dims), int(q.shape[0]), _ptr(q), _ptr(latent_cache),
+                                       _ptr(token_id_cache), _ptr(gate_table), _ptr(w_uk), _ptr(w_uv), _ptr(seq_lens),
+                                       _ptr(page_table), max_pages_per_seq, int(latent_cache.shape[0]), _ptr(out),
+                                       _stream(stream)), "eg_mla_decode_noalloc")
 
 
 def append(dims: Dims, x, token_ids, positions, slots, w_dkv, kv_norm_w, latent_cache, token_id_cache,

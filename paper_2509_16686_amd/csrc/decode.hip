@@ -17,6 +17,7 @@
 #include <algorithm>
 #include <cfloat>
 #include <cmath>
+#include <mutex>
 
 #include "device_common.h"
 #include "eg_mla.h"
@@ -436,21 +437,16 @@ hipError_t launch_split(const eg_mla_dims& d, const DecodePlan& p, const SplitAr
 }  // namespace
 }  // namespace egmla
 
-using namespace egmla;
+namespace egmla {
+namespace {
 
-extern "C" eg_mla_status eg_mla_decode_planned(const eg_mla_dims* dims, int32_t batch, const void* q,
-                                               const void* latent_cache, const int32_t* token_id_cache,
-                                               const void* gate_table, const void* w_uk, const void* w_uv,
-                                               const int32_t* seq_lens, const int32_t* page_table,
-                                               int32_t max_pages_per_seq, int64_t num_slots, void* workspace,
-                                               size_t workspace_bytes, void* out, void* stream_,
-                                               const eg_mla_plan* plan) {
-  DecodePlan p;
-  eg_mla_status st = validate_decode(dims, batch, q, latent_cache, token_id_cache, gate_table, w_uk, w_uv,
-                                     seq_lens, max_pages_per_seq, num_slots, page_table, workspace,
-                                     workspace_bytes, out, plan, &p);
-  if (st != EG_MLA_OK || batch == 0) return st;
-  const eg_mla_dims& d = *dims;
+// Enqueues one decode call whose arguments validate_decode has accepted, with
+// its workspace at `workspace` laid out by the plan p.
+eg_mla_status run_decode(const eg_mla_dims& d, const DecodePlan& p, int32_t batch, const void* q,
+                         const void* latent_cache, const int32_t* token_id_cache, const void* gate_table,
+                         const void* w_uk, const void* w_uv, const int32_t* seq_lens, const int32_t* page_table,
+                         int32_t max_pages_per_seq, int64_t num_slots, void* workspace, void* out, void* stream_,
+                         const eg_mla_plan* plan) {
   hipStream_t stream = static_cast<hipStream_t>(stream_);
   const bool bf = d.dtype == EG_MLA_BF16;
   (void)hipGetLastError();  // clear a stale error so the checks below are ours
@@ -576,6 +572,76 @@ extern "C" eg_mla_status eg_mla_decode_planned(const eg_mla_dims* dims, int32_t 
     if (hipGetLastError() != hipSuccess) return EG_MLA_ERR_HIP;
   }
   return EG_MLA_OK;
+}
+
+// Scratch of the allocation-free decode: one array per device, at file
+// scope.  Host code never passes `scratch` itself to a kernel (in host code it
+// names a host-side stand-in); it takes the device address that
+// hipGetSymbolAddress returns on each device, once, with that device current.
+constexpr int kScratchDevices = 64;
+__device__ __align__(256) unsigned char scratch[EG_MLA_NOALLOC_SCRATCH_BYTES];
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kScratchDevices] = {nullptr};
+
+// Device address of this device's scratch array, looked up on its first use
+// (nullptr if the device index is out of range or the lookup fails).
+void* device_scratch() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kScratchDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+    g_scratch_ptr[dev] = ptr;
+  }
+  return g_scratch_ptr[dev];
+}
+
+}  // namespace
+}  // namespace egmla
+
+using namespace egmla;
+
+extern "C" eg_mla_status eg_mla_decode_planned(const eg_mla_dims* dims, int32_t batch, const void* q,
+                                               const void* latent_cache, const int32_t* token_id_cache,
+                                               const void* gate_table, const void* w_uk, const void* w_uv,
+                                               const int32_t* seq_lens, const int32_t* page_table,
+                                               int32_t max_pages_per_seq, int64_t num_slots, void* workspace,
+                                               size_t workspace_bytes, void* out, void* stream,
+                                               const eg_mla_plan* plan) {
+  DecodePlan p;
+  eg_mla_status st = validate_decode(dims, batch, q, latent_cache, token_id_cache, gate_table, w_uk, w_uv,
+                                     seq_lens, max_pages_per_seq, num_slots, page_table, workspace,
+                                     workspace_bytes, out, plan, &p);
+  if (st != EG_MLA_OK || batch == 0) return st;
+  return run_decode(*dims, p, batch, q, latent_cache, token_id_cache, gate_table, w_uk, w_uv, seq_lens, page_table,
+                    max_pages_per_seq, num_slots, workspace, out, stream, plan);
+}
+
+extern "C" eg_mla_status eg_mla_decode_noalloc(const eg_mla_dims* dims, int32_t batch, const void* q,
+                                               const void* latent_cache, const int32_t* token_id_cache,
+                                               const void* gate_table, const void* w_uk, const void* w_uv,
+                                               const int32_t* seq_lens, const int32_t* page_table,
+                                               int32_t max_pages_per_seq, int64_t num_slots, void* out,
+                                               void* stream) {
+  // the plan's workspace must fit the scratch array: checked before any device call
+  DecodePlan p;
+  eg_mla_status st = check_dims(dims);
+  if (st != EG_MLA_OK) return st;
+  if (batch < 0 || max_pages_per_seq < 0) return EG_MLA_ERR_INVALID_ARG;
+  st = make_decode_plan(*dims, batch, max_pages_per_seq, nullptr, &p);
+  if (st != EG_MLA_OK) return st;
+  if (p.bytes > EG_MLA_NOALLOC_SCRATCH_BYTES) return EG_MLA_ERR_WORKSPACE;
+  if (batch == 0) return validate_decode(dims, batch, q, latent_cache, token_id_cache, gate_table, w_uk, w_uv,
+                                         seq_lens, max_pages_per_seq, num_slots, page_table, nullptr, 0, out,
+                                         nullptr, &p);
+  void* ws = device_scratch();
+  if (!ws) return EG_MLA_ERR_HIP;
+  st = validate_decode(dims, batch, q, latent_cache, token_id_cache, gate_table, w_uk, w_uv, seq_lens,
+                       max_pages_per_seq, num_slots, page_table, ws, EG_MLA_NOALLOC_SCRATCH_BYTES, out, nullptr, &p);
+  if (st != EG_MLA_OK) return st;
+  return run_decode(*dims, p, batch, q, latent_cache, token_id_cache, gate_table, w_uk, w_uv, seq_lens, page_table,
+                    max_pages_per_seq, num_slots, ws, out, stream, nullptr);
 }
 
 extern "C" eg_mla_status eg_mla_decode(const eg_mla_dims* dims, int32_t batch, const void* q,

@@ -117,6 +117,23 @@ def test_decode_rejects_before_launch(L):
     assert _decode_call(L, d, batch=0) == B.OK
 
 
+def test_decode_noalloc_rejects_before_launch(L):
+    z = ctypes.c_void_p(16 * 4096)
+    def call(d, batch=2, max_pages=4, num_slots=1 << 20):
+        return L.eg_mla_decode_noalloc(ctypes.byref(d), batch, z, z, z, z, z, z, z, None, max_pages, num_slots, z,
+                                       None)
+    # a plan beyond the scratch array: the 128-head d_c 512 layer at batch 64, 16384 tokens each
+    big = dims(num_heads=128, latent_dim=512, gate_dim=512, vocab_size=129280)
+    assert B.decode_workspace_size(big, 64, 256) > B.NOALLOC_SCRATCH_BYTES
+    assert call(big, batch=64, max_pages=256) == B.ERR_WORKSPACE
+    # the 16-head d_c 128 layer at batch 32, context 4096 fits
+    assert B.decode_workspace_size(dims(), 32, 64) <= B.NOALLOC_SCRATCH_BYTES
+    assert call(dims(num_heads=0)) == B.ERR_INVALID_ARG
+    assert call(dims(), batch=-1) == B.ERR_INVALID_ARG
+    assert call(dims(), max_pages=-1) == B.ERR_INVALID_ARG
+    assert call(dims(), batch=0) == B.OK      # a valid no-op that touches nothing
+
+
 def test_append_and_prefill_reject_before_launch(L):
     d = dims()
     vp = ctypes.c_void_p(256)
