@@ -131,28 +131,40 @@ def recorded_stream_ceiling(mib=60):
 
 
 def cpu_baseline(inp, seconds):
-    """The fp64 oracle as it stands, timed on the host over whole batches."""
+    """The fp64 oracle as it stands, timed on the host over whole batches: with every
+    BLAS thread the process has (the reported value), then limited to one thread."""
     from oracle import eg_mla_oracle as orc
     try:
-        from threadpoolctl import threadpool_info
+        from threadpoolctl import threadpool_info, threadpool_limits
         threads = max([i["num_threads"] for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
     except Exception:
+        threadpool_limits = None
         threads = 1
     wl = inp.wl
-    reps = 0
-    t0 = time.perf_counter()
-    while True:
-        orc.decode(inp.q, inp.latent_cache, inp.token_ids, inp.gate_table, inp.w_uk, inp.w_uv, inp.seq_lens,
-                   latent_dim=wl.latent_dim, head_dim=wl.head_dim, rope_dim=wl.rope_dim, storage=wl.dtype,
-                   page_table=inp.page_table, page_size=wl.page_size, max_pages=inp.max_pages)
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= seconds or reps >= 100:
-            break
-    return {"value": wl.batch * reps / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"{reps} full decode steps of the same workload ({wl.batch} sequences each), "
-                      f"{el:.1f} s, numpy fp64 with {threads} BLAS threads",
-            "cpu_model": cpu_model(), "host_cpus": len(os.sched_getaffinity(0))}
+
+    def rate(budget):
+        reps = 0
+        t0 = time.perf_counter()
+        while True:
+            orc.decode(inp.q, inp.latent_cache, inp.token_ids, inp.gate_table, inp.w_uk, inp.w_uv, inp.seq_lens,
+                       latent_dim=wl.latent_dim, head_dim=wl.head_dim, rope_dim=wl.rope_dim, storage=wl.dtype,
+                       page_table=inp.page_table, page_size=wl.page_size, max_pages=inp.max_pages)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= budget or reps >= 100:
+                return reps, el
+
+    reps, el = rate(seconds)
+    out = {"value": wl.batch * reps / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+           "sample": f"{reps} full decode steps of the same workload ({wl.batch} sequences each), "
+                     f"{el:.1f} s, numpy fp64 with {threads} BLAS threads",
+           "cpu_model": cpu_model(), "host_cpus": len(os.sched_getaffinity(0))}
+    if threadpool_limits is not None:
+        with threadpool_limits(limits=1, user_api="blas"):
+            reps1, el1 = rate(seconds / 2)
+        out["single_thread"] = {"value": wl.batch * reps1 / el1, "unit": "tokens/s", "cores": 1,
+                                "sample": f"{reps1} full decode steps, {el1:.1f} s, one BLAS thread"}
+    return out
 
 
 PREFILL_METRIC = "prefill tokens/s + achieved bf16 TFLOP/s (% of MFMA peak) for eg_mla_prefill_varlen, 1 GPU"
@@ -394,6 +406,93 @@ def literal_main(args):
     print(json.dumps(out), flush=True)
 
 
+def layer_group_main(args):
+    """Times a layer group (App. H): G layers decode one shared cache back to back,
+    each with its own query, W_UK, W_UV and gate table, against G layers each
+    decoding a cache of its own (no sharing).  One step = the G decode calls."""
+    import numpy as np
+    import torch
+
+    from paper_2509_16686_amd import accounting as A
+    from paper_2509_16686_amd import binding as B
+    from paper_2509_16686_amd import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    L = B.lib()
+    hip = Hip()
+    G = args.layer_group
+    wl = W.WORKLOADS[args.workload] if args.workload < len(W.WORKLOADS) else W.MLA_DC320_BIGBATCH
+    log(f"bench: generating a group of {G} layers of {wl.name}")
+    layers = W.generate_layer_group(wl, G)
+    staged = [B.stage_decode(l) for l in layers]
+    cache_bytes = staged[0].cache.numel() * staged[0].cache.element_size() + staged[0].ids.numel() * 4
+    per_layer = sum(t.numel() * t.element_size() for t in (staged[0].gate, staged[0].w_uk, staged[0].w_uv,
+                                                            staged[0].q))
+    # rotating copies of the whole group (its own caches in the unshared case), so that
+    # nothing is served from the MALL from one step to the next
+    R = max(1, math.ceil(args.rotate_bytes / (G * (cache_bytes + per_layer))))
+    ws_bytes = B.decode_workspace_size(staged[0].dims, wl.batch, staged[0].max_pages)
+    ws = B.alloc_workspace(ws_bytes)
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def copy_layer(dd, cache, ids):
+        return B.DeviceDecode(dims=dd.dims, q=dd.q.clone(), cache=cache, ids=ids, gate=dd.gate.clone(),
+                              w_uk=dd.w_uk.clone(), w_uv=dd.w_uv.clone(), seq_lens=dd.seq_lens,
+                              page_table=dd.page_table, max_pages=dd.max_pages, out=torch.empty_like(dd.out))
+
+    shared, separate = [], []
+    for _ in range(R):
+        c, i = staged[0].cache.clone(), staged[0].ids.clone()
+        shared.append([copy_layer(dd, c, i) for dd in staged])
+        separate.append([copy_layer(dd, staged[0].cache.clone(), staged[0].ids.clone()) for dd in staged])
+    call = L.eg_mla_decode
+
+    def args_of(dd):
+        return (ctypes.byref(dd.dims), wl.batch, dd.q.data_ptr(), dd.cache.data_ptr(), dd.ids.data_ptr(),
+                dd.gate.data_ptr(), dd.w_uk.data_ptr(), dd.w_uv.data_ptr(), dd.seq_lens.data_ptr(),
+                None if dd.page_table is None else dd.page_table.data_ptr(), dd.max_pages, int(dd.cache.shape[0]),
+                ws.data_ptr(), ws_bytes, dd.out.data_ptr(), stream)
+
+    K, Wm = args.steps, args.warmup
+
+    def time_group(groups):
+        steps = [[args_of(dd) for dd in groups[k % R]] for k in range(K)]
+        for k in range(max(Wm, 1)):
+            for a in steps[k % K]:
+                assert call(*a) == 0
+        torch.cuda.synchronize()
+        e0, e1 = hip.event(), hip.event()
+        torch.cuda._sleep(40_000_000)
+        hip.record(e0, stream)
+        for st in steps:
+            for a in st:
+                call(*a)
+        hip.record(e1, stream)
+        torch.cuda.synchronize()
+        return hip.elapsed_ms(e0, e1) / K
+
+    ms_shared = time_group(shared)
+    ms_sep = time_group(separate)
+    layers_model = MODEL_LAYERS
+    cache_tok = A.cache_bytes_per_token(layers=layers_model, latent_dim=wl.latent_dim, rope_dim=wl.rope_dim,
+                                        elem_bytes=wl.elem_bytes, layer_group=G)
+    cache_tok1 = A.cache_bytes_per_token(layers=layers_model, latent_dim=wl.latent_dim, rope_dim=wl.rope_dim,
+                                         elem_bytes=wl.elem_bytes)
+    log(f"bench: layer group of {G}: {ms_shared * 1e3 / G:.2f} us per layer on the shared cache, "
+        f"{ms_sep * 1e3 / G:.2f} us per layer on separate caches; cache {cache_tok} B/token over "
+        f"{layers_model} layers ({cache_tok1} B without grouping)")
+    out = {"metric": METRIC, "value": wl.batch / (ms_shared * 1e-3 / G), "unit": "tokens/s", "n_gpus": 1,
+           "steps": K, "warmup": Wm, "ms_per_step": ms_shared, "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "bf16" if wl.dtype == "bf16" else "fp32", "data": "synthetic",
+           "config": {"workload": f"layer_group{G}_{wl.name}", "layers_per_step": G, "rotating_copies": R},
+           "layer_group": {"size": G, "us_per_layer_shared": ms_shared * 1e3 / G,
+                           "us_per_layer_separate": ms_sep * 1e3 / G,
+                           "cache_bytes_per_token_model": cache_tok, "cache_bytes_per_token_model_ungrouped": cache_tok1,
+                           "model_layers": layers_model}}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -424,6 +523,9 @@ def main():
                     help="unfolded gate with embedding width E (the paper recommends 512): every step first "
                          "computes one gate row per cache row from its token embedding (eg_mla_gate_rows), then "
                          "decodes with the row indices as ids; 0 = the folded gate table")
+    ap.add_argument("--layer-group", type=int, default=0, metavar="G",
+                    help="time G layers of a layer group (App. H) decoding one shared cache, against G layers "
+                         "with caches of their own")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -438,6 +540,8 @@ def main():
         return literal_main(args)
     if args.append:
         return append_main(args)
+    if args.layer_group:
+        return layer_group_main(args)
 
     import numpy as np
     import torch

@@ -181,6 +181,20 @@ def decode_explicit(q, cache, token_ids, gate_table, w_uk, w_uv, seq_lens, *, la
     return out
 
 
+def decode_layer_group(cache, token_ids, seq_lens, layers, *, latent_dim: int, head_dim: int, rope_dim: int,
+                       storage: str, page_table=None, page_size: int = 64, max_pages: int = 0) -> list:
+    """Layer grouping of App. H (lgz consecutive layers share the first half of the
+    KV projection and its activations), decoded: the group caches one
+    [c | k^R] row and one token id per token, written by its first layer, and
+    every layer of the group decodes those rows with its own query, W_UK, W_UV
+    and gate table.  ``layers`` holds (q, gate_table, w_uk, w_uv) per layer;
+    returns each layer's out [B, H, d_v], the same as ``decode`` of that layer
+    over the shared rows."""
+    return [decode(q, cache, token_ids, gate, w_uk, w_uv, seq_lens, latent_dim=latent_dim, head_dim=head_dim,
+                   rope_dim=rope_dim, storage=storage, page_table=page_table, page_size=page_size,
+                   max_pages=max_pages) for (q, gate, w_uk, w_uv) in layers]
+
+
 # ---------------------------------------------------------------------------
 # the paper-literal gate (Sec. 3.1 Eq. (2)-(5) as printed, and the model
 # listing of App. E): the gate multiplies the up-projected keys and values of

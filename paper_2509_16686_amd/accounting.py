@@ -16,9 +16,17 @@ from dataclasses import dataclass
 
 def kv_cache_elements_per_token(mechanism: str, *, layers: int, heads: int = 0, head_dim: int = 0,
                                 groups: int = 0, latent_dim: int = 0, rope_dim: int = 0,
-                                compression: int = 1) -> int:
-    """Per-token KV-cache elements summed over ``layers`` layers (Table 5)."""
+                                compression: int = 1, layer_group: int = 1) -> int:
+    """Per-token KV-cache elements summed over ``layers`` layers (Table 5).
+
+    ``layer_group`` (App. H, lgz) applies to the latent mechanisms: the layers
+    of a group share one cached row, so ``ceil(layers / lgz)`` rows are kept."""
     m = mechanism.lower()
+    if layer_group != 1:
+        assert layer_group >= 1 and m in ("mla", "eg-mla", "egmla", "eg_mla")
+        rows = -(-layers // layer_group)
+        return kv_cache_elements_per_token(m, layers=rows, latent_dim=latent_dim, rope_dim=rope_dim,
+                                           compression=compression)
     if m == "mha":
         return 2 * heads * head_dim * layers
     if m == "gqa":
@@ -76,3 +84,13 @@ def decode_flops(*, batch: int, heads: int, head_dim: int, v_head_dim: int, late
     up = batch * heads * v_head_dim * latent_dim
     gate = total_tokens * latent_dim // 2                      # one multiply per latent element
     return 2 * (total_tokens * heads * per_token_head + absorb + up + gate)
+
+
+def cache_bytes_per_token(*, layers: int, latent_dim: int, rope_dim: int, elem_bytes: int,
+                          layer_group: int = 1) -> int:
+    """Bytes this library caches per token over ``layers`` layers: per cached
+    row (one per group of ``layer_group`` layers, App. H) the latent and RoPE
+    key in the storage type and one int32 token id (which Table 5 does not
+    count)."""
+    rows = -(-layers // layer_group)
+    return rows * ((latent_dim + rope_dim) * elem_bytes + 4)

@@ -231,6 +231,22 @@ def generate(wl: Workload, seq_lens: Optional[np.ndarray] = None) -> DecodeInput
         q=_store(q, wl.dtype), w_uk=_store(w_uk, wl.dtype), w_uv=_store(w_uv, wl.dtype))
 
 
+def generate_layer_group(wl: Workload, group_size: int, seq_lens: Optional[np.ndarray] = None) -> list:
+    """One layer group of App. H: ``group_size`` layers decoding one shared cache.
+
+    Layer 0 is ``generate(wl, seq_lens)``.  Layer k > 0 draws its own query,
+    W_UK, W_UV and gate table from seed ``wl.seed + 7919 k`` and takes layer 0's
+    lengths, page table, cache rows and token ids (the same arrays)."""
+    base = generate(wl, seq_lens)
+    layers = [base]
+    for k in range(1, group_size):
+        other = generate(wl.replace(seed=wl.seed + 7919 * k), seq_lens=base.seq_lens)
+        layers.append(dataclasses.replace(other, seq_lens=base.seq_lens, page_table=base.page_table,
+                                          max_pages=base.max_pages, num_rows=base.num_rows,
+                                          latent_cache=base.latent_cache, token_ids=base.token_ids))
+    return layers
+
+
 @dataclass
 class GateEmbedding:
     """Unfolded gate of Sec. 3.1 Eq. (3)-(4): an embedding table and W^UE.

@@ -57,3 +57,20 @@ def test_flops_count():
     f = A.decode_flops(batch=1, heads=1, head_dim=2, v_head_dim=2, latent_dim=2, rope_dim=0, total_tokens=1)
     # score 2 + value 2 MACs, absorb 4, up 4, gate 1 -> 13 MACs
     assert f == 2 * (1 * (2 + 2) + 4 + 4 + 1)
+
+
+def test_layer_group_cache_rows():
+    # App. H: lgz consecutive layers share one cached row; lgz = 1 is the App. F count
+    g = json.load(open(GOLD))
+    kv64 = A.kv_cache_elements_per_token("eg-mla", layers=12, latent_dim=64, rope_dim=64)
+    assert round(kv64 / 1000, 2) == 1.54                                   # App. F, EG-MLA-Base-kv64
+    assert A.kv_cache_elements_per_token("eg-mla", layers=12, latent_dim=64, rope_dim=64, layer_group=1) == kv64
+    assert A.kv_cache_elements_per_token("eg-mla", layers=12, latent_dim=64, rope_dim=64, layer_group=2) == kv64 // 2
+    assert A.kv_cache_elements_per_token("eg-mla", layers=12, latent_dim=64, rope_dim=64, layer_group=3) == kv64 // 3
+    # a last group shorter than lgz still keeps its row: 24 layers, lgz 5 -> 5 rows
+    assert A.kv_cache_elements_per_token("mla", layers=24, latent_dim=128, rope_dim=64, layer_group=5) == 5 * 192
+    assert g["layers"] == 12
+    # bytes of this library's cache (bf16 rows + int32 id) for the 24-layer 1.2B-class model
+    assert A.cache_bytes_per_token(layers=24, latent_dim=128, rope_dim=64, elem_bytes=2) == 24 * 388
+    assert A.cache_bytes_per_token(layers=24, latent_dim=128, rope_dim=64, elem_bytes=2, layer_group=2) == 12 * 388
+    assert A.cache_bytes_per_token(layers=24, latent_dim=128, rope_dim=64, elem_bytes=2, layer_group=3) == 8 * 388

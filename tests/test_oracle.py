@@ -475,3 +475,34 @@ def test_literal_ln_removes_latent_scale():
     inp2.latent_cache[r, :wl.latent_dim] *= 3
     assert rel_err(literal(inp2, lg), base) < 1e-5
     assert rel_err(literal(inp2, lg, use_ln=False), literal(inp, lg, use_ln=False)) > 1e-3
+
+
+# ---- App. H: layer grouping ----------------------------------------------------
+def test_layer_group_layers_read_the_shared_rows():
+    """Each layer of a group attends over the one shared set of cached rows with its
+    own query, weights and gate table: its output is SDPA (fp64, CPU) over keys and
+    values built from the shared rows with that layer's W_UK, W_UV and gate, and
+    layers with different weights give different outputs."""
+    wl = tiny(batch=2, heads=2, head_dim=5, v_head_dim=4, latent_dim=7, gate_dim=7, rope_dim=4, seq_len=9,
+              vocab=11, paged=True)
+    layers = W.generate_layer_group(wl, 3)
+    base = layers[0]
+    outs = orc.decode_layer_group(base.latent_cache, base.token_ids, base.seq_lens,
+                                  [(l.q, l.gate_table, l.w_uk, l.w_uv) for l in layers], **kw(base))
+    cf = orc.widen(base.latent_cache, "fp32")
+    for lay, out in zip(layers, outs):
+        assert lay.latent_cache is base.latent_cache and lay.token_ids is base.token_ids
+        g = orc.widen(lay.gate_table, "fp32")
+        q = orc.widen(lay.q, "fp32")
+        wk, wv = orc.widen(lay.w_uk, "fp32"), orc.widen(lay.w_uv, "fp32")
+        for b in range(2):
+            rows = base.slots_of(b)
+            cg = torch.from_numpy(cf[rows, :7] * g[base.token_ids[rows]])
+            kr = torch.from_numpy(cf[rows, 7:])
+            for h in range(2):
+                k = torch.cat([cg @ torch.from_numpy(wk[h]).T, kr], 1)[None, None]
+                v = (cg @ torch.from_numpy(wv[h]).T)[None, None]
+                ref = torch.nn.functional.scaled_dot_product_attention(torch.from_numpy(q[b, h])[None, None, None],
+                                                                       k, v)[0, 0, 0].numpy()
+                np.testing.assert_allclose(out[b, h], ref, rtol=1e-11, atol=1e-14)
+    assert rel_err(outs[0], outs[1]) > 1e-3 and rel_err(outs[1], outs[2]) > 1e-3
