@@ -63,6 +63,7 @@ __device__ __forceinline__ void lds_dma16_addr(uint64_t addr, uint32_t lds_base)
   asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds_base), "v"(addr));
 }
 
+
 // s_waitcnt with only the vector-memory counter constrained; also a compiler
 // memory barrier, so that no LDS access moves across it.
 template <int N>
@@ -104,7 +105,6 @@ struct WideCfg {
   static constexpr int LISTCAP = 1024;               // tokens listed at a time (a multiple of 32)
   static constexpr int QROPE = LIST + LISTCAP * 8;   // [NW][2 chunks][64 lanes] bf16x8: RoPE query (B operand)
   static constexpr int LDS_BYTES = QROPE + NW * 2 * 64 * 16;
-  static constexpr int DMA_PER_PAIR = 2 * 9;  // per wave and pair: 4 latent, 4 gate, 1 RoPE DMA per slot
   static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
   static_assert(SLOT % 16 == 0 && LIST % 16 == 0, "alignment");
 };
@@ -296,95 +296,131 @@ __global__ __launch_bounds__(WideCfg::NT, 1) void split_wide_kernel(SplitArgs a)
         }
         __syncthreads();  // the list is complete; every wave is done with the previous chunk's slots
 
-        // DMAs of slot s (list tokens 16 s ..) for this wave's rows 4w .. 4w + 3
-        auto issue_slot = [&](int s) {
-          const uint32_t sb = lds0 + (s % C::NS) * C::SLOT;
-          const int4 e01 = reinterpret_cast<const int4*>(list)[(16 * s + 4 * w) / 2];
-          const int4 e23 = reinterpret_cast<const int4*>(list)[(16 * s + 4 * w) / 2 + 1];
-          const int sl[4] = {__builtin_amdgcn_readfirstlane(e01.x), __builtin_amdgcn_readfirstlane(e01.z),
-                             __builtin_amdgcn_readfirstlane(e23.x), __builtin_amdgcn_readfirstlane(e23.z)};
-          const int id[4] = {__builtin_amdgcn_readfirstlane(e01.y), __builtin_amdgcn_readfirstlane(e01.w),
-                             __builtin_amdgcn_readfirstlane(e23.y), __builtin_amdgcn_readfirstlane(e23.w)};
+        // This wave's DMAs of pair p: tokens 4w .. 4w + 3 of slots 2p and 2p + 1,
+        // per slot 4 latent rows, 4 gate rows and one RoPE instruction (18 in
+        // all).  pair_entries reads the pair's list entries (wave-uniform, into
+        // scalar registers); dma_step(j) issues instruction j, so that the issue
+        // can be spread between the score products.  A pair index past the
+        // chunk takes the last pair's entries (its rows land in ring slots that
+        // are free, and are never read).
+        int psl[8], pid[8];
+        auto pair_entries = [&](int p) {
+          const int pe = min(p, npairs - 1);
 #pragma unroll
-          for (int k = 0; k < 4; ++k) {
-            lds_dma16(cache + static_cast<int64_t>(sl[k]) * DQ, dma_off[k], sb + C::HI + (4 * w + k) * LROW);
-            lds_dma16(gate + static_cast<int64_t>(id[k]) * DC, dma_off[k], sb + C::LO + (4 * w + k) * LROW);
+          for (int k = 0; k < 2; ++k) {
+            const int4 e01 = reinterpret_cast<const int4*>(list)[(16 * (2 * pe + k) + 4 * w) / 2];
+            const int4 e23 = reinterpret_cast<const int4*>(list)[(16 * (2 * pe + k) + 4 * w) / 2 + 1];
+            psl[4 * k + 0] = __builtin_amdgcn_readfirstlane(e01.x);
+            psl[4 * k + 1] = __builtin_amdgcn_readfirstlane(e01.z);
+            psl[4 * k + 2] = __builtin_amdgcn_readfirstlane(e23.x);
+            psl[4 * k + 3] = __builtin_amdgcn_readfirstlane(e23.z);
+            pid[4 * k + 0] = __builtin_amdgcn_readfirstlane(e01.y);
+            pid[4 * k + 1] = __builtin_amdgcn_readfirstlane(e01.w);
+            pid[4 * k + 2] = __builtin_amdgcn_readfirstlane(e23.y);
+            pid[4 * k + 3] = __builtin_amdgcn_readfirstlane(e23.w);
           }
-          // RoPE keys of the 4 rows: lane l < 32 reads row 4w + l / 8 (its own list entry)
-          const int slk = list[16 * s + rope_row].x;
-          const uint64_t addr = reinterpret_cast<uint64_t>(cache + static_cast<int64_t>(slk) * DQ) + rope_src;
-          if (lane < 32) lds_dma16_addr(addr, sb + C::ROPE + 4 * w * 128);
         };
-        auto issue_pair = [&](int p) {
-          issue_slot(2 * p);
-          issue_slot(2 * p + 1);
+        auto dma_step = [&](int p, int j) {
+          const int k = j / 9, i = j % 9;  // slot 2p + k of the ring, instruction i
+          const uint32_t sb = lds0 + ((2 * p + k) % C::NS) * C::SLOT;
+          if (i < 4) {
+            lds_dma16(cache + static_cast<int64_t>(psl[4 * k + i]) * DQ, dma_off[i], sb + C::HI + (4 * w + i) * LROW);
+          } else if (i < 8) {
+            lds_dma16(gate + static_cast<int64_t>(pid[4 * k + i - 4]) * DC, dma_off[i - 4],
+                      sb + C::LO + (4 * w + i - 4) * LROW);
+          } else {
+            // RoPE keys of the 4 rows: lane l < 32 reads row 4w + l / 8 (its own list entry)
+            const int slk = list[16 * (2 * min(p, npairs - 1) + k) + rope_row].x;
+            const uint64_t addr = reinterpret_cast<uint64_t>(cache + static_cast<int64_t>(slk) * DQ) + rope_src;
+            if (lane < 32) lds_dma16_addr(addr, sb + C::ROPE + 4 * w * 128);
+          }
         };
-        // gate this wave's rows of slot s in place: HI <- bf16(c g), LO <- c g - HI
-        // (one row's pieces are read while the previous row is gated)
-        auto gate_slot = [&](int s) {
-          unsigned char* sp = lds + (s % C::NS) * C::SLOT + off_gate;
-          u32x4_t lat[2], gat[2];
-          lat[0] = *reinterpret_cast<const u32x4_t*>(sp + C::HI);
-          gat[0] = *reinterpret_cast<const u32x4_t*>(sp + C::LO);
+
+        // gate this wave's rows of pair p in place: HI <- bf16(c g), LO <- c g - HI
+        // (per slot, the 8 reads of its 4 rows first, then the products)
+        auto gate_pair = [&](int p) {
 #pragma unroll
-          for (int k = 0; k < 4; ++k) {
-            if (k + 1 < 4) {
-              lat[(k + 1) & 1] = *reinterpret_cast<const u32x4_t*>(sp + C::HI + (k + 1) * LROW);
-              gat[(k + 1) & 1] = *reinterpret_cast<const u32x4_t*>(sp + C::LO + (k + 1) * LROW);
+          for (int k = 0; k < 2; ++k) {
+            unsigned char* sp = lds + ((2 * p + k) % C::NS) * C::SLOT + off_gate;
+            u32x4_t lat[4], gat[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              lat[r] = *reinterpret_cast<const u32x4_t*>(sp + C::HI + r * LROW);
+              gat[r] = *reinterpret_cast<const u32x4_t*>(sp + C::LO + r * LROW);
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              u32x4_t hi, lo;
+              gate_chunk_hilo(lat[r], gat[r], hi, lo);
+              *reinterpret_cast<u32x4_t*>(sp + C::HI + r * LROW) = hi;
+              *reinterpret_cast<u32x4_t*>(sp + C::LO + r * LROW) = lo;
             }
             __builtin_amdgcn_sched_barrier(0);
-            u32x4_t hi, lo;
-            gate_chunk_hilo(lat[k & 1], gat[k & 1], hi, lo);
-            *reinterpret_cast<u32x4_t*>(sp + C::HI + k * LROW) = hi;
-            *reinterpret_cast<u32x4_t*>(sp + C::LO + k * LROW) = lo;
-            __builtin_amdgcn_sched_barrier(0);
           }
         };
-        // S^T[token 4g + q][head r16] of slot s (unscaled), one accumulator
-        // chain.  The operands of chunk c + 1 are read while chunk c's products
-        // run, and nothing is hoisted further (every chunk's reads would
-        // otherwise be live at once).
-        auto scores = [&](int s) {
-          const unsigned char* sp = lds + (s % C::NS) * C::SLOT;
-          f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-          bf16x8_t ah[2], al[2];
+        // S^T[token 4g + q][head r16] of the pair's two slots (unscaled), on
+        // four accumulator chains (slot x query part) whose products alternate,
+        // so no product waits for the one before it.  The operands of chunk
+        // c + 1 are read while chunk c's products run, and nothing is hoisted
+        // further (every chunk's reads would otherwise be live at once).  Two of
+        // the next pair's DMAs go out with each of the first 9 chunks.
+        auto scores = [&](int s0, f32x4_t& sa, f32x4_t& sb, int pn) {
+          const unsigned char* spa = lds + (s0 % C::NS) * C::SLOT;
+          const unsigned char* spb = lds + ((s0 + 1) % C::NS) * C::SLOT;
+          f32x4_t a0 = {0.f, 0.f, 0.f, 0.f}, a1 = a0, b0 = a0, b1 = a0;
+          bf16x8_t ah[2], al[2], bh[2], bl[2];
           auto rd = [&](int c) {
             const int pc = off_sa + 64 * (c ^ (sa_x >> 2));
-            ah[c & 1] = *reinterpret_cast<const bf16x8_t*>(sp + C::HI + pc);
-            al[c & 1] = *reinterpret_cast<const bf16x8_t*>(sp + C::LO + pc);
+            ah[c & 1] = *reinterpret_cast<const bf16x8_t*>(spa + C::HI + pc);
+            al[c & 1] = *reinterpret_cast<const bf16x8_t*>(spa + C::LO + pc);
+            bh[c & 1] = *reinterpret_cast<const bf16x8_t*>(spb + C::HI + pc);
+            bl[c & 1] = *reinterpret_cast<const bf16x8_t*>(spb + C::LO + pc);
           };
           rd(0);
 #pragma unroll
           for (int c = 0; c < 16; ++c) {
             if (c + 1 < 16) rd(c + 1);
+            if (c < 9) {
+              dma_step(pn, 2 * c);
+              dma_step(pn, 2 * c + 1);
+            }
             __builtin_amdgcn_sched_barrier(0);
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[c & 1], qh[c], acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[c & 1], ql[c], acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[c & 1], qh[c], acc, 0, 0, 0);
+            a0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[c & 1], qh[c], a0, 0, 0, 0);
+            b0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bh[c & 1], qh[c], b0, 0, 0, 0);
+            a1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[c & 1], ql[c], a1, 0, 0, 0);
+            b1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bh[c & 1], ql[c], b1, 0, 0, 0);
+            a0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[c & 1], qh[c], a0, 0, 0, 0);
+            b0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bl[c & 1], qh[c], b0, 0, 0, 0);
             __builtin_amdgcn_sched_barrier(0);
           }
 #pragma unroll
           for (int c = 0; c < 2; ++c) {
-            const bf16x8_t ar = *reinterpret_cast<const bf16x8_t*>(sp + (c ? off_sr1 : off_sr));
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ar, qrope[64 * c], acc, 0, 0, 0);
+            const int off = c ? off_sr1 : off_sr;
+            const bf16x8_t ar = *reinterpret_cast<const bf16x8_t*>(spa + off);
+            const bf16x8_t br = *reinterpret_cast<const bf16x8_t*>(spb + off);
+            a1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ar, qrope[64 * c], a1, 0, 0, 0);
+            b1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(br, qrope[64 * c], b1, 0, 0, 0);
           }
-          return acc;
+          sa = a0 + a1;
+          sb = b0 + b1;
         };
 
-        issue_pair(0);
-        if (npairs > 1) issue_pair(1);
+        // Pair 0's DMAs go out now; pair p + 1's during the scores of pair p
+        // (into the slots of pair p - 1, free once every wave has passed pair
+        // p's barrier), so when iteration p starts, pair p's are the only loads
+        // in flight.
+        pair_entries(0);
+#pragma unroll
+        for (int j = 0; j < 18; ++j) dma_step(0, j);
         for (int p = 0; p < npairs; ++p) {
-          // this wave's DMAs of pair p have landed (those of pair p + 1 may be in flight)
-          if (p == 0 && npairs > 1) wait_vmcnt<C::DMA_PER_PAIR>();
-          else wait_vmcnt<0>();
-          gate_slot(2 * p);
-          gate_slot(2 * p + 1);
+          wait_vmcnt<0>();
+          gate_pair(p);
           lds_barrier();  // pair p gated and visible; every wave is done with pair p - 1
-          if (p >= 1 && p + 1 < npairs) issue_pair(p + 1);  // into the slots of pair p - 1
+          pair_entries(p + 1);
           __builtin_amdgcn_sched_barrier(0);
 
-          const f32x4_t sa = scores(2 * p);
-          const f32x4_t sb = scores(2 * p + 1);
+          f32x4_t sa, sb;
+          scores(2 * p, sa, sb, p + 1);
           float x[8];
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
@@ -426,25 +462,30 @@ __global__ __launch_bounds__(WideCfg::NT, 1) void split_wide_kernel(SplitArgs a)
           // O^T += C~^T P^T, A operand: dim 16 db + r16 of the same 8 tokens
           const unsigned char* sp0 = lds + ((2 * p) % C::NS) * C::SLOT + C::HI + off_tr;
           const unsigned char* sp1 = lds + ((2 * p + 1) % C::NS) * C::SLOT + C::HI + off_tr;
-          // (the operands of block db + 1 are read while block db's product runs)
-          s16x4_t v0[2], v1[2];
+          // (the operands of block db + 3 are read while block db's product runs)
+          s16x4_t v0[4], v1[4];
           auto rdv = [&](int db) {
             const int pd = 32 * (db ^ tr_fh);
-            v0[db & 1] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t*)(sp0 + pd));
-            v1[db & 1] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t*)(sp1 + pd));
+            v0[db & 3] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t*)(sp0 + pd));
+            v1[db & 3] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t*)(sp1 + pd));
           };
           rdv(0);
+          rdv(1);
+          rdv(2);
 #pragma unroll
           for (int db = 0; db < 32; ++db) {
-            if (db + 1 < 32) rdv(db + 1);
+            if (db + 3 < 32) rdv(db + 3);
             __builtin_amdgcn_sched_barrier(0);
             const bf16x8_t av =
-                __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(v0[db & 1], v1[db & 1], 0, 1, 2, 3, 4, 5, 6, 7));
+                __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(v0[db & 3], v1[db & 3], 0, 1, 2, 3, 4, 5, 6, 7));
             o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, pb, o[db], 0, 0, 0);
             __builtin_amdgcn_sched_barrier(0);
           }
           __builtin_amdgcn_sched_barrier(0);
         }
+        // the last pair's DMAs (issued past the chunk, never read) land before
+        // the list is rebuilt or the work-group exits
+        wait_vmcnt<0>();
       }
       // ---- partial result of this segment: this wave's 16 heads ----
       const int64_t pbase = (static_cast<int64_t>(wg) + b) * a.H + head0;
