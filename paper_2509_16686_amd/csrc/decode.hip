@@ -382,8 +382,15 @@ hipError_t launch_slice(const SplitArgs& a, int slices, int nblocks, hipStream_t
 }
 
 // Balanced head-split kernel: `ranges` token ranges x a.groups blocks of 64 heads.
+// Wide kernel: units in flight per wave.
+#ifndef EGMLA_WIDE_DEPTH
+#define EGMLA_WIDE_DEPTH 2
+#endif
+constexpr int kWideDepth = EGMLA_WIDE_DEPTH;
+
 hipError_t launch_wide(const SplitArgs& a, int ranges, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
-  hipExtLaunchKernelGGL(split_wide_kernel, dim3(ranges * a.groups), dim3(WideCfg::NT), 0, stream, ev0, ev1, 0, a);
+  hipExtLaunchKernelGGL((split_wide_kernel<kWideDepth>), dim3(ranges * a.groups), dim3(WideCfg::NT), 0, stream, ev0,
+                        ev1, 0, a);
   return hipGetLastError();
 }
 

@@ -1,112 +1,85 @@
 // Wide split kernel of EG-MLA decode: latent dim 512, RoPE dim 64, bf16
 // storage, heads in blocks of 64.  Included by decode.hip after SplitArgs.
 //
-// Work split.  One work-group of 4 waves (one per SIMD) per (token range, block
-// of 64 heads); wave w holds heads 16 w .. 16 w + 15 of the block over all 576
-// score dims and all 512 value dims, so no wave needs another wave's scores.
-// The two head blocks of a 128-head layer run the same token range on the same
-// XCD (blocks 8 apart), so the second fetch of a token's rows hits that XCD's
-// L2 cache.
+// Work split.  One work-group of 8 waves per (token range, block of 64
+// heads), in two roles; wave w runs on SIMD w % 4, so every SIMD holds one
+// wave of each role and the VALU and LDS work of one overlaps the matrix
+// products of the other.
+//   * Score wave s (w = s < 4) owns latent dims 128 s .. 128 s + 127 of every
+//     token: it loads its slice of a token's cache row and gate row straight
+//     from HBM into registers in the layout of the MFMA A operand (lane: token
+//     lane % 16, 8 consecutive dims), gates it there, writes the hi part into
+//     the unit's gated tile in LDS (row = token) and computes the partial
+//     scores S_s^T[token][head] of the 64 heads on v_mfma_f32_16x16x32_bf16,
+//     the absorbed query of its dims held in registers.  A chunk's loads for a
+//     later unit go out as soon as the chunk has been gated, so the work-
+//     group's loads reach the texture unit spread over the step.
+//   * Value wave t (w = 4 + t) owns head tile t (heads 16 t .. 16 t + 15) for
+//     the softmax and latent dims 128 t .. 128 t + 127 of the output: it adds
+//     the four partials of its head tile and the RoPE part (its own product
+//     over the 64 RoPE dims), runs the online softmax of its 16 heads (log2
+//     domain, lazy rescale), and accumulates O^T[dim][head] += C~^T P^T for
+//     its dims and all 64 heads on v_mfma_f32_16x16x16_bf16, the A operand
+//     read with ds_read_b64_tr_b16 from the gated tile.
+// Each role runs its own loop (so their registers do not add up) and both
+// meet the same barriers, one per unit of 16 tokens: the partials and gated
+// tile of unit u are written before barrier u; between barriers u and u + 1
+// the value waves run the softmax of unit u and the values of unit u - 1
+// (probabilities exchanged among them through LDS) while the score waves
+// compute unit u + 1.  The partial-score and probability buffers are
+// double-buffered, the gated tiles triple-buffered.
 //
-// Precision.  The absorbed query (fp32) is held as bf16 hi + lo, and each gated
+// Precision.  The absorbed query is held as bf16 hi + lo, and each gated
 // latent c * g (an exact fp32 product of two bf16 values, 16 significant bits)
 // as bf16 hi + lo whose sum is the product exactly.  A score's latent part is
-// hi.q_hi + hi.q_lo + lo.q_hi (the lo.lo product, below 2^-16 of the score, is
-// left out), so a score carries fp32-level error even when the logits are
-// large and the softmax is sharp; the RoPE part (bf16 x bf16) is exact.  The
-// value product takes the gated latent's hi part and bf16 probabilities.
+// hi.q_hi + lo.q_hi + hi.q_lo (only the lo.lo product, below 2^-16 of the
+// score, is left out); the RoPE part (bf16 x bf16) is exact.  The value
+// product takes the gated latent's hi part and bf16 probabilities.
 //
-// Staging.  Tokens are taken 16 at a time (a slot); a ring of 4 slots holds two
-// pairs of slots, one computed while the other's rows travel.  Cache rows and
-// gate rows go from HBM straight into LDS with global_load_lds_dwordx4 (no
-// registers): per token one 1024-byte latent DMA (into the slot's HI region),
-// one 1024-byte gate DMA (into its LO region) and a 128-byte RoPE key.  Wave w
-// fetches and then gates tokens 4 w .. 4 w + 3 of every slot in place: HI
-// receives bf16(c g), LO the remainder.
-//
-// Scores.  S^T[token][head] of a slot on v_mfma_f32_16x16x32_bf16: the A
-// operand (token lane % 16, 8 dims) is read from the slot, the B operand is
-// the query (16 heads) held in registers: 3 latent products per 32-dim chunk
-// on three accumulator chains, then the RoPE chunks.
-//
-// Softmax and values.  Per pair of slots the lane holds 8 scores of its head
-// (4 tokens of each slot); online softmax in the log2 domain with a lazy
-// rescale.  O^T[dim][head] += C~^T P^T on v_mfma_f32_16x16x32_bf16 with K = the
-// pair's 32 tokens: each lane's own 8 probabilities are its B operand, and two
-// ds_read_b64_tr_b16 (one per slot, the same 4 token rows) are its A operand,
-// so the token order inside K is the same for both operands.
-//
-// Registers per wave: query hi + lo 128 (its RoPE chunks wait in LDS), value
-// accumulators 128 (32 blocks of 16 dims x 16 heads), the score chain and the
-// operands in flight: one wave per SIMD.  Each phase (gating, scores, values)
-// reads its LDS operands at most two steps ahead of their use.
+// The two head blocks of a 128-head layer run the same token range on the same
+// XCD (block ids 8 apart), so the second fetch of a token's rows hits that
+// XCD's L2 cache.
 #pragma once
 
 namespace egmla {
 
-// LDS DMA of 16 bytes per lane from sbase + voff: lane l's bytes land at LDS
-// byte address lds_base + 16 l (M0 holds lds_base; one wait state separates
-// its write from the DMA).  The instruction is not visible to the compiler's
-// wait counters: the caller waits for it with s_waitcnt vmcnt before reading
-// the destination, and before the work-group exits.
-// (No memory clobber: the DMA's LDS writes become visible only through
-// wait_vmcnt, which is a compiler memory barrier, and the work-group barriers
-// order every access to a ring slot before the DMA that refills it.)
-__device__ __forceinline__ void lds_dma16(const void* sbase, uint32_t voff, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds_base), "v"(voff),
-               "s"(sbase));
-}
-
-// The same with a full 64-bit address per lane (lanes of one instruction may
-// read different rows); inactive lanes move nothing.
-__device__ __forceinline__ void lds_dma16_addr(uint64_t addr, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds_base), "v"(addr));
-}
-
-
-// s_waitcnt with only the vector-memory counter constrained; also a compiler
-// memory barrier, so that no LDS access moves across it.
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-
-// Work-group barrier that orders LDS accesses but does not wait for
-// outstanding global loads (the ring's DMA stays in flight across it).
+// Work-group barrier that orders LDS accesses; outstanding global loads stay
+// in flight across it (the workgroup-scope fences wait for LDS only).
 __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
   __builtin_amdgcn_s_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 }
 
-// Rows in a slot's HI and LO regions are stored with their 16-byte pieces
-// permuted: logical piece p of slot row r sits at piece p ^ lat_swz(r)
-// (lat_swz(r) < 16 takes 16 distinct values over r = 0..15).  The score read
-// (16 rows, one piece each: 4-bank group (p ^ lat_swz(r)) mod 16) and the
-// transposed value read (4 rows x one 32-byte pair each: pair index
-// (p / 2) ^ (lat_swz(r) / 2) differs over each group of 4 rows) are then free
-// of bank conflicts.
-__device__ __forceinline__ int lat_swz(int r) { return ((0xCA60 >> (4 * (r & 3))) & 15) ^ (r >> 2); }
-
 struct WideCfg {
   static constexpr int DC = 512, DR = 64, DQ = DC + DR;
-  static constexpr int NW = 4, NT = NW * 64;
-  static constexpr int HEADS = 64;        // heads per work-group
-  static constexpr int TOK = 16;          // tokens per slot
-  static constexpr int NS = 4;            // ring slots (two pairs)
-  static constexpr int LROW = DC * 2;     // bytes per latent row in LDS (pieces swizzled, see lat_swz)
-  static constexpr int HI = 0;                       // [16][LROW] latent, then bf16(c g)
-  static constexpr int LO = HI + TOK * LROW;         // [16][LROW] gate row, then c g - bf16(c g)
-  static constexpr int ROPE = LO + TOK * LROW;       // [16][128 B] RoPE keys, 16-byte pieces swizzled
-  static constexpr int SLOT = ROPE + TOK * DR * 2;   // bytes per slot
-  static constexpr int RING = NS * SLOT;
-  static constexpr int LIST = RING;                  // int2 (slot, id) per token
-  static constexpr int LISTCAP = 1024;               // tokens listed at a time (a multiple of 32)
-  static constexpr int QROPE = LIST + LISTCAP * 8;   // [NW][2 chunks][64 lanes] bf16x8: RoPE query (B operand)
-  static constexpr int LDS_BYTES = QROPE + NW * 2 * 64 * 16;
+  static constexpr int NV = 4;             // value waves (= score waves)
+  static constexpr int NW = 2 * NV;        // waves per work-group
+  static constexpr int NT = NW * 64;       // threads per work-group
+  static constexpr int HEADS = 64;         // heads per work-group
+  static constexpr int NHT = HEADS / 16;   // head tiles: one per value wave
+  static constexpr int DW = DC / NV;       // latent dims of a score wave / output dims of a value wave
+  static constexpr int NCH = DW / 32;      // 32-dim score chunks of a score wave
+  static constexpr int NRC = DR / 32;      // 32-dim RoPE chunks (value waves)
+  static constexpr int NDB = DW / 16;      // 16-dim value blocks of a value wave
+  static constexpr int TOK = 16;           // tokens per unit
+  static constexpr int NHB = 3;            // gated-tile buffers
+  // tile row: 512 gated dims + 32 bytes, so that the row stride is 8 banks
+  // (mod 64): the 16-byte row writes and the transposed 8-byte reads of 4
+  // rows are free of bank conflicts
+  static constexpr int TS = DC + 16;
+  static constexpr int HT = 0;                                // [NHB][16][TS] bf16: gated hi
+  static constexpr int SB = HT + NHB * TOK * TS * 2;          // [2][NV][NHT][64] f32x4: partial scores
+  static constexpr int PB = SB + 2 * NV * NHT * 64 * 16;      // [2][NHT][64] bf16 x 4: probabilities
+  static constexpr int AL = PB + 2 * NHT * 64 * 8;            // [2][16][NHT] f32: rescale factor of head 16 ht + r
+  static constexpr int FL = AL + 2 * HEADS * 4;               // [2][NHT] int: head tile rescaled
+  static constexpr int LIST = FL + 64;                        // int2 (slot, id) per token
+  static constexpr int LISTCAP = 4096;                        // tokens listed at a time
+  static constexpr int LDS_BYTES = LIST + LISTCAP * 8;
+  static_assert(NHT == NV && NHT == 4, "one head tile per value wave; 16-byte flag reads");
   static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
-  static_assert(SLOT % 16 == 0 && LIST % 16 == 0, "alignment");
+  static_assert(LISTCAP % NT == 0 && LISTCAP % TOK == 0, "list chunk");
+  static_assert(SB % 16 == 0 && PB % 16 == 0 && LIST % 16 == 0, "alignment");
 };
 
 // Balanced schedule of the wide kernel.  The batch's tokens, taken sequence
@@ -200,85 +173,33 @@ __device__ __forceinline__ void wide_block(int bid, int groups, int& range, int&
   range = (j / groups) * 8 + xcd;
 }
 
-__global__ __launch_bounds__(WideCfg::NT, 1) void split_wide_kernel(SplitArgs a) {
+// Walks this work-group's segments (its range's part of one sequence each)
+// and their list chunks: seg_begin(b) before the first chunk of sequence b's
+// segment, chunk(n, nunits) once the chunk's token list (n tokens, padded to
+// nunits units of 16 by repeating its last token) is in LDS, seg_end(b) after
+// the last chunk.  Every wave runs the same walk (the quantities it branches
+// on are uniform over the work-group).
+template <typename SegBegin, typename Chunk, typename SegEnd>
+__device__ __forceinline__ void wide_walk(const SplitArgs& a, int wg, int2* list, SegBegin seg_begin, Chunk chunk,
+                                          SegEnd seg_end) {
   using C = WideCfg;
-  constexpr int DC = C::DC, DQ = C::DQ, LROW = C::LROW;
-  __shared__ __attribute__((aligned(16))) unsigned char lds[C::LDS_BYTES];
-  const int2* list = reinterpret_cast<const int2*>(lds + C::LIST);
-  const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds));
-
-  int wg, hblk;
-  wide_block(blockIdx.x, a.groups, wg, hblk);
   const int64_t N = a.sched_hdr[0];
   const int Ge = static_cast<int>(a.sched_hdr[1]);
-  if (wg >= Ge) return;  // uniform over the work-group
   int64_t remaining = (static_cast<int64_t>(wg) + 1) * N / Ge - static_cast<int64_t>(wg) * N / Ge;
   int b = a.wg_start[wg].x, off = a.wg_start[wg].y;
-
-  const int tid = threadIdx.x, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
-  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int head0 = hblk * C::HEADS + 16 * w;  // first head of this wave
-
-  const uint16_t* __restrict__ cache = static_cast<const uint16_t*>(a.cache);
-  const uint16_t* __restrict__ gate = static_cast<const uint16_t*>(a.gate);
-  // latent / gate DMA of slot row 4w + k: lane l fetches logical piece l ^ lat_swz(4w + k)
-  uint32_t dma_off[4];
-#pragma unroll
-  for (int k = 0; k < 4; ++k) dma_off[k] = static_cast<uint32_t>(16 * (lane ^ lat_swz(4 * w + k)));
-  // RoPE DMA (lanes 0..31): lane l fills 16-byte position l % 8 of slot row
-  // 4w + l / 8 with logical piece (l % 8) ^ (row % 8)
-  const int rope_row = 4 * w + ((lane >> 3) & 3);
-  const uint32_t rope_src = static_cast<uint32_t>(2 * DC + 16 * ((lane & 7) ^ (rope_row & 7)));
-  // gating: lane l takes physical piece l of this wave's rows
-  const int off_gate = (4 * w) * LROW + 16 * lane;
-  // scores: lane (token r16, group g) reads logical piece 4 c + g of slot row r16
-  const int sa_x = g ^ lat_swz(r16);
-  const int off_sa = r16 * LROW + 16 * (sa_x & 3);                               // + 64 (c ^ (sa_x >> 2))
-  const int off_sr = C::ROPE + r16 * 128 + 16 * ((4 * 0 + g) ^ (r16 & 7));        // RoPE chunk 0
-  const int off_sr1 = C::ROPE + r16 * 128 + 16 * ((4 * 1 + g) ^ (r16 & 7));       // RoPE chunk 1
-  // values: lane r16 of group g reads dims 16 db + 4 (r16 % 4) .. + 3 of slot row
-  // 4g + r16 / 4 (logical piece 2 db + (r16 % 4) / 2, half r16 % 2)
-  const int tr_row = 4 * g + (r16 >> 2);
-  const int tr_f = lat_swz(tr_row);
-  const int tr_s = ((r16 & 3) >> 1) ^ (tr_f & 1);
-  const int off_tr = tr_row * LROW + 16 * tr_s + 8 * (r16 & 1);                    // + 32 (db ^ (tr_f >> 1))
-  const int tr_fh = tr_f >> 1;
-
-  bf16x8_t qh[16], ql[16];  // B operands: head r16, dims 8g .. 8g + 7 of each 32-dim chunk
-  bf16x8_t* qrope = reinterpret_cast<bf16x8_t*>(lds + C::QROPE) + w * 2 * 64 + lane;  // RoPE chunks c: [64 c]
-  f32x4_t o[32];                   // O^T[dim 16 db + 4g + i][head r16]
-  float m_run, l_run;              // head r16 (log2 domain); l: this lane's tokens
-
-  while (remaining > 0 && b < a.B) {  // one segment: this range's part of sequence b
+  const int tid = threadIdx.x;
+  while (remaining > 0 && b < a.B) {
     const int L = clamp_len(a.seq_lens[b], a.cap);
     const int take = static_cast<int>(min(static_cast<int64_t>(L - off), remaining));
     if (take > 0) {
-#pragma unroll
-      for (int db = 0; db < 32; ++db) o[db] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-      m_run = -INFINITY;
-      l_run = 0.f;
-      // query of this lane's head for sequence b, as the absorption wrote it:
-      // [q hi | q^R | q lo] in bf16
-      {
-        const uint16_t* qrow = reinterpret_cast<const uint16_t*>(a.qfull) +
-                               (static_cast<int64_t>(b) * a.H + head0 + r16) * (DC + DQ) + 8 * g;
-#pragma unroll
-        for (int c = 0; c < 16; ++c) {
-          qh[c] = *reinterpret_cast<const bf16x8_t*>(qrow + 32 * c);
-          ql[c] = *reinterpret_cast<const bf16x8_t*>(qrow + DQ + 32 * c);
-        }
-#pragma unroll
-        for (int c = 0; c < 2; ++c) qrope[64 * c] = *reinterpret_cast<const bf16x8_t*>(qrow + DC + 32 * c);  // own region
-      }
+      seg_begin(b);
       for (int c0 = 0; c0 < take; c0 += C::LISTCAP) {
         const int t0 = off + c0;
         const int n = min(C::LISTCAP, take - c0);
-        const int npairs = (n + 31) / 32;
-        // ---- token list: (slot, id) of positions t0 .. t0 + 32 npairs - 1 (past
-        // the segment the last token repeats; masked) ----
+        const int nunits = (n + C::TOK - 1) / C::TOK;
         {
           constexpr int PER = C::LISTCAP / C::NT;
-          const int npad = npairs * 32;
+          const int npad = nunits * C::TOK;
           const int nper = (npad + C::NT - 1) / C::NT;  // uniform
           int pp[PER], psl[PER], pid[PER];
 #pragma unroll
@@ -287,222 +208,295 @@ __global__ __launch_bounds__(WideCfg::NT, 1) void split_wide_kernel(SplitArgs a)
 #pragma unroll
           for (int e = 0; e < PER; ++e)
             if (e < nper) pid[e] = a.ids[psl[e]];
-          int2* lw = reinterpret_cast<int2*>(lds + C::LIST);
 #pragma unroll
           for (int e = 0; e < PER; ++e) {
             const int j = tid + e * C::NT;
-            if (e < nper && j < npad) lw[j] = make_int2(psl[e], clamp_id(pid[e], a.V));
+            if (e < nper && j < npad) list[j] = make_int2(psl[e], clamp_id(pid[e], a.V));
           }
         }
-        __syncthreads();  // the list is complete; every wave is done with the previous chunk's slots
-
-        // This wave's DMAs of pair p: tokens 4w .. 4w + 3 of slots 2p and 2p + 1,
-        // per slot 4 latent rows, 4 gate rows and one RoPE instruction (18 in
-        // all).  pair_entries reads the pair's list entries (wave-uniform, into
-        // scalar registers); dma_step(j) issues instruction j, so that the issue
-        // can be spread between the score products.  A pair index past the
-        // chunk takes the last pair's entries (its rows land in ring slots that
-        // are free, and are never read).
-        int psl[8], pid[8];
-        auto pair_entries = [&](int p) {
-          const int pe = min(p, npairs - 1);
-#pragma unroll
-          for (int k = 0; k < 2; ++k) {
-            const int4 e01 = reinterpret_cast<const int4*>(list)[(16 * (2 * pe + k) + 4 * w) / 2];
-            const int4 e23 = reinterpret_cast<const int4*>(list)[(16 * (2 * pe + k) + 4 * w) / 2 + 1];
-            psl[4 * k + 0] = __builtin_amdgcn_readfirstlane(e01.x);
-            psl[4 * k + 1] = __builtin_amdgcn_readfirstlane(e01.z);
-            psl[4 * k + 2] = __builtin_amdgcn_readfirstlane(e23.x);
-            psl[4 * k + 3] = __builtin_amdgcn_readfirstlane(e23.z);
-            pid[4 * k + 0] = __builtin_amdgcn_readfirstlane(e01.y);
-            pid[4 * k + 1] = __builtin_amdgcn_readfirstlane(e01.w);
-            pid[4 * k + 2] = __builtin_amdgcn_readfirstlane(e23.y);
-            pid[4 * k + 3] = __builtin_amdgcn_readfirstlane(e23.w);
-          }
-        };
-        auto dma_step = [&](int p, int j) {
-          const int k = j / 9, i = j % 9;  // slot 2p + k of the ring, instruction i
-          const uint32_t sb = lds0 + ((2 * p + k) % C::NS) * C::SLOT;
-          if (i < 4) {
-            lds_dma16(cache + static_cast<int64_t>(psl[4 * k + i]) * DQ, dma_off[i], sb + C::HI + (4 * w + i) * LROW);
-          } else if (i < 8) {
-            lds_dma16(gate + static_cast<int64_t>(pid[4 * k + i - 4]) * DC, dma_off[i - 4],
-                      sb + C::LO + (4 * w + i - 4) * LROW);
-          } else {
-            // RoPE keys of the 4 rows: lane l < 32 reads row 4w + l / 8 (its own list entry)
-            const int slk = list[16 * (2 * min(p, npairs - 1) + k) + rope_row].x;
-            const uint64_t addr = reinterpret_cast<uint64_t>(cache + static_cast<int64_t>(slk) * DQ) + rope_src;
-            if (lane < 32) lds_dma16_addr(addr, sb + C::ROPE + 4 * w * 128);
-          }
-        };
-
-        // gate this wave's rows of pair p in place: HI <- bf16(c g), LO <- c g - HI
-        // (per slot, the 8 reads of its 4 rows first, then the products)
-        auto gate_pair = [&](int p) {
-#pragma unroll
-          for (int k = 0; k < 2; ++k) {
-            unsigned char* sp = lds + ((2 * p + k) % C::NS) * C::SLOT + off_gate;
-            u32x4_t lat[4], gat[4];
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              lat[r] = *reinterpret_cast<const u32x4_t*>(sp + C::HI + r * LROW);
-              gat[r] = *reinterpret_cast<const u32x4_t*>(sp + C::LO + r * LROW);
-            }
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              u32x4_t hi, lo;
-              gate_chunk_hilo(lat[r], gat[r], hi, lo);
-              *reinterpret_cast<u32x4_t*>(sp + C::HI + r * LROW) = hi;
-              *reinterpret_cast<u32x4_t*>(sp + C::LO + r * LROW) = lo;
-            }
-            __builtin_amdgcn_sched_barrier(0);
-          }
-        };
-        // S^T[token 4g + q][head r16] of the pair's two slots (unscaled), on
-        // four accumulator chains (slot x query part) whose products alternate,
-        // so no product waits for the one before it.  The operands of chunk
-        // c + 1 are read while chunk c's products run, and nothing is hoisted
-        // further (every chunk's reads would otherwise be live at once).  Two of
-        // the next pair's DMAs go out with each of the first 9 chunks.
-        auto scores = [&](int s0, f32x4_t& sa, f32x4_t& sb, int pn) {
-          const unsigned char* spa = lds + (s0 % C::NS) * C::SLOT;
-          const unsigned char* spb = lds + ((s0 + 1) % C::NS) * C::SLOT;
-          f32x4_t a0 = {0.f, 0.f, 0.f, 0.f}, a1 = a0, b0 = a0, b1 = a0;
-          bf16x8_t ah[2], al[2], bh[2], bl[2];
-          auto rd = [&](int c) {
-            const int pc = off_sa + 64 * (c ^ (sa_x >> 2));
-            ah[c & 1] = *reinterpret_cast<const bf16x8_t*>(spa + C::HI + pc);
-            al[c & 1] = *reinterpret_cast<const bf16x8_t*>(spa + C::LO + pc);
-            bh[c & 1] = *reinterpret_cast<const bf16x8_t*>(spb + C::HI + pc);
-            bl[c & 1] = *reinterpret_cast<const bf16x8_t*>(spb + C::LO + pc);
-          };
-          rd(0);
-#pragma unroll
-          for (int c = 0; c < 16; ++c) {
-            if (c + 1 < 16) rd(c + 1);
-            if (c < 9) {
-              dma_step(pn, 2 * c);
-              dma_step(pn, 2 * c + 1);
-            }
-            __builtin_amdgcn_sched_barrier(0);
-            a0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[c & 1], qh[c], a0, 0, 0, 0);
-            b0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bh[c & 1], qh[c], b0, 0, 0, 0);
-            a1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[c & 1], ql[c], a1, 0, 0, 0);
-            b1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bh[c & 1], ql[c], b1, 0, 0, 0);
-            a0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[c & 1], qh[c], a0, 0, 0, 0);
-            b0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bl[c & 1], qh[c], b0, 0, 0, 0);
-            __builtin_amdgcn_sched_barrier(0);
-          }
-#pragma unroll
-          for (int c = 0; c < 2; ++c) {
-            const int off = c ? off_sr1 : off_sr;
-            const bf16x8_t ar = *reinterpret_cast<const bf16x8_t*>(spa + off);
-            const bf16x8_t br = *reinterpret_cast<const bf16x8_t*>(spb + off);
-            a1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ar, qrope[64 * c], a1, 0, 0, 0);
-            b1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(br, qrope[64 * c], b1, 0, 0, 0);
-          }
-          sa = a0 + a1;
-          sb = b0 + b1;
-        };
-
-        // Pair 0's DMAs go out now; pair p + 1's during the scores of pair p
-        // (into the slots of pair p - 1, free once every wave has passed pair
-        // p's barrier), so when iteration p starts, pair p's are the only loads
-        // in flight.
-        pair_entries(0);
-#pragma unroll
-        for (int j = 0; j < 18; ++j) dma_step(0, j);
-        for (int p = 0; p < npairs; ++p) {
-          wait_vmcnt<0>();
-          gate_pair(p);
-          lds_barrier();  // pair p gated and visible; every wave is done with pair p - 1
-          pair_entries(p + 1);
-          __builtin_amdgcn_sched_barrier(0);
-
-          f32x4_t sa, sb;
-          scores(2 * p, sa, sb, p + 1);
-          float x[8];
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            x[q] = sa[q] * a.scale_log2;
-            x[4 + q] = sb[q] * a.scale_log2;
-          }
-          const int nt = n - 32 * p;  // valid tokens of the pair (1..32)
-          if (nt < 32) {
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              if (4 * g + q >= nt) x[q] = -INFINITY;
-              if (16 + 4 * g + q >= nt) x[4 + q] = -INFINITY;
-            }
-          }
-          // online softmax of head r16 over the pair's 32 tokens
-          float mt = x[0];
-#pragma unroll
-          for (int q = 1; q < 8; ++q) mt = fmaxf(mt, x[q]);
-          mt = max_over_row_groups(mt);
-          const float m_new = fmaxf(m_run, mt);  // finite: the pair has a valid token
-          const bool grow = m_new > m_run + kLazyRescale;  // false while both are -inf
-          if (__builtin_amdgcn_ballot_w64(grow)) {
-            const float alpha = grow ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.0f;  // exp2(-inf) = 0
-            m_run = grow ? m_new : m_run;
-            l_run *= alpha;
-#pragma unroll
-            for (int db = 0; db < 32; ++db) o[db] *= alpha;
-          }
-          float pr[8];
-#pragma unroll
-          for (int q = 0; q < 8; ++q) {
-            pr[q] = __builtin_amdgcn_exp2f(x[q] - m_run);  // masked: exp2(-inf) = 0
-            l_run += pr[q];
-          }
-          // B operand: k = 8g + i <-> slot 2p token 4g + i (i < 4), slot 2p + 1 token 4g + i - 4
-          const bf16x8_t pb = __builtin_bit_cast(
-              bf16x8_t, u32x4_t{pack_bf16x2(pr[0], pr[1]), pack_bf16x2(pr[2], pr[3]), pack_bf16x2(pr[4], pr[5]),
-                                pack_bf16x2(pr[6], pr[7])});
-          // O^T += C~^T P^T, A operand: dim 16 db + r16 of the same 8 tokens
-          const unsigned char* sp0 = lds + ((2 * p) % C::NS) * C::SLOT + C::HI + off_tr;
-          const unsigned char* sp1 = lds + ((2 * p + 1) % C::NS) * C::SLOT + C::HI + off_tr;
-          // (the operands of block db + 3 are read while block db's product runs)
-          s16x4_t v0[4], v1[4];
-          auto rdv = [&](int db) {
-            const int pd = 32 * (db ^ tr_fh);
-            v0[db & 3] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t*)(sp0 + pd));
-            v1[db & 3] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t*)(sp1 + pd));
-          };
-          rdv(0);
-          rdv(1);
-          rdv(2);
-#pragma unroll
-          for (int db = 0; db < 32; ++db) {
-            if (db + 3 < 32) rdv(db + 3);
-            __builtin_amdgcn_sched_barrier(0);
-            const bf16x8_t av =
-                __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(v0[db & 3], v1[db & 3], 0, 1, 2, 3, 4, 5, 6, 7));
-            o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, pb, o[db], 0, 0, 0);
-            __builtin_amdgcn_sched_barrier(0);
-          }
-          __builtin_amdgcn_sched_barrier(0);
-        }
-        // the last pair's DMAs (issued past the chunk, never read) land before
-        // the list is rebuilt or the work-group exits
-        wait_vmcnt<0>();
+        __syncthreads();  // the list is complete; every wave is done with the previous chunk
+        chunk(n, nunits);
       }
-      // ---- partial result of this segment: this wave's 16 heads ----
-      const int64_t pbase = (static_cast<int64_t>(wg) + b) * a.H + head0;
-      const float l = sum_over_row_groups(l_run);
-      if (g == 0) {
-        __builtin_nontemporal_store(m_run, a.part_ml + (pbase + r16) * 2 + 0);
-        __builtin_nontemporal_store(l, a.part_ml + (pbase + r16) * 2 + 1);
-      }
-      float* obase = a.part_o + (pbase + r16) * DC + 4 * g;
-#pragma unroll
-      for (int db = 0; db < 32; ++db)
-        __builtin_nontemporal_store(o[db], reinterpret_cast<f32x4_t*>(obase + 16 * db));
+      seg_end(b);
     }
     remaining -= take > 0 ? take : 0;
     ++b;
     off = 0;
   }
+}
+
+// One wave's work in the split kernel: ROLE 0 = score wave s, ROLE 1 = value
+// wave t (the index is `idx`).  Every wave of the work-group walks the same
+// segments and chunks and meets the same barriers: one per unit, one more at
+// the end of each chunk.
+template <int ROLE, int D>
+__device__ __forceinline__ void wide_wave(const SplitArgs& a, unsigned char* lds, int wg, int hblk, int idx) {
+  using C = WideCfg;
+  constexpr int DC = C::DC, DQ = C::DQ, DW = C::DW, NHT = C::NHT, NV = C::NV, TS = C::TS, TOK = C::TOK;
+  constexpr int NCH = C::NCH, NDB = C::NDB, NRC = C::NRC;
+  constexpr int QROW = DC + DQ;  // absorbed query row: [q hi | q^R | q lo]
+  int2* list = reinterpret_cast<int2*>(lds + C::LIST);
+  f32x4_t* sbuf = reinterpret_cast<f32x4_t*>(lds + C::SB);  // [2][NV][NHT][64]
+  s16x4_t* pbuf = reinterpret_cast<s16x4_t*>(lds + C::PB);  // [2][NHT][64]
+  float* abuf = reinterpret_cast<float*>(lds + C::AL);      // [2][16][NHT]
+  int* fbuf = reinterpret_cast<int*>(lds + C::FL);          // [2][NHT]
+  auto htile = [&](int h) { return reinterpret_cast<uint16_t*>(lds + C::HT) + h * TOK * TS; };
+
+  const int lane = threadIdx.x & 63, r16 = lane & 15, g = lane >> 4;
+  const uint16_t* __restrict__ cache = static_cast<const uint16_t*>(a.cache);
+  const uint16_t* __restrict__ gate = static_cast<const uint16_t*>(a.gate);
+  const uint16_t* __restrict__ qfull = reinterpret_cast<const uint16_t*>(a.qfull);
+  const int64_t qbase = static_cast<int64_t>(hblk) * C::HEADS + r16;  // + b H: query row of head r16 of tile 0
+  const int dcol = DW * idx + 8 * g;  // score waves: this lane's first dim of chunk 0
+
+  if constexpr (ROLE == 0) {
+    // ======================= score wave s = idx =======================
+    bf16x8_t qh[NCH][NHT], ql[NCH][NHT];  // B operands: head 16 ht + r16, dims 8g .. 8g + 7 of chunk c
+    struct Unit {
+      u32x4_t lat[NCH];
+      u32x4_t gat[NCH];
+    };
+    auto seg_begin = [&](int b) {
+#pragma unroll
+      for (int ht = 0; ht < NHT; ++ht) {
+        const uint16_t* qrow = qfull + (static_cast<int64_t>(b) * a.H + qbase + 16 * ht) * QROW + dcol;
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+          qh[c][ht] = *reinterpret_cast<const bf16x8_t*>(qrow + 32 * c);
+          ql[c][ht] = *reinterpret_cast<const bf16x8_t*>(qrow + DQ + 32 * c);
+        }
+      }
+    };
+    auto chunk = [&](int, int nunits) {
+      // Rows of the unit being refilled (a unit past the chunk takes the last
+      // unit's rows, never used, so that every step issues the same loads);
+      // the list entry is read one unit ahead.
+      int2 e_next = list[r16];
+      const uint16_t* crow = nullptr;
+      const uint16_t* grow = nullptr;
+      auto next_rows = [&](int u) {
+        const int2 e = e_next;
+        e_next = list[TOK * min(u + 1, nunits - 1) + r16];
+        crow = cache + static_cast<int64_t>(e.x) * DQ + dcol;
+        grow = gate + static_cast<int64_t>(e.y) * DC + dcol;
+      };
+      auto issue_chunk = [&](Unit& U, int c) {
+        U.lat[c] = *reinterpret_cast<const u32x4_t*>(crow + 32 * c);
+        U.gat[c] = *reinterpret_cast<const u32x4_t*>(grow + 32 * c);
+      };
+      auto step = [&](Unit& U, int u) {
+        uint16_t* tw = htile(u % C::NHB) + r16 * TS + dcol;
+        f32x4_t acc[NHT];
+#pragma unroll
+        for (int ht = 0; ht < NHT; ++ht) acc[ht] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        next_rows(u + D);
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+          u32x4_t hi, lo;
+          gate_chunk_hilo(U.lat[c], U.gat[c], hi, lo);
+          issue_chunk(U, c);  // unit u + D into the registers just consumed
+          *reinterpret_cast<u32x4_t*>(tw + 32 * c) = hi;
+          const bf16x8_t h = __builtin_bit_cast(bf16x8_t, hi), l = __builtin_bit_cast(bf16x8_t, lo);
+#pragma unroll
+          for (int ht = 0; ht < NHT; ++ht)
+            acc[ht] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(h, qh[c][ht], acc[ht], 0, 0, 0);
+#pragma unroll
+          for (int ht = 0; ht < NHT; ++ht)
+            acc[ht] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(l, qh[c][ht], acc[ht], 0, 0, 0);
+#pragma unroll
+          for (int ht = 0; ht < NHT; ++ht)
+            acc[ht] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(h, ql[c][ht], acc[ht], 0, 0, 0);
+        }
+        const int k = u & 1;
+#pragma unroll
+        for (int ht = 0; ht < NHT; ++ht) sbuf[((k * NV + idx) * NHT + ht) * 64 + lane] = acc[ht];
+        lds_barrier();  // barrier u: partials and gated tile of unit u visible
+      };
+      Unit ring[D];
+#pragma unroll
+      for (int u = 0; u < D; ++u) {
+        next_rows(u);
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) issue_chunk(ring[u], c);
+      }
+      // Full groups of D units (ring slot u holds units u, u + D, ...), then
+      // the remaining nunits % D straight-line, so that on every path the
+      // same units are in flight in the same order.
+      const int nfull = nunits / D;
+      for (int i0 = 0; i0 < nfull * D; i0 += D) {
+#pragma unroll
+        for (int u = 0; u < D; ++u) {
+          __builtin_amdgcn_sched_barrier(0);
+          step(ring[u], i0 + u);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < D - 1; ++u) {
+        __builtin_amdgcn_sched_barrier(0);
+        if (nfull * D + u < nunits) step(ring[u], nfull * D + u);
+      }
+      lds_barrier();  // the value waves' last probabilities
+    };
+    wide_walk(a, wg, list, seg_begin, chunk, [](int) {});
+  } else {
+    // ======================= value wave t = idx =======================
+    bf16x8_t qr[NRC];                      // RoPE B operands: head 16 t + r16, dims 8g .. 8g + 7 of chunk c
+    f32x4_t o[NDB][NHT];                   // O^T[dim 128 t + 16 db + 4g + i][head 16 ht + r16]
+    float m_run = -INFINITY, l_run = 0.f;  // head 16 t + r16 (log2 domain); l: this lane's tokens
+    struct Unit {
+      u32x4_t rop[NRC];  // RoPE key of token r16: dims 8g .. 8g + 7 of each chunk
+    };
+    auto seg_begin = [&](int b) {
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int ht = 0; ht < NHT; ++ht) o[db][ht] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      m_run = -INFINITY;
+      l_run = 0.f;
+      const uint16_t* qrow = qfull + (static_cast<int64_t>(b) * a.H + qbase + 16 * idx) * QROW + DC + 8 * g;
+#pragma unroll
+      for (int c = 0; c < NRC; ++c) qr[c] = *reinterpret_cast<const bf16x8_t*>(qrow + 32 * c);
+    };
+    auto chunk = [&](int n, int nunits) {
+      auto issue = [&](Unit& U, int u) {
+        const int sl = list[TOK * min(u, nunits - 1) + r16].x;
+        const uint16_t* kr = cache + static_cast<int64_t>(sl) * DQ + DC + 8 * g;
+#pragma unroll
+        for (int c = 0; c < NRC; ++c) U.rop[c] = *reinterpret_cast<const u32x4_t*>(kr + 32 * c);
+      };
+      // O^T += C~^T P^T for unit u (its probabilities written before the last
+      // barrier); the LDS operands of a batch are read before any is used
+      auto values = [&](int u) {
+        const int k = u & 1;
+        const int4 fl = *reinterpret_cast<const int4*>(fbuf + k * NHT);
+        const float4 al = *reinterpret_cast<const float4*>(abuf + (k * 16 + r16) * NHT);
+        s16x4_t pb[NHT];
+#pragma unroll
+        for (int ht = 0; ht < NHT; ++ht) pb[ht] = pbuf[(k * NHT + ht) * 64 + lane];
+        // lane r16 of group g reads dims 16 db + 4 (r16 % 4) .. + 3 of token
+        // 4g + r16 / 4; the transposed read hands it dim 16 db + r16 of tokens 4g .. 4g + 3
+        const uint16_t* tr = htile(u % C::NHB) + (4 * g + (r16 >> 2)) * TS + DW * idx + 4 * (r16 & 3);
+        const int fls[NHT] = {fl.x, fl.y, fl.z, fl.w};
+        const float als[NHT] = {al.x, al.y, al.z, al.w};
+#pragma unroll
+        for (int d0 = 0; d0 < NDB; d0 += 4) {
+          s16x4_t at[4];
+#pragma unroll
+          for (int d = 0; d < 4; ++d)
+            at[d] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) s16x4_t*)(tr + 16 * (d0 + d)));
+          __builtin_amdgcn_sched_barrier(0);
+          if (d0 == 0) {
+#pragma unroll
+            for (int ht = 0; ht < NHT; ++ht) {
+              if (__builtin_amdgcn_readfirstlane(fls[ht])) {
+#pragma unroll
+                for (int db = 0; db < NDB; ++db) o[db][ht] *= als[ht];
+              }
+            }
+          }
+#pragma unroll
+          for (int d = 0; d < 4; ++d)
+#pragma unroll
+            for (int ht = 0; ht < NHT; ++ht)
+              o[d0 + d][ht] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(at[d], pb[ht], o[d0 + d][ht], 0, 0, 0);
+        }
+      };
+      // after barrier u: the softmax of head tile t over unit u, then the
+      // values of unit u - 1
+      auto step = [&](Unit& U, int u) {
+        lds_barrier();  // barrier u
+        const int k = u & 1;
+        // RoPE part of the scores, then this head tile's partials
+        f32x4_t sc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int c = 0; c < NRC; ++c)
+          sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, U.rop[c]), qr[c], sc, 0, 0, 0);
+        issue(U, u + D);
+        f32x4_t sv[NV];
+#pragma unroll
+        for (int v = 0; v < NV; ++v) sv[v] = sbuf[((k * NV + v) * NHT + idx) * 64 + lane];
+        __builtin_amdgcn_sched_barrier(0);
+        sc += (sv[0] + sv[1]) + (sv[2] + sv[3]);
+        float x[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) x[q] = sc[q] * a.scale_log2;
+        const int nt = n - TOK * u;  // valid tokens of the unit (>= 1)
+        if (nt < TOK) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            if (4 * g + q >= nt) x[q] = -INFINITY;
+        }
+        const float mt = max_over_row_groups(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));
+        const float m_new = fmaxf(m_run, mt);  // finite: the unit has a valid token
+        const bool grow = m_new > m_run + kLazyRescale;  // false while both are -inf
+        const float alpha = grow ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.0f;  // exp2(-inf) = 0
+        m_run = grow ? m_new : m_run;
+        l_run *= alpha;
+        float p[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          p[q] = __builtin_amdgcn_exp2f(x[q] - m_run);  // masked: exp2(-inf) = 0
+          l_run += p[q];
+        }
+        // B operand of the value product: k = token 4g + i, j = head r16
+        pbuf[(k * NHT + idx) * 64 + lane] =
+            __builtin_bit_cast(s16x4_t, u32x2_t{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3])});
+        if (g == 0) abuf[(k * 16 + r16) * NHT + idx] = alpha;
+        const uint64_t any = __builtin_amdgcn_ballot_w64(grow);
+        if (lane == 0) fbuf[k * NHT + idx] = any != 0;
+        if (u > 0) values(u - 1);
+      };
+      Unit ring[D];
+#pragma unroll
+      for (int u = 0; u < D; ++u) issue(ring[u], u);
+      const int nfull = nunits / D;
+      for (int i0 = 0; i0 < nfull * D; i0 += D) {
+#pragma unroll
+        for (int u = 0; u < D; ++u) {
+          __builtin_amdgcn_sched_barrier(0);
+          step(ring[u], i0 + u);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < D - 1; ++u) {
+        __builtin_amdgcn_sched_barrier(0);
+        if (nfull * D + u < nunits) step(ring[u], nfull * D + u);
+      }
+      lds_barrier();  // probabilities of the last unit visible
+      values(nunits - 1);
+    };
+    auto seg_end = [&](int b) {
+      const int64_t pbase = (static_cast<int64_t>(wg) + b) * a.H + hblk * C::HEADS;
+#pragma unroll
+      for (int ht = 0; ht < NHT; ++ht) {
+        float* orow = a.part_o + (pbase + 16 * ht + r16) * DC + DW * idx + 4 * g;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db)
+          __builtin_nontemporal_store(o[db][ht], reinterpret_cast<f32x4_t*>(orow + 16 * db));
+      }
+      const float l = sum_over_row_groups(l_run);
+      if (g == 0) {
+        __builtin_nontemporal_store(m_run, a.part_ml + (pbase + 16 * idx + r16) * 2 + 0);
+        __builtin_nontemporal_store(l, a.part_ml + (pbase + 16 * idx + r16) * 2 + 1);
+      }
+    };
+    wide_walk(a, wg, list, seg_begin, chunk, seg_end);
+  }
+}
+
+// Units of 16 tokens in flight per wave (its registers).
+template <int D>
+__global__ __launch_bounds__(WideCfg::NT, 1) void split_wide_kernel(SplitArgs a) {
+  __shared__ __attribute__((aligned(16))) unsigned char lds[WideCfg::LDS_BYTES];
+  int wg, hblk;
+  wide_block(blockIdx.x, a.groups, wg, hblk);
+  if (wg >= static_cast<int>(a.sched_hdr[1])) return;  // uniform over the work-group
+  const int w = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+  if (w < WideCfg::NV)
+    wide_wave<0, D>(a, lds, wg, hblk, w);
+  else
+    wide_wave<1, D>(a, lds, wg, hblk, w - WideCfg::NV);
 }
 
 }  // namespace egmla
