@@ -15,6 +15,9 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
+#include <chrono>
+#include <cstdlib>
 #include <cfloat>
 #include <cmath>
 #include <mutex>
@@ -107,6 +110,13 @@ struct SplitArgs {
   int64_t num_slots;
   int B, H, DC, DR, P, max_pages, V, cap, split, s_max, groups, hpg;
   float scale_log2;           // softmax scale * log2(e)
+  // Absorption inside the d_c 128 split kernel (null qin: a kernel of its own ran before)
+  const uint16_t* qin;        // query [B, H, DH + DR] (bf16)
+  const uint16_t* w_uk;       // W_UK [H, DH, DC] (bf16)
+  unsigned long long* qflags; // [B, groups, s_max]: stamp of the call whose absorbed heads a split has stored
+  unsigned long long stamp;   // this call's stamp (never 0, never repeated within the process)
+  int DH;
+  int spin_limit;             // polls of the stamps before a work-group absorbs every head itself
 };
 
 // ---------------------------------------------------------------------------
@@ -375,10 +385,35 @@ hipError_t launch_slice(const SplitArgs& a, int slices, int nblocks, hipStream_t
   if (slices == kIdSlices)
     hipExtLaunchKernelGGL((split_slice_kernel<DC, DR, kSliceWaves, kSliceDepth, kIdSlices>), dim3(nblocks * slices),
                           dim3(kSliceWaves * 64), 0, stream, ev0, ev1, 0, a);
+  else if (a.qin)
+    hipExtLaunchKernelGGL((split_slice_kernel<DC, DR, kSliceWaves, kSliceDepth, 1, true>), dim3(nblocks),
+                          dim3(kSliceWaves * 64), 0, stream, ev0, ev1, 0, a);
   else
     hipExtLaunchKernelGGL((split_slice_kernel<DC, DR, kSliceWaves, kSliceDepth, 1>), dim3(nblocks),
                           dim3(kSliceWaves * 64), 0, stream, ev0, ev1, 0, a);
   return hipGetLastError();
+}
+
+// Stamp of a decode call whose split kernel absorbs the query: distinct for
+// every call of the process and never 0, so that no stamp left in a
+// workspace by an earlier call (or found in fresh memory, but for a chance of
+// 2^-64 per stamp) matches.  The first value is drawn from the clock and the
+// address space layout.
+unsigned long long next_stamp() {
+  static std::atomic<unsigned long long> counter{
+      (static_cast<unsigned long long>(std::chrono::steady_clock::now().time_since_epoch().count()) * 0x9E3779B97F4A7C15ull) ^
+      reinterpret_cast<uintptr_t>(&counter)};
+  unsigned long long v;
+  do v = counter.fetch_add(1, std::memory_order_relaxed) + 1; while (v == 0);
+  return v;
+}
+
+// Polls of the absorption stamps before a work-group absorbs the query itself
+// (a few milliseconds); EGMLA_SPIN_LIMIT overrides it (0: always absorb locally).
+int absorb_spin_limit() {
+  const char* e = std::getenv("EGMLA_SPIN_LIMIT");
+  if (e && *e) return std::max(0, std::atoi(e));
+  return 1 << 16;
 }
 
 // Balanced head-split kernel: `ranges` token ranges x a.groups blocks of 64 heads.
@@ -475,8 +510,8 @@ eg_mla_status run_decode(const eg_mla_dims& d, const DecodePlan& p, int32_t batc
                        wide_groups(p.head_groups), sched_hdr, wg_start, seq_rows);
     if (hipGetLastError() != hipSuccess) return EG_MLA_ERR_HIP;
   }
-  // 1. absorption
-  {
+  // 1. absorption (or inside the split kernel)
+  if (!p.fused_absorb) {
     dim3 grid(d.num_heads, (d.latent_dim + kAbsorbCols - 1) / kAbsorbCols, (batch + kAbsorbRows - 1) / kAbsorbRows);
     const size_t lds = sizeof(float) * (kAbsorbRows * d.head_dim + 4 * kAbsorbRows * kAbsorbCols);
     if (bf && d.head_dim == 128) {
@@ -544,6 +579,19 @@ eg_mla_status run_decode(const eg_mla_dims& d, const DecodePlan& p, int32_t batc
     a.groups = p.head_groups;
     a.hpg = p.heads_per_group;
     a.scale_log2 = softmax_scale(d) * kLog2e;
+    a.qin = nullptr;
+    a.w_uk = nullptr;
+    a.qflags = nullptr;
+    a.stamp = 0;
+    a.DH = d.head_dim;
+    a.spin_limit = 0;
+    if (p.fused_absorb) {
+      a.qin = static_cast<const uint16_t*>(q);
+      a.w_uk = static_cast<const uint16_t*>(w_uk);
+      a.qflags = reinterpret_cast<unsigned long long*>(ws + p.off_flags);
+      a.stamp = next_stamp();
+      a.spin_limit = absorb_spin_limit();
+    }
     hipEvent_t ev0 = plan ? static_cast<hipEvent_t>(plan->split_start_event) : nullptr;
     hipEvent_t ev1 = plan ? static_cast<hipEvent_t>(plan->split_stop_event) : nullptr;
     if (launch_split(d, p, a, stream, ev0, ev1) != hipSuccess) return EG_MLA_ERR_HIP;

@@ -117,6 +117,11 @@ eg_mla_status make_decode_plan(const eg_mla_dims& d, int32_t batch, int32_t max_
     p.off_sched = off;
     off = align_up(off + 16 + kWideMaxGroups * 8 + B * 8);
   }
+  p.fused_absorb = sliced_kernel && p.slices == 1 && d.head_dim == 128;
+  if (p.fused_absorb) {
+    p.off_flags = off;
+    off = align_up(off + B * static_cast<size_t>(p.head_groups) * static_cast<size_t>(p.s_max) * 8);
+  }
   p.bytes = std::max<size_t>(off, kAlign);
   *out = p;
   return EG_MLA_OK;

@@ -46,11 +46,13 @@ struct DecodePlan {
   int heads_per_group = 0;
   int slices = 1;               // partials per (b, split, head group): token-id slices of the sliced kernel
   bool balanced = false;        // head-split kernel: balanced schedule (split_tokens = list chunk)
+  bool fused_absorb = false;    // d_c 128 split kernel absorbs the query itself (no id slices, d_h 128)
   // workspace layout (byte offsets)
   size_t off_q = 0;     // fp32 [B, H, d_c + d_r]  absorbed query | RoPE query
   size_t off_ml = 0;    // fp32 [rows, H, 2]   running max (log2 domain), sum
   size_t off_o = 0;     // fp32 [rows, H, d_c] unnormalised latent outputs
   size_t off_sched = 0; // balanced schedule: int64 [2] header, int2 [kWideMaxGroups] starts, int2 [B] rows
+  size_t off_flags = 0; // fused absorption: uint64 [B, head_groups, s_max] stamps
   size_t bytes = 0;     // rows: B * s_max * slices, or kWideMaxGroups + B when balanced
 };
 

@@ -122,7 +122,70 @@ __device__ __forceinline__ void split_slots(const SplitArgs& a, int b, int t0, c
   }
 }
 
-template <int DC, int DR, int NW, int D, int SL>
+// Absorption of one head inside the split kernel (256 threads, d_h = d_c =
+// 128): q_lat[b][h][c] = sum_k q^C[b][h][k] W_UK[h][k][c].  Thread t takes
+// columns 8 (t % 16) .. + 7 over rows 8 (t / 16) .. + 7 (exact bf16 products,
+// fp32 sums); the 16 row groups are added in LDS (red: 16 x 128 floats) in a
+// fixed order, so every work-group that absorbs a head produces the same
+// bits.  Threads t < 128 store column t with device-coherent stores (they
+// bypass this XCD's L2), for work-groups on any XCD to read once the stamp of
+// this work-group says they are complete.
+struct AbsorbRegs {
+  u32x4_t wv[8];  // W_UK rows 8 (t / 16) .. + 7, columns 8 (t % 16) .. + 7
+  u32x4_t qv;     // q^C[8 (t / 16) .. + 7]
+};
+__device__ __forceinline__ void absorb_load(const SplitArgs& a, int b, int h, AbsorbRegs& r) {
+  constexpr int DH = 128, DCa = 128;
+  const int tid = threadIdx.x, cg = tid & 15, kg = tid >> 4;
+  const uint16_t* wrow = a.w_uk + (static_cast<int64_t>(h) * DH + 8 * kg) * DCa + 8 * cg;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) r.wv[k] = *reinterpret_cast<const u32x4_t*>(wrow + k * DCa);
+  r.qv = *reinterpret_cast<const u32x4_t*>(a.qin + (static_cast<int64_t>(b) * a.H + h) * (DH + a.DR) + 8 * kg);
+}
+__device__ __forceinline__ void absorb_finish(const SplitArgs& a, int b, int h, const AbsorbRegs& ar, float* red) {
+  constexpr int DH = 128, DCa = 128;
+  const int tid = threadIdx.x, cg = tid & 15, kg = tid >> 4;
+  const u32x4_t* wv = ar.wv;
+  const u32x4_t qv = ar.qv;
+  float acc[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = 0.f;
+#pragma unroll
+  for (int r = 0; r < 8; ++r) {
+    const float qk = (r & 1) ? bf16_hi(qv[r >> 1]) : bf16_lo(qv[r >> 1]);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] = fmaf(qk, (i & 1) ? bf16_hi(wv[r][i >> 1]) : bf16_lo(wv[r][i >> 1]), acc[i]);
+  }
+  *reinterpret_cast<float4*>(red + kg * DCa + 8 * cg) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+  *reinterpret_cast<float4*>(red + kg * DCa + 8 * cg + 4) = make_float4(acc[4], acc[5], acc[6], acc[7]);
+  __syncthreads();
+  if (tid < DCa) {
+    float v = 0.f;
+#pragma unroll
+    for (int k = 0; k < DH / 8; ++k) v += red[k * DCa + tid];
+    float* qf = const_cast<float*>(a.qfull) + (static_cast<int64_t>(b) * a.H + h) * (a.DC + a.DR) + tid;
+    __hip_atomic_store(qf, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();  // red is free again
+}
+__device__ __forceinline__ void absorb_head_128(const SplitArgs& a, int b, int h, float* red) {
+  AbsorbRegs r;
+  absorb_load(a, b, h, r);
+  absorb_finish(a, b, h, r, red);
+}
+
+// FUSED (no id slices, d_h = 128): the work-groups of a sequence also absorb
+// its query.  Split s of the ns non-empty splits of sequence b absorbs the heads
+// j (of its group of 16) with j = s mod ns: their W_UK rows load with the page
+// table entries, the products are formed and stored device-coherently
+// before the token ids are loaded, and once the ids are in (vector memory
+// operations complete in issue order, so the stores are then complete) the
+// work-group publishes the call's stamp in qflags[b][group][s].  Before its first scores a work-group waits for the
+// stamps of splits 0 .. min(ns, 16) - 1 (the other work-groups of the
+// sequence run at the same time: one work-group per compute unit), polling at
+// most spin_limit times; if one is missing it absorbs all 16 heads itself
+// (the same bits), so the wait always ends.
+template <int DC, int DR, int NW, int D, int SL, bool FUSED = false>
 __global__ __launch_bounds__(NW * 64, 2) void split_slice_kernel(SplitArgs a) {
   using Cfg = SsplitCfg<DC, DR, NW>;
   constexpr int NC = Cfg::NC, NR = Cfg::NR, NB = Cfg::NB, DQ = Cfg::DQ, TS = Cfg::TS;
@@ -217,11 +280,28 @@ __global__ __launch_bounds__(NW * 64, 2) void split_slice_kernel(SplitArgs a) {
     int pp[PER], psl[PER], pid[PER];
 #pragma unroll
     for (int e = 0; e < PER; ++e) pp[e] = min(tid + e * NW * 64, n - 1);
+    // FUSED: this split's heads j = s, s + ns, ... < 16 of the group; the
+    // W_UK rows of the first two load together with the page table entries
+    const int ns = (L + a.split - 1) / a.split;  // non-empty splits of sequence b (s < ns)
+    AbsorbRegs pre[FUSED ? 2 : 1];
+    if constexpr (FUSED) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        if (s + i * ns < 16) absorb_load(a, b, hg * 16 + s + i * ns, pre[i]);
+    }
     split_slots(a, b, t0, pp, psl, nper);
+    if constexpr (FUSED) {
+      // (the LDS list is written after this)
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        if (s + i * ns < 16) absorb_finish(a, b, hg * 16 + s + i * ns, pre[i], reinterpret_cast<float*>(lds));
+      for (int j = s + 2 * ns; j < 16; j += ns) absorb_head_128(a, b, hg * 16 + j, reinterpret_cast<float*>(lds));
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);  // the stores above are issued before the loads below
+    }
 #pragma unroll
     for (int e = 0; e < PER; ++e)
       if (e < nper) pid[e] = a.ids[psl[e]];
-    load_q();
+    if constexpr (!FUSED) load_q();
     // The rows of this wave's first D units need no token id: issue them now,
     // after the ids (loads complete in issue order), so they stream while the
     // ids are on their way.
@@ -242,6 +322,18 @@ __global__ __launch_bounds__(NW * 64, 2) void split_slice_kernel(SplitArgs a) {
       }
     }
     ntok = n;
+    if constexpr (FUSED) {
+      if (s < 16) {
+        // Only the first rows' D * NRL loads, issued last, may still be in
+        // flight: this thread's absorbed stores, issued before its ids, are
+        // complete.  Then the stamp goes out.
+        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(D * NRL) : "memory");
+        __syncthreads();
+        if (tid == 0)
+          __hip_atomic_store(a.qflags + (static_cast<int64_t>(b) * a.groups + hg) * a.s_max + s, a.stamp,
+                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
   } else {
     // ---- phase 1a: slots and ids of this wave's scan rows (all loads first) ----
     const int nrows = (n + 255) / 256;
@@ -327,6 +419,55 @@ __global__ __launch_bounds__(NW * 64, 2) void split_slice_kernel(SplitArgs a) {
   // query chunks: absorbed query as bf16 hi + lo, RoPE query (a stored bf16 value: exact)
   bf16x8_t qh[NC], ql[NC];
   bf16x8_t qr[NR > 0 ? NR : 1];
+  if constexpr (FUSED) {
+    __syncthreads();  // the list is complete (and the absorption's LDS is free)
+    const int ns = (L + a.split - 1) / a.split;
+    const int np = min(ns, 16);
+    int* okp = reinterpret_cast<int*>(mbuf);
+    if (w == 0) {
+      const unsigned long long* fl = a.qflags + (static_cast<int64_t>(b) * a.groups + hg) * a.s_max;
+      bool ok = false;
+      for (int it = 0;; ++it) {
+        const unsigned long long v =
+            lane < np ? __hip_atomic_load(fl + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : a.stamp;
+        ok = __builtin_amdgcn_ballot_w64(v != a.stamp) == 0;
+        if (ok || it >= a.spin_limit) break;
+        __builtin_amdgcn_s_sleep(4);
+      }
+      if (lane == 0) okp[0] = ok ? 1 : 0;
+    }
+    __syncthreads();
+    if (okp[0] == 0) {
+      // a producer has not run yet: absorb the group's 16 heads here
+      for (int j = 0; j < 16; ++j) absorb_head_128(a, b, hg * 16 + j, reinterpret_cast<float*>(tile_all));
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __syncthreads();
+    }
+    // latent part: device-coherent 16-byte loads of the absorbed rows; RoPE
+    // part straight from the query
+    const int h = hg * 16 + r16;
+    const __amdgpu_buffer_rsrc_t rq = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(a.qfull), 0, static_cast<int>(static_cast<int64_t>(a.B) * a.H * (DC + DR) * 4), 0x00020000);
+    const int qoff = static_cast<int>(((static_cast<int64_t>(b) * a.H + h) * (DC + DR) + 8 * g) * 4);
+    f32x4_t xq[2 * NC];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      xq[2 * c] = __builtin_amdgcn_raw_buffer_load_b128(rq, qoff + 128 * c, 0, 16);
+      xq[2 * c + 1] = __builtin_amdgcn_raw_buffer_load_b128(rq, qoff + 128 * c + 16, 0, 16);
+    }
+    const uint16_t* qrr = a.qin + (static_cast<int64_t>(b) * a.H + h) * (a.DH + DR) + a.DH + 8 * g;
+#pragma unroll
+    for (int c = 0; c < NR; ++c) qr[c] = *reinterpret_cast<const bf16x8_t*>(qrr + 32 * c);
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float x = xq[2 * c + (e >> 2)][e & 3];
+        qh[c][e] = static_cast<__bf16>(x);
+        ql[c][e] = static_cast<__bf16>(x - static_cast<float>(qh[c][e]));
+      }
+    }
+  } else {
 #pragma unroll
   for (int c = 0; c < NC + NR; ++c) {
     const float x[8] = {qraw[2 * c].x, qraw[2 * c].y, qraw[2 * c].z, qraw[2 * c].w,
@@ -340,6 +481,7 @@ __global__ __launch_bounds__(NW * 64, 2) void split_slice_kernel(SplitArgs a) {
         qr[c - NC][e] = static_cast<__bf16>(x[e]);
       }
     }
+  }
   }
   __syncthreads();
 

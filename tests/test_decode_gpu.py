@@ -218,6 +218,29 @@ def test_repeatable_bitwise(gpu):
     assert np.array_equal(outs[0], outs[1]) and np.array_equal(outs[0], outs[2])
 
 
+@pytest.mark.parametrize("lens", [(1500, 700, 3, 4096), (512, 513, 0, 1)])
+def test_fused_absorption_fallback_same_bits(gpu, monkeypatch, lens):
+    """On the d_c 128 path the split kernel absorbs the query itself: each
+    non-empty split of a sequence absorbs a share of its heads and publishes a
+    stamp; a work-group that does not see every stamp within its poll limit
+    absorbs all 16 heads itself.  Forcing that path from the host (a limit of
+    0 polls) must give the same bits as the shared absorption, and both the
+    oracle's result.  The lengths give 3, 2, 1 and 8 non-empty splits of 512
+    tokens, one sequence of a single token and an empty one."""
+    wl = W.WORKLOADS[1].replace(batch=len(lens), seq_len=4096)
+    inp = W.generate(wl, seq_lens=np.array(lens, dtype=np.int32))
+    dd = B.stage_decode(inp)
+    say(f"decode fused absorption shared, lens={lens}")
+    B.run_decode(dd)
+    shared = B.out_to_f64(dd.out).copy()
+    monkeypatch.setenv("EGMLA_SPIN_LIMIT", "0")
+    say(f"decode fused absorption local, lens={lens}")
+    B.run_decode(dd)
+    local = B.out_to_f64(dd.out).copy()
+    assert np.array_equal(shared, local)
+    assert_close(shared, oracle_decode(inp), "bf16", "fused absorption")
+
+
 def test_split_choice_changes_result_within_tolerance(gpu):
     inp = full_inputs(2)
     ref = full_ref(2)
