@@ -131,6 +131,30 @@ eg_mla_status eg_mla_append(const eg_mla_dims* dims, int32_t n_tokens, int32_t h
                             int32_t* token_id_cache, int64_t num_slots, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * Append with a workspace: the same operation and arguments as eg_mla_append
+ * (Sec. 3.1 Eq. (1); App. C Eq. (C.10)), the same rows and ids, for calls
+ * of few tokens.  With bf16 storage, d_c = 128, d_r = 64, hidden a multiple
+ * of 256 and 1..2048 tokens, the hidden dimension is cut into 256-wide
+ * slices over many work-groups: pass 1 stores fp32 partial sums of W_DKV x_i
+ * per slice in the workspace ([hidden/256, n_tokens, d_c + d_r]), pass 2 adds
+ * them in slice order, applies the RMSNorm and RoPE and writes the rows.  Any
+ * other call runs eg_mla_append (the workspace is not touched).
+ *
+ *   workspace  at least eg_mla_append_workspace_size(dims, n_tokens, hidden)
+ *              bytes, 256-byte aligned, no initialisation needed; calls that
+ *              share it must be ordered.  Too small or misaligned:
+ *              EG_MLA_ERR_WORKSPACE before any launch.
+ * eg_mla_append_workspace_size returns 0 for invalid dims or sizes.
+ * ------------------------------------------------------------------------- */
+size_t eg_mla_append_workspace_size(const eg_mla_dims* dims, int32_t n_tokens, int32_t hidden);
+
+eg_mla_status eg_mla_append_ws(const eg_mla_dims* dims, int32_t n_tokens, int32_t hidden, const void* x,
+                               const int32_t* token_ids, const int32_t* positions, const int32_t* slots,
+                               const void* w_dkv, const void* kv_norm_w, float rope_theta, void* latent_cache,
+                               int32_t* token_id_cache, int64_t num_slots, void* workspace,
+                               size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
  * Decode: one query row per sequence against its whole cached context
  * (App. C Eq. (C.13) with t = the current token; the gate of Eq. (3)-(5)
  * applied to each cached latent through its token id).

@@ -24,7 +24,8 @@ PATH_AUTO, PATH_VALU, PATH_MFMA = 0, 1, 2
 EXPORTS = ["eg_mla_status_string", "eg_mla_check_dims", "eg_mla_append", "eg_mla_decode_workspace_size",
            "eg_mla_decode", "eg_mla_decode_planned", "eg_mla_gate_rows", "eg_mla_prefill_workspace_size",
            "eg_mla_prefill_ref", "eg_mla_prefill_varlen_workspace_size", "eg_mla_prefill_varlen",
-           "eg_mla_decode_literal_workspace_size", "eg_mla_decode_literal", "eg_mla_decode_noalloc"]
+           "eg_mla_decode_literal_workspace_size", "eg_mla_decode_literal", "eg_mla_decode_noalloc",
+           "eg_mla_append_workspace_size", "eg_mla_append_ws"]
 NOALLOC_SCRATCH_BYTES = 32 << 20  # EG_MLA_NOALLOC_SCRATCH_BYTES
 LITERAL_NO_LN, LITERAL_ADD = 1, 2
 
@@ -69,6 +70,10 @@ def lib() -> ctypes.CDLL:
     L.eg_mla_check_dims.argtypes = [pd]
     L.eg_mla_append.restype = ctypes.c_int
     L.eg_mla_append.argtypes = [pd, i32, i32, vp, vp, vp, vp, vp, vp, ctypes.c_float, vp, vp, i64, vp]
+    L.eg_mla_append_workspace_size.restype = sz
+    L.eg_mla_append_workspace_size.argtypes = [pd, i32, i32]
+    L.eg_mla_append_ws.restype = ctypes.c_int
+    L.eg_mla_append_ws.argtypes = [pd, i32, i32, vp, vp, vp, vp, vp, vp, ctypes.c_float, vp, vp, i64, vp, sz, vp]
     L.eg_mla_decode_workspace_size.restype = sz
     L.eg_mla_decode_workspace_size.argtypes = [pd, i32, i32, pp]
     L.eg_mla_decode.restype = ctypes.c_int
@@ -172,6 +177,21 @@ def append(dims: Dims, x, token_ids, positions, slots, w_dkv, kv_norm_w, latent_
     _check(lib().eg_mla_append(ctypes.byref(dims), n, hidden, _ptr(x), _ptr(token_ids), _ptr(positions),
                                _ptr(slots), _ptr(w_dkv), _ptr(kv_norm_w), rope_theta, _ptr(latent_cache),
                                _ptr(token_id_cache), int(latent_cache.shape[0]), _stream(stream)), "eg_mla_append")
+
+
+def append_workspace_size(dims: Dims, n_tokens: int, hidden: int) -> int:
+    return lib().eg_mla_append_workspace_size(ctypes.byref(dims), n_tokens, hidden)
+
+
+def append_ws(dims: Dims, x, token_ids, positions, slots, w_dkv, kv_norm_w, latent_cache, token_id_cache, workspace,
+              rope_theta: float = 10000.0, stream=None) -> None:
+    """eg_mla_append_ws over device tensors (workspace: a uint8 device tensor)."""
+    n, hidden = int(x.shape[0]), int(x.shape[1])
+    _check(lib().eg_mla_append_ws(ctypes.byref(dims), n, hidden, _ptr(x), _ptr(token_ids), _ptr(positions),
+                                  _ptr(slots), _ptr(w_dkv), _ptr(kv_norm_w), rope_theta, _ptr(latent_cache),
+                                  _ptr(token_id_cache), int(latent_cache.shape[0]), _ptr(workspace),
+                                  int(workspace.numel()) if workspace is not None else 0, _stream(stream)),
+           "eg_mla_append_ws")
 
 
 def gate_rows(dims: Dims, ids, emb, w_ue, out, stream=None) -> None:

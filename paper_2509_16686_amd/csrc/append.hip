@@ -10,6 +10,7 @@
 // d_c 128 / d_r 64 bf16 layer takes the MFMA kernel below.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 
 #include "device_common.h"
@@ -271,6 +272,132 @@ __global__ __launch_bounds__(256) void append_mfma_kernel(const uint16_t* __rest
                                        num_slots, n, hidden, red, freq);
 }
 
+// ---------------------------------------------------------------------------
+// Split append (eg_mla_append_ws) for the d_c 128 / d_r 64 bf16 layer: the
+// hidden dimension is cut into 256-wide slices so that a few tokens' call
+// spreads W_DKV over many work-groups instead of streaming it through two.
+//  Pass 1: work-group (ks, tg, ob) forms the partial sums of outputs
+//    32 ob .. + 31 (ob < 4: latent, 4 and 5: RoPE) of tokens 32 tg .. + 31 over
+//    hidden [256 ks, 256 ks + 256): wave w takes 64 of those k (4 chunks of 16)
+//    on v_mfma_f32_32x32x16_bf16 (A: W_DKV row o = lane % 32, 8 consecutive k;
+//    B: the token row, the same k), the 4 waves' sums are added in LDS in wave
+//    order and stored as fp32 part[ks][t][o].
+//  Pass 2: one wave per token adds the slices' sums in slice order, applies
+//    the latent RMSNorm (lane: latent outputs 2l, 2l + 1) and the RoPE
+//    rotation (lanes l < 32: pair l of the key), and writes the row and the id.
+// Every load is in bounds: token rows past n repeat the last token and are not
+// stored.
+// ---------------------------------------------------------------------------
+constexpr int kAppSlice = 256;        // hidden values per pass-1 work-group
+constexpr int kAppSplitMax = 2048;    // largest call taken by the split passes (measured crossover)
+constexpr int kAppOutBlocks = (kAppMfmaDC + kAppMfmaDR) / 32;
+
+__global__ __launch_bounds__(256) void append_slice_kernel(const uint16_t* __restrict__ x,
+                                                           const uint16_t* __restrict__ w_dkv,
+                                                           float* __restrict__ part, int n, int hidden) {
+  __shared__ float red[3 * 16 * 64];
+  constexpr int DQ = kAppMfmaDC + kAppMfmaDR;
+  const int ks = blockIdx.x, tg = blockIdx.y, ob = blockIdx.z;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r32 = lane & 31, h = lane >> 5;
+  const int tok = 32 * tg + r32;
+  const int k0 = kAppSlice * ks + 64 * w + 8 * h;
+  const uint16_t* xb = x + static_cast<int64_t>(min(tok, n - 1)) * hidden + k0;
+  const uint16_t* wb = w_dkv + static_cast<int64_t>(32 * ob + r32) * hidden + k0;
+  bf16x8_t av[4], bv[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    av[c] = *reinterpret_cast<const bf16x8_t*>(wb + 16 * c);
+    bv[c] = *reinterpret_cast<const bf16x8_t*>(xb + 16 * c);
+  }
+  app_f32x16_t acc;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[c], bv[c], acc, 0, 0, 0);
+  if (w > 0) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) red[((w - 1) * 16 + r) * 64 + lane] = acc[r];
+  }
+  __syncthreads();
+  if (w > 0 || tok >= n) return;
+#pragma unroll
+  for (int v = 0; v < 3; ++v)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] += red[(v * 16 + r) * 64 + lane];
+  // lane holds outputs 32 ob + 8 q + 4 h + (0..3) of token tok in acc[4 q + (0..3)]
+  float* dst = part + (static_cast<int64_t>(ks) * n + tok) * DQ + 32 * ob + 4 * h;
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    *reinterpret_cast<float4*>(dst + 8 * q) = make_float4(acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]);
+}
+
+__global__ __launch_bounds__(256) void append_finish_kernel(const float* __restrict__ part, int nks,
+                                                            const int32_t* __restrict__ token_ids,
+                                                            const int32_t* __restrict__ positions,
+                                                            const int32_t* __restrict__ slots,
+                                                            const uint16_t* __restrict__ kv_norm_w, float theta,
+                                                            uint16_t* __restrict__ cache, int32_t* __restrict__ ids,
+                                                            int64_t num_slots, int n) {
+  constexpr int DC = kAppMfmaDC, DR = kAppMfmaDR, DQ = DC + DR;
+  const int lane = threadIdx.x & 63;
+  const int t = 4 * blockIdx.x + (threadIdx.x >> 6);
+  if (t >= n) return;  // uniform over the wave
+  const int64_t slot = slots[t];
+  if (slot < 0 || slot >= num_slots) return;  // out-of-range destination: skipped
+  // this lane's latent outputs 2l, 2l + 1 and (l < DR / 2) RoPE outputs DC + 2l, DC + 2l + 1
+  // (the slices' sums are loaded 8 at a time, then added in slice order)
+  float2 c = make_float2(0.f, 0.f), r = make_float2(0.f, 0.f);
+  for (int k0 = 0; k0 < nks; k0 += 8) {
+    float2 av[8], bv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const float* row = part + (static_cast<int64_t>(min(k0 + u, nks - 1)) * n + t) * DQ;
+      av[u] = *reinterpret_cast<const float2*>(row + 2 * lane);
+      bv[u] = *reinterpret_cast<const float2*>(row + DC + 2 * (lane & (DR / 2 - 1)));
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      if (k0 + u < nks) {
+        c.x += av[u].x;
+        c.y += av[u].y;
+        r.x += bv[u].x;
+        r.y += bv[u].y;
+      }
+    }
+  }
+  uint16_t* dst = cache + slot * DQ;
+  if (kv_norm_w) {
+    const float ss = wave_sum(c.x * c.x + c.y * c.y);
+    const float inv_rms = 1.f / sqrtf(ss / static_cast<float>(DC) + kRmsEps);
+    const uint32_t wpair = *reinterpret_cast<const uint32_t*>(kv_norm_w + 2 * lane);
+    c.x = c.x * inv_rms * bf16_lo(wpair);
+    c.y = c.y * inv_rms * bf16_hi(wpair);
+  }
+  *reinterpret_cast<uint32_t*>(dst + 2 * lane) = pack_bf16x2(c.x, c.y);
+  if (lane < DR / 2) {
+    // the angle pos * theta^(-2m/d_r) and its reduction to [-pi, pi] in fp64,
+    // the sine and cosine of the reduced angle in fp32 (as the one-pass kernel)
+    constexpr double kTwoPi = 6.283185307179586476925286766559;
+    const double ang = static_cast<double>(positions[t]) *
+                       pow(static_cast<double>(theta), -2.0 * lane / static_cast<double>(DR));
+    const double turns = rint(ang * (1.0 / kTwoPi));
+    const float red_ang = static_cast<float>(fma(-turns, kTwoPi, ang));
+    float sn, cs;
+    sincosf(red_ang, &sn, &cs);
+    *reinterpret_cast<uint32_t*>(dst + DC + 2 * lane) = pack_bf16x2(r.x * cs - r.y * sn, r.x * sn + r.y * cs);
+  }
+  if (lane == 0) ids[slot] = token_ids[t];
+}
+
+bool append_split_shape(const eg_mla_dims& d, int32_t n_tokens, int32_t hidden) {
+  return d.dtype == EG_MLA_BF16 && d.latent_dim == kAppMfmaDC && d.rope_dim == kAppMfmaDR &&
+         hidden % kAppSlice == 0 && n_tokens >= 1 && n_tokens <= kAppSplitMax;
+}
+
+size_t append_split_bytes(int32_t n_tokens, int32_t hidden) {
+  return static_cast<size_t>(hidden / kAppSlice) * static_cast<size_t>(n_tokens) * (kAppMfmaDC + kAppMfmaDR) * 4;
+}
+
 }  // namespace egmla
 
 using namespace egmla;
@@ -324,5 +451,42 @@ extern "C" eg_mla_status eg_mla_append(const eg_mla_dims* dims, int32_t n_tokens
                        positions, slots, w_dkv, kv_norm_w, theta, latent_cache, token_id_cache, num_slots, hidden,
                        d.latent_dim, d.rope_dim);
   }
+  return hipGetLastError() == hipSuccess ? EG_MLA_OK : EG_MLA_ERR_HIP;
+}
+
+extern "C" size_t eg_mla_append_workspace_size(const eg_mla_dims* dims, int32_t n_tokens, int32_t hidden) {
+  if (check_dims(dims) != EG_MLA_OK || n_tokens < 0 || hidden < 1) return 0;
+  if (!append_split_shape(*dims, n_tokens, hidden)) return kAlign;
+  return std::max<size_t>(align_up(append_split_bytes(n_tokens, hidden)), kAlign);
+}
+
+extern "C" eg_mla_status eg_mla_append_ws(const eg_mla_dims* dims, int32_t n_tokens, int32_t hidden, const void* x,
+                                          const int32_t* token_ids, const int32_t* positions, const int32_t* slots,
+                                          const void* w_dkv, const void* kv_norm_w, float rope_theta,
+                                          void* latent_cache, int32_t* token_id_cache, int64_t num_slots,
+                                          void* workspace, size_t workspace_bytes, void* stream_) {
+  eg_mla_status st = validate_append(dims, n_tokens, hidden, x, token_ids, positions, slots, w_dkv, latent_cache,
+                                     token_id_cache, num_slots);
+  if (st != EG_MLA_OK || n_tokens == 0) return st;
+  const eg_mla_dims& d = *dims;
+  const bool aligned = reinterpret_cast<uintptr_t>(x) % 16 == 0 && reinterpret_cast<uintptr_t>(w_dkv) % 16 == 0 &&
+                       reinterpret_cast<uintptr_t>(latent_cache) % 4 == 0 &&
+                       reinterpret_cast<uintptr_t>(kv_norm_w) % 4 == 0;  // null passes
+  if (!append_split_shape(d, n_tokens, hidden) || !aligned)
+    return eg_mla_append(dims, n_tokens, hidden, x, token_ids, positions, slots, w_dkv, kv_norm_w, rope_theta,
+                         latent_cache, token_id_cache, num_slots, stream_);
+  if (!workspace || workspace_bytes < append_split_bytes(n_tokens, hidden) ||
+      reinterpret_cast<uintptr_t>(workspace) % kAlign != 0)
+    return EG_MLA_ERR_WORKSPACE;
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  const float theta = rope_theta > 0.f ? rope_theta : 10000.f;
+  (void)hipGetLastError();
+  const int nks = hidden / kAppSlice;
+  float* part = static_cast<float*>(workspace);
+  hipLaunchKernelGGL(append_slice_kernel, dim3(nks, (n_tokens + 31) / 32, kAppOutBlocks), dim3(256), 0, stream,
+                     static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w_dkv), part, n_tokens, hidden);
+  hipLaunchKernelGGL(append_finish_kernel, dim3((n_tokens + 3) / 4), dim3(256), 0, stream, part, nks, token_ids,
+                     positions, slots, static_cast<const uint16_t*>(kv_norm_w), theta,
+                     static_cast<uint16_t*>(latent_cache), token_id_cache, num_slots, n_tokens);
   return hipGetLastError() == hipSuccess ? EG_MLA_OK : EG_MLA_ERR_HIP;
 }

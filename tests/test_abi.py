@@ -137,6 +137,29 @@ def test_decode_noalloc_rejects_before_launch(L):
     assert call(dims(), batch=0) == B.OK      # a valid no-op that touches nothing
 
 
+def test_append_ws_sizes_and_rejections(L):
+    d = dims()
+    # hidden 2048 cut into 8 slices of 256: fp32 partial sums of the 192 outputs per token and slice
+    assert B.append_workspace_size(d, 32, 2048) == 8 * 32 * 192 * 4
+    assert B.append_workspace_size(d, 2048, 2048) == 8 * 2048 * 192 * 4
+    # calls the split passes do not take (more than 2048 tokens, hidden not a multiple
+    # of 256, another layer shape) run the one-pass append and need no workspace
+    assert B.append_workspace_size(d, 2049, 2048) == 256
+    assert B.append_workspace_size(d, 32, 2000) == 256
+    assert B.append_workspace_size(dims(latent_dim=512, gate_dim=512), 32, 2048) == 256
+    assert B.append_workspace_size(dims(num_heads=0), 32, 2048) == 0
+    assert B.append_workspace_size(d, -1, 2048) == 0
+    vp = ctypes.c_void_p(256)
+    def call(n, hidden, ws, ws_bytes):
+        return L.eg_mla_append_ws(ctypes.byref(d), n, hidden, vp, vp, vp, vp, vp, None, 0.0, vp, vp, 1 << 20, ws,
+                                  ws_bytes, None)
+    assert call(0, 2048, None, 0) == B.OK                                   # no-op
+    assert call(32, 2048, None, 0) == B.ERR_WORKSPACE                       # split path needs one
+    assert call(32, 2048, ctypes.c_void_p(4096), 8 * 32 * 192 * 4 - 1) == B.ERR_WORKSPACE   # too small
+    assert call(32, 2048, ctypes.c_void_p(4096 + 16), 8 * 32 * 192 * 4) == B.ERR_WORKSPACE  # misaligned
+    assert call(32, 40000, ctypes.c_void_p(4096), 1 << 30) == B.ERR_UNSUPPORTED
+
+
 def test_append_and_prefill_reject_before_launch(L):
     d = dims()
     vp = ctypes.c_void_p(256)

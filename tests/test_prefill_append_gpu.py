@@ -15,6 +15,15 @@ def stage(a, storage):
     return B.to_device_tensor(a, storage)
 
 
+def run_append(entry, dims, x, token_ids, positions, slots, w_dkv, kv_norm_w, cache, idc):
+    """eg_mla_append, or eg_mla_append_ws with a workspace of the size it asks for."""
+    if entry == "append":
+        B.append(dims, x, token_ids, positions, slots, w_dkv, kv_norm_w, cache, idc)
+    else:
+        ws = B.alloc_workspace(B.append_workspace_size(dims, int(x.shape[0]), int(x.shape[1])))
+        B.append_ws(dims, x, token_ids, positions, slots, w_dkv, kv_norm_w, cache, idc, ws)
+
+
 @pytest.mark.parametrize("wl,T", [(W.WORKLOADS[0], 128), (W.WORKLOADS[1], 300),
                                   (W.WORKLOADS[4].replace(heads=16), 130)])
 def test_prefill_ref_matches_oracle(gpu, wl, T):
@@ -67,9 +76,10 @@ def test_decode_row_equals_prefill_row(gpu):
     assert_close(a, b, "bf16", "decode vs prefill")
 
 
+@pytest.mark.parametrize("entry", ["append", "append_ws"])
 @pytest.mark.parametrize("wl,norm", [(W.WORKLOADS[1], True), (W.WORKLOADS[1], False), (W.WORKLOADS[4], True),
                                      (W.WORKLOADS[0], True)])
-def test_append_matches_oracle(gpu, wl, norm):
+def test_append_matches_oracle(gpu, wl, norm, entry):
     n, rows = 37, 256
     ap = W.generate_append(wl, n, rows, with_norm=norm)
     st = wl.dtype
@@ -79,9 +89,10 @@ def test_append_matches_oracle(gpu, wl, norm):
     idc = torch.full((rows,), -7, dtype=torch.int32, device="cuda")
     slots = ap.slots.copy()
     slots[5] = rows + 3          # out of range: skipped
-    say(f"append {wl.name} n={n} norm={norm}")
-    B.append(dims, stage(ap.x, st), stage(ap.token_ids, "int"), stage(ap.positions, "int"), stage(slots, "int"),
-             stage(ap.w_dkv, st), None if ap.kv_norm_w is None else stage(ap.kv_norm_w, st), cache, idc)
+    say(f"{entry} {wl.name} n={n} norm={norm}")
+    run_append(entry, dims, stage(ap.x, st), stage(ap.token_ids, "int"), stage(ap.positions, "int"),
+               stage(slots, "int"), stage(ap.w_dkv, st), None if ap.kv_norm_w is None else stage(ap.kv_norm_w, st),
+               cache, idc)
     torch.cuda.synchronize()
     ref = orc.append(ap.x, ap.w_dkv, ap.kv_norm_w, ap.positions, latent_dim=wl.latent_dim, rope_dim=wl.rope_dim,
                      storage=st)
@@ -121,8 +132,10 @@ def test_append_then_decode(gpu):
     assert_close(got, oracle_decode(inp), "bf16", "append then decode")
 
 
-@pytest.mark.parametrize("n", [1, 31, 33, 8192, 8193, 9000])
-def test_append_token_counts(gpu, n):
+@pytest.mark.parametrize("entry,n", [("append", 1), ("append", 31), ("append", 33), ("append", 8192),
+                                     ("append", 8193), ("append", 9000), ("append_ws", 1), ("append_ws", 32),
+                                     ("append_ws", 33), ("append_ws", 2048), ("append_ws", 2049)])
+def test_append_token_counts(gpu, entry, n):
     # the d_c 128 / d_r 64 layer's MFMA append: hidden split over the waves up
     # to 8192 tokens, 128 tokens per work-group above; ragged last tiles
     wl = W.WORKLOADS[1]
@@ -131,9 +144,9 @@ def test_append_token_counts(gpu, n):
     dims = B.dims_for(wl)
     cache = torch.zeros((rows, wl.row_dim), dtype=torch.bfloat16, device="cuda")
     idc = torch.full((rows,), -7, dtype=torch.int32, device="cuda")
-    say(f"append {wl.name} n={n}")
-    B.append(dims, stage(ap.x, "bf16"), stage(ap.token_ids, "int"), stage(ap.positions, "int"),
-             stage(ap.slots, "int"), stage(ap.w_dkv, "bf16"), stage(ap.kv_norm_w, "bf16"), cache, idc)
+    say(f"{entry} {wl.name} n={n}")
+    run_append(entry, dims, stage(ap.x, "bf16"), stage(ap.token_ids, "int"), stage(ap.positions, "int"),
+               stage(ap.slots, "int"), stage(ap.w_dkv, "bf16"), stage(ap.kv_norm_w, "bf16"), cache, idc)
     torch.cuda.synchronize()
     ref = orc.append(ap.x, ap.w_dkv, ap.kv_norm_w, ap.positions, latent_dim=wl.latent_dim, rope_dim=wl.rope_dim,
                      storage="bf16")
