@@ -60,6 +60,11 @@ class DecodeTraffic:
         """Bytes the token-streaming kernel must move: cache rows, ids, distinct gate rows."""
         return self.cache_rows + self.token_ids + self.gate_rows
 
+    @property
+    def main_kernel_absorbing(self) -> int:
+        """The same for a token-streaming kernel that also absorbs the query (reads q and W_UK once)."""
+        return self.main_kernel + self.q + self.w_uk
+
 
 def decode_bytes(*, batch: int, heads: int, head_dim: int, v_head_dim: int, latent_dim: int,
                  rope_dim: int, elem_bytes: int, total_tokens: int, distinct_ids: int) -> DecodeTraffic:
