@@ -117,7 +117,16 @@ eg_mla_status make_decode_plan(const eg_mla_dims& d, int32_t batch, int32_t max_
     p.off_sched = off;
     off = align_up(off + 16 + kWideMaxGroups * 8 + B * 8);
   }
-  p.fused_absorb = sliced_kernel && p.slices == 1 && d.head_dim == 128;
+  // The split kernel absorbs the query itself when that costs each work-group
+  // at most 2 heads' W_UK (8 to 16 splits per sequence, every split a
+  // producer) and every work-group is resident at once (2 per compute unit);
+  // otherwise (many splits, whose extra work-groups only wait, or a batch of
+  // several rounds of work-groups each reading 4 or more heads' W_UK) the
+  // absorption kernel runs first (measured: B32 L4096 25.2 against 25.7 us
+  // per call; B4 L32768 28.9 against 27.8; B256 L2048 70.8 against 59.4).
+  const int64_t nblk = static_cast<int64_t>(std::max(batch, 0)) * p.s_max * p.head_groups;
+  p.fused_absorb = sliced_kernel && p.slices == 1 && d.head_dim == 128 && p.s_max >= 8 && p.s_max <= 16 &&
+                   nblk <= 2 * kTargetWorkItemsTok;
   if (p.fused_absorb) {
     p.off_flags = off;
     off = align_up(off + B * static_cast<size_t>(p.head_groups) * static_cast<size_t>(p.s_max) * 8);
