@@ -339,9 +339,16 @@ def append_main(args):
     nbytes = n * wl.hidden * esz + wl.row_dim * wl.hidden * esz + n * (wl.row_dim * esz + 4) + 12 * n + \
         wl.latent_dim * esz
     gbs = nbytes / (ms * 1e-3) / 1e9
-    out["roofline"] = {"bound": "hbm", "kernel": "eg_mla_append_ws (whole call)", "achieved": gbs, "peak": HBM_PEAK_GBPS,
-                       "unit": "GB/s", "frac": gbs / HBM_PEAK_GBPS, "traffic": None,
-                       "algorithmic_bytes_per_call": nbytes, "mfma_tflops": flops / (ms * 1e-3) / 1e12}
+    tflops = flops / (ms * 1e-3) / 1e12
+    if st == "bf16" and flops / (MFMA_BF16_PEAK_TFLOPS * 1e12) > nbytes / (HBM_PEAK_GBPS * 1e9):
+        # many tokens: the product W_DKV x is the longer of the two floors
+        out["roofline"] = {"bound": "mfma", "kernel": "eg_mla_append_ws (whole call)", "achieved": tflops,
+                           "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": tflops / MFMA_BF16_PEAK_TFLOPS,
+                           "traffic": None, "algorithmic_flops_per_call": flops, "hbm_gbs": gbs}
+    else:
+        out["roofline"] = {"bound": "hbm", "kernel": "eg_mla_append_ws (whole call)", "achieved": gbs,
+                           "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBPS, "traffic": None,
+                           "algorithmic_bytes_per_call": nbytes, "mfma_tflops": tflops}
     print(json.dumps(out), flush=True)
 
 

@@ -132,11 +132,13 @@ eg_mla_status eg_mla_append(const eg_mla_dims* dims, int32_t n_tokens, int32_t h
 
 /* ---------------------------------------------------------------------------
  * Append with a workspace: the same operation and arguments as eg_mla_append
- * (Sec. 3.1 Eq. (1); App. C Eq. (C.10)), the same rows and ids, for calls
- * of few tokens.  With bf16 storage, d_c = 128, d_r = 64, hidden a multiple
- * of 256 and 1..2048 tokens, the hidden dimension is cut into 256-wide
- * slices over many work-groups: pass 1 stores fp32 partial sums of W_DKV x_i
- * per slice in the workspace ([hidden/256, n_tokens, d_c + d_r]), pass 2 adds
+ * (Sec. 3.1 Eq. (1); App. C Eq. (C.10)), the same rows and ids.  With bf16
+ * storage, d_r = 64, hidden a multiple of 256 and either d_c = 128 with
+ * 1..2048 tokens or d_c = 512 with 1..2^20 tokens, W_DKV x_i is formed in
+ * two passes: the hidden dimension is cut into S slices (S divides
+ * hidden/256; many for few tokens, so that W_DKV spreads over many
+ * work-groups, down to 1 for many tokens), pass 1 stores the fp32 partial
+ * sums per slice in the workspace ([S, n_tokens, d_c + d_r]), pass 2 adds
  * them in slice order, applies the RMSNorm and RoPE and writes the rows.  Any
  * other call runs eg_mla_append (the workspace is not touched).
  *

@@ -139,14 +139,26 @@ def test_decode_noalloc_rejects_before_launch(L):
 
 def test_append_ws_sizes_and_rejections(L):
     d = dims()
-    # hidden 2048 cut into 8 slices of 256: fp32 partial sums of the 192 outputs per token and slice
-    assert B.append_workspace_size(d, 32, 2048) == 8 * 32 * 192 * 4
-    assert B.append_workspace_size(d, 2048, 2048) == 8 * 2048 * 192 * 4
-    # calls the split passes do not take (more than 2048 tokens, hidden not a multiple
-    # of 256, another layer shape) run the one-pass append and need no workspace
+    # fp32 partial sums of the d_c + d_r outputs per token and slice.  The slice count is
+    # the fewest dividing hidden / 256 that give the first pass its target of work-groups
+    # (else hidden / 256): 512 of 32 outputs x 32 tokens (64 above 32 tokens), or from
+    # 256 x 576 outputs on, 128 of 192 outputs x 128 tokens (the LDS-tiled product)
+    assert B.append_workspace_size(d, 32, 2048) == 8 * 32 * 192 * 4        # 8 x 1 x 6 groups
+    assert B.append_workspace_size(d, 700, 2048) == 8 * 700 * 192 * 4      # 8 x 11 x 6 >= 512
+    assert B.append_workspace_size(d, 2048, 2048) == 8 * 2048 * 192 * 4    # tiled: 8 x 16 x 1
+    d512 = dims(latent_dim=512, gate_dim=512, num_heads=128)
+    assert B.append_workspace_size(d512, 64, 7168) == 28 * 64 * 576 * 4    # 28 x 1 x 18
+    assert B.append_workspace_size(d512, 255, 7168) == 14 * 255 * 576 * 4  # 14 x 4 x 18 >= 512
+    assert B.append_workspace_size(d512, 512, 7168) == 14 * 512 * 576 * 4  # tiled: 14 x 4 x 3 >= 128
+    assert B.append_workspace_size(d512, 4096, 7168) == 2 * 4096 * 576 * 4  # tiled: 2 x 32 x 3
+    assert B.append_workspace_size(d512, 16384, 7168) == 16384 * 576 * 4   # tiled: 1 x 128 x 3
+    assert B.append_workspace_size(d512, 1, 2048) == 8 * 576 * 4
+    # calls the split passes do not take (d_c 128 above 2048 tokens, hidden not a
+    # multiple of 256, another layer shape) run the one-pass append and need no workspace
     assert B.append_workspace_size(d, 2049, 2048) == 256
     assert B.append_workspace_size(d, 32, 2000) == 256
-    assert B.append_workspace_size(dims(latent_dim=512, gate_dim=512), 32, 2048) == 256
+    assert B.append_workspace_size(dims(latent_dim=256, gate_dim=256), 32, 2048) == 256
+    assert B.append_workspace_size(dims(latent_dim=512, gate_dim=512, rope_dim=32), 32, 2048) == 256
     assert B.append_workspace_size(dims(num_heads=0), 32, 2048) == 0
     assert B.append_workspace_size(d, -1, 2048) == 0
     vp = ctypes.c_void_p(256)

@@ -78,7 +78,7 @@ def test_decode_row_equals_prefill_row(gpu):
 
 @pytest.mark.parametrize("entry", ["append", "append_ws"])
 @pytest.mark.parametrize("wl,norm", [(W.WORKLOADS[1], True), (W.WORKLOADS[1], False), (W.WORKLOADS[4], True),
-                                     (W.WORKLOADS[0], True)])
+                                     (W.WORKLOADS[4], False), (W.WORKLOADS[0], True)])
 def test_append_matches_oracle(gpu, wl, norm, entry):
     n, rows = 37, 256
     ap = W.generate_append(wl, n, rows, with_norm=norm)
@@ -132,13 +132,19 @@ def test_append_then_decode(gpu):
     assert_close(got, oracle_decode(inp), "bf16", "append then decode")
 
 
-@pytest.mark.parametrize("entry,n", [("append", 1), ("append", 31), ("append", 33), ("append", 8192),
-                                     ("append", 8193), ("append", 9000), ("append_ws", 1), ("append_ws", 32),
-                                     ("append_ws", 33), ("append_ws", 2048), ("append_ws", 2049)])
-def test_append_token_counts(gpu, entry, n):
-    # the d_c 128 / d_r 64 layer's MFMA append: hidden split over the waves up
-    # to 8192 tokens, 128 tokens per work-group above; ragged last tiles
-    wl = W.WORKLOADS[1]
+@pytest.mark.parametrize("wi,entry,n", [(1, "append", 1), (1, "append", 31), (1, "append", 33), (1, "append", 8192),
+                                        (1, "append", 8193), (1, "append", 9000), (1, "append_ws", 1),
+                                        (1, "append_ws", 32), (1, "append_ws", 33), (1, "append_ws", 2048),
+                                        (1, "append_ws", 2049), (1, "append_ws", 300), (4, "append_ws", 1),
+                                        (4, "append_ws", 64), (4, "append_ws", 97), (4, "append_ws", 255),
+                                        (4, "append_ws", 256), (4, "append_ws", 512), (4, "append_ws", 3001)])
+def test_append_token_counts(gpu, wi, entry, n):
+    # the d_c 128 / d_r 64 layer's one-pass MFMA append: hidden split over the
+    # waves up to 8192 tokens, 128 tokens per work-group above; the two-pass
+    # append of both bf16 layers (d_c 128 at hidden 2048, d_c 512 at hidden
+    # 7168), its first pass from global memory below 256 tokens and LDS-tiled
+    # from 256, from 28 slices down to one; ragged last tiles
+    wl = W.WORKLOADS[wi]
     rows = n + 300
     ap = W.generate_append(wl, n, rows, with_norm=True, seed=71 + n)
     dims = B.dims_for(wl)
