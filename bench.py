@@ -172,11 +172,15 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0
 
 
 def prefill_flops(lens, heads=16, dc=128, dr=64, dh=128, dv=128):
-    """Algorithmic flops of one causal prefill call: scores and values over every (row, key <= row)
-    pair of each sequence, plus the absorption and the up-projection of every row."""
+    """Algorithmic flops of one causal prefill call.  Absorbed form (d_c 128, 16 heads): scores and
+    values over every (row, key <= row) pair of each sequence in the latent space, plus the absorption
+    and the up-projection of every row.  Explicit form (other layers): the projection of every token's
+    gated latent to each head's key and value, then scores and values per pair in the head space."""
     pairs = sum(t * (t + 1) // 2 for t in lens)
     rows = sum(lens) * heads
-    return pairs * heads * 2 * (dc + dr + dc) + rows * 2 * dh * dc + rows * 2 * dc * dv
+    if dc == 128 and heads == 16:
+        return pairs * heads * 2 * (dc + dr + dc) + rows * 2 * dh * dc + rows * 2 * dc * dv
+    return pairs * heads * 2 * (dh + dr + dv) + rows * 2 * dc * (dh + dv)
 
 
 def prefill_cpu_baseline(wl, seconds):
@@ -218,7 +222,7 @@ def prefill_main(args):
     hip = Hip()
     nb, T = (int(x) for x in args.prefill.lower().split("x"))
     lens = [T] * nb
-    wl = W.WORKLOADS[1]
+    wl = W.WORKLOADS[args.workload] if args.workload in (1, 4) else W.WORKLOADS[1]
     log(f"bench: generating a prefill of {nb} x {T} tokens ({wl.name} layer)")
     pb = W.generate_prefill_batch(wl, lens, seed=wl.seed + 3000)
     total = int(pb.cu_seqlens[-1])
@@ -257,7 +261,7 @@ def prefill_main(args):
     hip.record(e1, stream)
     torch.cuda.synchronize()
     ms = hip.elapsed_ms(e0, e1) / K
-    fl = prefill_flops(lens)
+    fl = prefill_flops(lens, heads=wl.heads, dc=wl.latent_dim, dr=wl.rope_dim, dh=wl.head_dim, dv=wl.v_head_dim)
     tflops = fl / (ms * 1e-3) / 1e12
     log(f"bench: prefill {nb} x {T}: {ms * 1e3:.1f} us/call, {total / ms * 1e3 / 1e6:.2f} M tokens/s, "
         f"{tflops:.0f} TFLOP/s ({100 * tflops / MFMA_BF16_PEAK_TFLOPS:.1f} % of the bf16 MFMA peak)")
@@ -268,8 +272,10 @@ def prefill_main(args):
         "config": {"workload": f"prefill_{nb}x{T}_{wl.name}", "sequences": nb, "tokens_per_sequence": T,
                    "heads": wl.heads, "latent_dim": wl.latent_dim, "rope_dim": wl.rope_dim, "storage": wl.dtype,
                    "rotating_copies": R},
-        "roofline": {"bound": "mfma", "kernel": "eg_mla_prefill_varlen (whole call: absorption, attention, "
-                                                "up-projection)",
+        "roofline": {"bound": "mfma", "kernel": ("eg_mla_prefill_varlen (whole call: absorption, attention, "
+                                                 "up-projection)") if wl.heads == 16 and wl.latent_dim == 128 else
+                                                ("eg_mla_prefill_varlen (whole call: projection to per-head keys "
+                                                 "and values, attention)"),
                      "achieved": tflops, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": tflops / MFMA_BF16_PEAK_TFLOPS, "traffic": None, "algorithmic_flops_per_call": fl,
                      "call_us": ms * 1e3},

@@ -215,20 +215,33 @@ eg_mla_status validate_prefill(const eg_mla_dims* d, int32_t seq_len, const void
   return EG_MLA_OK;
 }
 
+bool prefill_varlen_absorbed(const eg_mla_dims& d) {
+  return d.dtype == EG_MLA_BF16 && d.num_heads == 16 && d.head_dim == 128 && d.v_head_dim == 128 &&
+         d.latent_dim == 128 && d.rope_dim == 64 && d.gate_dim == d.latent_dim;
+}
+
+bool prefill_varlen_shape_ok(const eg_mla_dims& d) {
+  if (prefill_varlen_absorbed(d)) return true;
+  // the explicit form: any head count, d_c a multiple of 64
+  return d.dtype == EG_MLA_BF16 && d.head_dim == 128 && d.v_head_dim == 128 && d.rope_dim == 64 &&
+         d.latent_dim % 64 == 0 && d.gate_dim == d.latent_dim;
+}
+
 PrefillVarlenLayout prefill_varlen_layout(const eg_mla_dims& d, int32_t total_tokens) {
   const size_t T = static_cast<size_t>(std::max(total_tokens, 0));
   const size_t H = static_cast<size_t>(d.num_heads);
   PrefillVarlenLayout L;
-  L.off_seq_start = 0;                                                             // int32 [T]
-  L.off_qf = align_up(T * 4);                                                      // bf16 [T][H][d_c + d_r]
-  L.off_olat = L.off_qf + align_up(T * H * static_cast<size_t>(d.latent_dim + d.rope_dim) * 2);  // fp32 [T][H][d_c]
-  L.bytes = std::max<size_t>(L.off_olat + align_up(T * H * static_cast<size_t>(d.latent_dim) * 4), kAlign);
+  L.off_seq_start = 0;  // int32 [T]
+  if (prefill_varlen_absorbed(d)) {
+    L.off_qf = align_up(T * 4);                                                                    // bf16 [T][H][d_c + d_r]
+    L.off_olat = L.off_qf + align_up(T * H * static_cast<size_t>(d.latent_dim + d.rope_dim) * 2);  // fp32 [T][H][d_c]
+    L.bytes = std::max<size_t>(L.off_olat + align_up(T * H * static_cast<size_t>(d.latent_dim) * 4), kAlign);
+  } else {
+    L.off_qf = align_up(T * 4);                                                  // K^C: fp16 [H][T][d_h]
+    L.off_olat = L.off_qf + align_up(T * H * static_cast<size_t>(d.head_dim) * 2);  // V: fp16 [H][T][d_v]
+    L.bytes = std::max<size_t>(L.off_olat + align_up(T * H * static_cast<size_t>(d.v_head_dim) * 2), kAlign);
+  }
   return L;
-}
-
-bool prefill_varlen_shape_ok(const eg_mla_dims& d) {
-  return d.dtype == EG_MLA_BF16 && d.num_heads == 16 && d.head_dim == 128 && d.v_head_dim == 128 &&
-         d.latent_dim == 128 && d.rope_dim == 64 && d.gate_dim == d.latent_dim;
 }
 
 eg_mla_status validate_prefill_varlen(const eg_mla_dims* d, int32_t batch, int32_t total_tokens,

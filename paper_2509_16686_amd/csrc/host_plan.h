@@ -87,10 +87,13 @@ eg_mla_status validate_prefill(const eg_mla_dims* d, int32_t seq_len, const void
                                const void* out);
 
 // Batched (packed, variable-length) causal prefill on MFMA.
+// Absorbed form (d_c 128, 16 heads): off_qf = absorbed queries, off_olat =
+// latent outputs.  Explicit form (other shapes): off_qf = K^C, off_olat = V.
 struct PrefillVarlenLayout {
   size_t off_seq_start, off_qf, off_olat, bytes;
 };
 PrefillVarlenLayout prefill_varlen_layout(const eg_mla_dims& d, int32_t total_tokens);
+bool prefill_varlen_absorbed(const eg_mla_dims& d);
 bool prefill_varlen_shape_ok(const eg_mla_dims& d);
 eg_mla_status validate_prefill_varlen(const eg_mla_dims* d, int32_t batch, int32_t total_tokens,
                                       const int32_t* cu_seqlens, const void* q, const void* latent,

@@ -13,6 +13,7 @@
 #include "eg_mla.h"
 #include "host_plan.h"
 #include "prefill_mfma.h"
+#include "prefill_explicit.h"
 
 namespace egmla {
 
@@ -167,6 +168,34 @@ extern "C" eg_mla_status eg_mla_prefill_varlen(const eg_mla_dims* dims, int32_t 
 
   hipLaunchKernelGGL(prefill_seqmap_kernel, dim3((T + 255) / 256), dim3(256), 0, stream, cu_seqlens, batch, T,
                      seq_start);
+  if (!prefill_varlen_absorbed(d)) {
+    // explicit form: K^C and V per head (fp16), then the attention per head
+    uint16_t* kc = reinterpret_cast<uint16_t*>(ws + L.off_qf);
+    uint16_t* vv = reinterpret_cast<uint16_t*>(ws + L.off_olat);
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(prefill_x_proj_kernel),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, kPxProjLds) != hipSuccess ||
+        hipFuncSetAttribute(reinterpret_cast<const void*>(prefill_x_attn_kernel),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, 2 * kPxTileBytes) != hipSuccess)
+      return EG_MLA_ERR_HIP;
+    hipLaunchKernelGGL(prefill_x_proj_kernel, dim3((T + kPxTok - 1) / kPxTok, d.num_heads), dim3(256), kPxProjLds,
+                       stream, static_cast<const uint16_t*>(latent), token_ids,
+                       static_cast<const uint16_t*>(gate_table), static_cast<const uint16_t*>(w_uk),
+                       static_cast<const uint16_t*>(w_uv), kc, vv, T, d.latent_dim, d.vocab_size);
+    PrefillXArgs x;
+    x.q = static_cast<const uint16_t*>(q);
+    x.latent = static_cast<const uint16_t*>(latent);
+    x.kc = kc;
+    x.vv = vv;
+    x.seq_start = seq_start;
+    x.out = static_cast<uint16_t*>(out);
+    x.T = T;
+    x.H = d.num_heads;
+    x.DC = d.latent_dim;
+    x.scale_log2 = softmax_scale(d) * 1.4426950408889634f;
+    hipLaunchKernelGGL(prefill_x_attn_kernel, dim3((T + kPxQTok - 1) / kPxQTok, d.num_heads), dim3(256),
+                       2 * kPxTileBytes, stream, x);
+    return hipGetLastError() == hipSuccess ? EG_MLA_OK : EG_MLA_ERR_HIP;
+  }
   // q_lat (bf16) and q^R for every token
   const int side_wgs = ((T + kPfUvTokens - 1) / kPfUvTokens + kPfSideChunks - 1) / kPfSideChunks;
   hipLaunchKernelGGL(prefill_absorb_kernel, dim3(side_wgs, d.num_heads), dim3(256), 0, stream,

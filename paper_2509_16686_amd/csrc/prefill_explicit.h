@@ -1,0 +1,419 @@
+// Causal prefill of EG-MLA on gfx950 MFMA in the explicit form of App. C
+// Eq. (C.2), (C.6), (C.11)-(C.13), with the latent-space gate of Sec. 3.1
+// Eq. (5), for layers with many heads and a wide latent (d_c = 512 with 128
+// heads: there the absorbed form costs 2 (d_c + d_r + d_c) = 2176 flops per
+// (row, key) pair and head, the explicit one 2 (d_h + d_r + d_v) = 640).
+// Included by prefill.hip.  bf16 storage, d_h = d_v = 128, d_r = 64, d_c a
+// multiple of 64.
+//
+//   K^C[h][t] = W_UK[h] c~_t,  V[h][t] = W_UV[h] c~_t,  c~_t = c_t (.) G[id_t]
+//   out[t,h]  = sum_{j <= t, same sequence} softmax_j(tau (q^C[t,h].K^C[h][j] + q^R[t,h].k^R_j)) V[h][j]
+//
+// Two launches after the sequence map: the projection (a GEMM over d_c) and
+// the attention (a causal flash attention per head with 192-dim keys, the
+// RoPE key shared by all heads, and 128-dim values).
+//
+// Precision.  The gated latent enters the projection as bf16 hi + lo (their
+// sum is the fp32 product c * g exactly, two products per step), so K^C and V
+// carry only the rounding of their fp32 sums, which is to fp16 (11-bit
+// significand; values must stay below 65504 in magnitude, true of layers whose
+// keys and values are of order one to thousands).  The attention runs on the
+// fp16 MFMA: the bf16 query and RoPE key convert to fp16 exactly (for
+// magnitudes between 2^-14 and 65504), P is rounded to fp16, and the output is
+// rounded once to bf16.
+#pragma once
+
+namespace egmla {
+
+typedef __attribute__((ext_vector_type(8))) _Float16 f16x8_t;
+typedef __attribute__((ext_vector_type(2))) _Float16 f16x2_t;
+
+__device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, f16x2_t{static_cast<_Float16>(a), static_cast<_Float16>(b)});
+}
+
+// 8 bf16 values (16 bytes) to 8 fp16 values (exact within the fp16 range).
+__device__ __forceinline__ u32x4_t bf16x8_to_f16x8(u32x4_t v) {
+  u32x4_t r;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) r[e] = pack_f16x2(bf16_lo(v[e]), bf16_hi(v[e]));
+  return r;
+}
+
+constexpr int kPxDH = 128, kPxDR = 64, kPxDK = kPxDH + kPxDR;  // key dims per head (K^C | k^R)
+
+// ---------------------------------------------------------------------------
+// Projection.  Work-group (tt, h) forms K^C[h] and V[h] of tokens
+// 128 tt .. + 127: a product of the 128 gated latent rows (B operand, as hi
+// and lo) with the 256 rows W_UK[h] | W_UV[h] (A operand) over d_c, in steps
+// of 32: each step's rows (64 bytes each, the latent as hi rows then lo rows,
+// then the weights) are staged in LDS with a row stride of 80 bytes (the
+// operand reads of 16 rows by 16 lanes hit 64 distinct banks), double
+// buffered, the next step's global loads in registers.  Wave (wt, wo) =
+// (w % 2, w / 2) forms tokens 64 wt .. + 63 of K^C (wo = 0) or V (wo = 1):
+// 2 x 4 tiles of v_mfma_f32_32x32x16_bf16, two products per tile and step.
+// ---------------------------------------------------------------------------
+constexpr int kPxTok = 128, kPxOut = 256, kPxK = 32, kPxStride = kPxK + 8;
+constexpr int kPxRows = 2 * kPxTok + kPxOut;              // hi, lo, weights
+constexpr int kPxBuf = kPxRows * kPxStride;               // bf16 elements per buffer
+constexpr int kPxProjLds = 2 * kPxBuf * 2;                // bytes (two buffers)
+static_assert(2 * kPxProjLds <= 160 * 1024, "two work-groups per compute unit");
+
+__global__ __launch_bounds__(256, 2) void prefill_x_proj_kernel(const uint16_t* __restrict__ latent,
+                                                                const int32_t* __restrict__ ids,
+                                                                const uint16_t* __restrict__ gate,
+                                                                const uint16_t* __restrict__ w_uk,
+                                                                const uint16_t* __restrict__ w_uv,
+                                                                uint16_t* __restrict__ kc, uint16_t* __restrict__ vv,
+                                                                int T, int DC, int V) {
+  extern __shared__ __attribute__((aligned(16))) uint16_t stage[];  // [2][kPxRows][kPxStride]
+  const int tt = blockIdx.x, hh = blockIdx.y;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r32 = lane & 31, h = lane >> 5;
+  const int wt = w & 1, wo = w >> 1;
+  const int DQ = DC + kPxDR;
+  // copies of a step: latent and gate pieces j = tid + 256 i (i < 2) of token
+  // row j / 4, weight pieces j = tid + 256 i (i < 4) of weight row j / 4;
+  // 16 bytes at 8 (j % 4) of the row's 32 k
+  const uint16_t* lp[2];
+  const uint16_t* gp[2];
+  const uint16_t* wp[4];
+  int xo[2], wofs[4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int j = tid + 256 * i, row = j >> 2, c = j & 3;
+    const int t = min(kPxTok * tt + row, T - 1);
+    lp[i] = latent + static_cast<int64_t>(t) * DQ + 8 * c;
+    gp[i] = gate + static_cast<int64_t>(clamp_id(ids[t], V)) * DC + 8 * c;
+    xo[i] = row * kPxStride + 8 * c;
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int j = tid + 256 * i, row = j >> 2, c = j & 3;
+    wp[i] = (row < kPxDH ? w_uk + (static_cast<int64_t>(hh) * kPxDH + row) * DC
+                         : w_uv + (static_cast<int64_t>(hh) * kPxDH + row - kPxDH) * DC) + 8 * c;
+    wofs[i] = (2 * kPxTok + row) * kPxStride + 8 * c;
+  }
+  u32x4_t gl[2], gg[2], gw[4];
+  auto fetch = [&](int step) {
+    const int k = kPxK * step;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      gl[i] = *reinterpret_cast<const u32x4_t*>(lp[i] + k);
+      gg[i] = *reinterpret_cast<const u32x4_t*>(gp[i] + k);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) gw[i] = *reinterpret_cast<const u32x4_t*>(wp[i] + k);
+  };
+  auto put = [&](int buf) {
+    uint16_t* b = stage + buf * kPxBuf;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      u32x4_t hi, lo;
+      gate_chunk_hilo(gl[i], gg[i], hi, lo);
+      *reinterpret_cast<u32x4_t*>(b + xo[i]) = hi;
+      *reinterpret_cast<u32x4_t*>(b + kPxTok * kPxStride + xo[i]) = lo;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4_t*>(b + wofs[i]) = gw[i];
+  };
+  pf_f32x16_t acc[2][4];
+#pragma unroll
+  for (int tb = 0; tb < 2; ++tb)
+#pragma unroll
+    for (int ob = 0; ob < 4; ++ob)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[tb][ob][r] = 0.f;
+  const int brow = (64 * wt + r32) * kPxStride + 8 * h;
+  const int arow = (2 * kPxTok + 128 * wo + r32) * kPxStride + 8 * h;
+  auto compute = [&](int buf) {
+    const uint16_t* b = stage + buf * kPxBuf;
+#pragma unroll
+    for (int kk = 0; kk < kPxK / 16; ++kk) {
+      bf16x8_t bh[2], bl[2], av[4];
+#pragma unroll
+      for (int tb = 0; tb < 2; ++tb) {
+        bh[tb] = *reinterpret_cast<const bf16x8_t*>(b + brow + 32 * tb * kPxStride + 16 * kk);
+        bl[tb] = *reinterpret_cast<const bf16x8_t*>(b + kPxTok * kPxStride + brow + 32 * tb * kPxStride + 16 * kk);
+      }
+#pragma unroll
+      for (int ob = 0; ob < 4; ++ob)
+        av[ob] = *reinterpret_cast<const bf16x8_t*>(b + arow + 32 * ob * kPxStride + 16 * kk);
+#pragma unroll
+      for (int tb = 0; tb < 2; ++tb)
+#pragma unroll
+        for (int ob = 0; ob < 4; ++ob) {
+          acc[tb][ob] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[ob], bh[tb], acc[tb][ob], 0, 0, 0);
+          acc[tb][ob] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[ob], bl[tb], acc[tb][ob], 0, 0, 0);
+        }
+    }
+  };
+  // step s computes from buffer s % 2, then writes step s + 1 (in registers)
+  // to the other buffer and fetches step s + 2; the step count is even and the
+  // loop has no branch (past the last step the last one is fetched and
+  // written again, to a buffer nothing reads)
+  const int steps = DC / kPxK;
+  fetch(0);
+  put(0);
+  fetch(1);
+  __syncthreads();
+  for (int s0 = 0; s0 < steps; s0 += 2) {
+    compute(0);
+    put(1);
+    fetch(min(s0 + 2, steps - 1));
+    __syncthreads();
+    compute(1);
+    put(0);
+    fetch(min(s0 + 3, steps - 1));
+    __syncthreads();
+  }
+  // lane holds dims 32 ob + 8 q + 4 h + (0..3) of token 64 wt + 32 tb + r32 in acc[tb][ob][4 q + (0..3)]
+  uint16_t* dst = wo == 0 ? kc : vv;
+#pragma unroll
+  for (int tb = 0; tb < 2; ++tb) {
+    const int t = kPxTok * tt + 64 * wt + 32 * tb + r32;
+    if (t >= T) break;
+    uint16_t* row = dst + (static_cast<int64_t>(hh) * T + t) * kPxDH + 4 * h;
+#pragma unroll
+    for (int ob = 0; ob < 4; ++ob)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        *reinterpret_cast<u32x2_t*>(row + 32 * ob + 8 * q) =
+            u32x2_t{pack_f16x2(acc[tb][ob][4 * q], acc[tb][ob][4 * q + 1]),
+                    pack_f16x2(acc[tb][ob][4 * q + 2], acc[tb][ob][4 * q + 3])};
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Attention.  Work-group (block, h) takes the 128 consecutive tokens
+// 128 block .. + 127 of the packed stream for head h (a block may straddle
+// sequences: each row masks keys outside its own sequence) and walks tiles of
+// 64 keys from the first token's sequence start to the block's last token
+// (blocks launched last-in-the-stream first, the heads of a block together
+// in the grid's second dimension).  Wave w holds the rows of tokens
+// 32 w .. + 31 of the block, its query (fp16) in registers as the B operand of
+// v_mfma_f32_32x32x16_f16 (lane: row lane % 32, dims 8 (lane / 32) + 16 c).
+//  * Tile: K^C rows (256 bytes, fp16), k^R rows (128 bytes, converted from
+//    bf16 on the way) and V rows (256 bytes, fp16) of the next tile are loaded
+//    while the current one is computed and written to the other of two LDS
+//    buffers; 16-byte pieces XOR-swizzled by f(key) = 4 (key % 4) +
+//    (key / 4) % 4 in the 256-byte rows and (key / 2) % 8 in the RoPE rows.
+//  * Scores S^T[key][row]: 12 products per 32 keys, the tile rows as the A
+//    operand (8 of K^C, 4 of k^R).
+//  * Online softmax per row in the log2 domain with lazy rescale; a lane holds
+//    16 of each 32 keys' scores of its row, the other 16 are in lane ^ 32.
+//  * Values O^T[dim][row] += V^T P^T: the B operand is the lane's own
+//    probabilities (fp16), the A operand two ds_read_b64_tr_b16 of the V rows.
+// ---------------------------------------------------------------------------
+constexpr int kPxQTok = 128;                       // query tokens per work-group (4 waves x 32)
+constexpr int kPxKeys = 64;                        // keys per tile
+constexpr int kPxKcRow = 2 * kPxDH;                // bytes per K^C / V row
+constexpr int kPxRopeRow = 2 * kPxDR;              // bytes per k^R row
+constexpr int kPxRopeOff = kPxKeys * kPxKcRow;
+constexpr int kPxVOff = kPxRopeOff + kPxKeys * kPxRopeRow;
+constexpr int kPxTileBytes = kPxVOff + kPxKeys * kPxKcRow;   // 40 KB; two per work-group
+static_assert(2 * 2 * kPxTileBytes <= 160 * 1024, "two work-groups of two tile buffers per compute unit");
+
+struct PrefillXArgs {
+  const uint16_t* q;           // [T][H][192] bf16: q^C | q^R
+  const uint16_t* latent;      // [T][d_c + 64] bf16: c | k^R
+  const uint16_t* kc;          // [H][T][128] fp16
+  const uint16_t* vv;          // [H][T][128] fp16
+  const int32_t* seq_start;    // [T]
+  uint16_t* out;               // [T][H][128] bf16
+  int T, H, DC;
+  float scale_log2;            // tau log2(e)
+};
+
+__global__ __launch_bounds__(256, 2) void prefill_x_attn_kernel(PrefillXArgs a) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds[];  // two tile buffers
+  const int nblk = (a.T + kPxQTok - 1) / kPxQTok;
+  const int hh = blockIdx.y;
+  const int q0 = (nblk - 1 - static_cast<int>(blockIdx.x)) * kPxQTok;  // last blocks of the stream first
+  const int q_last = min(q0 + kPxQTok, a.T) - 1;
+  const int kbeg = min(max(a.seq_start[q0], 0), q0);                 // keys from here ...
+  const int kend = q_last + 1;                                       // ... to here (exclusive)
+  const int s_max = min(max(a.seq_start[q_last], kbeg), q_last);     // latest sequence start in the block
+  const int ntiles = (kend - kbeg + kPxKeys - 1) / kPxKeys;
+  const int DQ = a.DC + kPxDR;
+
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r32 = lane & 31, h = lane >> 5;
+  const int r16 = lane & 15, R1 = (lane >> 4) & 1;
+  // this lane's query row; rows past the stream repeat its last token and are not stored
+  const int t_row = q0 + 32 * w + r32;
+  const bool row_ok = t_row < a.T;
+  const int t_c = min(t_row, a.T - 1);
+  const int s_row = min(max(a.seq_start[t_c], kbeg), t_c);
+
+  f16x8_t qv[kPxDK / 16];
+  {
+    const uint16_t* qrow = a.q + (static_cast<int64_t>(t_c) * a.H + hh) * kPxDK + 8 * h;
+#pragma unroll
+    for (int c = 0; c < kPxDK / 16; ++c)
+      qv[c] = __builtin_bit_cast(f16x8_t, bf16x8_to_f16x8(*reinterpret_cast<const u32x4_t*>(qrow + 16 * c)));
+  }
+
+  // tile loads: K^C / V pieces pl of keys kl + 16 j, RoPE piece pr of keys kr + 32 j
+  constexpr int NKJ = kPxKeys * (kPxDH / 8) / 256, NRJ = kPxKeys * (kPxDR / 8) / 256;
+  const int kl = tid >> 4, pl = tid & 15, kr = tid >> 3, pr = tid & 7;
+  auto key_at = [&](int tile, int k) { return min(kbeg + tile * kPxKeys + k, kend - 1); };
+  const uint16_t* kc_h = a.kc + static_cast<int64_t>(hh) * a.T * kPxDH;
+  const uint16_t* vv_h = a.vv + static_cast<int64_t>(hh) * a.T * kPxDH;
+  u32x4_t nk[NKJ], nv[NKJ], nr[NRJ];
+  auto load_tile = [&](int tile) {
+#pragma unroll
+    for (int j = 0; j < NKJ; ++j) {
+      const int64_t key = key_at(tile, kl + 16 * j);
+      nk[j] = *reinterpret_cast<const u32x4_t*>(kc_h + key * kPxDH + 8 * pl);
+      nv[j] = *reinterpret_cast<const u32x4_t*>(vv_h + key * kPxDH + 8 * pl);
+    }
+#pragma unroll
+    for (int j = 0; j < NRJ; ++j)
+      nr[j] = *reinterpret_cast<const u32x4_t*>(a.latent + static_cast<int64_t>(key_at(tile, kr + 32 * j)) * DQ +
+                                                 a.DC + 8 * pr);
+  };
+  auto store_tile = [&](int buf) {
+    unsigned char* base = lds + buf * kPxTileBytes;
+#pragma unroll
+    for (int j = 0; j < NKJ; ++j) {
+      const int key = kl + 16 * j;
+      const int off = key * kPxKcRow + 16 * (pl ^ pf_lat_swz(key));
+      *reinterpret_cast<u32x4_t*>(base + off) = nk[j];
+      *reinterpret_cast<u32x4_t*>(base + kPxVOff + off) = nv[j];
+    }
+#pragma unroll
+    for (int j = 0; j < NRJ; ++j) {
+      const int key = kr + 32 * j;
+      *reinterpret_cast<u32x4_t*>(base + kPxRopeOff + key * kPxRopeRow + 16 * (pr ^ pf_rope_swz(key))) =
+          bf16x8_to_f16x8(nr[j]);
+    }
+  };
+
+  // per-lane LDS offsets (bytes within a tile buffer)
+  const int off_sk = r32 * kPxKcRow;                // score A: key row 32 kb + r32
+  const int swz_sk = pf_lat_swz(r32);
+  const int off_sr = kPxRopeOff + r32 * kPxRopeRow;
+  const int swz_sr = pf_rope_swz(r32);
+  // value A (transposed reads): rows 16 m + 4 h + r16 / 4 (+ 8), byte 8 (r16 % 2) of the piece
+  const int off_v = kPxVOff + (4 * h + (r16 >> 2)) * kPxKcRow + 8 * (r16 & 1);
+  const int vlo = 2 * R1 + ((r16 & 3) >> 1);  // low 2 bits of the logical piece
+
+  pf_f32x16_t o[kPxDH / 32];
+#pragma unroll
+  for (int db = 0; db < kPxDH / 32; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
+  float m_run = -1e30f, l_run = 0.f;  // finite start: a fully masked tile leaves both unchanged
+
+  load_tile(0);
+  store_tile(0);
+  __syncthreads();
+
+  for (int i = 0; i < ntiles; ++i) {
+    if (i + 1 < ntiles) load_tile(i + 1);
+    const unsigned char* tb = lds + (i & 1) * kPxTileBytes;
+    const int k_lo = kbeg + i * kPxKeys;
+
+    // ---- scores S^T[key][row] for keys k_lo + 32 kb + (0..31) ----
+    pf_f32x16_t s[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
+#pragma unroll
+    for (int c = 0; c < kPxDH / 16; ++c)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const f16x8_t av = *reinterpret_cast<const f16x8_t*>(tb + off_sk + 32 * kb * kPxKcRow +
+                                                              16 * ((2 * c + h) ^ swz_sk));
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, qv[c], s[kb], 0, 0, 0);
+      }
+#pragma unroll
+    for (int c = 0; c < kPxDR / 16; ++c)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const f16x8_t av = *reinterpret_cast<const f16x8_t*>(tb + off_sr + 32 * kb * kPxRopeRow +
+                                                              16 * ((2 * c + h) ^ swz_sr));
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, qv[kPxDH / 16 + c], s[kb], 0, 0, 0);
+      }
+    // keys outside [s_row, t_row] only in tiles that reach past the block's
+    // first token or start before its latest sequence start
+    if (k_lo + kPxKeys - 1 > q0 || k_lo < s_max) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = k_lo + 32 * kb + 8 * (r >> 2) + 4 * h + (r & 3);
+          if (key < s_row || key > t_c) s[kb][r] = -INFINITY;
+        }
+    }
+
+    // ---- online softmax (row = lane % 32; keys split between lanes L and L ^ 32) ----
+    float mt = s[0][0];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[kb][r]);
+    mt = pf_pair_max(mt) * a.scale_log2;
+    const float m_new = fmaxf(m_run, mt);
+    const bool grow = m_new > m_run + kLazyRescale;
+    const float alpha = grow ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.0f;
+    m_run = grow ? m_new : m_run;
+    l_run *= alpha;
+    if (__builtin_amdgcn_ballot_w64(grow)) {
+#pragma unroll
+      for (int db = 0; db < kPxDH / 32; ++db) o[db] *= alpha;
+    }
+    f16x8_t pb[2][2];  // [kb][16-key chunk m]: keys 16 m + 8 (e / 4) + 4 h + e % 4 of element e
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int m = 0; m < 2; ++m) {
+        float p[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][8 * m + e], a.scale_log2, -m_run));
+          l_run += p[e];
+        }
+        pb[kb][m] = __builtin_bit_cast(f16x8_t, u32x4_t{pack_f16x2(p[0], p[1]), pack_f16x2(p[2], p[3]),
+                                                        pack_f16x2(p[4], p[5]), pack_f16x2(p[6], p[7])});
+      }
+
+    // ---- values O^T[dim][row] += V^T P^T ----
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int m = 0; m < 2; ++m) {
+        const unsigned char* vp = tb + off_v + (32 * kb + 16 * m) * kPxKcRow;
+#pragma unroll
+        for (int db = 0; db < kPxDH / 32; ++db) {
+          // logical piece 4 db + vlo; rows +0 and +8 swizzle with 4 (r16 / 4) + h and + 2
+          const int p0 = 4 * (db ^ (r16 >> 2)) + (vlo ^ h);
+          const int p1 = 4 * (db ^ (r16 >> 2)) + (vlo ^ (h + 2));
+          const s16x4_t a0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) s16x4_t*)(vp + 16 * p0));
+          const s16x4_t a1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) s16x4_t*)(vp + 8 * kPxKcRow + 16 * p1));
+          const f16x8_t av = __builtin_bit_cast(f16x8_t, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
+          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, pb[kb][m], o[db], 0, 0, 0);
+        }
+      }
+
+    if (i + 1 < ntiles) store_tile((i + 1) & 1);
+    __syncthreads();
+  }
+
+  // ---- out = O / l in bf16: lane holds dims 32 db + 8 q + 4 h + 0..3 of its row ----
+  const float inv = 1.0f / pf_pair_sum(l_run);
+  if (row_ok) {
+    uint16_t* orow = a.out + (static_cast<int64_t>(t_row) * a.H + hh) * kPxDH + 4 * h;
+#pragma unroll
+    for (int db = 0; db < kPxDH / 32; ++db)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        *reinterpret_cast<u32x2_t*>(orow + 32 * db + 8 * q) =
+            u32x2_t{pack_bf16x2(o[db][4 * q] * inv, o[db][4 * q + 1] * inv),
+                    pack_bf16x2(o[db][4 * q + 2] * inv, o[db][4 * q + 3] * inv)};
+  }
+}
+
+}  // namespace egmla

@@ -227,11 +227,19 @@ def test_prefill_varlen_rejects_before_launch(L):
     assert call(d, 2, n, q=ctypes.c_void_p(258)) == B.ERR_INVALID_ARG  # misaligned
     assert call(d, 2, n, wsb=need - 1) == B.ERR_WORKSPACE
     assert call(d, 2, n, ws=ctypes.c_void_p(4100)) == B.ERR_WORKSPACE
-    # the MFMA prefill covers the d_c 128 / d_r 64 / 16-head bf16 layer only
-    for bad in (dims(num_heads=32), dims(latent_dim=512), dims(rope_dim=32), dims(dtype=B.FP32),
-                dims(v_head_dim=64)):
+    # the MFMA prefill covers bf16 layers with d_h = d_v = 128 and d_r = 64: the absorbed
+    # form for d_c 128 with 16 heads, the explicit form for any other head count and
+    # d_c a multiple of 64 (workspace: sequence starts, then K^C and V in fp16 per head)
+    for bad in (dims(latent_dim=96, gate_dim=96), dims(rope_dim=32), dims(dtype=B.FP32), dims(v_head_dim=64),
+                dims(head_dim=64)):
         assert call(bad, 2, n) == B.ERR_UNSUPPORTED
         assert L.eg_mla_prefill_varlen_workspace_size(ctypes.byref(bad), n) == 0
+    al = lambda x: (x + 255) // 256 * 256
+    for good, H in ((dims(num_heads=32), 32), (dims(latent_dim=512, gate_dim=512, num_heads=128), 128),
+                    (dims(latent_dim=256, gate_dim=256, num_heads=16), 16)):
+        need_x = L.eg_mla_prefill_varlen_workspace_size(ctypes.byref(good), n)
+        assert need_x == al(n * 4) + 2 * al(n * H * 128 * 2)
+        assert call(good, 2, n, wsb=need_x - 1) == B.ERR_WORKSPACE
 
 
 def test_decode_literal_rejects_before_launch(L):

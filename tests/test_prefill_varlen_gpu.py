@@ -1,6 +1,7 @@
-"""GPU parity of eg_mla_prefill_varlen (App. C Eq. (C.13), absorbed, with the
-latent-space gate of Sec. 3.1 Eq. (5)) against the fp64 oracle's single-sequence
-prefill, run sequence by sequence over the same packed inputs."""
+"""GPU parity of eg_mla_prefill_varlen (App. C Eq. (C.13), with the latent-space
+gate of Sec. 3.1 Eq. (5)) against the fp64 oracle's single-sequence prefill, run
+sequence by sequence over the same packed inputs: the absorbed form (d_c 128,
+16 heads) and the explicit form (the 128-head d_c 512 layer and other shapes)."""
 import numpy as np
 import pytest
 import torch
@@ -13,6 +14,7 @@ from parity import assert_close, say
 pytestmark = pytest.mark.gpu
 
 LAYER = W.WORKLOADS[1]  # 16 heads, d_c 128, d_r 64, bf16
+WIDE = W.WORKLOADS[4].replace(vocab=8192)  # 128 heads, d_c 512, d_r 64, bf16 (a smaller gate table)
 
 
 def run_varlen(pb):
@@ -91,3 +93,50 @@ def test_prefill_varlen_long_sequence_sampled(gpu):
                      rope_dim=wl.rope_dim, storage="bf16", page_table=np.zeros((len(rows), T // 64), np.int32)
                      + np.arange(T // 64, dtype=np.int32)[None, :], page_size=64, max_pages=T // 64)
     assert_close(got[rows], ref, "bf16", "prefill varlen T=4096 sampled")
+
+
+@pytest.mark.parametrize("lens", [
+    [1],                          # one token: the tile holds a single key
+    [17, 15],                     # a block straddling two sequences
+    [300],                        # several tiles, ragged last tile and block
+    [129, 127],                   # sequences straddling a 128-token block by one
+    [5, 0, 64, 1, 130, 0, 33],    # empty sequences, exact tiles, short ones
+    [700, 3, 300],                # long sequences around a short one
+])
+def test_prefill_varlen_explicit_matches_oracle(gpu, lens):
+    # the 128-head d_c 512 layer: projection to fp16 K^C, V, then attention per head
+    pb = W.generate_prefill_batch(WIDE, lens, seed=64)
+    say(f"prefill_varlen explicit lens={lens}")
+    assert_close(run_varlen(pb), oracle_varlen(pb), "bf16", f"prefill varlen explicit {lens}")
+
+
+def test_prefill_varlen_explicit_peaked(gpu):
+    # queries x 8 (exact in bf16): rows dominated by a few keys, where a key or value
+    # rounded to bf16 alone would exceed the element-wise bound
+    pb = W.generate_prefill_batch(WIDE, [300, 77], seed=65)
+    pb.q = W.f32_to_bf16_bits((orc.widen(pb.q, "bf16") * 8.0).astype(np.float32))
+    say("prefill_varlen explicit peaked q x8")
+    assert_close(run_varlen(pb), oracle_varlen(pb), "bf16", "prefill varlen explicit q x8")
+
+
+@pytest.mark.parametrize("heads,dc,lens", [(8, 256, [200, 57]), (16, 512, [150]), (32, 128, [97, 64])])
+def test_prefill_varlen_explicit_other_shapes(gpu, heads, dc, lens):
+    wl = WIDE.replace(heads=heads, latent_dim=dc, gate_dim=dc)
+    pb = W.generate_prefill_batch(wl, lens, seed=66)
+    say(f"prefill_varlen explicit H={heads} d_c={dc} lens={lens}")
+    assert_close(run_varlen(pb), oracle_varlen(pb), "bf16", f"prefill varlen explicit H{heads} dc{dc}")
+
+
+def test_prefill_varlen_explicit_long_sequence_sampled(gpu):
+    # 4096 tokens of the 128-head layer: every 97th row against the oracle's causal row
+    wl = WIDE
+    T = 4096
+    pb = W.generate_prefill_batch(wl, [T], seed=67)
+    say("prefill_varlen explicit T=4096 sampled rows")
+    got = run_varlen(pb)
+    rows = np.append(np.arange(0, T, 97), T - 1)
+    ref = orc.decode(pb.q[rows], pb.latent, pb.token_ids, pb.gate_table, pb.w_uk, pb.w_uv,
+                     (rows + 1).astype(np.int32), latent_dim=wl.latent_dim, head_dim=wl.head_dim,
+                     rope_dim=wl.rope_dim, storage="bf16", page_table=np.zeros((len(rows), T // 64), np.int32)
+                     + np.arange(T // 64, dtype=np.int32)[None, :], page_size=64, max_pages=T // 64)
+    assert_close(got[rows], ref, "bf16", "prefill varlen explicit T=4096 sampled")
