@@ -28,6 +28,23 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
 }
 
+typedef __attribute__((ext_vector_type(8))) _Float16 f16x8_t;
+typedef __attribute__((ext_vector_type(2))) _Float16 f16x2_t;
+
+// Two fp32 -> packed fp16 pair (lo in bits 0..15), round to nearest even.
+__device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, f16x2_t{static_cast<_Float16>(lo), static_cast<_Float16>(hi)});
+}
+
+// 8 bf16 values (16 bytes) to 8 fp16 values: exact for magnitudes between
+// 2^-14 and 65504 (a bf16 significand has 8 bits, an fp16 one 11).
+__device__ __forceinline__ u32x4_t bf16x8_to_f16x8(u32x4_t v) {
+  u32x4_t r;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) r[e] = pack_f16x2(bf16_lo(v[e]), bf16_hi(v[e]));
+  return r;
+}
+
 // Gated latent of one 16-byte chunk: word e of the result packs
 // bf16(lat.lo * gate.lo) and bf16(lat.hi * gate.hi) of word e.  Each product is
 // v_dot2_f32_bf16 of the latent word with the gate word's other half zeroed: a
@@ -97,6 +114,30 @@ __device__ __forceinline__ void gate_chunk_hilo(u32x4_t lat, u32x4_t gate, u32x4
         [h3] "v"(gate[3] & 0xffff0000u));
 #pragma unroll
   for (int e = 0; e < 4; ++e) lo[e] = pack_bf16x2(t[2 * e] - bf16_lo(hi[e]), t[2 * e + 1] - bf16_hi(hi[e]));
+}
+
+// Gated latent of one 16-byte chunk in fp16: the eight exact fp32 products
+// (formed as in gate_chunk), each rounded once to fp16.  The block ends with
+// 3 wait states (s_nop 2), so that the conversions after it may read the DOT
+// results.
+__device__ __forceinline__ u32x4_t gate_chunk_f16(u32x4_t lat, u32x4_t gate) {
+  float t[8];
+  asm("v_dot2_f32_bf16 %[t0], %[a0], %[l0], 0\n\t"
+      "v_dot2_f32_bf16 %[t1], %[a0], %[h0], 0\n\t"
+      "v_dot2_f32_bf16 %[t2], %[a1], %[l1], 0\n\t"
+      "v_dot2_f32_bf16 %[t3], %[a1], %[h1], 0\n\t"
+      "v_dot2_f32_bf16 %[t4], %[a2], %[l2], 0\n\t"
+      "v_dot2_f32_bf16 %[t5], %[a2], %[h2], 0\n\t"
+      "v_dot2_f32_bf16 %[t6], %[a3], %[l3], 0\n\t"
+      "v_dot2_f32_bf16 %[t7], %[a3], %[h3], 0\n\t"
+      "s_nop 2"
+      : [t0] "=&v"(t[0]), [t1] "=&v"(t[1]), [t2] "=&v"(t[2]), [t3] "=&v"(t[3]), [t4] "=&v"(t[4]),
+        [t5] "=&v"(t[5]), [t6] "=&v"(t[6]), [t7] "=&v"(t[7])
+      : [a0] "v"(lat[0]), [a1] "v"(lat[1]), [a2] "v"(lat[2]), [a3] "v"(lat[3]), [l0] "v"(gate[0] & 0xffffu),
+        [l1] "v"(gate[1] & 0xffffu), [l2] "v"(gate[2] & 0xffffu), [l3] "v"(gate[3] & 0xffffu),
+        [h0] "v"(gate[0] & 0xffff0000u), [h1] "v"(gate[1] & 0xffff0000u), [h2] "v"(gate[2] & 0xffff0000u),
+        [h3] "v"(gate[3] & 0xffff0000u));
+  return u32x4_t{pack_f16x2(t[0], t[1]), pack_f16x2(t[2], t[3]), pack_f16x2(t[4], t[5]), pack_f16x2(t[6], t[7])};
 }
 
 // Largest growth (log2 units) of a head's running maximum that an online

@@ -25,21 +25,6 @@
 
 namespace egmla {
 
-typedef __attribute__((ext_vector_type(8))) _Float16 f16x8_t;
-typedef __attribute__((ext_vector_type(2))) _Float16 f16x2_t;
-
-__device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
-  return __builtin_bit_cast(uint32_t, f16x2_t{static_cast<_Float16>(a), static_cast<_Float16>(b)});
-}
-
-// 8 bf16 values (16 bytes) to 8 fp16 values (exact within the fp16 range).
-__device__ __forceinline__ u32x4_t bf16x8_to_f16x8(u32x4_t v) {
-  u32x4_t r;
-#pragma unroll
-  for (int e = 0; e < 4; ++e) r[e] = pack_f16x2(bf16_lo(v[e]), bf16_hi(v[e]));
-  return r;
-}
-
 constexpr int kPxDH = 128, kPxDR = 64, kPxDK = kPxDH + kPxDR;  // key dims per head (K^C | k^R)
 
 // ---------------------------------------------------------------------------

@@ -13,9 +13,16 @@
 // values.
 //
 // Four launches: a map from each token to its sequence's first token; the
-// absorption (q_lat in bf16, with q^R, for every token); the attention kernel
+// absorption (q_lat in fp16, with q^R, for every token); the attention kernel
 // below, which writes o_lat / l in fp32; and the up-projection by W_UV per
 // head (o_lat as bf16 hi + lo).
+//
+// Precision: the attention runs on the fp16 MFMA.  q_lat is one rounding of
+// its fp32 sum to fp16, q^R and k^R convert from bf16 exactly, the gated
+// latent is one rounding of the exact fp32 product to fp16, and so is each
+// probability: 11-bit significands, where bf16 keys would need a second
+// (lo) product to keep rows dominated by a few keys within the element-wise
+// bound.  Values must stay below 65504 in magnitude.
 //
 // Attention kernel.  A work-group (4 waves; two per CU, whose barriers are
 // independent, so that one's softmax overlaps the other's products on the
@@ -26,19 +33,15 @@
 // first (last in the stream first).
 //  * Tile: 256 threads each load four 16-byte latent pieces with the matching
 //    gate pieces and two RoPE pieces of the next tile while the current one is
-//    computed; the gated latent (exact fp32 products) is written to the other
-//    of two LDS buffers as bf16 hi and the bf16 remainder lo (hi + lo is the
-//    product exactly; lo rows follow the hi rows).  Rows of 256 bytes hold the
-//    16-byte pieces XOR-swizzled by f(key) = 4 (key % 4) + (key / 4) % 4, RoPE
-//    rows of 128 bytes by (key / 2) % 8: the 16 lanes of a 16-byte read cycle
-//    and the 32 lanes of a transposed 8-byte read cycle each hit distinct banks.
+//    computed; the gated latent (fp16) and the RoPE key (fp16) are written to
+//    the other of two LDS buffers.  Rows of 256 bytes hold the 16-byte pieces
+//    XOR-swizzled by f(key) = 4 (key % 4) + (key / 4) % 4, RoPE rows of 128
+//    bytes by (key / 2) % 8: the 16 lanes of a 16-byte read cycle and the 32
+//    lanes of a transposed 8-byte read cycle each hit distinct banks.
 //  * Scores: wave w holds rows (tokens 2w, 2w + 1) x 16 heads = 32 rows, its
-//    query in registers as the B operand of v_mfma_f32_32x32x16_bf16 (lane:
-//    row lane % 32, dims 8 (lane / 32) + 16 c).  S^T[key][row] comes from 20
-//    products per 32 keys with the tile rows as the A operand: the latent part
-//    as hi and lo (so a score carries only the query's bf16 rounding, which is
-//    what lets rows dominated by a few keys meet the bound), the RoPE part
-//    once.
+//    query in registers as the B operand of v_mfma_f32_32x32x16_f16 (lane:
+//    row lane % 32, dims 8 (lane / 32) + 16 c).  S^T[key][row] comes from 12
+//    products per 32 keys with the tile rows as the A operand.
 //  * Online softmax per row in the log2 domain, lazy rescale (as the decode).
 //    A lane holds 16 of each 32 keys' scores of its row; the other 16 are in
 //    lane ^ 32 (one permlane32 swap for the maximum; the sums are combined
@@ -61,8 +64,8 @@ constexpr int kPfDC = 128, kPfDR = 64, kPfDQ = kPfDC + kPfDR;
 constexpr int kPfLatRow = 2 * kPfDC;    // bytes per key row of the gated latent
 constexpr int kPfRopeRow = 2 * kPfDR;   // bytes per key row of the RoPE key
 constexpr int kPfLatBytes = kPfKeys * kPfLatRow;
-constexpr int kPfRopeOff = 2 * kPfLatBytes;                       // after the hi and lo rows
-constexpr int kPfBufBytes = kPfRopeOff + kPfKeys * kPfRopeRow;    // one tile buffer (40 KB; two per work-group)
+constexpr int kPfRopeOff = kPfLatBytes;                           // after the latent rows
+constexpr int kPfBufBytes = kPfRopeOff + kPfKeys * kPfRopeRow;    // one tile buffer (24 KB; two per work-group)
 static_assert(2 * 2 * kPfBufBytes <= 160 * 1024, "two work-groups of two tile buffers per compute unit");
 constexpr int kPfUvTokens = 128;  // absorption and up-projection: tokens per chunk (4 waves x 32)
 constexpr int kPfSideChunks = 4;  // chunks per work-group: the head's weights are staged once for them
@@ -100,7 +103,7 @@ __global__ __launch_bounds__(256) void prefill_seqmap_kernel(const int32_t* __re
 }
 
 struct PrefillArgs {
-  const uint16_t* qf;          // [T][16][192] bf16: q_lat | q^R
+  const uint16_t* qf;          // [T][16][192] fp16: q_lat | q^R
   const uint16_t* latent;      // [T][192] bf16: c | k^R
   const int32_t* ids;          // [T]
   const uint16_t* gate;        // [V][128] bf16
@@ -129,11 +132,11 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_attn_mfma_kernel(Prefil
   const int head = r32 & 15;
   const int s_row = min(max(a.seq_start[t_c], kbeg), t_c);
 
-  bf16x8_t qv[kPfDQ / 16];
+  f16x8_t qv[kPfDQ / 16];
   {
     const uint16_t* qrow = a.qf + (static_cast<int64_t>(t_c) * kPfHeads + head) * kPfDQ + 8 * h;
 #pragma unroll
-    for (int c = 0; c < kPfDQ / 16; ++c) qv[c] = *reinterpret_cast<const bf16x8_t*>(qrow + 16 * c);
+    for (int c = 0; c < kPfDQ / 16; ++c) qv[c] = *reinterpret_cast<const f16x8_t*>(qrow + 16 * c);
   }
 
   // tile loads: latent/gate pieces pl of keys kl + 16 j, RoPE piece pr of keys kr + 32 j
@@ -166,15 +169,13 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_attn_mfma_kernel(Prefil
 #pragma unroll
     for (int j = 0; j < NLJ; ++j) {
       const int key = kl + 16 * j;
-      u32x4_t hi, lo;
-      gate_chunk_hilo(nl[j], ng[j], hi, lo);
-      *reinterpret_cast<u32x4_t*>(base + key * kPfLatRow + 16 * (pl ^ pf_lat_swz(key))) = hi;
-      *reinterpret_cast<u32x4_t*>(base + kPfLatBytes + key * kPfLatRow + 16 * (pl ^ pf_lat_swz(key))) = lo;
+      *reinterpret_cast<u32x4_t*>(base + key * kPfLatRow + 16 * (pl ^ pf_lat_swz(key))) = gate_chunk_f16(nl[j], ng[j]);
     }
 #pragma unroll
     for (int j = 0; j < NRJ; ++j) {
       const int key = kr + 32 * j;
-      *reinterpret_cast<u32x4_t*>(base + kPfRopeOff + key * kPfRopeRow + 16 * (pr ^ pf_rope_swz(key))) = nr[j];
+      *reinterpret_cast<u32x4_t*>(base + kPfRopeOff + key * kPfRopeRow + 16 * (pr ^ pf_rope_swz(key))) =
+          bf16x8_to_f16x8(nr[j]);
     }
   };
 
@@ -218,19 +219,17 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_attn_mfma_kernel(Prefil
     for (int c = 0; c < kPfDC / 16; ++c)
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        const int off = off_sl + 32 * kb * kPfLatRow + 16 * ((2 * c + h) ^ swz_sl);
-        const bf16x8_t av = *reinterpret_cast<const bf16x8_t*>(tb + off);
-        const bf16x8_t al = *reinterpret_cast<const bf16x8_t*>(tb + kPfLatBytes + off);
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qv[c], s[kb], 0, 0, 0);
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, qv[c], s[kb], 0, 0, 0);
+        const f16x8_t av =
+            *reinterpret_cast<const f16x8_t*>(tb + off_sl + 32 * kb * kPfLatRow + 16 * ((2 * c + h) ^ swz_sl));
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, qv[c], s[kb], 0, 0, 0);
       }
 #pragma unroll
     for (int c = 0; c < kPfDR / 16; ++c)
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        const bf16x8_t av = *reinterpret_cast<const bf16x8_t*>(tb + off_sr + 32 * kb * kPfRopeRow +
-                                                                16 * ((2 * c + h) ^ swz_sr));
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qv[kPfDC / 16 + c], s[kb], 0, 0, 0);
+        const f16x8_t av = *reinterpret_cast<const f16x8_t*>(tb + off_sr + 32 * kb * kPfRopeRow +
+                                                              16 * ((2 * c + h) ^ swz_sr));
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, qv[kPfDC / 16 + c], s[kb], 0, 0, 0);
       }
     // keys outside [s_row, t_row] (or past the block) only in tiles that reach
     // past the block's first token or start before its latest sequence start
@@ -261,7 +260,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_attn_mfma_kernel(Prefil
 #pragma unroll
       for (int db = 0; db < kPfDC / 32; ++db) o[db] *= alpha;
     }
-    bf16x8_t pb[2][2];  // [kb][16-key chunk m]: keys 16 m + 8 (e / 4) + 4 h + e % 4 of element e
+    f16x8_t pb[2][2];  // [kb][16-key chunk m]: keys 16 m + 8 (e / 4) + 4 h + e % 4 of element e
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -272,8 +271,8 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_attn_mfma_kernel(Prefil
           p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][8 * m + e], a.scale_log2, -m_run));
           l_run += p[e];
         }
-        pb[kb][m] = __builtin_bit_cast(bf16x8_t, u32x4_t{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
-                                                         pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7])});
+        pb[kb][m] = __builtin_bit_cast(f16x8_t, u32x4_t{pack_f16x2(p[0], p[1]), pack_f16x2(p[2], p[3]),
+                                                        pack_f16x2(p[4], p[5]), pack_f16x2(p[6], p[7])});
       }
 
     // ---- values O^T[dim][row] += C~^T P^T ----
@@ -291,9 +290,8 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_attn_mfma_kernel(Prefil
               (__attribute__((address_space(3))) s16x4_t*)(vp + 16 * p0));
           const s16x4_t a1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
               (__attribute__((address_space(3))) s16x4_t*)(vp + 8 * kPfLatRow + 16 * p1));
-          const bf16x8_t av =
-              __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
-          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[kb][m], o[db], 0, 0, 0);
+          const f16x8_t av = __builtin_bit_cast(f16x8_t, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
+          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, pb[kb][m], o[db], 0, 0, 0);
         }
       }
 
@@ -314,7 +312,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_attn_mfma_kernel(Prefil
   }
 }
 
-// q_lat[t, h, :] = W_UK[h]^T q^C[t, h, :] in bf16, and q^R copied, for up to
+// q_lat[t, h, :] = W_UK[h]^T q^C[t, h, :] in fp16, and q^R in fp16, for up to
 // 4 chunks of 128 tokens of one head per work-group (4 waves of 32 tokens; the
 // next chunk's rows load while a chunk computes and stores).  W_UK[h]
 // ([d_h][d_c] row-major, rows padded to 288 bytes) is staged in LDS once and
@@ -390,15 +388,15 @@ __global__ __launch_bounds__(256) void prefill_absorb_kernel(const uint16_t* __r
 #pragma unroll
         for (int qq = 0; qq < 4; ++qq)
           *reinterpret_cast<u32x2_t*>(dst + 32 * cb + 8 * qq) =
-              u32x2_t{pack_bf16x2(acc[cb][4 * qq], acc[cb][4 * qq + 1]),
-                      pack_bf16x2(acc[cb][4 * qq + 2], acc[cb][4 * qq + 3])};
+              u32x2_t{pack_f16x2(acc[cb][4 * qq], acc[cb][4 * qq + 1]),
+                      pack_f16x2(acc[cb][4 * qq + 2], acc[cb][4 * qq + 3])};
     }
     if (t0 + (tid >> 1) < T) {
       uint16_t* dr = qf + (static_cast<int64_t>(t0 + (tid >> 1)) * kPfHeads + hh) * kPfDQ + kPfDC + 32 * (tid & 1);
-      *reinterpret_cast<u32x4_t*>(dr) = r0;
-      *reinterpret_cast<u32x4_t*>(dr + 8) = r1;
-      *reinterpret_cast<u32x4_t*>(dr + 16) = r2;
-      *reinterpret_cast<u32x4_t*>(dr + 24) = r3;
+      *reinterpret_cast<u32x4_t*>(dr) = bf16x8_to_f16x8(r0);
+      *reinterpret_cast<u32x4_t*>(dr + 8) = bf16x8_to_f16x8(r1);
+      *reinterpret_cast<u32x4_t*>(dr + 16) = bf16x8_to_f16x8(r2);
+      *reinterpret_cast<u32x4_t*>(dr + 24) = bf16x8_to_f16x8(r3);
     }
   }
 }

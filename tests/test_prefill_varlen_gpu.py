@@ -61,6 +61,15 @@ def test_prefill_varlen_matches_oracle(gpu, lens):
     assert_close(got, ref, "bf16", f"prefill varlen {lens}")
 
 
+def test_prefill_varlen_peaked(gpu):
+    # queries x 8 (exact in bf16): rows dominated by a few keys, where a bf16 gated latent
+    # or query alone would exceed the element-wise bound
+    pb = W.generate_prefill_batch(LAYER, [300, 77], seed=68)
+    pb.q = W.f32_to_bf16_bits((orc.widen(pb.q, "bf16") * 8.0).astype(np.float32))
+    say("prefill_varlen peaked q x8")
+    assert_close(run_varlen(pb), oracle_varlen(pb), "bf16", "prefill varlen q x8")
+
+
 def test_prefill_varlen_equals_prefill_ref(gpu):
     # the same sequence through the MFMA path and the plain explicit-form kernels
     wl = LAYER
