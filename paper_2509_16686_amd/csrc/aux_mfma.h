@@ -27,10 +27,10 @@ constexpr int kAbsColsNarrow = 32;
 // Below this many work-groups the absorption takes the narrow column slices.
 constexpr int kAbsMinWorkGroups = 128;
 
-// SPLIT: instead of fp32 rows [B, H, DC + DR], write bf16 rows [B, H, 2 DC + DR]
-// = [q_lat hi | q^R | q_lat lo] with hi = bf16(q_lat) and lo = bf16(q_lat - hi),
-// the operands of the wide kernel's two query products.
-template <int DH, int BLOCKS, int COLS, bool SPLIT = false>
+// HALF: instead of fp32 rows [B, H, DC + DR], write 16-bit rows [B, H, DC + DR]
+// = [q_lat in fp16 (one rounding) | q^R in bf16 (copied)], the operands of the
+// wide kernel's fp16 latent product and exact bf16 RoPE product.
+template <int DH, int BLOCKS, int COLS, bool HALF = false>
 __global__ __launch_bounds__(256) void absorb_mfma_kernel(const uint16_t* __restrict__ q,
                                                           const uint16_t* __restrict__ w_uk,
                                                           float* __restrict__ qfull, int B, int H, int DC, int DR) {
@@ -117,11 +117,9 @@ __global__ __launch_bounds__(256) void absorb_mfma_kernel(const uint16_t* __rest
       for (int r = 0; r < 4; ++r) {
         const int b = b0 + rb * kAbsRows + 4 * g + r;
         if (b < B && c < DC) {
-          if constexpr (SPLIT) {
-            uint16_t* qs = reinterpret_cast<uint16_t*>(qfull) + (static_cast<int64_t>(b) * H + h) * (DQ + DC);
-            const uint16_t hi = f32_to_bf16(acc[rb][r]);
-            qs[c] = hi;
-            qs[DQ + c] = f32_to_bf16(acc[rb][r] - bf16_to_f32(hi));
+          if constexpr (HALF) {
+            reinterpret_cast<_Float16*>(qfull)[(static_cast<int64_t>(b) * H + h) * DQ + c] =
+                static_cast<_Float16>(acc[rb][r]);
           } else {
             qfull[(static_cast<int64_t>(b) * H + h) * DQ + c] = acc[rb][r];
           }
@@ -134,9 +132,9 @@ __global__ __launch_bounds__(256) void absorb_mfma_kernel(const uint16_t* __rest
     for (int rb = 0; rb < BLOCKS; ++rb) {
       const int b = b0 + rb * kAbsRows + rq_row;
       if (rq_row < kAbsRows && b < B) {
-        if constexpr (SPLIT)
-          *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(qfull) + (static_cast<int64_t>(b) * H + h) * (DQ + DC) +
-                                    DC + rq_col) = rq[rb];
+        if constexpr (HALF)
+          *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(qfull) + (static_cast<int64_t>(b) * H + h) * DQ + DC +
+                                    rq_col) = rq[rb];
         else
           *reinterpret_cast<float4*>(qfull + (static_cast<int64_t>(b) * H + h) * DQ + DC + rq_col) =
               make_float4(bf16_lo(rq[rb].x), bf16_hi(rq[rb].x), bf16_lo(rq[rb].y), bf16_hi(rq[rb].y));
@@ -147,8 +145,8 @@ __global__ __launch_bounds__(256) void absorb_mfma_kernel(const uint16_t* __rest
       const int bb = i / DR, r = i % DR;
       if (b0 + bb < B) {
         const uint16_t v = q[(static_cast<int64_t>(b0 + bb) * H + h) * DQin + DH + r];
-        if constexpr (SPLIT)
-          reinterpret_cast<uint16_t*>(qfull)[(static_cast<int64_t>(b0 + bb) * H + h) * (DQ + DC) + DC + r] = v;
+        if constexpr (HALF)
+          reinterpret_cast<uint16_t*>(qfull)[(static_cast<int64_t>(b0 + bb) * H + h) * DQ + DC + r] = v;
         else
           qfull[(static_cast<int64_t>(b0 + bb) * H + h) * DQ + DC + r] = bf16_to_f32(v);
       }

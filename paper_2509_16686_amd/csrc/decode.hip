@@ -97,7 +97,7 @@ __global__ __launch_bounds__(256) void absorb_kernel(const void* __restrict__ q,
 
 // Split-K bookkeeping shared by the split kernels.
 struct SplitArgs {
-  const float* qfull;         // [B, H, DQ] fp32; wide kernel: bf16 [B, H, DC + DQ] = [q hi | q^R | q lo]
+  const float* qfull;         // [B, H, DQ] fp32; wide kernel: 16-bit [B, H, DQ] = [q_lat fp16 | q^R bf16]
   const void* cache;          // [num_slots, DQ]
   const int32_t* ids;         // [num_slots]
   const void* gate;           // [V, DC]
@@ -529,7 +529,7 @@ eg_mla_status run_decode(const eg_mla_dims& d, const DecodePlan& p, int32_t batc
       dim3 ga(d.num_heads, row_blocks, (d.latent_dim + cols - 1) / cols);
       const uint16_t* q16 = static_cast<const uint16_t*>(q);
       const uint16_t* wuk16 = static_cast<const uint16_t*>(w_uk);
-      if (p.balanced)  // the wide kernel takes the query as bf16 hi + lo rows
+      if (p.balanced)  // the wide kernel takes the query as fp16 rows (q^R in bf16)
         hipLaunchKernelGGL((absorb_mfma_kernel<128, kAbsBlocks, kAbsCols, true>), ga, dim3(256), 0, stream, q16,
                            wuk16, qfull, batch, d.num_heads, d.latent_dim, d.rope_dim);
       else if (grouped)

@@ -29,6 +29,7 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 }
 
 typedef __attribute__((ext_vector_type(8))) _Float16 f16x8_t;
+typedef __attribute__((ext_vector_type(4))) _Float16 f16x4_t;
 typedef __attribute__((ext_vector_type(2))) _Float16 f16x2_t;
 
 // Two fp32 -> packed fp16 pair (lo in bits 0..15), round to nearest even.

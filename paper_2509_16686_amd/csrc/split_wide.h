@@ -8,10 +8,10 @@
 //   * Score wave s (w = s < 4) owns latent dims 128 s .. 128 s + 127 of every
 //     token: it loads its slice of a token's cache row and gate row straight
 //     from HBM into registers in the layout of the MFMA A operand (lane: token
-//     lane % 16, 8 consecutive dims), gates it there, writes the hi part into
-//     the unit's gated tile in LDS (row = token) and computes the partial
-//     scores S_s^T[token][head] of the 64 heads on v_mfma_f32_16x16x32_bf16,
-//     the absorbed query of its dims held in registers.  A chunk's loads for a
+//     lane % 16, 8 consecutive dims), gates it there, writes it into the
+//     unit's gated tile in LDS (row = token) and computes the partial scores
+//     S_s^T[token][head] of the 64 heads on v_mfma_f32_16x16x32_f16, the
+//     absorbed query of its dims held in registers.  A chunk's loads for a
 //     later unit go out as soon as the chunk has been gated, so the work-
 //     group's loads reach the texture unit spread over the step.
 //   * Value wave t (w = 4 + t) owns head tile t (heads 16 t .. 16 t + 15) for
@@ -19,7 +19,7 @@
 //     the four partials of its head tile and the RoPE part (its own product
 //     over the 64 RoPE dims), runs the online softmax of its 16 heads (log2
 //     domain, lazy rescale), and accumulates O^T[dim][head] += C~^T P^T for
-//     its dims and all 64 heads on v_mfma_f32_16x16x16_bf16, the A operand
+//     its dims and all 64 heads on v_mfma_f32_16x16x16_f16, the A operand
 //     read with ds_read_b64_tr_b16 from the gated tile.
 // Each role runs its own loop (so their registers do not add up) and both
 // meet the same barriers, one per unit of 16 tokens: the partials and gated
@@ -29,12 +29,13 @@
 // compute unit u + 1.  The partial-score and probability buffers are
 // double-buffered, the gated tiles triple-buffered.
 //
-// Precision.  The absorbed query is held as bf16 hi + lo, and each gated
-// latent c * g (an exact fp32 product of two bf16 values, 16 significant bits)
-// as bf16 hi + lo whose sum is the product exactly.  A score's latent part is
-// hi.q_hi + lo.q_hi + hi.q_lo (only the lo.lo product, below 2^-16 of the
-// score, is left out); the RoPE part (bf16 x bf16) is exact.  The value
-// product takes the gated latent's hi part and bf16 probabilities.
+// Precision.  The latent part of the scores and the values run on the fp16
+// MFMA: the absorbed query is one rounding of its fp32 sum to fp16, each gated
+// latent one rounding of the exact fp32 product c * g, each probability one
+// rounding to fp16 (11-bit significands: rows dominated by a few keys stay
+// within the element-wise bound, which bf16 operands would need hi + lo
+// products for).  The RoPE part (bf16 x bf16) is exact.  Magnitudes must stay
+// below 65504.
 //
 // The two head blocks of a 128-head layer run the same token range on the same
 // XCD (block ids 8 apart), so the second fetch of a token's rows hits that
@@ -68,9 +69,9 @@ struct WideCfg {
   // (mod 64): the 16-byte row writes and the transposed 8-byte reads of 4
   // rows are free of bank conflicts
   static constexpr int TS = DC + 16;
-  static constexpr int HT = 0;                                // [NHB][16][TS] bf16: gated hi
+  static constexpr int HT = 0;                                // [NHB][16][TS] fp16: gated latent
   static constexpr int SB = HT + NHB * TOK * TS * 2;          // [2][NV][NHT][64] f32x4: partial scores
-  static constexpr int PB = SB + 2 * NV * NHT * 64 * 16;      // [2][NHT][64] bf16 x 4: probabilities
+  static constexpr int PB = SB + 2 * NV * NHT * 64 * 16;      // [2][NHT][64] fp16 x 4: probabilities
   static constexpr int AL = PB + 2 * NHT * 64 * 8;            // [2][16][NHT] f32: rescale factor of head 16 ht + r
   static constexpr int FL = AL + 2 * HEADS * 4;               // [2][NHT] int: head tile rescaled
   static constexpr int LIST = FL + 64;                        // int2 (slot, id) per token
@@ -234,7 +235,7 @@ __device__ __forceinline__ void wide_wave(const SplitArgs& a, unsigned char* lds
   using C = WideCfg;
   constexpr int DC = C::DC, DQ = C::DQ, DW = C::DW, NHT = C::NHT, NV = C::NV, TS = C::TS, TOK = C::TOK;
   constexpr int NCH = C::NCH, NDB = C::NDB, NRC = C::NRC;
-  constexpr int QROW = DC + DQ;  // absorbed query row: [q hi | q^R | q lo]
+  constexpr int QROW = DQ;  // absorbed query row: [q_lat fp16 | q^R bf16]
   int2* list = reinterpret_cast<int2*>(lds + C::LIST);
   f32x4_t* sbuf = reinterpret_cast<f32x4_t*>(lds + C::SB);  // [2][NV][NHT][64]
   s16x4_t* pbuf = reinterpret_cast<s16x4_t*>(lds + C::PB);  // [2][NHT][64]
@@ -251,7 +252,7 @@ __device__ __forceinline__ void wide_wave(const SplitArgs& a, unsigned char* lds
 
   if constexpr (ROLE == 0) {
     // ======================= score wave s = idx =======================
-    bf16x8_t qh[NCH][NHT], ql[NCH][NHT];  // B operands: head 16 ht + r16, dims 8g .. 8g + 7 of chunk c
+    f16x8_t qh[NCH][NHT];  // B operands: head 16 ht + r16, dims 8g .. 8g + 7 of chunk c
     struct Unit {
       u32x4_t lat[NCH];
       u32x4_t gat[NCH];
@@ -261,10 +262,7 @@ __device__ __forceinline__ void wide_wave(const SplitArgs& a, unsigned char* lds
       for (int ht = 0; ht < NHT; ++ht) {
         const uint16_t* qrow = qfull + (static_cast<int64_t>(b) * a.H + qbase + 16 * ht) * QROW + dcol;
 #pragma unroll
-        for (int c = 0; c < NCH; ++c) {
-          qh[c][ht] = *reinterpret_cast<const bf16x8_t*>(qrow + 32 * c);
-          ql[c][ht] = *reinterpret_cast<const bf16x8_t*>(qrow + DQ + 32 * c);
-        }
+        for (int c = 0; c < NCH; ++c) qh[c][ht] = *reinterpret_cast<const f16x8_t*>(qrow + 32 * c);
       }
     };
     auto chunk = [&](int, int nunits) {
@@ -292,20 +290,13 @@ __device__ __forceinline__ void wide_wave(const SplitArgs& a, unsigned char* lds
         next_rows(u + D);
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
-          u32x4_t hi, lo;
-          gate_chunk_hilo(U.lat[c], U.gat[c], hi, lo);
+          const u32x4_t gv = gate_chunk_f16(U.lat[c], U.gat[c]);
           issue_chunk(U, c);  // unit u + D into the registers just consumed
-          *reinterpret_cast<u32x4_t*>(tw + 32 * c) = hi;
-          const bf16x8_t h = __builtin_bit_cast(bf16x8_t, hi), l = __builtin_bit_cast(bf16x8_t, lo);
+          *reinterpret_cast<u32x4_t*>(tw + 32 * c) = gv;
+          const f16x8_t h = __builtin_bit_cast(f16x8_t, gv);
 #pragma unroll
           for (int ht = 0; ht < NHT; ++ht)
-            acc[ht] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(h, qh[c][ht], acc[ht], 0, 0, 0);
-#pragma unroll
-          for (int ht = 0; ht < NHT; ++ht)
-            acc[ht] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(l, qh[c][ht], acc[ht], 0, 0, 0);
-#pragma unroll
-          for (int ht = 0; ht < NHT; ++ht)
-            acc[ht] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(h, ql[c][ht], acc[ht], 0, 0, 0);
+            acc[ht] = __builtin_amdgcn_mfma_f32_16x16x32_f16(h, qh[c][ht], acc[ht], 0, 0, 0);
         }
         const int k = u & 1;
 #pragma unroll
@@ -399,7 +390,9 @@ __device__ __forceinline__ void wide_wave(const SplitArgs& a, unsigned char* lds
           for (int d = 0; d < 4; ++d)
 #pragma unroll
             for (int ht = 0; ht < NHT; ++ht)
-              o[d0 + d][ht] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(at[d], pb[ht], o[d0 + d][ht], 0, 0, 0);
+              o[d0 + d][ht] = __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(f16x4_t, at[d]),
+                                                                    __builtin_bit_cast(f16x4_t, pb[ht]),
+                                                                    o[d0 + d][ht], 0, 0, 0);
         }
       };
       // after barrier u: the softmax of head tile t over unit u, then the
@@ -441,7 +434,7 @@ __device__ __forceinline__ void wide_wave(const SplitArgs& a, unsigned char* lds
         }
         // B operand of the value product: k = token 4g + i, j = head r16
         pbuf[(k * NHT + idx) * 64 + lane] =
-            __builtin_bit_cast(s16x4_t, u32x2_t{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3])});
+            __builtin_bit_cast(s16x4_t, u32x2_t{pack_f16x2(p[0], p[1]), pack_f16x2(p[2], p[3])});
         if (g == 0) abuf[(k * 16 + r16) * NHT + idx] = alpha;
         const uint64_t any = __builtin_amdgcn_ballot_w64(grow);
         if (lane == 0) fbuf[k * NHT + idx] = any != 0;
