@@ -326,7 +326,10 @@ hipError_t set_lds(K kernel, size_t bytes) {
 
 // Id-sliced kernel: waves per work-group and units in flight per wave.
 constexpr int kSliceWaves = 4;
-constexpr int kSliceDepth = 2;
+#ifndef EGMLA_SLICE_DEPTH
+#define EGMLA_SLICE_DEPTH 2
+#endif
+constexpr int kSliceDepth = EGMLA_SLICE_DEPTH;
 
 template <int DC>
 hipError_t launch_combine_dc(dim3 grid, hipStream_t stream, const float* pm, const float* po, const uint16_t* wv,

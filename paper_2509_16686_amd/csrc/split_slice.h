@@ -23,21 +23,22 @@
 //   * loads whole 128-byte lines: each latent and gate instruction covers 4
 //     tokens x 256 bytes (16 lanes per token, 16 bytes each), each RoPE-key
 //     instruction 8 tokens x 128 bytes;
-//   * gates in fp32 (exact product of two bf16 values) and stores the gated
-//     unit row-major ([token][latent hi | RoPE key | latent lo]) in its own
-//     LDS tile: the product rounded to bf16 (hi) and the bf16 remainder (lo),
-//     whose sum is the product exactly;
+//   * gates in fp32 (exact product of two bf16 values), rounds once to fp16
+//     and stores the gated unit row-major ([token][latent fp16 | RoPE key
+//     bf16]) in its own LDS tile;
 //   * reads the tile back in the layout of the MFMA A operand (lane: token
 //     lane % 16, 16 bytes = 8 consecutive dims of a 32-dim chunk) and
-//     computes S^T[token][head] with v_mfma_f32_16x16x32_bf16: the fp32
-//     absorbed query q enters as bf16 hi + lo, and the latent part of a score
-//     is hi.q_hi + hi.q_lo + lo.q_hi (only the lo.lo product, below 2^-16 of
-//     the score, is left out); the RoPE query (a stored bf16 value) once;
+//     computes S^T[token][head]: the latent part on v_mfma_f32_16x16x32_f16
+//     with the absorbed query rounded once to fp16, the RoPE part on
+//     v_mfma_f32_16x16x32_bf16 (bf16 x bf16: exact);
 //   * runs the online softmax on the accumulator layout (lane: one head, 4
 //     tokens), rescaling only when a head's maximum grows by more than 2^8;
 //   * reads each 16-dim block of the latent part with ds_read_b64_tr_b16,
-//     whose 16-lane transpose is the A operand of v_mfma_f32_16x16x16_bf16,
-//     and accumulates O^T[dim][head] += C~^T x P^T.
+//     whose 16-lane transpose is the A operand of v_mfma_f32_16x16x16_f16,
+//     and accumulates O^T[dim][head] += C~^T x P^T (P in fp16).
+// fp16's 11-bit significands keep rows dominated by a few keys within the
+// element-wise bound with one product per chunk, where bf16 operands needed
+// hi + lo products; magnitudes must stay below 65504.
 // Every global load of a unit depends only on the LDS list and is issued D
 // units ahead of its use, unconditionally (indexes past the list repeat its
 // last token), so the compiler's wait counters track each unit.
@@ -61,7 +62,7 @@ struct SsplitCfg {
   static constexpr int RPT = DR / 8;                 // lanes per token of a RoPE load
   static constexpr int TPR = RPT > 0 ? 64 / RPT : 1; // tokens per RoPE load instruction
   static constexpr int NRI = RPT > 0 ? 16 / TPR : 0; // RoPE load instructions per unit
-  static constexpr int TS = DQ + DC + 8;             // tile row: latent hi | RoPE key | latent lo | 16 bytes of padding
+  static constexpr int TS = DQ + 8;                  // tile row: latent (fp16) | RoPE key (bf16) | 16 bytes of padding
   static constexpr int ROWS = kMaxScanTokens / 256;  // scan rows of a work item, at most
   static constexpr int RPW = ROWS / NW;              // scan rows per wave, at most
   static constexpr int LDS_LIST = kMaxScanTokens * 8;            // slot + id of every kept token
@@ -416,8 +417,8 @@ __global__ __launch_bounds__(NW * 64, 2) void split_slice_kernel(SplitArgs a) {
       }
     }
   }
-  // query chunks: absorbed query as bf16 hi + lo, RoPE query (a stored bf16 value: exact)
-  bf16x8_t qh[NC], ql[NC];
+  // query chunks: absorbed query in fp16, RoPE query (a stored bf16 value: exact)
+  f16x8_t qh[NC];
   bf16x8_t qr[NR > 0 ? NR : 1];
   if constexpr (FUSED) {
     __syncthreads();  // the list is complete (and the absorption's LDS is free)
@@ -461,11 +462,7 @@ __global__ __launch_bounds__(NW * 64, 2) void split_slice_kernel(SplitArgs a) {
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float x = xq[2 * c + (e >> 2)][e & 3];
-        qh[c][e] = static_cast<__bf16>(x);
-        ql[c][e] = static_cast<__bf16>(x - static_cast<float>(qh[c][e]));
-      }
+      for (int e = 0; e < 8; ++e) qh[c][e] = static_cast<_Float16>(xq[2 * c + (e >> 2)][e & 3]);
     }
   } else {
 #pragma unroll
@@ -474,12 +471,8 @@ __global__ __launch_bounds__(NW * 64, 2) void split_slice_kernel(SplitArgs a) {
                         qraw[2 * c + 1].x, qraw[2 * c + 1].y, qraw[2 * c + 1].z, qraw[2 * c + 1].w};
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      if (c < NC) {
-        qh[c][e] = static_cast<__bf16>(x[e]);
-        ql[c][e] = static_cast<__bf16>(x[e] - static_cast<float>(qh[c][e]));
-      } else {
-        qr[c - NC][e] = static_cast<__bf16>(x[e]);
-      }
+      if (c < NC) qh[c][e] = static_cast<_Float16>(x[e]);
+      else qr[c - NC][e] = static_cast<__bf16>(x[e]);
     }
   }
   }
@@ -513,14 +506,10 @@ __global__ __launch_bounds__(NW * 64, 2) void split_slice_kernel(SplitArgs a) {
     uint16_t* tread = tile + (4 * g + (r16 >> 2)) * TS + 4 * (r16 & 3);
     auto process = [&](SliceRegs<NLI, NRI>& rg, int i, bool refill) {
       const int nt = ntok - (w + i * NW) * 16;  // valid tokens of the unit (>= 1)
-      // gate the latent (hi and lo); stage the unit row-major in this wave's tile
+      // gate the latent (fp16); stage the unit row-major in this wave's tile
 #pragma unroll
-      for (int c = 0; c < NLI; ++c) {
-        u32x4_t hi, lo;
-        gate_chunk_hilo(rg.lat[c], rg.gat[c], hi, lo);
-        *reinterpret_cast<u32x4_t*>(tile + (TPL * c + lt) * TS + lc) = hi;
-        *reinterpret_cast<u32x4_t*>(tile + (TPL * c + lt) * TS + DQ + lc) = lo;
-      }
+      for (int c = 0; c < NLI; ++c)
+        *reinterpret_cast<u32x4_t*>(tile + (TPL * c + lt) * TS + lc) = gate_chunk_f16(rg.lat[c], rg.gat[c]);
 #pragma unroll
       for (int c = 0; c < NRI; ++c) *reinterpret_cast<u32x4_t*>(tile + (TPR * c + rt) * TS + DC + rcol) = rg.rop[c];
       // this unit's registers are free: issue unit i + D into them
@@ -530,11 +519,8 @@ __global__ __launch_bounds__(NW * 64, 2) void split_slice_kernel(SplitArgs a) {
       f32x4_t acc = {0.f, 0.f, 0.f, 0.f}, acc2 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int c = 0; c < NC; ++c) {
-        const bf16x8_t av = *reinterpret_cast<const bf16x8_t*>(tile + r16 * TS + c * 32 + g * 8);
-        const bf16x8_t al = *reinterpret_cast<const bf16x8_t*>(tile + r16 * TS + DQ + c * 32 + g * 8);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, qh[c], acc, 0, 0, 0);
-        acc2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, qh[c], acc2, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, ql[c], acc, 0, 0, 0);
+        const f16x8_t av = *reinterpret_cast<const f16x8_t*>(tile + r16 * TS + c * 32 + g * 8);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(av, qh[c], acc, 0, 0, 0);
       }
 #pragma unroll
       for (int rc = 0; rc < NR; ++rc) {
@@ -568,9 +554,7 @@ __global__ __launch_bounds__(NW * 64, 2) void split_slice_kernel(SplitArgs a) {
         p[q] = __builtin_amdgcn_exp2f(x[q] - m_run);  // masked: exp2(-inf) = 0
         l_run += p[q];
       }
-      const uint32_t pb01 = pack_bf16x2(p[0], p[1]);
-      const uint32_t pb23 = pack_bf16x2(p[2], p[3]);
-      const s16x4_t pb = __builtin_bit_cast(s16x4_t, u32x2_t{pb01, pb23});
+      const f16x4_t pb = __builtin_bit_cast(f16x4_t, u32x2_t{pack_f16x2(p[0], p[1]), pack_f16x2(p[2], p[3])});
 
       // O^T[dim][head] += C~^T[dim][token] x P^T[token][head], 16 dims at a
       // time.  Lane r16 of group g reads dims 16 db + 4 (r16 % 4) .. + 3 of
@@ -580,7 +564,7 @@ __global__ __launch_bounds__(NW * 64, 2) void split_slice_kernel(SplitArgs a) {
       for (int db = 0; db < NB; ++db) {
         const s16x4_t at =
             __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t*)(tread + db * 16));
-        o[db] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(at, pb, o[db], 0, 0, 0);
+        o[db] = __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(f16x4_t, at), pb, o[db], 0, 0, 0);
       }
       // every lane's reads of the tile are done before the next unit overwrites it
       wave_lds_sync();
