@@ -8,18 +8,19 @@
 //   * loads its chunks of each token's row straight into the layout of the
 //     MFMA A operand (lane: token lane%16 of a 16-token half, 16 bytes = 8
 //     consecutive dims), the matching 16 bytes of the token's gate row, and
-//     gates in fp32 (exact product), rounding the gated latent to bf16 once;
+//     gates in fp32 (exact product), rounding the gated latent to fp16 once;
 //   * computes its partial scores S^T[token][head] over its dims with
-//     v_mfma_f32_16x16x32_bf16; the fp32 absorbed query enters as bf16
-//     hi + lo (two products), so a score carries only the rounding of the
-//     gated latent, and the RoPE part is exact;
+//     v_mfma_f32_16x16x32_f16, the fp32 absorbed query rounded once to fp16
+//     (11-bit significands: rows dominated by a few keys stay within the
+//     element-wise bound; magnitudes must stay below 65504), and the RoPE
+//     part with v_mfma_f32_16x16x32_bf16 (bf16 x bf16: exact);
 //   * adds the partial scores of all waves through LDS (double-buffered, one
 //     barrier per tile), so every wave holds the full scores;
 //   * runs the online softmax on the accumulator layout (lane: one head, 4
 //     tokens per half); the probabilities are exactly the B operand of the
 //     value product, so P never leaves registers;
-//   * accumulates O^T[dim][head] += C~^T x P^T for its own dims, reading the
-//     transposed gated latent it wrote to its own LDS region.
+//   * accumulates O^T[dim][head] += C~^T x P^T (fp16) for its own dims,
+//     reading the transposed gated latent it wrote to its own LDS region.
 // The waves' dims are disjoint and their softmax statistics identical, so
 // each writes its part of the split's partial result directly.
 //
@@ -43,7 +44,7 @@ struct DsplitCfg {
   static constexpr int RPW = NRC > 0 ? 1 : 0;          // RoPE chunk slots per wave (waves < NRC own theirs)
   static constexpr int NDB = CPW * 2;                  // 16-dim blocks of the value product per wave
   static constexpr int kDepth = DC == 128 ? 4 : 3;     // tiles in flight per wave
-  static constexpr int CT_STRIDE = 40;                 // 32 token slots + 8 pad (bf16 elements)
+  static constexpr int CT_STRIDE = 40;                 // 32 token slots + 8 pad (16-bit elements)
   static constexpr int LDS_CT = NW * CPW * 32 * CT_STRIDE * 2;
   static constexpr int LDS_SC = 2 * NW * 64 * 8 * 4;   // partial scores, double-buffered
   static constexpr int LDS_TOK = kMaxSplitTokensDevice * 8;  // slot + id of every token of the split
@@ -101,7 +102,7 @@ __global__ __launch_bounds__((DsplitCfg<DC, DR>::NW * 64)) void split_mfma_kerne
   }
   // Waves without a RoPE chunk of their own use a zero RoPE query, so their
   // (duplicate) RoPE product adds exactly zero and nothing depends on a branch.
-  bf16x8_t qh[CPW], ql[CPW];
+  f16x8_t qh[CPW];
   bf16x8_t qr = {};
   {
     const float* qrow = a.qfull + (static_cast<int64_t>(b) * a.H + hg * 16 + r16) * DQ + g * 8;
@@ -112,10 +113,7 @@ __global__ __launch_bounds__((DsplitCfg<DC, DR>::NW * 64)) void split_mfma_kerne
       const float4 x1 = *reinterpret_cast<const float4*>(p + 4);
       const float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        qh[c][e] = static_cast<__bf16>(x[e]);
-        ql[c][e] = static_cast<__bf16>(x[e] - static_cast<float>(qh[c][e]));
-      }
+      for (int e = 0; e < 8; ++e) qh[c][e] = static_cast<_Float16>(x[e]);
     }
     if constexpr (RPW > 0) {
       const float* p = qrow + DC + rope_chunk * 32;
@@ -194,18 +192,17 @@ __global__ __launch_bounds__((DsplitCfg<DC, DR>::NW * 64)) void split_mfma_kerne
           for (int e = 0; e < 4; ++e) {
             const float p0 = bf16_lo(r.lat[hf][c][e]) * bf16_lo(r.gat[hf][c][e]);
             const float p1 = bf16_hi(r.lat[hf][c][e]) * bf16_hi(r.gat[hf][c][e]);
-            pk[e] = pack_bf16x2(p0, p1);
+            pk[e] = pack_f16x2(p0, p1);
           }
           const u32x4_t hv = {pk[0], pk[1], pk[2], pk[3]};
-          const bf16x8_t av = __builtin_bit_cast(bf16x8_t, hv);
+          const f16x8_t av = __builtin_bit_cast(f16x8_t, hv);
           uint16_t* col = ct + (c * 32 + g * 8) * CTS + pos;
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             col[(2 * e) * CTS] = static_cast<uint16_t>(pk[e] & 0xffffu);
             col[(2 * e + 1) * CTS] = static_cast<uint16_t>(pk[e] >> 16);
           }
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, qh[c], acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, ql[c], acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(av, qh[c], acc, 0, 0, 0);
         }
         if constexpr (RPW > 0)
           acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, r.rop[hf][0]), qr, acc, 0, 0, 0);
@@ -245,12 +242,12 @@ __global__ __launch_bounds__((DsplitCfg<DC, DR>::NW * 64)) void split_mfma_kerne
       const float alpha = exp2f(m_run - m_new);
       m_run = m_new;
       float psum = 0.f;
-      bf16x8_t pb;
+      f16x8_t pb;
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         const float p = exp2f(sv[i] - m_new);
         psum += p;
-        pb[i] = static_cast<__bf16>(p);
+        pb[i] = static_cast<_Float16>(p);
       }
       l_run = l_run * alpha + psum;
 #pragma unroll
@@ -260,8 +257,8 @@ __global__ __launch_bounds__((DsplitCfg<DC, DR>::NW * 64)) void split_mfma_kerne
       wave_lds_sync();
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
-        const bf16x8_t av = *reinterpret_cast<const bf16x8_t*>(ct + (db * 16 + r16) * CTS + g * 8);
-        o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, pb, o[db], 0, 0, 0);
+        const f16x8_t av = *reinterpret_cast<const f16x8_t*>(ct + (db * 16 + r16) * CTS + g * 8);
+        o[db] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av, pb, o[db], 0, 0, 0);
       }
       wave_lds_sync();
     }
