@@ -279,9 +279,14 @@ eg_mla_status eg_mla_prefill_ref(const eg_mla_dims* dims, int32_t seq_len, const
  * sequence,
  *   out[t,h] = W_UV[h] sum_j softmax_j(tau (q_lat[t,h].c~_j + q^R[t,h].k^R_j)) c~_j,
  *   q_lat[t,h] = W_UK[h]^T q^C[t,h],  c~_j = c_j (.) G[token_ids[j]].
- * MFMA kernels for bf16 storage with 16 heads, d_h = d_v = d_c = 128 and
- * d_r = 64 (the d_c 128 layer); every other shape is EG_MLA_ERR_UNSUPPORTED
- * (eg_mla_prefill_ref covers any shape, one sequence at a time).
+ * MFMA kernels for bf16 storage with d_h = d_v = 128 and d_r = 64: the
+ * absorbed form for d_c = 128 with 16 heads (all heads share the gated latent
+ * as key and value), the explicit form of App. C Eq. (C.2), (C.6) for any
+ * other head count and d_c a multiple of 64 (K^C = W_UK[h] c~ and
+ * V = W_UV[h] c~ per head, then attention per head; 3.4x fewer flops per pair
+ * than the absorbed form at d_c 512).  Other shapes: EG_MLA_ERR_UNSUPPORTED
+ * (eg_mla_prefill_ref covers any shape, one sequence at a time).  The matrix
+ * products take fp16 operands (values below 65504 in magnitude).
  *
  *   cu_seqlens [batch + 1] int32 (device): sequence b is tokens
  *       cu_seqlens[b] .. cu_seqlens[b+1]-1; cu_seqlens[0] = 0,
@@ -292,8 +297,9 @@ eg_mla_status eg_mla_prefill_ref(const eg_mla_dims* dims, int32_t seq_len, const
  *       (rows as eg_mla_append writes them); token_ids [total];
  *   gate_table, w_uk, w_uv as for decode;  out [total, H, d_v].
  *   workspace: eg_mla_prefill_varlen_workspace_size bytes, 256-byte aligned
- *       (per-token sequence starts, the absorbed queries in bf16 and the
- *       normalised latent outputs in fp32).
+ *       (per-token sequence starts; absorbed form: the absorbed queries in
+ *       fp16 and the normalised latent outputs in fp32, [T][H][d_c] each;
+ *       explicit form: K^C and V in fp16, [H][T][128] each).
  * Pointers 16-byte aligned.  total_tokens == 0 is a no-op.
  * ------------------------------------------------------------------------- */
 size_t eg_mla_prefill_varlen_workspace_size(const eg_mla_dims* dims, int32_t total_tokens);
