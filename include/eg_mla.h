@@ -177,13 +177,13 @@ eg_mla_status eg_mla_append_ws(const eg_mla_dims* dims, int32_t n_tokens, int32_
  *   out           [B, H, d_v]  in the storage type
  *
  * Arithmetic (bf16 storage, MFMA path): each gated latent is the exact fp32
- * product of two bf16 values, held as bf16 hi + lo (lo the exact remainder);
- * scores are bf16 x bf16 products accumulated in fp32 with the absorbed query
- * also split into hi + lo (latent part hi.q_hi + hi.q_lo + lo.q_hi; the RoPE
- * part exact); the value sum takes the gated latent's hi part and the
- * probabilities rounded to bf16; the split merge is fp32 and the
- * up-projection takes the merged latent as bf16 hi + lo.  The VALU path
- * computes in fp32.  The call is asynchronous on `stream`; calls that share a
+ * product of two bf16 values rounded once to fp16, and the absorbed query
+ * (fp32) is rounded once to fp16; the latent part of a score is one fp16
+ * product accumulated in fp32, the RoPE part bf16 x bf16 (exact); the value
+ * sum takes the fp16 gated latent and the probabilities rounded to fp16; the
+ * split merge is fp32 and the up-projection takes the merged latent as bf16
+ * hi + lo.  Queries, latents and their products must stay below 65504 in
+ * magnitude (fp16's range).  The VALU path computes in fp32.  The call is asynchronous on `stream`; calls that share a
  * workspace must be ordered (same stream or synchronised).
  * ------------------------------------------------------------------------- */
 size_t eg_mla_decode_workspace_size(const eg_mla_dims* dims, int32_t batch, int32_t max_pages_per_seq,
