@@ -164,10 +164,10 @@ def test_balanced_schedule_dc512(gpu, case):
 
 def test_peaked_logits_dc512(gpu):
     # query x 8: logits of standard deviation about 8, so the softmax is sharp
-    # and a score error of 2^-9 relative moves the output by more than the bar;
-    # the 128-head kernel must take the query and the gated latent as bf16 hi +
-    # lo.  Running maxima also grow by more than 2^8 between the tiles of a
-    # range, so the kernel rescales its accumulators.
+    # and a score error of 2^-9 relative (one bf16 rounding of either operand)
+    # moves the output by more than the bar; the 128-head kernel's fp16
+    # operands (2^-12) stay within it.  Running maxima also grow by more than
+    # 2^8 between the tiles of a range, so the kernel rescales its accumulators.
     wl = W.WORKLOADS[4].replace(name="peaked_dc512", batch=4, seq_len_range=(2500, 3500), seed=46)
     inp = W.generate(wl)
     inp.q[:] = W.f32_to_bf16_bits(W.bf16_bits_to_f32(inp.q) * np.float32(8.0))
