@@ -286,10 +286,11 @@ __global__ __launch_bounds__(256) void append_mfma_kernel(const uint16_t* __rest
 //    B: the token row, the same k; one A serves NTG token blocks); the 4
 //    waves' sums are added in LDS in wave order and stored as fp32
 //    part[ks][t][o].
-//  Pass 2: d_c / 2 threads per token add the slices' sums in slice order
-//    (thread l: latent outputs 2l, 2l + 1, and for l < d_r / 2 the RoPE pair
-//    l), apply the latent RMSNorm and the rotation, and write the row and the
-//    id.
+//  Pass 2: a wave per token (d_c 128; d_c 512 with few slices, 4 latent
+//    pairs per lane) or a work-group per token (d_c 512 with many slices, a
+//    pair per thread) adds the slices' sums in slice order (lane l: latent
+//    pairs l + T i, and for l < d_r / 2 the RoPE pair l), applies the latent
+//    RMSNorm and the rotation, and writes the row and the id.
 // Every load is in bounds: token rows past n repeat the last token and are not
 // stored.
 // ---------------------------------------------------------------------------
@@ -306,6 +307,7 @@ constexpr int kAppGemmTarget = EGMLA_APPEND_GEMM_TARGET;   // the same for the t
 #define EGMLA_APPEND_GEMM_MIN (256 * 576)
 #endif
 constexpr int64_t kAppGemmMin = EGMLA_APPEND_GEMM_MIN;  // outputs (tokens x (d_c + d_r)) from which the tiled product pays
+constexpr int kAppFinishWaveSlices = 4;  // d_c 512: pass 2 takes a wave per token up to this many slices
 constexpr int kAppSplitMax128 = 2048;   // d_c 128: largest call taken by the split passes (measured crossover)
 constexpr int kAppSplitMax512 = 1 << 20;  // d_c 512: every call (the one-pass kernel is the general one)
 
@@ -487,7 +489,7 @@ __global__ __launch_bounds__(256, 2) void append_gemm_kernel(const uint16_t* __r
   }
 }
 
-template <int DC, int DR>
+template <int DC, int DR, int TPT>
 __global__ __launch_bounds__(256) void append_finish_kernel(const float* __restrict__ part, int nks,
                                                             const int32_t* __restrict__ token_ids,
                                                             const int32_t* __restrict__ positions,
@@ -495,8 +497,10 @@ __global__ __launch_bounds__(256) void append_finish_kernel(const float* __restr
                                                             const uint16_t* __restrict__ kv_norm_w, float theta,
                                                             uint16_t* __restrict__ cache, int32_t* __restrict__ ids,
                                                             int64_t num_slots, int n) {
-  constexpr int DQ = DC + DR, TPT = DC / 2, TPB = 256 / TPT, WPT = TPT / 64;
-  static_assert(TPT % 64 == 0 && 256 % TPT == 0 && DR / 2 <= TPT, "token groups are whole waves");
+  // TPT threads per token, each with NPL latent pairs (l + TPT i) and, for
+  // l < d_r / 2, the RoPE pair l
+  constexpr int DQ = DC + DR, TPB = 256 / TPT, WPT = TPT / 64, NPL = DC / 2 / TPT;
+  static_assert(TPT % 64 == 0 && 256 % TPT == 0 && DC % (2 * TPT) == 0 && DR / 2 <= TPT, "token groups");
   __shared__ float red[WPT];
   const int tid = threadIdx.x, l = tid % TPT, lane = tid & 63;
   const int t = TPB * blockIdx.x + tid / TPT;
@@ -507,27 +511,36 @@ __global__ __launch_bounds__(256) void append_finish_kernel(const float* __restr
   const int32_t tok_id = token_ids[t];
   const int32_t pos = positions[t];
   const bool rope = l < DR / 2;
-  const uint32_t wpair = kv_norm_w ? *reinterpret_cast<const uint32_t*>(kv_norm_w + 2 * l) : 0u;
+  uint32_t wpair[NPL];
+#pragma unroll
+  for (int i = 0; i < NPL; ++i)
+    wpair[i] = kv_norm_w ? *reinterpret_cast<const uint32_t*>(kv_norm_w + 2 * (l + TPT * i)) : 0u;
   // the slices' sums are loaded kBatch at a time (one round trip for up to
   // kBatch slices: this pass is bound by the latency of its loads), then added
   // in slice order
-  constexpr int kBatch = 32;
-  float2 c = make_float2(0.f, 0.f), r = make_float2(0.f, 0.f);
+  constexpr int kBatch = 32 / NPL;
+  float2 c[NPL], r = make_float2(0.f, 0.f);
+#pragma unroll
+  for (int i = 0; i < NPL; ++i) c[i] = make_float2(0.f, 0.f);
   for (int k0 = 0; k0 < nks; k0 += kBatch) {
-    float2 av[kBatch], bv[kBatch];
+    float2 av[kBatch][NPL], bv[kBatch];
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
       if (k0 + u < nks) {
         const float* row = part + (static_cast<int64_t>(k0 + u) * n + t) * DQ;
-        av[u] = *reinterpret_cast<const float2*>(row + 2 * l);
+#pragma unroll
+        for (int i = 0; i < NPL; ++i) av[u][i] = *reinterpret_cast<const float2*>(row + 2 * (l + TPT * i));
         bv[u] = rope ? *reinterpret_cast<const float2*>(row + DC + 2 * l) : make_float2(0.f, 0.f);
       }
     }
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
       if (k0 + u < nks) {
-        c.x += av[u].x;
-        c.y += av[u].y;
+#pragma unroll
+        for (int i = 0; i < NPL; ++i) {
+          c[i].x += av[u][i].x;
+          c[i].y += av[u][i].y;
+        }
         r.x += bv[u].x;
         r.y += bv[u].y;
       }
@@ -538,7 +551,10 @@ __global__ __launch_bounds__(256) void append_finish_kernel(const float* __restr
   if (slot < 0 || slot >= num_slots) return;  // out-of-range destination: skipped
   uint16_t* dst = cache + slot * DQ;
   if (kv_norm_w) {
-    float ss = wave_sum(c.x * c.x + c.y * c.y);
+    float ss = 0.f;
+#pragma unroll
+    for (int i = 0; i < NPL; ++i) ss += c[i].x * c[i].x + c[i].y * c[i].y;
+    ss = wave_sum(ss);
     if constexpr (WPT > 1) {
       if (lane == 0) red[tid >> 6] = ss;
       __syncthreads();
@@ -547,10 +563,15 @@ __global__ __launch_bounds__(256) void append_finish_kernel(const float* __restr
       for (int v = 1; v < WPT; ++v) ss += red[v];
     }
     const float inv_rms = 1.f / sqrtf(ss / static_cast<float>(DC) + kRmsEps);
-    c.x = c.x * inv_rms * bf16_lo(wpair);
-    c.y = c.y * inv_rms * bf16_hi(wpair);
+#pragma unroll
+    for (int i = 0; i < NPL; ++i) {
+      c[i].x = c[i].x * inv_rms * bf16_lo(wpair[i]);
+      c[i].y = c[i].y * inv_rms * bf16_hi(wpair[i]);
+    }
   }
-  *reinterpret_cast<uint32_t*>(dst + 2 * l) = pack_bf16x2(c.x, c.y);
+#pragma unroll
+  for (int i = 0; i < NPL; ++i)
+    *reinterpret_cast<uint32_t*>(dst + 2 * (l + TPT * i)) = pack_bf16x2(c[i].x, c[i].y);
   if (rope) {
     // the angle pos * theta^(-2m/d_r) and its reduction to [-pi, pi] in fp64,
     // the sine and cosine of the reduced angle in fp32 (as the one-pass kernel)
@@ -703,14 +724,20 @@ extern "C" eg_mla_status eg_mla_append_ws(const eg_mla_dims* dims, int32_t n_tok
     if (gemm) pass1(append_gemm_kernel<192>);
     else if (per == 32) pass1(append_slice_kernel<192, 1>);
     else pass1(append_slice_kernel<192, 2>);
-    hipLaunchKernelGGL((append_finish_kernel<128, 64>), dim3((n_tokens + 3) / 4), dim3(256), 0, stream, part, nks,
-                       token_ids, positions, slots, nw, theta, cb, token_id_cache, num_slots, n_tokens);
+    hipLaunchKernelGGL((append_finish_kernel<128, 64, 64>), dim3((n_tokens + 3) / 4), dim3(256), 0, stream, part,
+                       nks, token_ids, positions, slots, nw, theta, cb, token_id_cache, num_slots, n_tokens);
   } else {
     if (gemm) pass1(append_gemm_kernel<576>);
     else if (per == 32) pass1(append_slice_kernel<576, 1>);
     else pass1(append_slice_kernel<576, 2>);
-    hipLaunchKernelGGL((append_finish_kernel<512, 64>), dim3(n_tokens), dim3(256), 0, stream, part, nks, token_ids,
-                       positions, slots, nw, theta, cb, token_id_cache, num_slots, n_tokens);
+    // pass 2: a wave per token when the slices are few (4 tokens per
+    // work-group), a work-group per token (one pair per thread) when many
+    if (nks <= kAppFinishWaveSlices)
+      hipLaunchKernelGGL((append_finish_kernel<512, 64, 64>), dim3((n_tokens + 3) / 4), dim3(256), 0, stream, part,
+                         nks, token_ids, positions, slots, nw, theta, cb, token_id_cache, num_slots, n_tokens);
+    else
+      hipLaunchKernelGGL((append_finish_kernel<512, 64, 256>), dim3(n_tokens), dim3(256), 0, stream, part, nks,
+                         token_ids, positions, slots, nw, theta, cb, token_id_cache, num_slots, n_tokens);
   }
   return hipGetLastError() == hipSuccess ? EG_MLA_OK : EG_MLA_ERR_HIP;
 }

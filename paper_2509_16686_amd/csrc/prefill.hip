@@ -192,7 +192,7 @@ extern "C" eg_mla_status eg_mla_prefill_varlen(const eg_mla_dims* dims, int32_t 
     x.H = d.num_heads;
     x.DC = d.latent_dim;
     x.scale_log2 = softmax_scale(d) * 1.4426950408889634f;
-    hipLaunchKernelGGL(prefill_x_attn_kernel, dim3((T + kPxQTok - 1) / kPxQTok, d.num_heads), dim3(256),
+    hipLaunchKernelGGL(prefill_x_attn_kernel, dim3(((T + kPxQTok - 1) / kPxQTok) * d.num_heads), dim3(256),
                        2 * kPxTileBytes, stream, x);
     return hipGetLastError() == hipSuccess ? EG_MLA_OK : EG_MLA_ERR_HIP;
   }

@@ -173,8 +173,7 @@ __global__ __launch_bounds__(256, 2) void prefill_x_proj_kernel(const uint16_t* 
 // 128 block .. + 127 of the packed stream for head h (a block may straddle
 // sequences: each row masks keys outside its own sequence) and walks tiles of
 // 64 keys from the first token's sequence start to the block's last token
-// (blocks launched last-in-the-stream first, the heads of a block together
-// in the grid's second dimension).  Wave w holds the rows of tokens
+// (a head's blocks on one XCD, last-in-the-stream first).  Wave w holds the rows of tokens
 // 32 w .. + 31 of the block, its query (fp16) in registers as the B operand of
 // v_mfma_f32_32x32x16_f16 (lane: row lane % 32, dims 8 (lane / 32) + 16 c).
 //  * Tile: K^C rows (256 bytes, fp16), k^R rows (128 bytes, converted from
@@ -211,9 +210,13 @@ struct PrefillXArgs {
 
 __global__ __launch_bounds__(256, 2) void prefill_x_attn_kernel(PrefillXArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];  // two tile buffers
+  // one XCD takes whole heads (a contiguous range of the head-major order), so
+  // the blocks of a head read its K^C and V tiles through one L2 cache; within
+  // a head the last blocks of the stream (the heaviest) come first
   const int nblk = (a.T + kPxQTok - 1) / kPxQTok;
-  const int hh = blockIdx.y;
-  const int q0 = (nblk - 1 - static_cast<int>(blockIdx.x)) * kPxQTok;  // last blocks of the stream first
+  const int lb = xcd_logical_block(static_cast<int>(blockIdx.x), nblk * a.H);
+  const int hh = lb / nblk;
+  const int q0 = (nblk - 1 - lb % nblk) * kPxQTok;
   const int q_last = min(q0 + kPxQTok, a.T) - 1;
   const int kbeg = min(max(a.seq_start[q0], 0), q0);                 // keys from here ...
   const int kend = q_last + 1;                                       // ... to here (exclusive)

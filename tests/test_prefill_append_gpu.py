@@ -137,7 +137,8 @@ def test_append_then_decode(gpu):
                                         (1, "append_ws", 32), (1, "append_ws", 33), (1, "append_ws", 2048),
                                         (1, "append_ws", 2049), (1, "append_ws", 300), (4, "append_ws", 1),
                                         (4, "append_ws", 64), (4, "append_ws", 97), (4, "append_ws", 255),
-                                        (4, "append_ws", 256), (4, "append_ws", 512), (4, "append_ws", 3001)])
+                                        (4, "append_ws", 256), (4, "append_ws", 512), (4, "append_ws", 3001),
+                                        (4, "append_ws", 9000)])
 def test_append_token_counts(gpu, wi, entry, n):
     # the d_c 128 / d_r 64 layer's one-pass MFMA append: hidden split over the
     # waves up to 8192 tokens, 128 tokens per work-group above; the two-pass
