@@ -478,8 +478,10 @@ __device__ __forceinline__ void wide_wave(const SplitArgs& a, unsigned char* lds
   }
 }
 
-// Units of 16 tokens in flight per wave (its registers).
-template <int D>
+// Units of 16 tokens in flight per score wave (DS) and per value wave (DV)
+// (their registers: a score wave holds 32 VGPRs of rows per unit, a value wave
+// 8 beside its 128 accumulators).
+template <int DS, int DV>
 __global__ __launch_bounds__(WideCfg::NT, 1) void split_wide_kernel(SplitArgs a) {
   __shared__ __attribute__((aligned(16))) unsigned char lds[WideCfg::LDS_BYTES];
   int wg, hblk;
@@ -487,9 +489,9 @@ __global__ __launch_bounds__(WideCfg::NT, 1) void split_wide_kernel(SplitArgs a)
   if (wg >= static_cast<int>(a.sched_hdr[1])) return;  // uniform over the work-group
   const int w = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
   if (w < WideCfg::NV)
-    wide_wave<0, D>(a, lds, wg, hblk, w);
+    wide_wave<0, DS>(a, lds, wg, hblk, w);
   else
-    wide_wave<1, D>(a, lds, wg, hblk, w - WideCfg::NV);
+    wide_wave<1, DV>(a, lds, wg, hblk, w - WideCfg::NV);
 }
 
 }  // namespace egmla
