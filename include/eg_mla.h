@@ -323,9 +323,12 @@ eg_mla_status eg_mla_prefill_varlen(const eg_mla_dims* dims, int32_t batch, int3
  * decode applies the gate to the latent; this call is the literal variant
  * and its two ablations.)
  *
- * bf16 storage with d_c = d_h = d_v = 128, d_r = 64, at most 160 heads
- * (per-head state of a 128-token tile lives in LDS) and a gate table below
- * 4 GB (32-bit row offsets); other shapes
+ * The MFMA tile kernel takes bf16 storage with d_c = d_h = d_v = 128,
+ * d_r = 64, at most 160 heads and a gate table below 4 GB (32-bit row
+ * offsets).  Every other layer (any d_c, d_h, d_v, d_r, bf16 or fp32
+ * storage) takes a generic kernel of the same arithmetic, plain fp32 and not
+ * tuned, while its per-tile state fits the LDS: 4 (8 d_c + H (d_v + 21) + 88)
+ * bytes <= 160 KB (the 128-head d_c 512 layer fits); beyond that
  * EG_MLA_ERR_UNSUPPORTED.  dims->gate_dim is not used here (it must still
  * pass eg_mla_check_dims).  Softmax partials are formed per 128-token tile
  * and merged, so the context length is not limited.

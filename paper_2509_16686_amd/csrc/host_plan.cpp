@@ -264,6 +264,20 @@ eg_mla_status validate_prefill_varlen(const eg_mla_dims* d, int32_t batch, int32
   return EG_MLA_OK;
 }
 
+bool literal_tile_shape(const eg_mla_dims& d) {
+  return d.dtype == EG_MLA_BF16 && d.latent_dim == 128 && d.head_dim == 128 && d.v_head_dim == 128 &&
+         d.rope_dim == 64 && d.num_heads <= 160 && literal_lds_bytes(d.num_heads) <= 160 * 1024;
+}
+
+size_t literal_generic_lds_bytes(const eg_mla_dims& d) {
+  // latents of a group of 8 tokens, key dots and weights [8][H], moment sums
+  // [4][8][2], per-token figures [3][8], per-head sums [2][H] and softmax
+  // state [3][H], value sums [H][d_v] (all fp32)
+  const size_t H = static_cast<size_t>(d.num_heads);
+  return 4 * (8 * static_cast<size_t>(d.latent_dim) + 16 * H + 64 + 24 + 5 * H +
+              H * static_cast<size_t>(d.v_head_dim));
+}
+
 size_t literal_lds_bytes(int num_heads) {
   // weight / gate-tile region, per-wave scores [4][H][32], value sums [4][d_v],
   // two sums per head, per-wave figures per head, token means [4][32] (all fp32)
@@ -288,13 +302,14 @@ eg_mla_status validate_literal(const eg_mla_dims* d, int32_t batch, const void* 
   if (st != EG_MLA_OK) return st;
   if (batch < 0 || max_pages_per_seq < 0 || num_slots < 0) return EG_MLA_ERR_INVALID_ARG;
   if ((flags & ~(EG_MLA_LITERAL_NO_LN | EG_MLA_LITERAL_ADD)) != 0) return EG_MLA_ERR_INVALID_ARG;
-  if (d->dtype != EG_MLA_BF16 || d->latent_dim != 128 || d->head_dim != 128 || d->v_head_dim != 128 ||
-      d->rope_dim != 64)
-    return EG_MLA_ERR_UNSUPPORTED;
-  // per-head state of a tile lives in LDS: 160 heads fit in 160 KB
-  if (d->num_heads > 160 || literal_lds_bytes(d->num_heads) > 160 * 1024) return EG_MLA_ERR_UNSUPPORTED;
-  if (static_cast<int64_t>(d->vocab_size) * d->num_heads * (d->head_dim + d->v_head_dim) * 2 >= (int64_t{1} << 32))
-    return EG_MLA_ERR_UNSUPPORTED;  // gate rows are addressed by 32-bit byte offsets
+  if (literal_tile_shape(*d)) {
+    // gate rows are addressed by 32-bit byte offsets in the tile kernel
+    if (static_cast<int64_t>(d->vocab_size) * d->num_heads * (d->head_dim + d->v_head_dim) * 2 >=
+        (int64_t{1} << 32))
+      return EG_MLA_ERR_UNSUPPORTED;
+  } else if (literal_generic_lds_bytes(*d) > 160 * 1024) {
+    return EG_MLA_ERR_UNSUPPORTED;  // the generic kernel's tile state does not fit in LDS
+  }
   if (static_cast<int64_t>(max_pages_per_seq) * d->page_size > (int64_t{1} << 30)) return EG_MLA_ERR_UNSUPPORTED;
   if (num_slots >= (int64_t{1} << 31)) return EG_MLA_ERR_UNSUPPORTED;
   if (batch == 0) return EG_MLA_OK;

@@ -103,9 +103,13 @@ eg_mla_status validate_prefill_varlen(const eg_mla_dims* d, int32_t batch, int32
 
 // Decode with the paper-literal gate: workspace = one fp32 record per
 // (sequence, 128-token tile, head): d_v centred value sums, the tile's max,
-// sum of p, two pads.  LDS of the tile kernel for a head count.
+// sum of p, two pads.  LDS of the tile kernel for a head count; whether a
+// layer takes the tile kernel (bf16, d_c = d_h = d_v = 128, d_r = 64, at most
+// 160 heads) or the generic one, and the generic kernel's LDS.
 size_t literal_workspace_bytes(const eg_mla_dims& d, int32_t batch, int32_t max_pages_per_seq);
 size_t literal_lds_bytes(int num_heads);
+bool literal_tile_shape(const eg_mla_dims& d);
+size_t literal_generic_lds_bytes(const eg_mla_dims& d);
 eg_mla_status validate_literal(const eg_mla_dims* d, int32_t batch, const void* q, const void* latent_cache,
                                const int32_t* token_id_cache, const void* gate_full, const void* w_uk,
                                const void* w_uv, const void* ln_w, const void* ln_b, uint32_t flags,

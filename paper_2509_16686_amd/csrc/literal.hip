@@ -37,6 +37,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <type_traits>
 
 #include "device_common.h"
 #include "eg_mla.h"
@@ -456,6 +457,258 @@ __global__ __launch_bounds__(128) void literal_merge_kernel(const float* __restr
   orow[v] = f32_to_bf16(wv * o / l + bv);  // o: sum of a_j (x_j - mu_j), already centred
 }
 
+// ---------------------------------------------------------------------------
+// Other shapes (any d_c, d_h, d_v, d_r and head count that fit the LDS, bf16 or
+// fp32 storage): the same arithmetic as the tile kernel (the LayerNorm applied
+// through each token's moments about a pivot, its first gated value; scores in
+// the log2 domain; per 128-token tile and head the record (o, max, sum) that
+// the merge combines) in plain fp32 VALU code.  One work-group of 4 waves per
+// (sequence, 128-token tile) walks the tile in groups of 8 tokens: their
+// latents go to LDS; in pass A wave w takes heads w, w + 4, ..., its lanes a
+// head's up-projected outputs 64 at a time, each lane one W row against the 8
+// latents (broadcast LDS reads, so a row is read once per 8 tokens), forming
+// the tokens' moments and the heads' key dots; then an online softmax per head
+// (state in LDS); pass B the value sums the same way.  Not tuned: it serves
+// the layers the tile kernel does not take.
+// ---------------------------------------------------------------------------
+constexpr int kLgTok = 8;  // tokens per group
+
+struct LiteralGenericArgs {
+  const void* q;
+  const void* cache;
+  const int32_t* ids;
+  const void* gate;
+  const void* w_uk;
+  const void* w_uv;
+  const void* ln_w;
+  const void* ln_b;
+  const int32_t* seq_lens;
+  const int32_t* page_table;
+  int P, max_pages;
+  int64_t num_slots;
+  int H, DH, DV, DC, DR, V;
+  float scale_log2;
+  float* part;
+};
+
+template <bool BF16, bool LN, bool ADD>
+__global__ __launch_bounds__(256) void literal_generic_tile_kernel(LiteralGenericArgs a) {
+  extern __shared__ float lg[];
+  const int H = a.H, DH = a.DH, DV = a.DV, DC = a.DC, DR = a.DR, HW = DH + DV;
+  float* cs = lg;                      // [8][d_c] the group's latents
+  float* kdot = cs + kLgTok * DC;      // [8][H] key dots sum q w (x - K)
+  float* pst = kdot + kLgTok * H;      // [8][H] weights of the value sums (p, or p rstd)
+  float* mom = pst + kLgTok * H;       // [4 waves][8][2] moment sums
+  float* tokf = mom + 4 * kLgTok * 2;  // [3][8] pivot K, mean - K, rstd
+  float* sq = tokf + 3 * kLgTok;       // [2][H] sum q w, sum q b (key dims)
+  float* hst = sq + 2 * H;             // [3][H] running max, sum, this group's rescale
+  float* ob = hst + 3 * H;             // [H][d_v] value sums
+  const int b = blockIdx.y, tile = blockIdx.x;
+  const int L = clamp_len(a.seq_lens[b], a.P * a.max_pages);
+  const int j0 = tile * 128;
+  if (j0 >= L) return;  // whole work-group, before any barrier
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  const int nj = min(128, L - j0);
+  const int64_t qb = static_cast<int64_t>(b) * H * (DH + DR);
+  const int64_t grow_len = static_cast<int64_t>(H) * HW;
+  for (int h = w; h < H; h += 4) {
+    float sw = 0.f, sb = 0.f;
+    if (LN) {
+      for (int d = lane; d < DH; d += 64) {
+        const float qd = ld<BF16>(a.q, qb + static_cast<int64_t>(h) * (DH + DR) + d);
+        sw = fmaf(qd, ld<BF16>(a.ln_w, static_cast<int64_t>(h) * HW + d), sw);
+        sb = fmaf(qd, ld<BF16>(a.ln_b, static_cast<int64_t>(h) * HW + d), sb);
+      }
+    }
+    sw = wave_sum(sw);
+    sb = wave_sum(sb);
+    if (lane == 0) {
+      sq[h] = sw;
+      sq[H + h] = sb;
+      hst[h] = -INFINITY;
+      hst[H + h] = 0.f;
+    }
+  }
+  for (int i = tid; i < H * DV; i += 256) ob[i] = 0.f;
+  __syncthreads();
+  for (int g0 = 0; g0 < nj; g0 += kLgTok) {
+    // the group's tokens (past the tile's end the last token again, weight 0)
+    int64_t rowk[kLgTok];
+    int idk[kLgTok];
+#pragma unroll
+    for (int k = 0; k < kLgTok; ++k) {
+      rowk[k] = cache_slot(a.page_table, b, j0 + min(g0 + k, nj - 1), a.P, a.max_pages, a.num_slots);
+      idk[k] = clamp_id(a.ids[rowk[k]], a.V);
+    }
+    for (int i = tid; i < kLgTok * DC; i += 256) cs[i] = ld<BF16>(a.cache, rowk[i / DC] * (DC + DR) + i % DC);
+    __syncthreads();
+    if (tid < kLgTok) {
+      // pivot: the token's first gated value (output 0 of head 0); none without a LayerNorm
+      float x = 0.f;
+      for (int c = 0; c < DC; ++c) x = fmaf(ld<BF16>(a.w_uk, c), cs[tid * DC + c], x);
+      const float gg = ld<BF16>(a.gate, static_cast<int64_t>(idk[tid]) * grow_len);
+      tokf[tid] = LN ? (ADD ? x + gg : x * gg) : 0.f;
+    }
+    __syncthreads();
+    float piv[kLgTok];
+#pragma unroll
+    for (int k = 0; k < kLgTok; ++k) piv[k] = tokf[k];
+    // ---- pass A: moments about the pivot, key dots ----
+    float s1[kLgTok], s2[kLgTok];
+#pragma unroll
+    for (int k = 0; k < kLgTok; ++k) s1[k] = s2[k] = 0.f;
+    for (int h = w; h < H; h += 4) {
+      float kd[kLgTok];
+#pragma unroll
+      for (int k = 0; k < kLgTok; ++k) kd[k] = 0.f;
+      for (int e = lane; e < HW; e += 64) {
+        const bool isk = e < DH;
+        const void* wm = isk ? a.w_uk : a.w_uv;
+        const int64_t wrow = (static_cast<int64_t>(h) * (isk ? DH : DV) + (isk ? e : e - DH)) * DC;
+        float x[kLgTok];
+#pragma unroll
+        for (int k = 0; k < kLgTok; ++k) x[k] = 0.f;
+        for (int c = 0; c < DC; ++c) {
+          const float wc = ld<BF16>(wm, wrow + c);
+#pragma unroll
+          for (int k = 0; k < kLgTok; ++k) x[k] = fmaf(wc, cs[k * DC + c], x[k]);
+        }
+        const float qw = isk ? ld<BF16>(a.q, qb + static_cast<int64_t>(h) * (DH + DR) + e) *
+                                   (LN ? ld<BF16>(a.ln_w, static_cast<int64_t>(h) * HW + e) : 1.f)
+                             : 0.f;
+#pragma unroll
+        for (int k = 0; k < kLgTok; ++k) {
+          const float gg = ld<BF16>(a.gate, static_cast<int64_t>(idk[k]) * grow_len + static_cast<int64_t>(h) * HW + e);
+          const float y = (ADD ? x[k] + gg : x[k] * gg) - piv[k];
+          s1[k] += y;
+          s2[k] = fmaf(y, y, s2[k]);
+          kd[k] = fmaf(qw, y, kd[k]);
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < kLgTok; ++k) {
+        const float t = wave_sum(kd[k]);
+        if (lane == 0) kdot[k * H + h] = t;
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < kLgTok; ++k) {
+      const float t1 = wave_sum(s1[k]), t2 = wave_sum(s2[k]);
+      if (lane == 0) {
+        mom[(w * kLgTok + k) * 2] = t1;
+        mom[(w * kLgTok + k) * 2 + 1] = t2;
+      }
+    }
+    __syncthreads();
+    if (tid < kLgTok) {
+      const float n = static_cast<float>(grow_len);
+      float t1 = 0.f, t2 = 0.f;
+      for (int v = 0; v < 4; ++v) {
+        t1 += mom[(v * kLgTok + tid) * 2];
+        t2 += mom[(v * kLgTok + tid) * 2 + 1];
+      }
+      const float m1 = t1 / n, m2 = t2 / n;
+      tokf[kLgTok + tid] = LN ? m1 : 0.f;  // mean - K
+      tokf[2 * kLgTok + tid] = LN ? 1.0f / sqrtf(fmaxf(m2 - m1 * m1, 0.f) + kLtLnEps) : 1.f;
+    }
+    __syncthreads();
+    // ---- scores and the online softmax of each head ----
+    for (int h = tid; h < H; h += 256) {
+      float sc[kLgTok], mx = -INFINITY;
+#pragma unroll
+      for (int k = 0; k < kLgTok; ++k) {
+        const float base = LN ? tokf[2 * kLgTok + k] * (kdot[k * H + h] - tokf[kLgTok + k] * sq[h]) + sq[H + h]
+                              : kdot[k * H + h];
+        float rd = 0.f;
+        for (int r = 0; r < DR; ++r)
+          rd = fmaf(ld<BF16>(a.q, qb + static_cast<int64_t>(h) * (DH + DR) + DH + r),
+                    ld<BF16>(a.cache, rowk[k] * (DC + DR) + DC + r), rd);
+        sc[k] = g0 + k < nj ? a.scale_log2 * (base + rd) : -INFINITY;
+        mx = fmaxf(mx, sc[k]);
+      }
+      const float m_new = fmaxf(hst[h], mx);  // finite: token g0 is in the tile
+      const float alpha = exp2f(hst[h] - m_new);
+      float l = hst[H + h] * alpha;
+#pragma unroll
+      for (int k = 0; k < kLgTok; ++k) {
+        const float p = exp2f(sc[k] - m_new);
+        l += p;
+        pst[k * H + h] = LN ? p * tokf[2 * kLgTok + k] : p;
+      }
+      hst[h] = m_new;
+      hst[H + h] = l;
+      hst[2 * H + h] = alpha;
+    }
+    __syncthreads();
+    // ---- pass B: value sums (centred on each token's mean with a LayerNorm) ----
+    for (int h = w; h < H; h += 4) {
+      const float alpha = hst[2 * H + h];
+      for (int e = lane; e < DV; e += 64) {
+        const int64_t wrow = (static_cast<int64_t>(h) * DV + e) * DC;
+        float x[kLgTok];
+#pragma unroll
+        for (int k = 0; k < kLgTok; ++k) x[k] = 0.f;
+        for (int c = 0; c < DC; ++c) {
+          const float wc = ld<BF16>(a.w_uv, wrow + c);
+#pragma unroll
+          for (int k = 0; k < kLgTok; ++k) x[k] = fmaf(wc, cs[k * DC + c], x[k]);
+        }
+        float acc = ob[h * DV + e] * alpha;
+#pragma unroll
+        for (int k = 0; k < kLgTok; ++k) {
+          const float gg =
+              ld<BF16>(a.gate, static_cast<int64_t>(idk[k]) * grow_len + static_cast<int64_t>(h) * HW + DH + e);
+          const float xg = ADD ? x[k] + gg : x[k] * gg;
+          acc = fmaf(pst[k * H + h], LN ? xg - (piv[k] + tokf[kLgTok + k]) : xg, acc);
+        }
+        ob[h * DV + e] = acc;
+      }
+    }
+    __syncthreads();  // the next group overwrites the latents and the weights
+  }
+  // the tile's records: o, the maximum, the sum (as the tile kernel's)
+  float* pb = a.part + (static_cast<int64_t>(b) * gridDim.x + tile) * H * (DV + 4);
+  for (int i = tid; i < H * DV; i += 256) pb[static_cast<int64_t>(i / DV) * (DV + 4) + i % DV] = ob[i];
+  for (int h = tid; h < H; h += 256) {
+    pb[static_cast<int64_t>(h) * (DV + 4) + DV] = hst[h];
+    pb[static_cast<int64_t>(h) * (DV + 4) + DV + 1] = hst[H + h];
+  }
+}
+
+// The merge for the generic tile kernel's records (any d_v, bf16 or fp32 output).
+template <bool BF16>
+__global__ __launch_bounds__(256) void literal_generic_merge_kernel(const float* __restrict__ part,
+                                                                    const void* __restrict__ ln_w,
+                                                                    const void* __restrict__ ln_b, int use_ln,
+                                                                    const int32_t* __restrict__ seq_lens, int cap,
+                                                                    int tiles, int H, int DH, int DV,
+                                                                    void* __restrict__ out) {
+  const int hh = blockIdx.x, b = blockIdx.y;
+  const int L = clamp_len(seq_lens[b], cap);
+  const int nt = (L + 127) / 128;
+  const int64_t obase = (static_cast<int64_t>(b) * H + hh) * DV;
+  if (nt == 0) {
+    for (int v = threadIdx.x; v < DV; v += 256) st<BF16>(out, obase + v, 0.f);
+    return;
+  }
+  const int64_t stride = static_cast<int64_t>(H) * (DV + 4);
+  const float* pp = part + static_cast<int64_t>(b) * tiles * stride + static_cast<int64_t>(hh) * (DV + 4);
+  float m = -INFINITY;
+  for (int i = 0; i < nt; ++i) m = fmaxf(m, pp[i * stride + DV]);
+  for (int v = threadIdx.x; v < DV; v += 256) {
+    float o = 0.f, l = 0.f;
+    for (int i = 0; i < nt; ++i) {
+      const float e = exp2f(pp[i * stride + DV] - m);
+      o = fmaf(e, pp[i * stride + v], o);
+      l = fmaf(e, pp[i * stride + DV + 1], l);
+    }
+    const int64_t c = static_cast<int64_t>(hh) * (DH + DV) + DH + v;
+    const float wv = use_ln ? ld<BF16>(ln_w, c) : 1.f;
+    const float bv = use_ln ? ld<BF16>(ln_b, c) : 0.f;
+    st<BF16>(out, obase + v, wv * o / l + bv);
+  }
+}
+
 }  // namespace egmla
 
 using namespace egmla;
@@ -484,13 +737,54 @@ extern "C" eg_mla_status eg_mla_decode_literal(const eg_mla_dims* dims, int32_t 
   float* part = static_cast<float*>(workspace);
   const bool use_ln = (flags & EG_MLA_LITERAL_NO_LN) == 0;
   const bool add = (flags & EG_MLA_LITERAL_ADD) != 0;
+  const float scale_log2 = softmax_scale(d) * 1.4426950408889634f;
+  if (!literal_tile_shape(d)) {
+    LiteralGenericArgs g;
+    g.q = q;
+    g.cache = latent_cache;
+    g.ids = token_id_cache;
+    g.gate = gate_full;
+    g.w_uk = w_uk;
+    g.w_uv = w_uv;
+    g.ln_w = ln_weight;
+    g.ln_b = ln_bias;
+    g.seq_lens = seq_lens;
+    g.page_table = page_table;
+    g.P = P;
+    g.max_pages = max_pages_per_seq;
+    g.num_slots = num_slots;
+    g.H = H;
+    g.DH = d.head_dim;
+    g.DV = d.v_head_dim;
+    g.DC = d.latent_dim;
+    g.DR = d.rope_dim;
+    g.V = d.vocab_size;
+    g.scale_log2 = scale_log2;
+    g.part = part;
+    const bool bf = d.dtype == EG_MLA_BF16;
+    auto pick = [&](auto b16) {
+      constexpr bool BF = decltype(b16)::value;
+      return use_ln ? (add ? literal_generic_tile_kernel<BF, true, true> : literal_generic_tile_kernel<BF, true, false>)
+                    : (add ? literal_generic_tile_kernel<BF, false, true>
+                           : literal_generic_tile_kernel<BF, false, false>);
+    };
+    const auto gk = bf ? pick(std::true_type{}) : pick(std::false_type{});
+    const int glds = static_cast<int>(literal_generic_lds_bytes(d));
+    if (glds > 65536 && hipFuncSetAttribute(reinterpret_cast<const void*>(gk),
+                                            hipFuncAttributeMaxDynamicSharedMemorySize, glds) != hipSuccess)
+      return EG_MLA_ERR_HIP;
+    hipLaunchKernelGGL(gk, dim3(tiles, batch), dim3(256), glds, stream, g);
+    const auto mk = bf ? literal_generic_merge_kernel<true> : literal_generic_merge_kernel<false>;
+    hipLaunchKernelGGL(mk, dim3(H, batch), dim3(256), 0, stream, part, ln_weight, ln_bias, use_ln ? 1 : 0, seq_lens,
+                       cap, tiles, H, d.head_dim, d.v_head_dim, out);
+    return hipGetLastError() == hipSuccess ? EG_MLA_OK : EG_MLA_ERR_HIP;
+  }
   const auto kern = use_ln ? (add ? literal_tile_kernel<true, true> : literal_tile_kernel<true, false>)
                            : (add ? literal_tile_kernel<false, true> : literal_tile_kernel<false, false>);
   const int lds = static_cast<int>(literal_lds_bytes(H));
   if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, lds) !=
       hipSuccess)
     return EG_MLA_ERR_HIP;
-  const float scale_log2 = softmax_scale(d) * 1.4426950408889634f;
   hipLaunchKernelGGL(kern, dim3(tiles, batch), dim3(256), lds, stream, static_cast<const uint16_t*>(q),
                      static_cast<const uint16_t*>(latent_cache), token_id_cache, static_cast<const uint16_t*>(gate_full),
                      static_cast<const uint16_t*>(w_uk), static_cast<const uint16_t*>(w_uv),

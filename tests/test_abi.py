@@ -265,7 +265,14 @@ def test_decode_literal_rejects_before_launch(L):
     big = L.eg_mla_decode_literal_workspace_size(ctypes.byref(d), 2, 1024)
     assert big >= 2 * (1024 * 64 // 128) * 16 * (128 + 4) * 4  # 65536-token capacity: no limit on the context
     assert call(maxp=1024, nslots=2 * 1024 * 64, wsb=big - 1) == B.ERR_WORKSPACE
-    for bad in (dims(latent_dim=512, gate_dim=512), dims(rope_dim=32), dims(dtype=B.FP32), dims(v_head_dim=64),
-                dims(num_heads=161),   # per-head tile state beyond the LDS
-                dims(vocab_size=600000)):  # a gate table of 4 GB or more
+    # the tile kernel takes bf16, d_c = d_h = d_v = 128, d_r = 64, at most 160 heads and a gate
+    # table below 4 GB; other layers take the generic kernel while its tile state fits the LDS
+    # (value sums of all heads, [H][d_v] fp32, and 8 latents)
+    assert call(dd=dims(vocab_size=600000)) == B.ERR_UNSUPPORTED   # a gate table of 4 GB or more
+    for dd in (dims(latent_dim=512, gate_dim=512, num_heads=128), dims(rope_dim=32), dims(dtype=B.FP32),
+               dims(v_head_dim=64), dims(num_heads=161)):
+        n = L.eg_mla_decode_literal_workspace_size(ctypes.byref(dd), 2, 4)
+        assert call(dd=dd, wsb=n - 1) == B.ERR_WORKSPACE            # accepted shapes, checked up to the workspace
+    for bad in (dims(num_heads=320),                              # 320 x 128 value sums: 160 KB of LDS
+                dims(latent_dim=4096, gate_dim=4096, num_heads=250)):
         assert call(dd=bad) == B.ERR_UNSUPPORTED

@@ -26,6 +26,18 @@ def run_literal(inp, lg, flags):
     return B.out_to_f64(dd.out)
 
 
+def run_literal_storage(inp, lg, flags):
+    """As run_literal, with the gate and LayerNorm arrays in the workload's storage type."""
+    st = inp.wl.dtype
+    dd = B.stage_decode(inp)
+    ws = B.alloc_workspace(B.decode_literal_workspace_size(dd.dims, int(dd.q.shape[0]), dd.max_pages))
+    gate = B.to_device_tensor(lg.gate_full, st)
+    lw, lb = B.to_device_tensor(lg.ln_w, st), B.to_device_tensor(lg.ln_b, st)
+    B.decode_literal(dd, gate, lw, lb, flags, ws)
+    torch.cuda.synchronize()
+    return B.out_to_f64(dd.out)
+
+
 def oracle_literal(inp, lg, mode, use_ln):
     wl = inp.wl
     return orc.decode_literal(inp.q, inp.latent_cache, inp.token_ids, lg.gate_full, inp.w_uk, inp.w_uv, lg.ln_w,
@@ -107,3 +119,34 @@ def test_literal_full_size_sampled(gpu):
                                  storage=wl.dtype, page_table=None, page_size=P, max_pages=-(-L // P), mode="mul",
                                  use_ln=True)
         assert_close(got[b:b + 1], ref, "bf16", f"literal full size, sequence {b}")
+
+
+@pytest.mark.parametrize("flags,mode,use_ln", MODES, ids=["mul_ln", "mul", "add_ln", "add"])
+def test_literal_generic_dc512_h128(gpu, flags, mode, use_ln):
+    # the 128-head d_c 512 layer (paged, ragged): the generic kernel
+    wl = W.WORKLOADS[4].replace(batch=3, seq_len_range=(1, 300), vocab=500, seed=85)
+    inp = W.generate(wl, seq_lens=np.array([300, 129, 1]))
+    lg = W.generate_literal_gate(wl)
+    say(f"literal decode generic H128 d_c512 mode={mode} ln={use_ln}")
+    assert_close(run_literal_storage(inp, lg, flags), oracle_literal(inp, lg, mode, use_ln), "bf16",
+                 f"literal generic d_c512 {mode} ln={use_ln}")
+
+
+@pytest.mark.parametrize("case", ["fp32_tiny", "bf16_odd", "bf16_offset_rows"])
+def test_literal_generic_shapes(gpu, case):
+    # other layers: the tiny fp32 one (no RoPE part), a bf16 one with d_h != d_v and
+    # a short latent, and additive gate rows centred at 100 (|mu| ~ 100 sigma)
+    if case == "fp32_tiny":
+        wl = W.WORKLOADS[0].replace(batch=3, seq_len=None, seq_len_range=(1, 300), seed=86)
+        lens, flags, mode, use_ln, center = [300, 0, 77], 0, "mul", True, 1.0
+    else:
+        wl = W.WORKLOADS[1].replace(heads=5, head_dim=64, v_head_dim=48, latent_dim=96, gate_dim=96, rope_dim=32,
+                                    batch=2, seq_len=None, seq_len_range=(1, 260), paged=True, vocab=700, seed=87)
+        lens = [260, 31]
+        flags, mode, use_ln, center = ((0, "mul", True, 1.0) if case == "bf16_odd"
+                                       else (B.LITERAL_ADD, "add", True, 100.0))
+    inp = W.generate(wl, seq_lens=np.array(lens))
+    lg = W.generate_literal_gate(wl, center=center)
+    say(f"literal decode generic {case}")
+    assert_close(run_literal_storage(inp, lg, flags), oracle_literal(inp, lg, mode, use_ln), wl.dtype,
+                 f"literal generic {case}")
