@@ -420,19 +420,14 @@ int absorb_spin_limit() {
 }
 
 // Balanced head-split kernel: `ranges` token ranges x a.groups blocks of 64 heads.
-// Wide kernel: units in flight per wave of each role (measured: 3 or 4 for the
-// score waves alone, at 10 and 35 spilled registers, were no faster).
+// Wide kernel: units in flight per score wave.
 #ifndef EGMLA_WIDE_DEPTH
 #define EGMLA_WIDE_DEPTH 2
 #endif
-#ifndef EGMLA_WIDE_VDEPTH
-#define EGMLA_WIDE_VDEPTH 2
-#endif
-constexpr int kWideDepth = EGMLA_WIDE_DEPTH;    // units in flight per score wave
-constexpr int kWideVDepth = EGMLA_WIDE_VDEPTH;  // units in flight per value wave
+constexpr int kWideDepth = EGMLA_WIDE_DEPTH;
 
 hipError_t launch_wide(const SplitArgs& a, int ranges, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
-  hipExtLaunchKernelGGL((split_wide_kernel<kWideDepth, kWideVDepth>), dim3(ranges * a.groups), dim3(WideCfg::NT), 0,
+  hipExtLaunchKernelGGL((split_wide_kernel<kWideDepth>), dim3(ranges * a.groups), dim3(WideCfg::NT), 0,
                         stream, ev0, ev1, 0, a);
   return hipGetLastError();
 }

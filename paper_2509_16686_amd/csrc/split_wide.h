@@ -64,23 +64,28 @@ struct WideCfg {
   static constexpr int NRC = DR / 32;      // 32-dim RoPE chunks (value waves)
   static constexpr int NDB = DW / 16;      // 16-dim value blocks of a value wave
   static constexpr int TOK = 16;           // tokens per unit
-  static constexpr int NHB = 3;            // gated-tile buffers
+  static constexpr int NHB = 5;            // gated-tile buffers (a unit's tile lives 5 unit steps)
+  static constexpr int NRB = 2;            // RoPE-key buffers
   // tile row: 512 gated dims + 32 bytes, so that the row stride is 8 banks
   // (mod 64): the 16-byte row writes and the transposed 8-byte reads of 4
   // rows are free of bank conflicts
   static constexpr int TS = DC + 16;
+  // RoPE tile row: 64 dims + 16 bytes (36 banks mod 64): the 16 rows of an
+  // operand read fall on 16 distinct groups of 4 banks
+  static constexpr int RS = DR + 8;
   static constexpr int HT = 0;                                // [NHB][16][TS] fp16: gated latent
-  static constexpr int SB = HT + NHB * TOK * TS * 2;          // [2][NV][NHT][64] f32x4: partial scores
-  static constexpr int PB = SB + 2 * NV * NHT * 64 * 16;      // [2][NHT][64] fp16 x 4: probabilities
-  static constexpr int AL = PB + 2 * NHT * 64 * 8;            // [2][16][NHT] f32: rescale factor of head 16 ht + r
-  static constexpr int FL = AL + 2 * HEADS * 4;               // [2][NHT] int: head tile rescaled
-  static constexpr int LIST = FL + 64;                        // int2 (slot, id) per token
-  static constexpr int LISTCAP = 4096;                        // tokens listed at a time
+  static constexpr int RT = HT + NHB * TOK * TS * 2;          // [NRB][16][RS] bf16: RoPE keys
+  static constexpr int SB = RT + NRB * TOK * RS * 2;          // [2][NV][NHT][64] f32x4: partial scores
+  static constexpr int PB = SB + 2 * NV * NHT * 64 * 16;      // [2][NHT][64][2] fp16 x 4: probabilities of unit pairs
+  static constexpr int AL = PB + 2 * NHT * 64 * 16;           // [4][16][NHT] f32: rescale factor of head 16 ht + r
+  static constexpr int LIST = AL + 4 * HEADS * 4;             // int2 (slot, id) per token
+  static constexpr int LISTCAP = 3072;                        // tokens listed at a time
   static constexpr int LDS_BYTES = LIST + LISTCAP * 8;
-  static_assert(NHT == NV && NHT == 4, "one head tile per value wave; 16-byte flag reads");
+  static_assert(NHT == NV && NHT == 4, "one head tile per value wave; 16-byte factor reads");
   static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
   static_assert(LISTCAP % NT == 0 && LISTCAP % TOK == 0, "list chunk");
-  static_assert(SB % 16 == 0 && PB % 16 == 0 && LIST % 16 == 0, "alignment");
+  static_assert(RT % 16 == 0 && SB % 16 == 0 && PB % 16 == 0 && LIST % 16 == 0, "alignment");
+  static_assert(TOK == 4 * NV, "a score wave loads the RoPE lines of 4 tokens per unit");
 };
 
 // Balanced schedule of the wide kernel.  The batch's tokens, taken sequence
@@ -226,6 +231,11 @@ __device__ __forceinline__ void wide_walk(const SplitArgs& a, int wg, int2* list
   }
 }
 
+// Unit steps (barriers) of a list chunk of nunits units: one per unit, then
+// the two halves of the values of the last pair of units (a lone last unit
+// is a pair whose second unit has no tokens).
+__device__ __forceinline__ int wide_steps(int nunits) { return 2 * ((nunits + 1) / 2) + 2; }
+
 // One wave's work in the split kernel: ROLE 0 = score wave s, ROLE 1 = value
 // wave t (the index is `idx`).  Every wave of the work-group walks the same
 // segments and chunks and meets the same barriers: one per unit, one more at
@@ -238,10 +248,10 @@ __device__ __forceinline__ void wide_wave(const SplitArgs& a, unsigned char* lds
   constexpr int QROW = DQ;  // absorbed query row: [q_lat fp16 | q^R bf16]
   int2* list = reinterpret_cast<int2*>(lds + C::LIST);
   f32x4_t* sbuf = reinterpret_cast<f32x4_t*>(lds + C::SB);  // [2][NV][NHT][64]
-  s16x4_t* pbuf = reinterpret_cast<s16x4_t*>(lds + C::PB);  // [2][NHT][64]
-  float* abuf = reinterpret_cast<float*>(lds + C::AL);      // [2][16][NHT]
-  int* fbuf = reinterpret_cast<int*>(lds + C::FL);          // [2][NHT]
+  s16x4_t* pbuf = reinterpret_cast<s16x4_t*>(lds + C::PB);  // [2][NHT][64][2]: pair (u / 2) % 2, unit u % 2
+  float* abuf = reinterpret_cast<float*>(lds + C::AL);      // [4][16][NHT]: unit u % 4
   auto htile = [&](int h) { return reinterpret_cast<uint16_t*>(lds + C::HT) + h * TOK * TS; };
+  auto rtile = [&](int u) { return reinterpret_cast<uint16_t*>(lds + C::RT) + (u % C::NRB) * TOK * C::RS; };
 
   const int lane = threadIdx.x & 63, r16 = lane & 15, g = lane >> 4;
   const uint16_t* __restrict__ cache = static_cast<const uint16_t*>(a.cache);
@@ -253,10 +263,18 @@ __device__ __forceinline__ void wide_wave(const SplitArgs& a, unsigned char* lds
   if constexpr (ROLE == 0) {
     // ======================= score wave s = idx =======================
     f16x8_t qh[NCH][NHT];  // B operands: head 16 ht + r16, dims 8g .. 8g + 7 of chunk c
+    // Loads in whole 128-byte lines: instruction j brings the 256 bytes of
+    // this wave's dims of token 4g + j (lane r16: dims 8 r16 .. 8 r16 + 7) of
+    // the cache row and of the gate row, and one more instruction the RoPE
+    // line of token 4g + s (lane r16: dims 4 r16 .. 4 r16 + 3).  Gated, they
+    // go to the unit's tiles in the same layout; the score products read their
+    // A operands (token r16, 8 dims) back from the tile.
     struct Unit {
-      u32x4_t lat[NCH];
-      u32x4_t gat[NCH];
+      u32x4_t lat[4];
+      u32x4_t gat[4];
+      u32x2_t rop;
     };
+    const int lcol = DW * idx + 8 * r16;  // this lane's dims in the cache and gate rows
     auto seg_begin = [&](int b) {
 #pragma unroll
       for (int ht = 0; ht < NHT; ++ht) {
@@ -268,47 +286,72 @@ __device__ __forceinline__ void wide_wave(const SplitArgs& a, unsigned char* lds
     auto chunk = [&](int, int nunits) {
       // Rows of the unit being refilled (a unit past the chunk takes the last
       // unit's rows, never used, so that every step issues the same loads);
-      // the list entry is read one unit ahead.
-      int2 e_next = list[r16];
-      const uint16_t* crow = nullptr;
-      const uint16_t* grow = nullptr;
+      // the list entries of tokens 4g .. 4g + 3 are read one unit ahead.
+      int4 en0 = *reinterpret_cast<const int4*>(list + 4 * g);
+      int4 en1 = *reinterpret_cast<const int4*>(list + 4 * g + 2);
+      const uint16_t* crow[4];
+      const uint16_t* grow[4];
+      const uint16_t* rrow = nullptr;
       auto next_rows = [&](int u) {
-        const int2 e = e_next;
-        e_next = list[TOK * min(u + 1, nunits - 1) + r16];
-        crow = cache + static_cast<int64_t>(e.x) * DQ + dcol;
-        grow = gate + static_cast<int64_t>(e.y) * DC + dcol;
+        const int sl[4] = {en0.x, en0.z, en1.x, en1.z};
+        const int id[4] = {en0.y, en0.w, en1.y, en1.w};
+        const int nx = TOK * min(u + 1, nunits - 1) + 4 * g;
+        en0 = *reinterpret_cast<const int4*>(list + nx);
+        en1 = *reinterpret_cast<const int4*>(list + nx + 2);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          crow[j] = cache + static_cast<int64_t>(sl[j]) * DQ + lcol;
+          grow[j] = gate + static_cast<int64_t>(id[j]) * DC + lcol;
+        }
+        const int rs = idx == 0 ? sl[0] : idx == 1 ? sl[1] : idx == 2 ? sl[2] : sl[3];  // token 4g + s
+        rrow = cache + static_cast<int64_t>(rs) * DQ + DC + 4 * r16;
       };
-      auto issue_chunk = [&](Unit& U, int c) {
-        U.lat[c] = *reinterpret_cast<const u32x4_t*>(crow + 32 * c);
-        U.gat[c] = *reinterpret_cast<const u32x4_t*>(grow + 32 * c);
+      auto issue_chunk = [&](Unit& U, int j) {
+        U.lat[j] = *reinterpret_cast<const u32x4_t*>(crow[j]);
+        U.gat[j] = *reinterpret_cast<const u32x4_t*>(grow[j]);
       };
+      auto issue_rope = [&](Unit& U) { U.rop = *reinterpret_cast<const u32x2_t*>(rrow); };
       auto step = [&](Unit& U, int u) {
-        uint16_t* tw = htile(u % C::NHB) + r16 * TS + dcol;
+        uint16_t* tw = htile(u % C::NHB);
         f32x4_t acc[NHT];
 #pragma unroll
         for (int ht = 0; ht < NHT; ++ht) acc[ht] = f32x4_t{0.f, 0.f, 0.f, 0.f};
         next_rows(u + D);
 #pragma unroll
-        for (int c = 0; c < NCH; ++c) {
-          const u32x4_t gv = gate_chunk_f16(U.lat[c], U.gat[c]);
-          issue_chunk(U, c);  // unit u + D into the registers just consumed
-          *reinterpret_cast<u32x4_t*>(tw + 32 * c) = gv;
-          const f16x8_t h = __builtin_bit_cast(f16x8_t, gv);
+        for (int j = 0; j < 4; ++j) {
+          const u32x4_t gv = gate_chunk_f16(U.lat[j], U.gat[j]);
+          issue_chunk(U, j);  // unit u + D into the registers just consumed
+          *reinterpret_cast<u32x4_t*>(tw + (4 * g + j) * TS + lcol) = gv;
+          __builtin_amdgcn_sched_barrier(0);  // the loads go out here, not after the products
+        }
+        *reinterpret_cast<u32x2_t*>(rtile(u) + (4 * g + idx) * C::RS + 4 * r16) = U.rop;
+        issue_rope(U);
+        __builtin_amdgcn_sched_barrier(0);
+        // A operands: token r16, dims 8g .. 8g + 7 of chunk c (this wave's own writes)
+        f16x8_t h[NCH];
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) h[c] = *reinterpret_cast<const f16x8_t*>(tw + r16 * TS + dcol + 32 * c);
+#pragma unroll
+        for (int c = 0; c < NCH; ++c)
 #pragma unroll
           for (int ht = 0; ht < NHT; ++ht)
-            acc[ht] = __builtin_amdgcn_mfma_f32_16x16x32_f16(h, qh[c][ht], acc[ht], 0, 0, 0);
-        }
+            acc[ht] = __builtin_amdgcn_mfma_f32_16x16x32_f16(h[c], qh[c][ht], acc[ht], 0, 0, 0);
         const int k = u & 1;
 #pragma unroll
         for (int ht = 0; ht < NHT; ++ht) sbuf[((k * NV + idx) * NHT + ht) * 64 + lane] = acc[ht];
-        lds_barrier();  // barrier u: partials and gated tile of unit u visible
+        lds_barrier();  // barrier u: partials, gated tile and RoPE keys of unit u visible
       };
       Unit ring[D];
 #pragma unroll
       for (int u = 0; u < D; ++u) {
         next_rows(u);
 #pragma unroll
-        for (int c = 0; c < NCH; ++c) issue_chunk(ring[u], c);
+        for (int j = 0; j < 4; ++j) {
+          issue_chunk(ring[u], j);
+          __builtin_amdgcn_sched_barrier(0);  // the loop's issue order, so that its waits stay exact
+        }
+        issue_rope(ring[u]);
+        __builtin_amdgcn_sched_barrier(0);
       }
       // Full groups of D units (ring slot u holds units u, u + D, ...), then
       // the remaining nunits % D straight-line, so that on every path the
@@ -326,7 +369,8 @@ __device__ __forceinline__ void wide_wave(const SplitArgs& a, unsigned char* lds
         __builtin_amdgcn_sched_barrier(0);
         if (nfull * D + u < nunits) step(ring[u], nfull * D + u);
       }
-      lds_barrier();  // the value waves' last probabilities
+      // the value waves' steps past the last unit (their last values)
+      for (int u = nunits; u < wide_steps(nunits); ++u) lds_barrier();
     };
     wide_walk(a, wg, list, seg_begin, chunk, [](int) {});
   } else {
@@ -334,9 +378,6 @@ __device__ __forceinline__ void wide_wave(const SplitArgs& a, unsigned char* lds
     bf16x8_t qr[NRC];                      // RoPE B operands: head 16 t + r16, dims 8g .. 8g + 7 of chunk c
     f32x4_t o[NDB][NHT];                   // O^T[dim 128 t + 16 db + 4g + i][head 16 ht + r16]
     float m_run = -INFINITY, l_run = 0.f;  // head 16 t + r16 (log2 domain); l: this lane's tokens
-    struct Unit {
-      u32x4_t rop[NRC];  // RoPE key of token r16: dims 8g .. 8g + 7 of each chunk
-    };
     auto seg_begin = [&](int b) {
 #pragma unroll
       for (int db = 0; db < NDB; ++db)
@@ -349,77 +390,89 @@ __device__ __forceinline__ void wide_wave(const SplitArgs& a, unsigned char* lds
       for (int c = 0; c < NRC; ++c) qr[c] = *reinterpret_cast<const bf16x8_t*>(qrow + 32 * c);
     };
     auto chunk = [&](int n, int nunits) {
-      auto issue = [&](Unit& U, int u) {
-        const int sl = list[TOK * min(u, nunits - 1) + r16].x;
-        const uint16_t* kr = cache + static_cast<int64_t>(sl) * DQ + DC + 8 * g;
+      // Values: O^T += C~^T P^T for the units ua (even) and ua + 1 (if
+      // `pair`), their probabilities written before the last barrier, on the
+      // K = 32 product: lane group g's 8 k-slots are tokens 4g .. 4g + 3 of
+      // unit ua, then the same tokens of unit ua + 1 (a lone unit: zero
+      // probabilities for the second half, its own tile read twice).
+      // vals_prep reads the probabilities and applies the rescale factors:
+      // unit ua's probabilities by unit ub's factor, the sums by both (a
+      // branch per head tile in which a head's maximum grew: rare).
+      auto vals_prep = [&](int ua, bool pair, f16x8_t (&pb)[NHT]) {
+        const int ub = pair ? ua + 1 : ua;
+        const float4 aa = *reinterpret_cast<const float4*>(abuf + ((ua & 3) * 16 + r16) * NHT);
+        const float4 ab = *reinterpret_cast<const float4*>(abuf + ((ub & 3) * 16 + r16) * NHT);
+        const int pr = (ua >> 1) & 1;
 #pragma unroll
-        for (int c = 0; c < NRC; ++c) U.rop[c] = *reinterpret_cast<const u32x4_t*>(kr + 32 * c);
-      };
-      // O^T += C~^T P^T for unit u (its probabilities written before the last
-      // barrier); the LDS operands of a batch are read before any is used
-      auto values = [&](int u) {
-        const int k = u & 1;
-        const int4 fl = *reinterpret_cast<const int4*>(fbuf + k * NHT);
-        const float4 al = *reinterpret_cast<const float4*>(abuf + (k * 16 + r16) * NHT);
-        s16x4_t pb[NHT];
+        for (int ht = 0; ht < NHT; ++ht)
+          pb[ht] = *reinterpret_cast<const f16x8_t*>(pbuf + ((pr * NHT + ht) * 64 + lane) * 2);
+        const float aas[NHT] = {aa.x, aa.y, aa.z, aa.w};
+        const float abs_[NHT] = {ab.x, ab.y, ab.z, ab.w};
+        if (!pair) {
 #pragma unroll
-        for (int ht = 0; ht < NHT; ++ht) pb[ht] = pbuf[(k * NHT + ht) * 64 + lane];
-        // lane r16 of group g reads dims 16 db + 4 (r16 % 4) .. + 3 of token
-        // 4g + r16 / 4; the transposed read hands it dim 16 db + r16 of tokens 4g .. 4g + 3
-        const uint16_t* tr = htile(u % C::NHB) + (4 * g + (r16 >> 2)) * TS + DW * idx + 4 * (r16 & 3);
-        const int fls[NHT] = {fl.x, fl.y, fl.z, fl.w};
-        const float als[NHT] = {al.x, al.y, al.z, al.w};
+          for (int ht = 0; ht < NHT; ++ht)
 #pragma unroll
-        for (int d0 = 0; d0 < NDB; d0 += 4) {
-          s16x4_t at[4];
+            for (int e = 4; e < 8; ++e) pb[ht][e] = static_cast<_Float16>(0.f);
+        }
 #pragma unroll
-          for (int d = 0; d < 4; ++d)
-            at[d] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                (__attribute__((address_space(3))) s16x4_t*)(tr + 16 * (d0 + d)));
-          __builtin_amdgcn_sched_barrier(0);
-          if (d0 == 0) {
+        for (int ht = 0; ht < NHT; ++ht) {
+          const float fbh = pair ? abs_[ht] : 1.f;
+          if (__builtin_amdgcn_ballot_w64(fbh != 1.f)) {
+            const _Float16 sb = static_cast<_Float16>(fbh);
 #pragma unroll
-            for (int ht = 0; ht < NHT; ++ht) {
-              if (__builtin_amdgcn_readfirstlane(fls[ht])) {
-#pragma unroll
-                for (int db = 0; db < NDB; ++db) o[db][ht] *= als[ht];
-              }
-            }
+            for (int e = 0; e < 4; ++e) pb[ht][e] *= sb;
           }
+          const float f = aas[ht] * fbh;
+          if (__builtin_amdgcn_ballot_w64(f != 1.f)) {
 #pragma unroll
-          for (int d = 0; d < 4; ++d)
-#pragma unroll
-            for (int ht = 0; ht < NHT; ++ht)
-              o[d0 + d][ht] = __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(f16x4_t, at[d]),
-                                                                    __builtin_bit_cast(f16x4_t, pb[ht]),
-                                                                    o[d0 + d][ht], 0, 0, 0);
+            for (int db = 0; db < NDB; ++db) o[db][ht] *= f;
+          }
         }
       };
-      // after barrier u: the softmax of head tile t over unit u, then the
-      // values of unit u - 1
-      auto step = [&](Unit& U, int u) {
-        lds_barrier();  // barrier u
-        const int k = u & 1;
-        // RoPE part of the scores, then this head tile's partials
+      // lane r16 of group g reads dims 16 db + 4 (r16 % 4) .. + 3 of token
+      // 4g + r16 / 4; the transposed read hands it dim 16 db + r16 of tokens 4g .. 4g + 3
+      const int toff = (4 * g + (r16 >> 2)) * TS + DW * idx + 4 * (r16 & 3);
+      auto vals_reads = [&](int ua, bool pair, int d0, s16x4_t (&ta)[4], s16x4_t (&tb)[4]) {
+        const uint16_t* tra = htile(ua % C::NHB) + toff;
+        const uint16_t* trb = htile((pair ? ua + 1 : ua) % C::NHB) + toff;
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+          ta[d] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) s16x4_t*)(tra + 16 * (d0 + d)));
+          tb[d] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) s16x4_t*)(trb + 16 * (d0 + d)));
+        }
+      };
+      auto vals_mfma = [&](int d0, const s16x4_t (&ta)[4], const s16x4_t (&tb)[4], const f16x8_t (&pb)[NHT]) {
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+          const f16x8_t av =
+              __builtin_bit_cast(f16x8_t, __builtin_shufflevector(ta[d], tb[d], 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+          for (int ht = 0; ht < NHT; ++ht)
+            o[d0 + d][ht] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av, pb[ht], o[d0 + d][ht], 0, 0, 0);
+        }
+      };
+      // Softmax of head tile t over unit u: the RoPE part of the scores (A
+      // operand: token r16, dims 8g .. 8g + 7 of chunk c) and this head
+      // tile's four partials are read by soft_reads; soft_math is free of
+      // branches, so that its VALU work interleaves with the value products.
+      auto soft_reads = [&](int u, bf16x8_t (&ra)[NRC], f32x4_t (&sv)[NV]) {
+        const uint16_t* rr = rtile(u) + r16 * C::RS + 8 * g;
+#pragma unroll
+        for (int c = 0; c < NRC; ++c) ra[c] = *reinterpret_cast<const bf16x8_t*>(rr + 32 * c);
+#pragma unroll
+        for (int v = 0; v < NV; ++v) sv[v] = sbuf[(((u & 1) * NV + v) * NHT + idx) * 64 + lane];
+      };
+      auto soft_math = [&](int u, const bf16x8_t (&ra)[NRC], const f32x4_t (&sv)[NV]) {
         f32x4_t sc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int c = 0; c < NRC; ++c)
-          sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, U.rop[c]), qr[c], sc, 0, 0, 0);
-        issue(U, u + D);
-        f32x4_t sv[NV];
-#pragma unroll
-        for (int v = 0; v < NV; ++v) sv[v] = sbuf[((k * NV + v) * NHT + idx) * 64 + lane];
-        __builtin_amdgcn_sched_barrier(0);
+        for (int c = 0; c < NRC; ++c) sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ra[c], qr[c], sc, 0, 0, 0);
         sc += (sv[0] + sv[1]) + (sv[2] + sv[3]);
+        const int nt = n - TOK * u;  // valid tokens of the unit (>= 1)
         float x[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) x[q] = sc[q] * a.scale_log2;
-        const int nt = n - TOK * u;  // valid tokens of the unit (>= 1)
-        if (nt < TOK) {
-#pragma unroll
-          for (int q = 0; q < 4; ++q)
-            if (4 * g + q >= nt) x[q] = -INFINITY;
-        }
+        for (int q = 0; q < 4; ++q) x[q] = 4 * g + q < nt ? sc[q] * a.scale_log2 : -INFINITY;
         const float mt = max_over_row_groups(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));
         const float m_new = fmaxf(m_run, mt);  // finite: the unit has a valid token
         const bool grow = m_new > m_run + kLazyRescale;  // false while both are -inf
@@ -432,32 +485,50 @@ __device__ __forceinline__ void wide_wave(const SplitArgs& a, unsigned char* lds
           p[q] = __builtin_amdgcn_exp2f(x[q] - m_run);  // masked: exp2(-inf) = 0
           l_run += p[q];
         }
-        // B operand of the value product: k = token 4g + i, j = head r16
-        pbuf[(k * NHT + idx) * 64 + lane] =
+        // B operand of the value product: k = token 4g + i of the unit's half,
+        // j = head r16; the factor of head r16 (the four lanes of a head
+        // write the same value)
+        pbuf[((((u >> 1) & 1) * NHT + idx) * 64 + lane) * 2 + (u & 1)] =
             __builtin_bit_cast(s16x4_t, u32x2_t{pack_f16x2(p[0], p[1]), pack_f16x2(p[2], p[3])});
-        if (g == 0) abuf[(k * 16 + r16) * NHT + idx] = alpha;
-        const uint64_t any = __builtin_amdgcn_ballot_w64(grow);
-        if (lane == 0) fbuf[k * NHT + idx] = any != 0;
-        if (u > 0) values(u - 1);
+        abuf[((u & 3) * 16 + r16) * NHT + idx] = alpha;
       };
-      Unit ring[D];
+      // After barrier u: the softmax of unit u (past the last unit every
+      // token is masked, which leaves the running maximum and sum as they
+      // are) and half h = u % 2 of the values of the pair of units k2, k2 + 1
+      // (k2 = 2 (u / 2) - 2): dims 64 h .. 64 h + 63 of this wave's 128,
+      // interleaved with the softmax.  The steps go in pairs, straight-line,
+      // so that each accumulator has one product site and stays in place; in
+      // the first pair of steps no pair of units is complete, and the
+      // products add zero (probabilities zero, unit 0's tile read).
+      // pb: the probabilities of the pair, read on the first step of the two
+      auto step = [&](int u, int d0, f16x8_t (&pb)[NHT]) {
+        lds_barrier();  // barrier u
+        const bool live = u >= 2;
+        const int k2 = live ? (u & ~1) - 2 : 0;
+        const bool pair = live && k2 + 1 < nunits;
+        if (d0 == 0) {
+          if (live) {
+            vals_prep(k2, pair, pb);
+          } else {
 #pragma unroll
-      for (int u = 0; u < D; ++u) issue(ring[u], u);
-      const int nfull = nunits / D;
-      for (int i0 = 0; i0 < nfull * D; i0 += D) {
+            for (int ht = 0; ht < NHT; ++ht)
 #pragma unroll
-        for (int u = 0; u < D; ++u) {
-          __builtin_amdgcn_sched_barrier(0);
-          step(ring[u], i0 + u);
+              for (int e = 0; e < 8; ++e) pb[ht][e] = static_cast<_Float16>(0.f);
+          }
         }
+        bf16x8_t ra[NRC];
+        f32x4_t sv[NV];
+        s16x4_t ta[4], tb[4];
+        soft_reads(u, ra, sv);
+        vals_reads(k2, pair, d0, ta, tb);
+        vals_mfma(d0, ta, tb, pb);
+        soft_math(u, ra, sv);
+      };
+      for (int u = 0; u < wide_steps(nunits); u += 2) {
+        f16x8_t pb[NHT];
+        step(u, 0, pb);
+        step(u + 1, 4, pb);
       }
-#pragma unroll
-      for (int u = 0; u < D - 1; ++u) {
-        __builtin_amdgcn_sched_barrier(0);
-        if (nfull * D + u < nunits) step(ring[u], nfull * D + u);
-      }
-      lds_barrier();  // probabilities of the last unit visible
-      values(nunits - 1);
     };
     auto seg_end = [&](int b) {
       const int64_t pbase = (static_cast<int64_t>(wg) + b) * a.H + hblk * C::HEADS;
@@ -478,10 +549,9 @@ __device__ __forceinline__ void wide_wave(const SplitArgs& a, unsigned char* lds
   }
 }
 
-// Units of 16 tokens in flight per score wave (DS) and per value wave (DV)
-// (their registers: a score wave holds 32 VGPRs of rows per unit, a value wave
-// 8 beside its 128 accumulators).
-template <int DS, int DV>
+// D: units of 16 tokens in flight per score wave (34 VGPRs of rows each; the
+// value waves load nothing from global memory inside the unit loop).
+template <int D>
 __global__ __launch_bounds__(WideCfg::NT, 1) void split_wide_kernel(SplitArgs a) {
   __shared__ __attribute__((aligned(16))) unsigned char lds[WideCfg::LDS_BYTES];
   int wg, hblk;
@@ -489,9 +559,9 @@ __global__ __launch_bounds__(WideCfg::NT, 1) void split_wide_kernel(SplitArgs a)
   if (wg >= static_cast<int>(a.sched_hdr[1])) return;  // uniform over the work-group
   const int w = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
   if (w < WideCfg::NV)
-    wide_wave<0, DS>(a, lds, wg, hblk, w);
+    wide_wave<0, D>(a, lds, wg, hblk, w);
   else
-    wide_wave<1, DV>(a, lds, wg, hblk, w - WideCfg::NV);
+    wide_wave<1, D>(a, lds, wg, hblk, w - WideCfg::NV);
 }
 
 }  // namespace egmla
