@@ -395,17 +395,20 @@ __device__ __forceinline__ void wide_wave(const SplitArgs& a, unsigned char* lds
       // K = 32 product: lane group g's 8 k-slots are tokens 4g .. 4g + 3 of
       // unit ua, then the same tokens of unit ua + 1 (a lone unit: zero
       // probabilities for the second half, its own tile read twice).
-      // vals_prep reads the probabilities and applies the rescale factors:
-      // unit ua's probabilities by unit ub's factor, the sums by both (a
-      // branch per head tile in which a head's maximum grew: rare).
-      auto vals_prep = [&](int ua, bool pair, f16x8_t (&pb)[NHT]) {
+      // prep_reads reads the probabilities and the rescale factors,
+      // prep_apply scales unit ua's probabilities by unit ub's factor and the
+      // sums by both (a branch per head tile in which a head's maximum grew:
+      // rare).
+      auto prep_reads = [&](int ua, bool pair, f16x8_t (&pb)[NHT], float4& aa, float4& ab) {
         const int ub = pair ? ua + 1 : ua;
-        const float4 aa = *reinterpret_cast<const float4*>(abuf + ((ua & 3) * 16 + r16) * NHT);
-        const float4 ab = *reinterpret_cast<const float4*>(abuf + ((ub & 3) * 16 + r16) * NHT);
+        aa = *reinterpret_cast<const float4*>(abuf + ((ua & 3) * 16 + r16) * NHT);
+        ab = *reinterpret_cast<const float4*>(abuf + ((ub & 3) * 16 + r16) * NHT);
         const int pr = (ua >> 1) & 1;
 #pragma unroll
         for (int ht = 0; ht < NHT; ++ht)
           pb[ht] = *reinterpret_cast<const f16x8_t*>(pbuf + ((pr * NHT + ht) * 64 + lane) * 2);
+      };
+      auto prep_apply = [&](bool pair, f16x8_t (&pb)[NHT], const float4& aa, const float4& ab) {
         const float aas[NHT] = {aa.x, aa.y, aa.z, aa.w};
         const float abs_[NHT] = {ab.x, ab.y, ab.z, ab.w};
         if (!pair) {
@@ -506,9 +509,18 @@ __device__ __forceinline__ void wide_wave(const SplitArgs& a, unsigned char* lds
         const bool live = u >= 2;
         const int k2 = live ? (u & ~1) - 2 : 0;
         const bool pair = live && k2 + 1 < nunits;
+        // every LDS read of the step first (one round trip), then the
+        // branches of the rescale, then the products and the softmax
+        float4 aa, ab;
+        if (d0 == 0) prep_reads(k2, pair, pb, aa, ab);
+        bf16x8_t ra[NRC];
+        f32x4_t sv[NV];
+        s16x4_t ta[4], tb[4];
+        soft_reads(u, ra, sv);
+        vals_reads(k2, pair, d0, ta, tb);
         if (d0 == 0) {
           if (live) {
-            vals_prep(k2, pair, pb);
+            prep_apply(pair, pb, aa, ab);
           } else {
 #pragma unroll
             for (int ht = 0; ht < NHT; ++ht)
@@ -516,11 +528,6 @@ __device__ __forceinline__ void wide_wave(const SplitArgs& a, unsigned char* lds
               for (int e = 0; e < 8; ++e) pb[ht][e] = static_cast<_Float16>(0.f);
           }
         }
-        bf16x8_t ra[NRC];
-        f32x4_t sv[NV];
-        s16x4_t ta[4], tb[4];
-        soft_reads(u, ra, sv);
-        vals_reads(k2, pair, d0, ta, tb);
         vals_mfma(d0, ta, tb, pb);
         soft_math(u, ra, sv);
       };
