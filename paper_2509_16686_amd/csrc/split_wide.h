@@ -6,36 +6,45 @@
 // wave of each role and the VALU and LDS work of one overlaps the matrix
 // products of the other.
 //   * Score wave s (w = s < 4) owns latent dims 128 s .. 128 s + 127 of every
-//     token: it loads its slice of a token's cache row and gate row straight
-//     from HBM into registers in the layout of the MFMA A operand (lane: token
-//     lane % 16, 8 consecutive dims), gates it there, writes it into the
-//     unit's gated tile in LDS (row = token) and computes the partial scores
+//     token.  It loads its 256 bytes of a token's cache row and gate row in
+//     whole 128-byte lines (one instruction: 4 tokens, 16 lanes each) and the
+//     RoPE line of tokens 4g + s, gates the latent (fp16), writes both into
+//     the unit's tiles in LDS (row = token), reads its A operands (token
+//     lane % 16, 8 dims) back and computes the partial scores
 //     S_s^T[token][head] of the 64 heads on v_mfma_f32_16x16x32_f16, the
-//     absorbed query of its dims held in registers.  A chunk's loads for a
-//     later unit go out as soon as the chunk has been gated, so the work-
-//     group's loads reach the texture unit spread over the step.
+//     absorbed query of its dims held in registers.  A chunk's loads for the
+//     unit two ahead go out as soon as the chunk has been gated.
 //   * Value wave t (w = 4 + t) owns head tile t (heads 16 t .. 16 t + 15) for
 //     the softmax and latent dims 128 t .. 128 t + 127 of the output: it adds
 //     the four partials of its head tile and the RoPE part (its own product
-//     over the 64 RoPE dims), runs the online softmax of its 16 heads (log2
-//     domain, lazy rescale), and accumulates O^T[dim][head] += C~^T P^T for
-//     its dims and all 64 heads on v_mfma_f32_16x16x16_f16, the A operand
-//     read with ds_read_b64_tr_b16 from the gated tile.
+//     over the 64 RoPE dims, A operand from the RoPE tile), runs the online
+//     softmax of its 16 heads (log2 domain, lazy rescale), and accumulates
+//     O^T[dim][head] += C~^T P^T for its dims and all 64 heads over pairs of
+//     units on v_mfma_f32_16x16x32_f16 (k-slots of lane group g: tokens
+//     4g .. 4g + 3 of both units; A operands read with ds_read_b64_tr_b16
+//     from the gated tiles).  It loads nothing from global memory in the unit
+//     loop.
 // Each role runs its own loop (so their registers do not add up) and both
-// meet the same barriers, one per unit of 16 tokens: the partials and gated
-// tile of unit u are written before barrier u; between barriers u and u + 1
-// the value waves run the softmax of unit u and the values of unit u - 1
-// (probabilities exchanged among them through LDS) while the score waves
-// compute unit u + 1.  The partial-score and probability buffers are
-// double-buffered, the gated tiles triple-buffered.
+// meet the same barriers, one per unit of 16 tokens: the partials and tiles
+// of unit u are written before barrier u; between barriers u and u + 1 the
+// value waves run the softmax of unit u and half of the value product of the
+// last complete pair of units (dims 64 h .. 64 h + 63 of their 128, h = u % 2)
+// in one basic block, so that the two interleave, while the score waves
+// compute unit u + 1.  Partial scores are double-buffered, probabilities kept
+// per pair (two pairs), rescale factors per unit (four), RoPE keys in two
+// buffers and gated tiles in five (a tile lives five unit steps).  Loads in
+// whole lines matter: a load-only copy of the kernel's access pattern with
+// 16 rows x 64 bytes per instruction takes about twice as long.
 //
 // Precision.  The latent part of the scores and the values run on the fp16
 // MFMA: the absorbed query is one rounding of its fp32 sum to fp16, each gated
 // latent one rounding of the exact fp32 product c * g, each probability one
 // rounding to fp16 (11-bit significands: rows dominated by a few keys stay
 // within the element-wise bound, which bf16 operands would need hi + lo
-// products for).  The RoPE part (bf16 x bf16) is exact.  Magnitudes must stay
-// below 65504.
+// products for); where the second unit of a pair raised a head's maximum,
+// the first unit's probabilities are scaled by that factor (below 2^-8) in
+// fp16, a second rounding of terms at most 2^-8 of the new maximum.  The RoPE
+// part (bf16 x bf16) is exact.  Magnitudes must stay below 65504.
 //
 // The two head blocks of a 128-head layer run the same token range on the same
 // XCD (block ids 8 apart), so the second fetch of a token's rows hits that
