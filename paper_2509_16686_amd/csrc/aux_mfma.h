@@ -165,6 +165,8 @@ __global__ __launch_bounds__(256) void absorb_mfma_kernel(const uint16_t* __rest
 //     wps = 16 / pow2ceil(n) waves, and wave p of a sequence merges its
 //     partials p, p + wps, ... in batches of 4, 8 or 16 (at most 8 for
 //     d_c > 128) (maxima, sums and partial outputs loaded together) into LDS.
+//     NORM (the head-split kernel's partials): each partial output is an fp16
+//     row already divided by its sum l, and enters with weight e * l.
 //  3. All threads merge each sequence's wps parts into its latent row o / l.
 //  4. out^T[v][b] = W_UV[h][v][:] . o[b][:] on v_mfma_f32_16x16x32_bf16, the
 //     16 sequences being the 16 columns of the B operand, o split into bf16
@@ -187,19 +189,30 @@ __device__ __forceinline__ int comb_dim(int lane, int j) {
 
 // One batch of SB splits of the online merge: the splits first + stride * t
 // for t = s0 .. s0 + SB - 1 (t clamped to ns - 1, counted while t < ns).
-// Their maxima, sums and partial outputs load together.
-template <int DC, int SB>
-__device__ __forceinline__ void merge_batch(const float* __restrict__ part_ml, const float* __restrict__ part_o,
+// Their maxima, sums and partial outputs load together.  NORM: the partial
+// outputs are fp16 rows already divided by their sums (weight e * l).
+template <int DC, int SB, bool NORM = false>
+__device__ __forceinline__ void merge_batch(const float* __restrict__ part_ml, const void* __restrict__ part_ov,
                                             int64_t base, int H, int first, int stride, int s0, int ns, int lane,
                                             float& M, float& Ls, float (&acc)[DC / 64]) {
   constexpr int PER = DC / 64;
+  const float* __restrict__ part_o = static_cast<const float*>(part_ov);
+  const uint16_t* __restrict__ part_h = static_cast<const uint16_t*>(part_ov);
   float pv[SB][PER];
   float2 ml[SB];
 #pragma unroll
   for (int u = 0; u < SB; ++u) {
     const int64_t row = base + static_cast<int64_t>(first + stride * min(s0 + u, ns - 1)) * H;
     ml[u] = *reinterpret_cast<const float2*>(part_ml + row * 2);
-    if constexpr (PER % 2 == 0) {
+    if constexpr (NORM) {
+      static_assert(PER % 2 == 0, "fp16 partial rows: adjacent pairs per lane");
+#pragma unroll
+      for (int i = 0; i < PER / 2; ++i) {
+        const uint32_t v = *reinterpret_cast<const uint32_t*>(part_h + row * DC + 128 * i + 2 * lane);
+        pv[u][2 * i] = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(v & 0xffffu)));
+        pv[u][2 * i + 1] = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(v >> 16)));
+      }
+    } else if constexpr (PER % 2 == 0) {
 #pragma unroll
       for (int i = 0; i < PER / 2; ++i) {
         const float2 v = *reinterpret_cast<const float2*>(part_o + row * DC + 128 * i + 2 * lane);
@@ -226,15 +239,16 @@ __device__ __forceinline__ void merge_batch(const float* __restrict__ part_ml, c
   for (int u = 0; u < SB; ++u) {
     const float e = s0 + u < ns && live ? __builtin_amdgcn_exp2f(ml[u].x - Mn) : 0.f;
     Ls += ml[u].y * e;
+    const float wgt = NORM ? e * ml[u].y : e;
 #pragma unroll
-    for (int j = 0; j < PER; ++j) acc[j] = fmaf(e, pv[u][j], acc[j]);
+    for (int j = 0; j < PER; ++j) acc[j] = fmaf(wgt, pv[u][j], acc[j]);
   }
   M = Mn;
 }
 
-template <int DC, int DV>
+template <int DC, int DV, bool NORM = false>
 __global__ __launch_bounds__(kCombWaves * 64) void combine_mfma_kernel(const float* __restrict__ part_ml,
-                                                                       const float* __restrict__ part_o,
+                                                                       const void* __restrict__ part_o,
                                                                        const uint16_t* __restrict__ w_uv,
                                                                        const int32_t* __restrict__ seq_lens,
                                                                        uint16_t* __restrict__ out, int B, int H,
@@ -293,12 +307,12 @@ __global__ __launch_bounds__(kCombWaves * 64) void combine_mfma_kernel(const flo
     const int64_t row0 = seq_rows ? seq_rows[b].x : static_cast<int64_t>(b) * s_max * slices;
     const int64_t base = row0 * H + h;  // + partial * H
     if (ns <= 4) {
-      merge_batch<DC, 4>(part_ml, part_o, base, H, part, wps, 0, ns, lane, M, Ls, acc);
+      merge_batch<DC, 4, NORM>(part_ml, part_o, base, H, part, wps, 0, ns, lane, M, Ls, acc);
     } else if (ns <= 8) {
-      merge_batch<DC, 8>(part_ml, part_o, base, H, part, wps, 0, ns, lane, M, Ls, acc);
+      merge_batch<DC, 8, NORM>(part_ml, part_o, base, H, part, wps, 0, ns, lane, M, Ls, acc);
     } else {
       for (int s0 = 0; s0 < ns; s0 += kSBMax)
-        merge_batch<DC, kSBMax>(part_ml, part_o, base, H, part, wps, s0, ns, lane, M, Ls, acc);
+        merge_batch<DC, kSBMax, NORM>(part_ml, part_o, base, H, part, wps, s0, ns, lane, M, Ls, acc);
     }
   }
 #pragma unroll

@@ -346,10 +346,20 @@ hipError_t launch_combine_dc(dim3 grid, hipStream_t stream, const float* pm, con
     return hipGetLastError();
   }
   const size_t lds = combine_lds_bytes(DC);
+  if constexpr (DC == 512) {
+    // the head-split kernel (balanced schedule) writes fp16 rows normalised by their sums
+    if (seq_rows) {
+      hipError_t e = set_lds(combine_mfma_kernel<DC, 128, true>, lds);
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL((combine_mfma_kernel<DC, 128, true>), grid, dim3(kCombWaves * 64), lds, stream, pm,
+                         static_cast<const void*>(po), wv, seq_lens, ov, B, H, cap, split, s_max, slices, seq_rows);
+      return hipGetLastError();
+    }
+  }
   hipError_t e = set_lds(combine_mfma_kernel<DC, 128>, lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((combine_mfma_kernel<DC, 128>), grid, dim3(kCombWaves * 64), lds, stream, pm, po, wv, seq_lens,
-                     ov, B, H, cap, split, s_max, slices, seq_rows);
+  hipLaunchKernelGGL((combine_mfma_kernel<DC, 128>), grid, dim3(kCombWaves * 64), lds, stream, pm,
+                     static_cast<const void*>(po), wv, seq_lens, ov, B, H, cap, split, s_max, slices, seq_rows);
   return hipGetLastError();
 }
 

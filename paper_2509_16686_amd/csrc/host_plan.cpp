@@ -26,7 +26,8 @@ bool mfma_shape_supported(const eg_mla_dims& d) {
 
 bool tok_kernel_shape(const eg_mla_dims& d) { return d.latent_dim == 128 && d.rope_dim == 64; }
 bool heads_kernel_shape(const eg_mla_dims& d) {
-  return d.latent_dim == 512 && d.rope_dim == 64 && d.head_dim == 128 && d.num_heads % kHeadsPerItemWide == 0;
+  return d.latent_dim == 512 && d.rope_dim == 64 && d.head_dim == 128 && d.v_head_dim == 128 &&
+         d.num_heads % kHeadsPerItemWide == 0;
 }
 
 eg_mla_status check_dims(const eg_mla_dims* d) {
@@ -111,8 +112,9 @@ eg_mla_status make_decode_plan(const eg_mla_dims& d, int32_t batch, int32_t max_
   off = align_up(off + B * H * DQ * 4);
   p.off_ml = off;
   off = align_up(off + rows * H * 2 * 4);
+  // partial outputs: fp32 sums, or (balanced schedule) fp16 rows normalised by their sums
   p.off_o = off;
-  off = align_up(off + rows * H * static_cast<size_t>(d.latent_dim) * 4);
+  off = align_up(off + rows * H * static_cast<size_t>(d.latent_dim) * (p.balanced ? 2 : 4));
   if (p.balanced) {
     p.off_sched = off;
     off = align_up(off + 16 + kWideMaxGroups * 8 + B * 8);

@@ -87,13 +87,14 @@ struct WideCfg {
   static constexpr int SB = RT + NRB * TOK * RS * 2;          // [2][NV][NHT][64] f32x4: partial scores
   static constexpr int PB = SB + 2 * NV * NHT * 64 * 16;      // [2][NHT][64][2] fp16 x 4: probabilities of unit pairs
   static constexpr int AL = PB + 2 * NHT * 64 * 16;           // [4][16][NHT] f32: rescale factor of head 16 ht + r
-  static constexpr int LIST = AL + 4 * HEADS * 4;             // int2 (slot, id) per token
+  static constexpr int LB = AL + 4 * HEADS * 4;               // [16][NHT] f32: softmax sum of head 16 ht + r
+  static constexpr int LIST = LB + HEADS * 4;                 // int2 (slot, id) per token
   static constexpr int LISTCAP = 3072;                        // tokens listed at a time
   static constexpr int LDS_BYTES = LIST + LISTCAP * 8;
   static_assert(NHT == NV && NHT == 4, "one head tile per value wave; 16-byte factor reads");
   static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
   static_assert(LISTCAP % NT == 0 && LISTCAP % TOK == 0, "list chunk");
-  static_assert(RT % 16 == 0 && SB % 16 == 0 && PB % 16 == 0 && LIST % 16 == 0, "alignment");
+  static_assert(RT % 16 == 0 && SB % 16 == 0 && PB % 16 == 0 && LB % 16 == 0 && LIST % 16 == 0, "alignment");
   static_assert(TOK == 4 * NV, "a score wave loads the RoPE lines of 4 tokens per unit");
 };
 
@@ -259,6 +260,7 @@ __device__ __forceinline__ void wide_wave(const SplitArgs& a, unsigned char* lds
   f32x4_t* sbuf = reinterpret_cast<f32x4_t*>(lds + C::SB);  // [2][NV][NHT][64]
   s16x4_t* pbuf = reinterpret_cast<s16x4_t*>(lds + C::PB);  // [2][NHT][64][2]: pair (u / 2) % 2, unit u % 2
   float* abuf = reinterpret_cast<float*>(lds + C::AL);      // [4][16][NHT]: unit u % 4
+  float* lbuf = reinterpret_cast<float*>(lds + C::LB);      // [16][NHT]
   auto htile = [&](int h) { return reinterpret_cast<uint16_t*>(lds + C::HT) + h * TOK * TS; };
   auto rtile = [&](int u) { return reinterpret_cast<uint16_t*>(lds + C::RT) + (u % C::NRB) * TOK * C::RS; };
 
@@ -539,6 +541,13 @@ __device__ __forceinline__ void wide_wave(const SplitArgs& a, unsigned char* lds
         }
         vals_mfma(d0, ta, tb, pb);
         soft_math(u, ra, sv);
+        // the softmax sums of this head tile (final: the last unit's softmax
+        // ran at step nunits - 1), for the normalised partial rows written
+        // after the last barrier
+        if (u == wide_steps(nunits) - 2) {
+          const float lt = sum_over_row_groups(l_run);
+          if (g == 0) lbuf[r16 * NHT + idx] = lt;
+        }
       };
       for (int u = 0; u < wide_steps(nunits); u += 2) {
         f16x8_t pb[NHT];
@@ -546,19 +555,28 @@ __device__ __forceinline__ void wide_wave(const SplitArgs& a, unsigned char* lds
         step(u + 1, 4, pb);
       }
     };
+    // The segment's partial: each row O / l in fp16 (the sums of all four head
+    // tiles were written to LDS before the last barrier) and, for this head
+    // tile, (m, l) in fp32.
     auto seg_end = [&](int b) {
       const int64_t pbase = (static_cast<int64_t>(wg) + b) * a.H + hblk * C::HEADS;
+      const float4 lt = *reinterpret_cast<const float4*>(lbuf + r16 * NHT);
+      const float lts[NHT] = {lt.x, lt.y, lt.z, lt.w};
+      uint16_t* part = reinterpret_cast<uint16_t*>(a.part_o);
 #pragma unroll
       for (int ht = 0; ht < NHT; ++ht) {
-        float* orow = a.part_o + (pbase + 16 * ht + r16) * DC + DW * idx + 4 * g;
+        const float inv = 1.f / lts[ht];  // >= 1: the maximum's own term
+        uint16_t* orow = part + (pbase + 16 * ht + r16) * DC + DW * idx + 4 * g;
 #pragma unroll
-        for (int db = 0; db < NDB; ++db)
-          __builtin_nontemporal_store(o[db][ht], reinterpret_cast<f32x4_t*>(orow + 16 * db));
+        for (int db = 0; db < NDB; ++db) {
+          const f32x4_t v = o[db][ht];
+          const u32x2_t h = {pack_f16x2(v[0] * inv, v[1] * inv), pack_f16x2(v[2] * inv, v[3] * inv)};
+          __builtin_nontemporal_store(h, reinterpret_cast<u32x2_t*>(orow + 16 * db));
+        }
       }
-      const float l = sum_over_row_groups(l_run);
       if (g == 0) {
         __builtin_nontemporal_store(m_run, a.part_ml + (pbase + 16 * idx + r16) * 2 + 0);
-        __builtin_nontemporal_store(l, a.part_ml + (pbase + 16 * idx + r16) * 2 + 1);
+        __builtin_nontemporal_store(lts[idx], a.part_ml + (pbase + 16 * idx + r16) * 2 + 1);
       }
     };
     wide_walk(a, wg, list, seg_begin, chunk, seg_end);
