@@ -542,6 +542,9 @@ def main():
                     help="unfolded gate with embedding width E (the paper recommends 512): every step first "
                          "computes one gate row per cache row from its token embedding (eg_mla_gate_rows), then "
                          "decodes with the row indices as ids; 0 = the folded gate table")
+    ap.add_argument("--unfolded-distinct", action="store_true",
+                    help="with --unfolded-gate: each step computes the gate row of each distinct token id once "
+                         "into a [V, d_c] table (eg_mla_gate_table), which the decode takes with the step's own ids")
     ap.add_argument("--layer-group", type=int, default=0, metavar="G",
                     help="time G layers of a layer group (App. H) decoding one shared cache, against G layers "
                          "with caches of their own")
@@ -596,19 +599,33 @@ def main():
         ge = W.generate_gate_embedding(wl, E)
         emb_d, wue_d = B.to_device_tensor(ge.emb, wl.dtype), B.to_device_tensor(ge.w_ue, wl.dtype)
         n_rows = inp.num_rows
-        row_gate = torch.empty((n_rows, wl.latent_dim), dtype=dd0.gate.dtype, device="cuda")
-        row_ids = torch.arange(n_rows, dtype=torch.int32, device="cuda")
-        dims_u = B.dims_for(wl.replace(vocab=n_rows))
-        # one embedding table per rotating copy, so that the table (tens of MB)
-        # is not served from the 256 MB MALL from one step to the next
-        for k, c in enumerate(copies):
-            c.gate_src_ids, c.dims, c.gate, c.ids = c.ids, dims_u, row_gate, row_ids
-            c.emb = emb_d if k == 0 else emb_d.clone()
-        gate_call = L.eg_mla_gate_rows
-        # the decode now gathers one distinct gate row per cache row
-        traffic = A.decode_bytes(batch=wl.batch, heads=wl.heads, head_dim=wl.head_dim, v_head_dim=wl.v_head_dim,
-                                 latent_dim=wl.latent_dim, rope_dim=wl.rope_dim, elem_bytes=wl.elem_bytes,
-                                 total_tokens=inp.total_tokens(), distinct_ids=inp.total_tokens())
+        n_distinct = int(np.unique(np.clip(inp.token_ids, 0, wl.vocab - 1)).size)
+        if args.unfolded_distinct:
+            # a [V, d_c] table refilled each step for the step's distinct ids;
+            # the decode keeps its own ids and dims
+            row_gate = torch.empty((wl.vocab, wl.latent_dim), dtype=dd0.gate.dtype, device="cuda")
+            dims_g = B.dims_for(wl)
+            marks_bytes = B.gate_table_marks_size(dims_g, E, wl.vocab)
+            marks = torch.zeros((marks_bytes + 3) // 4, dtype=torch.int32, device="cuda")
+            for k, c in enumerate(copies):
+                c.gate_src_ids, c.gate = c.ids, row_gate
+                c.emb = emb_d if k == 0 else emb_d.clone()
+            gate_call = L.eg_mla_gate_table
+        else:
+            row_gate = torch.empty((n_rows, wl.latent_dim), dtype=dd0.gate.dtype, device="cuda")
+            row_ids = torch.arange(n_rows, dtype=torch.int32, device="cuda")
+            dims_u = B.dims_for(wl.replace(vocab=n_rows))
+            # one embedding table per rotating copy, so that the table (tens of MB)
+            # is not served from the 256 MB MALL from one step to the next
+            for k, c in enumerate(copies):
+                c.gate_src_ids, c.dims, c.gate, c.ids = c.ids, dims_u, row_gate, row_ids
+                c.emb = emb_d if k == 0 else emb_d.clone()
+            gate_call = L.eg_mla_gate_rows
+            # the decode now gathers one distinct gate row per cache row
+            traffic = A.decode_bytes(batch=wl.batch, heads=wl.heads, head_dim=wl.head_dim,
+                                     v_head_dim=wl.v_head_dim, latent_dim=wl.latent_dim, rope_dim=wl.rope_dim,
+                                     elem_bytes=wl.elem_bytes, total_tokens=inp.total_tokens(),
+                                     distinct_ids=inp.total_tokens())
     path = {"auto": B.PATH_AUTO, "valu": B.PATH_VALU, "mfma": B.PATH_MFMA}[args.path]
     plan0 = B.make_plan(path, args.split, id_slices=args.id_slices)
     ws_bytes = B.decode_workspace_size(dd0.dims, wl.batch, dd0.max_pages, plan0)
@@ -630,7 +647,15 @@ def main():
 
     call = L.eg_mla_decode_planned
 
+    stamp = [0]
+
     def gate_args(dd):
+        if args.unfolded_distinct:
+            # a fresh stamp for every call: each call computes every distinct id of its step
+            stamp[0] += 1
+            return (ctypes.byref(dims_g), E, int(dd.emb.shape[0]), n_rows, dd.gate_src_ids.data_ptr(),
+                    dd.emb.data_ptr(), wue_d.data_ptr(), row_gate.data_ptr(), marks.data_ptr(), marks_bytes,
+                    stamp[0], stream)
         return (ctypes.byref(dd.dims), E, int(dd.emb.shape[0]), n_rows, dd.gate_src_ids.data_ptr(),
                 dd.emb.data_ptr(), wue_d.data_ptr(), row_gate.data_ptr(), stream)
 
@@ -745,7 +770,9 @@ def main():
                    "latent_dim": wl.latent_dim, "rope_dim": wl.rope_dim, "vocab": wl.vocab,
                    "context": wl.seq_len if wl.seq_len else list(wl.seq_len_range), "paged": wl.paged,
                    "storage": wl.dtype, "path": args.path, "split_tokens": args.split, "id_slices": args.id_slices,
-                   "rotating_copies": R, "gate": f"unfolded, embedding width {E}" if E > 0 else "folded table"},
+                   "rotating_copies": R,
+                   "gate": (f"unfolded, embedding width {E}" + (", per distinct id" if args.unfolded_distinct else ""))
+                   if E > 0 else "folded table"},
         "hbm_gbps_call": traffic.total / (ms_per_step * 1e-3) / 1e9,
         "hbm_frac_call": traffic.total / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
         # estimate, not a measurement: every layer of a 24-layer model taking one such call
@@ -758,11 +785,15 @@ def main():
                      "algorithmic_bytes_per_launch": k_bytes, "traffic_bytes_per_launch": t_bytes, "kernel_us": k_avg_ms * 1e3},
     }
     if E > 0:
-        # algorithmic: the gathered embedding rows, the gate rows written, the ids, W^UE once
-        g_bytes = n_rows * (E * wl.elem_bytes + wl.latent_dim * wl.elem_bytes + 4) + wl.latent_dim * E * wl.elem_bytes
-        out["unfolded_gate"] = {"emb_dim": E, "rows": n_rows, "gate_rows_us": gate_ms * 1e3,
+        # algorithmic: the gathered embedding rows, the gate rows written, the ids, W^UE once (distinct
+        # ids: one embedding row and one table row per distinct id, the ids and one claim per row)
+        n_g = n_distinct if args.unfolded_distinct else n_rows
+        g_bytes = (n_g * (E * wl.elem_bytes + wl.latent_dim * wl.elem_bytes) + n_rows * 4 * (2 if args.unfolded_distinct else 1)
+                   + wl.latent_dim * E * wl.elem_bytes)
+        out["unfolded_gate"] = {"emb_dim": E, "rows": n_rows, "distinct_ids": n_distinct,
+                                "per_distinct_id": bool(args.unfolded_distinct), "gate_rows_us": gate_ms * 1e3,
                                 "gate_rows_gbps": g_bytes / (gate_ms * 1e-3) / 1e9,
-                                "gate_rows_tflops": 2.0 * n_rows * E * wl.latent_dim / (gate_ms * 1e-3) / 1e12,
+                                "gate_rows_tflops": 2.0 * n_g * E * wl.latent_dim / (gate_ms * 1e-3) / 1e12,
                                 "algorithmic_bytes": g_bytes}
         log(f"bench: gate rows {gate_ms * 1e3:.2f} us ({out['unfolded_gate']['gate_rows_gbps']:.0f} GB/s)")
     if not args.no_cpu_baseline:

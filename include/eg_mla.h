@@ -238,8 +238,9 @@ eg_mla_status eg_mla_decode_noalloc(const eg_mla_dims* dims, int32_t batch, cons
  *   out[i, :] = W^UE Emb[ids[i], :]
  * with e = emb_dim embedding components in and d_c = dims->latent_dim gate
  * values out, products accumulated in fp32 and rounded once to the storage
- * type (bf16 x bf16 MFMA products when dtype is bf16, emb_dim % 32 == 0,
- * d_c % 16 == 0 and emb/w_ue are 16-byte aligned; fp32 VALU otherwise).
+ * type (bf16 x bf16 MFMA products when dtype is bf16, emb_dim % 128 == 0,
+ * d_c % 32 == 0, emb/w_ue 16-byte and out 8-byte aligned; fp32 VALU
+ * otherwise).
  *   - ids = 0 .. V-1 gives the folded gate table G = Emb W^UE^T that
  *     eg_mla_decode takes (the table-lookup variant of Sec. 5.2, folded
  *     once when the model is loaded);
@@ -254,6 +255,41 @@ eg_mla_status eg_mla_decode_noalloc(const eg_mla_dims* dims, int32_t batch, cons
  * ------------------------------------------------------------------------- */
 eg_mla_status eg_mla_gate_rows(const eg_mla_dims* dims, int32_t emb_dim, int32_t emb_vocab, int64_t n,
                                const int32_t* ids, const void* emb, const void* w_ue, void* out, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Gate rows of the distinct ids of a step (Sec. 3.1 Eq. (3)-(4)): for every
+ * id among ids[0 .. n),
+ *   table[id, :] = W^UE Emb[id, :]
+ * with the arithmetic of eg_mla_gate_rows (the same bits); rows of ids not
+ * in the list are left as they are.  This is the unfolded model's gate
+ * computation with each distinct id computed once: eg_mla_decode then takes
+ * `table` as its gate table with the step's own token ids
+ * (dims->vocab_size = emb_vocab).  On the MFMA path a first kernel claims
+ * each id with an atomic exchange of `stamp` into `marks` and lists the ids
+ * whose claim found another value; the gate rows are computed over that
+ * list only.  Other paths compute every row and store identical bits for
+ * repeated ids.
+ *
+ *   emb, w_ue, ids as for eg_mla_gate_rows;  table [emb_vocab, d_c]
+ *   marks  device workspace of eg_mla_gate_table_marks_size(dims, emb_dim,
+ *          emb_vocab) bytes (a 128-byte stamp line per id, two counters, an
+ *          id list),
+ *          4-byte aligned, owned by the caller: zero it before the first
+ *          call and keep it between calls;
+ *   stamp  1 on the first call after the marks were zeroed, then the previous
+ *          call's stamp plus one (the counters alternate by the stamp's
+ *          parity); zero the marks again before the stamp would wrap to 0.
+ * Calls that share marks must be ordered (same stream or synchronised).
+ * n == 0 is a no-op (the stamp is not consumed: the next call takes it);
+ * stamp == 0 is EG_MLA_ERR_INVALID_ARG; marks null, misaligned or smaller
+ * than the query is EG_MLA_ERR_WORKSPACE.
+ * eg_mla_gate_table_marks_size returns 0 for invalid dims or sizes.
+ * ------------------------------------------------------------------------- */
+size_t eg_mla_gate_table_marks_size(const eg_mla_dims* dims, int32_t emb_dim, int32_t emb_vocab);
+
+eg_mla_status eg_mla_gate_table(const eg_mla_dims* dims, int32_t emb_dim, int32_t emb_vocab, int64_t n,
+                                const int32_t* ids, const void* emb, const void* w_ue, void* table, void* marks,
+                                size_t marks_bytes, uint32_t stamp, void* stream);
 
 /* ---------------------------------------------------------------------------
  * Prefill reference: plain causal attention over one sequence of T tokens in

@@ -25,7 +25,8 @@ EXPORTS = ["eg_mla_status_string", "eg_mla_check_dims", "eg_mla_append", "eg_mla
            "eg_mla_decode", "eg_mla_decode_planned", "eg_mla_gate_rows", "eg_mla_prefill_workspace_size",
            "eg_mla_prefill_ref", "eg_mla_prefill_varlen_workspace_size", "eg_mla_prefill_varlen",
            "eg_mla_decode_literal_workspace_size", "eg_mla_decode_literal", "eg_mla_decode_noalloc",
-           "eg_mla_append_workspace_size", "eg_mla_append_ws"]
+           "eg_mla_append_workspace_size", "eg_mla_append_ws", "eg_mla_gate_table_marks_size",
+           "eg_mla_gate_table"]
 NOALLOC_SCRATCH_BYTES = 32 << 20  # EG_MLA_NOALLOC_SCRATCH_BYTES
 LITERAL_NO_LN, LITERAL_ADD = 1, 2
 
@@ -84,6 +85,10 @@ def lib() -> ctypes.CDLL:
     L.eg_mla_decode_noalloc.argtypes = [pd, i32, vp, vp, vp, vp, vp, vp, vp, vp, i32, i64, vp, vp]
     L.eg_mla_gate_rows.restype = ctypes.c_int
     L.eg_mla_gate_rows.argtypes = [pd, i32, i32, i64, vp, vp, vp, vp, vp]
+    L.eg_mla_gate_table_marks_size.restype = sz
+    L.eg_mla_gate_table_marks_size.argtypes = [pd, i32, i32]
+    L.eg_mla_gate_table.restype = ctypes.c_int
+    L.eg_mla_gate_table.argtypes = [pd, i32, i32, i64, vp, vp, vp, vp, vp, sz, ctypes.c_uint32, vp]
     L.eg_mla_prefill_workspace_size.restype = sz
     L.eg_mla_prefill_workspace_size.argtypes = [pd, i32]
     L.eg_mla_prefill_ref.restype = ctypes.c_int
@@ -200,6 +205,19 @@ def gate_rows(dims: Dims, ids, emb, w_ue, out, stream=None) -> None:
     emb_vocab, emb_dim = int(emb.shape[0]), int(emb.shape[1])
     _check(lib().eg_mla_gate_rows(ctypes.byref(dims), emb_dim, emb_vocab, n, _ptr(ids), _ptr(emb), _ptr(w_ue),
                                   _ptr(out), _stream(stream)), "eg_mla_gate_rows")
+
+
+def gate_table_marks_size(dims: Dims, emb_dim: int, emb_vocab: int) -> int:
+    return int(lib().eg_mla_gate_table_marks_size(ctypes.byref(dims), emb_dim, emb_vocab))
+
+
+def gate_table(dims: Dims, ids, emb, w_ue, table, marks, stamp: int, stream=None) -> None:
+    """eg_mla_gate_table over device tensors: table[id] = W_UE Emb[id] for the distinct ids."""
+    n = int(ids.shape[0])
+    emb_vocab, emb_dim = int(emb.shape[0]), int(emb.shape[1])
+    _check(lib().eg_mla_gate_table(ctypes.byref(dims), emb_dim, emb_vocab, n, _ptr(ids), _ptr(emb), _ptr(w_ue),
+                                   _ptr(table), _ptr(marks), int(marks.numel() * marks.element_size()), stamp,
+                                   _stream(stream)), "eg_mla_gate_table")
 
 
 def decode_literal_workspace_size(dims: Dims, batch: int, max_pages: int) -> int:

@@ -38,6 +38,7 @@ constexpr int kGateThreads = 256;        // VALU kernel
 constexpr int kGateWaves = 8;            // MFMA kernel: waves per work-group (2 per SIMD)
 constexpr int kGateLdsBudget = 150 * 1024;  // bytes of W^UE slice in LDS, at most
 
+
 typedef __attribute__((ext_vector_type(16))) float gate_f32x16_t;
 
 // One half-pass of a 32-row block: chunks 0 .. NH-1 of bq against W^UE
@@ -68,9 +69,9 @@ __device__ __forceinline__ void gate_products(const bf16x8_t (&bq)[NH], const ui
 // Stores a finished 32-row block: lane holds out^T[column 32 cb + 8 q + 4 h + t][row]
 // in acc[cb][4 q + t].
 template <int NCB>
-__device__ __forceinline__ void gate_store(const gate_f32x16_t (&acc)[NCB], uint16_t* out, int64_t orow, int64_t n,
+__device__ __forceinline__ void gate_store(const gate_f32x16_t (&acc)[NCB], uint16_t* out, int64_t orow, bool live,
                                            int DC, int c0, int nc, int h) {
-  if (orow >= n) return;
+  if (!live) return;
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb)
     if (32 * cb < nc) {
@@ -82,12 +83,23 @@ __device__ __forceinline__ void gate_store(const gate_f32x16_t (&acc)[NCB], uint
     }
 }
 
-template <int EP, int NCB, bool ONE_PASS>
+// TABLE: `ids` is the list of distinct ids that gate_claim_kernel built, its
+// length counts[parity] (read on the device; n bounds it), and row i writes
+// out[ids[i]], a [V, d_c] table.  Thread 0 zeroes counts[parity ^ 1], the
+// slot of the next call.
+template <int EP, int NCB, bool ONE_PASS, bool TABLE = false>
 __global__ __launch_bounds__(64 * kGateWaves, 1) void gate_rows_mfma_kernel(const int32_t* __restrict__ ids,
                                                                             const uint16_t* __restrict__ emb,
                                                                             const uint16_t* __restrict__ w_ue,
                                                                             uint16_t* __restrict__ out, int64_t n,
-                                                                            int E, int DC, int V, int S) {
+                                                                            int E, int DC, int V, int S,
+                                                                            unsigned int* __restrict__ counts,
+                                                                            unsigned int parity) {
+  if constexpr (TABLE) {
+    n = min(n, static_cast<int64_t>(counts[parity]));
+    if (blockIdx.x == 0 && threadIdx.x == 0) counts[parity ^ 1u] = 0u;
+  }
+  if (n <= 0) return;  // uniform over the work-group
   constexpr int CB = 32 * NCB;
   constexpr int NC = EP / 16;  // 16-component chunks per pass
   extern __shared__ __attribute__((aligned(16))) uint16_t wl[];  // [CB][E + 8]
@@ -140,13 +152,14 @@ __global__ __launch_bounds__(64 * kGateWaves, 1) void gate_rows_mfma_kernel(cons
       __builtin_amdgcn_sched_barrier(0);
       gate_products<NH, NCB>(bA, arow, RS, 0, acc);
       gate_products<NH, NCB>(bB, arow, RS, 16 * NH, acc);
-      gate_store<NCB>(acc, out, rb * 32 + i32, n, DC, c0, nc, h);
+      gate_store<NCB>(acc, out, TABLE ? id_next : rb * 32 + i32, rb * 32 + i32 < n, DC, c0, nc, h);
       id_next = id_after;
     }
   } else {
   // e above one pass: each block takes E / EP passes, every load of a pass in flight at once
   for (; rb < nrb; rb += step) {
-    const uint16_t* erow = erow_of(row_id(rb));
+    const int id = row_id(rb);
+    const uint16_t* erow = erow_of(id);
     gate_f32x16_t acc[NCB];
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb)
@@ -161,12 +174,53 @@ __global__ __launch_bounds__(64 * kGateWaves, 1) void gate_rows_mfma_kernel(cons
       gate_products<NH, NCB>(bA, arow, RS, p0, acc);
       gate_products<NH, NCB>(bB, arow, RS, p0 + 16 * NH, acc);
     }
-    gate_store<NCB>(acc, out, rb * 32 + i32, n, DC, c0, nc, h);
+    gate_store<NCB>(acc, out, TABLE ? id : rb * 32 + i32, rb * 32 + i32 < n, DC, c0, nc, h);
   }
   }
 }
 
-template <bool BF16>
+// Stamp slots one 128-byte line apart, so that claims of different ids do
+// not queue on one line.
+constexpr int kMarkStride = 32;
+constexpr int kClaimThreads = 1024;
+
+// Distinct ids of a list (pass 1 of eg_mla_gate_table): row i claims its id
+// with an atomic exchange of `stamp` into marks[id kMarkStride]; a row that
+// finds another value appends the id to `list`.  The work-group gathers its
+// winners in LDS and reserves their places with one atomic add (the
+// counter is one address: an add per wave queued ~2000 of them there).
+// counts[stamp % 2] counts the list and must be zero on entry; the pass over
+// the list zeroes the other slot for the next call.
+__global__ __launch_bounds__(kClaimThreads) void gate_claim_kernel(const int32_t* __restrict__ ids, int64_t n, int V,
+                                                                   unsigned int* __restrict__ marks,
+                                                                   unsigned int stamp, int32_t* __restrict__ list) {
+  __shared__ unsigned int wave_n[kClaimThreads / 64];
+  __shared__ unsigned int wg_base;
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * kClaimThreads + threadIdx.x;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int id = 0;
+  bool win = false;
+  if (i < n) {
+    id = clamp_id(ids[i], V);
+    win = atomicExch(marks + static_cast<int64_t>(id) * kMarkStride, stamp) != stamp;
+  }
+  const uint64_t mask = __builtin_amdgcn_ballot_w64(win);
+  if (lane == 0) wave_n[w] = static_cast<unsigned int>(__builtin_popcountll(mask));
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    unsigned int tot = 0;
+    for (int k = 0; k < kClaimThreads / 64; ++k) tot += wave_n[k];
+    wg_base = tot > 0 ? atomicAdd(marks + static_cast<int64_t>(V) * kMarkStride + (stamp & 1u), tot) : 0u;
+  }
+  __syncthreads();
+  unsigned int before = wg_base;
+  for (int k = 0; k < w; ++k) before += wave_n[k];
+  const unsigned int pos = before + static_cast<unsigned int>(__builtin_popcountll(mask & ((uint64_t{1} << lane) - 1)));
+  if (win && pos < static_cast<unsigned int>(V)) list[pos] = id;  // a counter left nonzero cannot overrun
+}
+
+// TABLE: row i writes out[ids[i]] (rows with the same id write the same bits)
+template <bool BF16, bool TABLE = false>
 __global__ __launch_bounds__(kGateThreads) void gate_rows_valu_kernel(const int32_t* __restrict__ ids,
                                                                        const void* __restrict__ emb,
                                                                        const void* __restrict__ w_ue,
@@ -180,46 +234,83 @@ __global__ __launch_bounds__(kGateThreads) void gate_rows_valu_kernel(const int3
   if (c >= DC) return;
   float acc = 0.f;
   for (int k = 0; k < E; ++k) acc = fmaf(ld<BF16>(w_ue, static_cast<int64_t>(c) * E + k), erow[k], acc);
-  st<BF16>(out, i * DC + c, acc);
+  st<BF16>(out, (TABLE ? static_cast<int64_t>(id) : i) * DC + c, acc);
 }
 
 }  // namespace egmla
 
 using namespace egmla;
 
-extern "C" eg_mla_status eg_mla_gate_rows(const eg_mla_dims* dims, int32_t emb_dim, int32_t emb_vocab, int64_t n,
-                                          const int32_t* ids, const void* emb, const void* w_ue, void* out,
-                                          void* stream_) {
-  eg_mla_status st = validate_gate_rows(dims, emb_dim, emb_vocab, n, ids, emb, w_ue, out);
-  if (st != EG_MLA_OK || n == 0) return st;
+namespace {
+
+// Column slices and LDS of the MFMA kernel for this shape (0 slices: the VALU
+// kernel runs).
+struct GateShape {
+  int ncb = 0, S = 0, ep = 0;
+  bool one = false;
+  size_t lds = 0;
+};
+
+GateShape gate_shape(const eg_mla_dims& d, int E) {
+  GateShape g;
+  const int DC = d.latent_dim;
+  // slice width: as many 32-column blocks (up to 4) as d_c needs and the LDS holds
+  int ncb = DC >= 96 ? 4 : (DC >= 64 ? 2 : 1);
+  while (ncb > 1 && static_cast<int64_t>(32 * ncb) * (E + 8) * 2 > kGateLdsBudget) ncb /= 2;
+  if (!(d.dtype == EG_MLA_BF16 && E % 128 == 0 && DC % 32 == 0 &&
+        static_cast<int64_t>(32 * ncb) * (E + 8) * 2 <= kGateLdsBudget))
+    return g;
+  g.S = (DC + 32 * ncb - 1) / (32 * ncb);
+  // one pass when the whole embedding row fits the registers (e <= 512),
+  // else passes of 256 (or 128) components
+  g.one = E <= 512;
+  g.ep = g.one ? E : (E % 256 == 0 ? 256 : 128);
+  if (g.one && ncb == 1) ncb = 2;  // d_c 32: a padded 64-column slice (fits: e <= 512)
+  g.ncb = ncb;
+  g.lds = static_cast<size_t>(32 * ncb) * (E + 8) * 2;
+  return g;
+}
+
+eg_mla_status launch_gate(const eg_mla_dims* dims, int32_t emb_dim, int32_t emb_vocab, int64_t n, const int32_t* ids,
+                          const void* emb, const void* w_ue, void* out, bool table, unsigned int* marks,
+                          unsigned int stamp, void* stream_) {
   hipStream_t stream = static_cast<hipStream_t>(stream_);
   (void)hipGetLastError();
   const int E = emb_dim, DC = dims->latent_dim;
   const bool bf = dims->dtype == EG_MLA_BF16;
-  // slice width: as many 32-column blocks (up to 4) as d_c needs and the LDS holds
-  int ncb = DC >= 96 ? 4 : (DC >= 64 ? 2 : 1);
-  while (ncb > 1 && static_cast<int64_t>(32 * ncb) * (E + 8) * 2 > kGateLdsBudget) ncb /= 2;
-  const bool mfma = bf && E % 128 == 0 && DC % 32 == 0 && static_cast<int64_t>(32 * ncb) * (E + 8) * 2 <= kGateLdsBudget &&
-                    reinterpret_cast<uintptr_t>(emb) % 16 == 0 && reinterpret_cast<uintptr_t>(w_ue) % 16 == 0 &&
-                    reinterpret_cast<uintptr_t>(out) % 8 == 0;
+  const GateShape gs = gate_shape(*dims, E);
+  const bool mfma = gs.S > 0 && reinterpret_cast<uintptr_t>(emb) % 16 == 0 &&
+                    reinterpret_cast<uintptr_t>(w_ue) % 16 == 0 && reinterpret_cast<uintptr_t>(out) % 8 == 0;
+  unsigned int* counts = nullptr;
+  if (mfma && table) {
+    // pass 1: the distinct ids into a list (marks: [V] stamp lines, [2] counts, [V] list)
+    if (n > (int64_t{1} << 40)) return EG_MLA_ERR_UNSUPPORTED;
+    unsigned int* cnt = marks + static_cast<int64_t>(emb_vocab) * kMarkStride;
+    int32_t* list = reinterpret_cast<int32_t*>(cnt + 2);
+    hipLaunchKernelGGL(gate_claim_kernel, dim3(static_cast<unsigned>((n + kClaimThreads - 1) / kClaimThreads)),
+                       dim3(kClaimThreads), 0, stream, ids, n, emb_vocab, marks, stamp, list);
+    counts = cnt;
+    ids = list;
+    n = std::min<int64_t>(n, emb_vocab);  // the list holds distinct ids only
+  }
   if (mfma) {
-    const int S = (DC + 32 * ncb - 1) / (32 * ncb);
+    const int S = gs.S, ncb = gs.ncb, ep = gs.ep;
+    const bool one = gs.one;
     const int64_t nrb = (n + 31) / 32;
     // one work-group per compute unit: 8 XCDs x k teams x S slices, with no
     // more teams than give each of a work-group's waves a row block
     const int per_xcd = std::max(1, device_cus() / 8 / S);
+    // (the distinct-id pass too: 2 or 4 blocks per wave measured slower, each
+    // work-group staging its W^UE slice first)
     const int64_t want = (nrb + kGateWaves - 1) / kGateWaves;
     const int k = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(per_xcd, (want + 7) / 8)));
     const int grid = 8 * k * S;
-    // one pass when the whole embedding row fits the registers (e <= 512),
-    // else passes of 256 (or 128) components
-    const bool one = E <= 512;
-    const int ep = one ? E : (E % 256 == 0 ? 256 : 128);
-    if (one && ncb == 1) ncb = 2;  // d_c 32: a padded 64-column slice (fits: e <= 512)
-    const size_t lds = static_cast<size_t>(32 * ncb) * (E + 8) * 2;
+    const size_t lds = gs.lds;
     const void* fn = nullptr;
-#define EGMLA_GATE_CASE(EPV, NCBV, ONE)                                                  \
-    if (ep == EPV && ncb == NCBV && one == ONE) fn = reinterpret_cast<const void*>(gate_rows_mfma_kernel<EPV, NCBV, ONE>);
+#define EGMLA_GATE_CASE(EPV, NCBV, ONE)                                                                    \
+    if (ep == EPV && ncb == NCBV && one == ONE)                                                           \
+      fn = table ? reinterpret_cast<const void*>(gate_rows_mfma_kernel<EPV, NCBV, ONE, true>)              \
+                 : reinterpret_cast<const void*>(gate_rows_mfma_kernel<EPV, NCBV, ONE, false>);
     EGMLA_GATE_CASE(512, 4, true) EGMLA_GATE_CASE(512, 2, true)
     EGMLA_GATE_CASE(384, 4, true) EGMLA_GATE_CASE(384, 2, true)
     EGMLA_GATE_CASE(256, 4, true) EGMLA_GATE_CASE(256, 2, true)
@@ -235,30 +326,60 @@ extern "C" eg_mla_status eg_mla_gate_rows(const eg_mla_dims* dims, int32_t emb_d
     const uint16_t* emb_c = static_cast<const uint16_t*>(emb);
     const uint16_t* w_c = static_cast<const uint16_t*>(w_ue);
     uint16_t* out_c = static_cast<uint16_t*>(out);
-    int V = emb_vocab;
-    void* args[] = {&ids_c, &emb_c, &w_c, &out_c, &n, const_cast<int*>(&E), const_cast<int*>(&DC), &V,
-                    const_cast<int*>(&S)};
+    int V = emb_vocab, Ev = E, DCv = DC, Sv = S;
+    unsigned int* counts_c = counts;
+    unsigned int parity = stamp & 1u;
+    void* args[] = {&ids_c, &emb_c, &w_c, &out_c, &n, &Ev, &DCv, &V, &Sv, &counts_c, &parity};
     if (hipLaunchKernel(fn, dim3(grid), dim3(64 * kGateWaves), args, lds, stream) != hipSuccess)
       return EG_MLA_ERR_HIP;
   } else {
     if (n > 0x7fffffff) return EG_MLA_ERR_UNSUPPORTED;
     const size_t lds = static_cast<size_t>(E) * sizeof(float);
     dim3 grid(static_cast<unsigned>(n), (DC + kGateThreads - 1) / kGateThreads);
-    if (bf) {
-      if (lds > 65536 && hipFuncSetAttribute(reinterpret_cast<const void*>(gate_rows_valu_kernel<true>),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize,
-                                             static_cast<int>(lds)) != hipSuccess)
-        return EG_MLA_ERR_HIP;
-      hipLaunchKernelGGL(gate_rows_valu_kernel<true>, grid, dim3(kGateThreads), lds, stream, ids, emb, w_ue, out,
-                         E, DC, emb_vocab);
-    } else {
-      if (lds > 65536 && hipFuncSetAttribute(reinterpret_cast<const void*>(gate_rows_valu_kernel<false>),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize,
-                                             static_cast<int>(lds)) != hipSuccess)
-        return EG_MLA_ERR_HIP;
-      hipLaunchKernelGGL(gate_rows_valu_kernel<false>, grid, dim3(kGateThreads), lds, stream, ids, emb, w_ue, out,
-                         E, DC, emb_vocab);
-    }
+    const void* fn = bf ? (table ? reinterpret_cast<const void*>(gate_rows_valu_kernel<true, true>)
+                                 : reinterpret_cast<const void*>(gate_rows_valu_kernel<true, false>))
+                        : (table ? reinterpret_cast<const void*>(gate_rows_valu_kernel<false, true>)
+                                 : reinterpret_cast<const void*>(gate_rows_valu_kernel<false, false>));
+    if (lds > 65536 &&
+        hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)) != hipSuccess)
+      return EG_MLA_ERR_HIP;
+    int Ev = E, DCv = DC, V = emb_vocab;
+    const int32_t* ids_c = ids;
+    const void* emb_c = emb;
+    const void* w_c = w_ue;
+    void* out_c = out;
+    void* args[] = {&ids_c, &emb_c, &w_c, &out_c, &Ev, &DCv, &V};
+    if (hipLaunchKernel(fn, grid, dim3(kGateThreads), args, lds, stream) != hipSuccess) return EG_MLA_ERR_HIP;
   }
   return hipGetLastError() == hipSuccess ? EG_MLA_OK : EG_MLA_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" eg_mla_status eg_mla_gate_rows(const eg_mla_dims* dims, int32_t emb_dim, int32_t emb_vocab, int64_t n,
+                                          const int32_t* ids, const void* emb, const void* w_ue, void* out,
+                                          void* stream) {
+  eg_mla_status st = validate_gate_rows(dims, emb_dim, emb_vocab, n, ids, emb, w_ue, out);
+  if (st != EG_MLA_OK || n == 0) return st;
+  return launch_gate(dims, emb_dim, emb_vocab, n, ids, emb, w_ue, out, false, nullptr, 0u, stream);
+}
+
+extern "C" size_t eg_mla_gate_table_marks_size(const eg_mla_dims* dims, int32_t emb_dim, int32_t emb_vocab) {
+  if (validate_gate_rows(dims, emb_dim, emb_vocab, 0, nullptr, nullptr, nullptr, nullptr) != EG_MLA_OK) return 0;
+  // a stamp line per id, two counts, the id list
+  return ((kMarkStride + 1) * static_cast<size_t>(emb_vocab) + 2) * sizeof(unsigned int);
+}
+
+extern "C" eg_mla_status eg_mla_gate_table(const eg_mla_dims* dims, int32_t emb_dim, int32_t emb_vocab, int64_t n,
+                                           const int32_t* ids, const void* emb, const void* w_ue, void* table,
+                                           void* marks, size_t marks_bytes, uint32_t stamp, void* stream) {
+  eg_mla_status st = validate_gate_rows(dims, emb_dim, emb_vocab, n, ids, emb, w_ue, table);
+  if (st != EG_MLA_OK) return st;
+  if (stamp == 0) return EG_MLA_ERR_INVALID_ARG;
+  if (n == 0) return EG_MLA_OK;
+  if (!marks || reinterpret_cast<uintptr_t>(marks) % 4 != 0 ||
+      marks_bytes < eg_mla_gate_table_marks_size(dims, emb_dim, emb_vocab))
+    return EG_MLA_ERR_WORKSPACE;
+  return launch_gate(dims, emb_dim, emb_vocab, n, ids, emb, w_ue, table, true, static_cast<unsigned int*>(marks),
+                     stamp, stream);
 }

@@ -207,6 +207,29 @@ def test_gate_rows_rejects_before_launch(L):
     assert L.eg_mla_gate_rows(ctypes.byref(bad), 512, 1000, 5, vp, vp, vp, vp, None) == B.ERR_UNSUPPORTED
 
 
+def test_gate_table_sizes_and_rejections(L):
+    # marks: a stamp line (128 bytes) per id, two list counters, a list of up to V ids
+    d = dims()
+    assert L.eg_mla_gate_table_marks_size(ctypes.byref(d), 512, 1000) == (33 * 1000 + 2) * 4  # stamp lines, counts, list
+    d512 = dims(latent_dim=512, gate_dim=512)
+    assert L.eg_mla_gate_table_marks_size(ctypes.byref(d512), 512, 1000) == (33 * 1000 + 2) * 4
+    assert L.eg_mla_gate_table_marks_size(ctypes.byref(d), 0, 1000) == 0
+    assert L.eg_mla_gate_table_marks_size(ctypes.byref(d), 512, 0) == 0
+    vp = ctypes.c_void_p(256)
+    mk = ctypes.c_void_p(4096)
+    need = (33 * 1000 + 2) * 4
+    call = L.eg_mla_gate_table
+    assert call(ctypes.byref(d), 512, 1000, 0, None, None, None, None, None, 0, 1, None) == B.OK  # no-op
+    assert call(ctypes.byref(d), 512, 1000, 5, vp, vp, vp, vp, mk, need, 0, None) == B.ERR_INVALID_ARG  # stamp 0
+    assert call(ctypes.byref(d), 512, 1000, 5, None, vp, vp, vp, mk, need, 1, None) == B.ERR_INVALID_ARG
+    assert call(ctypes.byref(d), 512, 1000, 5, vp, vp, vp, None, mk, need, 1, None) == B.ERR_INVALID_ARG
+    assert call(ctypes.byref(d), 512, 1000, 5, vp, vp, vp, vp, None, need, 1, None) == B.ERR_WORKSPACE
+    assert call(ctypes.byref(d), 512, 1000, 5, vp, vp, vp, vp, mk, need - 4, 1, None) == B.ERR_WORKSPACE
+    assert call(ctypes.byref(d), 512, 1000, 5, vp, vp, vp, vp, ctypes.c_void_p(4098), need, 1, None) == \
+        B.ERR_WORKSPACE
+    assert call(ctypes.byref(d), 20000, 1000, 5, vp, vp, vp, vp, mk, need, 1, None) == B.ERR_UNSUPPORTED
+
+
 def test_prefill_varlen_rejects_before_launch(L):
     d = dims()
     vp = ctypes.c_void_p(256)

@@ -131,3 +131,74 @@ def test_unfolded_step_decode(gpu, wl):
                      rope_dim=wl.rope_dim, storage="f64", page_table=inp.page_table, page_size=wl.page_size,
                      max_pages=inp.max_pages)
     assert_close(B.out_to_f64(dd.out), ref, "bf16", f"unfolded {wl.name}")
+
+
+def gpu_gate_table(wl, ge, ids, table, marks, stamp):
+    """eg_mla_gate_table into `table` (device [emb_vocab, d_c]) with the given marks and stamp."""
+    import torch
+    ids_d = B.to_device_tensor(np.ascontiguousarray(ids, dtype=np.int32), "int")
+    B.gate_table(B.dims_for(wl), ids_d, B.to_device_tensor(ge.emb, wl.dtype), B.to_device_tensor(ge.w_ue, wl.dtype),
+                 table, marks, stamp)
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("latent_dim,emb_dim,n,vocab", [
+    (128, 512, 5000, 700),     # MFMA claims: about 7 rows per id
+    (512, 512, 3001, 900),     # four column slices, each claiming its ids
+    (128, 256, 65, 64),        # a ragged last block
+    (32, 128, 300, 40),        # d_c 32: a padded 64-column slice
+    (128, 1024, 300, 200),     # passes of 256 components: every row stores
+    (144, 40, 90, 50),         # VALU: every row stores
+])
+def test_gate_table_rows(gpu, latent_dim, emb_dim, n, vocab):
+    # table[id] = W^UE Emb[id] for the distinct ids of a list: the same bits
+    # as eg_mla_gate_rows, within the oracle's bound, other rows untouched;
+    # then a second call with another stamp and another list
+    import torch
+    wl = W.WORKLOADS[1].replace(latent_dim=latent_dim, gate_dim=latent_dim, vocab=vocab, seed=55)
+    ge = W.generate_gate_embedding(wl, emb_dim)
+    dims = B.dims_for(wl)
+    rng = np.random.default_rng(8)
+    ids1 = rng.integers(-3, vocab // 2 + 3, size=n).astype(np.int32)   # out of range: clamped
+    ids2 = rng.integers(vocab // 3, vocab, size=n).astype(np.int32)
+    sentinel = 0x7bcd
+    table = torch.full((vocab, latent_dim), sentinel, dtype=torch.int16, device="cuda").view(torch.bfloat16)
+    mbytes = B.gate_table_marks_size(dims, emb_dim, vocab)
+    assert mbytes > 0
+    marks = torch.zeros((mbytes + 3) // 4, dtype=torch.int32, device="cuda")
+    written = np.zeros(vocab, dtype=bool)
+    for stamp, ids in ((1, ids1), (2, ids2)):
+        say(f"gate table d_c={latent_dim} e={emb_dim} n={n} vocab={vocab} stamp={stamp}")
+        gpu_gate_table(wl, ge, ids, table, marks, stamp)
+        rows = gpu_gate_rows(wl, ge, ids)
+        got = table.view(torch.int16).cpu().numpy()
+        cid = np.clip(ids, 0, vocab - 1)
+        assert np.array_equal(got[cid], rows.view(torch.int16).cpu().numpy()), "table rows differ from gate rows"
+        written[cid] = True
+        assert np.all(got[~written] == sentinel), "a row outside the lists was written"
+    distinct = np.flatnonzero(written).astype(np.int32)
+    check_rows(B.out_to_f64(table[torch.from_numpy(distinct).long().cuda()]), ge, distinct, "bf16")
+
+
+def test_unfolded_step_through_table(gpu):
+    # the unfolded step with each distinct id computed once: the decode takes
+    # the table with the step's own token ids
+    import torch
+    wl = W.WORKLOADS[1].replace(batch=3, seq_len=900, vocab=2000, seed=56)
+    inp = W.generate(wl)
+    ge = W.generate_gate_embedding(wl, 512)
+    dims = B.dims_for(wl)
+    table = torch.zeros((wl.vocab, wl.latent_dim), dtype=torch.bfloat16, device="cuda")
+    marks = torch.zeros((B.gate_table_marks_size(dims, 512, wl.vocab) + 3) // 4, dtype=torch.int32, device="cuda")
+    say(f"unfolded step through the table {wl.name}: {inp.num_rows} rows, then decode")
+    gpu_gate_table(wl, ge, inp.token_ids, table, marks, 1)
+    dd = B.stage_decode(inp)
+    dd.gate = table
+    B.run_decode(dd)
+    torch.cuda.synchronize()
+    Gref = orc.gate_rows(ge.emb, ge.w_ue, np.arange(wl.vocab, dtype=np.int32), storage="bf16")
+    ref = orc.decode(orc.widen(inp.q, "bf16"), orc.widen(inp.latent_cache, "bf16"), inp.token_ids, Gref,
+                     orc.widen(inp.w_uk, "bf16"), orc.widen(inp.w_uv, "bf16"), inp.seq_lens,
+                     latent_dim=wl.latent_dim, head_dim=wl.head_dim, rope_dim=wl.rope_dim, storage="f64",
+                     page_table=inp.page_table, page_size=wl.page_size, max_pages=inp.max_pages)
+    assert_close(B.out_to_f64(dd.out), ref, "bf16", "unfolded step through the table")
