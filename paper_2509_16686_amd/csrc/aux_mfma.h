@@ -155,8 +155,9 @@ __global__ __launch_bounds__(256) void absorb_mfma_kernel(const uint16_t* __rest
 }
 
 // ---------------------------------------------------------------------------
-// Combine on MFMA: grid (H, ceil(B / 16)), 1024 threads (16 waves), one head
-// and up to 16 sequences per work-group.
+// Combine on MFMA: grid (H, ceil(B / spw)), 1024 threads (16 waves), one head
+// and up to spw <= 16 sequences per work-group (fewer for small batches, so
+// that the grid still spreads over the chip).
 //  1. Waves 0 .. nvt-1 issue the W_UV rows of their 16-row output tile (first
 //     for d_c <= 128; after step 3 for wider latents, to stay in registers).
 //  2. The partials of each sequence (`slices` per context split; a partial
@@ -253,7 +254,7 @@ __global__ __launch_bounds__(kCombWaves * 64) void combine_mfma_kernel(const flo
                                                                        const int32_t* __restrict__ seq_lens,
                                                                        uint16_t* __restrict__ out, int B, int H,
                                                                        int cap, int split, int s_max, int slices,
-                                                                       const int2* __restrict__ seq_rows) {
+                                                                       const int2* __restrict__ seq_rows, int spw) {
   constexpr int OS = DC + 4;
   constexpr int PER = DC / 64;  // latent columns per lane
   constexpr int NKC = DC / 32;
@@ -265,10 +266,10 @@ __global__ __launch_bounds__(kCombWaves * 64) void combine_mfma_kernel(const flo
   float* m_part = o_part + kCombWaves * DC;                         // [kCombWaves]
   float* l_part = m_part + kCombWaves;                              // [kCombWaves]
   const int h = blockIdx.x;
-  const int b0 = blockIdx.y * kCombSeq;
+  const int b0 = blockIdx.y * spw;  // spw <= kCombSeq sequences per work-group
   const int tid = threadIdx.x, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int nseq = min(kCombSeq, B - b0);
+  const int nseq = min(spw, B - b0);
   int np2 = 1;
   while (np2 < nseq) np2 <<= 1;
   const int wps = kCombWaves / np2;  // waves per sequence (power of two)
