@@ -162,6 +162,20 @@ def test_balanced_schedule_dc512(gpu, case):
     assert_close(got, oracle_decode(inp), "bf16", f"balanced {case}")
 
 
+@pytest.mark.parametrize("total", [393310, 395300])
+def test_list_chunk_edges_dc512(gpu, total):
+    # Token ranges just past one token list (3072 tokens) per work-group at
+    # 128 heads (128 ranges on a 256-CU device): the second list of a range
+    # holds a lone unit (393310 tokens: 3072 or 3073 per range) or one to two
+    # units (395300: 3088 or 3089), the ends of the value product's pairs.
+    lens = np.array([total - 5, 5])
+    wl = W.WORKLOADS[4].replace(name=f"chunk_edges_{total}_dc512", batch=2, paged=True, seed=48,
+                                seq_len_range=(1, int(lens.max())))
+    inp = W.generate(wl, seq_lens=lens)
+    say(f"decode dc512 list-chunk edges: {total} tokens over 2 sequences")
+    assert_close(gpu_decode(inp), oracle_decode(inp), "bf16", f"chunk edges {total}")
+
+
 def test_peaked_logits_dc512(gpu):
     # query x 8: logits of standard deviation about 8, so the softmax is sharp
     # and a score error of 2^-9 relative (one bf16 rounding of either operand)
