@@ -29,12 +29,22 @@ constexpr int kAbsMinWorkGroups = 128;
 
 // HALF: instead of fp32 rows [B, H, DC + DR], write 16-bit rows [B, H, DC + DR]
 // = [q_lat in fp16 (one rounding) | q^R in bf16 (copied)], the operands of the
-// wide kernel's fp16 latent product and exact bf16 RoPE product.
+// wide kernel's fp16 latent product and exact bf16 RoPE product; the grid then
+// has one more column of work-groups (blockIdx.x == H), the first of which
+// computes the wide kernel's balanced schedule from the lengths (sa).
 template <int DH, int BLOCKS, int COLS, bool HALF = false>
 __global__ __launch_bounds__(256) void absorb_mfma_kernel(const uint16_t* __restrict__ q,
                                                           const uint16_t* __restrict__ w_uk,
-                                                          float* __restrict__ qfull, int B, int H, int DC, int DR) {
+                                                          float* __restrict__ qfull, int B, int H, int DC, int DR,
+                                                          WideSchedArgs sa) {
   static_assert(BLOCKS >= 1 && BLOCKS <= kAbsBlocks, "row blocks per work-group");
+  if constexpr (HALF) {
+    // the extra column of work-groups: the head-split kernel's schedule
+    if (blockIdx.x == H) {
+      if (blockIdx.y == 0 && blockIdx.z == 0) wide_schedule<256>(sa, B);
+      return;
+    }
+  }
   static_assert(COLS % 16 == 0 && COLS <= 128, "latent columns per work-group");
   constexpr int RS = COLS + 8;  // padded LDS row (bf16 elements)
   constexpr int NK = DH / 32;
@@ -166,17 +176,18 @@ __global__ __launch_bounds__(256) void absorb_mfma_kernel(const uint16_t* __rest
 //     wps = 16 / pow2ceil(n) waves, and wave p of a sequence merges its
 //     partials p, p + wps, ... in batches of 4, 8 or 16 (at most 8 for
 //     d_c > 128) (maxima, sums and partial outputs loaded together) into LDS.
-//     NORM (the head-split kernel's partials): each partial output is an fp16
-//     row already divided by its sum l, and enters with weight e * l.
-//  3. All threads merge each sequence's wps parts into its latent row o / l.
+//  3. All threads merge each sequence's wps parts into its latent row o / l,
+//     split once into bf16 hi + lo in LDS.
 //  4. out^T[v][b] = W_UV[h][v][:] . o[b][:] on v_mfma_f32_16x16x32_bf16, the
-//     16 sequences being the 16 columns of the B operand, o split into bf16
-//     hi + lo (two products) so the up-projection adds only W_UV's own
-//     rounding.
+//     16 sequences being the 16 columns of the B operand, a product each for
+//     hi and lo, so the up-projection adds only W_UV's own rounding.
 // ---------------------------------------------------------------------------
 constexpr int kCombSeq = 16;
 constexpr int kCombWaves = 16;
-constexpr size_t combine_lds_bytes(int DC) { return sizeof(float) * (kCombSeq * (DC + 4) + kCombWaves * DC + 2 * kCombWaves); }
+// merged rows as bf16 hi + lo ([2][kCombSeq][DC + 8]), then the waves' partial merges and their (m, l)
+constexpr size_t combine_lds_bytes(int DC) {
+  return 2 * sizeof(uint16_t) * kCombSeq * (DC + 8) + sizeof(float) * (kCombWaves * DC + 2 * kCombWaves);
+}
 
 // Latent dim held in accumulator j of a combine lane: with an even number of
 // dims per lane, lane l holds the adjacent pairs 128 i + 2 l + {0, 1} (8-byte
@@ -190,30 +201,19 @@ __device__ __forceinline__ int comb_dim(int lane, int j) {
 
 // One batch of SB splits of the online merge: the splits first + stride * t
 // for t = s0 .. s0 + SB - 1 (t clamped to ns - 1, counted while t < ns).
-// Their maxima, sums and partial outputs load together.  NORM: the partial
-// outputs are fp16 rows already divided by their sums (weight e * l).
-template <int DC, int SB, bool NORM = false>
-__device__ __forceinline__ void merge_batch(const float* __restrict__ part_ml, const void* __restrict__ part_ov,
+// Their maxima, sums and partial outputs load together.
+template <int DC, int SB>
+__device__ __forceinline__ void merge_batch(const float* __restrict__ part_ml, const float* __restrict__ part_o,
                                             int64_t base, int H, int first, int stride, int s0, int ns, int lane,
                                             float& M, float& Ls, float (&acc)[DC / 64]) {
   constexpr int PER = DC / 64;
-  const float* __restrict__ part_o = static_cast<const float*>(part_ov);
-  const uint16_t* __restrict__ part_h = static_cast<const uint16_t*>(part_ov);
   float pv[SB][PER];
   float2 ml[SB];
 #pragma unroll
   for (int u = 0; u < SB; ++u) {
     const int64_t row = base + static_cast<int64_t>(first + stride * min(s0 + u, ns - 1)) * H;
     ml[u] = *reinterpret_cast<const float2*>(part_ml + row * 2);
-    if constexpr (NORM) {
-      static_assert(PER % 2 == 0, "fp16 partial rows: adjacent pairs per lane");
-#pragma unroll
-      for (int i = 0; i < PER / 2; ++i) {
-        const uint32_t v = *reinterpret_cast<const uint32_t*>(part_h + row * DC + 128 * i + 2 * lane);
-        pv[u][2 * i] = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(v & 0xffffu)));
-        pv[u][2 * i + 1] = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(v >> 16)));
-      }
-    } else if constexpr (PER % 2 == 0) {
+    if constexpr (PER % 2 == 0) {
 #pragma unroll
       for (int i = 0; i < PER / 2; ++i) {
         const float2 v = *reinterpret_cast<const float2*>(part_o + row * DC + 128 * i + 2 * lane);
@@ -240,29 +240,28 @@ __device__ __forceinline__ void merge_batch(const float* __restrict__ part_ml, c
   for (int u = 0; u < SB; ++u) {
     const float e = s0 + u < ns && live ? __builtin_amdgcn_exp2f(ml[u].x - Mn) : 0.f;
     Ls += ml[u].y * e;
-    const float wgt = NORM ? e * ml[u].y : e;
 #pragma unroll
-    for (int j = 0; j < PER; ++j) acc[j] = fmaf(wgt, pv[u][j], acc[j]);
+    for (int j = 0; j < PER; ++j) acc[j] = fmaf(e, pv[u][j], acc[j]);
   }
   M = Mn;
 }
 
-template <int DC, int DV, bool NORM = false>
+template <int DC, int DV>
 __global__ __launch_bounds__(kCombWaves * 64) void combine_mfma_kernel(const float* __restrict__ part_ml,
-                                                                       const void* __restrict__ part_o,
+                                                                       const float* __restrict__ part_o,
                                                                        const uint16_t* __restrict__ w_uv,
                                                                        const int32_t* __restrict__ seq_lens,
                                                                        uint16_t* __restrict__ out, int B, int H,
                                                                        int cap, int split, int s_max, int slices,
                                                                        const int2* __restrict__ seq_rows, int spw) {
-  constexpr int OS = DC + 4;
+  constexpr int OS = DC + 8;     // bf16 elements per merged row in LDS
   constexpr int PER = DC / 64;  // latent columns per lane
   constexpr int NKC = DC / 32;
   constexpr int nvt = (DV + 15) / 16;
   static_assert(nvt <= kCombWaves, "one output tile per wave");
   extern __shared__ __attribute__((aligned(16))) float comb_lds[];  // combine_lds_bytes(DC) bytes
-  float* o_s = comb_lds;                                            // [kCombSeq][OS]: merged rows (B operand)
-  float* o_part = o_s + kCombSeq * OS;                              // [kCombWaves][DC]: each wave's partial merge
+  uint16_t* o_s = reinterpret_cast<uint16_t*>(comb_lds);           // [2][kCombSeq][OS]: merged rows, hi then lo
+  float* o_part = comb_lds + kCombSeq * OS;                         // [kCombWaves][DC]: each wave's partial merge
   float* m_part = o_part + kCombWaves * DC;                         // [kCombWaves]
   float* l_part = m_part + kCombWaves;                              // [kCombWaves]
   const int h = blockIdx.x;
@@ -308,12 +307,12 @@ __global__ __launch_bounds__(kCombWaves * 64) void combine_mfma_kernel(const flo
     const int64_t row0 = seq_rows ? seq_rows[b].x : static_cast<int64_t>(b) * s_max * slices;
     const int64_t base = row0 * H + h;  // + partial * H
     if (ns <= 4) {
-      merge_batch<DC, 4, NORM>(part_ml, part_o, base, H, part, wps, 0, ns, lane, M, Ls, acc);
+      merge_batch<DC, 4>(part_ml, part_o, base, H, part, wps, 0, ns, lane, M, Ls, acc);
     } else if (ns <= 8) {
-      merge_batch<DC, 8, NORM>(part_ml, part_o, base, H, part, wps, 0, ns, lane, M, Ls, acc);
+      merge_batch<DC, 8>(part_ml, part_o, base, H, part, wps, 0, ns, lane, M, Ls, acc);
     } else {
       for (int s0 = 0; s0 < ns; s0 += kSBMax)
-        merge_batch<DC, kSBMax, NORM>(part_ml, part_o, base, H, part, wps, s0, ns, lane, M, Ls, acc);
+        merge_batch<DC, kSBMax>(part_ml, part_o, base, H, part, wps, s0, ns, lane, M, Ls, acc);
     }
   }
 #pragma unroll
@@ -342,7 +341,9 @@ __global__ __launch_bounds__(kCombWaves * 64) void combine_mfma_kernel(const flo
         v = num / den;
       }
     }
-    o_s[kk * OS + c] = v;
+    const __bf16 hi = static_cast<__bf16>(v);
+    o_s[kk * OS + c] = __builtin_bit_cast(uint16_t, hi);
+    o_s[(kCombSeq + kk) * OS + c] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v - static_cast<float>(hi)));
   }
   __syncthreads();
 
@@ -352,16 +353,9 @@ __global__ __launch_bounds__(kCombWaves * 64) void combine_mfma_kernel(const flo
     f32x4_t o = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kc = 0; kc < NKC; ++kc) {
-      const float* orow = o_s + r16 * OS + kc * 32 + g * 8;
-      const float4 x0 = *reinterpret_cast<const float4*>(orow);
-      const float4 x1 = *reinterpret_cast<const float4*>(orow + 4);
-      const float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
-      bf16x8_t hi, lo;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        hi[e] = static_cast<__bf16>(x[e]);
-        lo[e] = static_cast<__bf16>(x[e] - static_cast<float>(hi[e]));
-      }
+      const int row = r16 * OS + kc * 32 + g * 8;
+      const bf16x8_t hi = *reinterpret_cast<const bf16x8_t*>(o_s + row);
+      const bf16x8_t lo = *reinterpret_cast<const bf16x8_t*>(o_s + kCombSeq * OS + row);
       const bf16x8_t av = __builtin_bit_cast(bf16x8_t, wa[kc]);
       o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, hi, o, 0, 0, 0);
       o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, lo, o, 0, 0, 0);
@@ -378,6 +372,159 @@ __global__ __launch_bounds__(kCombWaves * 64) void combine_mfma_kernel(const flo
 }
 
 // ---------------------------------------------------------------------------
+// Merge of the head-split kernel's partial rows (d_c 512, d_v 128): grid
+// (H, ceil(B / 32)), 512 threads (8 waves), one head and up to 32 sequences
+// per work-group.  Each partial row is O / l in fp16 with (m, l) in fp32, and
+// seq_rows[b] = (first row, number of rows) lists sequence b's rows.
+//  1. Wave w loads the row lists of sequences w + 8 k (k = 0 .. 3) of the
+//     group, then the first 4 rows of each (lane l: latent dims 8 l .. 8 l + 7,
+//     one 16-byte load per row), then the W_UV rows of output tile w (rows
+//     16 w .. 16 w + 15, all 512 latent columns).  Loads complete in issue
+//     order, so the merge waits for the rows only while W_UV is on its way.
+//  2. Each sequence's rows are merged online in fp32 with weights e l,
+//     e = exp2(m - M) (loads past a sequence's rows re-read its last row and
+//     enter with weight 0; rows past the fourth are loaded as the merge
+//     reaches them).  The merged row o / l goes to LDS split once into bf16
+//     hi + lo (zero for an empty sequence), the B operands of every tile.
+//  3. out^T[v][b] = W_UV[h][v][:] . o[b][:] for tile w and both blocks of 16
+//     sequences on v_mfma_f32_16x16x32_bf16, a product each for hi and lo, so
+//     the up-projection adds only W_UV's own rounding.
+// ---------------------------------------------------------------------------
+constexpr int kCombWideSeq = 32;
+constexpr int kCombWideWaves = 8;
+constexpr int kCombWideOS = 512 + 8;  // LDS row of a merged sequence (bf16 elements; 16-byte rotation per row)
+constexpr size_t combine_wide_lds_bytes() { return 2 * sizeof(uint16_t) * kCombWideSeq * kCombWideOS; }
+
+__global__ __launch_bounds__(kCombWideWaves * 64) void combine_wide_kernel(const float* __restrict__ part_ml,
+                                                                          const uint16_t* __restrict__ part_o,
+                                                                          const uint16_t* __restrict__ w_uv,
+                                                                          const int2* __restrict__ seq_rows,
+                                                                          uint16_t* __restrict__ out, int B, int H) {
+  constexpr int DC = 512, DV = 128, NKC = DC / 32, OS = kCombWideOS;
+  constexpr int SPW = kCombWideSeq / kCombWideWaves;  // sequences per wave
+  static_assert(DV / 16 == kCombWideWaves && SPW % 2 == 0, "one output tile per wave; sequences in pairs");
+  // merged rows o / l as bf16 hi + lo: [2][kCombWideSeq][OS]
+  extern __shared__ __attribute__((aligned(16))) uint16_t cw_lds[];
+  const int h = blockIdx.x;
+  const int b0 = blockIdx.y * kCombWideSeq;
+  const int tid = threadIdx.x, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+  // (1) the row lists of this wave's sequences, then the first 4 rows of
+  // each (lane l: latent dims 8 l .. 8 l + 7), then W_UV rows 16 w + r16
+  // (columns 32 kc + 8 g .. + 7): loads complete in issue order, so the merge
+  // waits for the rows only and W_UV arrives while it runs
+  int2 sr[SPW];
+#pragma unroll
+  for (int k = 0; k < SPW; ++k) {
+    const int b = b0 + w + kCombWideWaves * k;  // uniform over the wave
+    sr[k] = b < B ? seq_rows[b] : make_int2(0, 0);
+  }
+  const int coff = 8 * lane;
+  float2 ml[SPW][4];
+  u32x4_t pv[SPW][4];
+  // rows s0 .. s0 + 3 of sequence k (rows past its list repeat its last row)
+  auto load_rows = [&](int k, int s0, float2 (&m4)[4], u32x4_t (&p4)[4]) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int64_t row = static_cast<int64_t>(sr[k].x + min(s0 + u, sr[k].y - 1)) * H + h;
+      m4[u] = *reinterpret_cast<const float2*>(part_ml + row * 2);
+      p4[u] = *reinterpret_cast<const u32x4_t*>(part_o + row * DC + coff);
+    }
+  };
+#pragma unroll
+  for (int k = 0; k < SPW; ++k)
+    if (sr[k].y > 0) load_rows(k, 0, ml[k], pv[k]);
+  u32x4_t wa[NKC];
+  {
+    const uint16_t* wrow = w_uv + (static_cast<int64_t>(h) * DV + 16 * w + r16) * DC + 8 * g;
+#pragma unroll
+    for (int kc = 0; kc < NKC; ++kc) wa[kc] = *reinterpret_cast<const u32x4_t*>(wrow + 32 * kc);
+  }
+
+  // (2) online merge of each sequence's rows in fp32, weights e l with
+  // e = exp2(m - M) (rows past the list: weight 0), into LDS as o / l
+  auto fold = [&](int n, int s0, const float2 (&m4)[4], const u32x4_t (&p4)[4], float& M, float& Ls,
+                  float (&acc)[8]) {
+    float mb = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) mb = fmaxf(mb, s0 + u < n ? m4[u].x : -INFINITY);
+    const float Mn = fmaxf(M, mb);
+    // nothing is accumulated while every row so far has maximum -inf
+    const bool live = Mn > -INFINITY;
+    const float sc = live ? __builtin_amdgcn_exp2f(M - Mn) : 1.f;  // 0 for the first live batch
+    Ls *= sc;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] *= sc;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float e = s0 + u < n && live ? __builtin_amdgcn_exp2f(m4[u].x - Mn) : 0.f;
+      Ls = fmaf(m4[u].y, e, Ls);
+      const float wgt = e * m4[u].y;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t v = p4[u][j];
+        acc[2 * j] = fmaf(wgt, static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(v & 0xffffu))),
+                          acc[2 * j]);
+        acc[2 * j + 1] =
+            fmaf(wgt, static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(v >> 16))), acc[2 * j + 1]);
+      }
+    }
+    M = Mn;
+  };
+#pragma unroll
+  for (int k = 0; k < SPW; ++k) {
+    const int n = sr[k].y;
+    float M = -INFINITY, Ls = 0.f;
+    float acc[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] = 0.f;
+    if (n > 0) {
+      fold(n, 0, ml[k], pv[k], M, Ls, acc);
+      for (int s0 = 4; s0 < n; s0 += 4) {  // sequences over more than 4 token ranges
+        float2 m4[4];
+        u32x4_t p4[4];
+        load_rows(k, s0, m4, p4);
+        fold(n, s0, m4, p4, M, Ls, acc);
+      }
+    }
+    const float inv = Ls > 0.f ? 1.f / Ls : 0.f;  // a sequence with tokens has Ls >= 1
+    bf16x8_t hi, lo;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float x = acc[e] * inv;
+      hi[e] = static_cast<__bf16>(x);
+      lo[e] = static_cast<__bf16>(x - static_cast<float>(hi[e]));
+    }
+    const int row = (w + kCombWideWaves * k) * OS + coff;
+    *reinterpret_cast<bf16x8_t*>(cw_lds + row) = hi;
+    *reinterpret_cast<bf16x8_t*>(cw_lds + kCombWideSeq * OS + row) = lo;
+  }
+  __syncthreads();
+
+  // (3) out^T[16 w + 4 g + r][b0 + 16 bb + r16]
+#pragma unroll
+  for (int bb = 0; bb < kCombWideSeq / 16; ++bb) {
+    f32x4_t o = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kc = 0; kc < NKC; ++kc) {
+      const int row = (16 * bb + r16) * OS + 32 * kc + 8 * g;
+      const bf16x8_t hi = *reinterpret_cast<const bf16x8_t*>(cw_lds + row);
+      const bf16x8_t lo = *reinterpret_cast<const bf16x8_t*>(cw_lds + kCombWideSeq * OS + row);
+      const bf16x8_t av = __builtin_bit_cast(bf16x8_t, wa[kc]);
+      o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, hi, o, 0, 0, 0);
+      o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, lo, o, 0, 0, 0);
+    }
+    const int b = b0 + 16 * bb + r16;
+    if (b < B) {
+      uint16_t* orow = out + (static_cast<int64_t>(b) * H + h) * DV + 16 * w + 4 * g;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) orow[r] = f32_to_bf16(o[r]);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Merge on MFMA with small work-groups: grid (H, ceil(B / 4)), 256 threads,
 // one head and up to 4 sequences per work-group.  For batches whose partials
 // fit one merge batch per sequence, many small work-groups finish sooner than
@@ -385,21 +532,20 @@ __global__ __launch_bounds__(kCombWaves * 64) void combine_mfma_kernel(const flo
 // per context split) online in fp32 and writes its row o / l to LDS; then
 // out^T[v][b] = W_UV[h][v][:] . o[b][:] on v_mfma_f32_16x16x32_bf16, wave w
 // taking output tiles w, w + 4, ... of 16 rows, the merged rows as the B
-// operand's first 4 columns (bf16 hi + lo).  The W_UV rows are loaded first;
+// operand's first 4 columns (split once into bf16 hi + lo as they go to LDS,
+// a product each).  The W_UV rows are loaded first;
 // `wait(b)` is called by each wave before it loads the partials of its
 // sequence (nothing to wait for in a kernel of its own).
 // ---------------------------------------------------------------------------
 constexpr int kComb4Seq = 4;
-template <int DC>
-constexpr int combine4_lds_bytes() { return kComb4Seq * (DC + 4) * 4; }
 
 template <int DC, int DV, typename Wait>
 __device__ __forceinline__ void combine4_block(const float* __restrict__ part_ml, const float* __restrict__ part_o,
                                                const uint16_t* __restrict__ w_uv,
                                                const int32_t* __restrict__ seq_lens, uint16_t* __restrict__ out,
                                                int B, int H, int cap, int split, int s_max, int slices, int h,
-                                               int b0, float* o_s, Wait wait) {
-  constexpr int OS = DC + 4;
+                                               int b0, uint16_t* o_s, Wait wait) {
+  constexpr int OS = DC + 8;  // bf16 elements: o / l hi in rows 0 .. 3, lo in rows 4 .. 7
   constexpr int PER = DC / 64;
   constexpr int NKC = DC / 32;
   constexpr int nvt = (DV + 15) / 16;
@@ -439,7 +585,13 @@ __device__ __forceinline__ void combine4_block(const float* __restrict__ part_ml
     }
     const float inv = Ls > 0.f ? 1.f / Ls : 0.f;  // a sequence with tokens has Ls >= 1
 #pragma unroll
-    for (int j = 0; j < PER; ++j) o_s[w * OS + comb_dim<DC>(lane, j)] = acc[j] * inv;
+    for (int j = 0; j < PER; ++j) {
+      const float x = acc[j] * inv;
+      const __bf16 hi = static_cast<__bf16>(x);
+      o_s[w * OS + comb_dim<DC>(lane, j)] = __builtin_bit_cast(uint16_t, hi);
+      o_s[(kComb4Seq + w) * OS + comb_dim<DC>(lane, j)] =
+          __builtin_bit_cast(uint16_t, static_cast<__bf16>(x - static_cast<float>(hi)));
+    }
   }
   __syncthreads();
   // (3) out^T[vt*16 + 4g + r][b0 + r16] for this wave's tiles
@@ -450,21 +602,12 @@ __device__ __forceinline__ void combine4_block(const float* __restrict__ part_ml
     f32x4_t o = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kc = 0; kc < NKC; ++kc) {
-      float x[8];
+      u32x4_t hv = {0u, 0u, 0u, 0u}, lv = {0u, 0u, 0u, 0u};
       if (r16 < kComb4Seq) {
-        const float4 x0 = *reinterpret_cast<const float4*>(o_s + r16 * OS + kc * 32 + g * 8);
-        const float4 x1 = *reinterpret_cast<const float4*>(o_s + r16 * OS + kc * 32 + g * 8 + 4);
-        x[0] = x0.x; x[1] = x0.y; x[2] = x0.z; x[3] = x0.w; x[4] = x1.x; x[5] = x1.y; x[6] = x1.z; x[7] = x1.w;
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) x[e] = 0.f;
+        hv = *reinterpret_cast<const u32x4_t*>(o_s + r16 * OS + kc * 32 + g * 8);
+        lv = *reinterpret_cast<const u32x4_t*>(o_s + (kComb4Seq + r16) * OS + kc * 32 + g * 8);
       }
-      bf16x8_t hi, lo;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        hi[e] = static_cast<__bf16>(x[e]);
-        lo[e] = static_cast<__bf16>(x[e] - static_cast<float>(hi[e]));
-      }
+      const bf16x8_t hi = __builtin_bit_cast(bf16x8_t, hv), lo = __builtin_bit_cast(bf16x8_t, lv);
       const bf16x8_t av = __builtin_bit_cast(bf16x8_t, wa[t][kc]);
       o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, hi, o, 0, 0, 0);
       o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, lo, o, 0, 0, 0);
@@ -483,7 +626,7 @@ __global__ __launch_bounds__(256) void combine4_kernel(const float* __restrict__
                                                        const uint16_t* __restrict__ w_uv, const int32_t* __restrict__ seq_lens,
                                                        uint16_t* __restrict__ out, int B, int H, int cap, int split,
                                                        int s_max, int slices) {
-  __shared__ __attribute__((aligned(16))) float o_s[kComb4Seq * (DC + 4)];
+  __shared__ __attribute__((aligned(16))) uint16_t o_s[2 * kComb4Seq * (DC + 8)];
   combine4_block<DC, DV>(part_ml, part_o, w_uv, seq_lens, out, B, H, cap, split, s_max, slices, blockIdx.x,
                          blockIdx.y * kComb4Seq, o_s, [](int) {});
 }

@@ -349,18 +349,18 @@ hipError_t launch_combine_dc(dim3 grid, hipStream_t stream, const float* pm, con
   if constexpr (DC == 512) {
     // the head-split kernel (balanced schedule) writes fp16 rows normalised by their sums
     if (seq_rows) {
-      hipError_t e = set_lds(combine_mfma_kernel<DC, 128, true>, lds);
+      hipError_t e = set_lds(combine_wide_kernel, combine_wide_lds_bytes());
       if (e != hipSuccess) return e;
-      hipLaunchKernelGGL((combine_mfma_kernel<DC, 128, true>), grid, dim3(kCombWaves * 64), lds, stream, pm,
-                         static_cast<const void*>(po), wv, seq_lens, ov, B, H, cap, split, s_max, slices, seq_rows,
-                         spw);
+      hipLaunchKernelGGL(combine_wide_kernel, dim3(H, (B + kCombWideSeq - 1) / kCombWideSeq),
+                         dim3(kCombWideWaves * 64), combine_wide_lds_bytes(), stream, pm,
+                         reinterpret_cast<const uint16_t*>(po), wv, seq_rows, ov, B, H);
       return hipGetLastError();
     }
   }
   hipError_t e = set_lds(combine_mfma_kernel<DC, 128>, lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((combine_mfma_kernel<DC, 128>), grid, dim3(kCombWaves * 64), lds, stream, pm,
-                     static_cast<const void*>(po), wv, seq_lens, ov, B, H, cap, split, s_max, slices, seq_rows, spw);
+  hipLaunchKernelGGL((combine_mfma_kernel<DC, 128>), grid, dim3(kCombWaves * 64), lds, stream, pm, po, wv, seq_lens,
+                     ov, B, H, cap, split, s_max, slices, seq_rows, spw);
   return hipGetLastError();
 }
 
@@ -520,13 +520,13 @@ eg_mla_status run_decode(const eg_mla_dims& d, const DecodePlan& p, int32_t batc
   int2* seq_rows = nullptr;
   if (p.balanced) {
     // 0. balanced schedule of the head-split kernel (token ranges per work-group)
+    // (computed by the absorption launch below)
     sched_hdr = reinterpret_cast<int64_t*>(ws + p.off_sched);
     wg_start = reinterpret_cast<int2*>(ws + p.off_sched + 16);
     seq_rows = reinterpret_cast<int2*>(ws + p.off_sched + 16 + kWideMaxGroups * 8);
-    hipLaunchKernelGGL(wide_schedule_kernel, dim3(1), dim3(kSchedThreads), 0, stream, seq_lens, batch, p.capacity,
-                       wide_groups(p.head_groups), sched_hdr, wg_start, seq_rows);
-    if (hipGetLastError() != hipSuccess) return EG_MLA_ERR_HIP;
   }
+  const WideSchedArgs sched{seq_lens, p.capacity, p.balanced ? wide_groups(p.head_groups) : 0, sched_hdr, wg_start,
+                            seq_rows};
   // 1. absorption (or inside the split kernel)
   if (!p.fused_absorb) {
     dim3 grid(d.num_heads, (d.latent_dim + kAbsorbCols - 1) / kAbsorbCols, (batch + kAbsorbRows - 1) / kAbsorbRows);
@@ -546,18 +546,19 @@ eg_mla_status run_decode(const eg_mla_dims& d, const DecodePlan& p, int32_t batc
       dim3 ga(d.num_heads, row_blocks, (d.latent_dim + cols - 1) / cols);
       const uint16_t* q16 = static_cast<const uint16_t*>(q);
       const uint16_t* wuk16 = static_cast<const uint16_t*>(w_uk);
-      if (p.balanced)  // the wide kernel takes the query as fp16 rows (q^R in bf16)
-        hipLaunchKernelGGL((absorb_mfma_kernel<128, kAbsBlocks, kAbsCols, true>), ga, dim3(256), 0, stream, q16,
-                           wuk16, qfull, batch, d.num_heads, d.latent_dim, d.rope_dim);
+      if (p.balanced)  // the wide kernel takes the query as fp16 rows (q^R in bf16); one more column: its schedule
+        hipLaunchKernelGGL((absorb_mfma_kernel<128, kAbsBlocks, kAbsCols, true>), dim3(ga.x + 1, ga.y, ga.z),
+                           dim3(256), 0, stream, q16, wuk16, qfull, batch, d.num_heads, d.latent_dim, d.rope_dim,
+                           sched);
       else if (grouped)
         hipLaunchKernelGGL((absorb_mfma_kernel<128, kAbsBlocks, kAbsCols>), ga, dim3(256), 0, stream, q16, wuk16,
-                           qfull, batch, d.num_heads, d.latent_dim, d.rope_dim);
+                           qfull, batch, d.num_heads, d.latent_dim, d.rope_dim, sched);
       else if (narrow)
         hipLaunchKernelGGL((absorb_mfma_kernel<128, 1, kAbsColsNarrow>), ga, dim3(256), 0, stream, q16, wuk16, qfull,
-                           batch, d.num_heads, d.latent_dim, d.rope_dim);
+                           batch, d.num_heads, d.latent_dim, d.rope_dim, sched);
       else
         hipLaunchKernelGGL((absorb_mfma_kernel<128, 1, kAbsCols>), ga, dim3(256), 0, stream, q16, wuk16, qfull, batch,
-                           d.num_heads, d.latent_dim, d.rope_dim);
+                           d.num_heads, d.latent_dim, d.rope_dim, sched);
     } else if (bf) {
       if (set_lds(absorb_kernel<true>, lds) != hipSuccess) return EG_MLA_ERR_HIP;
       hipLaunchKernelGGL(absorb_kernel<true>, grid, dim3(256), lds, stream, q, w_uk, qfull, batch, d.num_heads,

@@ -106,22 +106,32 @@ struct WideCfg {
 // own partial result, stored at partial row g + b: along the staircase of
 // (range, sequence) pairs that have tokens, g + b grows by one at every step,
 // so the rows are distinct (at most G_eff + B - 1 of them) and those of
-// sequence b are consecutive.  One work-group of 1024 threads computes the
-// prefix sums of the lengths and writes:
+// sequence b are consecutive.  One work-group of NT threads (an extra
+// work-group of the absorption kernel, which runs just before the split
+// kernel) computes the prefix sums of the lengths and writes:
 //   hdr[0] = N, hdr[1] = G_eff;
 //   wg_start[g] = (sequence, offset) of position g N / G_eff;
 //   seq_rows[b] = (first partial row, number of rows) of sequence b (0 rows
 //                 for an empty sequence).
-constexpr int kSchedThreads = 1024;
+struct WideSchedArgs {
+  const int32_t* seq_lens;
+  int cap, G;
+  int64_t* hdr;
+  int2* wg_start;
+  int2* seq_rows;
+};
 
-__global__ __launch_bounds__(kSchedThreads) void wide_schedule_kernel(const int32_t* __restrict__ seq_lens, int B,
-                                                                      int cap, int G, int64_t* __restrict__ hdr,
-                                                                      int2* __restrict__ wg_start,
-                                                                      int2* __restrict__ seq_rows) {
-  __shared__ int64_t wsum[kSchedThreads / 64];
+template <int NT>
+__device__ __forceinline__ void wide_schedule(const WideSchedArgs& sa, int B) {
+  const int32_t* __restrict__ seq_lens = sa.seq_lens;
+  const int cap = sa.cap, G = sa.G;
+  int64_t* __restrict__ hdr = sa.hdr;
+  int2* __restrict__ wg_start = sa.wg_start;
+  int2* __restrict__ seq_rows = sa.seq_rows;
+  __shared__ int64_t wsum[NT / 64];
   __shared__ int64_t carry_s;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  constexpr int NWV = kSchedThreads / 64;
+  constexpr int NWV = NT / 64;
   // inclusive prefix over the work-group of one value per thread; returns the
   // exclusive prefix and leaves the total in `tot`
   auto block_scan = [&](int64_t v, int64_t& tot) {
@@ -143,7 +153,7 @@ __global__ __launch_bounds__(kSchedThreads) void wide_schedule_kernel(const int3
     return before + x - v;
   };
   int64_t N = 0;
-  for (int base = 0; base < B; base += kSchedThreads) {
+  for (int base = 0; base < B; base += NT) {
     const int b = base + tid;
     int64_t tot;
     block_scan(b < B ? clamp_len(seq_lens[b], cap) : 0, tot);
@@ -156,7 +166,7 @@ __global__ __launch_bounds__(kSchedThreads) void wide_schedule_kernel(const int3
     carry_s = 0;
   }
   __syncthreads();
-  for (int base = 0; base < B; base += kSchedThreads) {
+  for (int base = 0; base < B; base += NT) {
     const int b = base + tid;
     const int L = b < B ? clamp_len(seq_lens[b], cap) : 0;
     int64_t tot;
