@@ -162,6 +162,22 @@ def test_balanced_schedule_dc512(gpu, case):
     assert_close(got, oracle_decode(inp), "bf16", f"balanced {case}")
 
 
+@pytest.mark.parametrize("batch", [300, 700])
+def test_balanced_schedule_large_batch(gpu, batch):
+    # More sequences than the schedule's work-group has threads (256): its
+    # prefix sums over the lengths run in several passes; 64 heads (one head
+    # block), lengths 0 .. 40 with a quarter of the sequences empty.
+    wl = W.WORKLOADS[4].replace(name=f"sched_b{batch}_h64_dc512", heads=64, paged=True, seed=49, batch=batch,
+                                seq_len_range=(1, 40))
+    lens = np.random.default_rng(batch).integers(0, 41, size=batch)
+    lens[::4] = 0
+    inp = W.generate(wl, seq_lens=lens)
+    say(f"decode dc512 balanced schedule, {batch} sequences: {int(lens.sum())} tokens")
+    got = gpu_decode(inp)
+    assert np.all(got[lens == 0] == 0)
+    assert_close(got, oracle_decode(inp), "bf16", f"balanced batch {batch}")
+
+
 @pytest.mark.parametrize("total", [393310, 395300])
 def test_list_chunk_edges_dc512(gpu, total):
     # Token ranges just past one token list (3072 tokens) per work-group at
