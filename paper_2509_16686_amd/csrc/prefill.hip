@@ -173,9 +173,7 @@ extern "C" eg_mla_status eg_mla_prefill_varlen(const eg_mla_dims* dims, int32_t 
     uint16_t* kc = reinterpret_cast<uint16_t*>(ws + L.off_qf);
     uint16_t* vv = reinterpret_cast<uint16_t*>(ws + L.off_olat);
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(prefill_x_proj_kernel),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, kPxProjLds) != hipSuccess ||
-        hipFuncSetAttribute(reinterpret_cast<const void*>(prefill_x_attn_kernel),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, 2 * kPxTileBytes) != hipSuccess)
+                            hipFuncAttributeMaxDynamicSharedMemorySize, kPxProjLds) != hipSuccess)
       return EG_MLA_ERR_HIP;
     hipLaunchKernelGGL(prefill_x_proj_kernel, dim3((T + kPxTok - 1) / kPxTok, d.num_heads), dim3(256), kPxProjLds,
                        stream, static_cast<const uint16_t*>(latent), token_ids,
@@ -192,8 +190,8 @@ extern "C" eg_mla_status eg_mla_prefill_varlen(const eg_mla_dims* dims, int32_t 
     x.H = d.num_heads;
     x.DC = d.latent_dim;
     x.scale_log2 = softmax_scale(d) * 1.4426950408889634f;
-    hipLaunchKernelGGL(prefill_x_attn_kernel, dim3(((T + kPxQTok - 1) / kPxQTok) * d.num_heads), dim3(256),
-                       2 * kPxTileBytes, stream, x);
+    hipLaunchKernelGGL(prefill_x_attn_kernel, dim3(((T + kPxQTok - 1) / kPxQTok) * d.num_heads), dim3(256), 0,
+                       stream, x);
     return hipGetLastError() == hipSuccess ? EG_MLA_OK : EG_MLA_ERR_HIP;
   }
   // q_lat (bf16) and q^R for every token

@@ -18,14 +18,18 @@
 // carry only the rounding of their fp32 sums, which is to fp16 (11-bit
 // significand; values must stay below 65504 in magnitude, true of layers whose
 // keys and values are of order one to thousands).  The attention runs on the
-// fp16 MFMA: the bf16 query and RoPE key convert to fp16 exactly (for
-// magnitudes between 2^-14 and 65504), P is rounded to fp16, and the output is
-// rounded once to bf16.
+// fp16 MFMA for the latent part of the scores and for the values (the bf16
+// query converts to fp16 exactly for magnitudes between 2^-14 and 65504) and on
+// the bf16 MFMA for the RoPE part (bf16 query and key: exact products); P is
+// rounded to fp16, and the output is rounded once to bf16.
 #pragma once
 
 namespace egmla {
 
 constexpr int kPxDH = 128, kPxDR = 64, kPxDK = kPxDH + kPxDR;  // key dims per head (K^C | k^R)
+// Word 3 of a raw buffer resource on gfx9 (32-bit data format; stride 0, so
+// the record count is a byte count and offsets past it read zeros).
+constexpr int kBufRsrcWord3 = 0x00020000;
 
 // ---------------------------------------------------------------------------
 // Projection.  Work-group (tt, h) forms K^C[h] and V[h] of tokens
@@ -176,13 +180,21 @@ __global__ __launch_bounds__(256, 2) void prefill_x_proj_kernel(const uint16_t* 
 // (a head's blocks on one XCD, last-in-the-stream first).  Wave w holds the rows of tokens
 // 32 w .. + 31 of the block, its query (fp16) in registers as the B operand of
 // v_mfma_f32_32x32x16_f16 (lane: row lane % 32, dims 8 (lane / 32) + 16 c).
-//  * Tile: K^C rows (256 bytes, fp16), k^R rows (128 bytes, converted from
-//    bf16 on the way) and V rows (256 bytes, fp16) of the next tile are loaded
-//    while the current one is computed and written to the other of two LDS
-//    buffers; 16-byte pieces XOR-swizzled by f(key) = 4 (key % 4) +
-//    (key / 4) % 4 in the 256-byte rows and (key / 2) % 8 in the RoPE rows.
+//  * Tile: K^C rows (256 bytes, fp16), k^R rows (128 bytes, bf16) and V rows
+//    (256 bytes, fp16) of the next tile go straight from global memory into
+//    the other of two LDS buffers while the current one is computed
+//    (buffer_load_dwordx4 ... lds through buffer resources based at the
+//    tile's first key: lane L's 16 bytes land at the instruction's LDS base +
+//    16 L, so each lane fetches the piece that belongs in its slot); 16-byte
+//    pieces XOR-swizzled by f(key) = 4 (key % 4) + (key / 4) % 4 in the
+//    256-byte rows and (key / 2) % 8 in the RoPE rows.  No register holds a
+//    tile in flight, and the buffer form (unlike the global one) leaves the
+//    compiler's waits for LDS reads exact while the copies are in flight.
+//  * The A operands of each score chunk are read one chunk ahead of its
+//    products (scheduling hints), so a pair of products waits for reads
+//    issued a pair earlier.
 //  * Scores S^T[key][row]: 12 products per 32 keys, the tile rows as the A
-//    operand (8 of K^C, 4 of k^R).
+//    operand (8 of K^C on the fp16 MFMA, 4 of k^R on the bf16 MFMA).
 //  * Online softmax per row in the log2 domain with lazy rescale; a lane holds
 //    16 of each 32 keys' scores of its row, the other 16 are in lane ^ 32.
 //  * Values O^T[dim][row] += V^T P^T: the B operand is the lane's own
@@ -209,7 +221,11 @@ struct PrefillXArgs {
 };
 
 __global__ __launch_bounds__(256, 2) void prefill_x_attn_kernel(PrefillXArgs a) {
-  extern __shared__ __attribute__((aligned(16))) unsigned char lds[];  // two tile buffers
+  // two tile buffers, distinct objects: the compiler then knows that a tile's
+  // copies into one do not alias the reads of the other, and does not wait for
+  // the copies before those reads
+  __shared__ __attribute__((aligned(16))) unsigned char lds0[kPxTileBytes];
+  __shared__ __attribute__((aligned(16))) unsigned char lds1[kPxTileBytes];
   // one XCD takes whole heads (a contiguous range of the head-major order), so
   // the blocks of a head read its K^C and V tiles through one L2 cache; within
   // a head the last blocks of the stream (the heaviest) come first
@@ -232,49 +248,51 @@ __global__ __launch_bounds__(256, 2) void prefill_x_attn_kernel(PrefillXArgs a) 
   const int t_c = min(t_row, a.T - 1);
   const int s_row = min(max(a.seq_start[t_c], kbeg), t_c);
 
-  f16x8_t qv[kPxDK / 16];
+  f16x8_t qv[kPxDH / 16];   // latent part (fp16)
+  bf16x8_t qr[kPxDR / 16];  // RoPE part (bf16)
   {
     const uint16_t* qrow = a.q + (static_cast<int64_t>(t_c) * a.H + hh) * kPxDK + 8 * h;
 #pragma unroll
-    for (int c = 0; c < kPxDK / 16; ++c)
+    for (int c = 0; c < kPxDH / 16; ++c)
       qv[c] = __builtin_bit_cast(f16x8_t, bf16x8_to_f16x8(*reinterpret_cast<const u32x4_t*>(qrow + 16 * c)));
+#pragma unroll
+    for (int c = 0; c < kPxDR / 16; ++c) qr[c] = *reinterpret_cast<const bf16x8_t*>(qrow + kPxDH + 16 * c);
   }
 
-  // tile loads: K^C / V pieces pl of keys kl + 16 j, RoPE piece pr of keys kr + 32 j
-  constexpr int NKJ = kPxKeys * (kPxDH / 8) / 256, NRJ = kPxKeys * (kPxDR / 8) / 256;
-  const int kl = tid >> 4, pl = tid & 15, kr = tid >> 3, pr = tid & 7;
+  // tile loads into LDS: wave w issues K^C and V instructions I = 4 w + j
+  // (keys 4 I .. 4 I + 3; lane: key 4 I + lane / 16, slot lane % 16) and RoPE
+  // instructions I = 2 w + j (keys 8 I .. 8 I + 7; lane: key 8 I + lane / 8,
+  // slot lane % 8); slot s of a row holds logical piece s ^ swizzle(key)
+  constexpr int NKI = kPxKeys / 4 / 4, NRI = kPxKeys / 8 / 4;
   auto key_at = [&](int tile, int k) { return min(kbeg + tile * kPxKeys + k, kend - 1); };
   const uint16_t* kc_h = a.kc + static_cast<int64_t>(hh) * a.T * kPxDH;
   const uint16_t* vv_h = a.vv + static_cast<int64_t>(hh) * a.T * kPxDH;
-  u32x4_t nk[NKJ], nv[NKJ], nr[NRJ];
-  auto load_tile = [&](int tile) {
+  auto lds_ptr = [](unsigned char* p) { return (__attribute__((address_space(3))) void*)p; };
+  auto issue_tile = [&](int tile, unsigned char* base) {
+    // buffer resources from the tile's first key (offsets within the tile's rows)
+    const int t0 = kbeg + tile * kPxKeys;
+    const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(kc_h + static_cast<int64_t>(t0) * kPxDH), 0, kPxKeys * kPxKcRow, kBufRsrcWord3);
+    const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(vv_h + static_cast<int64_t>(t0) * kPxDH), 0, kPxKeys * kPxKcRow, kBufRsrcWord3);
+    const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(a.latent + static_cast<int64_t>(t0) * DQ + a.DC), 0, kPxKeys * DQ * 2, kBufRsrcWord3);
 #pragma unroll
-    for (int j = 0; j < NKJ; ++j) {
-      const int64_t key = key_at(tile, kl + 16 * j);
-      nk[j] = *reinterpret_cast<const u32x4_t*>(kc_h + key * kPxDH + 8 * pl);
-      nv[j] = *reinterpret_cast<const u32x4_t*>(vv_h + key * kPxDH + 8 * pl);
+    for (int j = 0; j < NKI; ++j) {
+      const int I = NKI * w + j, key = 4 * I + (lane >> 4), piece = (lane & 15) ^ pf_lat_swz(key);
+      const int off = (key_at(tile, key) - t0) * kPxKcRow + 16 * piece;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, lds_ptr(base + 4 * I * kPxKcRow), 16, off, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, lds_ptr(base + kPxVOff + 4 * I * kPxKcRow), 16, off, 0, 0, 0);
     }
 #pragma unroll
-    for (int j = 0; j < NRJ; ++j)
-      nr[j] = *reinterpret_cast<const u32x4_t*>(a.latent + static_cast<int64_t>(key_at(tile, kr + 32 * j)) * DQ +
-                                                 a.DC + 8 * pr);
-  };
-  auto store_tile = [&](int buf) {
-    unsigned char* base = lds + buf * kPxTileBytes;
-#pragma unroll
-    for (int j = 0; j < NKJ; ++j) {
-      const int key = kl + 16 * j;
-      const int off = key * kPxKcRow + 16 * (pl ^ pf_lat_swz(key));
-      *reinterpret_cast<u32x4_t*>(base + off) = nk[j];
-      *reinterpret_cast<u32x4_t*>(base + kPxVOff + off) = nv[j];
-    }
-#pragma unroll
-    for (int j = 0; j < NRJ; ++j) {
-      const int key = kr + 32 * j;
-      *reinterpret_cast<u32x4_t*>(base + kPxRopeOff + key * kPxRopeRow + 16 * (pr ^ pf_rope_swz(key))) =
-          bf16x8_to_f16x8(nr[j]);
+    for (int j = 0; j < NRI; ++j) {
+      const int I = NRI * w + j, key = 8 * I + (lane >> 3), piece = (lane & 7) ^ pf_rope_swz(key);
+      const int off = (key_at(tile, key) - t0) * DQ * 2 + 16 * piece;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rr, lds_ptr(base + kPxRopeOff + 8 * I * kPxRopeRow), 16, off, 0, 0, 0);
     }
   };
+  // the tile's copies have landed (this wave's); the barrier after it covers every wave's
+  auto tile_landed = []() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); };
 
   // per-lane LDS offsets (bytes within a tile buffer)
   const int off_sk = r32 * kPxKcRow;                // score A: key row 32 kb + r32
@@ -292,13 +310,14 @@ __global__ __launch_bounds__(256, 2) void prefill_x_attn_kernel(PrefillXArgs a) 
     for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
   float m_run = -1e30f, l_run = 0.f;  // finite start: a fully masked tile leaves both unchanged
 
-  load_tile(0);
-  store_tile(0);
+  issue_tile(0, lds0);
+  tile_landed();
   __syncthreads();
 
-  for (int i = 0; i < ntiles; ++i) {
-    if (i + 1 < ntiles) load_tile(i + 1);
-    const unsigned char* tb = lds + (i & 1) * kPxTileBytes;
+  // step i computes tile i from buffer tb and copies tile i + 1 into nb (last
+  // read in step i - 1, which ended in a barrier)
+  auto step = [&](int i, const unsigned char* tb, unsigned char* nb) {
+    if (i + 1 < ntiles) issue_tile(i + 1, nb);
     const int k_lo = kbeg + i * kPxKeys;
 
     // ---- scores S^T[key][row] for keys k_lo + 32 kb + (0..31) ----
@@ -319,10 +338,20 @@ __global__ __launch_bounds__(256, 2) void prefill_x_attn_kernel(PrefillXArgs a) 
     for (int c = 0; c < kPxDR / 16; ++c)
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        const f16x8_t av = *reinterpret_cast<const f16x8_t*>(tb + off_sr + 32 * kb * kPxRopeRow +
-                                                              16 * ((2 * c + h) ^ swz_sr));
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, qv[kPxDH / 16 + c], s[kb], 0, 0, 0);
+        const bf16x8_t av = *reinterpret_cast<const bf16x8_t*>(tb + off_sr + 32 * kb * kPxRopeRow +
+                                                                16 * ((2 * c + h) ^ swz_sr));
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qr[c], s[kb], 0, 0, 0);
       }
+    // issue order: the A operands of a chunk (both key blocks) one chunk ahead
+    // of its two products, so that each pair of products waits for reads issued
+    // a pair earlier
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+    for (int c = 0; c < (kPxDH + kPxDR) / 16 - 1; ++c) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
     // keys outside [s_row, t_row] only in tiles that reach past the block's
     // first token or start before its latest sequence start
     if (k_lo + kPxKeys - 1 > q0 || k_lo < s_max) {
@@ -386,8 +415,12 @@ __global__ __launch_bounds__(256, 2) void prefill_x_attn_kernel(PrefillXArgs a) 
         }
       }
 
-    if (i + 1 < ntiles) store_tile((i + 1) & 1);
+    tile_landed();
     __syncthreads();
+  };
+  for (int i = 0; i < ntiles; i += 2) {
+    step(i, lds0, lds1);
+    if (i + 1 < ntiles) step(i + 1, lds1, lds0);
   }
 
   // ---- out = O / l in bf16: lane holds dims 32 db + 8 q + 4 h + 0..3 of its row ----
