@@ -198,21 +198,20 @@ extern "C" eg_mla_status eg_mla_prefill_varlen(const eg_mla_dims* dims, int32_t 
   const int side_wgs = ((T + kPfUvTokens - 1) / kPfUvTokens + kPfSideChunks - 1) / kPfSideChunks;
   hipLaunchKernelGGL(prefill_absorb_kernel, dim3(side_wgs, d.num_heads), dim3(256), 0, stream,
                      static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(w_uk), qf, T);
+  // the gated latent of every token, once (keys and values of every head)
+  uint16_t* ct = reinterpret_cast<uint16_t*>(ws + L.off_ct);
+  const dim3 gate_grid(static_cast<unsigned>((static_cast<int64_t>(T) * 16 + 255) / 256));
+  hipLaunchKernelGGL(prefill_gate_kernel, gate_grid, dim3(256), 0, stream, static_cast<const uint16_t*>(latent),
+                     token_ids, static_cast<const uint16_t*>(gate_table), ct, T, d.vocab_size);
   PrefillArgs a;
   a.qf = qf;
   a.latent = static_cast<const uint16_t*>(latent);
-  a.ids = token_ids;
-  a.gate = static_cast<const uint16_t*>(gate_table);
+  a.ct = ct;
   a.seq_start = seq_start;
   a.olat = olat;
   a.T = T;
-  a.V = d.vocab_size;
   a.scale_log2 = softmax_scale(d) * 1.4426950408889634f;
-  const size_t lds = 2 * kPfBufBytes;  // 80 KB: above the 64 KB default, so it is requested explicitly
-  if (hipFuncSetAttribute(reinterpret_cast<const void*>(prefill_attn_mfma_kernel),
-                          hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)) != hipSuccess)
-    return EG_MLA_ERR_HIP;
-  hipLaunchKernelGGL(prefill_attn_mfma_kernel, dim3((T + kPfTokens - 1) / kPfTokens), dim3(kPfThreads), lds, stream,
+  hipLaunchKernelGGL(prefill_attn_mfma_kernel, dim3((T + kPfTokens - 1) / kPfTokens), dim3(kPfThreads), 0, stream,
                      a);
   hipLaunchKernelGGL(prefill_uv_kernel, dim3(side_wgs, d.num_heads), dim3(256), 0, stream,
                      olat, static_cast<const uint16_t*>(w_uv), static_cast<uint16_t*>(out), T);

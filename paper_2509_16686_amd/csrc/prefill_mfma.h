@@ -12,17 +12,19 @@
 // the kernel is a multi-query flash attention with 192-dim keys and 128-dim
 // values.
 //
-// Four launches: a map from each token to its sequence's first token; the
-// absorption (q_lat in fp16, with q^R, for every token); the attention kernel
-// below, which writes o_lat / l in fp32; and the up-projection by W_UV per
-// head (o_lat as bf16 hi + lo).
+// Five launches: a map from each token to its sequence's first token; the
+// gated latent of every token (fp16, once: the attention's keys and values);
+// the absorption (q_lat in fp16, q^R copied in bf16, for every token); the
+// attention kernel below, which writes o_lat / l in fp32; and the
+// up-projection by W_UV per head (o_lat as bf16 hi + lo).
 //
-// Precision: the attention runs on the fp16 MFMA.  q_lat is one rounding of
-// its fp32 sum to fp16, q^R and k^R convert from bf16 exactly, the gated
-// latent is one rounding of the exact fp32 product to fp16, and so is each
-// probability: 11-bit significands, where bf16 keys would need a second
-// (lo) product to keep rows dominated by a few keys within the element-wise
-// bound.  Values must stay below 65504 in magnitude.
+// Precision: the latent part of the attention runs on the fp16 MFMA.  q_lat
+// is one rounding of its fp32 sum to fp16, the gated latent one rounding of
+// the exact fp32 product to fp16, and so is each probability: 11-bit
+// significands, where bf16 keys would need a second (lo) product to keep rows
+// dominated by a few keys within the element-wise bound.  The RoPE part runs
+// on the bf16 MFMA (bf16 q^R and k^R: exact products).  Values must stay
+// below 65504 in magnitude.
 //
 // Attention kernel.  A work-group (4 waves; two per CU, whose barriers are
 // independent, so that one's softmax overlaps the other's products on the
@@ -31,17 +33,24 @@
 // outside its own sequence) and walks tiles of 64 keys from the first token's
 // sequence start to the block's last token.  Blocks are launched heaviest
 // first (last in the stream first).
-//  * Tile: 256 threads each load four 16-byte latent pieces with the matching
-//    gate pieces and two RoPE pieces of the next tile while the current one is
-//    computed; the gated latent (fp16) and the RoPE key (fp16) are written to
-//    the other of two LDS buffers.  Rows of 256 bytes hold the 16-byte pieces
+//  * Tile: the gated latent rows (fp16) and RoPE keys (bf16) of the next tile
+//    go straight from global memory into the other of two LDS buffers while
+//    the current one is computed (buffer_load_dwordx4 ... lds through buffer
+//    resources based at the tile's first key: lane L's 16 bytes land at the
+//    instruction's LDS base + 16 L, so each lane fetches the piece that
+//    belongs in its slot).  Rows of 256 bytes hold the 16-byte pieces
 //    XOR-swizzled by f(key) = 4 (key % 4) + (key / 4) % 4, RoPE rows of 128
 //    bytes by (key / 2) % 8: the 16 lanes of a 16-byte read cycle and the 32
-//    lanes of a transposed 8-byte read cycle each hit distinct banks.
+//    lanes of a transposed 8-byte read cycle each hit distinct banks.  The two
+//    buffers are separate LDS objects and the tile loop is unrolled by two, so
+//    that the compiler knows a tile's copies do not alias the other buffer's
+//    reads (and does not wait for them before those reads).
 //  * Scores: wave w holds rows (tokens 2w, 2w + 1) x 16 heads = 32 rows, its
-//    query in registers as the B operand of v_mfma_f32_32x32x16_f16 (lane:
-//    row lane % 32, dims 8 (lane / 32) + 16 c).  S^T[key][row] comes from 12
-//    products per 32 keys with the tile rows as the A operand.
+//    query in registers as the B operand of v_mfma_f32_32x32x16_f16 (latent
+//    part) and v_mfma_f32_32x32x16_bf16 (RoPE part) (lane: row lane % 32, dims
+//    8 (lane / 32) + 16 c).  S^T[key][row] comes from 12 products per 32 keys
+//    with the tile rows as the A operand, each chunk's operands read one chunk
+//    ahead of its products.
 //  * Online softmax per row in the log2 domain, lazy rescale (as the decode).
 //    A lane holds 16 of each 32 keys' scores of its row; the other 16 are in
 //    lane ^ 32 (one permlane32 swap for the maximum; the sums are combined
@@ -102,19 +111,36 @@ __global__ __launch_bounds__(256) void prefill_seqmap_kernel(const int32_t* __re
   seq_start[t] = min(max(cu[lo], 0), t);
 }
 
+// ct[t] = c_t (.) G[id_t] in fp16 (the exact fp32 products, each rounded
+// once): 16 threads per token, 8 dims each.
+__global__ __launch_bounds__(256) void prefill_gate_kernel(const uint16_t* __restrict__ latent,
+                                                           const int32_t* __restrict__ ids,
+                                                           const uint16_t* __restrict__ gate,
+                                                           uint16_t* __restrict__ ct, int T, int V) {
+  const int i = blockIdx.x * 256 + threadIdx.x, t = i >> 4, p = i & 15;
+  if (t >= T) return;
+  const u32x4_t c = *reinterpret_cast<const u32x4_t*>(latent + static_cast<int64_t>(t) * kPfDQ + 8 * p);
+  const u32x4_t g = *reinterpret_cast<const u32x4_t*>(gate + static_cast<int64_t>(clamp_id(ids[t], V)) * kPfDC + 8 * p);
+  *reinterpret_cast<u32x4_t*>(ct + static_cast<int64_t>(t) * kPfDC + 8 * p) = gate_chunk_f16(c, g);
+}
+
+// Word 3 of a raw buffer resource on gfx9 (32-bit data format; stride 0, so
+// the record count is a byte count and offsets past it read zeros).
+constexpr int kPfBufRsrcWord3 = 0x00020000;
+
 struct PrefillArgs {
-  const uint16_t* qf;          // [T][16][192] fp16: q_lat | q^R
+  const uint16_t* qf;          // [T][16][192]: q_lat fp16 | q^R bf16
   const uint16_t* latent;      // [T][192] bf16: c | k^R
-  const int32_t* ids;          // [T]
-  const uint16_t* gate;        // [V][128] bf16
+  const uint16_t* ct;          // [T][128] fp16: gated latent
   const int32_t* seq_start;    // [T]
   float* olat;                 // [T][16][128] fp32: o_lat / l
-  int T, V;
+  int T;
   float scale_log2;            // tau log2(e)
 };
 
 __global__ __launch_bounds__(kPfThreads, 2) void prefill_attn_mfma_kernel(PrefillArgs a) {
-  extern __shared__ __attribute__((aligned(16))) unsigned char lds[];  // two tile buffers
+  __shared__ __attribute__((aligned(16))) unsigned char lds0[kPfBufBytes];  // two tile buffers
+  __shared__ __attribute__((aligned(16))) unsigned char lds1[kPfBufBytes];
   const int nblk = (a.T + kPfTokens - 1) / kPfTokens;
   const int q0 = (nblk - 1 - static_cast<int>(blockIdx.x)) * kPfTokens;  // heaviest blocks first
   const int q_last = min(q0 + kPfTokens, a.T) - 1;
@@ -132,52 +158,45 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_attn_mfma_kernel(Prefil
   const int head = r32 & 15;
   const int s_row = min(max(a.seq_start[t_c], kbeg), t_c);
 
-  f16x8_t qv[kPfDQ / 16];
+  f16x8_t qv[kPfDC / 16];   // q_lat (fp16)
+  bf16x8_t qr[kPfDR / 16];  // q^R (bf16)
   {
     const uint16_t* qrow = a.qf + (static_cast<int64_t>(t_c) * kPfHeads + head) * kPfDQ + 8 * h;
 #pragma unroll
-    for (int c = 0; c < kPfDQ / 16; ++c) qv[c] = *reinterpret_cast<const f16x8_t*>(qrow + 16 * c);
+    for (int c = 0; c < kPfDC / 16; ++c) qv[c] = *reinterpret_cast<const f16x8_t*>(qrow + 16 * c);
+#pragma unroll
+    for (int c = 0; c < kPfDR / 16; ++c) qr[c] = *reinterpret_cast<const bf16x8_t*>(qrow + kPfDC + 16 * c);
   }
 
-  // tile loads: latent/gate pieces pl of keys kl + 16 j, RoPE piece pr of keys kr + 32 j
-  constexpr int NLJ = kPfKeys * (kPfDC / 8) / kPfThreads, NRJ = kPfKeys * (kPfDR / 8) / kPfThreads;
-  const int kl = tid >> 4, pl = tid & 15, kr = tid >> 3, pr = tid & 7;
+  // tile copies into LDS: wave w issues latent instructions I = 4 w + j (keys
+  // 4 I .. 4 I + 3; lane: key 4 I + lane / 16, slot lane % 16) and RoPE
+  // instructions I = 2 w + j (keys 8 I .. 8 I + 7; lane: key 8 I + lane / 8,
+  // slot lane % 8); slot s of a row holds logical piece s ^ swizzle(key)
+  constexpr int NLI = kPfKeys / 4 / 4, NRI = kPfKeys / 8 / 4;
   auto key_at = [&](int tile, int k) { return min(kbeg + tile * kPfKeys + k, kend - 1); };
-  u32x4_t nl[NLJ], ng[NLJ], nr[NRJ];
-  int idn[NLJ];
-  // the ids are clamped only where they become gate addresses, one iteration
-  // after their loads: clamping right away would wait for them, and the loads
-  // complete in order, so that wait would also take the tile loads before them
-  auto load_ids = [&](int tile) {
+  auto lds_ptr = [](unsigned char* p) { return (__attribute__((address_space(3))) void*)p; };
+  auto issue_tile = [&](int tile, unsigned char* base) {
+    const int t0 = kbeg + tile * kPfKeys;
+    const __amdgpu_buffer_rsrc_t rl = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(a.ct + static_cast<int64_t>(t0) * kPfDC), 0, kPfKeys * kPfLatRow, kPfBufRsrcWord3);
+    const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(a.latent + static_cast<int64_t>(t0) * kPfDQ + kPfDC), 0, kPfKeys * kPfDQ * 2,
+        kPfBufRsrcWord3);
 #pragma unroll
-    for (int j = 0; j < NLJ; ++j) idn[j] = a.ids[key_at(tile, kl + 16 * j)];
-  };
-  auto load_tile = [&](int tile) {
-#pragma unroll
-    for (int j = 0; j < NLJ; ++j) {
-      nl[j] = *reinterpret_cast<const u32x4_t*>(a.latent + static_cast<int64_t>(key_at(tile, kl + 16 * j)) * kPfDQ +
-                                                 8 * pl);
-      ng[j] = *reinterpret_cast<const u32x4_t*>(a.gate + static_cast<int64_t>(clamp_id(idn[j], a.V)) * kPfDC + 8 * pl);
+    for (int j = 0; j < NLI; ++j) {
+      const int I = NLI * w + j, key = 4 * I + (lane >> 4), piece = (lane & 15) ^ pf_lat_swz(key);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rl, lds_ptr(base + 4 * I * kPfLatRow), 16,
+                                               (key_at(tile, key) - t0) * kPfLatRow + 16 * piece, 0, 0, 0);
     }
 #pragma unroll
-    for (int j = 0; j < NRJ; ++j)
-      nr[j] = *reinterpret_cast<const u32x4_t*>(a.latent + static_cast<int64_t>(key_at(tile, kr + 32 * j)) * kPfDQ +
-                                                 kPfDC + 8 * pr);
-  };
-  auto store_tile = [&](int buf) {
-    unsigned char* base = lds + buf * kPfBufBytes;
-#pragma unroll
-    for (int j = 0; j < NLJ; ++j) {
-      const int key = kl + 16 * j;
-      *reinterpret_cast<u32x4_t*>(base + key * kPfLatRow + 16 * (pl ^ pf_lat_swz(key))) = gate_chunk_f16(nl[j], ng[j]);
-    }
-#pragma unroll
-    for (int j = 0; j < NRJ; ++j) {
-      const int key = kr + 32 * j;
-      *reinterpret_cast<u32x4_t*>(base + kPfRopeOff + key * kPfRopeRow + 16 * (pr ^ pf_rope_swz(key))) =
-          bf16x8_to_f16x8(nr[j]);
+    for (int j = 0; j < NRI; ++j) {
+      const int I = NRI * w + j, key = 8 * I + (lane >> 3), piece = (lane & 7) ^ pf_rope_swz(key);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rr, lds_ptr(base + kPfRopeOff + 8 * I * kPfRopeRow), 16,
+                                               (key_at(tile, key) - t0) * kPfDQ * 2 + 16 * piece, 0, 0, 0);
     }
   };
+  // this wave's copies have landed; the barrier after it covers every wave's
+  auto tile_landed = []() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); };
 
   // per-lane LDS offsets (bytes within a tile buffer)
   const int off_sl = r32 * kPfLatRow;               // score A: key row 32 kb + r32 (+ 32 kb rows)
@@ -195,18 +214,14 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_attn_mfma_kernel(Prefil
     for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
   float m_run = -1e30f, l_run = 0.f;  // finite start: a fully masked tile leaves both unchanged
 
-  load_ids(0);
-  load_tile(0);
-  if (ntiles > 1) load_ids(1);
-  store_tile(0);
+  issue_tile(0, lds0);
+  tile_landed();
   __syncthreads();
 
-  for (int i = 0; i < ntiles; ++i) {
-    if (i + 1 < ntiles) {
-      load_tile(i + 1);
-      if (i + 2 < ntiles) load_ids(i + 2);
-    }
-    const unsigned char* tb = lds + (i & 1) * kPfBufBytes;
+  // step i computes tile i from buffer tb and copies tile i + 1 into nb (last
+  // read in step i - 1, which ended in a barrier)
+  auto step = [&](int i, const unsigned char* tb, unsigned char* nb) {
+    if (i + 1 < ntiles) issue_tile(i + 1, nb);
     const int k_lo = kbeg + i * kPfKeys;
 
     // ---- scores S^T[key][row] for keys k_lo + 32 kb + (0..31) ----
@@ -227,10 +242,19 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_attn_mfma_kernel(Prefil
     for (int c = 0; c < kPfDR / 16; ++c)
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        const f16x8_t av = *reinterpret_cast<const f16x8_t*>(tb + off_sr + 32 * kb * kPfRopeRow +
-                                                              16 * ((2 * c + h) ^ swz_sr));
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, qv[kPfDC / 16 + c], s[kb], 0, 0, 0);
+        const bf16x8_t av = *reinterpret_cast<const bf16x8_t*>(tb + off_sr + 32 * kb * kPfRopeRow +
+                                                                16 * ((2 * c + h) ^ swz_sr));
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qr[c], s[kb], 0, 0, 0);
       }
+    // issue order: the A operands of a chunk (both key blocks) one chunk ahead
+    // of its two products
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+    for (int c = 0; c < kPfDQ / 16 - 1; ++c) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
     // keys outside [s_row, t_row] (or past the block) only in tiles that reach
     // past the block's first token or start before its latest sequence start
     if (k_lo + kPfKeys - 1 > q0 || k_lo < s_max) {
@@ -295,8 +319,12 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_attn_mfma_kernel(Prefil
         }
       }
 
-    if (i + 1 < ntiles) store_tile((i + 1) & 1);
+    tile_landed();
     __syncthreads();
+  };
+  for (int i = 0; i < ntiles; i += 2) {
+    step(i, lds0, lds1);
+    if (i + 1 < ntiles) step(i + 1, lds1, lds0);
   }
 
   // ---- o_lat / l: lane holds dims 32 db + 8 q + 4 h + 0..3 of its row ----
@@ -312,7 +340,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_attn_mfma_kernel(Prefil
   }
 }
 
-// q_lat[t, h, :] = W_UK[h]^T q^C[t, h, :] in fp16, and q^R in fp16, for up to
+// q_lat[t, h, :] = W_UK[h]^T q^C[t, h, :] in fp16, and q^R copied in bf16, for up to
 // 4 chunks of 128 tokens of one head per work-group (4 waves of 32 tokens; the
 // next chunk's rows load while a chunk computes and stores).  W_UK[h]
 // ([d_h][d_c] row-major, rows padded to 288 bytes) is staged in LDS once and
@@ -393,10 +421,10 @@ __global__ __launch_bounds__(256) void prefill_absorb_kernel(const uint16_t* __r
     }
     if (t0 + (tid >> 1) < T) {
       uint16_t* dr = qf + (static_cast<int64_t>(t0 + (tid >> 1)) * kPfHeads + hh) * kPfDQ + kPfDC + 32 * (tid & 1);
-      *reinterpret_cast<u32x4_t*>(dr) = bf16x8_to_f16x8(r0);
-      *reinterpret_cast<u32x4_t*>(dr + 8) = bf16x8_to_f16x8(r1);
-      *reinterpret_cast<u32x4_t*>(dr + 16) = bf16x8_to_f16x8(r2);
-      *reinterpret_cast<u32x4_t*>(dr + 24) = bf16x8_to_f16x8(r3);
+      *reinterpret_cast<u32x4_t*>(dr) = r0;
+      *reinterpret_cast<u32x4_t*>(dr + 8) = r1;
+      *reinterpret_cast<u32x4_t*>(dr + 16) = r2;
+      *reinterpret_cast<u32x4_t*>(dr + 24) = r3;
     }
   }
 }
