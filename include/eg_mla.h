@@ -322,7 +322,8 @@ eg_mla_status eg_mla_prefill_ref(const eg_mla_dims* dims, int32_t seq_len, const
  * V = W_UV[h] c~ per head, then attention per head; 3.4x fewer flops per pair
  * than the absorbed form at d_c 512).  Other shapes: EG_MLA_ERR_UNSUPPORTED
  * (eg_mla_prefill_ref covers any shape, one sequence at a time).  The matrix
- * products take fp16 operands (values below 65504 in magnitude).
+ * products take fp16 operands for the latent parts (values below 65504 in
+ * magnitude) and bf16 ones for the RoPE parts.
  *
  *   cu_seqlens [batch + 1] int32 (device): sequence b is tokens
  *       cu_seqlens[b] .. cu_seqlens[b+1]-1; cu_seqlens[0] = 0,
@@ -333,8 +334,9 @@ eg_mla_status eg_mla_prefill_ref(const eg_mla_dims* dims, int32_t seq_len, const
  *       (rows as eg_mla_append writes them); token_ids [total];
  *   gate_table, w_uk, w_uv as for decode;  out [total, H, d_v].
  *   workspace: eg_mla_prefill_varlen_workspace_size bytes, 256-byte aligned
- *       (per-token sequence starts; absorbed form: the absorbed queries in
- *       fp16 and the normalised latent outputs in fp32, [T][H][d_c] each;
+ *       (per-token sequence starts; absorbed form: the absorbed queries
+ *       [T][H][d_c + d_r] (q_lat fp16, q^R bf16), the normalised latent
+ *       outputs in fp32 [T][H][d_c] and the gated latents in fp16 [T][d_c];
  *       explicit form: K^C and V in fp16, [H][T][128] each).
  * Pointers 16-byte aligned.  total_tokens == 0 is a no-op.
  * ------------------------------------------------------------------------- */
