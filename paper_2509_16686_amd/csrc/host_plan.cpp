@@ -242,7 +242,8 @@ PrefillVarlenLayout prefill_varlen_layout(const eg_mla_dims& d, int32_t total_to
   } else {
     L.off_qf = align_up(T * 4);                                                  // K^C: fp16 [H][T][d_h]
     L.off_olat = L.off_qf + align_up(T * H * static_cast<size_t>(d.head_dim) * 2);  // V: fp16 [H][T][d_v]
-    L.bytes = std::max<size_t>(L.off_olat + align_up(T * H * static_cast<size_t>(d.v_head_dim) * 2), kAlign);
+    L.off_ct = L.off_olat + align_up(T * H * static_cast<size_t>(d.v_head_dim) * 2);  // bf16 hi, lo [2][T][d_c]
+    L.bytes = std::max<size_t>(L.off_ct + 2 * align_up(T * static_cast<size_t>(d.latent_dim) * 2), kAlign);
   }
   return L;
 }

@@ -88,8 +88,9 @@ eg_mla_status validate_prefill(const eg_mla_dims* d, int32_t seq_len, const void
 
 // Batched (packed, variable-length) causal prefill on MFMA.
 // Absorbed form (d_c 128, 16 heads): off_qf = absorbed queries, off_olat =
-// latent outputs, off_ct = gated latents.  Explicit form (other shapes):
-// off_qf = K^C, off_olat = V (off_ct unused).
+// latent outputs, off_ct = gated latents (fp16).  Explicit form (other
+// shapes): off_qf = K^C, off_olat = V, off_ct = gated latents (bf16 hi rows,
+// then lo rows).
 struct PrefillVarlenLayout {
   size_t off_seq_start, off_qf, off_olat, off_ct = 0, bytes;
 };

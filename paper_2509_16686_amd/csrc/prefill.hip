@@ -172,13 +172,16 @@ extern "C" eg_mla_status eg_mla_prefill_varlen(const eg_mla_dims* dims, int32_t 
     // explicit form: K^C and V per head (fp16), then the attention per head
     uint16_t* kc = reinterpret_cast<uint16_t*>(ws + L.off_qf);
     uint16_t* vv = reinterpret_cast<uint16_t*>(ws + L.off_olat);
-    if (hipFuncSetAttribute(reinterpret_cast<const void*>(prefill_x_proj_kernel),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, kPxProjLds) != hipSuccess)
-      return EG_MLA_ERR_HIP;
-    hipLaunchKernelGGL(prefill_x_proj_kernel, dim3((T + kPxTok - 1) / kPxTok, d.num_heads), dim3(256), kPxProjLds,
-                       stream, static_cast<const uint16_t*>(latent), token_ids,
-                       static_cast<const uint16_t*>(gate_table), static_cast<const uint16_t*>(w_uk),
-                       static_cast<const uint16_t*>(w_uv), kc, vv, T, d.latent_dim, d.vocab_size);
+    // the gated latent of every token, once, as bf16 hi + lo rows
+    uint16_t* ct_hi = reinterpret_cast<uint16_t*>(ws + L.off_ct);
+    uint16_t* ct_lo = reinterpret_cast<uint16_t*>(ws + L.off_ct + align_up(static_cast<size_t>(T) * d.latent_dim * 2));
+    const dim3 gate_grid(static_cast<unsigned>((static_cast<int64_t>(T) * (d.latent_dim / 8) + 255) / 256));
+    hipLaunchKernelGGL(prefill_x_gate_kernel, gate_grid, dim3(256), 0, stream, static_cast<const uint16_t*>(latent),
+                       token_ids, static_cast<const uint16_t*>(gate_table), ct_hi, ct_lo, T, d.latent_dim,
+                       d.vocab_size);
+    hipLaunchKernelGGL(prefill_x_proj_kernel, dim3((T + kPxTok - 1) / kPxTok, d.num_heads), dim3(256), 0, stream,
+                       ct_hi, ct_lo, static_cast<const uint16_t*>(w_uk), static_cast<const uint16_t*>(w_uv), kc, vv, T,
+                       d.latent_dim);
     PrefillXArgs x;
     x.q = static_cast<const uint16_t*>(q);
     x.latent = static_cast<const uint16_t*>(latent);

@@ -32,79 +32,94 @@ constexpr int kPxDH = 128, kPxDR = 64, kPxDK = kPxDH + kPxDR;  // key dims per h
 constexpr int kBufRsrcWord3 = 0x00020000;
 
 // ---------------------------------------------------------------------------
+// Gated latent, once per token: c~_t = c_t (.) G[id_t] as bf16 hi + lo rows
+// (ct_hi[t] + ct_lo[t] is the exact fp32 product), 8 dims per thread.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void prefill_x_gate_kernel(const uint16_t* __restrict__ latent,
+                                                             const int32_t* __restrict__ ids,
+                                                             const uint16_t* __restrict__ gate,
+                                                             uint16_t* __restrict__ ct_hi, uint16_t* __restrict__ ct_lo,
+                                                             int T, int DC, int V) {
+  const int per = DC / 8;  // threads per token
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int t = static_cast<int>(i / per), p = static_cast<int>(i % per);
+  if (t >= T) return;
+  const u32x4_t c = *reinterpret_cast<const u32x4_t*>(latent + static_cast<int64_t>(t) * (DC + kPxDR) + 8 * p);
+  const u32x4_t g = *reinterpret_cast<const u32x4_t*>(gate + static_cast<int64_t>(clamp_id(ids[t], V)) * DC + 8 * p);
+  u32x4_t hi, lo;
+  gate_chunk_hilo(c, g, hi, lo);
+  *reinterpret_cast<u32x4_t*>(ct_hi + static_cast<int64_t>(t) * DC + 8 * p) = hi;
+  *reinterpret_cast<u32x4_t*>(ct_lo + static_cast<int64_t>(t) * DC + 8 * p) = lo;
+}
+
+// ---------------------------------------------------------------------------
 // Projection.  Work-group (tt, h) forms K^C[h] and V[h] of tokens
 // 128 tt .. + 127: a product of the 128 gated latent rows (B operand, as hi
 // and lo) with the 256 rows W_UK[h] | W_UV[h] (A operand) over d_c, in steps
-// of 32: each step's rows (64 bytes each, the latent as hi rows then lo rows,
-// then the weights) are staged in LDS with a row stride of 80 bytes (the
-// operand reads of 16 rows by 16 lanes hit 64 distinct banks), double
-// buffered, the next step's global loads in registers.  Wave (wt, wo) =
-// (w % 2, w / 2) forms tokens 64 wt .. + 63 of K^C (wo = 0) or V (wo = 1):
-// 2 x 4 tiles of v_mfma_f32_32x32x16_bf16, two products per tile and step.
+// of 32.  Each step's rows (64 bytes each: hi rows, lo rows, weights) go
+// straight from global memory into the other of two LDS buffers while the
+// current step is computed (buffer_load_dwordx4 ... lds: one instruction
+// fills 16 rows; lane L's 16 bytes land at the instruction's LDS base + 16 L,
+// so each lane fetches the piece that belongs in its slot); the four 16-byte
+// pieces of a row are XOR-swizzled by (row / 4) % 4, so that the operand
+// reads of 8 rows by 8 lanes hit distinct banks.  The two buffers are
+// separate LDS objects and the step loop is unrolled by two (the compiler
+// then knows the copies into one do not alias the other's reads).  Wave
+// (wt, wo) = (w % 2, w / 2) forms tokens 64 wt .. + 63 of K^C (wo = 0) or V
+// (wo = 1): 2 x 4 tiles of v_mfma_f32_32x32x16_bf16, two products per tile
+// and step.
 // ---------------------------------------------------------------------------
-constexpr int kPxTok = 128, kPxOut = 256, kPxK = 32, kPxStride = kPxK + 8;
-constexpr int kPxRows = 2 * kPxTok + kPxOut;              // hi, lo, weights
-constexpr int kPxBuf = kPxRows * kPxStride;               // bf16 elements per buffer
-constexpr int kPxProjLds = 2 * kPxBuf * 2;                // bytes (two buffers)
-static_assert(2 * kPxProjLds <= 160 * 1024, "two work-groups per compute unit");
+constexpr int kPxTok = 128, kPxOut = 256, kPxK = 32;
+constexpr int kPxRowB = 2 * kPxK;                          // bytes per staged row (64)
+constexpr int kPxRows = 2 * kPxTok + kPxOut;               // hi, lo, weights
+constexpr int kPxProjBuf = kPxRows * kPxRowB;              // bytes per buffer (32 KB)
+static_assert(2 * 2 * kPxProjBuf <= 160 * 1024, "two work-groups per compute unit");
 
-__global__ __launch_bounds__(256, 2) void prefill_x_proj_kernel(const uint16_t* __restrict__ latent,
-                                                                const int32_t* __restrict__ ids,
-                                                                const uint16_t* __restrict__ gate,
+__device__ __forceinline__ int px_swz(int row) { return (row >> 2) & 3; }
+
+__global__ __launch_bounds__(256, 2) void prefill_x_proj_kernel(const uint16_t* __restrict__ ct_hi,
+                                                                const uint16_t* __restrict__ ct_lo,
                                                                 const uint16_t* __restrict__ w_uk,
                                                                 const uint16_t* __restrict__ w_uv,
                                                                 uint16_t* __restrict__ kc, uint16_t* __restrict__ vv,
-                                                                int T, int DC, int V) {
-  extern __shared__ __attribute__((aligned(16))) uint16_t stage[];  // [2][kPxRows][kPxStride]
+                                                                int T, int DC) {
+  __shared__ __attribute__((aligned(16))) unsigned char st0[kPxProjBuf];
+  __shared__ __attribute__((aligned(16))) unsigned char st1[kPxProjBuf];
   const int tt = blockIdx.x, hh = blockIdx.y;
-  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r32 = lane & 31, h = lane >> 5;
+  const int tid = threadIdx.x, lane = tid & 63, r32 = lane & 31, h = lane >> 5;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wt = w & 1, wo = w >> 1;
-  const int DQ = DC + kPxDR;
-  // copies of a step: latent and gate pieces j = tid + 256 i (i < 2) of token
-  // row j / 4, weight pieces j = tid + 256 i (i < 4) of weight row j / 4;
-  // 16 bytes at 8 (j % 4) of the row's 32 k
-  const uint16_t* lp[2];
-  const uint16_t* gp[2];
-  const uint16_t* wp[4];
-  int xo[2], wofs[4];
+  const int t0 = kPxTok * tt;
+  // buffer resources: the block's hi and lo rows, and the head's weight rows
+  const int ntok = min(kPxTok, T - t0);
+  const __amdgpu_buffer_rsrc_t rh =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(ct_hi + static_cast<int64_t>(t0) * DC), 0, ntok * DC * 2,
+                                        kBufRsrcWord3);
+  const __amdgpu_buffer_rsrc_t rl =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(ct_lo + static_cast<int64_t>(t0) * DC), 0, ntok * DC * 2,
+                                        kBufRsrcWord3);
+  const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(w_uk + static_cast<int64_t>(hh) * kPxDH * DC), 0, kPxDH * DC * 2, kBufRsrcWord3);
+  const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(w_uv + static_cast<int64_t>(hh) * kPxDH * DC), 0, kPxDH * DC * 2, kBufRsrcWord3);
+  // copies of a step: wave w fills rows 16 I .. 16 I + 15 for I = 8 w + j
+  // (j < 8): region w of the four of 128 rows (hi, lo, W_UK, W_UV); lane: row
+  // 16 I + lane / 4, slot lane % 4, which holds piece slot ^ swizzle(row)
+  auto lds_ptr = [](unsigned char* p) { return (__attribute__((address_space(3))) void*)p; };
+  auto issue_step = [&](int step, unsigned char* base) {
+    const int kb = kPxRowB * step;  // byte offset of the step's 32 k in a row
+    // wave w (uniform) takes one region: 0 hi rows, 1 lo rows, 2 W_UK rows, 3 W_UV rows
+    const __amdgpu_buffer_rsrc_t rs = w == 0 ? rh : w == 1 ? rl : w == 2 ? rk : rv;
+    const int nrow = w < 2 ? ntok : kPxDH;  // rows of the region (latent rows past the end repeat the last)
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int j = tid + 256 * i, row = j >> 2, c = j & 3;
-    const int t = min(kPxTok * tt + row, T - 1);
-    lp[i] = latent + static_cast<int64_t>(t) * DQ + 8 * c;
-    gp[i] = gate + static_cast<int64_t>(clamp_id(ids[t], V)) * DC + 8 * c;
-    xo[i] = row * kPxStride + 8 * c;
-  }
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int j = tid + 256 * i, row = j >> 2, c = j & 3;
-    wp[i] = (row < kPxDH ? w_uk + (static_cast<int64_t>(hh) * kPxDH + row) * DC
-                         : w_uv + (static_cast<int64_t>(hh) * kPxDH + row - kPxDH) * DC) + 8 * c;
-    wofs[i] = (2 * kPxTok + row) * kPxStride + 8 * c;
-  }
-  u32x4_t gl[2], gg[2], gw[4];
-  auto fetch = [&](int step) {
-    const int k = kPxK * step;
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      gl[i] = *reinterpret_cast<const u32x4_t*>(lp[i] + k);
-      gg[i] = *reinterpret_cast<const u32x4_t*>(gp[i] + k);
+    for (int j = 0; j < 8; ++j) {
+      const int I = 8 * w + j, row = 16 * I + (lane >> 2), piece = (lane & 3) ^ px_swz(row);
+      const int r = min(row & (kPxTok - 1), nrow - 1);  // row within the region
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, lds_ptr(base + 16 * I * kPxRowB), 16, r * DC * 2 + kb + 16 * piece,
+                                               0, 0, 0);
     }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) gw[i] = *reinterpret_cast<const u32x4_t*>(wp[i] + k);
   };
-  auto put = [&](int buf) {
-    uint16_t* b = stage + buf * kPxBuf;
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      u32x4_t hi, lo;
-      gate_chunk_hilo(gl[i], gg[i], hi, lo);
-      *reinterpret_cast<u32x4_t*>(b + xo[i]) = hi;
-      *reinterpret_cast<u32x4_t*>(b + kPxTok * kPxStride + xo[i]) = lo;
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4_t*>(b + wofs[i]) = gw[i];
-  };
+  auto step_landed = []() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); };
   pf_f32x16_t acc[2][4];
 #pragma unroll
   for (int tb = 0; tb < 2; ++tb)
@@ -112,21 +127,23 @@ __global__ __launch_bounds__(256, 2) void prefill_x_proj_kernel(const uint16_t* 
     for (int ob = 0; ob < 4; ++ob)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[tb][ob][r] = 0.f;
-  const int brow = (64 * wt + r32) * kPxStride + 8 * h;
-  const int arow = (2 * kPxTok + 128 * wo + r32) * kPxStride + 8 * h;
-  auto compute = [&](int buf) {
-    const uint16_t* b = stage + buf * kPxBuf;
+  // operand rows of this lane: latent row 64 wt + 32 tb + r32, weight row 128 wo + 32 ob + r32
+  auto compute = [&](const unsigned char* b) {
 #pragma unroll
     for (int kk = 0; kk < kPxK / 16; ++kk) {
       bf16x8_t bh[2], bl[2], av[4];
 #pragma unroll
       for (int tb = 0; tb < 2; ++tb) {
-        bh[tb] = *reinterpret_cast<const bf16x8_t*>(b + brow + 32 * tb * kPxStride + 16 * kk);
-        bl[tb] = *reinterpret_cast<const bf16x8_t*>(b + kPxTok * kPxStride + brow + 32 * tb * kPxStride + 16 * kk);
+        const int row = 64 * wt + 32 * tb + r32;
+        const int off = row * kPxRowB + 16 * ((2 * kk + h) ^ px_swz(row));
+        bh[tb] = *reinterpret_cast<const bf16x8_t*>(b + off);
+        bl[tb] = *reinterpret_cast<const bf16x8_t*>(b + kPxTok * kPxRowB + off);
       }
 #pragma unroll
-      for (int ob = 0; ob < 4; ++ob)
-        av[ob] = *reinterpret_cast<const bf16x8_t*>(b + arow + 32 * ob * kPxStride + 16 * kk);
+      for (int ob = 0; ob < 4; ++ob) {
+        const int row = 2 * kPxTok + 128 * wo + 32 * ob + r32;
+        av[ob] = *reinterpret_cast<const bf16x8_t*>(b + row * kPxRowB + 16 * ((2 * kk + h) ^ px_swz(row)));
+      }
 #pragma unroll
       for (int tb = 0; tb < 2; ++tb)
 #pragma unroll
@@ -136,30 +153,31 @@ __global__ __launch_bounds__(256, 2) void prefill_x_proj_kernel(const uint16_t* 
         }
     }
   };
-  // step s computes from buffer s % 2, then writes step s + 1 (in registers)
-  // to the other buffer and fetches step s + 2; the step count is even and the
-  // loop has no branch (past the last step the last one is fetched and
-  // written again, to a buffer nothing reads)
+  // step s computes from one buffer while step s + 1 is copied into the other
+  // (last read in step s - 1, which ended in a barrier); the step count is even
   const int steps = DC / kPxK;
-  fetch(0);
-  put(0);
-  fetch(1);
+  issue_step(0, st0);
+  step_landed();
   __syncthreads();
+  // (a scheduling barrier after each issue keeps the copies at the start of
+  // the step instead of sunk below its products)
   for (int s0 = 0; s0 < steps; s0 += 2) {
-    compute(0);
-    put(1);
-    fetch(min(s0 + 2, steps - 1));
+    issue_step(s0 + 1, st1);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(st0);
+    step_landed();
     __syncthreads();
-    compute(1);
-    put(0);
-    fetch(min(s0 + 3, steps - 1));
+    if (s0 + 2 < steps) issue_step(s0 + 2, st0);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(st1);
+    step_landed();
     __syncthreads();
   }
   // lane holds dims 32 ob + 8 q + 4 h + (0..3) of token 64 wt + 32 tb + r32 in acc[tb][ob][4 q + (0..3)]
   uint16_t* dst = wo == 0 ? kc : vv;
 #pragma unroll
   for (int tb = 0; tb < 2; ++tb) {
-    const int t = kPxTok * tt + 64 * wt + 32 * tb + r32;
+    const int t = t0 + 64 * wt + 32 * tb + r32;
     if (t >= T) break;
     uint16_t* row = dst + (static_cast<int64_t>(hh) * T + t) * kPxDH + 4 * h;
 #pragma unroll

@@ -261,7 +261,8 @@ def test_prefill_varlen_rejects_before_launch(L):
     for good, H in ((dims(num_heads=32), 32), (dims(latent_dim=512, gate_dim=512, num_heads=128), 128),
                     (dims(latent_dim=256, gate_dim=256, num_heads=16), 16)):
         need_x = L.eg_mla_prefill_varlen_workspace_size(ctypes.byref(good), n)
-        assert need_x == al(n * 4) + 2 * al(n * H * 128 * 2)
+        # sequence starts, K^C and V (fp16), the gated latent as bf16 hi and lo rows
+        assert need_x == al(n * 4) + 2 * al(n * H * 128 * 2) + 2 * al(n * good.latent_dim * 2)
         assert call(good, 2, n, wsb=need_x - 1) == B.ERR_WORKSPACE
 
 
