@@ -208,9 +208,9 @@ __global__ __launch_bounds__(256, 2) void prefill_x_proj_kernel(const uint16_t* 
 //    256-byte rows and (key / 2) % 8 in the RoPE rows.  No register holds a
 //    tile in flight, and the buffer form (unlike the global one) leaves the
 //    compiler's waits for LDS reads exact while the copies are in flight.
-//  * The A operands of each score chunk are read one chunk ahead of its
+//  * The A operands of each score chunk are read two chunks ahead of its
 //    products (scheduling hints), so a pair of products waits for reads
-//    issued a pair earlier.
+//    issued two pairs earlier.
 //  * Scores S^T[key][row]: 12 products per 32 keys, the tile rows as the A
 //    operand (8 of K^C on the fp16 MFMA, 4 of k^R on the bf16 MFMA).
 //  * Online softmax per row in the log2 domain with lazy rescale; a lane holds
@@ -360,16 +360,16 @@ __global__ __launch_bounds__(256, 2) void prefill_x_attn_kernel(PrefillXArgs a) 
                                                                 16 * ((2 * c + h) ^ swz_sr));
         s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qr[c], s[kb], 0, 0, 0);
       }
-    // issue order: the A operands of a chunk (both key blocks) one chunk ahead
+    // issue order: the A operands of a chunk (both key blocks) two chunks ahead
     // of its two products, so that each pair of products waits for reads issued
-    // a pair earlier
-    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+    // two pairs earlier
+    __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
 #pragma unroll
-    for (int c = 0; c < (kPxDH + kPxDR) / 16 - 1; ++c) {
+    for (int c = 0; c < (kPxDH + kPxDR) / 16 - 1 - 1; ++c) {
       __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
       __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
     // keys outside [s_row, t_row] only in tiles that reach past the block's
     // first token or start before its latest sequence start
     if (k_lo + kPxKeys - 1 > q0 || k_lo < s_max) {
