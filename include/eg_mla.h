@@ -336,7 +336,7 @@ eg_mla_status eg_mla_prefill_ref(const eg_mla_dims* dims, int32_t seq_len, const
  *   workspace: eg_mla_prefill_varlen_workspace_size bytes, 256-byte aligned
  *       (per-token sequence starts; absorbed form: the absorbed queries
  *       [T][H][d_c + d_r] (q_lat fp16, q^R bf16), the normalised latent
- *       outputs in fp32 [T][H][d_c] and the gated latents in fp16 [T][d_c];
+ *       outputs in fp16 [T][H][d_c] and the gated latents in fp16 [T][d_c];
  *       explicit form: K^C and V in fp16, [H][T][128] each, and the gated
  *       latents as bf16 hi and lo rows, [T][d_c] each).
  * Pointers 16-byte aligned.  total_tokens == 0 is a no-op.

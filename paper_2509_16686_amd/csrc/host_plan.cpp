@@ -236,8 +236,8 @@ PrefillVarlenLayout prefill_varlen_layout(const eg_mla_dims& d, int32_t total_to
   L.off_seq_start = 0;  // int32 [T]
   if (prefill_varlen_absorbed(d)) {
     L.off_qf = align_up(T * 4);                                                                    // fp16 | bf16 [T][H][d_c + d_r]
-    L.off_olat = L.off_qf + align_up(T * H * static_cast<size_t>(d.latent_dim + d.rope_dim) * 2);  // fp32 [T][H][d_c]
-    L.off_ct = L.off_olat + align_up(T * H * static_cast<size_t>(d.latent_dim) * 4);             // fp16 [T][d_c]
+    L.off_olat = L.off_qf + align_up(T * H * static_cast<size_t>(d.latent_dim + d.rope_dim) * 2);  // fp16 [T][H][d_c]
+    L.off_ct = L.off_olat + align_up(T * H * static_cast<size_t>(d.latent_dim) * 2);             // fp16 [T][d_c]
     L.bytes = std::max<size_t>(L.off_ct + align_up(T * static_cast<size_t>(d.latent_dim) * 2), kAlign);
   } else {
     L.off_qf = align_up(T * 4);                                                  // K^C: fp16 [H][T][d_h]

@@ -164,7 +164,7 @@ extern "C" eg_mla_status eg_mla_prefill_varlen(const eg_mla_dims* dims, int32_t 
   unsigned char* ws = static_cast<unsigned char*>(workspace);
   int32_t* seq_start = reinterpret_cast<int32_t*>(ws + L.off_seq_start);
   uint16_t* qf = reinterpret_cast<uint16_t*>(ws + L.off_qf);
-  float* olat = reinterpret_cast<float*>(ws + L.off_olat);
+  uint16_t* olat = reinterpret_cast<uint16_t*>(ws + L.off_olat);
 
   hipLaunchKernelGGL(prefill_seqmap_kernel, dim3((T + 255) / 256), dim3(256), 0, stream, cu_seqlens, batch, T,
                      seq_start);

@@ -15,8 +15,8 @@
 // Five launches: a map from each token to its sequence's first token; the
 // gated latent of every token (fp16, once: the attention's keys and values);
 // the absorption (q_lat in fp16, q^R copied in bf16, for every token); the
-// attention kernel below, which writes o_lat / l in fp32; and the
-// up-projection by W_UV per head (o_lat as bf16 hi + lo).
+// attention kernel below, which writes o_lat / l in fp16; and the
+// up-projection by W_UV per head (W_UV converted exactly to fp16).
 //
 // Precision: the latent part of the attention runs on the fp16 MFMA.  q_lat
 // is one rounding of its fp32 sum to fp16, the gated latent one rounding of
@@ -133,7 +133,7 @@ struct PrefillArgs {
   const uint16_t* latent;      // [T][192] bf16: c | k^R
   const uint16_t* ct;          // [T][128] fp16: gated latent
   const int32_t* seq_start;    // [T]
-  float* olat;                 // [T][16][128] fp32: o_lat / l
+  uint16_t* olat;              // [T][16][128] fp16: o_lat / l
   int T;
   float scale_log2;            // tau log2(e)
 };
@@ -330,13 +330,14 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_attn_mfma_kernel(Prefil
   // ---- o_lat / l: lane holds dims 32 db + 8 q + 4 h + 0..3 of its row ----
   const float inv = 1.0f / pf_pair_sum(l_run);
   if (row_ok) {
-    float* orow = a.olat + (static_cast<int64_t>(t_row) * kPfHeads + head) * kPfDC + 4 * h;
+    uint16_t* orow = a.olat + (static_cast<int64_t>(t_row) * kPfHeads + head) * kPfDC + 4 * h;
 #pragma unroll
     for (int db = 0; db < kPfDC / 32; ++db)
 #pragma unroll
       for (int q = 0; q < 4; ++q)
-        *reinterpret_cast<f32x4_t*>(orow + 32 * db + 8 * q) =
-            f32x4_t{o[db][4 * q] * inv, o[db][4 * q + 1] * inv, o[db][4 * q + 2] * inv, o[db][4 * q + 3] * inv};
+        *reinterpret_cast<u32x2_t*>(orow + 32 * db + 8 * q) =
+            u32x2_t{pack_f16x2(o[db][4 * q] * inv, o[db][4 * q + 1] * inv),
+                    pack_f16x2(o[db][4 * q + 2] * inv, o[db][4 * q + 3] * inv)};
   }
 }
 
@@ -431,11 +432,13 @@ __global__ __launch_bounds__(256) void prefill_absorb_kernel(const uint16_t* __r
 
 // out[t, h, :] = W_UV[h] o_lat[t, h, :] for up to 4 chunks of 128 tokens of
 // one head per work-group (4 waves of 32 tokens; the next chunk's rows load
-// while a chunk is stored and converted): W_UV[h] ([d_v][d_c], rows padded by 16
-// bytes) in LDS as the A operand, o_lat rows straight from global as the B
-// operand, split into bf16 hi + lo (two products, so o_lat keeps ~16 bits);
-// the accumulator holds out^T, stored 4 consecutive v at a time.
-__global__ __launch_bounds__(256) void prefill_uv_kernel(const float* __restrict__ olat,
+// while a chunk is stored): W_UV[h] ([d_v][d_c], rows padded by 16 bytes)
+// converted to fp16 (exact for magnitudes between 2^-14 and 65504; smaller
+// weights become fp16 subnormals, an absolute error below 2^-25) in LDS as the
+// A operand, the fp16 o_lat rows straight from global as the B operand of
+// v_mfma_f32_32x32x16_f16; the accumulator holds out^T, stored 4 consecutive v
+// at a time.
+__global__ __launch_bounds__(256) void prefill_uv_kernel(const uint16_t* __restrict__ olat,
                                                          const uint16_t* __restrict__ w_uv,
                                                          uint16_t* __restrict__ out, int T) {
   constexpr int DV = 128, RS = kPfDC + 8;
@@ -444,37 +447,25 @@ __global__ __launch_bounds__(256) void prefill_uv_kernel(const float* __restrict
   const int c0 = blockIdx.x * kPfSideChunks;
   const int nch = min(kPfSideChunks, (T + kPfUvTokens - 1) / kPfUvTokens - c0);
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r32 = lane & 31, h = lane >> 5;
-  f32x4_t ov[kPfDC / 16][2];  // the lane's token's o_lat, dims 16 c + 8 h .. + 7
+  f16x8_t ov[kPfDC / 16];  // the lane's token's o_lat, dims 16 c + 8 h .. + 7
   auto load = [&](int chunk) {
     const int tc = min(chunk * kPfUvTokens + 32 * w + r32, T - 1);
-    const float* orow = olat + (static_cast<int64_t>(tc) * kPfHeads + hh) * kPfDC + 8 * h;
+    const uint16_t* orow = olat + (static_cast<int64_t>(tc) * kPfHeads + hh) * kPfDC + 8 * h;
 #pragma unroll
-    for (int c = 0; c < kPfDC / 16; ++c)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) ov[c][j] = *reinterpret_cast<const f32x4_t*>(orow + 16 * c + 4 * j);
+    for (int c = 0; c < kPfDC / 16; ++c) ov[c] = *reinterpret_cast<const f16x8_t*>(orow + 16 * c);
   };
   load(c0);
   for (int p = tid; p < DV * kPfDC / 8; p += 256) {
     const int v = p / (kPfDC / 8), k8 = (p % (kPfDC / 8)) * 8;
     *reinterpret_cast<u32x4_t*>(wl + v * RS + k8) =
-        *reinterpret_cast<const u32x4_t*>(w_uv + (static_cast<int64_t>(hh) * DV + v) * kPfDC + k8);
+        bf16x8_to_f16x8(*reinterpret_cast<const u32x4_t*>(w_uv + (static_cast<int64_t>(hh) * DV + v) * kPfDC + k8));
   }
   __syncthreads();
   for (int k = 0; k < nch; ++k) {
     const int t = (c0 + k) * kPfUvTokens + 32 * w + r32;
-    bf16x8_t ob_hi[kPfDC / 16], ob_lo[kPfDC / 16];
+    f16x8_t ob[kPfDC / 16];
 #pragma unroll
-    for (int c = 0; c < kPfDC / 16; ++c) {
-      uint32_t hi[4], lo[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float x0 = ov[c][e >> 1][2 * (e & 1)], x1 = ov[c][e >> 1][2 * (e & 1) + 1];
-        hi[e] = pack_bf16x2(x0, x1);
-        lo[e] = pack_bf16x2(x0 - bf16_lo(hi[e]), x1 - bf16_hi(hi[e]));
-      }
-      ob_hi[c] = __builtin_bit_cast(bf16x8_t, u32x4_t{hi[0], hi[1], hi[2], hi[3]});
-      ob_lo[c] = __builtin_bit_cast(bf16x8_t, u32x4_t{lo[0], lo[1], lo[2], lo[3]});
-    }
+    for (int c = 0; c < kPfDC / 16; ++c) ob[c] = ov[c];
     pf_f32x16_t acc[DV / 32];
 #pragma unroll
     for (int vb = 0; vb < DV / 32; ++vb)
@@ -484,9 +475,8 @@ __global__ __launch_bounds__(256) void prefill_uv_kernel(const float* __restrict
     for (int c = 0; c < kPfDC / 16; ++c)
 #pragma unroll
       for (int vb = 0; vb < DV / 32; ++vb) {
-        const bf16x8_t av = *reinterpret_cast<const bf16x8_t*>(wl + (32 * vb + r32) * RS + 16 * c + 8 * h);
-        acc[vb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, ob_hi[c], acc[vb], 0, 0, 0);
-        acc[vb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, ob_lo[c], acc[vb], 0, 0, 0);
+        const f16x8_t av = *reinterpret_cast<const f16x8_t*>(wl + (32 * vb + r32) * RS + 16 * c + 8 * h);
+        acc[vb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, ob[c], acc[vb], 0, 0, 0);
       }
     // the next chunk's rows travel while this one is stored (the last chunk loads itself again)
     __builtin_amdgcn_sched_barrier(0);
