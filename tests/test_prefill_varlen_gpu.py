@@ -128,6 +128,21 @@ def test_prefill_varlen_explicit_peaked(gpu):
     assert_close(run_varlen(pb), oracle_varlen(pb), "bf16", "prefill varlen explicit q x8")
 
 
+@pytest.mark.parametrize("form", ["absorbed", "explicit"])
+def test_prefill_varlen_out_of_range_ids_clamped(gpu, form):
+    # ids below 0 or at least V select the first or last gate row (the gate
+    # passes clamp them); the oracle is fed the clamped ids
+    wl = LAYER if form == "absorbed" else WIDE
+    pb = W.generate_prefill_batch(wl, [130, 61], seed=67)
+    bad = np.random.default_rng(67).choice(len(pb.token_ids), 24, replace=False)
+    pb.token_ids[bad[:12]] = -3
+    pb.token_ids[bad[12:]] = wl.vocab + 7
+    say(f"prefill_varlen {form}: out-of-range ids")
+    got = run_varlen(pb)
+    pb.token_ids = np.clip(pb.token_ids, 0, wl.vocab - 1).astype(np.int32)
+    assert_close(got, oracle_varlen(pb), "bf16", f"prefill varlen {form} clamped ids")
+
+
 @pytest.mark.parametrize("heads,dc,lens", [(8, 256, [200, 57]), (16, 512, [150]), (32, 128, [97, 64])])
 def test_prefill_varlen_explicit_other_shapes(gpu, heads, dc, lens):
     wl = WIDE.replace(heads=heads, latent_dim=dc, gate_dim=dc)
